@@ -1,0 +1,250 @@
+"""Plain CPU oracle for the prefix-cache hot path.
+
+TEST INFRASTRUCTURE ONLY: only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package.  The product library
+never calls it, and it shares no code with it.
+
+Each function states the definition it computes and the passage of the paper
+(*When Fancy Eviction Fails*, Liu, Yu & Yang) that fixes it:
+
+* ``hash_requests``: block identity -- a block's KV state is reusable only if
+  the whole token sequence before and including it matches (Sec. 2.2); blocks
+  are 16 tokens (Sec. 2.2, Sec. 3.1).  The hash itself is not given in the
+  paper; the reading used is splitmix64's finalizer as a step function folded
+  over token-pair words and chained from the parent block.
+* ``prev_next``: previous / next access of the same block; the next-use time
+  is what Belady-style analysis ranks by (Sec. 3.2, Sec. 5.2 "BeladyCompute").
+* ``lru``: one LRU cache simulated per capacity (Sec. 5 "LRU as a bedrock");
+  the block hit ratio counts every access, compulsory misses included
+  (Sec. 3.2, Sec. 4.6).
+* ``stack_distance_walk`` / ``stack_distance_bit``: the exact LRU stack
+  distance (distinct blocks touched since the previous access); Appendix B
+  reads "reuses reachable within capacity C" off these distances.
+* ``mrc_bins`` / ``curves``: hit ratio and compute-savings ratio -- every hit
+  weighted by the recompute cost it avoids, over the cost of all accesses
+  (Sec. 5.2 "Compute-awareness"); uniform cost gives the hit ratio back.
+* ``belady``: demand-paging MIN per capacity (the offline ceiling, Sec. 3.2).
+* ``nextuse_hist``: histogram of next-use gaps ``next(t) - t``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+NONE = 0xFFFFFFFF
+_lib = None
+
+_u64p = ctypes.POINTER(ctypes.c_uint64)
+_u32p = ctypes.POINTER(ctypes.c_uint32)
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_u8p = ctypes.POINTER(ctypes.c_uint8)
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        path = _build.build(force=False)
+        L = ctypes.CDLL(path)
+        L.orc_mix64.restype = ctypes.c_uint64
+        L.orc_mix64.argtypes = [ctypes.c_uint64]
+        L.orc_step.restype = ctypes.c_uint64
+        L.orc_step.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+        L.orc_block_digest.restype = ctypes.c_uint64
+        L.orc_block_digest.argtypes = [_i32p, ctypes.c_uint32]
+        L.orc_hash_requests.restype = ctypes.c_uint64
+        L.orc_hash_requests.argtypes = [_i32p, _u64p, _u32p, ctypes.c_uint64, ctypes.c_uint32,
+                                        _u64p, ctypes.c_uint64, _u64p, _u32p]
+        L.orc_key_ids.restype = ctypes.c_uint64
+        L.orc_key_ids.argtypes = [_u64p, ctypes.c_uint64, _u32p]
+        L.orc_prev_next.restype = ctypes.c_int
+        L.orc_prev_next.argtypes = [_u32p, ctypes.c_uint64, ctypes.c_uint64, _u32p, _u32p]
+        L.orc_stack_distance_walk.restype = ctypes.c_int
+        L.orc_stack_distance_walk.argtypes = [_u32p, ctypes.c_uint64, ctypes.c_uint64, _u32p]
+        L.orc_stack_distance_bit.restype = ctypes.c_int
+        L.orc_stack_distance_bit.argtypes = [_u32p, ctypes.c_uint64, _u32p]
+        L.orc_lru_sim.restype = ctypes.c_int
+        L.orc_lru_sim.argtypes = [_u32p, _u32p, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64,
+                                  _u64p, _u64p, _u8p]
+        L.orc_belady_sim.restype = ctypes.c_int
+        L.orc_belady_sim.argtypes = [_u32p, _u32p, ctypes.c_uint64, ctypes.c_uint64,
+                                     ctypes.c_uint64, _u64p, _u8p]
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray, t):
+    return a.ctypes.data_as(t)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(np.asarray(a), dtype=dtype)
+
+
+def mix64(z: int) -> int:
+    return int(lib().orc_mix64(z & (2 ** 64 - 1)))
+
+
+def step(x: int, w: int) -> int:
+    return int(lib().orc_step(x & (2 ** 64 - 1), w & (2 ** 64 - 1)))
+
+
+def hash_requests(tokens, tok_start, tok_len, block_size=16, parent=None, root=0):
+    """Keys and depths of every full block of every request, request-major.
+
+    key(b) = S(key(b-1), digest(block b)), key(-1) = root or parent[r];
+    digest = S folded over the block's token-pair words from 0;
+    S(x, w) = mix64((x xor w) + 0x9E3779B97F4A7C15)."""
+    if block_size < 2 or block_size % 2:
+        raise ValueError("block size must be even and >= 2")
+    tokens = _c(tokens, np.int32)
+    tok_start = _c(tok_start, np.uint64)
+    tok_len = _c(tok_len, np.uint32)
+    n = int((tok_len.astype(np.uint64) // np.uint64(block_size)).sum())
+    keys = np.empty(n, np.uint64)
+    depth = np.empty(n, np.uint32)
+    par = _c(parent, np.uint64) if parent is not None else None
+    got = lib().orc_hash_requests(_p(tokens, _i32p), _p(tok_start, _u64p), _p(tok_len, _u32p),
+                                  tok_len.size, block_size,
+                                  _p(par, _u64p) if par is not None else None, root,
+                                  _p(keys, _u64p), _p(depth, _u32p))
+    assert got == n
+    return keys, depth
+
+
+def hash_trace(trace, block_size=None):
+    return hash_requests(trace.tokens, trace.tok_start, trace.tok_len,
+                         block_size or trace.block_size)
+
+
+def key_ids(keys):
+    keys = _c(keys, np.uint64)
+    ids = np.empty(keys.size, np.uint32)
+    n_ids = lib().orc_key_ids(_p(keys, _u64p), keys.size, _p(ids, _u32p))
+    if n_ids == 2 ** 64 - 1:
+        raise MemoryError("oracle dictionary")
+    return ids, int(n_ids)
+
+
+def prev_next(keys, ids=None):
+    if ids is None:
+        ids = key_ids(keys)
+    id_, n_ids = ids
+    prev = np.empty(id_.size, np.uint32)
+    nxt = np.empty(id_.size, np.uint32)
+    assert lib().orc_prev_next(_p(id_, _u32p), id_.size, n_ids, _p(prev, _u32p), _p(nxt, _u32p)) == 0
+    return prev, nxt
+
+
+def stack_distance_walk(keys, ids=None):
+    """Exact D by walking the MRU list (O(N*D), small traces only)."""
+    if ids is None:
+        ids = key_ids(keys)
+    id_, n_ids = ids
+    d = np.empty(id_.size, np.uint32)
+    assert lib().orc_stack_distance_walk(_p(id_, _u32p), id_.size, n_ids, _p(d, _u32p)) == 0
+    return d
+
+
+def stack_distance_bit(prev):
+    """Exact D from prev[] with a Fenwick tree over last-occurrence marks."""
+    prev = _c(prev, np.uint32)
+    d = np.empty(prev.size, np.uint32)
+    assert lib().orc_stack_distance_bit(_p(prev, _u32p), prev.size, _p(d, _u32p)) == 0
+    return d
+
+
+def lru(keys, caps, depth=None, ids=None, flags=False):
+    """Per capacity: (hits, sum of depth over hits[, per-access hit flags])."""
+    if ids is None:
+        ids = key_ids(keys)
+    id_, n_ids = ids
+    dep = _c(depth, np.uint32) if depth is not None else None
+    out = []
+    for c in caps:
+        h = ctypes.c_uint64(0)
+        dh = ctypes.c_uint64(0)
+        fl = np.empty(id_.size, np.uint8) if flags else None
+        assert lib().orc_lru_sim(_p(id_, _u32p), _p(dep, _u32p) if dep is not None else None,
+                                 id_.size, n_ids, int(c), ctypes.byref(h), ctypes.byref(dh),
+                                 _p(fl, _u8p) if fl is not None else None) == 0
+        out.append((h.value, dh.value, fl) if flags else (h.value, dh.value))
+    return out
+
+
+def belady(keys, caps, ids=None, nxt=None, flags=False):
+    if ids is None:
+        ids = key_ids(keys)
+    id_, n_ids = ids
+    if nxt is None:
+        _, nxt = prev_next(keys, ids)
+    nxt = _c(nxt, np.uint32)
+    out = []
+    for c in caps:
+        h = ctypes.c_uint64(0)
+        fl = np.empty(id_.size, np.uint8) if flags else None
+        assert lib().orc_belady_sim(_p(id_, _u32p), _p(nxt, _u32p), id_.size, n_ids, int(c),
+                                    ctypes.byref(h), _p(fl, _u8p) if fl is not None else None) == 0
+        out.append((h.value, fl) if flags else h.value)
+    return out
+
+
+def mrc_bins(keys, caps, depth=None, alpha=1, beta=0, ids=None):
+    """Bins over the capacity edges, from one LRU simulation per capacity.
+
+    Bin k (k < K) holds the accesses that hit at caps[k] but not at the
+    previous edge; bin K holds the accesses that miss at every capacity
+    (cold or too far).  Returns python-int lists count[K+1], depthsum[K+1],
+    cost[K+1] with cost = alpha*count + beta*depthsum (exact integers)."""
+    keys = _c(keys, np.uint64)
+    n = keys.size
+    if depth is None:
+        depth = np.zeros(n, np.uint32)
+    res = lru(keys, caps, depth, ids)
+    count, dsum = [], []
+    ph, pd = 0, 0
+    for h, dh in res:
+        count.append(h - ph)
+        dsum.append(dh - pd)
+        ph, pd = h, dh
+    count.append(n - ph)
+    dsum.append(int(np.asarray(depth, np.uint64).sum(dtype=np.uint64)) - pd)
+    cost = [alpha * c + beta * d for c, d in zip(count, dsum)]
+    return count, dsum, cost
+
+
+def curves(count, cost):
+    """Cumulative hit ratio and compute-savings ratio at each capacity edge.
+
+    HR(c_k) = hits(c_k) / N, CSR(c_k) = saved(c_k) / total cost, both from
+    exact integers rounded once to float64 before one division."""
+    n = sum(count)
+    total = sum(cost)
+    hr, csr = [], []
+    h, s = 0, 0
+    for k in range(len(count) - 1):
+        h += count[k]
+        s += cost[k]
+        hr.append(float(h) / float(n) if n else 0.0)
+        csr.append(float(s) / float(total) if total else 0.0)
+    return hr, csr
+
+
+def nextuse_hist(nxt, caps):
+    """Histogram of next(t) - t over the capacity edges (never reused -> last
+    bin); bin k = number of edges <= gap."""
+    nxt = np.asarray(nxt, np.uint32)
+    t = np.arange(nxt.size, dtype=np.uint64)
+    caps = np.asarray(caps, np.uint64)
+    hist = [0] * (caps.size + 1)
+    none = nxt == NONE
+    gap = nxt.astype(np.uint64) - t
+    k = np.searchsorted(caps, gap[~none], side="right")
+    bc = np.bincount(k, minlength=caps.size + 1)
+    for i in range(caps.size + 1):
+        hist[i] = int(bc[i])
+    hist[caps.size] += int(none.sum())
+    return hist

@@ -1,0 +1,335 @@
+/*
+ * Plain CPU oracle for the prefix-cache hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the tests, the entry point's smoke check and the
+ * benchmark's CPU-baseline leg use it.  It shares no code, header, constant
+ * table or helper with the GPU library: every definition below is written
+ * out again from the paper's statement of the problem and from the
+ * published algorithms it names.
+ *
+ * It is deliberately slow and literal:
+ *   - block hashing walks every request's tokens in order;
+ *   - prev/next-use indices come from a "last seen" dictionary scan;
+ *   - LRU is simulated per capacity with an explicit recency list
+ *     (Mattson et al. 1970 define the stack; we simply run the list);
+ *   - exact stack distances come from walking the MRU list, and a second,
+ *     independent exact method uses a Fenwick tree over "last occurrence"
+ *     marks (Bennett & Kruskal 1975);
+ *   - Belady's MIN is simulated per capacity with a max-heap on next use.
+ *
+ * Conventions (the paper leaves them open; these are the oracle's readings):
+ *   - positions are uint32, 0xFFFFFFFF = none (cold / never reused);
+ *   - the distance D(t) counts the distinct other blocks touched since the
+ *     previous access of the same block; a hit at capacity c means D < c;
+ *   - only full blocks of a request are accesses, in ascending depth order.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_NONE 0xFFFFFFFFu
+
+/* ------------------------------------------------------------------ */
+/* Block identity (Sec. 2.2: a cached KV state is reusable only if the */
+/* whole preceding token sequence matches; Sec. 3.1: 16-token blocks). */
+/* The paper does not give the hash.  Reading: splitmix64's finalizer  */
+/* (Steele, Lea & Flood 2014) as a step function folded over 64-bit    */
+/* token-pair words, then chained from the parent block.               */
+/* ------------------------------------------------------------------ */
+
+uint64_t orc_mix64(uint64_t z)
+{
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+/* one step: S(x, w) = mix64((x xor w) + golden gamma) */
+uint64_t orc_step(uint64_t x, uint64_t w)
+{
+    return orc_mix64((x ^ w) + 0x9E3779B97F4A7C15ull);
+}
+
+/* digest of one block of B tokens (B even): fold S over the B/2 words
+ * w_k = tok[2k] | tok[2k+1] << 32, starting from 0 */
+uint64_t orc_block_digest(const int32_t *tok, uint32_t B)
+{
+    uint64_t d = 0;
+    for (uint32_t k = 0; k < B / 2; k++) {
+        uint64_t lo = (uint64_t)(uint32_t)tok[2 * k];
+        uint64_t hi = (uint64_t)(uint32_t)tok[2 * k + 1];
+        d = orc_step(d, lo | (hi << 32));
+    }
+    return d;
+}
+
+/* Hash every full block of every request, request by request.
+ * Request r covers tokens[tok_start[r] .. tok_start[r]+tok_len[r]).
+ * Output layout: requests in order, blocks of a request in depth order.
+ * key of block b = S(key of block b-1, digest_b), key of block -1 = root
+ * (or parent[r] when parent is given).  depth[i] = b.
+ * Returns the number of blocks written. */
+uint64_t orc_hash_requests(const int32_t *tokens, const uint64_t *tok_start,
+                           const uint32_t *tok_len, uint64_t n_req, uint32_t B,
+                           const uint64_t *parent, uint64_t root,
+                           uint64_t *keys, uint32_t *depth)
+{
+    uint64_t out = 0;
+    for (uint64_t r = 0; r < n_req; r++) {
+        uint64_t key = parent ? parent[r] : root;
+        uint32_t nb = tok_len[r] / B;
+        const int32_t *t = tokens + tok_start[r];
+        for (uint32_t b = 0; b < nb; b++) {
+            key = orc_step(key, orc_block_digest(t + (uint64_t)b * B, B));
+            keys[out] = key;
+            if (depth) depth[out] = b;
+            out++;
+        }
+    }
+    return out;
+}
+
+/* ------------------------------------------------------------------ */
+/* Dense ids: an open-addressing dictionary from key to first-seen id. */
+/* ------------------------------------------------------------------ */
+
+static uint64_t slot_of(uint64_t key, uint64_t mask)
+{
+    /* any well-mixed spread works; the dictionary is exact either way */
+    return (key * 0x9E3779B97F4A7C15ull >> 17) & mask;
+}
+
+/* id[t] = index of key[t] among distinct keys in order of first access.
+ * Returns the number of distinct keys, or (uint64_t)-1 on allocation failure. */
+uint64_t orc_key_ids(const uint64_t *keys, uint64_t n, uint32_t *id)
+{
+    uint64_t cap = 16;
+    while (cap < 2 * n + 2) cap <<= 1;
+    uint64_t *tk = (uint64_t *)malloc(cap * sizeof(uint64_t));
+    uint32_t *tv = (uint32_t *)malloc(cap * sizeof(uint32_t));
+    if (!tk || !tv) { free(tk); free(tv); return (uint64_t)-1; }
+    for (uint64_t i = 0; i < cap; i++) tv[i] = ORC_NONE;
+    uint64_t mask = cap - 1, distinct = 0;
+    for (uint64_t t = 0; t < n; t++) {
+        uint64_t s = slot_of(keys[t], mask);
+        while (tv[s] != ORC_NONE && tk[s] != keys[t]) s = (s + 1) & mask;
+        if (tv[s] == ORC_NONE) { tk[s] = keys[t]; tv[s] = (uint32_t)distinct++; }
+        id[t] = tv[s];
+    }
+    free(tk); free(tv);
+    return distinct;
+}
+
+/* prev[t] = last earlier position with the same key, next[t] = first later
+ * one; ORC_NONE when there is none.  Scan in time order keeping, per id,
+ * the position where it was last seen. */
+int orc_prev_next(const uint32_t *id, uint64_t n, uint64_t n_ids,
+                  uint32_t *prev, uint32_t *next)
+{
+    uint32_t *last = (uint32_t *)malloc((n_ids ? n_ids : 1) * sizeof(uint32_t));
+    if (!last) return -1;
+    for (uint64_t u = 0; u < n_ids; u++) last[u] = ORC_NONE;
+    for (uint64_t t = 0; t < n; t++) {
+        uint32_t p = last[id[t]];
+        prev[t] = p;
+        next[t] = ORC_NONE;
+        if (p != ORC_NONE) next[p] = (uint32_t)t;
+        last[id[t]] = (uint32_t)t;
+    }
+    free(last);
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* LRU as an explicit recency list (Sec. 5 "LRU as a bedrock").        */
+/* ------------------------------------------------------------------ */
+
+/* Exact stack distance by walking the MRU list: D(t) = number of distinct
+ * blocks used more recently than key[t]'s previous use; ORC_NONE if cold.
+ * O(N * D): only for small traces. */
+int orc_stack_distance_walk(const uint32_t *id, uint64_t n, uint64_t n_ids, uint32_t *dist)
+{
+    uint32_t *nx = (uint32_t *)malloc((n_ids + 1) * sizeof(uint32_t));
+    uint32_t *pv = (uint32_t *)malloc((n_ids + 1) * sizeof(uint32_t));
+    uint8_t *seen = (uint8_t *)calloc(n_ids + 1, 1);
+    if (!nx || !pv || !seen) { free(nx); free(pv); free(seen); return -1; }
+    uint32_t head = ORC_NONE;
+    for (uint64_t t = 0; t < n; t++) {
+        uint32_t u = id[t];
+        if (!seen[u]) {
+            dist[t] = ORC_NONE;
+            seen[u] = 1;
+        } else {
+            uint32_t d = 0, x = head;
+            while (x != u) { x = nx[x]; d++; }
+            dist[t] = d;
+            /* unlink u */
+            if (pv[u] != ORC_NONE) nx[pv[u]] = nx[u]; else head = nx[u];
+            if (nx[u] != ORC_NONE) pv[nx[u]] = pv[u];
+        }
+        /* push u at the front */
+        pv[u] = ORC_NONE;
+        nx[u] = head;
+        if (head != ORC_NONE) pv[head] = u;
+        head = u;
+    }
+    free(nx); free(pv); free(seen);
+    return 0;
+}
+
+/* Second exact method (Bennett & Kruskal 1975): keep a mark at the last
+ * occurrence of every key; D(t) = marks strictly between prev(t) and t. */
+static void bit_add(int32_t *bit, uint64_t n, uint64_t i, int32_t v)
+{
+    for (i++; i <= n; i += i & (~i + 1)) bit[i] += v;
+}
+static int64_t bit_sum(const int32_t *bit, uint64_t i) /* sum of [0, i) */
+{
+    int64_t s = 0;
+    for (; i > 0; i -= i & (~i + 1)) s += bit[i];
+    return s;
+}
+int orc_stack_distance_bit(const uint32_t *prev, uint64_t n, uint32_t *dist)
+{
+    int32_t *bit = (int32_t *)calloc(n + 1, sizeof(int32_t));
+    if (!bit) return -1;
+    for (uint64_t t = 0; t < n; t++) {
+        uint32_t p = prev[t];
+        if (p == ORC_NONE) {
+            dist[t] = ORC_NONE;
+        } else {
+            dist[t] = (uint32_t)(bit_sum(bit, t) - bit_sum(bit, (uint64_t)p + 1));
+            bit_add(bit, n, p, -1);
+        }
+        bit_add(bit, n, t, +1);
+    }
+    free(bit);
+    return 0;
+}
+
+/* One LRU cache of `cap` blocks run over the whole trace.  A block that is
+ * resident when accessed is a hit; otherwise it is inserted at the front and,
+ * if the cache then holds more than cap blocks, the least recently used one
+ * is evicted.  cap = 0 never hits.
+ * Outputs: hit count, sum of depth over hits, optional per-access hit flags. */
+int orc_lru_sim(const uint32_t *id, const uint32_t *depth, uint64_t n, uint64_t n_ids,
+                uint64_t cap, uint64_t *hits_out, uint64_t *depth_hits_out, uint8_t *hit_flag)
+{
+    uint32_t *nx = (uint32_t *)malloc((n_ids + 1) * sizeof(uint32_t));
+    uint32_t *pv = (uint32_t *)malloc((n_ids + 1) * sizeof(uint32_t));
+    uint8_t *in = (uint8_t *)calloc(n_ids + 1, 1);
+    if (!nx || !pv || !in) { free(nx); free(pv); free(in); return -1; }
+    uint32_t head = ORC_NONE, tail = ORC_NONE;
+    uint64_t size = 0, hits = 0, dh = 0;
+    for (uint64_t t = 0; t < n; t++) {
+        uint32_t u = id[t];
+        int hit = 0;
+        if (cap == 0) {
+            if (hit_flag) hit_flag[t] = 0;
+            continue;
+        }
+        if (in[u]) {
+            hit = 1;
+            hits++;
+            if (depth) dh += depth[t];
+            if (u != head) { /* move to front */
+                nx[pv[u]] = nx[u];
+                if (nx[u] != ORC_NONE) pv[nx[u]] = pv[u]; else tail = pv[u];
+                pv[u] = ORC_NONE; nx[u] = head; pv[head] = u; head = u;
+            }
+        } else {
+            in[u] = 1;
+            pv[u] = ORC_NONE; nx[u] = head;
+            if (head != ORC_NONE) pv[head] = u; else tail = u;
+            head = u;
+            if (++size > cap) { /* evict the least recently used */
+                uint32_t v = tail;
+                tail = pv[v];
+                nx[tail] = ORC_NONE;
+                in[v] = 0;
+                size--;
+            }
+        }
+        if (hit_flag) hit_flag[t] = (uint8_t)hit;
+    }
+    *hits_out = hits;
+    if (depth_hits_out) *depth_hits_out = dh;
+    free(nx); free(pv); free(in);
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Belady's MIN (Sec. 3.2: offline ceiling), demand paging: every      */
+/* accessed block is inserted; on overflow evict the resident block    */
+/* whose next use is farthest away (never reused = farthest).          */
+/* ------------------------------------------------------------------ */
+
+typedef struct { uint64_t when; uint32_t u; } heap_ent;
+
+static void heap_push(heap_ent *h, uint64_t *n, heap_ent e)
+{
+    uint64_t i = (*n)++;
+    while (i > 0) {
+        uint64_t p = (i - 1) / 2;
+        if (h[p].when >= e.when) break;
+        h[i] = h[p];
+        i = p;
+    }
+    h[i] = e;
+}
+
+static heap_ent heap_pop(heap_ent *h, uint64_t *n)
+{
+    heap_ent top = h[0], last = h[--(*n)];
+    uint64_t i = 0;
+    for (;;) {
+        uint64_t c = 2 * i + 1;
+        if (c >= *n) break;
+        if (c + 1 < *n && h[c + 1].when > h[c].when) c++;
+        if (h[c].when <= last.when) break;
+        h[i] = h[c];
+        i = c;
+    }
+    if (*n > 0) h[i] = last;
+    return top;
+}
+
+int orc_belady_sim(const uint32_t *id, const uint32_t *next, uint64_t n, uint64_t n_ids,
+                   uint64_t cap, uint64_t *hits_out, uint8_t *hit_flag)
+{
+    /* heap entries are (next use, id); stale entries are skipped on pop */
+    heap_ent *h = (heap_ent *)malloc((n + 1) * sizeof(heap_ent));
+    uint64_t *cur = (uint64_t *)malloc((n_ids + 1) * sizeof(uint64_t));
+    uint8_t *in = (uint8_t *)calloc(n_ids + 1, 1);
+    if (!h || !cur || !in) { free(h); free(cur); free(in); return -1; }
+    uint64_t hn = 0, size = 0, hits = 0;
+    for (uint64_t t = 0; t < n; t++) {
+        uint32_t u = id[t];
+        uint64_t when = next[t] == ORC_NONE ? UINT64_MAX : (uint64_t)next[t];
+        int hit = 0;
+        if (cap == 0) { if (hit_flag) hit_flag[t] = 0; continue; }
+        if (in[u]) {
+            hit = 1;
+            hits++;
+        } else {
+            if (size == cap) {
+                /* evict the resident block used farthest in the future;
+                 * u is not resident, so every live heap entry is another block */
+                heap_ent v;
+                do { v = heap_pop(h, &hn); } while (!in[v.u] || cur[v.u] != v.when);
+                in[v.u] = 0;
+                size--;
+            }
+            in[u] = 1;
+            size++;
+        }
+        cur[u] = when;
+        heap_ent e = { when, u };
+        heap_push(h, &hn, e);
+        if (hit_flag) hit_flag[t] = (uint8_t)hit;
+    }
+    *hits_out = hits;
+    free(h); free(cur); free(in);
+    return 0;
+}

@@ -1,0 +1,308 @@
+"""Pins for the CPU oracle: published values, textbook examples, brute force
+and invariants that a plausible mistake in the oracle would break.  CPU only."""
+import itertools
+import random
+
+import numpy as np
+import pytest
+
+import oracle
+from conftest import read_golden
+
+NONE = oracle.NONE
+G = 0x9E3779B97F4A7C15
+M64 = 2 ** 64 - 1
+
+
+# ---------------------------------------------------------------- hashing
+
+def test_mix64_matches_published_splitmix64_outputs():
+    for k, out in read_golden("splitmix64_seed0.txt"):
+        k, out = int(k), int(out, 16)
+        assert oracle.mix64((k * G) & M64) == out
+
+
+def test_step_adds_golden_gamma_after_xor():
+    # S(x, w) = mix64((x ^ w) + G): (0,0) -> mix64(G), (G,0) -> mix64(2G),
+    # (0, 2G) -> mix64(3G); all three are published splitmix64 outputs.
+    outs = {int(k): int(v, 16) for k, v in read_golden("splitmix64_seed0.txt")}
+    assert oracle.step(0, 0) == outs[1]
+    assert oracle.step(G, 0) == outs[2]
+    assert oracle.step(0, (2 * G) & M64) == outs[3]
+    assert oracle.step(5, 5) == outs[1]          # x ^ w cancels
+
+
+def _req(tokens_list):
+    toks = np.concatenate([np.asarray(t, np.int32) for t in tokens_list])
+    lens = np.array([len(t) for t in tokens_list], np.uint32)
+    starts = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.uint64)
+    return toks, starts, lens
+
+
+def test_only_full_blocks_count():
+    toks, st, ln = _req([np.arange(33), np.arange(15), np.arange(32)])
+    keys, depth = oracle.hash_requests(toks, st, ln, 16)
+    assert keys.size == 2 + 0 + 2
+    assert list(depth) == [0, 1, 0, 1]
+
+
+def test_shared_prefix_gives_shared_keys_and_divergence_propagates():
+    rng = np.random.default_rng(0)
+    base = rng.integers(0, 151936, size=16 * 6).astype(np.int32)
+    other = base.copy()
+    other[16 * 3 + 5] += 1                      # change one token of block 3
+    toks, st, ln = _req([base, other])
+    keys, _ = oracle.hash_requests(toks, st, ln, 16)
+    a, b = keys[:6], keys[6:]
+    assert np.array_equal(a[:3], b[:3])
+    assert np.all(a[3:] != b[3:])               # the change reaches every later block
+
+
+def test_block_position_matters():
+    # the same 16 tokens at depth 0 and at depth 1 must not collide
+    blk = np.arange(100, 116, dtype=np.int32)
+    toks, st, ln = _req([np.concatenate([blk, blk])])
+    keys, _ = oracle.hash_requests(toks, st, ln, 16)
+    assert keys[0] != keys[1]
+
+
+def test_word_packing_is_order_sensitive():
+    toks, st, ln = _req([[1, 2], [2, 1], [1, 2, 3, 4], [3, 4, 1, 2]])
+    keys, _ = oracle.hash_requests(toks, st, ln, 2)
+    assert keys[0] != keys[1]
+    k4, _ = oracle.hash_requests(toks, st, ln, 4)
+    assert k4[0] != k4[1]
+
+
+def test_parent_chaining_equals_one_pass():
+    rng = np.random.default_rng(1)
+    t = rng.integers(0, 151936, size=16 * 10).astype(np.int32)
+    full, _ = oracle.hash_requests(*_req([t]), 16)
+    first, _ = oracle.hash_requests(*_req([t[:16 * 4]]), 16)
+    rest, _ = oracle.hash_requests(*_req([t[16 * 4:]]), 16, parent=[first[-1]])
+    assert np.array_equal(full, np.concatenate([first, rest]))
+    rooted, _ = oracle.hash_requests(*_req([t]), 16, root=123)
+    assert np.all(rooted != full)
+
+
+def test_digest_is_fold_over_words_from_zero():
+    # a block of B=2 tokens is one word: digest = S(0, w); key = S(root, digest)
+    w = 7 | (9 << 32)
+    keys, _ = oracle.hash_requests(*_req([[7, 9]]), 2)
+    assert int(keys[0]) == oracle.step(0, oracle.step(0, w))
+
+
+# ---------------------------------------------------------- prev / next
+
+def brute_prev_next(keys):
+    n = len(keys)
+    prev = [NONE] * n
+    nxt = [NONE] * n
+    for t in range(n):
+        for i in range(t - 1, -1, -1):
+            if keys[i] == keys[t]:
+                prev[t] = i
+                break
+        for i in range(t + 1, n):
+            if keys[i] == keys[t]:
+                nxt[t] = i
+                break
+    return prev, nxt
+
+
+def random_streams(count=60, seed=0):
+    rng = random.Random(seed)
+    for _ in range(count):
+        n = rng.randint(0, 120)
+        m = rng.randint(1, 30)
+        hot = rng.random() < 0.3
+        ks = []
+        for _ in range(n):
+            if hot and rng.random() < 0.5:
+                ks.append(1)
+            else:
+                ks.append(rng.randrange(m) * 0x10001 + 7)
+        yield np.array(ks, dtype=np.uint64)
+
+
+def test_prev_next_brute_force():
+    for keys in random_streams():
+        p, n = oracle.prev_next(keys)
+        bp, bn = brute_prev_next(list(keys))
+        assert list(p) == bp and list(n) == bn
+
+
+# ------------------------------------------------------ stack distances
+
+def brute_distance(keys):
+    """Distinct keys strictly between the previous use and t."""
+    out = []
+    for t, k in enumerate(keys):
+        p = None
+        for i in range(t - 1, -1, -1):
+            if keys[i] == k:
+                p = i
+                break
+        out.append(NONE if p is None else len(set(keys[p + 1:t])))
+    return out
+
+
+def next_form_distance(keys):
+    """#{i in (prev(t), t) : next(i) > t}, cold -> NONE."""
+    prev, nxt = brute_prev_next(list(keys))
+    out = []
+    for t in range(len(keys)):
+        p = prev[t]
+        if p == NONE:
+            out.append(NONE)
+        else:
+            out.append(sum(1 for i in range(p + 1, t) if nxt[i] == NONE or nxt[i] > t))
+    return out
+
+
+def _golden_streams():
+    for row in read_golden("stack_distance_examples.txt"):
+        bar = row.index("|")
+        names = row[1:bar]
+        want = [NONE if v == "-" else int(v) for v in row[bar + 1:]]
+        ids = {}
+        keys = np.array([ids.setdefault(x, len(ids) + 100) for x in names], np.uint64)
+        yield row[0], keys, want
+
+
+def test_hand_worked_examples():
+    for name, keys, want in _golden_streams():
+        assert list(oracle.stack_distance_walk(keys)) == want, name
+        p, _ = oracle.prev_next(keys)
+        assert list(oracle.stack_distance_bit(p)) == want, name
+
+
+def test_walk_and_fenwick_match_brute_force_and_next_form():
+    for keys in random_streams(80, seed=3):
+        want = brute_distance(list(keys))
+        assert list(oracle.stack_distance_walk(keys)) == want
+        p, _ = oracle.prev_next(keys)
+        assert list(oracle.stack_distance_bit(p)) == want
+        assert next_form_distance(keys) == want
+
+
+# ------------------------------------------------------------- LRU / MIN
+
+def test_textbook_page_replacement_example():
+    rows = read_golden("page_replacement_textbook.txt")
+    ref = np.array([int(x) + 1 for x in rows[0]], np.uint64)
+    frames, lru_faults, opt_faults = (int(x) for x in rows[1])
+    (h, _), = oracle.lru(ref, [frames])
+    assert ref.size - h == lru_faults
+    (b,) = oracle.belady(ref, [frames])
+    assert ref.size - b == opt_faults
+
+
+def test_lru_hit_iff_distance_below_capacity():
+    for keys in random_streams(40, seed=5):
+        d = oracle.stack_distance_walk(keys)
+        caps = [0, 1, 2, 3, 5, 8, 13, 40]
+        res = oracle.lru(keys, caps, flags=True)
+        prev_flags = None
+        for c, (h, _, fl) in zip(caps, res):
+            want = (d != NONE) & (d < c)
+            assert np.array_equal(fl.astype(bool), want), c
+            assert h == int(want.sum())
+            if prev_flags is not None:                  # inclusion, per access
+                assert np.all(fl >= prev_flags)
+            prev_flags = fl
+
+
+def test_lru_special_capacities():
+    for keys in random_streams(40, seed=7):
+        n = keys.size
+        distinct = len(set(keys.tolist()))
+        (h1, _), (hbig, _) = oracle.lru(keys, [1, max(distinct, 1)])
+        assert h1 == sum(1 for t in range(1, n) if keys[t] == keys[t - 1])
+        assert hbig == n - distinct
+
+
+def brute_min(keys, cap):
+    """Exhaustive offline optimum for demand paging (tiny inputs)."""
+    best = 0
+
+    def rec(t, cache, hits):
+        nonlocal best
+        if t == len(keys):
+            best = max(best, hits)
+            return
+        if hits + (len(keys) - t) <= best:
+            return
+        k = keys[t]
+        if k in cache:
+            rec(t + 1, cache, hits + 1)
+        elif len(cache) < cap:
+            rec(t + 1, cache | {k}, hits)
+        else:
+            for v in cache:
+                rec(t + 1, (cache - {v}) | {k}, hits)
+
+    if cap == 0:
+        return 0
+    rec(0, frozenset(), 0)
+    return best
+
+
+def test_belady_is_the_exhaustive_optimum():
+    rng = random.Random(11)
+    for _ in range(40):
+        n = rng.randint(1, 11)
+        keys = np.array([rng.randrange(5) + 1 for _ in range(n)], np.uint64)
+        for c in range(0, 5):
+            assert oracle.belady(keys, [c])[0] == brute_min(keys.tolist(), c)
+
+
+def test_lru_never_beats_belady_and_meets_it_when_everything_fits():
+    for keys in random_streams(40, seed=13):
+        distinct = len(set(keys.tolist()))
+        caps = [1, 2, 4, 8, max(distinct, 1)]
+        lru_h = [h for h, _ in oracle.lru(keys, caps)]
+        opt_h = oracle.belady(keys, caps)
+        assert all(a <= b for a, b in zip(lru_h, opt_h))
+        assert lru_h[-1] == opt_h[-1] == keys.size - distinct
+
+
+# --------------------------------------------------------------- curves
+
+def test_uniform_cost_savings_equal_hit_ratio():
+    for keys in random_streams(20, seed=17):
+        if keys.size == 0:
+            continue
+        depth = np.arange(keys.size, dtype=np.uint32) % 7
+        caps = [1, 2, 3, 10, 100]
+        count, dsum, cost = oracle.mrc_bins(keys, caps, depth, alpha=1, beta=0)
+        assert sum(count) == keys.size
+        hr, csr = oracle.curves(count, cost)
+        assert hr == csr
+
+
+def test_linear_cost_closed_form_on_one_session():
+    # example (ii): contexts of 3, 5, 6 blocks; depth = block index.
+    # At capacity 5 (> 4) every re-access hits: hits are depths 0..2 and 0..4.
+    # linear cost d+1 -> saved = (1+2+3) + (1+2+3+4+5) = 21, total = 6+15+21 = 42.
+    _, keys, _ = [g for g in _golden_streams() if g[0] == "ii"][0]
+    depth = np.array([0, 1, 2, 0, 1, 2, 3, 4, 0, 1, 2, 3, 4, 5], np.uint32)
+    count, dsum, cost = oracle.mrc_bins(keys, [3, 5], depth, alpha=1, beta=1)
+    assert count == [3, 5, 6]           # D=2 re-reads, D=4 re-reads, cold blocks
+    hr, csr = oracle.curves(count, cost)
+    assert csr[1] == 21 / 42
+    assert hr[1] == 8 / 14
+
+
+def test_nextuse_histogram_brute_force():
+    for keys in random_streams(30, seed=19):
+        _, nxt = oracle.prev_next(keys)
+        caps = [1, 2, 3, 5, 9]
+        want = [0] * (len(caps) + 1)
+        for t in range(keys.size):
+            if nxt[t] == NONE:
+                want[-1] += 1
+            else:
+                gap = int(nxt[t]) - t
+                want[sum(1 for c in caps if c <= gap)] += 1
+        assert oracle.nextuse_hist(nxt, caps) == want
