@@ -1,0 +1,187 @@
+/*
+ * libpc -- the prefix-cache eviction hot path on one AMD Instinct MI355X
+ * (gfx950): chained block hashing, prev/next-use indexing, exact LRU stack
+ * distance and the hit-ratio / compute-savings histograms over every cache
+ * capacity at once.
+ *
+ * Paper: Y. Liu, M. Yu, J. Yang, "When Fancy Eviction Fails: Rethinking Cache
+ * Replacement For LLM Prefix Reuse".  Each entry point cites the passage
+ * that defines what it computes.
+ *
+ * Common rules
+ *   - Every array argument is DEVICE memory (hipMalloc / a torch tensor on the
+ *     GPU) unless stated otherwise.  The caller owns all memory; the library
+ *     never allocates, frees or synchronises.  Scratch space comes only from
+ *     the caller's workspace `ws` of at least the size the matching `*_ws`
+ *     query returns (256-byte aligned).
+ *   - Work is enqueued on `stream` and the call returns; outputs are valid once
+ *     the stream has completed.  Calls are thread-safe given distinct
+ *     workspaces; two calls that share a workspace must be ordered on a stream.
+ *   - Positions are uint32; PC_NONE (0xFFFFFFFF) means "none" (no previous /
+ *     next use, or an infinite distance).  Hence n must be below 2^32 - 1.
+ *   - Arguments are checked before anything is launched; on error nothing is
+ *     enqueued and outputs are untouched.  A failed launch returns
+ *     PC_ERR_DEVICE.  Nothing throws across this interface.
+ */
+#ifndef PC_H
+#define PC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PC_OK = 0,
+    PC_ERR_INVALID = -1,     /* NULL required pointer, bad block size, bad caps */
+    PC_ERR_TOO_LARGE = -2,   /* n >= 2^32 - 1 (positions must fit uint32)       */
+    PC_ERR_WORKSPACE = -3,   /* ws NULL or smaller than the query               */
+    PC_ERR_DEVICE = -4,      /* a HIP call or kernel launch failed              */
+    PC_ERR_UNSUPPORTED = -5  /* no usable gfx950 device                          */
+} pc_status;
+
+#define PC_NONE 0xFFFFFFFFu
+#define PC_MAX_CAPS 1024u
+
+/* Human-readable name of a status code (static storage). */
+const char *pc_status_string(pc_status s);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int pc_version(void);
+
+/* ------------------------------------------------------------------------
+ * Chained block hashing.
+ *
+ * Paper: a cached KV state is reusable only if the whole preceding token
+ * sequence matches (Sec. 2.2 "LLM Serving Prefix Cache"); KV state is managed
+ * in fixed-size blocks of 16 tokens (Sec. 2.2; Sec. 3.1 "Traces": 16-token
+ * blocks with block identity scoped across sessions).  The paper does not
+ * give the hash; this library fixes it as follows (all arithmetic mod 2^64):
+ *     mix64(z)  = splitmix64 finalizer (Steele, Lea & Flood 2014)
+ *     S(x, w)   = mix64((x ^ w) + 0x9E3779B97F4A7C15)
+ *     word k    = (uint32)tok[2k] | (uint64)(uint32)tok[2k+1] << 32
+ *     digest(b) = S folded over the B/2 words of block b, starting from 0
+ *     key(b)    = S(key(b-1), digest(b)),  key(-1) = parent[r] or root
+ * Only full blocks count: request r yields floor(tok_len[r] / B) accesses, in
+ * ascending depth order.
+ *
+ *   tokens     int32[n_tokens] token buffer
+ *   tok_start  uint64[n_seqs]  first token of request r inside `tokens`
+ *   tok_len    uint32[n_seqs]  token count of request r (views may overlap:
+ *                               all turns of one session can share one stream)
+ *   block_size B, even, 2..1024
+ *   parent     uint64[n_seqs] chain start per request, or NULL to use `root`
+ *   blk_off    uint64[n_seqs+1] exclusive prefix sum of floor(tok_len/B):
+ *                               block b of request r goes to keys[blk_off[r]+b];
+ *                               blk_off[n_seqs] must equal n_blocks
+ *   keys       uint64[n_blocks] output
+ *   depth      uint32[n_blocks] output block index b inside its request, or NULL
+ * A request whose tokens run past n_tokens, or whose blocks run past
+ * n_blocks, is skipped and the workspace status (pc_workspace_status) is set
+ * to 2; nothing is read or written out of bounds.
+ * ------------------------------------------------------------------------ */
+size_t pc_hash_blocks_ws(uint32_t n_seqs);
+pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_t *tok_start,
+                         const uint32_t *tok_len, uint32_t n_seqs, uint32_t block_size,
+                         const uint64_t *parent, uint64_t root, const uint64_t *blk_off,
+                         uint64_t n_blocks, uint64_t *keys, uint32_t *depth,
+                         void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Previous / next use of every access.
+ *
+ * prev[t] = max{ i < t : keys[i] == keys[t] } or PC_NONE;
+ * next[t] = min{ i > t : keys[i] == keys[t] } or PC_NONE.
+ * The next-use time is what Belady-style offline analysis ranks blocks by
+ * (Sec. 3.2 "Belady's optimum"; Sec. 5.2 "BeladyCompute", time until next
+ * access); prev == PC_NONE marks a compulsory miss (Sec. 4.6).
+ *
+ *   keys  uint64[n]; prev, next uint32[n] outputs.
+ * ------------------------------------------------------------------------ */
+size_t pc_prev_next_use_ws(uint64_t n);
+pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uint32_t *next,
+                           void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Exact LRU stack distance of every access.
+ *
+ * dist[t] = #{ i in (prev(t), t) : next(i) > t }  (next(i) = PC_NONE counts
+ * as infinity), i.e. the number of distinct other blocks touched since the
+ * previous access of the same block; PC_NONE when prev(t) = PC_NONE.  LRU is
+ * a stack algorithm, so an access hits in an LRU cache of c blocks exactly
+ * when dist < c, at every c at once (Sec. 5 "LRU as a bedrock"; Appendix B
+ * "stack distance between reuses", "reuses reachable within capacity").
+ *
+ *   prev, next uint32[n] as produced by pc_prev_next_use; dist uint32[n] out.
+ * ------------------------------------------------------------------------ */
+size_t pc_stack_distance_ws(uint64_t n);
+pc_status pc_stack_distance(const uint32_t *prev, const uint32_t *next, uint64_t n,
+                            uint32_t *dist, void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Hit-ratio and compute-savings histograms over capacity edges.
+ *
+ * Paper: block hit ratio counts every access, compulsory misses included
+ * (Sec. 3.2); the compute-savings ratio weights every hit by the recompute
+ * cost it avoids and divides by the cost of all accesses (Sec. 5.2
+ * "Compute-awareness"); the cost grows with the block's token depth
+ * (Sec. 4.4 "Position-Dependent Miss Costs"); a linear-in-depth model is
+ * the extreme case (Appendix C).  Here cost(t) = alpha + beta * depth[t].
+ *
+ * Bin k in [0, n_caps) counts accesses with caps[k-1] <= dist < caps[k]
+ * (caps[-1] = 0); bin n_caps counts dist >= caps[n_caps-1] and dist == PC_NONE.
+ * So hits at capacity caps[k] = sum of count[0..k].  Per bin:
+ *     count[k]     uint64  number of accesses
+ *     depthsum[k]  uint64  sum of depth over them (0 when depth is NULL)
+ *     cost_hi:lo   uint128 alpha*count[k] + beta*depthsum[k] (exact)
+ * When `next` is not NULL, nextuse_hist[k] bins the next-use gap next[t] - t
+ * on the same edges (PC_NONE goes to bin n_caps).
+ *
+ *   dist   uint32[n]; depth uint32[n] or NULL; next uint32[n] or NULL
+ *   caps   uint64[n_caps] non-decreasing, 1 <= n_caps <= PC_MAX_CAPS (device
+ *          memory; the order is checked on the device: a decreasing pair sets
+ *          the workspace status to 3 and leaves the bins undefined)
+ *   count, depthsum, cost_lo, cost_hi: uint64[n_caps+1] outputs (required)
+ *   nextuse_hist: uint64[n_caps+1] output, required when next != NULL; when
+ *          given it is always zeroed (and stays zero when next is NULL)
+ * Outputs are zeroed on `stream` first, then accumulated.
+ * ------------------------------------------------------------------------ */
+size_t pc_mrc_weighted_ws(uint64_t n, uint32_t n_caps);
+pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uint32_t *next,
+                          uint64_t n, const uint64_t *caps, uint32_t n_caps, uint64_t alpha,
+                          uint64_t beta, uint64_t *count, uint64_t *depthsum, uint64_t *cost_lo,
+                          uint64_t *cost_hi, uint64_t *nextuse_hist, void *ws, size_t ws_bytes,
+                          void *stream);
+
+/* ------------------------------------------------------------------------
+ * Device-side status.  Every call clears word 0 of its workspace; kernels
+ * record a non-zero code there instead of faulting or hanging:
+ *   1  a wait on another workgroup (decoupled look-back) gave up after a
+ *      bounded spin (outputs undefined);
+ *   2  pc_hash_blocks: a request's tokens or blocks fall outside the arrays
+ *      (that request was skipped);
+ *   3  pc_mrc_weighted: caps not non-decreasing (bins undefined).
+ * This call copies the code of workspace `ws` to *code_out after
+ * synchronising `stream` (the only synchronising call in the library).
+ * ------------------------------------------------------------------------ */
+pc_status pc_workspace_status(const void *ws, size_t ws_bytes, void *stream, int32_t *code_out);
+
+/* ------------------------------------------------------------------------
+ * Optional per-kernel timing with HIP events on the launch stream.
+ * pc_prof_enable(1) makes every later launch record an event pair; after the
+ * caller has synchronised, pc_prof_read fills per-kernel launch counts and
+ * summed milliseconds (kernels in a fixed internal order) and clears them.
+ * Host-side state, not thread-safe.
+ * ------------------------------------------------------------------------ */
+void pc_prof_enable(int on);
+int pc_prof_kernel_count(void);
+const char *pc_prof_kernel_name(int i);
+pc_status pc_prof_read(uint64_t *launches, double *total_ms, int n);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PC_H */

@@ -1,0 +1,133 @@
+// libpc: status strings, workspace status, fill kernel and the optional
+// per-kernel event timing shared by every entry point.
+#include <vector>
+
+#include "pc_internal.h"
+
+namespace pc {
+
+static const char *kKernelNames[K_COUNT] = {
+    "fill_u32",          "hash_blocks",        "sort_digit_hist", "sort_digit_scan",
+    "sort_onesweep_pass", "link_prev_next",    "sd_cold_count",   "sd_scan",
+    "sd_tile_map",       "sd_dominance_pass",  "sd_local_finish", "mrc_hist",
+    "mrc_cost"};
+
+struct ProfEvent {
+    int kid;
+    hipEvent_t a, b;
+};
+
+static bool g_prof = false;
+static std::vector<ProfEvent> g_events;
+static std::vector<hipEvent_t> g_pool;
+static hipEvent_t g_pending = nullptr;
+static uint64_t g_launches[K_COUNT];
+static double g_ms[K_COUNT];
+
+static hipEvent_t get_event() {
+    if (!g_pool.empty()) {
+        hipEvent_t e = g_pool.back();
+        g_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+void prof_begin(int kid, hipStream_t s) {
+    (void)kid;
+    if (!g_prof) return;
+    g_pending = get_event();
+    if (g_pending && hipEventRecord(g_pending, s) != hipSuccess) g_pending = nullptr;
+}
+
+void prof_end(int kid, hipStream_t s) {
+    if (!g_prof || !g_pending) return;
+    hipEvent_t b = get_event();
+    if (!b) return;
+    if (hipEventRecord(b, s) != hipSuccess) return;
+    g_events.push_back({kid, g_pending, b});
+    g_pending = nullptr;
+}
+
+int device_cus() {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        return 256;
+    return cus;
+}
+
+__global__ void fill_u32_kernel(uint32_t *__restrict__ p, uint32_t value, size_t count) {
+    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (; i < count; i += stride) p[i] = value;
+}
+
+pc_status fill_u32(uint32_t *p, uint32_t value, size_t count, hipStream_t s) {
+    if (count == 0) return PC_OK;
+    size_t blocks = (count + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    PC_LAUNCH(K_FILL32, fill_u32_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, value, count);
+    return PC_OK;
+}
+
+}  // namespace pc
+
+extern "C" {
+
+const char *pc_status_string(pc_status s) {
+    switch (s) {
+        case PC_OK: return "ok";
+        case PC_ERR_INVALID: return "invalid argument";
+        case PC_ERR_TOO_LARGE: return "too large: positions must fit uint32 below 0xFFFFFFFF";
+        case PC_ERR_WORKSPACE: return "workspace missing or too small";
+        case PC_ERR_DEVICE: return "HIP device call or kernel launch failed";
+        case PC_ERR_UNSUPPORTED: return "unsupported device";
+    }
+    return "unknown status";
+}
+
+int pc_version(void) { return 100; }
+
+pc_status pc_workspace_status(const void *ws, size_t ws_bytes, void *stream, int32_t *code_out) {
+    if (!ws || !code_out) return PC_ERR_INVALID;
+    if (ws_bytes < pc::WS_HEADER) return PC_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    int32_t v = 0;
+    if (hipMemcpyAsync(&v, ws, sizeof(v), hipMemcpyDeviceToHost, s) != hipSuccess) return PC_ERR_DEVICE;
+    if (hipStreamSynchronize(s) != hipSuccess) return PC_ERR_DEVICE;
+    *code_out = v;
+    return PC_OK;
+}
+
+void pc_prof_enable(int on) { pc::g_prof = on != 0; }
+
+int pc_prof_kernel_count(void) { return pc::K_COUNT; }
+
+const char *pc_prof_kernel_name(int i) {
+    return (i >= 0 && i < pc::K_COUNT) ? pc::kKernelNames[i] : "";
+}
+
+pc_status pc_prof_read(uint64_t *launches, double *total_ms, int n) {
+    for (auto &e : pc::g_events) {
+        float ms = 0.f;
+        if (hipEventSynchronize(e.b) != hipSuccess) return PC_ERR_DEVICE;
+        if (hipEventElapsedTime(&ms, e.a, e.b) != hipSuccess) return PC_ERR_DEVICE;
+        pc::g_launches[e.kid] += 1;
+        pc::g_ms[e.kid] += ms;
+        pc::g_pool.push_back(e.a);
+        pc::g_pool.push_back(e.b);
+    }
+    pc::g_events.clear();
+    for (int i = 0; i < n && i < pc::K_COUNT; ++i) {
+        if (launches) launches[i] = pc::g_launches[i];
+        if (total_ms) total_ms[i] = pc::g_ms[i];
+        pc::g_launches[i] = 0;
+        pc::g_ms[i] = 0.0;
+    }
+    return PC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,149 @@
+// Internal helpers of libpc (gfx950 / CDNA4, wave64).  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "pc.h"
+
+namespace pc {
+
+constexpr uint32_t NONE = PC_NONE;
+constexpr int WAVE = 64;
+
+// ---------------------------------------------------------------- workspace
+// Every workspace starts with a 256-byte header; word 0 is the device-side
+// status code (0 = fine), cleared at the start of every call.
+constexpr size_t WS_HEADER = 256;
+constexpr size_t WS_ALIGN = 256;
+
+inline size_t align_up(size_t x, size_t a = WS_ALIGN) { return (x + a - 1) / a * a; }
+
+struct Carver {
+    char *base;
+    size_t off;
+    template <class T>
+    T *take(size_t count) {
+        T *p = reinterpret_cast<T *>(base ? base + off : nullptr);
+        off = align_up(off + count * sizeof(T));
+        return p;
+    }
+};
+
+// error codes written to the workspace header
+constexpr int32_t DEV_ERR_LOOKBACK_TIMEOUT = 1;
+constexpr int32_t DEV_ERR_BAD_LAYOUT = 2;
+constexpr int32_t DEV_ERR_BAD_CAPS = 3;
+
+// ------------------------------------------------------------ kernel launches
+enum KernelId {
+    K_FILL32 = 0,
+    K_HASH,
+    K_SORT_HIST,
+    K_SORT_SCAN,
+    K_SORT_PASS,
+    K_LINK,
+    K_SD_COLD,
+    K_SD_SCAN,
+    K_SD_TILES,
+    K_SD_PASS,
+    K_SD_LOCAL,
+    K_MRC_HIST,
+    K_MRC_COST,
+    K_COUNT
+};
+
+void prof_begin(int kid, hipStream_t s);
+void prof_end(int kid, hipStream_t s);
+
+// Launch, bracket with profiling events, and turn a launch error into
+// PC_ERR_DEVICE.  Must be used inside a function returning pc_status.
+#define PC_LAUNCH(kid, kernel, grid, block, shmem, stream, ...)                   \
+    do {                                                                          \
+        ::pc::prof_begin((kid), (stream));                                        \
+        hipLaunchKernelGGL(kernel, (grid), (block), (shmem), (stream), __VA_ARGS__); \
+        ::pc::prof_end((kid), (stream));                                          \
+        if (hipGetLastError() != hipSuccess) return PC_ERR_DEVICE;                \
+    } while (0)
+
+// compute units of the current device (256 on MI355X)
+int device_cus();
+
+// fill a uint32 array with a value on a stream (used instead of memset so the
+// same code stays valid under graph capture)
+pc_status fill_u32(uint32_t *p, uint32_t value, size_t count, hipStream_t s);
+
+// ------------------------------------------------------------ device helpers
+__device__ __forceinline__ uint64_t lanemask_lt() {
+    const int lane = threadIdx.x & (WAVE - 1);
+    return lane ? (~0ull >> (64 - lane)) : 0ull;
+}
+
+// popcount of (mask & lanes below me)
+__device__ __forceinline__ uint32_t mbcnt(uint64_t mask) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+
+__device__ __forceinline__ uint32_t ld_acquire(const uint32_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_release(uint32_t *p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t ld_acquire64(const uint64_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_release64(uint64_t *p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// exclusive prefix sum across the 64 lanes of a wave
+__device__ __forceinline__ uint32_t wave_excl_scan(uint32_t v) {
+    const int lane = threadIdx.x & (WAVE - 1);
+    uint32_t x = v;
+#pragma unroll
+    for (int d = 1; d < WAVE; d <<= 1) {
+        uint32_t y = __shfl_up(x, d, WAVE);
+        if (lane >= d) x += y;
+    }
+    return x - v;
+}
+
+// exclusive prefix-OR of 64-bit masks across the 64 lanes of a wave
+__device__ __forceinline__ uint64_t wave_excl_or(uint64_t v) {
+    const int lane = threadIdx.x & (WAVE - 1);
+    uint64_t x = v;
+#pragma unroll
+    for (int d = 1; d < WAVE; d <<= 1) {
+        uint64_t y = __shfl_up(x, d, WAVE);
+        if (lane >= d) x |= y;
+    }
+    uint64_t e = __shfl_up(x, 1, WAVE);
+    return lane ? e : 0ull;
+}
+
+// Block-wide exclusive scan of one value per thread (blockDim.x <= 1024).
+// `tmp` must hold blockDim.x/64 uint32.  Returns the block total in *total.
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t *tmp, uint32_t *total) {
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int w = threadIdx.x / WAVE;
+    const int nw = blockDim.x / WAVE;
+    uint32_t e = wave_excl_scan(v);
+    if (lane == WAVE - 1) tmp[w] = e + v;
+    __syncthreads();
+    uint32_t base = 0, tot = 0;
+    for (int i = 0; i < nw; ++i) {
+        uint32_t s = tmp[i];
+        if (i < w) base += s;
+        tot += s;
+    }
+    __syncthreads();
+    *total = tot;
+    return base + e;
+}
+
+}  // namespace pc

@@ -1,0 +1,134 @@
+// Hit-ratio and compute-savings histograms (pc_mrc_weighted).
+//
+// The block hit ratio counts every access, compulsory misses included
+// (Sec. 3.2); the compute-savings ratio weights each hit by the recompute
+// cost it avoids over the cost of all accesses (Sec. 5.2), with a cost that
+// grows with the block's depth (Sec. 4.4; linear model in Appendix C):
+// cost(t) = alpha + beta * depth[t].  Because LRU hits at capacity c exactly
+// when D < c, binning D on the capacity edges gives every capacity at once.
+//
+// GPU mapping: a grid-stride stream over dist / depth / next; each workgroup
+// keeps private LDS bins (count, depth sum, next-use gap count) filled with
+// LDS atomics after an upper-bound search of the edges held in LDS, then adds
+// its non-zero bins to the outputs with global 64-bit atomics.  Integer
+// atomics make the result independent of scheduling order.  A last tiny
+// kernel forms alpha*count + beta*depthsum exactly as 128-bit integers.
+#include "pc_internal.h"
+
+namespace pc {
+
+constexpr int MRC_THREADS = 256;
+
+// number of edges <= x (edges non-decreasing)
+__device__ __forceinline__ uint32_t upper_bound(const uint64_t *e, uint32_t m, uint64_t x) {
+    uint32_t lo = 0, hi = m;
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (e[mid] <= x) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+}
+
+__global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
+    const uint32_t *__restrict__ dist, const uint32_t *__restrict__ depth,
+    const uint32_t *__restrict__ next, uint64_t n, const uint64_t *__restrict__ caps, uint32_t K,
+    uint64_t *__restrict__ count, uint64_t *__restrict__ depthsum, uint64_t *__restrict__ nexthist,
+    int32_t *__restrict__ err) {
+    extern __shared__ uint64_t smem[];
+    uint64_t *s_caps = smem;                  // K
+    uint64_t *s_ds = s_caps + K;              // K+1
+    uint32_t *s_cnt = reinterpret_cast<uint32_t *>(s_ds + K + 1);   // K+1
+    uint32_t *s_nh = s_cnt + K + 1;           // K+1
+    for (uint32_t i = threadIdx.x; i < K; i += blockDim.x) {
+        s_caps[i] = caps[i];
+        if (blockIdx.x == 0 && i + 1 < K && caps[i] > caps[i + 1]) atomicOr(err, DEV_ERR_BAD_CAPS);
+    }
+    for (uint32_t i = threadIdx.x; i <= K; i += blockDim.x) {
+        s_ds[i] = 0;
+        s_cnt[i] = 0;
+        s_nh[i] = 0;
+    }
+    __syncthreads();
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n; t += stride) {
+        const uint32_t d = dist[t];
+        const uint32_t bin = d == NONE ? K : upper_bound(s_caps, K, d);
+        atomicAdd(&s_cnt[bin], 1u);
+        if (depth) {
+            const uint32_t dep = depth[t];
+            if (dep) atomicAdd(reinterpret_cast<unsigned long long *>(&s_ds[bin]), (unsigned long long)dep);
+        }
+        if (next) {
+            const uint32_t q = next[t];
+            const uint32_t nb = q == NONE ? K : upper_bound(s_caps, K, (uint64_t)q - t);
+            atomicAdd(&s_nh[nb], 1u);
+        }
+    }
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i <= K; i += blockDim.x) {
+        if (s_cnt[i]) atomicAdd(reinterpret_cast<unsigned long long *>(&count[i]), (unsigned long long)s_cnt[i]);
+        if (s_ds[i]) atomicAdd(reinterpret_cast<unsigned long long *>(&depthsum[i]), (unsigned long long)s_ds[i]);
+        if (next && s_nh[i])
+            atomicAdd(reinterpret_cast<unsigned long long *>(&nexthist[i]), (unsigned long long)s_nh[i]);
+    }
+}
+
+// cost = alpha*count + beta*depthsum as a 128-bit integer (hi:lo), mod 2^128
+__global__ void mrc_cost_kernel(const uint64_t *__restrict__ count, const uint64_t *__restrict__ depthsum,
+                                uint32_t bins, uint64_t alpha, uint64_t beta, uint64_t *__restrict__ lo,
+                                uint64_t *__restrict__ hi) {
+    const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= bins) return;
+    const uint64_t c = count[i], d = depthsum[i];
+    const uint64_t a_lo = alpha * c, a_hi = __umul64hi(alpha, c);
+    const uint64_t b_lo = beta * d, b_hi = __umul64hi(beta, d);
+    const uint64_t s = a_lo + b_lo;
+    lo[i] = s;
+    hi[i] = a_hi + b_hi + (s < a_lo ? 1ull : 0ull);
+}
+
+}  // namespace pc
+
+extern "C" {
+
+size_t pc_mrc_weighted_ws(uint64_t n, uint32_t n_caps) {
+    (void)n;
+    (void)n_caps;
+    return pc::WS_HEADER;
+}
+
+pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uint32_t *next, uint64_t n,
+                          const uint64_t *caps, uint32_t n_caps, uint64_t alpha, uint64_t beta,
+                          uint64_t *count, uint64_t *depthsum, uint64_t *cost_lo, uint64_t *cost_hi,
+                          uint64_t *nextuse_hist, void *ws, size_t ws_bytes, void *stream) {
+    if (n >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
+    if (n_caps == 0 || n_caps > PC_MAX_CAPS) return PC_ERR_INVALID;
+    if (!caps || !count || !depthsum || !cost_lo || !cost_hi) return PC_ERR_INVALID;
+    if (n > 0 && !dist) return PC_ERR_INVALID;
+    if (next && !nextuse_hist) return PC_ERR_INVALID;
+    if (!ws) return PC_ERR_WORKSPACE;
+    if (ws_bytes < pc_mrc_weighted_ws(n, n_caps)) return PC_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    int32_t *hdr = reinterpret_cast<int32_t *>(ws);
+    const uint32_t bins = n_caps + 1;
+    pc_status st;
+    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(hdr), 0u, 1, s)) != PC_OK) return st;
+    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(count), 0u, 2 * (size_t)bins, s)) != PC_OK) return st;
+    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(depthsum), 0u, 2 * (size_t)bins, s)) != PC_OK) return st;
+    if (nextuse_hist &&
+        (st = pc::fill_u32(reinterpret_cast<uint32_t *>(nextuse_hist), 0u, 2 * (size_t)bins, s)) != PC_OK)
+        return st;
+
+    const int cus = pc::device_cus();
+    uint64_t grid = (n + pc::MRC_THREADS * 16 - 1) / (pc::MRC_THREADS * 16);
+    if (grid > (uint64_t)cus * 8) grid = (uint64_t)cus * 8;
+    if (grid == 0) grid = 1;
+    const size_t shmem = (size_t)n_caps * 8 + (size_t)bins * 8 + (size_t)bins * 8;
+    PC_LAUNCH(pc::K_MRC_HIST, pc::mrc_hist_kernel, dim3((unsigned)grid), dim3(pc::MRC_THREADS), shmem, s, dist,
+              depth, next, n, caps, n_caps, count, depthsum, nextuse_hist, hdr);
+    PC_LAUNCH(pc::K_MRC_COST, pc::mrc_cost_kernel, dim3((bins + 255) / 256), dim3(256), 0, s, count, depthsum,
+              bins, alpha, beta, cost_lo, cost_hi);
+    return PC_OK;
+}
+
+}  // extern "C"

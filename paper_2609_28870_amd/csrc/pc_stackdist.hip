@@ -1,0 +1,569 @@
+// Exact LRU stack distance (pc_stack_distance).
+//
+// Definition: D(t) = #{ i in (prev(t), t) : next(i) > t }, the number of
+// distinct blocks touched since the previous use; an LRU cache of c blocks
+// hits exactly when D < c (LRU is a stack algorithm; Sec. 5 "LRU as a
+// bedrock", Appendix B "stack distance between reuses").
+//
+// Reformulation used here.  With v(j) = prev(j) + 1 (0 for a cold access),
+// the number of j < t with v(j) < v(t) is prev(t) + 1 + D(t): every i <=
+// prev(t) qualifies, and in the window (prev(t), t) exactly the first use of
+// each distinct block does.  Non-cold v are distinct, so with Z(t) = number of
+// cold accesses before t and C'(t) = #{ non-cold j < t : v(j) < v(t) }:
+//        D(t) = Z(t) + C'(t) - v(t).
+// C' is a two-dimensional dominance count.  The non-cold accesses are taken in
+// v order -- that is just next[] read in index order, since next[p] = t
+// exactly when v(t) = p + 1 -- and partitioned by the bits of t from the top
+// (MSD radix).  At every level an element adds the number of elements that
+// precede it in v order, sit in the same bucket (same higher bits of t) and
+// carry a smaller digit.  Summed over all levels this is exactly C'(t), and
+// the last level leaves every element at its own t.
+//
+// Buckets are ranges of t, so their sizes are known in advance from the
+// per-4096 prefix of cold counts: #non-cold t < X = X - Z(X).
+//   * sd_cold_count + sd_scan      -> Z at every multiple of 4096
+//   * sd_dominance_pass (1-3 times) -> 8-bit digits above bit 12; per tile of
+//     2048 elements: wave ballots build per-chunk digit masks (two 16-entry
+//     nibble tables) that give, for every lane, the earlier lanes with a
+//     smaller / equal digit; a 2-D prefix over (chunk, digit) in LDS extends
+//     that to the tile; a per-bucket decoupled look-back extends it across
+//     tiles; the tile is then written out digit-partitioned through LDS.
+//   * sd_local_finish -> one workgroup per 4096-range of t: two in-LDS levels
+//     of 6 bits finish the count, then D is written in t order with the cold
+//     prefix from a block scan.
+#include "pc_internal.h"
+
+namespace pc {
+
+constexpr int LOCAL_BITS = 12;
+constexpr uint32_t LOCAL_SPAN = 1u << LOCAL_BITS;   // 4096
+constexpr int DOM_THREADS = 256;
+constexpr int DOM_WAVES = DOM_THREADS / WAVE;
+constexpr int DOM_CHUNKS_PER_WAVE = 8;
+constexpr int DOM_CHUNKS = DOM_WAVES * DOM_CHUNKS_PER_WAVE;   // 32
+constexpr int DOM_TILE = DOM_CHUNKS * WAVE;                    // 2048
+constexpr int DOM_RADIX = 256;
+constexpr int LOC_THREADS = 256;
+constexpr int LOC_WAVES = LOC_THREADS / WAVE;
+constexpr int LOC_CHUNKS = LOCAL_SPAN / WAVE;                  // 64
+constexpr int LOC_CPW = LOC_CHUNKS / LOC_WAVES;                // 16
+constexpr uint32_t ST_AGG = 1u << 30;
+constexpr uint32_t ST_INC = 2u << 30;
+constexpr uint32_t ST_VAL = (1u << 30) - 1;
+constexpr uint32_t SD_SPIN_LIMIT = 1u << 22;
+constexpr int SCAN_THREADS = 1024;
+
+// number of non-cold accesses t < X (X a multiple of 4096, or X = n)
+__device__ __forceinline__ uint64_t cnt_lt(uint64_t X, const uint32_t *__restrict__ Zc) {
+    return X - Zc[(X + LOCAL_SPAN - 1) >> LOCAL_BITS];
+}
+
+__global__ __launch_bounds__(256) void sd_cold_count_kernel(const uint32_t *__restrict__ prev,
+                                                            uint64_t n, uint32_t *__restrict__ cnt) {
+    __shared__ uint32_t tmp[4];
+    const uint64_t base = (uint64_t)blockIdx.x * LOCAL_SPAN;
+    uint32_t c = 0;
+    for (int j = 0; j < (int)(LOCAL_SPAN / 256); ++j) {
+        const uint64_t t = base + (uint64_t)j * 256 + threadIdx.x;
+        if (t < n && prev[t] == NONE) ++c;
+    }
+    uint32_t total;
+    block_excl_scan(c, tmp, &total);
+    if (threadIdx.x == 0) cnt[blockIdx.x] = total;
+}
+
+// exclusive scan of m values (one workgroup); out[m] = total
+__global__ __launch_bounds__(SCAN_THREADS) void sd_scan_kernel(const uint32_t *__restrict__ in,
+                                                               uint64_t m,
+                                                               uint32_t *__restrict__ out) {
+    __shared__ uint32_t tmp[SCAN_THREADS / WAVE];
+    const uint64_t seg = (m + SCAN_THREADS - 1) / SCAN_THREADS;
+    const uint64_t lo = threadIdx.x * seg;
+    const uint64_t hi = lo + seg < m ? lo + seg : m;
+    uint32_t s = 0;
+    for (uint64_t i = lo; i < hi; ++i) s += in[i];
+    uint32_t total;
+    uint32_t run = block_excl_scan(s, tmp, &total);
+    for (uint64_t i = lo; i < hi; ++i) {
+        const uint32_t x = in[i];
+        out[i] = run;
+        run += x;
+    }
+    if (threadIdx.x == 0) out[m] = total;
+}
+
+// tiles per bucket of a dominance pass (bucket = t >> S)
+__global__ void sd_tile_count_kernel(const uint32_t *__restrict__ Zc, uint64_t n, int S,
+                                     uint64_t nbuckets, uint32_t *__restrict__ tcount) {
+    const uint64_t b = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= nbuckets) return;
+    uint64_t lo = b << S, hi = (b + 1) << S;
+    lo = lo < n ? lo : n;
+    hi = hi < n ? hi : n;
+    const uint64_t size = cnt_lt(hi, Zc) - cnt_lt(lo, Zc);
+    tcount[b] = (uint32_t)((size + DOM_TILE - 1) / DOM_TILE);
+}
+
+// One MSD level of the dominance count over 8-bit digits d = (t >> s) & mask.
+// FIRST: the input is next[] in index order (= v order), one bucket, tiles
+// over index ranges; otherwise the input is the previous level's output and
+// tiles never straddle a bucket (bucket = t >> (s + k)).
+template <bool FIRST>
+__global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
+    const uint32_t *__restrict__ in_t, const uint32_t *__restrict__ in_acc,
+    uint32_t *__restrict__ out_t, uint32_t *__restrict__ out_acc, uint64_t n,
+    const uint32_t *__restrict__ Zc, int s, int k, const uint32_t *__restrict__ tfirst,
+    uint64_t nbuckets, uint32_t *__restrict__ status, uint32_t *__restrict__ counter,
+    int32_t *__restrict__ err) {
+    __shared__ uint16_t s_h[DOM_CHUNKS][DOM_RADIX];     // chunk histograms -> column prefix
+    __shared__ uint16_t s_pl[DOM_CHUNKS][DOM_RADIX];    // 2-D prefix (earlier chunks, smaller digit)
+    __shared__ uint32_t s_st[DOM_TILE];                 // staged t
+    __shared__ uint32_t s_sa[DOM_TILE];                 // staged acc
+    __shared__ uint64_t s_mt[DOM_WAVES][4][16];         // nibble mask tables per wave
+    __shared__ uint32_t s_lstart[DOM_RADIX];
+    __shared__ uint32_t s_gl[DOM_RADIX];
+    __shared__ uint32_t s_base[DOM_RADIX];
+    __shared__ uint32_t s_tmp[DOM_WAVES];
+    __shared__ uint32_t s_tile;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (WAVE - 1);
+    const int w = tid / WAVE;
+    const uint32_t dmask = (1u << k) - 1u;
+    const int S = s + k;
+
+    if (tid == 0) s_tile = atomicAdd(counter, 1u);
+    {
+        uint64_t *z = reinterpret_cast<uint64_t *>(&s_h[0][0]);
+        for (int i = tid; i < DOM_CHUNKS * DOM_RADIX / 4; i += DOM_THREADS) z[i] = 0;
+    }
+    __syncthreads();
+    const uint32_t tile = s_tile;
+
+    // ---- locate the tile
+    uint64_t bucket = 0, e0 = 0, e1 = 0, first_tile = 0;
+    if (FIRST) {
+        const uint64_t tiles = (n + DOM_TILE - 1) / DOM_TILE;
+        if (tile >= tiles) return;
+        e0 = (uint64_t)tile * DOM_TILE;
+        e1 = e0 + DOM_TILE < n ? e0 + DOM_TILE : n;
+    } else {
+        if (tile >= tfirst[nbuckets]) return;
+        uint64_t lo = 0, hi = nbuckets;   // largest b with tfirst[b] <= tile
+        while (hi - lo > 1) {
+            const uint64_t mid = (lo + hi) >> 1;
+            if (tfirst[mid] <= tile) lo = mid; else hi = mid;
+        }
+        bucket = lo;
+        first_tile = tfirst[bucket];
+        uint64_t blo = bucket << S, bhi = (bucket + 1) << S;
+        blo = blo < n ? blo : n;
+        bhi = bhi < n ? bhi : n;
+        const uint64_t bs = cnt_lt(blo, Zc), be = cnt_lt(bhi, Zc);
+        e0 = bs + (uint64_t)(tile - first_tile) * DOM_TILE;
+        e1 = e0 + DOM_TILE < be ? e0 + DOM_TILE : be;
+    }
+
+    // ---- load and rank inside each 64-lane chunk
+    uint32_t t[DOM_CHUNKS_PER_WAVE], acc[DOM_CHUNKS_PER_WAVE];
+    uint16_t q_ic[DOM_CHUNKS_PER_WAVE], l_ic[DOM_CHUNKS_PER_WAVE];
+    bool ok[DOM_CHUNKS_PER_WAVE];
+#pragma unroll
+    for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
+        const uint64_t e = e0 + (uint64_t)(w * DOM_CHUNKS_PER_WAVE + i) * WAVE + lane;
+        if (FIRST) {
+            const uint32_t x = e < e1 ? in_t[e] : NONE;
+            ok[i] = x != NONE;
+            t[i] = x;
+            acc[i] = 0;
+        } else {
+            ok[i] = e < e1;
+            t[i] = ok[i] ? in_t[e] : 0u;
+            acc[i] = ok[i] ? in_acc[e] : 0u;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
+        const int c = w * DOM_CHUNKS_PER_WAVE + i;
+        const uint32_t d = (t[i] >> s) & dmask;
+        const uint64_t vm = ballot(ok[i]);
+        uint64_t B[8];
+#pragma unroll
+        for (int b = 0; b < 8; ++b) B[b] = ballot(ok[i] && ((d >> b) & 1));
+        // lanes 0..15 build the nibble tables: lanes whose high / low nibble
+        // equals q, and the union over smaller q
+        uint64_t mh = 0, ml = 0;
+        if (lane < 16) {
+            mh = vm;
+            ml = vm;
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                const bool bit = (lane >> b) & 1;
+                mh &= bit ? B[4 + b] : ~B[4 + b];
+                ml &= bit ? B[b] : ~B[b];
+            }
+        }
+        const uint64_t lh = wave_excl_or(mh);
+        const uint64_t ll = wave_excl_or(ml);
+        if (lane < 16) {
+            s_mt[w][0][lane] = mh;
+            s_mt[w][1][lane] = ml;
+            s_mt[w][2][lane] = lh;
+            s_mt[w][3][lane] = ll;
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (ok[i]) {
+            const uint32_t h = d >> 4, l = d & 15;
+            const uint64_t Mh = s_mt[w][0][h], Ml = s_mt[w][1][l];
+            const uint64_t Lh = s_mt[w][2][h], Ll = s_mt[w][3][l];
+            const uint64_t eq = Mh & Ml;
+            const uint64_t lt = Lh | (Mh & Ll);
+            q_ic[i] = (uint16_t)mbcnt(eq);
+            l_ic[i] = (uint16_t)mbcnt(lt);
+            if (q_ic[i] == 0) s_h[c][d] = (uint16_t)__popcll(eq);
+        } else {
+            q_ic[i] = 0;
+            l_ic[i] = 0;
+        }
+        __builtin_amdgcn_wave_barrier();
+    }
+    __syncthreads();
+
+    // ---- column prefix over chunks (thread = digit) and tile totals
+    uint32_t tot = 0;
+    {
+        const int d = tid;
+        for (int c = 0; c < DOM_CHUNKS; ++c) {
+            const uint32_t h = s_h[c][d];
+            s_h[c][d] = (uint16_t)tot;
+            tot += h;
+        }
+    }
+    __syncthreads();
+    // ---- row prefix over digits: s_pl[c][d] = sum_{d' < d} s_h[c][d']
+    for (int c = w * (DOM_CHUNKS / DOM_WAVES); c < (w + 1) * (DOM_CHUNKS / DOM_WAVES); ++c) {
+        const uint32_t a0 = s_h[c][4 * lane + 0], a1 = s_h[c][4 * lane + 1];
+        const uint32_t a2 = s_h[c][4 * lane + 2], a3 = s_h[c][4 * lane + 3];
+        const uint32_t x = wave_excl_scan(a0 + a1 + a2 + a3);
+        s_pl[c][4 * lane + 0] = (uint16_t)x;
+        s_pl[c][4 * lane + 1] = (uint16_t)(x + a0);
+        s_pl[c][4 * lane + 2] = (uint16_t)(x + a0 + a1);
+        s_pl[c][4 * lane + 3] = (uint16_t)(x + a0 + a1 + a2);
+    }
+    uint32_t n_valid;
+    const uint32_t lst = block_excl_scan(tot, s_tmp, &n_valid);
+
+    // ---- look-back across the bucket's earlier tiles (thread = digit)
+    uint32_t G = 0;
+    {
+        uint32_t *mine = status + (uint64_t)tile * DOM_RADIX + tid;
+        if (tile == first_tile) {
+            st_release(mine, ST_INC | tot);
+        } else {
+            st_release(mine, ST_AGG | tot);
+            int64_t j = (int64_t)tile - 1;
+            uint32_t spins = 0;
+            while (j >= (int64_t)first_tile) {
+                const uint32_t x = ld_acquire(status + (uint64_t)j * DOM_RADIX + tid);
+                if ((x & (ST_AGG | ST_INC)) == 0) {
+                    if (++spins > SD_SPIN_LIMIT) {
+                        atomicOr(err, DEV_ERR_LOOKBACK_TIMEOUT);
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                    continue;
+                }
+                G += x & ST_VAL;
+                if (x & ST_INC) break;
+                --j;
+            }
+            st_release(mine, ST_INC | ((G + tot) & ST_VAL));
+        }
+    }
+    uint32_t gsum;
+    const uint32_t GL = block_excl_scan(G, s_tmp, &gsum);
+    {
+        const uint64_t X = ((bucket << k) + (uint64_t)tid) << s;
+        const uint64_t sub = cnt_lt(X < n ? X : n, Zc);
+        s_lstart[tid] = lst;
+        s_gl[tid] = GL;
+        s_base[tid] = (uint32_t)(sub + G - lst);   // wraps mod 2^32 like positions
+    }
+    __syncthreads();
+
+    // ---- stage the tile digit-partitioned, with the level's count added
+#pragma unroll
+    for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
+        if (ok[i]) {
+            const int c = w * DOM_CHUNKS_PER_WAVE + i;
+            const uint32_t d = (t[i] >> s) & dmask;
+            const uint32_t j = s_lstart[d] + s_h[c][d] + q_ic[i];
+            s_st[j] = t[i];
+            s_sa[j] = acc[i] + s_gl[d] + s_pl[c][d] + l_ic[i];
+        }
+    }
+    __syncthreads();
+    for (uint32_t j = tid; j < n_valid; j += DOM_THREADS) {
+        const uint32_t tt = s_st[j];
+        const uint32_t d = (tt >> s) & dmask;
+        const uint32_t dst = s_base[d] + j;
+        // consistent prev/next always land inside; inconsistent input is
+        // reported instead of written out of bounds
+        if (dst < n) {
+            out_t[dst] = tt;
+            out_acc[dst] = s_sa[j];
+        } else {
+            atomicOr(err, DEV_ERR_BAD_LAYOUT);
+        }
+    }
+}
+
+// Last 12 bits, one workgroup per 4096-range of t, then D in t order.
+__global__ __launch_bounds__(LOC_THREADS) void sd_local_kernel(
+    const uint32_t *__restrict__ in_t, const uint32_t *__restrict__ in_acc,
+    const uint32_t *__restrict__ prev, uint64_t n, const uint32_t *__restrict__ Zc,
+    uint32_t *__restrict__ dist) {
+    __shared__ uint32_t s_st[LOCAL_SPAN];
+    __shared__ uint32_t s_sa[LOCAL_SPAN];
+    __shared__ uint32_t s_work[LOCAL_SPAN];   // [64][64] u16 tables, then the slot array
+    __shared__ uint32_t s_tot[64];
+    __shared__ uint32_t s_lstart[64];
+    __shared__ uint32_t s_tmp[LOC_WAVES];
+    uint16_t(*s_h)[64] = reinterpret_cast<uint16_t(*)[64]>(&s_work[0]);
+    uint16_t(*s_pl)[64] = reinterpret_cast<uint16_t(*)[64]>(&s_work[LOCAL_SPAN / 2]);
+    uint32_t *slot = s_work;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (WAVE - 1);
+    const int w = tid / WAVE;
+    const uint64_t r0 = (uint64_t)blockIdx.x * LOCAL_SPAN;
+    const uint64_t r1 = r0 + LOCAL_SPAN < n ? r0 + LOCAL_SPAN : n;
+    const uint64_t e0 = cnt_lt(r0, Zc), e1 = cnt_lt(r1, Zc);
+
+    // ---- level A: digit = bits 6..11 of t, chunks of 64 in v order
+    uint32_t t[LOC_CPW], acc[LOC_CPW];
+    uint8_t qa[LOC_CPW], la[LOC_CPW];
+    bool ok[LOC_CPW];
+#pragma unroll
+    for (int i = 0; i < LOC_CPW; ++i) {
+        const uint64_t e = e0 + (uint64_t)(w * LOC_CPW + i) * WAVE + lane;
+        ok[i] = e < e1;
+        t[i] = ok[i] ? in_t[e] : 0u;
+        acc[i] = ok[i] ? in_acc[e] : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < LOC_CPW; ++i) {
+        const int c = w * LOC_CPW + i;
+        const uint32_t d = (t[i] >> 6) & 63;
+        const uint64_t vm = ballot(ok[i]);
+        uint64_t m = vm;
+#pragma unroll
+        for (int b = 0; b < 6; ++b) {
+            const uint64_t B = ballot(ok[i] && ((d >> b) & 1));
+            m &= ((lane >> b) & 1) ? B : ~B;   // lanes whose digit equals this lane's index
+        }
+        const uint64_t lmask = wave_excl_or(m);
+        s_h[c][lane] = (uint16_t)__popcll(m);
+        const uint64_t eq = __shfl(m, (int)d, WAVE);
+        const uint64_t lt = __shfl(lmask, (int)d, WAVE);
+        qa[i] = ok[i] ? (uint8_t)mbcnt(eq) : 0;
+        la[i] = ok[i] ? (uint8_t)mbcnt(lt) : 0;
+    }
+    __syncthreads();
+    if (tid < 64) {
+        uint32_t run = 0;
+        for (int c = 0; c < LOC_CHUNKS; ++c) {
+            const uint32_t h = s_h[c][tid];
+            s_h[c][tid] = (uint16_t)run;
+            run += h;
+        }
+        s_tot[tid] = run;
+        s_lstart[tid] = wave_excl_scan(run);
+    }
+    __syncthreads();
+    for (int c = w * LOC_CPW; c < (w + 1) * LOC_CPW; ++c) {
+        s_pl[c][lane] = (uint16_t)wave_excl_scan(s_h[c][lane]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < LOC_CPW; ++i) {
+        if (ok[i]) {
+            const int c = w * LOC_CPW + i;
+            const uint32_t d = (t[i] >> 6) & 63;
+            const uint32_t j = s_lstart[d] + s_h[c][d] + qa[i];
+            s_st[j] = t[i];
+            s_sa[j] = acc[i] + s_pl[c][d] + la[i];
+        }
+    }
+    __syncthreads();
+
+    // ---- level B: bits 0..5 inside each 64-range (at most 64 elements)
+    for (int g = w; g < 64; g += LOC_WAVES) {
+        const uint32_t cnt = s_tot[g];
+        const uint32_t base = s_lstart[g];
+        const bool okb = (uint32_t)lane < cnt;
+        const uint32_t tb = okb ? s_st[base + lane] : 0u;
+        const uint32_t ab = okb ? s_sa[base + lane] : 0u;
+        const uint32_t d = tb & 63;
+        const uint64_t vm = ballot(okb);
+        uint64_t m = vm;
+#pragma unroll
+        for (int b = 0; b < 6; ++b) {
+            const uint64_t B = ballot(okb && ((d >> b) & 1));
+            m &= ((lane >> b) & 1) ? B : ~B;
+        }
+        const uint64_t lmask = wave_excl_or(m);
+        const uint64_t lt = __shfl(lmask, (int)d, WAVE);
+        // slot[] aliases the level-A tables, which are dead after the barrier
+        if (okb) slot[tb & (LOCAL_SPAN - 1)] = ab + mbcnt(lt);
+    }
+    __syncthreads();
+
+    // ---- D in t order: Z(t) from a block scan of cold flags
+    constexpr int PER = LOCAL_SPAN / LOC_THREADS;   // 16
+    const uint64_t tbase = r0 + (uint64_t)tid * PER;
+    uint32_t p[PER];
+    uint32_t cold = 0;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const uint64_t tt = tbase + j;
+        p[j] = tt < n ? prev[tt] : 0u;
+        cold += (tt < n && p[j] == NONE) ? 1u : 0u;
+    }
+    uint32_t allcold;
+    uint32_t z = Zc[blockIdx.x] + block_excl_scan(cold, s_tmp, &allcold);
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const uint64_t tt = tbase + j;
+        if (tt < n) {
+            if (p[j] == NONE) {
+                dist[tt] = NONE;
+                ++z;
+            } else {
+                dist[tt] = z + slot[tt - r0] - (p[j] + 1u);
+            }
+        }
+    }
+}
+
+struct SdPlan {
+    int passes;
+    int s[4], k[4];
+    uint64_t nbuckets[4];
+    uint64_t grid[4];
+    uint64_t max_buckets, max_grid;
+};
+
+static SdPlan plan_sd(uint64_t n) {
+    SdPlan p{};
+    int nbits = 0;
+    while (nbits < 64 && (1ull << nbits) < n) ++nbits;   // bits of n-1
+    const int g = nbits > LOCAL_BITS ? nbits - LOCAL_BITS : 0;
+    p.passes = g == 0 ? 1 : (g + 7) / 8;
+    if (g == 0) {
+        p.k[0] = 1;
+    } else {
+        p.k[0] = g - 8 * (p.passes - 1);
+        for (int i = 1; i < p.passes; ++i) p.k[i] = 8;
+    }
+    p.s[p.passes - 1] = LOCAL_BITS;
+    for (int i = p.passes - 2; i >= 0; --i) p.s[i] = p.s[i + 1] + p.k[i + 1];
+    p.max_buckets = 1;
+    p.max_grid = 1;
+    for (int i = 0; i < p.passes; ++i) {
+        const int S = p.s[i] + p.k[i];
+        p.nbuckets[i] = S >= 64 ? 1 : (n + (1ull << S) - 1) >> S;
+        if (p.nbuckets[i] == 0) p.nbuckets[i] = 1;
+        p.grid[i] = (n + DOM_TILE - 1) / DOM_TILE + (i == 0 ? 0 : p.nbuckets[i]);
+        if (p.grid[i] == 0) p.grid[i] = 1;
+        if (p.nbuckets[i] > p.max_buckets) p.max_buckets = p.nbuckets[i];
+        if (p.grid[i] > p.max_grid) p.max_grid = p.grid[i];
+    }
+    return p;
+}
+
+struct SdWs {
+    int32_t *hdr;
+    uint32_t *cold, *Zc, *tcount, *tfirst, *counters;
+    uint32_t *at, *aa, *bt, *ba;
+    uint32_t *status;
+    size_t bytes;
+};
+
+static SdWs carve_sd(void *ws, uint64_t n, const SdPlan &p) {
+    Carver c{(char *)ws, 0};
+    SdWs w;
+    const uint64_t nchunks = (n + LOCAL_SPAN - 1) / LOCAL_SPAN;
+    w.hdr = c.take<int32_t>(WS_HEADER / sizeof(int32_t));
+    w.cold = c.take<uint32_t>(nchunks + 1);
+    w.Zc = c.take<uint32_t>(nchunks + 2);
+    w.tcount = c.take<uint32_t>(p.max_buckets + 1);
+    w.tfirst = c.take<uint32_t>(p.max_buckets + 2);
+    w.counters = c.take<uint32_t>(4);
+    w.at = c.take<uint32_t>(n);
+    w.aa = c.take<uint32_t>(n);
+    w.bt = c.take<uint32_t>(n);
+    w.ba = c.take<uint32_t>(n);
+    w.status = c.take<uint32_t>(p.max_grid * DOM_RADIX);
+    w.bytes = c.off;
+    return w;
+}
+
+}  // namespace pc
+
+extern "C" {
+
+size_t pc_stack_distance_ws(uint64_t n) {
+    const pc::SdPlan p = pc::plan_sd(n);
+    return pc::carve_sd(nullptr, n, p).bytes;
+}
+
+pc_status pc_stack_distance(const uint32_t *prev, const uint32_t *next, uint64_t n, uint32_t *dist,
+                            void *ws, size_t ws_bytes, void *stream) {
+    if (n >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
+    if (n > 0 && (!prev || !next || !dist)) return PC_ERR_INVALID;
+    if (!ws) return PC_ERR_WORKSPACE;
+    if (ws_bytes < pc_stack_distance_ws(n)) return PC_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    const pc::SdPlan p = pc::plan_sd(n);
+    pc::SdWs w = pc::carve_sd(ws, n, p);
+    pc_status st = pc::fill_u32(reinterpret_cast<uint32_t *>(w.hdr), 0u, 1, s);
+    if (st != PC_OK || n == 0) return st;
+
+    const uint64_t nchunks = (n + pc::LOCAL_SPAN - 1) / pc::LOCAL_SPAN;
+    PC_LAUNCH(pc::K_SD_COLD, pc::sd_cold_count_kernel, dim3((unsigned)nchunks), dim3(256), 0, s, prev, n,
+              w.cold);
+    PC_LAUNCH(pc::K_SD_SCAN, pc::sd_scan_kernel, dim3(1), dim3(pc::SCAN_THREADS), 0, s, w.cold, nchunks,
+              w.Zc);
+    if ((st = pc::fill_u32(w.counters, 0u, 4, s)) != PC_OK) return st;
+
+    uint32_t *src_t = nullptr, *src_a = nullptr;
+    for (int i = 0; i < p.passes; ++i) {
+        uint32_t *dt = (i & 1) ? w.bt : w.at;
+        uint32_t *da = (i & 1) ? w.ba : w.aa;
+        const int S = p.s[i] + p.k[i];
+        if ((st = pc::fill_u32(w.status, 0u, p.grid[i] * pc::DOM_RADIX, s)) != PC_OK) return st;
+        if (i == 0) {
+            PC_LAUNCH(pc::K_SD_PASS, pc::sd_dominance_kernel<true>, dim3((unsigned)p.grid[i]),
+                      dim3(pc::DOM_THREADS), 0, s, next, (const uint32_t *)nullptr, dt, da, n, w.Zc,
+                      p.s[i], p.k[i], (const uint32_t *)nullptr, (uint64_t)1, w.status, w.counters + i,
+                      w.hdr);
+        } else {
+            const uint64_t nb = p.nbuckets[i];
+            PC_LAUNCH(pc::K_SD_TILES, pc::sd_tile_count_kernel, dim3((unsigned)((nb + 255) / 256)), dim3(256),
+                      0, s, w.Zc, n, S, nb, w.tcount);
+            PC_LAUNCH(pc::K_SD_SCAN, pc::sd_scan_kernel, dim3(1), dim3(pc::SCAN_THREADS), 0, s, w.tcount, nb,
+                      w.tfirst);
+            PC_LAUNCH(pc::K_SD_PASS, pc::sd_dominance_kernel<false>, dim3((unsigned)p.grid[i]),
+                      dim3(pc::DOM_THREADS), 0, s, src_t, src_a, dt, da, n, w.Zc, p.s[i], p.k[i],
+                      w.tfirst, nb, w.status, w.counters + i, w.hdr);
+        }
+        src_t = dt;
+        src_a = da;
+    }
+    PC_LAUNCH(pc::K_SD_LOCAL, pc::sd_local_kernel, dim3((unsigned)nchunks), dim3(pc::LOC_THREADS), 0, s,
+              src_t, src_a, prev, n, w.Zc, dist);
+    return PC_OK;
+}
+
+}  // extern "C"

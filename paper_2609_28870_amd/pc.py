@@ -1,0 +1,301 @@
+"""Thin ctypes binding of libpc (include/pc.h).
+
+Argument marshalling only: every step of the hot path runs in the HIP
+kernels of ``libpc.so``.  PyTorch provides device memory and the current HIP
+stream.  Unsigned arrays travel in signed torch tensors of the same width
+(uint64 bit patterns in int64, uint32 in int32); ``as_u64`` / ``as_u32``
+reinterpret them on the host.
+
+There is no fallback: if ``libpc.so`` is missing or no GPU is visible, calls
+raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "_lib", "libpc.so")
+NONE = 0xFFFFFFFF
+
+_lib = None
+
+_vp = ctypes.c_void_p
+_u64 = ctypes.c_uint64
+_u32 = ctypes.c_uint32
+_sz = ctypes.c_size_t
+_st = ctypes.c_int
+
+
+class PcError(RuntimeError):
+    pass
+
+
+def lib():
+    """Load libpc.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise PcError("libpc.so not built: run paper_2609_28870_amd/build.py (or __graft_entry__.build())")
+    L = ctypes.CDLL(LIB_PATH)
+    L.pc_status_string.restype = ctypes.c_char_p
+    L.pc_status_string.argtypes = [_st]
+    L.pc_version.restype = ctypes.c_int
+    L.pc_hash_blocks_ws.restype = _sz
+    L.pc_hash_blocks_ws.argtypes = [_u32]
+    L.pc_hash_blocks.restype = _st
+    L.pc_hash_blocks.argtypes = [_vp, _u64, _vp, _vp, _u32, _u32, _vp, _u64, _vp, _u64, _vp, _vp,
+                                 _vp, _sz, _vp]
+    L.pc_prev_next_use_ws.restype = _sz
+    L.pc_prev_next_use_ws.argtypes = [_u64]
+    L.pc_prev_next_use.restype = _st
+    L.pc_prev_next_use.argtypes = [_vp, _u64, _vp, _vp, _vp, _sz, _vp]
+    L.pc_stack_distance_ws.restype = _sz
+    L.pc_stack_distance_ws.argtypes = [_u64]
+    L.pc_stack_distance.restype = _st
+    L.pc_stack_distance.argtypes = [_vp, _vp, _u64, _vp, _vp, _sz, _vp]
+    L.pc_mrc_weighted_ws.restype = _sz
+    L.pc_mrc_weighted_ws.argtypes = [_u64, _u32]
+    L.pc_mrc_weighted.restype = _st
+    L.pc_mrc_weighted.argtypes = [_vp, _vp, _vp, _u64, _vp, _u32, _u64, _u64, _vp, _vp, _vp, _vp,
+                                  _vp, _vp, _sz, _vp]
+    L.pc_workspace_status.restype = _st
+    L.pc_workspace_status.argtypes = [_vp, _sz, _vp, ctypes.POINTER(ctypes.c_int32)]
+    L.pc_prof_enable.restype = None
+    L.pc_prof_enable.argtypes = [ctypes.c_int]
+    L.pc_prof_kernel_count.restype = ctypes.c_int
+    L.pc_prof_kernel_name.restype = ctypes.c_char_p
+    L.pc_prof_kernel_name.argtypes = [ctypes.c_int]
+    L.pc_prof_read.restype = _st
+    L.pc_prof_read.argtypes = [ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_double),
+                               ctypes.c_int]
+    _lib = L
+    return L
+
+
+def check(status: int) -> None:
+    if status != 0:
+        raise PcError("libpc: %s (%d)" % (lib().pc_status_string(status).decode(), status))
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise PcError("expected a GPU tensor")
+    if not t.is_contiguous():
+        raise PcError("expected a contiguous tensor")
+    return t.data_ptr()
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _dev():
+    if not torch.cuda.is_available():
+        raise PcError("no GPU visible: libpc needs an MI355X (gfx950)")
+    return torch.device("cuda", torch.cuda.current_device())
+
+
+def workspace(nbytes: int) -> torch.Tensor:
+    """Device scratch for one call (torch's allocator aligns to >= 256 B)."""
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=_dev())
+
+
+def workspace_status(ws: torch.Tensor) -> int:
+    """Device-side status code of a workspace (synchronises the stream)."""
+    code = ctypes.c_int32(0)
+    check(lib().pc_workspace_status(_ptr(ws), ws.numel(), _stream(), ctypes.byref(code)))
+    return int(code.value)
+
+
+def as_u64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().cpu().numpy().view(np.uint64)
+
+
+def as_u32(t: torch.Tensor) -> np.ndarray:
+    return t.detach().cpu().numpy().view(np.uint32)
+
+
+def to_dev_u64(a) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint64).view(np.int64)).to(_dev())
+
+
+def to_dev_u32(a) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint32).view(np.int32)).to(_dev())
+
+
+# ------------------------------------------------------------------ stages
+
+def hash_blocks(tokens: torch.Tensor, tok_start: torch.Tensor, tok_len: torch.Tensor,
+                blk_off: torch.Tensor, n_blocks: int, block_size: int = 16,
+                parent: Optional[torch.Tensor] = None, root: int = 0, want_depth: bool = True,
+                keys: Optional[torch.Tensor] = None, depth: Optional[torch.Tensor] = None,
+                ws: Optional[torch.Tensor] = None):
+    """pc_hash_blocks: keys (int64 bits of uint64) and depth (int32 bits)."""
+    L = lib()
+    dev = _dev()
+    n_seqs = tok_len.numel()
+    if keys is None:
+        keys = torch.empty(n_blocks, dtype=torch.int64, device=dev)
+    if want_depth and depth is None:
+        depth = torch.empty(n_blocks, dtype=torch.int32, device=dev)
+    if ws is None:
+        ws = workspace(L.pc_hash_blocks_ws(n_seqs))
+    check(L.pc_hash_blocks(_ptr(tokens), tokens.numel(), _ptr(tok_start), _ptr(tok_len), n_seqs,
+                           block_size, _ptr(parent), root & (2 ** 64 - 1), _ptr(blk_off), n_blocks,
+                           _ptr(keys), _ptr(depth) if want_depth else None, _ptr(ws), ws.numel(),
+                           _stream()))
+    return keys, (depth if want_depth else None), ws
+
+
+def prev_next_use(keys: torch.Tensor, prev: Optional[torch.Tensor] = None,
+                  nxt: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
+    L = lib()
+    n = keys.numel()
+    dev = _dev()
+    if prev is None:
+        prev = torch.empty(n, dtype=torch.int32, device=dev)
+    if nxt is None:
+        nxt = torch.empty(n, dtype=torch.int32, device=dev)
+    if ws is None:
+        ws = workspace(L.pc_prev_next_use_ws(n))
+    check(L.pc_prev_next_use(_ptr(keys), n, _ptr(prev), _ptr(nxt), _ptr(ws), ws.numel(), _stream()))
+    return prev, nxt, ws
+
+
+def stack_distance(prev: torch.Tensor, nxt: torch.Tensor, dist: Optional[torch.Tensor] = None,
+                   ws: Optional[torch.Tensor] = None):
+    L = lib()
+    n = prev.numel()
+    if dist is None:
+        dist = torch.empty(n, dtype=torch.int32, device=_dev())
+    if ws is None:
+        ws = workspace(L.pc_stack_distance_ws(n))
+    check(L.pc_stack_distance(_ptr(prev), _ptr(nxt), n, _ptr(dist), _ptr(ws), ws.numel(), _stream()))
+    return dist, ws
+
+
+def mrc_weighted(dist: torch.Tensor, caps: torch.Tensor, depth: Optional[torch.Tensor] = None,
+                 nxt: Optional[torch.Tensor] = None, alpha: int = 1, beta: int = 0,
+                 out: Optional[dict] = None, ws: Optional[torch.Tensor] = None):
+    """pc_mrc_weighted: per-bin count, depthsum, cost (lo/hi) and next-use
+    histogram as int64 tensors of n_caps+1 entries (uint64 bit patterns)."""
+    L = lib()
+    n = dist.numel()
+    k = caps.numel()
+    dev = _dev()
+    if out is None:
+        out = {name: torch.empty(k + 1, dtype=torch.int64, device=dev)
+               for name in ("count", "depthsum", "cost_lo", "cost_hi", "nextuse")}
+    if ws is None:
+        ws = workspace(L.pc_mrc_weighted_ws(n, k))
+    check(L.pc_mrc_weighted(_ptr(dist), _ptr(depth), _ptr(nxt), n, _ptr(caps), k,
+                            alpha & (2 ** 64 - 1), beta & (2 ** 64 - 1), _ptr(out["count"]),
+                            _ptr(out["depthsum"]), _ptr(out["cost_lo"]), _ptr(out["cost_hi"]),
+                            _ptr(out["nextuse"]) if nxt is not None else None, _ptr(ws), ws.numel(),
+                            _stream()))
+    return out, ws
+
+
+def bins_to_host(out: dict) -> dict:
+    """Device bins -> python ints (cost as exact 128-bit integers)."""
+    c = as_u64(out["count"]).tolist()
+    d = as_u64(out["depthsum"]).tolist()
+    lo = as_u64(out["cost_lo"]).tolist()
+    hi = as_u64(out["cost_hi"]).tolist()
+    nu = as_u64(out["nextuse"]).tolist()
+    return {"count": [int(x) for x in c], "depthsum": [int(x) for x in d],
+            "cost": [int(h) << 64 | int(l) for l, h in zip(lo, hi)], "nextuse": [int(x) for x in nu]}
+
+
+def curves(count, cost):
+    """Hit ratio and compute-savings ratio at each capacity edge from exact
+    integer bins: hits(c_k) = sum count[0..k], saved(c_k) = sum cost[0..k];
+    each ratio is one float64 division of exactly rounded integers."""
+    n = sum(count)
+    total = sum(cost)
+    hr, csr = [], []
+    h = s = 0
+    for k in range(len(count) - 1):
+        h += count[k]
+        s += cost[k]
+        hr.append(float(h) / float(n) if n else 0.0)
+        csr.append(float(s) / float(total) if total else 0.0)
+    return hr, csr
+
+
+# --------------------------------------------------------------- profiling
+
+def prof_enable(on: bool = True) -> None:
+    lib().pc_prof_enable(1 if on else 0)
+
+
+def prof_read() -> dict:
+    """{kernel: (launches, total_ms)} since the last read (caller syncs)."""
+    L = lib()
+    n = L.pc_prof_kernel_count()
+    la = (ctypes.c_uint64 * n)()
+    ms = (ctypes.c_double * n)()
+    check(L.pc_prof_read(la, ms, n))
+    return {L.pc_prof_kernel_name(i).decode(): (int(la[i]), float(ms[i])) for i in range(n)}
+
+
+# ---------------------------------------------------------------- pipeline
+
+class Pipeline:
+    """All four stages over one trace with buffers and workspaces allocated
+    once; ``run()`` enqueues hash -> prev/next -> stack distance -> bins."""
+
+    def __init__(self, tokens, tok_start, tok_len, blk_off, n_blocks: int, caps,
+                 block_size: int = 16, alpha: int = 1, beta: int = 0, with_nextuse: bool = True):
+        L = lib()
+        dev = _dev()
+        self.tokens, self.tok_start, self.tok_len, self.blk_off = tokens, tok_start, tok_len, blk_off
+        self.n = int(n_blocks)
+        self.B = block_size
+        self.caps = caps
+        self.alpha, self.beta = alpha, beta
+        self.with_nextuse = with_nextuse
+        n = self.n
+        self.keys = torch.empty(n, dtype=torch.int64, device=dev)
+        self.depth = torch.empty(n, dtype=torch.int32, device=dev)
+        self.prev = torch.empty(n, dtype=torch.int32, device=dev)
+        self.next = torch.empty(n, dtype=torch.int32, device=dev)
+        self.dist = torch.empty(n, dtype=torch.int32, device=dev)
+        k = caps.numel()
+        self.bins = {name: torch.empty(k + 1, dtype=torch.int64, device=dev)
+                     for name in ("count", "depthsum", "cost_lo", "cost_hi", "nextuse")}
+        self.ws_hash = workspace(L.pc_hash_blocks_ws(tok_len.numel()))
+        self.ws_pn = workspace(L.pc_prev_next_use_ws(n))
+        self.ws_sd = workspace(L.pc_stack_distance_ws(n))
+        self.ws_mrc = workspace(L.pc_mrc_weighted_ws(n, k))
+
+    def run(self):
+        hash_blocks(self.tokens, self.tok_start, self.tok_len, self.blk_off, self.n, self.B,
+                    keys=self.keys, depth=self.depth, ws=self.ws_hash)
+        prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn)
+        stack_distance(self.prev, self.next, self.dist, ws=self.ws_sd)
+        mrc_weighted(self.dist, self.caps, self.depth, self.next if self.with_nextuse else None,
+                     self.alpha, self.beta, out=self.bins, ws=self.ws_mrc)
+
+    def status(self) -> dict:
+        return {name: workspace_status(ws) for name, ws in
+                (("hash", self.ws_hash), ("prev_next", self.ws_pn), ("stack_distance", self.ws_sd),
+                 ("mrc", self.ws_mrc))}
+
+
+def upload_trace(trace, block_size: Optional[int] = None):
+    """Copy a pcgen.Trace's arrays to the GPU (input preparation, untimed)."""
+    B = block_size or trace.block_size
+    off = trace.blk_off(B)
+    dev = _dev()
+    return dict(tokens=torch.from_numpy(trace.tokens).to(dev),
+                tok_start=to_dev_u64(trace.tok_start), tok_len=to_dev_u32(trace.tok_len),
+                blk_off=to_dev_u64(off), n_blocks=int(off[-1]), block_size=B)

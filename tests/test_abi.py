@@ -1,0 +1,110 @@
+"""The C ABI: libpc loads, exports every function include/pc.h declares, and
+rejects bad arguments before touching the device.  CPU only (no compute)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_28870_amd import pc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "pc.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(pc_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(pc.LIB_PATH):
+        pytest.fail("libpc.so is not built (run __graft_entry__.build())")
+    return pc.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert len(names) >= 15
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_status_strings(L):
+    for code in (0, -1, -2, -3, -4, -5):
+        assert L.pc_status_string(code)
+    assert L.pc_version() >= 100
+
+
+def test_workspace_queries_grow_with_n(L):
+    a = L.pc_prev_next_use_ws(1000)
+    b = L.pc_prev_next_use_ws(10 ** 6)
+    assert 0 < a < b
+    assert L.pc_stack_distance_ws(10 ** 6) > L.pc_stack_distance_ws(1000) > 0
+    assert L.pc_hash_blocks_ws(10) >= 256
+    assert L.pc_mrc_weighted_ws(10, 69) >= 256
+
+
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation
+
+
+def test_hash_rejects_bad_arguments(L):
+    ws = L.pc_hash_blocks_ws(4)
+    args = lambda B=16, n_seqs=4, nb=100, wsz=ws, tokens=FAKE, w=FAKE: (
+        tokens, 1000, FAKE, FAKE, n_seqs, B, None, 0, FAKE, nb, FAKE, None, w, wsz, None)
+    assert L.pc_hash_blocks(*args(B=15)) == -1
+    assert L.pc_hash_blocks(*args(B=0)) == -1
+    assert L.pc_hash_blocks(*args(B=2048)) == -1
+    assert L.pc_hash_blocks(*args(n_seqs=0x80000000)) == -2
+    assert L.pc_hash_blocks(*args(nb=0xFFFFFFFF)) == -2
+    assert L.pc_hash_blocks(*args(tokens=None)) == -1
+    assert L.pc_hash_blocks(*args(w=None)) == -3
+    assert L.pc_hash_blocks(*args(wsz=ws - 1)) == -3
+
+
+def test_prev_next_rejects_bad_arguments(L):
+    n = 1000
+    ws = L.pc_prev_next_use_ws(n)
+    assert L.pc_prev_next_use(FAKE, 0xFFFFFFFF, FAKE, FAKE, FAKE, 1 << 40, None) == -2
+    assert L.pc_prev_next_use(None, n, FAKE, FAKE, FAKE, ws, None) == -1
+    assert L.pc_prev_next_use(FAKE, n, FAKE, None, FAKE, ws, None) == -1
+    assert L.pc_prev_next_use(FAKE, n, FAKE, FAKE, None, ws, None) == -3
+    assert L.pc_prev_next_use(FAKE, n, FAKE, FAKE, FAKE, ws - 1, None) == -3
+
+
+def test_stack_distance_rejects_bad_arguments(L):
+    n = 5000
+    ws = L.pc_stack_distance_ws(n)
+    assert L.pc_stack_distance(FAKE, FAKE, 0xFFFFFFFF, FAKE, FAKE, 1 << 40, None) == -2
+    assert L.pc_stack_distance(FAKE, None, n, FAKE, FAKE, ws, None) == -1
+    assert L.pc_stack_distance(FAKE, FAKE, n, None, FAKE, ws, None) == -1
+    assert L.pc_stack_distance(FAKE, FAKE, n, FAKE, FAKE, ws - 1, None) == -3
+
+
+def test_mrc_rejects_bad_arguments(L):
+    ws = L.pc_mrc_weighted_ws(10, 4)
+    ok = lambda **kw: dict(dict(dist=FAKE, depth=None, nxt=None, n=10, caps=FAKE, k=4, a=1, b=0,
+                                cnt=FAKE, ds=FAKE, lo=FAKE, hi=FAKE, nh=None, w=FAKE, wsz=ws), **kw)
+    call = lambda d: L.pc_mrc_weighted(d["dist"], d["depth"], d["nxt"], d["n"], d["caps"], d["k"],
+                                       d["a"], d["b"], d["cnt"], d["ds"], d["lo"], d["hi"], d["nh"],
+                                       d["w"], d["wsz"], None)
+    assert call(ok(k=0)) == -1
+    assert call(ok(k=1025)) == -1
+    assert call(ok(caps=None)) == -1
+    assert call(ok(nxt=FAKE)) == -1          # next without nextuse_hist
+    assert call(ok(n=0xFFFFFFFF)) == -2
+    assert call(ok(w=None)) == -3
+
+
+def test_workspace_status_rejects_null(L):
+    code = ctypes.c_int32(0)
+    assert L.pc_workspace_status(None, 256, None, ctypes.byref(code)) == -1
+    assert L.pc_workspace_status(FAKE, 16, None, ctypes.byref(code)) == -3
+
+
+def test_profiling_table(L):
+    n = L.pc_prof_kernel_count()
+    names = [L.pc_prof_kernel_name(i).decode() for i in range(n)]
+    assert "hash_blocks" in names and "sd_dominance_pass" in names and "mrc_hist" in names
+    assert pc.prof_read() is not None

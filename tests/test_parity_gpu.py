@@ -1,0 +1,222 @@
+"""Parity of the HIP path (through the C ABI) against the CPU oracle.
+
+Every stage is checked on its own, fed with the oracle's inputs, and then end
+to end.  Integer outputs (keys, prev/next, distances, bins, 128-bit costs)
+must be bit-exact; the float64 ratios are formed from the exact integers and
+must agree to 1e-12 relative (they come out identical)."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import pcgen
+from paper_2609_28870_amd import pc
+
+pytestmark = pytest.mark.gpu
+NONE = pc.NONE
+CUSTOM_COSTS = [(1, 0), (2 * 16 * 3_000_000_000, 2 * 16 * 16), (1, 1)]   # uniform, literal, linear(d+1)
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def gpu_hash(trace, B=16, parent=None, root=0):
+    up = pc.upload_trace(trace, B)
+    par = pc.to_dev_u64(parent) if parent is not None else None
+    keys, depth, ws = pc.hash_blocks(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"],
+                                     up["n_blocks"], B, parent=par, root=root)
+    assert pc.workspace_status(ws) == 0
+    return pc.as_u64(keys), pc.as_u32(depth)
+
+
+def gpu_prev_next(keys_np):
+    keys = pc.to_dev_u64(keys_np)
+    prev, nxt, ws = pc.prev_next_use(keys)
+    assert pc.workspace_status(ws) == 0
+    return pc.as_u32(prev), pc.as_u32(nxt)
+
+
+def gpu_dist(prev_np, next_np):
+    dist, ws = pc.stack_distance(pc.to_dev_u32(prev_np), pc.to_dev_u32(next_np))
+    assert pc.workspace_status(ws) == 0
+    return pc.as_u32(dist)
+
+
+def gpu_bins(dist_np, caps, depth_np=None, next_np=None, alpha=1, beta=0):
+    out, ws = pc.mrc_weighted(pc.to_dev_u32(dist_np), pc.to_dev_u64(caps),
+                              pc.to_dev_u32(depth_np) if depth_np is not None else None,
+                              pc.to_dev_u32(next_np) if next_np is not None else None, alpha, beta)
+    assert pc.workspace_status(ws) == 0
+    return pc.bins_to_host(out)
+
+
+def check_keys_path(keys, depth=None, caps=None, label=""):
+    """prev/next, distances and bins of a key stream against the oracle."""
+    n = keys.size
+    say("case", label, "n", n)
+    ids = oracle.key_ids(keys)
+    op, on = oracle.prev_next(keys, ids)
+    gp, gn = gpu_prev_next(keys)
+    assert np.array_equal(gp, op), label + " prev"
+    assert np.array_equal(gn, on), label + " next"
+    od = oracle.stack_distance_bit(op)
+    gd = gpu_dist(op, on)
+    bad = np.nonzero(gd != od)[0]
+    assert bad.size == 0, "%s dist: %d mismatches, first t=%s gpu=%s want=%s" % (
+        label, bad.size, bad[:5], gd[bad[:5]], od[bad[:5]])
+    if caps is not None:
+        dep = depth if depth is not None else np.zeros(n, np.uint32)
+        for a, b in CUSTOM_COSTS:
+            cnt, dsum, cost = oracle.mrc_bins(keys, caps, dep, a, b, ids)
+            g = gpu_bins(od, caps, dep, on, a, b)
+            assert g["count"] == cnt and g["depthsum"] == dsum and g["cost"] == cost, (label, a, b)
+            assert g["nextuse"] == oracle.nextuse_hist(on, caps)
+            hr, csr = pc.curves(g["count"], g["cost"])
+            ohr, ocsr = oracle.curves(cnt, cost)
+            np.testing.assert_allclose(hr, ohr, rtol=1e-12, atol=0)
+            np.testing.assert_allclose(csr, ocsr, rtol=1e-12, atol=0)
+    return od
+
+
+# ------------------------------------------------------------------ stages
+
+def test_hash_tiny_trace_bit_exact():
+    tr = pcgen.make_trace("tiny")
+    ok, od = oracle.hash_trace(tr)
+    gk, gd = gpu_hash(tr)
+    assert np.array_equal(gk, ok) and np.array_equal(gd, od)
+
+
+@pytest.mark.parametrize("B", [2, 6, 64, 256])
+def test_hash_other_block_sizes(B):
+    tr = pcgen.make_trace("tiny")
+    ok, od = oracle.hash_trace(tr, B)
+    gk, gd = gpu_hash(tr, B)
+    assert np.array_equal(gk, ok) and np.array_equal(gd, od)
+
+
+def test_hash_unaligned_views_parent_and_root():
+    tr = pcgen.make_trace("tiny")
+    r = tr.n_requests
+    # shift every request by one token (4-byte aligned only) and give parents
+    tr2 = pcgen.subtrace(tr, 0, r)
+    tr2.tok_start = tr.tok_start + np.uint64(1)
+    tr2.tok_len = np.maximum(tr.tok_len.astype(np.int64) - 1, 0).astype(np.uint32)
+    parent = (np.arange(r, dtype=np.uint64) * np.uint64(0x9E3779B97F4A7C15))
+    ok, _ = oracle.hash_requests(tr2.tokens, tr2.tok_start, tr2.tok_len, 16, parent=parent)
+    gk, _ = gpu_hash(tr2, 16, parent=parent)
+    assert np.array_equal(gk, ok)
+    ok, _ = oracle.hash_requests(tr.tokens, tr.tok_start, tr.tok_len, 16, root=77)
+    gk, _ = gpu_hash(tr, 16, root=77)
+    assert np.array_equal(gk, ok)
+
+
+def test_tiny_trace_every_stage():
+    tr = pcgen.make_trace("tiny")
+    keys, depth = oracle.hash_trace(tr)
+    od = check_keys_path(keys, depth, tr.caps(), "tiny")
+    assert np.array_equal(od, oracle.stack_distance_walk(keys))
+
+
+def test_tiny_trace_end_to_end_pipeline():
+    tr = pcgen.make_trace("tiny")
+    keys, depth = oracle.hash_trace(tr)
+    caps = tr.caps()
+    up = pc.upload_trace(tr)
+    a, b = CUSTOM_COSTS[1]
+    p = pc.Pipeline(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
+                    pc.to_dev_u64(caps), 16, a, b)
+    p.run()
+    torch.cuda.synchronize()
+    assert p.status() == {"hash": 0, "prev_next": 0, "stack_distance": 0, "mrc": 0}
+    assert np.array_equal(pc.as_u64(p.keys), keys)
+    op, on = oracle.prev_next(keys)
+    assert np.array_equal(pc.as_u32(p.prev), op) and np.array_equal(pc.as_u32(p.next), on)
+    assert np.array_equal(pc.as_u32(p.dist), oracle.stack_distance_walk(keys))
+    g = pc.bins_to_host(p.bins)
+    cnt, dsum, cost = oracle.mrc_bins(keys, caps, depth, a, b)
+    assert g["count"] == cnt and g["depthsum"] == dsum and g["cost"] == cost
+
+
+# -------------------------------------------------------------- edge cases
+
+def stream(kind, n, seed=0):
+    rng = np.random.default_rng(seed)
+    if kind == "equal":
+        return np.full(n, 0xABCDEF, np.uint64)
+    if kind == "distinct":
+        return (rng.permutation(n).astype(np.uint64) * np.uint64(2654435761) + np.uint64(1))
+    if kind == "hot":
+        return pcgen.random_keys(n, max(n // 50, 1), seed, hot=0.5)
+    if kind == "few":
+        return pcgen.random_keys(n, 7, seed)
+    if kind == "cyclic":
+        m = max(n // 7, 1)
+        return (np.arange(n) % m).astype(np.uint64) + np.uint64(5)
+    return pcgen.random_keys(n, max(n // 10, 1), seed)
+
+
+@pytest.mark.parametrize("n", [0, 1, 2, 3, 63, 64, 65, 2047, 2048, 2049, 4095, 4096, 4097, 8193])
+def test_small_and_ragged_sizes(n):
+    check_keys_path(stream("mixed", n, n), caps=np.array([1, 2, 5, 100, 1000], np.uint64),
+                    label="ragged%d" % n)
+
+
+@pytest.mark.parametrize("kind", ["equal", "distinct", "hot", "few", "cyclic", "mixed"])
+def test_degenerate_streams(kind):
+    check_keys_path(stream(kind, 70001, 3), caps=np.array([0, 1, 2, 7, 10000, 10 ** 8], np.uint64),
+                    label=kind)
+
+
+@pytest.mark.parametrize("n", [(1 << 20) + 12345, (1 << 21) - 1])
+def test_two_level_sizes(n):
+    check_keys_path(stream("mixed", n, 9), label="twolevel%d" % n)
+
+
+def test_determinism():
+    keys = stream("hot", 300000, 4)
+    op, on = oracle.prev_next(keys)
+    d1 = gpu_dist(op, on)
+    d2 = gpu_dist(op, on)
+    assert np.array_equal(d1, d2)
+    caps = np.array([1, 10, 100, 1000], np.uint64)
+    assert gpu_bins(d1, caps) == gpu_bins(d2, caps)
+
+
+# ------------------------------------------------------- workload-shaped
+
+def test_agent_trace_reduced_all_stages():
+    tr = pcgen.make_trace("agent", n_sessions=250)
+    keys, depth = oracle.hash_trace(tr)
+    gk, gd = gpu_hash(tr)
+    assert np.array_equal(gk, keys) and np.array_equal(gd, depth)
+    check_keys_path(keys, depth, tr.caps(), "agent250")
+
+
+@pytest.mark.parametrize("B", [64, 256])
+def test_agent_trace_granularity_sweep(B):
+    tr = pcgen.make_trace("agent", n_sessions=250)
+    keys, depth = oracle.hash_trace(tr, B)
+    gk, _ = gpu_hash(tr, B)
+    assert np.array_equal(gk, keys)
+    check_keys_path(keys, depth, pcgen.capacities("tokens64", B), "agent250-B%d" % B)
+
+
+def test_chat_trace_reduced_with_shared_prompts():
+    tr = pcgen.make_trace("chat", n_sessions=1500)
+    keys, depth = oracle.hash_trace(tr)
+    gk, _ = gpu_hash(tr)
+    assert np.array_equal(gk, keys)
+    caps = tr.caps()[::6]
+    check_keys_path(keys, depth, caps, "chat1500")
