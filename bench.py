@@ -1,0 +1,205 @@
+"""Throughput of the prefix-cache hot path on one MI355X.
+
+One step = the whole path over the resident trace: chained block hashing ->
+prev/next-use indexing -> exact LRU stack distance -> hit-ratio /
+compute-savings bins over every capacity.  Inputs (token streams and the
+request table) are generated on the host, copied to HBM before timing, and
+stay resident; the timed region contains only the four library calls.
+
+Prints one JSON line (rank 0): block accesses per second, per-kernel times
+from HIP events recorded by the library on its launch stream, the roofline
+of the dominant kernel and the CPU oracle timed on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+# 32-bit integer vector lane-ops: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+ALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+P_LIN = 3_000_000_000          # FLOPs per token, linear part (agent cost model)
+
+# algorithmic bytes per element for each kernel (inputs it must read and
+# outputs it must write, once each)
+ALGO_BYTES = {
+    "hash_blocks": lambda B: 4 * B + 8 + 4,       # tokens, key, depth
+    "sort_onesweep_pass": lambda B: 12 + 12,      # (key, t) in and out
+    "link_prev_next": lambda B: 12 + 8,           # sorted (key, t) in, prev+next out
+    "sd_dominance_pass": lambda B: 8 + 8,         # (t, acc) in and out
+    "sd_local_finish": lambda B: 8 + 4 + 4,       # (t, acc), prev in; dist out
+    "mrc_hist": lambda B: 12,                     # dist, depth, next in
+}
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(trace, caps, alpha, beta, budget_accesses):
+    """The oracle (plain C, one thread) over the first requests of the same
+    trace: hash, prev/next, next-use histogram and one LRU simulation per
+    capacity edge -- the same outputs as one GPU step."""
+    import oracle
+    import pcgen
+    nb = (trace.tok_len // np.uint32(trace.block_size)).astype(np.int64)
+    r = int(np.searchsorted(np.cumsum(nb), budget_accesses)) + 1
+    r = min(r, trace.n_requests)
+    sub = pcgen.subtrace(trace, 0, r)
+    t0 = time.perf_counter()
+    keys, depth = oracle.hash_trace(sub)
+    ids = oracle.key_ids(keys)
+    _, nxt = oracle.prev_next(keys, ids)
+    oracle.nextuse_hist(nxt, caps)
+    oracle.mrc_bins(keys, caps, depth, alpha, beta, ids)
+    dt = time.perf_counter() - t0
+    return {"value": keys.size / dt, "unit": "block-accesses/s", "cores": 1, "kind": "oracle",
+            "sample": "first %d requests (%d block accesses) of the same trace; hash + prev/next + "
+                      "%d per-capacity LRU simulations; %.1f s" % (r, keys.size, len(caps), dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="full", choices=["tiny", "chat", "agent", "full"])
+    ap.add_argument("--sessions", type=int, default=None, help="override the session count")
+    ap.add_argument("--block-size", type=int, default=16)
+    ap.add_argument("--cpu-sample", type=int, default=20_000_000,
+                    help="block accesses in the oracle's timed sample (0 = skip)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 4 GiB device copy (for rocprof counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the hot path here is single-GPU "
+              "(multi-GPU sharding is a design note, not built); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import pcgen
+    from paper_2609_28870_amd import pc
+
+    B = args.block_size
+    t0 = time.perf_counter()
+    trace = pcgen.make_trace(args.workload, n_sessions=args.sessions, block_size=B)
+    caps_np = trace.caps(B)
+    n_blocks = trace.n_blocks(B)
+    log("trace %s: %d requests, %d block accesses, %d processed tokens, generated in %.1f s" % (
+        args.workload, trace.n_requests, n_blocks, trace.processed_tokens(), time.perf_counter() - t0))
+
+    torch.cuda.set_device(0)
+    alpha, beta = 2 * B * P_LIN, 2 * B * B
+    up = pc.upload_trace(trace, B)
+    caps = pc.to_dev_u64(caps_np)
+    pipe = pc.Pipeline(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
+                       caps, B, alpha, beta)
+    torch.cuda.synchronize()
+    log("inputs resident in HBM; device memory in use %.1f GB" % (torch.cuda.memory_allocated() / 1e9))
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log("copy calibration: 4 GiB read + 4 GiB written")
+
+    for i in range(args.warmup):
+        pipe.run()
+    torch.cuda.synchronize()
+    st = pipe.status()
+    if any(st.values()):
+        raise SystemExit("device status after warm-up: %s" % st)
+    log("warm-up done")
+
+    pc.prof_enable(True)
+    pc.prof_read()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for i in range(args.steps):
+        pipe.run()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t1
+    pc.prof_enable(False)
+    prof = pc.prof_read()
+    st = pipe.status()
+    if any(st.values()):
+        raise SystemExit("device status after timing: %s" % st)
+    log("timed %d steps in %.3f s" % (args.steps, wall))
+
+    ms_step = wall * 1e3 / args.steps
+    value = n_blocks / (ms_step / 1e3)
+    kernels = {}
+    for name, (launches, ms) in prof.items():
+        if launches == 0:
+            continue
+        per_step = ms / args.steps
+        entry = {"launches_per_step": launches // args.steps, "ms_per_step": round(per_step, 4),
+                 "avg_launch_ms": round(ms / launches, 4)}
+        if name in ALGO_BYTES:
+            per_launch = ALGO_BYTES[name](B) * n_blocks
+            entry["algo_bytes_per_launch"] = per_launch
+            entry["algo_GBps"] = round(per_launch / (ms / launches) / 1e6, 1)
+        kernels[name] = entry
+    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    d = kernels[dom]
+    if dom == "hash_blocks":
+        # nine splitmix steps per 16-token block; ~50 32-bit lane-ops per step
+        roof = {"bound": "alu", "achieved": None, "peak": ALU_PEAK_TOPS, "unit": "Tops/s"}
+    else:
+        achieved = d["algo_GBps"]
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    roof["kernel"] = dom
+    roof["traffic"] = None
+
+    # the curves themselves (exact integers -> float64 ratios)
+    bins = pc.bins_to_host(pipe.bins)
+    hr, csr = pc.curves(bins["count"], bins["cost"])
+    cb = None
+    if args.cpu_sample > 0:
+        log("timing the CPU oracle on a %d-access sample" % args.cpu_sample)
+        cb = cpu_baseline(trace, caps_np, alpha, beta, args.cpu_sample)
+
+    out = {
+        "metric": "KV-block accesses/sec for hash+stack-distance+MRC; achieved HBM GB/s",
+        "value": value,
+        "unit": "block-accesses/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "strong",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s trace (%s), block size %d" % (
+                args.workload, "70%% chat / 30%% agent sessions up to 2e9 context tokens"
+                if args.workload == "full" else "%s sessions" % (args.sessions or "default"), B),
+            "n_block_accesses": n_blocks,
+            "n_requests": trace.n_requests,
+            "processed_tokens": trace.processed_tokens(),
+            "capacities": int(caps_np.size),
+            "cost_model": "2*B*(P_lin + B*depth), P_lin=3e9",
+            "parallelism": "single GPU",
+        },
+        "roofline": roof,
+        "cpu_baseline": cb,
+        "kernels": kernels,
+        "curves_at": {str(int(c)): [round(h, 6), round(s, 6)]
+                      for c, h, s in zip(caps_np, hr, csr) if int(c) in pcgen.GIB_BLOCKS.values()},
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

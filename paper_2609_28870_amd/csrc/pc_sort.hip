@@ -141,13 +141,13 @@ __global__ __launch_bounds__(SORT_THREADS) void sort_pass_kernel(
         uint64_t *mine = status + (uint64_t)tile * RADIX + tid;
         uint32_t excl = 0;
         if (tile == 0) {
-            st_release64(mine, ep | FLAG_INC | cnt);
+            st_status64(mine, ep | FLAG_INC | cnt);
         } else {
-            st_release64(mine, ep | FLAG_AGG | cnt);
+            st_status64(mine, ep | FLAG_AGG | cnt);
             int64_t j = (int64_t)tile - 1;
             uint32_t spins = 0;
             while (j >= 0) {
-                const uint64_t x = ld_acquire64(status + (uint64_t)j * RADIX + tid);
+                const uint64_t x = ld_status64(status + (uint64_t)j * RADIX + tid);
                 if ((x >> 34) != epoch || (x & (FLAG_AGG | FLAG_INC)) == 0) {
                     if (++spins > SPIN_LIMIT) {
                         atomicOr(err, DEV_ERR_LOOKBACK_TIMEOUT);
@@ -160,7 +160,7 @@ __global__ __launch_bounds__(SORT_THREADS) void sort_pass_kernel(
                 if (x & FLAG_INC) break;
                 --j;
             }
-            st_release64(mine, ep | FLAG_INC | (uint32_t)(excl + cnt));
+            st_status64(mine, ep | FLAG_INC | (uint32_t)(excl + cnt));
         }
         s_gbase[tid] = start[tid] + excl - lst;
     }

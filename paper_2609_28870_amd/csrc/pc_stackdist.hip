@@ -258,13 +258,13 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     {
         uint32_t *mine = status + (uint64_t)tile * DOM_RADIX + tid;
         if (tile == first_tile) {
-            st_release(mine, ST_INC | tot);
+            st_status(mine, ST_INC | tot);
         } else {
-            st_release(mine, ST_AGG | tot);
+            st_status(mine, ST_AGG | tot);
             int64_t j = (int64_t)tile - 1;
             uint32_t spins = 0;
             while (j >= (int64_t)first_tile) {
-                const uint32_t x = ld_acquire(status + (uint64_t)j * DOM_RADIX + tid);
+                const uint32_t x = ld_status(status + (uint64_t)j * DOM_RADIX + tid);
                 if ((x & (ST_AGG | ST_INC)) == 0) {
                     if (++spins > SD_SPIN_LIMIT) {
                         atomicOr(err, DEV_ERR_LOOKBACK_TIMEOUT);
@@ -277,7 +277,7 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
                 if (x & ST_INC) break;
                 --j;
             }
-            st_release(mine, ST_INC | ((G + tot) & ST_VAL));
+            st_status(mine, ST_INC | ((G + tot) & ST_VAL));
         }
     }
     uint32_t gsum;

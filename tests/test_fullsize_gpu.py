@@ -1,0 +1,168 @@
+"""Parity at the benchmark's full size and launch configuration.
+
+The full-scale mixed trace (2e9 context tokens, ~2.1e9 block accesses) runs
+through the same Pipeline bench.py times.  The oracle cannot redo the whole
+trace, so it checks:
+
+* keys of sampled requests (hashed one by one by the oracle);
+* exact windows: distances and prev links only depend on the past, so for a
+  window [a, b) of the trace the oracle's own run over that window gives the
+  exact prev/next/dist of every access whose previous use lies inside it
+  (and the first window, a = 0, gives every access in it);
+* properties that hold at any size, checked with plain torch ops on the GPU
+  (independent of libpc): prev/next are inverse links between equal keys,
+  cold accesses equal first occurrences, and the bins equal a torch
+  bucketize of the distances.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import pcgen
+from paper_2609_28870_amd import pc
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(1500)]
+NONE = pc.NONE
+P_LIN = 3_000_000_000
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def full():
+    assert torch.cuda.is_available()
+    tr = pcgen.make_trace("full")
+    say("full trace generated:", tr.n_requests, "requests", tr.n_blocks(), "accesses")
+    caps = tr.caps()
+    B = 16
+    up = pc.upload_trace(tr, B)
+    p = pc.Pipeline(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
+                    pc.to_dev_u64(caps), B, 2 * B * P_LIN, 2 * B * B)
+    p.run()
+    torch.cuda.synchronize()
+    say("pipeline done, status", p.status())
+    yield tr, caps, p
+    del p
+    torch.cuda.empty_cache()
+
+
+def test_device_status_clean(full):
+    _, _, p = full
+    assert p.status() == {"hash": 0, "prev_next": 0, "stack_distance": 0, "mrc": 0}
+
+
+def test_sampled_request_keys(full):
+    tr, _, p = full
+    off = tr.blk_off()
+    rng = np.random.default_rng(0)
+    reqs = np.unique(np.concatenate([np.arange(200), rng.integers(0, tr.n_requests, 300),
+                                     [tr.n_requests - 1]]))
+    for r in reqs:
+        lo, hi = int(off[r]), int(off[r + 1])
+        if hi == lo:
+            continue
+        want, wd = oracle.hash_requests(tr.tokens, tr.tok_start[r:r + 1], tr.tok_len[r:r + 1], 16)
+        got = pc.as_u64(p.keys[lo:hi])
+        assert np.array_equal(got, want), r
+        assert np.array_equal(pc.as_u32(p.depth[lo:hi]), wd), r
+
+
+def window_requests(tr, a, b):
+    """Requests covering accesses [a, b) and the access offset of the first."""
+    off = tr.blk_off()
+    r0 = int(np.searchsorted(off, a, side="right")) - 1
+    r1 = int(np.searchsorted(off, b, side="left"))
+    return r0, r1, int(off[r0])
+
+
+@pytest.mark.parametrize("where", ["start", "middle", "end"])
+def test_exact_windows(full, where):
+    tr, _, p = full
+    n = p.n
+    m = 3_000_000
+    a = {"start": 0, "middle": n // 2, "end": n - m}[where]
+    r0, r1, base = window_requests(tr, a, a + m)
+    keys, _ = oracle.hash_requests(tr.tokens, tr.tok_start[r0:r1], tr.tok_len[r0:r1], 16)
+    keys = keys[a - base:a - base + m]
+    assert np.array_equal(pc.as_u64(p.keys[a:a + m]), keys)
+    op, on = oracle.prev_next(keys)
+    od = oracle.stack_distance_bit(op)
+    gp = pc.as_u32(p.prev[a:a + m]).astype(np.int64)
+    gn = pc.as_u32(p.next[a:a + m]).astype(np.int64)
+    gd = pc.as_u32(p.dist[a:a + m])
+    inside = op != NONE
+    say(where, "window", a, "accesses with in-window reuse:", int(inside.sum()))
+    assert np.array_equal(gp[inside], op[inside].astype(np.int64) + a)
+    assert np.array_equal(gd[inside], od[inside])
+    # accesses whose previous use is before the window: GPU says so too
+    outside = ~inside
+    assert np.all((gp[outside] == NONE) | (gp[outside] < a))
+    if a == 0:
+        assert np.all(gp[outside] == NONE) and np.all(gd[outside] == NONE)
+    has_next = on != NONE
+    assert np.array_equal(gn[has_next], on[has_next].astype(np.int64) + a)
+    assert np.all((gn[~has_next] == NONE) | (gn[~has_next] >= a + m))
+
+
+def test_links_are_consistent_everywhere(full):
+    _, _, p = full
+    n = p.n
+    chunk = 1 << 27
+    cold = last = 0
+    for lo in range(0, n, chunk):
+        hi = min(n, lo + chunk)
+        t = torch.arange(lo, hi, device="cuda", dtype=torch.int64)
+        pv = p.prev[lo:hi].to(torch.int64) & 0xFFFFFFFF
+        nx = p.next[lo:hi].to(torch.int64) & 0xFFFFFFFF
+        hp = pv != NONE
+        assert bool((pv[hp] < t[hp]).all())
+        back = p.next[pv[hp]].to(torch.int64) & 0xFFFFFFFF
+        assert bool((back == t[hp]).all())
+        assert bool((p.keys[pv[hp]] == p.keys[lo:hi][hp]).all())
+        hn = nx != NONE
+        assert bool((nx[hn] > t[hn]).all())
+        fwd = p.prev[nx[hn]].to(torch.int64) & 0xFFFFFFFF
+        assert bool((fwd == t[hn]).all())
+        cold += int((~hp).sum())
+        last += int((~hn).sum())
+        dd = p.dist[lo:hi].to(torch.int64) & 0xFFFFFFFF
+        assert bool(((dd == NONE) == (~hp)).all())
+        # D(t) counts distinct blocks strictly inside (prev, t)
+        assert bool((dd[hp] <= t[hp] - pv[hp] - 1).all())
+    assert cold == last   # first uses and last uses of each distinct key
+
+
+def test_bins_match_torch_bucketize(full):
+    tr, caps, p = full
+    n = p.n
+    k = caps.size
+    edges = torch.tensor(caps.astype(np.int64), device="cuda")
+    count = torch.zeros(k + 1, dtype=torch.int64, device="cuda")
+    dsum = torch.zeros(k + 1, dtype=torch.int64, device="cuda")
+    nuse = torch.zeros(k + 1, dtype=torch.int64, device="cuda")
+    chunk = 1 << 27
+    for lo in range(0, n, chunk):
+        hi = min(n, lo + chunk)
+        d = p.dist[lo:hi].to(torch.int64) & 0xFFFFFFFF
+        b = torch.bucketize(d, edges, right=True)
+        b[d == NONE] = k
+        count += torch.bincount(b, minlength=k + 1)
+        dep = p.depth[lo:hi].to(torch.int64)
+        dsum.scatter_add_(0, b, dep)
+        nx = p.next[lo:hi].to(torch.int64) & 0xFFFFFFFF
+        gap = nx - torch.arange(lo, hi, device="cuda", dtype=torch.int64)
+        nb = torch.bucketize(gap, edges, right=True)
+        nb[nx == NONE] = k
+        nuse += torch.bincount(nb, minlength=k + 1)
+    g = pc.bins_to_host(p.bins)
+    assert g["count"] == count.cpu().tolist()
+    assert g["depthsum"] == dsum.cpu().tolist()
+    assert g["nextuse"] == nuse.cpu().tolist()
+    a, b = 2 * 16 * P_LIN, 2 * 16 * 16
+    assert g["cost"] == [a * c + b * d for c, d in zip(g["count"], g["depthsum"])]
+    assert sum(g["count"]) == n
