@@ -6,14 +6,16 @@
 // as a step S(x, w) = mix64((x ^ w) + gamma), folded over the block's
 // token-pair words from 0 (the digest) and chained block to block.
 //
-// GPU mapping.  The chain is serial inside a request, so one lane owns one
-// request at a time and walks its blocks in order; the wave keeps all 64
-// lanes busy by refilling a lane from a global request counter (one atomic
-// per wave refill) as soon as its request ends, so long and short requests
-// mix without leaving lanes idle.  A lane reads its block's 16 tokens as four
-// 16-byte loads (one 64-byte segment) and writes the 8-byte key (and the
-// depth) to the request's slice of the output.  The step is integer ALU work
-// (two 64x64 multiplies per step, nine steps per 16-token block).
+// GPU mapping, two phases.  (1) Digests are independent per block: one wave
+// takes one request and lane j hashes block j, so a wave reads 4 KiB of
+// tokens in one coalesced sweep and writes 64 digests contiguously.  (2) The
+// chain is serial inside a request: one lane owns one request and walks its
+// digests in place; the digests move between HBM and an LDS tile one request
+// at a time (coalesced 512-byte accesses) and are chained from LDS.  A wave
+// refills lanes from a global request counter as their requests end, so long
+// and short requests mix without idle lanes.  Per 16-token block the
+// work is nine splitmix steps (two 64x64 multiplies each) and 64 bytes of
+// tokens read.
 #include "pc_internal.h"
 
 namespace pc {
@@ -56,22 +58,69 @@ __device__ __forceinline__ uint64_t digest_any(const int32_t *p, uint32_t B) {
 }
 
 constexpr int HASH_THREADS = 256;
-constexpr int HASH_CHUNK = 16;   // blocks a lane hashes between refills
 
-__global__ __launch_bounds__(HASH_THREADS) void hash_blocks_kernel(
+// true when every token and block of request r lies inside the arrays
+__device__ __forceinline__ bool request_in_bounds(uint64_t st, uint32_t len, uint32_t nb, uint64_t out,
+                                                  uint64_t n_tokens, uint64_t n_blocks) {
+    return st <= n_tokens && len <= n_tokens - st && out <= n_blocks && nb <= n_blocks - out;
+}
+
+// Phase 1: digests.  One wave per request, lane = block: a wave reads 64
+// consecutive 64-byte token blocks (4 KiB, fully coalesced) and writes 64
+// consecutive 8-byte digests into the key array.  Requests come from an
+// atomic counter so long and short requests balance across waves.
+__global__ __launch_bounds__(HASH_THREADS) void hash_digest_kernel(
     const int32_t *__restrict__ tokens, uint64_t n_tokens, const uint64_t *__restrict__ tok_start,
+    const uint32_t *__restrict__ tok_len, uint32_t n_seqs, uint32_t B,
+    const uint64_t *__restrict__ blk_off, uint64_t n_blocks, uint64_t *__restrict__ keys,
+    uint32_t *__restrict__ counter, int32_t *__restrict__ err) {
+    const int lane = threadIdx.x & (WAVE - 1);
+    while (true) {
+        uint32_t r = 0;
+        if (lane == 0) r = atomicAdd(counter, 1u);
+        r = __shfl(r, 0, WAVE);
+        if (r >= n_seqs) break;
+        const uint32_t len = tok_len[r];
+        const uint64_t st = tok_start[r];
+        const uint32_t nb = len / B;
+        const uint64_t out = blk_off[r];
+        if (!request_in_bounds(st, len, nb, out, n_tokens, n_blocks)) {
+            if (lane == 0) atomicOr(err, DEV_ERR_BAD_LAYOUT);
+            continue;
+        }
+        const int32_t *tp = tokens + st;
+        const bool fast = (B == 16) && ((reinterpret_cast<uintptr_t>(tp) & 15) == 0);
+        for (uint32_t j = lane; j < nb; j += WAVE) {
+            const int32_t *p = tp + (uint64_t)j * B;
+            keys[out + j] = fast ? digest16(p) : digest_any(p, B);
+        }
+    }
+}
+
+// Phase 2: the chain, serial inside a request.  A wave owns up to 64
+// requests (one per lane) and advances all of them by up to 64 blocks per
+// round.  Memory moves per request, not per lane: for each of its requests
+// the wave loads the next 64 digests with one coalesced 512-byte access into
+// an LDS tile (row = request, padded against bank conflicts), every lane then
+// chains its own row in LDS, and the keys (and depths) go back the same way.
+// Lanes whose request ended take the next one from an atomic counter at the
+// start of the round.
+constexpr int CHAIN_THREADS = 128;                       // two waves per workgroup
+constexpr int CHAIN_WAVES = CHAIN_THREADS / WAVE;
+constexpr int CHAIN_ROW = WAVE + 1;                      // padded row of 64 digests
+
+__global__ __launch_bounds__(CHAIN_THREADS) void hash_chain_kernel(
     const uint32_t *__restrict__ tok_len, uint32_t n_seqs, uint32_t B,
     const uint64_t *__restrict__ parent, uint64_t root, const uint64_t *__restrict__ blk_off,
     uint64_t n_blocks, uint64_t *__restrict__ keys, uint32_t *__restrict__ depth,
-    uint32_t *__restrict__ counter, int32_t *__restrict__ err) {
+    uint32_t *__restrict__ counter) {
+    __shared__ uint64_t s_tile[CHAIN_WAVES][WAVE * CHAIN_ROW];
     const int lane = threadIdx.x & (WAVE - 1);
-    bool done = false;
-    bool busy = false;
+    const int w = threadIdx.x / WAVE;
+    uint64_t *tile = s_tile[w];
+    bool done = false, busy = false;
     uint32_t b = 0, nb = 0;
     uint64_t key = 0, out = 0;
-    const int32_t *tp = nullptr;
-    bool fast = false;
-
     while (true) {
         const bool need = !done && !busy;
         const uint64_t needmask = ballot(need);
@@ -85,36 +134,53 @@ __global__ __launch_bounds__(HASH_THREADS) void hash_blocks_kernel(
                 if (r >= n_seqs) {
                     done = true;
                 } else {
-                    const uint32_t len = tok_len[r];
-                    const uint64_t st = tok_start[r];
-                    nb = len / B;
+                    nb = tok_len[r] / B;
+                    out = blk_off[r];
                     b = 0;
                     key = parent ? parent[r] : root;
-                    tp = tokens + st;
-                    out = blk_off[r];
-                    fast = (B == 16) && ((reinterpret_cast<uintptr_t>(tp) & 15) == 0);
-                    busy = nb > 0;
-                    // never touch memory outside the caller's arrays
-                    if (st > n_tokens || len > n_tokens - st || out > n_blocks ||
-                        nb > n_blocks - out) {
-                        busy = false;
-                        atomicOr(err, DEV_ERR_BAD_LAYOUT);
-                    }
+                    // phase 1 wrote digests only for in-bounds requests
+                    busy = nb > 0 && out <= n_blocks && nb <= n_blocks - out;
                 }
             }
         }
-        if (ballot(!done) == 0) break;
-#pragma unroll 1
-        for (int it = 0; it < HASH_CHUNK; ++it) {
-            if (busy) {
-                const int32_t *p = tp + (uint64_t)b * B;
-                const uint64_t d = fast ? digest16(p) : digest_any(p, B);
-                key = hstep(key, d);
-                keys[out + b] = key;
-                if (depth) depth[out + b] = b;
-                ++b;
-                busy = b < nb;
+        const uint64_t active = ballot(busy);
+        if (active == 0) {
+            if (ballot(!done) == 0) break;
+            continue;
+        }
+        const uint32_t m = busy ? (nb - b < (uint32_t)WAVE ? nb - b : (uint32_t)WAVE) : 0u;
+        const uint64_t pos = out + b;
+        // gather: row i <- the next m_i digests of lane i's request
+        for (uint64_t act = active; act; act &= act - 1) {
+            const int i = __ffsll((unsigned long long)act) - 1;
+            const uint32_t mi = __shfl(m, i, WAVE);
+            const uint64_t pi = __shfl(pos, i, WAVE);
+            if ((uint32_t)lane < mi) tile[i * CHAIN_ROW + lane] = keys[pi + lane];
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (busy) {
+            uint64_t *row = tile + lane * CHAIN_ROW;
+            for (uint32_t j = 0; j < m; ++j) {
+                key = hstep(key, row[j]);
+                row[j] = key;
             }
+        }
+        __builtin_amdgcn_wave_barrier();
+        // scatter back: keys and depths of row i, coalesced
+        for (uint64_t act = active; act; act &= act - 1) {
+            const int i = __ffsll((unsigned long long)act) - 1;
+            const uint32_t mi = __shfl(m, i, WAVE);
+            const uint64_t pi = __shfl(pos, i, WAVE);
+            const uint32_t bi = __shfl(b, i, WAVE);
+            if ((uint32_t)lane < mi) {
+                keys[pi + lane] = tile[i * CHAIN_ROW + lane];
+                if (depth) depth[pi + lane] = bi + lane;
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (busy) {
+            b += m;
+            busy = b < nb;
         }
     }
 }
@@ -125,7 +191,7 @@ extern "C" {
 
 size_t pc_hash_blocks_ws(uint32_t n_seqs) {
     (void)n_seqs;
-    return pc::WS_HEADER + pc::WS_ALIGN;
+    return pc::WS_HEADER + pc::WS_ALIGN;   // header + two work counters
 }
 
 pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_t *tok_start,
@@ -145,21 +211,27 @@ pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_
 
     pc::Carver c{(char *)ws, 0};
     int32_t *hdr = c.take<int32_t>(pc::WS_HEADER / sizeof(int32_t));
-    uint32_t *counter = c.take<uint32_t>(1);
+    uint32_t *counters = c.take<uint32_t>(2);
     pc_status st = pc::fill_u32(reinterpret_cast<uint32_t *>(hdr), 0u, 1, s);
     if (st != PC_OK) return st;
-    st = pc::fill_u32(counter, 0u, 1, s);
+    st = pc::fill_u32(counters, 0u, 2, s);
     if (st != PC_OK) return st;
 
     const int cus = pc::device_cus();
-    // persistent grid: enough waves to fill every SIMD several times over
-    uint64_t want = ((uint64_t)n_seqs + pc::HASH_THREADS - 1) / pc::HASH_THREADS;
+    // persistent grids: a few workgroups per CU, work handed out by counters
+    uint64_t want = ((uint64_t)n_seqs * pc::WAVE + pc::HASH_THREADS - 1) / pc::HASH_THREADS;
     uint64_t cap = (uint64_t)cus * 8;
     unsigned grid = (unsigned)(want < cap ? want : cap);
     if (grid == 0) grid = 1;
-    PC_LAUNCH(pc::K_HASH, pc::hash_blocks_kernel, dim3(grid), dim3(pc::HASH_THREADS), 0, s,
-              tokens, n_tokens, tok_start, tok_len, n_seqs, block_size, parent, root, blk_off,
-              n_blocks, keys, depth, counter, hdr);
+    PC_LAUNCH(pc::K_HASH_DIGEST, pc::hash_digest_kernel, dim3(grid), dim3(pc::HASH_THREADS), 0, s,
+              tokens, n_tokens, tok_start, tok_len, n_seqs, block_size, blk_off, n_blocks, keys,
+              counters, hdr);
+    want = ((uint64_t)n_seqs + pc::CHAIN_THREADS - 1) / pc::CHAIN_THREADS;
+    cap = (uint64_t)cus * 8;
+    grid = (unsigned)(want < cap ? want : cap);
+    if (grid == 0) grid = 1;
+    PC_LAUNCH(pc::K_HASH, pc::hash_chain_kernel, dim3(grid), dim3(pc::CHAIN_THREADS), 0, s, tok_len,
+              n_seqs, block_size, parent, root, blk_off, n_blocks, keys, depth, counters + 1);
     return PC_OK;
 }
 

@@ -39,11 +39,14 @@ constexpr int32_t DEV_ERR_BAD_CAPS = 3;
 // ------------------------------------------------------------ kernel launches
 enum KernelId {
     K_FILL32 = 0,
+    K_HASH_DIGEST,
     K_HASH,
     K_SORT_HIST,
     K_SORT_SCAN,
     K_SORT_PASS,
     K_LINK,
+    K_PERM,
+    K_PERM_LOCAL,
     K_SD_COLD,
     K_SD_SCAN,
     K_SD_TILES,
@@ -105,29 +108,40 @@ __device__ __forceinline__ void st_status64(uint64_t *p, uint64_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// exclusive prefix sum across the 64 lanes of a wave
-__device__ __forceinline__ uint32_t wave_excl_scan(uint32_t v) {
-    const int lane = threadIdx.x & (WAVE - 1);
-    uint32_t x = v;
-#pragma unroll
-    for (int d = 1; d < WAVE; d <<= 1) {
-        uint32_t y = __shfl_up(x, d, WAVE);
-        if (lane >= d) x += y;
-    }
-    return x - v;
+// Inclusive prefix sum across the 64 lanes of a wave with DPP: four row
+// shifts build the sums inside each row of 16 lanes, two row broadcasts carry
+// row totals into the rows above (the gfx9 DPP scan).  Lanes shifted in from
+// outside a row, and rows outside a broadcast's row mask, contribute 0.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false);   // row_shr:1
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false);   // row_shr:2
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false);   // row_shr:4
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false);   // row_shr:8
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);   // row_bcast:15
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);   // row_bcast:31
+    return x;
 }
 
-// exclusive prefix-OR of 64-bit masks across the 64 lanes of a wave
-__device__ __forceinline__ uint64_t wave_excl_or(uint64_t v) {
-    const int lane = threadIdx.x & (WAVE - 1);
-    uint64_t x = v;
+// exclusive prefix sum across the 64 lanes of a wave
+__device__ __forceinline__ uint32_t wave_excl_scan(uint32_t v) { return wave_incl_scan(v) - v; }
+
+// Lanes whose `bits`-bit digit equals q (eq) and is smaller than q (lt), for
+// q = this lane's own index, from the per-bit ballots B[0..bits) of the
+// digits (bit b of every valid lane's digit) and the valid-lane mask vm.
+// Walks the bits from the top: a lane is smaller than q at the first bit
+// where it has 0 and q has 1, all higher bits being equal.
+template <int BITS>
+__device__ __forceinline__ void digit_masks(const uint64_t *B, uint64_t vm, uint32_t q, uint64_t &eq,
+                                            uint64_t &lt) {
+    uint64_t e = vm, l = 0;
 #pragma unroll
-    for (int d = 1; d < WAVE; d <<= 1) {
-        uint64_t y = __shfl_up(x, d, WAVE);
-        if (lane >= d) x |= y;
+    for (int b = BITS - 1; b >= 0; --b) {
+        const bool bit = (q >> b) & 1;
+        if (bit) l |= e & ~B[b];
+        e &= bit ? B[b] : ~B[b];
     }
-    uint64_t e = __shfl_up(x, 1, WAVE);
-    return lane ? e : 0ull;
+    eq = e;
+    lt = l;
 }
 
 // Block-wide exclusive scan of one value per thread (blockDim.x <= 1024).

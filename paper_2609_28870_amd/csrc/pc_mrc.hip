@@ -7,10 +7,12 @@
 // cost(t) = alpha + beta * depth[t].  Because LRU hits at capacity c exactly
 // when D < c, binning D on the capacity edges gives every capacity at once.
 //
-// GPU mapping: a grid-stride stream over dist / depth / next; each workgroup
-// keeps private LDS bins (count, depth sum, next-use gap count) filled with
-// LDS atomics after an upper-bound search of the edges held in LDS, then adds
-// its non-zero bins to the outputs with global 64-bit atomics.  Integer
+// GPU mapping: each thread takes 16 consecutive accesses (64-byte vector
+// loads of dist / depth / next), finds each one's bin by an upper-bound
+// search of the edges held in LDS (trying the previous access's bin first)
+// and accumulates runs of equal bins in registers, so one LDS atomic covers a
+// run; each workgroup then adds its non-zero LDS bins to the outputs with
+// global 64-bit atomics.  Integer
 // atomics make the result independent of scheduling order.  A last tiny
 // kernel forms alpha*count + beta*depthsum exactly as 128-bit integers.
 #include "pc_internal.h"
@@ -27,6 +29,15 @@ __device__ __forceinline__ uint32_t upper_bound(const uint64_t *e, uint32_t m, u
         if (e[mid] <= x) lo = mid + 1; else hi = mid;
     }
     return lo;
+}
+
+constexpr int MRC_PER = 16;   // consecutive accesses per thread
+
+// bin of x: number of edges <= x, trying the previous bin first (neighbouring
+// accesses of one request usually share it)
+__device__ __forceinline__ uint32_t bin_of(const uint64_t *e, uint32_t K, uint64_t x, uint32_t hint) {
+    if (hint <= K && (hint == 0 || e[hint - 1] <= x) && (hint == K || x < e[hint])) return hint;
+    return upper_bound(e, K, x);
 }
 
 __global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
@@ -49,20 +60,75 @@ __global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
         s_nh[i] = 0;
     }
     __syncthreads();
+    const uint64_t chunks = (n + MRC_PER - 1) / MRC_PER;
+    // vector loads only when every base pointer is 16-byte aligned
+    const bool vec = ((reinterpret_cast<uintptr_t>(dist) | reinterpret_cast<uintptr_t>(depth) |
+                       reinterpret_cast<uintptr_t>(next)) & 15) == 0;
     const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-    for (uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n; t += stride) {
-        const uint32_t d = dist[t];
-        const uint32_t bin = d == NONE ? K : upper_bound(s_caps, K, d);
-        atomicAdd(&s_cnt[bin], 1u);
-        if (depth) {
-            const uint32_t dep = depth[t];
-            if (dep) atomicAdd(reinterpret_cast<unsigned long long *>(&s_ds[bin]), (unsigned long long)dep);
+    for (uint64_t ch = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; ch < chunks; ch += stride) {
+        const uint64_t t0 = ch * MRC_PER;
+        const bool full = t0 + MRC_PER <= n;
+        uint32_t dv[MRC_PER], pv[MRC_PER], nv[MRC_PER];
+        if (full && vec) {
+#pragma unroll
+            for (int q = 0; q < MRC_PER / 4; ++q) {
+                const uint4 a = reinterpret_cast<const uint4 *>(dist + t0)[q];
+                dv[4 * q] = a.x; dv[4 * q + 1] = a.y; dv[4 * q + 2] = a.z; dv[4 * q + 3] = a.w;
+                if (depth) {
+                    const uint4 b = reinterpret_cast<const uint4 *>(depth + t0)[q];
+                    pv[4 * q] = b.x; pv[4 * q + 1] = b.y; pv[4 * q + 2] = b.z; pv[4 * q + 3] = b.w;
+                }
+                if (next) {
+                    const uint4 c = reinterpret_cast<const uint4 *>(next + t0)[q];
+                    nv[4 * q] = c.x; nv[4 * q + 1] = c.y; nv[4 * q + 2] = c.z; nv[4 * q + 3] = c.w;
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < MRC_PER; ++j) {
+                const bool in = t0 + j < n;
+                dv[j] = in ? dist[t0 + j] : 0u;
+                pv[j] = (in && depth) ? depth[t0 + j] : 0u;
+                nv[j] = (in && next) ? next[t0 + j] : 0u;
+            }
         }
-        if (next) {
-            const uint32_t q = next[t];
-            const uint32_t nb = q == NONE ? K : upper_bound(s_caps, K, (uint64_t)q - t);
-            atomicAdd(&s_nh[nb], 1u);
+        if (!depth) {
+#pragma unroll
+            for (int j = 0; j < MRC_PER; ++j) pv[j] = 0;
         }
+        const int m = full ? MRC_PER : (int)(n - t0);
+        uint32_t cur = K + 1, cnt = 0, ncur = K + 1, ncnt = 0;
+        uint64_t ds = 0;
+        for (int j = 0; j < m; ++j) {
+            const uint32_t d = dv[j];
+            const uint32_t bin = d == NONE ? K : bin_of(s_caps, K, d, cur);
+            if (bin != cur) {
+                if (cnt) {
+                    atomicAdd(&s_cnt[cur], cnt);
+                    if (ds) atomicAdd(reinterpret_cast<unsigned long long *>(&s_ds[cur]), (unsigned long long)ds);
+                }
+                cur = bin;
+                cnt = 0;
+                ds = 0;
+            }
+            ++cnt;
+            ds += pv[j];
+            if (next) {
+                const uint32_t q = nv[j];
+                const uint32_t nb = q == NONE ? K : bin_of(s_caps, K, (uint64_t)q - (t0 + j), ncur);
+                if (nb != ncur) {
+                    if (ncnt) atomicAdd(&s_nh[ncur], ncnt);
+                    ncur = nb;
+                    ncnt = 0;
+                }
+                ++ncnt;
+            }
+        }
+        if (cnt) {
+            atomicAdd(&s_cnt[cur], cnt);
+            if (ds) atomicAdd(reinterpret_cast<unsigned long long *>(&s_ds[cur]), (unsigned long long)ds);
+        }
+        if (ncnt) atomicAdd(&s_nh[ncur], ncnt);
     }
     __syncthreads();
     for (uint32_t i = threadIdx.x; i <= K; i += blockDim.x) {
@@ -120,7 +186,7 @@ pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uin
         return st;
 
     const int cus = pc::device_cus();
-    uint64_t grid = (n + pc::MRC_THREADS * 16 - 1) / (pc::MRC_THREADS * 16);
+    uint64_t grid = (n + pc::MRC_THREADS * pc::MRC_PER - 1) / (pc::MRC_THREADS * pc::MRC_PER);
     if (grid > (uint64_t)cus * 8) grid = (uint64_t)cus * 8;
     if (grid == 0) grid = 1;
     const size_t shmem = (size_t)n_caps * 8 + (size_t)bins * 8 + (size_t)bins * 8;

@@ -16,7 +16,8 @@
 //     per-digit counts and reads its predecessors' with a decoupled
 //     look-back, then writes the tile out through LDS so each digit run is a
 //     contiguous burst;
-//   * the link kernel reads sorted neighbours and scatters prev/next.
+//   * the link + partition kernels read sorted neighbours into (t, prev,
+//     next) triples and move them back to time order (see below).
 // Waits in the look-back are bounded: after the spin limit the kernel
 // records an error in the workspace header instead of hanging.
 #include "pc_internal.h"
@@ -176,20 +177,154 @@ __global__ __launch_bounds__(SORT_THREADS) void sort_pass_kernel(
     }
 }
 
-// equal neighbours in (key, t) order are consecutive uses of one key
-__global__ __launch_bounds__(256) void link_kernel(const uint64_t *__restrict__ sk,
-                                                   const uint32_t *__restrict__ sv, uint64_t n,
-                                                   uint32_t *__restrict__ prev,
-                                                   uint32_t *__restrict__ next) {
-    const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    const uint64_t k = sk[i];
-    const uint32_t t = sv[i];
-    const uint32_t p = (i > 0 && sk[i - 1] == k) ? sv[i - 1] : NONE;
-    const uint32_t q = (i + 1 < n && sk[i + 1] == k) ? sv[i + 1] : NONE;
-    if (t < n) {   // always true for a complete sort; guards the scatter anyway
-        prev[t] = p;
-        next[t] = q;
+// ---- links, and the way back to time order -------------------------------
+// Equal neighbours in (key, t) order are consecutive uses of one key, giving
+// the triple (t, prev(t), next(t)).  t is a permutation of [0, n), so the
+// triples with t in [a, b) fill exactly positions [a, b) once they are
+// partitioned by the top bits of t; the order inside a range does not matter
+// because the last step places every triple at its own t.  Each partition
+// pass therefore reserves its output runs with one global atomic per
+// (workgroup, digit) instead of a look-back, stages each tile digit-sorted
+// in LDS and writes each run contiguously.
+constexpr int PERM_THREADS = 512;
+constexpr int PERM_ITEMS = 8;
+constexpr int PERM_TILE = PERM_THREADS * PERM_ITEMS;   // 4096
+constexpr int PERM_RADIX = 1024;
+constexpr int PERM_LOCAL_BITS = 12;
+
+// One workgroup owns a contiguous chunk of the input.  It first counts the
+// chunk's digits, reserves one run per digit in the bucket's output range with
+// a single global atomic (so each bucket cursor sees one atomic per workgroup,
+// not per tile), then streams the chunk tile by tile: LDS counters give each
+// element its slot inside its digit, the tile is staged digit-sorted in LDS,
+// and each digit's part is appended to the workgroup's run.  A chunk spans at
+// most 1024 consecutive buckets (see the plan), so digit = bucket mod 1024
+// names them without collision.
+template <bool FROM_SORT>
+__global__ __launch_bounds__(PERM_THREADS) void perm_partition_kernel(
+    const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t,
+    const uint32_t *__restrict__ in_p, const uint32_t *__restrict__ in_n, uint64_t n, int s,
+    uint64_t per_wg, uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t,
+    uint32_t *__restrict__ out_p, uint32_t *__restrict__ out_n) {
+    __shared__ uint32_t s_t[PERM_TILE], s_p[PERM_TILE], s_n[PERM_TILE];
+    __shared__ uint32_t s_cnt[PERM_RADIX];
+    __shared__ uint32_t s_lstart[PERM_RADIX];
+    __shared__ uint32_t s_cur[PERM_RADIX];
+    __shared__ uint32_t s_bucket[PERM_RADIX];
+    __shared__ uint32_t s_tmp[PERM_THREADS / WAVE];
+    constexpr int DPT = PERM_RADIX / PERM_THREADS;   // digits per thread
+    const int tid = threadIdx.x;
+    const uint64_t lo = (uint64_t)blockIdx.x * per_wg;
+    if (lo >= n) return;
+    const uint64_t hi = lo + per_wg < n ? lo + per_wg : n;
+
+    // ---- count the chunk's digits and reserve one run per digit
+    for (int i = tid; i < PERM_RADIX; i += PERM_THREADS) s_cnt[i] = 0;
+    __syncthreads();
+    for (uint64_t i = lo + tid; i < hi; i += PERM_THREADS) {
+        const uint32_t tt = in_t[i];
+        const uint32_t d = (tt >> s) & (PERM_RADIX - 1);
+        atomicAdd(&s_cnt[d], 1u);
+        s_bucket[d] = tt >> s;   // every writer of digit d writes the same bucket
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < DPT; ++q) {
+        const int d = tid * DPT + q;
+        const uint32_t c = s_cnt[d];
+        if (c) s_cur[d] = atomicAdd(&cursor[s_bucket[d]], c);
+    }
+    __syncthreads();
+
+    // ---- stream the chunk tile by tile
+    for (uint64_t base = lo; base < hi; base += PERM_TILE) {
+        for (int i = tid; i < PERM_RADIX; i += PERM_THREADS) s_cnt[i] = 0;
+        __syncthreads();
+        uint32_t t[PERM_ITEMS], pv[PERM_ITEMS], nx[PERM_ITEMS], off[PERM_ITEMS];
+        bool ok[PERM_ITEMS];
+#pragma unroll
+        for (int j = 0; j < PERM_ITEMS; ++j) {
+            const uint64_t i = base + (uint64_t)j * PERM_THREADS + tid;
+            ok[j] = i < hi;
+            if (!ok[j]) continue;
+            t[j] = in_t[i];
+            if (FROM_SORT) {
+                const uint64_t k = sk[i];
+                pv[j] = (i > 0 && sk[i - 1] == k) ? in_t[i - 1] : NONE;
+                nx[j] = (i + 1 < n && sk[i + 1] == k) ? in_t[i + 1] : NONE;
+            } else {
+                pv[j] = in_p[i];
+                nx[j] = in_n[i];
+            }
+            off[j] = atomicAdd(&s_cnt[(t[j] >> s) & (PERM_RADIX - 1)], 1u);
+        }
+        __syncthreads();
+        uint32_t c[DPT], mine = 0, total;
+#pragma unroll
+        for (int q = 0; q < DPT; ++q) {
+            c[q] = s_cnt[tid * DPT + q];
+            mine += c[q];
+        }
+        uint32_t run = block_excl_scan(mine, s_tmp, &total);
+#pragma unroll
+        for (int q = 0; q < DPT; ++q) {
+            s_lstart[tid * DPT + q] = run;
+            run += c[q];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < PERM_ITEMS; ++j) {
+            if (!ok[j]) continue;
+            const uint32_t pos = s_lstart[(t[j] >> s) & (PERM_RADIX - 1)] + off[j];
+            s_t[pos] = t[j];
+            s_p[pos] = pv[j];
+            s_n[pos] = nx[j];
+        }
+        __syncthreads();
+        for (uint32_t j = tid; j < total; j += PERM_THREADS) {
+            const uint32_t tt = s_t[j];
+            const uint32_t d = (tt >> s) & (PERM_RADIX - 1);
+            const uint32_t dst = s_cur[d] + (j - s_lstart[d]);
+            if (dst < n) {
+                out_t[dst] = tt;
+                out_p[dst] = s_p[j];
+                out_n[dst] = s_n[j];
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < DPT; ++q) s_cur[tid * DPT + q] += c[q];
+        __syncthreads();
+    }
+}
+
+// cursor[b] = b << s: each bucket's output run starts at its first t
+__global__ void perm_cursor_kernel(uint32_t *__restrict__ cursor, uint64_t nb, int s) {
+    const uint64_t b = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (b < nb) cursor[b] = (uint32_t)(b << s);
+}
+
+// every 4096-range of t holds exactly its own triples: place them by t in
+// LDS and write prev / next in time order
+__global__ __launch_bounds__(256) void perm_local_kernel(const uint32_t *__restrict__ in_t,
+                                                         const uint32_t *__restrict__ in_p,
+                                                         const uint32_t *__restrict__ in_n, uint64_t n,
+                                                         uint32_t *__restrict__ prev,
+                                                         uint32_t *__restrict__ next) {
+    constexpr uint32_t SPAN = 1u << PERM_LOCAL_BITS;
+    __shared__ uint32_t s_p[SPAN], s_n[SPAN];
+    const uint64_t r0 = (uint64_t)blockIdx.x * SPAN;
+    const uint32_t cnt = n - r0 < SPAN ? (uint32_t)(n - r0) : SPAN;
+    for (uint32_t j = threadIdx.x; j < cnt; j += blockDim.x) {
+        const uint32_t tt = in_t[r0 + j];
+        const uint32_t slot = (uint32_t)(tt - r0) & (SPAN - 1);
+        s_p[slot] = in_p[r0 + j];
+        s_n[slot] = in_n[r0 + j];
+    }
+    __syncthreads();
+    for (uint32_t j = threadIdx.x; j < cnt; j += blockDim.x) {
+        prev[r0 + j] = s_p[j];
+        next[r0 + j] = s_n[j];
     }
 }
 
@@ -199,8 +334,49 @@ struct SortWs {
     uint64_t *k1, *k2;
     uint32_t *v1, *v2;
     uint64_t *status;
+    uint32_t *cursor;
     size_t bytes;
 };
+
+// Partition plan for the way back to time order.  The last pass uses
+// 4096-ranges of t.  The first pass has at most 1024 buckets; every later pass
+// splits a bucket into at most 512, so a workgroup chunk (at most 2^20
+// elements, smaller than any earlier bucket of >= 2^21) spans at most two
+// earlier buckets, i.e. at most 1024 consecutive buckets of its own pass, and
+// (bucket mod 1024) names them without collision inside the chunk.
+struct PermPlan {
+    int passes;
+    int s[4];
+    uint64_t buckets[4];
+    uint64_t max_buckets;
+};
+
+static PermPlan plan_perm(uint64_t n) {
+    PermPlan p{};
+    int nbits = 0;
+    while (nbits < 64 && (1ull << nbits) < n) ++nbits;
+    int hi = nbits;   // bits above PERM_LOCAL_BITS still to split
+    int cur = nbits;
+    int shifts[4], k = 0;
+    // first pass: up to 10 bits; later passes: up to 9 bits
+    int width = 10;
+    while (cur > PERM_LOCAL_BITS && k < 4) {
+        int next_s = cur - width > PERM_LOCAL_BITS ? cur - width : PERM_LOCAL_BITS;
+        shifts[k++] = next_s;
+        cur = next_s;
+        width = 9;
+    }
+    (void)hi;
+    if (k == 0) shifts[k++] = PERM_LOCAL_BITS;
+    p.passes = k;
+    p.max_buckets = 1;
+    for (int i = 0; i < k; ++i) {
+        p.s[i] = shifts[i];
+        p.buckets[i] = (n + (1ull << shifts[i]) - 1) >> shifts[i];
+        if (p.buckets[i] > p.max_buckets) p.max_buckets = p.buckets[i];
+    }
+    return p;
+}
 
 static SortWs carve_sort(void *ws, uint64_t n) {
     Carver c{(char *)ws, 0};
@@ -215,6 +391,7 @@ static SortWs carve_sort(void *ws, uint64_t n) {
     w.v1 = c.take<uint32_t>(n);
     w.v2 = c.take<uint32_t>(n);
     w.status = c.take<uint64_t>(tiles * RADIX);
+    w.cursor = c.take<uint32_t>(plan_perm(n).max_buckets + 1);
     w.bytes = c.off;
     return w;
 }
@@ -259,8 +436,42 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
         kin = kout;
         vin = vout;
     }
-    const uint64_t lg = (n + 255) / 256;
-    PC_LAUNCH(pc::K_LINK, pc::link_kernel, dim3((unsigned)lg), dim3(256), 0, s, kin, vin, n, prev, next);
+    // links + partition back to time order.  The sort left (key, t) in
+    // (k2, v2); triples (t, prev, next) ping-pong between the first sort
+    // buffers (k1 viewed as two u32 arrays, v1) and, once the sorted keys
+    // have been consumed, the second ones (k2 as two u32 arrays, v2).
+    const pc::PermPlan pp = pc::plan_perm(n);
+    uint32_t *bt[2] = {reinterpret_cast<uint32_t *>(w.k1), reinterpret_cast<uint32_t *>(w.k2)};
+    uint32_t *bp[2] = {bt[0] + n, bt[1] + n};
+    uint32_t *bn[2] = {w.v1, w.v2};
+    // chunks of at most 2^20 elements: small enough that a chunk of a later
+    // pass spans at most two buckets of the previous one, large enough that
+    // each bucket cursor sees few atomics
+    uint64_t per_wg = (n + (uint64_t)cus * 2 - 1) / ((uint64_t)cus * 2);
+    per_wg = (per_wg + pc::PERM_TILE - 1) / pc::PERM_TILE * pc::PERM_TILE;
+    if (per_wg > (1ull << 20)) per_wg = 1ull << 20;
+    if (per_wg < (uint64_t)pc::PERM_TILE) per_wg = pc::PERM_TILE;
+    const unsigned ptiles = (unsigned)((n + per_wg - 1) / per_wg);
+    int cur = 0;
+    for (int i = 0; i < pp.passes; ++i) {
+        const unsigned cg = (unsigned)((pp.buckets[i] + 255) / 256);
+        PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg), dim3(256), 0, s, w.cursor, pp.buckets[i],
+                  pp.s[i]);
+        if (i == 0) {
+            PC_LAUNCH(pc::K_LINK, pc::perm_partition_kernel<true>, dim3(ptiles), dim3(pc::PERM_THREADS), 0, s,
+                      kin, vin, (const uint32_t *)nullptr, (const uint32_t *)nullptr, n, pp.s[i], per_wg,
+                      w.cursor, bt[0], bp[0], bn[0]);
+            cur = 0;
+        } else {
+            const int nxt = cur ^ 1;
+            PC_LAUNCH(pc::K_PERM, pc::perm_partition_kernel<false>, dim3(ptiles), dim3(pc::PERM_THREADS), 0,
+                      s, (const uint64_t *)nullptr, bt[cur], bp[cur], bn[cur], n, pp.s[i], per_wg,
+                      w.cursor, bt[nxt], bp[nxt], bn[nxt]);
+            cur = nxt;
+        }
+    }
+    PC_LAUNCH(pc::K_PERM_LOCAL, pc::perm_local_kernel, dim3((unsigned)((n + 4095) / 4096)), dim3(256), 0, s,
+              bt[cur], bp[cur], bn[cur], n, prev, next);
     return PC_OK;
 }
 

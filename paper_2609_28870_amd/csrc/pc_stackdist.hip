@@ -191,21 +191,11 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
 #pragma unroll
         for (int b = 0; b < 8; ++b) B[b] = ballot(ok[i] && ((d >> b) & 1));
         // lanes 0..15 build the nibble tables: lanes whose high / low nibble
-        // equals q, and the union over smaller q
-        uint64_t mh = 0, ml = 0;
+        // equals q, and lanes whose nibble is smaller than q
         if (lane < 16) {
-            mh = vm;
-            ml = vm;
-#pragma unroll
-            for (int b = 0; b < 4; ++b) {
-                const bool bit = (lane >> b) & 1;
-                mh &= bit ? B[4 + b] : ~B[4 + b];
-                ml &= bit ? B[b] : ~B[b];
-            }
-        }
-        const uint64_t lh = wave_excl_or(mh);
-        const uint64_t ll = wave_excl_or(ml);
-        if (lane < 16) {
+            uint64_t mh, lh, ml, ll;
+            digit_masks<4>(B + 4, vm, (uint32_t)lane, mh, lh);
+            digit_masks<4>(B, vm, (uint32_t)lane, ml, ll);
             s_mt[w][0][lane] = mh;
             s_mt[w][1][lane] = ml;
             s_mt[w][2][lane] = lh;
@@ -229,14 +219,18 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     }
     __syncthreads();
 
-    // ---- column prefix over chunks (thread = digit) and tile totals
+    // ---- column prefix over chunks (thread = digit) and tile totals; all
+    // loads are issued before any store so they pipeline
     uint32_t tot = 0;
     {
         const int d = tid;
+        uint16_t h[DOM_CHUNKS];
+#pragma unroll
+        for (int c = 0; c < DOM_CHUNKS; ++c) h[c] = s_h[c][d];
+#pragma unroll
         for (int c = 0; c < DOM_CHUNKS; ++c) {
-            const uint32_t h = s_h[c][d];
             s_h[c][d] = (uint16_t)tot;
-            tot += h;
+            tot += h[c];
         }
     }
     __syncthreads();
@@ -328,6 +322,7 @@ __global__ __launch_bounds__(LOC_THREADS) void sd_local_kernel(
     __shared__ uint32_t s_work[LOCAL_SPAN];   // [64][64] u16 tables, then the slot array
     __shared__ uint32_t s_tot[64];
     __shared__ uint32_t s_lstart[64];
+    __shared__ uint32_t s_part[4][64];
     __shared__ uint32_t s_tmp[LOC_WAVES];
     uint16_t(*s_h)[64] = reinterpret_cast<uint16_t(*)[64]>(&s_work[0]);
     uint16_t(*s_pl)[64] = reinterpret_cast<uint16_t(*)[64]>(&s_work[LOCAL_SPAN / 2]);
@@ -356,13 +351,11 @@ __global__ __launch_bounds__(LOC_THREADS) void sd_local_kernel(
         const int c = w * LOC_CPW + i;
         const uint32_t d = (t[i] >> 6) & 63;
         const uint64_t vm = ballot(ok[i]);
-        uint64_t m = vm;
+        uint64_t B[6];
 #pragma unroll
-        for (int b = 0; b < 6; ++b) {
-            const uint64_t B = ballot(ok[i] && ((d >> b) & 1));
-            m &= ((lane >> b) & 1) ? B : ~B;   // lanes whose digit equals this lane's index
-        }
-        const uint64_t lmask = wave_excl_or(m);
+        for (int b = 0; b < 6; ++b) B[b] = ballot(ok[i] && ((d >> b) & 1));
+        uint64_t m, lmask;   // lanes whose digit equals / is below this lane's index
+        digit_masks<6>(B, vm, (uint32_t)lane, m, lmask);
         s_h[c][lane] = (uint16_t)__popcll(m);
         const uint64_t eq = __shfl(m, (int)d, WAVE);
         const uint64_t lt = __shfl(lmask, (int)d, WAVE);
@@ -370,15 +363,35 @@ __global__ __launch_bounds__(LOC_THREADS) void sd_local_kernel(
         la[i] = ok[i] ? (uint8_t)mbcnt(lt) : 0;
     }
     __syncthreads();
-    if (tid < 64) {
-        uint32_t run = 0;
-        for (int c = 0; c < LOC_CHUNKS; ++c) {
-            const uint32_t h = s_h[c][tid];
-            s_h[c][tid] = (uint16_t)run;
-            run += h;
+    // column prefix: thread (digit d, quarter q) scans 16 chunks, then the
+    // four quarter sums are combined
+    {
+        const int d = tid & 63, q = tid >> 6;
+        uint16_t h[LOC_CHUNKS / 4];
+        uint32_t sum = 0;
+#pragma unroll
+        for (int c = 0; c < LOC_CHUNKS / 4; ++c) {
+            h[c] = s_h[q * (LOC_CHUNKS / 4) + c][d];
+            sum += h[c];
         }
-        s_tot[tid] = run;
-        s_lstart[tid] = wave_excl_scan(run);
+        s_part[q][d] = sum;
+        __syncthreads();
+        uint32_t run = 0, tot = 0;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+            const uint32_t v = s_part[x][d];
+            if (x < q) run += v;
+            tot += v;
+        }
+#pragma unroll
+        for (int c = 0; c < LOC_CHUNKS / 4; ++c) {
+            s_h[q * (LOC_CHUNKS / 4) + c][d] = (uint16_t)run;
+            run += h[c];
+        }
+        if (q == 0) {
+            s_tot[d] = tot;
+            s_lstart[d] = wave_excl_scan(tot);
+        }
     }
     __syncthreads();
     for (int c = w * LOC_CPW; c < (w + 1) * LOC_CPW; ++c) {
@@ -406,13 +419,11 @@ __global__ __launch_bounds__(LOC_THREADS) void sd_local_kernel(
         const uint32_t ab = okb ? s_sa[base + lane] : 0u;
         const uint32_t d = tb & 63;
         const uint64_t vm = ballot(okb);
-        uint64_t m = vm;
+        uint64_t B[6];
 #pragma unroll
-        for (int b = 0; b < 6; ++b) {
-            const uint64_t B = ballot(okb && ((d >> b) & 1));
-            m &= ((lane >> b) & 1) ? B : ~B;
-        }
-        const uint64_t lmask = wave_excl_or(m);
+        for (int b = 0; b < 6; ++b) B[b] = ballot(okb && ((d >> b) & 1));
+        uint64_t m, lmask;
+        digit_masks<6>(B, vm, (uint32_t)lane, m, lmask);
         const uint64_t lt = __shfl(lmask, (int)d, WAVE);
         // slot[] aliases the level-A tables, which are dead after the barrier
         if (okb) slot[tb & (LOCAL_SPAN - 1)] = ab + mbcnt(lt);
