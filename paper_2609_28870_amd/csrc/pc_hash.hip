@@ -98,16 +98,17 @@ __global__ __launch_bounds__(HASH_THREADS) void hash_digest_kernel(
 }
 
 // Phase 2: the chain, serial inside a request.  A wave owns up to 64
-// requests (one per lane) and advances all of them by up to 64 blocks per
+// requests (one per lane) and advances all of them by up to 32 blocks per
 // round.  Memory moves per request, not per lane: for each of its requests
-// the wave loads the next 64 digests with one coalesced 512-byte access into
+// the wave loads the next 32 digests with one coalesced 256-byte access into
 // an LDS tile (row = request, padded against bank conflicts), every lane then
 // chains its own row in LDS, and the keys (and depths) go back the same way.
 // Lanes whose request ended take the next one from an atomic counter at the
 // start of the round.
 constexpr int CHAIN_THREADS = 128;                       // two waves per workgroup
 constexpr int CHAIN_WAVES = CHAIN_THREADS / WAVE;
-constexpr int CHAIN_ROW = WAVE + 1;                      // padded row of 64 digests
+constexpr int CHAIN_SPAN = 32;                           // blocks per request per round
+constexpr int CHAIN_ROW = CHAIN_SPAN + 1;                // padded LDS row
 
 __global__ __launch_bounds__(CHAIN_THREADS) void hash_chain_kernel(
     const uint32_t *__restrict__ tok_len, uint32_t n_seqs, uint32_t B,
@@ -148,7 +149,7 @@ __global__ __launch_bounds__(CHAIN_THREADS) void hash_chain_kernel(
             if (ballot(!done) == 0) break;
             continue;
         }
-        const uint32_t m = busy ? (nb - b < (uint32_t)WAVE ? nb - b : (uint32_t)WAVE) : 0u;
+        const uint32_t m = busy ? (nb - b < (uint32_t)CHAIN_SPAN ? nb - b : (uint32_t)CHAIN_SPAN) : 0u;
         const uint64_t pos = out + b;
         // gather: row i <- the next m_i digests of lane i's request
         for (uint64_t act = active; act; act &= act - 1) {

@@ -44,12 +44,15 @@ enum KernelId {
     K_SORT_HIST,
     K_SORT_SCAN,
     K_SORT_PASS,
+    K_SORT_CHECK,
     K_LINK,
     K_PERM,
     K_PERM_LOCAL,
     K_SD_COLD,
     K_SD_SCAN,
     K_SD_TILES,
+    K_SD_COUNT,
+    K_SD_SEG,
     K_SD_PASS,
     K_SD_LOCAL,
     K_MRC_HIST,

@@ -7,6 +7,11 @@
 //
 // GPU mapping: a stable LSD radix sort of (key, t) groups equal keys with t
 // ascending; neighbours in sorted order are exactly the (prev, next) links.
+// Keys are 64-bit hashes, so sorting by their low 32 bits already makes
+// equal keys contiguous except where different keys share those bits; the
+// link step resolves such short "mixed" runs by scanning them, and a device
+// check switches on the four passes over the high bits when a mixed run could
+// be long (then the full 64-bit sort makes equal keys adjacent).
 //   * one pass computes all eight 8-bit digit histograms (LDS-privatised,
 //     then global atomics), one workgroup scans them into digit bases;
 //   * each of the eight sort passes is a single "onesweep" kernel: a
@@ -67,7 +72,9 @@ __global__ __launch_bounds__(SORT_THREADS) void sort_pass_kernel(
     const uint64_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
     uint64_t *__restrict__ keys_out, uint32_t *__restrict__ vals_out, uint64_t n, int shift,
     const uint32_t *__restrict__ start, uint64_t *__restrict__ status, uint32_t *__restrict__ counter,
-    uint32_t epoch, int32_t *__restrict__ err) {
+    uint32_t epoch, int32_t *__restrict__ err, const int32_t *__restrict__ only_if) {
+    // passes over the high key bits run only when the link step needs them
+    if (only_if && *only_if == 0) return;
     __shared__ uint64_t s_key[SORT_TILE];
     __shared__ uint32_t s_val[SORT_TILE];
     __shared__ uint32_t s_wcnt[SORT_WAVES][RADIX];
@@ -192,6 +199,111 @@ constexpr int PERM_TILE = PERM_THREADS * PERM_ITEMS;   // 4096
 constexpr int PERM_RADIX = 1024;
 constexpr int PERM_LOCAL_BITS = 12;
 
+// After the four passes over the low 32 key bits, equal keys are contiguous
+// unless different keys share those bits ("mixed" runs, a few percent of the
+// accesses for 64-bit hashes).  The link step resolves them by scanning the
+// run: an element inside a block of equal keys finds its neighbour in one
+// step, while a block boundary scans back (or forward) to the previous (next)
+// block of its key or the run's end.  This check bounds the total of those
+// boundary scans from above (short runs are charged their probe length,
+// long ones are scanned); when the total exceeds a budget (adversarial keys:
+// many keys sharing low bits) it switches on the four passes over the high
+// bits, after which equal keys are adjacent and every scan is one step.
+__device__ __forceinline__ bool same_low(uint64_t a, uint64_t b) { return (uint32_t)a == (uint32_t)b; }
+
+// Scan from position `from` (inclusive) in direction dir (-1 / +1) over
+// elements sharing k's low bits; stop at k (found), at the run's end, or
+// after `limit` steps.  Keys are read 8 at a time so a long scan costs one
+// memory latency per 8 elements.  Returns the number of elements examined;
+// *hit = position of k or UINT64_MAX.
+constexpr int SCAN_BATCH = 8;
+__device__ __forceinline__ uint64_t scan_run(const uint64_t *__restrict__ sk, uint64_t n, uint64_t k,
+                                             uint64_t from, int dir, uint64_t limit, uint64_t *hit) {
+    uint64_t steps = 0;
+    *hit = ~0ull;
+    int64_t j = (int64_t)from;
+    while (steps < limit) {
+        uint64_t kb[SCAN_BATCH];
+#pragma unroll
+        for (int q = 0; q < SCAN_BATCH; ++q) {
+            const int64_t x = j + dir * q;
+            kb[q] = (x >= 0 && (uint64_t)x < n) ? sk[x] : ~k;   // ~k: differs from k in the low bits
+        }
+#pragma unroll
+        for (int q = 0; q < SCAN_BATCH; ++q) {
+            ++steps;
+            if (kb[q] == k) {
+                *hit = (uint64_t)(j + dir * q);
+                return steps;
+            }
+            if (!same_low(kb[q], k)) return steps;
+        }
+        j += dir * SCAN_BATCH;
+    }
+    return steps;
+}
+
+__global__ __launch_bounds__(256) void sort_mix_check_kernel(const uint64_t *__restrict__ sk, uint64_t n,
+                                                             uint64_t budget,
+                                                             unsigned long long *__restrict__ work,
+                                                             int32_t *__restrict__ need_high) {
+    __shared__ uint32_t s_tmp[256 / WAVE];
+    // When the run ends within PROBE positions (one probe load), charge PROBE
+    // without scanning: the total stays an upper bound.
+    constexpr uint64_t PROBE = 32;
+    uint64_t cost = 0;
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n && cost <= budget; i += stride) {
+        const uint64_t k = sk[i];
+        uint64_t hit;
+        if (i > 0) {
+            const uint64_t kp = sk[i - 1];
+            if (same_low(kp, k) && kp != k) {
+                if (i < PROBE || !same_low(sk[i - PROBE], k)) cost += PROBE;
+                else cost += scan_run(sk, n, k, i - 1, -1, budget + 1, &hit);
+            }
+        }
+        if (i + 1 < n) {
+            const uint64_t kn = sk[i + 1];
+            if (same_low(kn, k) && kn != k) {
+                if (i + PROBE >= n || !same_low(sk[i + PROBE], k)) cost += PROBE;
+                else cost += scan_run(sk, n, k, i + 1, +1, budget + 1, &hit);
+            }
+        }
+    }
+    // one atomic per workgroup
+    const uint32_t c32 = cost > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)cost;
+    uint32_t total32;
+    block_excl_scan(c32, s_tmp, &total32);
+    if (threadIdx.x == 0 && total32) {
+        const uint64_t total = atomicAdd(work, (unsigned long long)total32) + total32;
+        if (total > budget || total32 == 0xFFFFFFFFu) atomicOr(need_high, 1);
+    }
+}
+
+// previous / next element with the same full key: within a run of equal low
+// bits (total work bounded by the check above), or just the neighbour after a
+// full sort
+__device__ __forceinline__ void link_of(const uint64_t *__restrict__ sk, const uint32_t *__restrict__ sv,
+                                        uint64_t n, uint64_t i, bool full, uint32_t &p, uint32_t &q) {
+    const uint64_t k = sk[i];
+    p = NONE;
+    q = NONE;
+    uint64_t hit;
+    if (i > 0) {
+        const uint64_t kp = sk[i - 1];
+        if (kp == k) p = sv[i - 1];
+        else if (!full && same_low(kp, k) && (scan_run(sk, n, k, i - 1, -1, ~0ull, &hit), hit != ~0ull))
+            p = sv[hit];
+    }
+    if (i + 1 < n) {
+        const uint64_t kn = sk[i + 1];
+        if (kn == k) q = sv[i + 1];
+        else if (!full && same_low(kn, k) && (scan_run(sk, n, k, i + 1, +1, ~0ull, &hit), hit != ~0ull))
+            q = sv[hit];
+    }
+}
+
 // One workgroup owns a contiguous chunk of the input.  It first counts the
 // chunk's digits, reserves one run per digit in the bucket's output range with
 // a single global atomic (so each bucket cursor sees one atomic per workgroup,
@@ -205,7 +317,7 @@ __global__ __launch_bounds__(PERM_THREADS) void perm_partition_kernel(
     const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t,
     const uint32_t *__restrict__ in_p, const uint32_t *__restrict__ in_n, uint64_t n, int s,
     uint64_t per_wg, uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t,
-    uint32_t *__restrict__ out_p, uint32_t *__restrict__ out_n) {
+    uint32_t *__restrict__ out_p, uint32_t *__restrict__ out_n, const int32_t *__restrict__ need_high) {
     __shared__ uint32_t s_t[PERM_TILE], s_p[PERM_TILE], s_n[PERM_TILE];
     __shared__ uint32_t s_cnt[PERM_RADIX];
     __shared__ uint32_t s_lstart[PERM_RADIX];
@@ -217,6 +329,7 @@ __global__ __launch_bounds__(PERM_THREADS) void perm_partition_kernel(
     const uint64_t lo = (uint64_t)blockIdx.x * per_wg;
     if (lo >= n) return;
     const uint64_t hi = lo + per_wg < n ? lo + per_wg : n;
+    const bool full = FROM_SORT && need_high && *need_high != 0;
 
     // ---- count the chunk's digits and reserve one run per digit
     for (int i = tid; i < PERM_RADIX; i += PERM_THREADS) s_cnt[i] = 0;
@@ -249,9 +362,7 @@ __global__ __launch_bounds__(PERM_THREADS) void perm_partition_kernel(
             if (!ok[j]) continue;
             t[j] = in_t[i];
             if (FROM_SORT) {
-                const uint64_t k = sk[i];
-                pv[j] = (i > 0 && sk[i - 1] == k) ? in_t[i - 1] : NONE;
-                nx[j] = (i + 1 < n && sk[i + 1] == k) ? in_t[i + 1] : NONE;
+                link_of(sk, in_t, n, i, full, pv[j], nx[j]);
             } else {
                 pv[j] = in_p[i];
                 nx[j] = in_n[i];
@@ -425,14 +536,25 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
     PC_LAUNCH(pc::K_SORT_HIST, pc::sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n, w.hist);
     PC_LAUNCH(pc::K_SORT_SCAN, pc::sort_scan_kernel, dim3(1), dim3(pc::RADIX), 0, s, w.hist, w.start);
 
+    // passes 0-3 sort by the low 32 key bits; passes 4-7 run only if the
+    // check finds a long mixed run (flag in header word 1)
+    int32_t *need_high = w.hdr + 1;
+    unsigned long long *mix_work = reinterpret_cast<unsigned long long *>(w.hdr + 2);
+    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(w.hdr + 1), 0u, 3, s)) != PC_OK) return st;
     const uint64_t *kin = keys;
     const uint32_t *vin = nullptr;
     for (int p = 0; p < pc::SORT_PASSES; ++p) {
+        if (p == pc::SORT_PASSES / 2) {
+            uint64_t cg = (n + 255) / 256;
+            if (cg > (uint64_t)cus * 8) cg = (uint64_t)cus * 8;
+            PC_LAUNCH(pc::K_SORT_CHECK, pc::sort_mix_check_kernel, dim3((unsigned)cg), dim3(256), 0, s, kin, n,
+                      (uint64_t)2 * n + 4096, mix_work, need_high);
+        }
         uint64_t *kout = (p & 1) ? w.k2 : w.k1;
         uint32_t *vout = (p & 1) ? w.v2 : w.v1;
         PC_LAUNCH(pc::K_SORT_PASS, pc::sort_pass_kernel, dim3((unsigned)tiles), dim3(pc::SORT_THREADS), 0, s,
                   kin, vin, kout, vout, n, 8 * p, w.start + p * pc::RADIX, w.status, w.counters + p,
-                  (uint32_t)(p + 1), w.hdr);
+                  (uint32_t)(p + 1), w.hdr, p >= pc::SORT_PASSES / 2 ? (const int32_t *)need_high : nullptr);
         kin = kout;
         vin = vout;
     }
@@ -460,13 +582,13 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
         if (i == 0) {
             PC_LAUNCH(pc::K_LINK, pc::perm_partition_kernel<true>, dim3(ptiles), dim3(pc::PERM_THREADS), 0, s,
                       kin, vin, (const uint32_t *)nullptr, (const uint32_t *)nullptr, n, pp.s[i], per_wg,
-                      w.cursor, bt[0], bp[0], bn[0]);
+                      w.cursor, bt[0], bp[0], bn[0], (const int32_t *)need_high);
             cur = 0;
         } else {
             const int nxt = cur ^ 1;
             PC_LAUNCH(pc::K_PERM, pc::perm_partition_kernel<false>, dim3(ptiles), dim3(pc::PERM_THREADS), 0,
                       s, (const uint64_t *)nullptr, bt[cur], bp[cur], bn[cur], n, pp.s[i], per_wg,
-                      w.cursor, bt[nxt], bp[nxt], bn[nxt]);
+                      w.cursor, bt[nxt], bp[nxt], bn[nxt], (const int32_t *)nullptr);
             cur = nxt;
         }
     }

@@ -22,12 +22,15 @@
 // Buckets are ranges of t, so their sizes are known in advance from the
 // per-4096 prefix of cold counts: #non-cold t < X = X - Z(X).
 //   * sd_cold_count + sd_scan      -> Z at every multiple of 4096
-//   * sd_dominance_pass (1-3 times) -> 8-bit digits above bit 12; per tile of
-//     2048 elements: wave ballots build per-chunk digit masks (two 16-entry
-//     nibble tables) that give, for every lane, the earlier lanes with a
-//     smaller / equal digit; a 2-D prefix over (chunk, digit) in LDS extends
-//     that to the tile; a per-bucket decoupled look-back extends it across
-//     tiles; the tile is then written out digit-partitioned through LDS.
+//   * per level (1-3 levels of 8-bit digits above bit 12), over tiles of 1024
+//     elements: sd_count (per-tile digit counts), a segmented scan of those
+//     counts over the tiles of each bucket (sd_seg: reduce, carry, scan --
+//     no waiting on other workgroups), then sd_dominance_pass: wave ballots
+//     build per-chunk digit masks (two 16-entry nibble tables) giving every
+//     lane the earlier lanes with a smaller / equal digit, a 2-D prefix over
+//     (chunk, digit) in LDS extends that to the tile, the scanned counts
+//     extend it across tiles, and the tile is written out digit-partitioned
+//     through LDS.
 //   * sd_local_finish -> one workgroup per 4096-range of t: two in-LDS levels
 //     of 6 bits finish the count, then D is written in t order with the cold
 //     prefix from a block scan.
@@ -39,18 +42,14 @@ constexpr int LOCAL_BITS = 12;
 constexpr uint32_t LOCAL_SPAN = 1u << LOCAL_BITS;   // 4096
 constexpr int DOM_THREADS = 256;
 constexpr int DOM_WAVES = DOM_THREADS / WAVE;
-constexpr int DOM_CHUNKS_PER_WAVE = 8;
+constexpr int DOM_CHUNKS_PER_WAVE = 4;
 constexpr int DOM_CHUNKS = DOM_WAVES * DOM_CHUNKS_PER_WAVE;   // 32
-constexpr int DOM_TILE = DOM_CHUNKS * WAVE;                    // 2048
+constexpr int DOM_TILE = DOM_CHUNKS * WAVE;                    // 1024
 constexpr int DOM_RADIX = 256;
 constexpr int LOC_THREADS = 256;
 constexpr int LOC_WAVES = LOC_THREADS / WAVE;
 constexpr int LOC_CHUNKS = LOCAL_SPAN / WAVE;                  // 64
 constexpr int LOC_CPW = LOC_CHUNKS / LOC_WAVES;                // 16
-constexpr uint32_t ST_AGG = 1u << 30;
-constexpr uint32_t ST_INC = 2u << 30;
-constexpr uint32_t ST_VAL = (1u << 30) - 1;
-constexpr uint32_t SD_SPIN_LIMIT = 1u << 22;
 constexpr int SCAN_THREADS = 1024;
 
 // number of non-cold accesses t < X (X a multiple of 4096, or X = n)
@@ -104,17 +103,233 @@ __global__ void sd_tile_count_kernel(const uint32_t *__restrict__ Zc, uint64_t n
     tcount[b] = (uint32_t)((size + DOM_TILE - 1) / DOM_TILE);
 }
 
-// One MSD level of the dominance count over 8-bit digits d = (t >> s) & mask.
-// FIRST: the input is next[] in index order (= v order), one bucket, tiles
-// over index ranges; otherwise the input is the previous level's output and
-// tiles never straddle a bucket (bucket = t >> (s + k)).
+// ---- one MSD level of the dominance count (8-bit digits of t) -----------
+// Tiles: FIRST reads next[] in index order (= v order) in fixed index ranges,
+// one bucket; later levels read the previous level's output with tiles that
+// never straddle a bucket (bucket = t >> (s + k)), located through tfirst.
+struct TileLoc {
+    uint64_t bucket, e0, e1, first_tile;
+    bool valid;
+};
+
+template <bool FIRST>
+__device__ __forceinline__ TileLoc locate_tile(uint64_t tile, uint64_t n, const uint32_t *__restrict__ Zc,
+                                               int S, const uint32_t *__restrict__ tfirst, uint64_t nbuckets) {
+    TileLoc L{0, 0, 0, 0, true};
+    if (FIRST) {
+        const uint64_t tiles = (n + DOM_TILE - 1) / DOM_TILE;
+        if (tile >= tiles) { L.valid = false; return L; }
+        L.e0 = tile * DOM_TILE;
+        L.e1 = L.e0 + DOM_TILE < n ? L.e0 + DOM_TILE : n;
+        return L;
+    }
+    if (tile >= tfirst[nbuckets]) { L.valid = false; return L; }
+    uint64_t lo = 0, hi = nbuckets;   // largest b with tfirst[b] <= tile
+    while (hi - lo > 1) {
+        const uint64_t mid = (lo + hi) >> 1;
+        if (tfirst[mid] <= tile) lo = mid; else hi = mid;
+    }
+    L.bucket = lo;
+    L.first_tile = tfirst[lo];
+    uint64_t blo = lo << S, bhi = (lo + 1) << S;
+    blo = blo < n ? blo : n;
+    bhi = bhi < n ? bhi : n;
+    const uint64_t bs = cnt_lt(blo, Zc), be = cnt_lt(bhi, Zc);
+    L.e0 = bs + (tile - L.first_tile) * DOM_TILE;
+    L.e1 = L.e0 + DOM_TILE < be ? L.e0 + DOM_TILE : be;
+    return L;
+}
+
+template <bool FIRST>
+__device__ __forceinline__ void load_tile(const TileLoc &L, const uint32_t *__restrict__ in_t,
+                                          const uint32_t *__restrict__ in_acc, int w, int lane,
+                                          uint32_t (&t)[DOM_CHUNKS_PER_WAVE], uint32_t (&acc)[DOM_CHUNKS_PER_WAVE],
+                                          bool (&ok)[DOM_CHUNKS_PER_WAVE], bool want_acc) {
+#pragma unroll
+    for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
+        const uint64_t e = L.e0 + (uint64_t)(w * DOM_CHUNKS_PER_WAVE + i) * WAVE + lane;
+        if (FIRST) {
+            const uint32_t x = e < L.e1 ? in_t[e] : NONE;
+            ok[i] = x != NONE;
+            t[i] = x;
+            acc[i] = 0;
+        } else {
+            ok[i] = e < L.e1;
+            t[i] = ok[i] ? in_t[e] : 0u;
+            acc[i] = (ok[i] && want_acc) ? in_acc[e] : 0u;
+        }
+    }
+}
+
+// Rank the lanes of one 64-element chunk by digit: eq = lanes with the same
+// digit, lt = lanes with a smaller digit, built from eight ballots through
+// two 16-entry nibble tables in LDS (rows of `mt`, one set per wave).
+__device__ __forceinline__ void chunk_masks(bool ok, uint32_t d, int lane, uint64_t (*mt)[16], uint64_t &eq,
+                                            uint64_t &lt) {
+    const uint64_t vm = ballot(ok);
+    uint64_t B[8];
+#pragma unroll
+    for (int b = 0; b < 8; ++b) B[b] = ballot(ok && ((d >> b) & 1));
+    if (lane < 16) {
+        uint64_t mh, lh, ml, ll;
+        digit_masks<4>(B + 4, vm, (uint32_t)lane, mh, lh);
+        digit_masks<4>(B, vm, (uint32_t)lane, ml, ll);
+        mt[0][lane] = mh;
+        mt[1][lane] = ml;
+        mt[2][lane] = lh;
+        mt[3][lane] = ll;
+    }
+    __builtin_amdgcn_wave_barrier();
+    const uint32_t h = d >> 4, l = d & 15;
+    const uint64_t Mh = mt[0][h], Ml = mt[1][l], Lh = mt[2][h], Ll = mt[3][l];
+    eq = Mh & Ml;
+    lt = Lh | (Mh & Ll);
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Per-tile digit counts (and whether the tile starts a bucket), the input of
+// the segmented scan over tiles.
+template <bool FIRST>
+__global__ __launch_bounds__(DOM_THREADS) void sd_count_kernel(
+    const uint32_t *__restrict__ in_t, uint64_t n, const uint32_t *__restrict__ Zc, int s, int k,
+    const uint32_t *__restrict__ tfirst, uint64_t nbuckets, uint16_t *__restrict__ cnt,
+    uint8_t *__restrict__ seg) {
+    __shared__ uint32_t s_cnt[DOM_RADIX];
+    __shared__ uint64_t s_mt[DOM_WAVES][4][16];
+    const int tid = threadIdx.x, lane = tid & (WAVE - 1), w = tid / WAVE;
+    const uint64_t tile = blockIdx.x;
+    const TileLoc L = locate_tile<FIRST>(tile, n, Zc, s + k, tfirst, nbuckets);
+    if (!L.valid) return;
+    s_cnt[tid] = 0;
+    __syncthreads();
+    uint32_t t[DOM_CHUNKS_PER_WAVE], acc[DOM_CHUNKS_PER_WAVE];
+    bool ok[DOM_CHUNKS_PER_WAVE];
+    load_tile<FIRST>(L, in_t, nullptr, w, lane, t, acc, ok, false);
+    const uint32_t dmask = (1u << k) - 1u;
+#pragma unroll
+    for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
+        const uint32_t d = (t[i] >> s) & dmask;
+        uint64_t eq, lt;
+        chunk_masks(ok[i], d, lane, s_mt[w], eq, lt);
+        if (ok[i] && mbcnt(eq) == 0) atomicAdd(&s_cnt[d], (uint32_t)__popcll(eq));
+    }
+    __syncthreads();
+    cnt[tile * DOM_RADIX + tid] = (uint16_t)s_cnt[tid];
+    if (tid == 0) seg[tile] = FIRST ? (tile == 0) : (tile == L.first_tile);
+}
+
+// Segmented exclusive scan over tiles, per digit (a bucket's first tile
+// restarts the sum), in three steps over groups of SEG_GROUP tiles.
+constexpr int SEG_GROUP = 1024;
+constexpr int SEG_BATCH = 16;
+
+__device__ __forceinline__ uint64_t total_tiles(const uint32_t *tfirst_end, uint64_t fixed) {
+    return tfirst_end ? (uint64_t)*tfirst_end : fixed;
+}
+
+// A: per group, the sum after its last bucket start, and whether it has one
+__global__ __launch_bounds__(DOM_RADIX) void sd_seg_reduce_kernel(const uint16_t *__restrict__ cnt,
+                                                                  const uint8_t *__restrict__ seg,
+                                                                  const uint32_t *tfirst_end, uint64_t fixed,
+                                                                  uint32_t *__restrict__ gsum,
+                                                                  uint8_t *__restrict__ ghas) {
+    const uint64_t rows = total_tiles(tfirst_end, fixed);
+    const uint64_t r0 = (uint64_t)blockIdx.x * SEG_GROUP;
+    if (r0 >= rows) return;
+    const uint64_t r1 = r0 + SEG_GROUP < rows ? r0 + SEG_GROUP : rows;
+    const int d = threadIdx.x;
+    uint32_t tail = 0;
+    bool has = false;
+    for (uint64_t r = r0; r < r1; r += SEG_BATCH) {
+        uint32_t c[SEG_BATCH];
+        bool f[SEG_BATCH];
+#pragma unroll
+        for (int q = 0; q < SEG_BATCH; ++q) {
+            const bool in = r + q < r1;
+            c[q] = in ? cnt[(r + q) * DOM_RADIX + d] : 0u;
+            f[q] = in && seg[r + q];
+        }
+#pragma unroll
+        for (int q = 0; q < SEG_BATCH; ++q) {
+            if (f[q]) { tail = 0; has = true; }
+            tail += c[q];
+        }
+    }
+    gsum[blockIdx.x * DOM_RADIX + d] = tail;
+    if (d == 0) ghas[blockIdx.x] = has;
+}
+
+// B: carry into every group (one workgroup, thread = digit)
+__global__ __launch_bounds__(DOM_RADIX) void sd_seg_carry_kernel(const uint32_t *__restrict__ gsum,
+                                                                 const uint8_t *__restrict__ ghas,
+                                                                 const uint32_t *tfirst_end, uint64_t fixed,
+                                                                 uint32_t *__restrict__ gin) {
+    const uint64_t rows = total_tiles(tfirst_end, fixed);
+    const uint64_t groups = (rows + SEG_GROUP - 1) / SEG_GROUP;
+    const int d = threadIdx.x;
+    uint32_t carry = 0;
+    for (uint64_t g = 0; g < groups; g += SEG_BATCH) {
+        uint32_t v[SEG_BATCH];
+        bool h[SEG_BATCH];
+#pragma unroll
+        for (int q = 0; q < SEG_BATCH; ++q) {
+            const bool in = g + q < groups;
+            v[q] = in ? gsum[(g + q) * DOM_RADIX + d] : 0u;
+            h[q] = in && ghas[g + q];
+        }
+#pragma unroll
+        for (int q = 0; q < SEG_BATCH; ++q) {
+            if (g + q < groups) {
+                gin[(g + q) * DOM_RADIX + d] = carry;
+                carry = h[q] ? v[q] : carry + v[q];
+            }
+        }
+    }
+}
+
+// C: per group, the exclusive prefix of every tile
+__global__ __launch_bounds__(DOM_RADIX) void sd_seg_scan_kernel(const uint16_t *__restrict__ cnt,
+                                                                const uint8_t *__restrict__ seg,
+                                                                const uint32_t *tfirst_end, uint64_t fixed,
+                                                                const uint32_t *__restrict__ gin,
+                                                                uint32_t *__restrict__ pre) {
+    const uint64_t rows = total_tiles(tfirst_end, fixed);
+    const uint64_t r0 = (uint64_t)blockIdx.x * SEG_GROUP;
+    if (r0 >= rows) return;
+    const uint64_t r1 = r0 + SEG_GROUP < rows ? r0 + SEG_GROUP : rows;
+    const int d = threadIdx.x;
+    uint32_t run = gin[blockIdx.x * DOM_RADIX + d];
+    for (uint64_t r = r0; r < r1; r += SEG_BATCH) {
+        uint32_t c[SEG_BATCH];
+        bool f[SEG_BATCH];
+#pragma unroll
+        for (int q = 0; q < SEG_BATCH; ++q) {
+            const bool in = r + q < r1;
+            c[q] = in ? cnt[(r + q) * DOM_RADIX + d] : 0u;
+            f[q] = in && seg[r + q];
+        }
+#pragma unroll
+        for (int q = 0; q < SEG_BATCH; ++q) {
+            if (r + q < r1) {
+                if (f[q]) run = 0;
+                pre[(r + q) * DOM_RADIX + d] = run;
+                run += c[q];
+            }
+        }
+    }
+}
+
+// The level itself: per tile, every element adds the number of earlier
+// elements of its bucket (in v order) with a smaller digit -- from earlier
+// tiles (the scanned counts), earlier chunks of the tile (2-D prefix over
+// (chunk, digit) in LDS) and earlier lanes of its chunk (ballot masks) --
+// and the tile is written out digit-partitioned through LDS.
 template <bool FIRST>
 __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     const uint32_t *__restrict__ in_t, const uint32_t *__restrict__ in_acc,
     uint32_t *__restrict__ out_t, uint32_t *__restrict__ out_acc, uint64_t n,
     const uint32_t *__restrict__ Zc, int s, int k, const uint32_t *__restrict__ tfirst,
-    uint64_t nbuckets, uint32_t *__restrict__ status, uint32_t *__restrict__ counter,
-    int32_t *__restrict__ err) {
+    uint64_t nbuckets, const uint32_t *__restrict__ pre, int32_t *__restrict__ err) {
     __shared__ uint16_t s_h[DOM_CHUNKS][DOM_RADIX];     // chunk histograms -> column prefix
     __shared__ uint16_t s_pl[DOM_CHUNKS][DOM_RADIX];    // 2-D prefix (earlier chunks, smaller digit)
     __shared__ uint32_t s_st[DOM_TILE];                 // staged t
@@ -124,98 +339,35 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     __shared__ uint32_t s_gl[DOM_RADIX];
     __shared__ uint32_t s_base[DOM_RADIX];
     __shared__ uint32_t s_tmp[DOM_WAVES];
-    __shared__ uint32_t s_tile;
 
     const int tid = threadIdx.x;
     const int lane = tid & (WAVE - 1);
     const int w = tid / WAVE;
     const uint32_t dmask = (1u << k) - 1u;
-    const int S = s + k;
-
-    if (tid == 0) s_tile = atomicAdd(counter, 1u);
+    const uint64_t tile = blockIdx.x;
+    const TileLoc L = locate_tile<FIRST>(tile, n, Zc, s + k, tfirst, nbuckets);
+    if (!L.valid) return;
+    const uint32_t G = pre[tile * DOM_RADIX + tid];   // same digit, earlier tiles of the bucket
     {
         uint64_t *z = reinterpret_cast<uint64_t *>(&s_h[0][0]);
         for (int i = tid; i < DOM_CHUNKS * DOM_RADIX / 4; i += DOM_THREADS) z[i] = 0;
     }
-    __syncthreads();
-    const uint32_t tile = s_tile;
-
-    // ---- locate the tile
-    uint64_t bucket = 0, e0 = 0, e1 = 0, first_tile = 0;
-    if (FIRST) {
-        const uint64_t tiles = (n + DOM_TILE - 1) / DOM_TILE;
-        if (tile >= tiles) return;
-        e0 = (uint64_t)tile * DOM_TILE;
-        e1 = e0 + DOM_TILE < n ? e0 + DOM_TILE : n;
-    } else {
-        if (tile >= tfirst[nbuckets]) return;
-        uint64_t lo = 0, hi = nbuckets;   // largest b with tfirst[b] <= tile
-        while (hi - lo > 1) {
-            const uint64_t mid = (lo + hi) >> 1;
-            if (tfirst[mid] <= tile) lo = mid; else hi = mid;
-        }
-        bucket = lo;
-        first_tile = tfirst[bucket];
-        uint64_t blo = bucket << S, bhi = (bucket + 1) << S;
-        blo = blo < n ? blo : n;
-        bhi = bhi < n ? bhi : n;
-        const uint64_t bs = cnt_lt(blo, Zc), be = cnt_lt(bhi, Zc);
-        e0 = bs + (uint64_t)(tile - first_tile) * DOM_TILE;
-        e1 = e0 + DOM_TILE < be ? e0 + DOM_TILE : be;
-    }
-
-    // ---- load and rank inside each 64-lane chunk
     uint32_t t[DOM_CHUNKS_PER_WAVE], acc[DOM_CHUNKS_PER_WAVE];
-    uint16_t q_ic[DOM_CHUNKS_PER_WAVE], l_ic[DOM_CHUNKS_PER_WAVE];
     bool ok[DOM_CHUNKS_PER_WAVE];
-#pragma unroll
-    for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
-        const uint64_t e = e0 + (uint64_t)(w * DOM_CHUNKS_PER_WAVE + i) * WAVE + lane;
-        if (FIRST) {
-            const uint32_t x = e < e1 ? in_t[e] : NONE;
-            ok[i] = x != NONE;
-            t[i] = x;
-            acc[i] = 0;
-        } else {
-            ok[i] = e < e1;
-            t[i] = ok[i] ? in_t[e] : 0u;
-            acc[i] = ok[i] ? in_acc[e] : 0u;
-        }
-    }
+    load_tile<FIRST>(L, in_t, in_acc, w, lane, t, acc, ok, true);
+    __syncthreads();
+
+    // ---- rank inside each 64-lane chunk
+    uint16_t q_ic[DOM_CHUNKS_PER_WAVE], l_ic[DOM_CHUNKS_PER_WAVE];
 #pragma unroll
     for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
         const int c = w * DOM_CHUNKS_PER_WAVE + i;
         const uint32_t d = (t[i] >> s) & dmask;
-        const uint64_t vm = ballot(ok[i]);
-        uint64_t B[8];
-#pragma unroll
-        for (int b = 0; b < 8; ++b) B[b] = ballot(ok[i] && ((d >> b) & 1));
-        // lanes 0..15 build the nibble tables: lanes whose high / low nibble
-        // equals q, and lanes whose nibble is smaller than q
-        if (lane < 16) {
-            uint64_t mh, lh, ml, ll;
-            digit_masks<4>(B + 4, vm, (uint32_t)lane, mh, lh);
-            digit_masks<4>(B, vm, (uint32_t)lane, ml, ll);
-            s_mt[w][0][lane] = mh;
-            s_mt[w][1][lane] = ml;
-            s_mt[w][2][lane] = lh;
-            s_mt[w][3][lane] = ll;
-        }
-        __builtin_amdgcn_wave_barrier();
-        if (ok[i]) {
-            const uint32_t h = d >> 4, l = d & 15;
-            const uint64_t Mh = s_mt[w][0][h], Ml = s_mt[w][1][l];
-            const uint64_t Lh = s_mt[w][2][h], Ll = s_mt[w][3][l];
-            const uint64_t eq = Mh & Ml;
-            const uint64_t lt = Lh | (Mh & Ll);
-            q_ic[i] = (uint16_t)mbcnt(eq);
-            l_ic[i] = (uint16_t)mbcnt(lt);
-            if (q_ic[i] == 0) s_h[c][d] = (uint16_t)__popcll(eq);
-        } else {
-            q_ic[i] = 0;
-            l_ic[i] = 0;
-        }
-        __builtin_amdgcn_wave_barrier();
+        uint64_t eq, lt;
+        chunk_masks(ok[i], d, lane, s_mt[w], eq, lt);
+        q_ic[i] = ok[i] ? (uint16_t)mbcnt(eq) : 0;
+        l_ic[i] = ok[i] ? (uint16_t)mbcnt(lt) : 0;
+        if (ok[i] && q_ic[i] == 0) s_h[c][d] = (uint16_t)__popcll(eq);
     }
     __syncthreads();
 
@@ -246,38 +398,10 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     }
     uint32_t n_valid;
     const uint32_t lst = block_excl_scan(tot, s_tmp, &n_valid);
-
-    // ---- look-back across the bucket's earlier tiles (thread = digit)
-    uint32_t G = 0;
-    {
-        uint32_t *mine = status + (uint64_t)tile * DOM_RADIX + tid;
-        if (tile == first_tile) {
-            st_status(mine, ST_INC | tot);
-        } else {
-            st_status(mine, ST_AGG | tot);
-            int64_t j = (int64_t)tile - 1;
-            uint32_t spins = 0;
-            while (j >= (int64_t)first_tile) {
-                const uint32_t x = ld_status(status + (uint64_t)j * DOM_RADIX + tid);
-                if ((x & (ST_AGG | ST_INC)) == 0) {
-                    if (++spins > SD_SPIN_LIMIT) {
-                        atomicOr(err, DEV_ERR_LOOKBACK_TIMEOUT);
-                        break;
-                    }
-                    __builtin_amdgcn_s_sleep(1);
-                    continue;
-                }
-                G += x & ST_VAL;
-                if (x & ST_INC) break;
-                --j;
-            }
-            st_status(mine, ST_INC | ((G + tot) & ST_VAL));
-        }
-    }
     uint32_t gsum;
-    const uint32_t GL = block_excl_scan(G, s_tmp, &gsum);
+    const uint32_t GL = block_excl_scan(G, s_tmp, &gsum);   // smaller digit, earlier tiles
     {
-        const uint64_t X = ((bucket << k) + (uint64_t)tid) << s;
+        const uint64_t X = ((L.bucket << k) + (uint64_t)tid) << s;
         const uint64_t sub = cnt_lt(X < n ? X : n, Zc);
         s_lstart[tid] = lst;
         s_gl[tid] = GL;
@@ -495,9 +619,11 @@ static SdPlan plan_sd(uint64_t n) {
 
 struct SdWs {
     int32_t *hdr;
-    uint32_t *cold, *Zc, *tcount, *tfirst, *counters;
+    uint32_t *cold, *Zc, *tcount, *tfirst;
     uint32_t *at, *aa, *bt, *ba;
-    uint32_t *status;
+    uint16_t *cnt;
+    uint8_t *seg, *ghas;
+    uint32_t *gsum, *gin, *pre;
     size_t bytes;
 };
 
@@ -505,17 +631,22 @@ static SdWs carve_sd(void *ws, uint64_t n, const SdPlan &p) {
     Carver c{(char *)ws, 0};
     SdWs w;
     const uint64_t nchunks = (n + LOCAL_SPAN - 1) / LOCAL_SPAN;
+    const uint64_t groups = (p.max_grid + SEG_GROUP - 1) / SEG_GROUP;
     w.hdr = c.take<int32_t>(WS_HEADER / sizeof(int32_t));
     w.cold = c.take<uint32_t>(nchunks + 1);
     w.Zc = c.take<uint32_t>(nchunks + 2);
     w.tcount = c.take<uint32_t>(p.max_buckets + 1);
     w.tfirst = c.take<uint32_t>(p.max_buckets + 2);
-    w.counters = c.take<uint32_t>(4);
     w.at = c.take<uint32_t>(n);
     w.aa = c.take<uint32_t>(n);
     w.bt = c.take<uint32_t>(n);
     w.ba = c.take<uint32_t>(n);
-    w.status = c.take<uint32_t>(p.max_grid * DOM_RADIX);
+    w.cnt = c.take<uint16_t>(p.max_grid * DOM_RADIX);
+    w.seg = c.take<uint8_t>(p.max_grid);
+    w.ghas = c.take<uint8_t>(groups);
+    w.gsum = c.take<uint32_t>(groups * DOM_RADIX);
+    w.gin = c.take<uint32_t>(groups * DOM_RADIX);
+    w.pre = c.take<uint32_t>(p.max_grid * DOM_RADIX);
     w.bytes = c.off;
     return w;
 }
@@ -546,28 +677,41 @@ pc_status pc_stack_distance(const uint32_t *prev, const uint32_t *next, uint64_t
               w.cold);
     PC_LAUNCH(pc::K_SD_SCAN, pc::sd_scan_kernel, dim3(1), dim3(pc::SCAN_THREADS), 0, s, w.cold, nchunks,
               w.Zc);
-    if ((st = pc::fill_u32(w.counters, 0u, 4, s)) != PC_OK) return st;
 
     uint32_t *src_t = nullptr, *src_a = nullptr;
     for (int i = 0; i < p.passes; ++i) {
         uint32_t *dt = (i & 1) ? w.bt : w.at;
         uint32_t *da = (i & 1) ? w.ba : w.aa;
         const int S = p.s[i] + p.k[i];
-        if ((st = pc::fill_u32(w.status, 0u, p.grid[i] * pc::DOM_RADIX, s)) != PC_OK) return st;
+        const unsigned grid = (unsigned)p.grid[i];
+        const unsigned groups = (unsigned)((p.grid[i] + pc::SEG_GROUP - 1) / pc::SEG_GROUP);
+        const uint64_t fixed = (n + pc::DOM_TILE - 1) / pc::DOM_TILE;
         if (i == 0) {
-            PC_LAUNCH(pc::K_SD_PASS, pc::sd_dominance_kernel<true>, dim3((unsigned)p.grid[i]),
-                      dim3(pc::DOM_THREADS), 0, s, next, (const uint32_t *)nullptr, dt, da, n, w.Zc,
-                      p.s[i], p.k[i], (const uint32_t *)nullptr, (uint64_t)1, w.status, w.counters + i,
-                      w.hdr);
+            PC_LAUNCH(pc::K_SD_COUNT, pc::sd_count_kernel<true>, dim3(grid), dim3(pc::DOM_THREADS), 0, s, next, n,
+                      w.Zc, p.s[i], p.k[i], (const uint32_t *)nullptr, (uint64_t)1, w.cnt, w.seg);
         } else {
             const uint64_t nb = p.nbuckets[i];
             PC_LAUNCH(pc::K_SD_TILES, pc::sd_tile_count_kernel, dim3((unsigned)((nb + 255) / 256)), dim3(256),
                       0, s, w.Zc, n, S, nb, w.tcount);
             PC_LAUNCH(pc::K_SD_SCAN, pc::sd_scan_kernel, dim3(1), dim3(pc::SCAN_THREADS), 0, s, w.tcount, nb,
                       w.tfirst);
-            PC_LAUNCH(pc::K_SD_PASS, pc::sd_dominance_kernel<false>, dim3((unsigned)p.grid[i]),
-                      dim3(pc::DOM_THREADS), 0, s, src_t, src_a, dt, da, n, w.Zc, p.s[i], p.k[i],
-                      w.tfirst, nb, w.status, w.counters + i, w.hdr);
+            PC_LAUNCH(pc::K_SD_COUNT, pc::sd_count_kernel<false>, dim3(grid), dim3(pc::DOM_THREADS), 0, s, src_t,
+                      n, w.Zc, p.s[i], p.k[i], w.tfirst, nb, w.cnt, w.seg);
+        }
+        const uint32_t *tend = i == 0 ? nullptr : w.tfirst + p.nbuckets[i];
+        PC_LAUNCH(pc::K_SD_SEG, pc::sd_seg_reduce_kernel, dim3(groups), dim3(pc::DOM_RADIX), 0, s, w.cnt, w.seg,
+                  tend, fixed, w.gsum, w.ghas);
+        PC_LAUNCH(pc::K_SD_SEG, pc::sd_seg_carry_kernel, dim3(1), dim3(pc::DOM_RADIX), 0, s, w.gsum, w.ghas, tend,
+                  fixed, w.gin);
+        PC_LAUNCH(pc::K_SD_SEG, pc::sd_seg_scan_kernel, dim3(groups), dim3(pc::DOM_RADIX), 0, s, w.cnt, w.seg,
+                  tend, fixed, w.gin, w.pre);
+        if (i == 0) {
+            PC_LAUNCH(pc::K_SD_PASS, pc::sd_dominance_kernel<true>, dim3(grid), dim3(pc::DOM_THREADS), 0, s,
+                      next, (const uint32_t *)nullptr, dt, da, n, w.Zc, p.s[i], p.k[i],
+                      (const uint32_t *)nullptr, (uint64_t)1, w.pre, w.hdr);
+        } else {
+            PC_LAUNCH(pc::K_SD_PASS, pc::sd_dominance_kernel<false>, dim3(grid), dim3(pc::DOM_THREADS), 0, s,
+                      src_t, src_a, dt, da, n, w.Zc, p.s[i], p.k[i], w.tfirst, p.nbuckets[i], w.pre, w.hdr);
         }
         src_t = dt;
         src_a = da;

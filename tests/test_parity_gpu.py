@@ -164,6 +164,22 @@ def stream(kind, n, seed=0):
     if kind == "cyclic":
         m = max(n // 7, 1)
         return (np.arange(n) % m).astype(np.uint64) + np.uint64(5)
+    if kind == "lowpairs":
+        # every low-32-bit value is shared by two keys: short mixed runs
+        low = rng.integers(1, 2 ** 32, size=max(n // 40, 1), dtype=np.uint64)
+        pick = rng.integers(0, low.size, size=n)
+        high = rng.integers(1, 3, size=n).astype(np.uint64)
+        return low[pick] | (high << np.uint64(32))
+    if kind == "lowsame":
+        # one low-32-bit value for everything, 1000 keys: one huge mixed run
+        return np.uint64(0x1234ABCD) | (rng.integers(1, 1001, size=n).astype(np.uint64) << np.uint64(32))
+    if kind == "lowhot":
+        # a hot key and a rare key sharing its low bits among random keys
+        k = pcgen.random_keys(n, max(n // 20, 1), seed)
+        u = rng.random(n)
+        k[u < 0.4] = np.uint64(0x77 | (5 << 32))
+        k[u > 0.999] = np.uint64(0x77 | (9 << 32))
+        return k
     return pcgen.random_keys(n, max(n // 10, 1), seed)
 
 
@@ -173,7 +189,8 @@ def test_small_and_ragged_sizes(n):
                     label="ragged%d" % n)
 
 
-@pytest.mark.parametrize("kind", ["equal", "distinct", "hot", "few", "cyclic", "mixed"])
+@pytest.mark.parametrize("kind", ["equal", "distinct", "hot", "few", "cyclic", "mixed", "lowpairs",
+                                  "lowsame", "lowhot"])
 def test_degenerate_streams(kind):
     check_keys_path(stream(kind, 70001, 3), caps=np.array([0, 1, 2, 7, 10000, 10 ** 8], np.uint64),
                     label=kind)
