@@ -105,10 +105,17 @@ __global__ __launch_bounds__(HASH_THREADS) void hash_digest_kernel(
 // chains its own row in LDS, and the keys (and depths) go back the same way.
 // Lanes whose request ended take the next one from an atomic counter at the
 // start of the round.
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int i) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, i);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), i);
+    return (uint64_t)lo | ((uint64_t)hi << 32);
+}
+
 constexpr int CHAIN_THREADS = 128;                       // two waves per workgroup
 constexpr int CHAIN_WAVES = CHAIN_THREADS / WAVE;
 constexpr int CHAIN_SPAN = 32;                           // blocks per request per round
 constexpr int CHAIN_ROW = CHAIN_SPAN + 1;                // padded LDS row
+constexpr int GATHER_BATCH = 16;                         // requests per load round
 
 __global__ __launch_bounds__(CHAIN_THREADS) void hash_chain_kernel(
     const uint32_t *__restrict__ tok_len, uint32_t n_seqs, uint32_t B,
@@ -151,12 +158,35 @@ __global__ __launch_bounds__(CHAIN_THREADS) void hash_chain_kernel(
         }
         const uint32_t m = busy ? (nb - b < (uint32_t)CHAIN_SPAN ? nb - b : (uint32_t)CHAIN_SPAN) : 0u;
         const uint64_t pos = out + b;
-        // gather: row i <- the next m_i digests of lane i's request
-        for (uint64_t act = active; act; act &= act - 1) {
-            const int i = __ffsll((unsigned long long)act) - 1;
-            const uint32_t mi = __shfl(m, i, WAVE);
-            const uint64_t pi = __shfl(pos, i, WAVE);
-            if ((uint32_t)lane < mi) tile[i * CHAIN_ROW + lane] = keys[pi + lane];
+        // gather: row i <- the next m_i digests of lane i's request.  Loads
+        // for GATHER_BATCH requests are issued before their LDS stores, so a
+        // round waits for a few memory latencies instead of one per request.
+        {
+            uint64_t act = active;
+            while (act) {
+                int ids[GATHER_BATCH];
+                uint64_t v[GATHER_BATCH];
+#pragma unroll
+                for (int q = 0; q < GATHER_BATCH; ++q) {
+                    ids[q] = -1;
+                    v[q] = 0;
+                    if (act) {
+                        const int i = __ffsll((unsigned long long)act) - 1;   // wave-uniform
+                        act &= act - 1;
+                        ids[q] = i;
+                        const uint32_t mi = (uint32_t)__builtin_amdgcn_readlane((int)m, i);
+                        const uint64_t pi = readlane64(pos, i);
+                        if ((uint32_t)lane < mi) v[q] = keys[pi + lane];
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < GATHER_BATCH; ++q) {
+                    if (ids[q] >= 0) {
+                        const uint32_t mi = (uint32_t)__builtin_amdgcn_readlane((int)m, ids[q]);
+                        if ((uint32_t)lane < mi) tile[ids[q] * CHAIN_ROW + lane] = v[q];
+                    }
+                }
+            }
         }
         __builtin_amdgcn_wave_barrier();
         if (busy) {
@@ -167,15 +197,37 @@ __global__ __launch_bounds__(CHAIN_THREADS) void hash_chain_kernel(
             }
         }
         __builtin_amdgcn_wave_barrier();
-        // scatter back: keys and depths of row i, coalesced
-        for (uint64_t act = active; act; act &= act - 1) {
-            const int i = __ffsll((unsigned long long)act) - 1;
-            const uint32_t mi = __shfl(m, i, WAVE);
-            const uint64_t pi = __shfl(pos, i, WAVE);
-            const uint32_t bi = __shfl(b, i, WAVE);
-            if ((uint32_t)lane < mi) {
-                keys[pi + lane] = tile[i * CHAIN_ROW + lane];
-                if (depth) depth[pi + lane] = bi + lane;
+        // scatter back: keys and depths of row i, coalesced (LDS reads for a
+        // batch of requests first, then their stores)
+        {
+            uint64_t act = active;
+            while (act) {
+                int ids[GATHER_BATCH];
+                uint64_t v[GATHER_BATCH];
+#pragma unroll
+                for (int q = 0; q < GATHER_BATCH; ++q) {
+                    ids[q] = -1;
+                    v[q] = 0;
+                    if (act) {
+                        const int i = __ffsll((unsigned long long)act) - 1;
+                        act &= act - 1;
+                        ids[q] = i;
+                        v[q] = tile[i * CHAIN_ROW + (lane < CHAIN_SPAN ? lane : 0)];
+                    }
+                }
+#pragma unroll
+                for (int q = 0; q < GATHER_BATCH; ++q) {
+                    if (ids[q] >= 0) {
+                        const int i = ids[q];
+                        const uint32_t mi = (uint32_t)__builtin_amdgcn_readlane((int)m, i);
+                        const uint64_t pi = readlane64(pos, i);
+                        const uint32_t bi = (uint32_t)__builtin_amdgcn_readlane((int)b, i);
+                        if ((uint32_t)lane < mi) {
+                            keys[pi + lane] = v[q];
+                            if (depth) depth[pi + lane] = bi + lane;
+                        }
+                    }
+                }
             }
         }
         __builtin_amdgcn_wave_barrier();

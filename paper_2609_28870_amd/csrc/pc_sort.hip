@@ -281,27 +281,30 @@ __global__ __launch_bounds__(256) void sort_mix_check_kernel(const uint64_t *__r
     }
 }
 
-// previous / next element with the same full key: within a run of equal low
-// bits (total work bounded by the check above), or just the neighbour after a
-// full sort
-__device__ __forceinline__ void link_of(const uint64_t *__restrict__ sk, const uint32_t *__restrict__ sv,
-                                        uint64_t n, uint64_t i, bool full, uint32_t &p, uint32_t &q) {
-    const uint64_t k = sk[i];
-    p = NONE;
-    q = NONE;
+// previous / next element with the same full key inside a mixed run (total
+// work bounded by the check above)
+__device__ __forceinline__ void link_prev(const uint64_t *__restrict__ sk, const uint32_t *__restrict__ sv,
+                                          uint64_t n, uint64_t i, uint32_t &p) {
     uint64_t hit;
-    if (i > 0) {
-        const uint64_t kp = sk[i - 1];
-        if (kp == k) p = sv[i - 1];
-        else if (!full && same_low(kp, k) && (scan_run(sk, n, k, i - 1, -1, ~0ull, &hit), hit != ~0ull))
-            p = sv[hit];
-    }
-    if (i + 1 < n) {
-        const uint64_t kn = sk[i + 1];
-        if (kn == k) q = sv[i + 1];
-        else if (!full && same_low(kn, k) && (scan_run(sk, n, k, i + 1, +1, ~0ull, &hit), hit != ~0ull))
-            q = sv[hit];
-    }
+    scan_run(sk, n, sk[i], i - 1, -1, ~0ull, &hit);
+    p = hit != ~0ull ? sv[hit] : NONE;
+}
+__device__ __forceinline__ void link_next(const uint64_t *__restrict__ sk, const uint32_t *__restrict__ sv,
+                                          uint64_t n, uint64_t i, uint32_t &q) {
+    uint64_t hit;
+    scan_run(sk, n, sk[i], i + 1, +1, ~0ull, &hit);
+    q = hit != ~0ull ? sv[hit] : NONE;
+}
+
+__device__ __forceinline__ uint64_t shfl_up64(uint64_t v) {
+    const uint32_t lo = (uint32_t)__shfl_up((int)(uint32_t)v, 1, WAVE);
+    const uint32_t hi = (uint32_t)__shfl_up((int)(uint32_t)(v >> 32), 1, WAVE);
+    return (uint64_t)lo | ((uint64_t)hi << 32);
+}
+__device__ __forceinline__ uint64_t shfl_down64(uint64_t v) {
+    const uint32_t lo = (uint32_t)__shfl_down((int)(uint32_t)v, 1, WAVE);
+    const uint32_t hi = (uint32_t)__shfl_down((int)(uint32_t)(v >> 32), 1, WAVE);
+    return (uint64_t)lo | ((uint64_t)hi << 32);
 }
 
 // One workgroup owns a contiguous chunk of the input.  It first counts the
@@ -334,11 +337,22 @@ __global__ __launch_bounds__(PERM_THREADS) void perm_partition_kernel(
     // ---- count the chunk's digits and reserve one run per digit
     for (int i = tid; i < PERM_RADIX; i += PERM_THREADS) s_cnt[i] = 0;
     __syncthreads();
-    for (uint64_t i = lo + tid; i < hi; i += PERM_THREADS) {
-        const uint32_t tt = in_t[i];
-        const uint32_t d = (tt >> s) & (PERM_RADIX - 1);
-        atomicAdd(&s_cnt[d], 1u);
-        s_bucket[d] = tt >> s;   // every writer of digit d writes the same bucket
+    // eight loads in flight per thread before their LDS updates
+    for (uint64_t i0 = lo + tid; i0 < hi; i0 += 8 * PERM_THREADS) {
+        uint32_t tt[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const uint64_t i = i0 + (uint64_t)q * PERM_THREADS;
+            tt[q] = i < hi ? in_t[i] : 0u;
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            if (i0 + (uint64_t)q * PERM_THREADS < hi) {
+                const uint32_t d = (tt[q] >> s) & (PERM_RADIX - 1);
+                atomicAdd(&s_cnt[d], 1u);
+                s_bucket[d] = tt[q] >> s;   // every writer of digit d writes the same bucket
+            }
+        }
     }
     __syncthreads();
 #pragma unroll
@@ -362,7 +376,22 @@ __global__ __launch_bounds__(PERM_THREADS) void perm_partition_kernel(
             if (!ok[j]) continue;
             t[j] = in_t[i];
             if (FROM_SORT) {
-                link_of(sk, in_t, n, i, full, pv[j], nx[j]);
+                // consecutive lanes hold consecutive sorted positions: the
+                // neighbours' keys and times come from the adjacent lanes
+                // (the wave's first and last lanes load theirs)
+                const uint64_t k = sk[i];
+                const int lane = tid & (WAVE - 1);
+                uint64_t kp = shfl_up64(k), kn = shfl_down64(k);
+                uint32_t tp = (uint32_t)__shfl_up((int)t[j], 1, WAVE);
+                uint32_t tn = (uint32_t)__shfl_down((int)t[j], 1, WAVE);
+                if (lane == 0 && i > 0) { kp = sk[i - 1]; tp = in_t[i - 1]; }
+                if ((lane == WAVE - 1 || i + 1 >= hi) && i + 1 < n) { kn = sk[i + 1]; tn = in_t[i + 1]; }
+                if (i > 0 && kp == k) pv[j] = tp;
+                else if (i > 0 && !full && same_low(kp, k)) link_prev(sk, in_t, n, i, pv[j]);
+                else pv[j] = NONE;
+                if (i + 1 < n && kn == k) nx[j] = tn;
+                else if (i + 1 < n && !full && same_low(kn, k)) link_next(sk, in_t, n, i, nx[j]);
+                else nx[j] = NONE;
             } else {
                 pv[j] = in_p[i];
                 nx[j] = in_n[i];
