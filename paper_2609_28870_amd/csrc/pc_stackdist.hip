@@ -112,9 +112,24 @@ struct TileLoc {
     bool valid;
 };
 
+// tile -> bucket of a level (largest b with tfirst[b] <= tile), computed
+// once per level so the level's kernels need one load instead of a search
+__global__ void sd_tile_bucket_kernel(const uint32_t *__restrict__ tfirst, uint64_t nbuckets, uint64_t max_tiles,
+                                      uint32_t *__restrict__ tile_bucket) {
+    const uint64_t tile = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (tile >= max_tiles || tile >= tfirst[nbuckets]) return;
+    uint64_t lo = 0, hi = nbuckets;
+    while (hi - lo > 1) {
+        const uint64_t mid = (lo + hi) >> 1;
+        if (tfirst[mid] <= tile) lo = mid; else hi = mid;
+    }
+    tile_bucket[tile] = (uint32_t)lo;
+}
+
 template <bool FIRST>
 __device__ __forceinline__ TileLoc locate_tile(uint64_t tile, uint64_t n, const uint32_t *__restrict__ Zc,
-                                               int S, const uint32_t *__restrict__ tfirst, uint64_t nbuckets) {
+                                               int S, const uint32_t *__restrict__ tfirst, uint64_t nbuckets,
+                                               const uint32_t *__restrict__ tile_bucket) {
     TileLoc L{0, 0, 0, 0, true};
     if (FIRST) {
         const uint64_t tiles = (n + DOM_TILE - 1) / DOM_TILE;
@@ -124,11 +139,7 @@ __device__ __forceinline__ TileLoc locate_tile(uint64_t tile, uint64_t n, const 
         return L;
     }
     if (tile >= tfirst[nbuckets]) { L.valid = false; return L; }
-    uint64_t lo = 0, hi = nbuckets;   // largest b with tfirst[b] <= tile
-    while (hi - lo > 1) {
-        const uint64_t mid = (lo + hi) >> 1;
-        if (tfirst[mid] <= tile) lo = mid; else hi = mid;
-    }
+    const uint64_t lo = tile_bucket[tile];
     L.bucket = lo;
     L.first_tile = tfirst[lo];
     uint64_t blo = lo << S, bhi = (lo + 1) << S;
@@ -192,13 +203,13 @@ __device__ __forceinline__ void chunk_masks(bool ok, uint32_t d, int lane, uint6
 template <bool FIRST>
 __global__ __launch_bounds__(DOM_THREADS) void sd_count_kernel(
     const uint32_t *__restrict__ in_t, uint64_t n, const uint32_t *__restrict__ Zc, int s, int k,
-    const uint32_t *__restrict__ tfirst, uint64_t nbuckets, uint16_t *__restrict__ cnt,
-    uint8_t *__restrict__ seg) {
+    const uint32_t *__restrict__ tfirst, uint64_t nbuckets, const uint32_t *__restrict__ tile_bucket,
+    uint16_t *__restrict__ cnt, uint8_t *__restrict__ seg) {
     __shared__ uint32_t s_cnt[DOM_RADIX];
     __shared__ uint64_t s_mt[DOM_WAVES][4][16];
     const int tid = threadIdx.x, lane = tid & (WAVE - 1), w = tid / WAVE;
     const uint64_t tile = blockIdx.x;
-    const TileLoc L = locate_tile<FIRST>(tile, n, Zc, s + k, tfirst, nbuckets);
+    const TileLoc L = locate_tile<FIRST>(tile, n, Zc, s + k, tfirst, nbuckets, tile_bucket);
     if (!L.valid) return;
     s_cnt[tid] = 0;
     __syncthreads();
@@ -329,7 +340,8 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     const uint32_t *__restrict__ in_t, const uint32_t *__restrict__ in_acc,
     uint32_t *__restrict__ out_t, uint32_t *__restrict__ out_acc, uint64_t n,
     const uint32_t *__restrict__ Zc, int s, int k, const uint32_t *__restrict__ tfirst,
-    uint64_t nbuckets, const uint32_t *__restrict__ pre, int32_t *__restrict__ err) {
+    uint64_t nbuckets, const uint32_t *__restrict__ tile_bucket, const uint32_t *__restrict__ pre,
+    int32_t *__restrict__ err) {
     __shared__ uint16_t s_h[DOM_CHUNKS][DOM_RADIX];     // chunk histograms -> column prefix
     __shared__ uint16_t s_pl[DOM_CHUNKS][DOM_RADIX];    // 2-D prefix (earlier chunks, smaller digit)
     __shared__ uint32_t s_st[DOM_TILE];                 // staged t
@@ -345,7 +357,7 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     const int w = tid / WAVE;
     const uint32_t dmask = (1u << k) - 1u;
     const uint64_t tile = blockIdx.x;
-    const TileLoc L = locate_tile<FIRST>(tile, n, Zc, s + k, tfirst, nbuckets);
+    const TileLoc L = locate_tile<FIRST>(tile, n, Zc, s + k, tfirst, nbuckets, tile_bucket);
     if (!L.valid) return;
     const uint32_t G = pre[tile * DOM_RADIX + tid];   // same digit, earlier tiles of the bucket
     {
@@ -623,7 +635,7 @@ struct SdWs {
     uint32_t *at, *aa, *bt, *ba;
     uint16_t *cnt;
     uint8_t *seg, *ghas;
-    uint32_t *gsum, *gin, *pre;
+    uint32_t *gsum, *gin, *pre, *tile_bucket;
     size_t bytes;
 };
 
@@ -647,6 +659,7 @@ static SdWs carve_sd(void *ws, uint64_t n, const SdPlan &p) {
     w.gsum = c.take<uint32_t>(groups * DOM_RADIX);
     w.gin = c.take<uint32_t>(groups * DOM_RADIX);
     w.pre = c.take<uint32_t>(p.max_grid * DOM_RADIX);
+    w.tile_bucket = c.take<uint32_t>(p.max_grid);
     w.bytes = c.off;
     return w;
 }
@@ -688,15 +701,18 @@ pc_status pc_stack_distance(const uint32_t *prev, const uint32_t *next, uint64_t
         const uint64_t fixed = (n + pc::DOM_TILE - 1) / pc::DOM_TILE;
         if (i == 0) {
             PC_LAUNCH(pc::K_SD_COUNT, pc::sd_count_kernel<true>, dim3(grid), dim3(pc::DOM_THREADS), 0, s, next, n,
-                      w.Zc, p.s[i], p.k[i], (const uint32_t *)nullptr, (uint64_t)1, w.cnt, w.seg);
+                      w.Zc, p.s[i], p.k[i], (const uint32_t *)nullptr, (uint64_t)1, (const uint32_t *)nullptr,
+                      w.cnt, w.seg);
         } else {
             const uint64_t nb = p.nbuckets[i];
             PC_LAUNCH(pc::K_SD_TILES, pc::sd_tile_count_kernel, dim3((unsigned)((nb + 255) / 256)), dim3(256),
                       0, s, w.Zc, n, S, nb, w.tcount);
             PC_LAUNCH(pc::K_SD_SCAN, pc::sd_scan_kernel, dim3(1), dim3(pc::SCAN_THREADS), 0, s, w.tcount, nb,
                       w.tfirst);
+            PC_LAUNCH(pc::K_SD_TILES, pc::sd_tile_bucket_kernel, dim3((unsigned)((p.grid[i] + 255) / 256)),
+                      dim3(256), 0, s, w.tfirst, nb, p.grid[i], w.tile_bucket);
             PC_LAUNCH(pc::K_SD_COUNT, pc::sd_count_kernel<false>, dim3(grid), dim3(pc::DOM_THREADS), 0, s, src_t,
-                      n, w.Zc, p.s[i], p.k[i], w.tfirst, nb, w.cnt, w.seg);
+                      n, w.Zc, p.s[i], p.k[i], w.tfirst, nb, w.tile_bucket, w.cnt, w.seg);
         }
         const uint32_t *tend = i == 0 ? nullptr : w.tfirst + p.nbuckets[i];
         PC_LAUNCH(pc::K_SD_SEG, pc::sd_seg_reduce_kernel, dim3(groups), dim3(pc::DOM_RADIX), 0, s, w.cnt, w.seg,
@@ -708,10 +724,11 @@ pc_status pc_stack_distance(const uint32_t *prev, const uint32_t *next, uint64_t
         if (i == 0) {
             PC_LAUNCH(pc::K_SD_PASS, pc::sd_dominance_kernel<true>, dim3(grid), dim3(pc::DOM_THREADS), 0, s,
                       next, (const uint32_t *)nullptr, dt, da, n, w.Zc, p.s[i], p.k[i],
-                      (const uint32_t *)nullptr, (uint64_t)1, w.pre, w.hdr);
+                      (const uint32_t *)nullptr, (uint64_t)1, (const uint32_t *)nullptr, w.pre, w.hdr);
         } else {
             PC_LAUNCH(pc::K_SD_PASS, pc::sd_dominance_kernel<false>, dim3(grid), dim3(pc::DOM_THREADS), 0, s,
-                      src_t, src_a, dt, da, n, w.Zc, p.s[i], p.k[i], w.tfirst, p.nbuckets[i], w.pre, w.hdr);
+                      src_t, src_a, dt, da, n, w.Zc, p.s[i], p.k[i], w.tfirst, p.nbuckets[i], w.tile_bucket,
+                      w.pre, w.hdr);
         }
         src_t = dt;
         src_a = da;

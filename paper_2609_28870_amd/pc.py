@@ -285,6 +285,12 @@ class Pipeline:
         mrc_weighted(self.dist, self.caps, self.depth, self.next if self.with_nextuse else None,
                      self.alpha, self.beta, out=self.bins, ws=self.ws_mrc)
 
+    def high_key_passes_ran(self) -> bool:
+        """Whether the last prev/next call also sorted by the high 32 key
+        bits (decided on the device; see pc_prev_next_use).  Synchronises."""
+        torch.cuda.current_stream().synchronize()
+        return bool(int(self.ws_pn[4:8].view(torch.int32).item()))
+
     def status(self) -> dict:
         return {name: workspace_status(ws) for name, ws in
                 (("hash", self.ws_hash), ("prev_next", self.ws_pn), ("stack_distance", self.ws_sd),
