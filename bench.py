@@ -137,10 +137,11 @@ def main():
 
     ms_step = wall * 1e3 / args.steps
     value = n_blocks / (ms_step / 1e3)
-    # the four high-key sort passes exit at once unless the device check
+    # the four high-key sort passes exit at once unless the first link
     # asked for them; count only passes that moved data
     high = pipe.high_key_passes_ran()
-    work_launches = {"sort_onesweep_pass": 8 if high else 4}
+    work_launches = {"sort_onesweep_pass": 8 if high else 4, "link_partition": 2 if high else 1,
+                     "sort_digit_hist": 2 if high else 1}
     kernels = {}
     for name, (launches, ms) in prof.items():
         if launches == 0:
@@ -164,7 +165,7 @@ def main():
     roof["traffic"] = None
     stage_of = {"hash_digest": "hash", "hash_chain": "hash", "sort_digit_hist": "prev_next",
                 "sort_digit_scan": "prev_next", "sort_onesweep_pass": "prev_next",
-                "sort_mix_check": "prev_next", "link_partition": "prev_next",
+                "link_partition": "prev_next",
                 "perm_partition": "prev_next", "perm_local": "prev_next", "mrc_hist": "mrc",
                 "mrc_cost": "mrc"}
     stage_bytes = {"hash": 4 * B + 8 + 4, "prev_next": 16, "stack_distance": 8, "mrc": 12}

@@ -99,6 +99,10 @@ pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_
  * access); prev == PC_NONE marks a compulsory miss (Sec. 4.6).
  *
  *   keys  uint64[n]; prev, next uint32[n] outputs.
+ * Keys are grouped by their low 32 bits first; only when many different keys
+ * share those bits does the call also sort by the high 32 bits.  Once the
+ * stream has completed, 32-bit word 1 of the workspace tells which happened
+ * (1 = the high bits were sorted too); the outputs are the same either way.
  * ------------------------------------------------------------------------ */
 size_t pc_prev_next_use_ws(uint64_t n);
 pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uint32_t *next,

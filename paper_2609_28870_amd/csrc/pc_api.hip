@@ -7,10 +7,10 @@
 namespace pc {
 
 static const char *kKernelNames[K_COUNT] = {
-    "fill_u32",          "hash_digest",       "hash_chain",        "sort_digit_hist", "sort_digit_scan",
-    "sort_onesweep_pass", "sort_mix_check",    "link_partition",    "perm_partition",  "perm_local",    "sd_cold_count",   "sd_scan",
-    "sd_tile_map",       "sd_count",          "sd_seg_scan",     "sd_dominance_pass",  "sd_local_finish", "mrc_hist",
-    "mrc_cost"};
+    "fill_u32",         "hash_digest",   "hash_chain",      "sort_digit_hist",   "sort_digit_scan",
+    "sort_onesweep_pass", "link_partition", "perm_partition", "perm_local",        "sd_cold_count",
+    "sd_scan",          "sd_tile_map",   "sd_count",        "sd_seg_scan",       "sd_dominance_pass",
+    "sd_local_finish",  "mrc_hist",      "mrc_cost"};
 
 struct ProfEvent {
     int kid;

@@ -44,7 +44,6 @@ enum KernelId {
     K_SORT_HIST,
     K_SORT_SCAN,
     K_SORT_PASS,
-    K_SORT_CHECK,
     K_LINK,
     K_PERM,
     K_PERM_LOCAL,

@@ -9,11 +9,12 @@
 // ascending; neighbours in sorted order are exactly the (prev, next) links.
 // Keys are 64-bit hashes, so sorting by their low 32 bits already makes
 // equal keys contiguous except where different keys share those bits; the
-// link step resolves such short "mixed" runs by scanning them, and a device
-// check switches on the four passes over the high bits when a mixed run could
-// be long (then the full 64-bit sort makes equal keys adjacent).
-//   * one pass computes all eight 8-bit digit histograms (LDS-privatised,
-//     then global atomics), one workgroup scans them into digit bases;
+// link step resolves such short "mixed" runs by scanning them, and when a
+// run is too long to scan it flags the four passes over the high bits and a
+// second link (then the full 64-bit sort makes equal keys adjacent).
+//   * one pass computes the four 8-bit digit histograms of a group of
+//     passes (LDS-privatised, then global atomics), one workgroup scans them
+//     into digit bases;
 //   * each of the eight sort passes is a single "onesweep" kernel: a
 //     workgroup takes the next tile from an atomic counter (so every tile it
 //     waits on is already running), ranks its 4096 elements by digit with
@@ -39,45 +40,54 @@ constexpr uint64_t FLAG_AGG = 1ull << 32;
 constexpr uint64_t FLAG_INC = 1ull << 33;
 constexpr uint32_t SPIN_LIMIT = 1u << 22;
 
-__global__ __launch_bounds__(256) void sort_hist_kernel(const uint64_t *__restrict__ keys,
-                                                        uint64_t n, uint32_t *__restrict__ hist) {
-    __shared__ uint32_t h[SORT_PASSES][RADIX];
-    for (int i = threadIdx.x; i < SORT_PASSES * RADIX; i += blockDim.x) (&h[0][0])[i] = 0;
+// Histograms of the four byte digits p0 .. p0+3 (one group of passes) in one
+// read of the keys; the group over the high bytes runs only when asked.
+constexpr int HIST_DIGITS = SORT_PASSES / 2;
+__global__ __launch_bounds__(256) void sort_hist_kernel(const uint64_t *__restrict__ keys, uint64_t n, int p0,
+                                                        uint32_t *__restrict__ hist,
+                                                        const int32_t *__restrict__ only_if) {
+    if (only_if && *only_if == 0) return;
+    __shared__ uint32_t h[HIST_DIGITS][RADIX];
+    for (int i = threadIdx.x; i < HIST_DIGITS * RADIX; i += blockDim.x) (&h[0][0])[i] = 0;
     __syncthreads();
     const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
     for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-        const uint64_t k = keys[i];
+        const uint32_t k = (uint32_t)(keys[i] >> (8 * p0));
 #pragma unroll
-        for (int p = 0; p < SORT_PASSES; ++p) atomicAdd(&h[p][(k >> (8 * p)) & 0xFF], 1u);
+        for (int p = 0; p < HIST_DIGITS; ++p) atomicAdd(&h[p][(k >> (8 * p)) & 0xFF], 1u);
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < SORT_PASSES * RADIX; i += blockDim.x) {
+    for (int i = threadIdx.x; i < HIST_DIGITS * RADIX; i += blockDim.x) {
         const uint32_t v = (&h[0][0])[i];
-        if (v) atomicAdd(&hist[i], v);
+        if (v) atomicAdd(&hist[p0 * RADIX + i], v);
     }
 }
 
 // exclusive scan of each pass's 256-bin histogram -> digit bases
-__global__ __launch_bounds__(RADIX) void sort_scan_kernel(const uint32_t *__restrict__ hist,
-                                                          uint32_t *__restrict__ start) {
+__global__ __launch_bounds__(RADIX) void sort_scan_kernel(const uint32_t *__restrict__ hist, int p0,
+                                                          uint32_t *__restrict__ start,
+                                                          const int32_t *__restrict__ only_if) {
+    if (only_if && *only_if == 0) return;
     __shared__ uint32_t tmp[RADIX / WAVE];
-    for (int p = 0; p < SORT_PASSES; ++p) {
+    for (int p = p0; p < p0 + HIST_DIGITS; ++p) {
         uint32_t total;
         const uint32_t e = block_excl_scan(hist[p * RADIX + threadIdx.x], tmp, &total);
         start[p * RADIX + threadIdx.x] = e;
     }
 }
 
-__global__ __launch_bounds__(SORT_THREADS) void sort_pass_kernel(
+__global__ __launch_bounds__(SORT_THREADS, 8) void sort_pass_kernel(
     const uint64_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
     uint64_t *__restrict__ keys_out, uint32_t *__restrict__ vals_out, uint64_t n, int shift,
     const uint32_t *__restrict__ start, uint64_t *__restrict__ status, uint32_t *__restrict__ counter,
     uint32_t epoch, int32_t *__restrict__ err, const int32_t *__restrict__ only_if) {
     // passes over the high key bits run only when the link step needs them
     if (only_if && *only_if == 0) return;
-    __shared__ uint64_t s_key[SORT_TILE];
-    __shared__ uint32_t s_val[SORT_TILE];
-    __shared__ uint32_t s_wcnt[SORT_WAVES][RADIX];
+    // LDS is kept under 40 KB so four workgroups share a CU: the tile is
+    // staged twice through one buffer (keys, then values) and the per-wave
+    // digit counters are 16-bit (a tile holds at most 4096 elements)
+    __shared__ uint64_t s_stage[SORT_TILE];
+    __shared__ uint16_t s_wcnt[SORT_WAVES][RADIX];
     __shared__ uint32_t s_lstart[RADIX];
     __shared__ uint32_t s_gbase[RADIX];
     __shared__ uint32_t s_tmp[SORT_WAVES];
@@ -87,14 +97,14 @@ __global__ __launch_bounds__(SORT_THREADS) void sort_pass_kernel(
     const int lane = tid & (WAVE - 1);
     const int w = tid / WAVE;
     if (tid == 0) s_tile = atomicAdd(counter, 1u);
-    for (int i = tid; i < SORT_WAVES * RADIX; i += SORT_THREADS) (&s_wcnt[0][0])[i] = 0;
+    for (int i = tid; i < SORT_WAVES * RADIX / 2; i += SORT_THREADS) reinterpret_cast<uint32_t *>(&s_wcnt[0][0])[i] = 0;
     __syncthreads();
     const uint32_t tile = s_tile;
     const uint64_t base = (uint64_t)tile * SORT_TILE;
 
     uint64_t k[SORT_ITEMS];
     uint32_t v[SORT_ITEMS];
-    uint32_t rank[SORT_ITEMS];
+    uint32_t pos[SORT_ITEMS];
     bool ok[SORT_ITEMS];
 #pragma unroll
     for (int j = 0; j < SORT_ITEMS; ++j) {
@@ -118,15 +128,15 @@ __global__ __launch_bounds__(SORT_THREADS) void sort_pass_kernel(
         const uint32_t before = mbcnt(m);
         uint32_t cur = 0;
         if (ok[j]) cur = s_wcnt[w][d];
-        rank[j] = cur + before;
-        if (ok[j] && before == 0) s_wcnt[w][d] = cur + (uint32_t)__popcll(m);
+        pos[j] = cur + before;
+        if (ok[j] && before == 0) s_wcnt[w][d] = (uint16_t)(cur + (uint32_t)__popcll(m));
     }
     __syncthreads();
     uint32_t cnt = 0;
     if (tid < RADIX) {
         for (int x = 0; x < SORT_WAVES; ++x) {
             const uint32_t c = s_wcnt[x][tid];
-            s_wcnt[x][tid] = cnt;
+            s_wcnt[x][tid] = (uint16_t)cnt;
             cnt += c;
         }
     }
@@ -138,9 +148,8 @@ __global__ __launch_bounds__(SORT_THREADS) void sort_pass_kernel(
     for (int j = 0; j < SORT_ITEMS; ++j) {
         if (ok[j]) {
             const uint32_t d = (uint32_t)(k[j] >> shift) & 0xFF;
-            const uint32_t pos = s_lstart[d] + s_wcnt[w][d] + rank[j];
-            s_key[pos] = k[j];
-            s_val[pos] = v[j];
+            pos[j] += s_lstart[d] + s_wcnt[w][d];
+            s_stage[pos[j]] = k[j];
         }
     }
     // decoupled look-back over the per-digit counts of earlier tiles
@@ -175,12 +184,28 @@ __global__ __launch_bounds__(SORT_THREADS) void sort_pass_kernel(
     __syncthreads();
     const uint64_t left = n - base;
     const uint32_t n_tile = left < (uint64_t)SORT_TILE ? (uint32_t)left : (uint32_t)SORT_TILE;
-    for (uint32_t i = tid; i < n_tile; i += SORT_THREADS) {
-        const uint64_t kk = s_key[i];
-        const uint32_t d = (uint32_t)(kk >> shift) & 0xFF;
-        const uint32_t dst = s_gbase[d] + i;
-        keys_out[dst] = kk;
-        vals_out[dst] = s_val[i];
+    // keys out, remembering each slot's destination for the values
+    uint32_t dst[SORT_ITEMS];
+#pragma unroll
+    for (int r = 0; r < SORT_ITEMS; ++r) {
+        const uint32_t i = (uint32_t)(tid + r * SORT_THREADS);
+        dst[r] = 0;
+        if (i < n_tile) {
+            const uint64_t kk = s_stage[i];
+            dst[r] = s_gbase[(uint32_t)(kk >> shift) & 0xFF] + i;
+            keys_out[dst[r]] = kk;
+        }
+    }
+    __syncthreads();
+    uint32_t *s_val = reinterpret_cast<uint32_t *>(s_stage);
+#pragma unroll
+    for (int j = 0; j < SORT_ITEMS; ++j)
+        if (ok[j]) s_val[pos[j]] = v[j];
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < SORT_ITEMS; ++r) {
+        const uint32_t i = (uint32_t)(tid + r * SORT_THREADS);
+        if (i < n_tile) vals_out[dst[r]] = s_val[i];
     }
 }
 
@@ -204,25 +229,25 @@ constexpr int PERM_LOCAL_BITS = 12;
 // accesses for 64-bit hashes).  The link step resolves them by scanning the
 // run: an element inside a block of equal keys finds its neighbour in one
 // step, while a block boundary scans back (or forward) to the previous (next)
-// block of its key or the run's end.  This check bounds the total of those
-// boundary scans from above (short runs are charged their probe length,
-// long ones are scanned); when the total exceeds a budget (adversarial keys:
-// many keys sharing low bits) it switches on the four passes over the high
-// bits, after which equal keys are adjacent and every scan is one step.
+// block of its key or the run's end.  The scans of a workgroup share a budget
+// of twice its element count; running out of it (adversarial keys: many keys
+// sharing low bits) raises a flag that switches on the four passes over the
+// high bits and a second link over the fully sorted keys, where equal keys
+// are adjacent and no scan is needed.
 __device__ __forceinline__ bool same_low(uint64_t a, uint64_t b) { return (uint32_t)a == (uint32_t)b; }
 
 // Scan from position `from` (inclusive) in direction dir (-1 / +1) over
 // elements sharing k's low bits; stop at k (found), at the run's end, or
 // after `limit` steps.  Keys are read 8 at a time so a long scan costs one
-// memory latency per 8 elements.  Returns the number of elements examined;
-// *hit = position of k or UINT64_MAX.
+// memory latency per 8 elements.  Returns false when the limit was reached
+// first; *hit = position of k or UINT64_MAX.
 constexpr int SCAN_BATCH = 8;
-__device__ __forceinline__ uint64_t scan_run(const uint64_t *__restrict__ sk, uint64_t n, uint64_t k,
-                                             uint64_t from, int dir, uint64_t limit, uint64_t *hit) {
-    uint64_t steps = 0;
+constexpr uint32_t LINK_SCAN_LIMIT = 64;   // memory steps a lane takes alone
+__device__ __forceinline__ bool scan_run(const uint64_t *__restrict__ sk, uint64_t n, uint64_t k, uint64_t from,
+                                         int dir, uint32_t limit, uint64_t *hit) {
     *hit = ~0ull;
     int64_t j = (int64_t)from;
-    while (steps < limit) {
+    for (uint32_t steps = 0; steps < limit; steps += SCAN_BATCH) {
         uint64_t kb[SCAN_BATCH];
 #pragma unroll
         for (int q = 0; q < SCAN_BATCH; ++q) {
@@ -231,69 +256,15 @@ __device__ __forceinline__ uint64_t scan_run(const uint64_t *__restrict__ sk, ui
         }
 #pragma unroll
         for (int q = 0; q < SCAN_BATCH; ++q) {
-            ++steps;
             if (kb[q] == k) {
                 *hit = (uint64_t)(j + dir * q);
-                return steps;
+                return true;
             }
-            if (!same_low(kb[q], k)) return steps;
+            if (!same_low(kb[q], k)) return true;
         }
         j += dir * SCAN_BATCH;
     }
-    return steps;
-}
-
-__global__ __launch_bounds__(256) void sort_mix_check_kernel(const uint64_t *__restrict__ sk, uint64_t n,
-                                                             uint64_t budget,
-                                                             unsigned long long *__restrict__ work,
-                                                             int32_t *__restrict__ need_high) {
-    __shared__ uint32_t s_tmp[256 / WAVE];
-    // When the run ends within PROBE positions (one probe load), charge PROBE
-    // without scanning: the total stays an upper bound.
-    constexpr uint64_t PROBE = 32;
-    uint64_t cost = 0;
-    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n && cost <= budget; i += stride) {
-        const uint64_t k = sk[i];
-        uint64_t hit;
-        if (i > 0) {
-            const uint64_t kp = sk[i - 1];
-            if (same_low(kp, k) && kp != k) {
-                if (i < PROBE || !same_low(sk[i - PROBE], k)) cost += PROBE;
-                else cost += scan_run(sk, n, k, i - 1, -1, budget + 1, &hit);
-            }
-        }
-        if (i + 1 < n) {
-            const uint64_t kn = sk[i + 1];
-            if (same_low(kn, k) && kn != k) {
-                if (i + PROBE >= n || !same_low(sk[i + PROBE], k)) cost += PROBE;
-                else cost += scan_run(sk, n, k, i + 1, +1, budget + 1, &hit);
-            }
-        }
-    }
-    // one atomic per workgroup
-    const uint32_t c32 = cost > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)cost;
-    uint32_t total32;
-    block_excl_scan(c32, s_tmp, &total32);
-    if (threadIdx.x == 0 && total32) {
-        const uint64_t total = atomicAdd(work, (unsigned long long)total32) + total32;
-        if (total > budget || total32 == 0xFFFFFFFFu) atomicOr(need_high, 1);
-    }
-}
-
-// previous / next element with the same full key inside a mixed run (total
-// work bounded by the check above)
-__device__ __forceinline__ void link_prev(const uint64_t *__restrict__ sk, const uint32_t *__restrict__ sv,
-                                          uint64_t n, uint64_t i, uint32_t &p) {
-    uint64_t hit;
-    scan_run(sk, n, sk[i], i - 1, -1, ~0ull, &hit);
-    p = hit != ~0ull ? sv[hit] : NONE;
-}
-__device__ __forceinline__ void link_next(const uint64_t *__restrict__ sk, const uint32_t *__restrict__ sv,
-                                          uint64_t n, uint64_t i, uint32_t &q) {
-    uint64_t hit;
-    scan_run(sk, n, sk[i], i + 1, +1, ~0ull, &hit);
-    q = hit != ~0ull ? sv[hit] : NONE;
+    return false;
 }
 
 __device__ __forceinline__ uint64_t shfl_up64(uint64_t v) {
@@ -306,48 +277,145 @@ __device__ __forceinline__ uint64_t shfl_down64(uint64_t v) {
     const uint32_t hi = (uint32_t)__shfl_down((int)(uint32_t)(v >> 32), 1, WAVE);
     return (uint64_t)lo | ((uint64_t)hi << 32);
 }
+__device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
+    const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src, WAVE);
+    const uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(v >> 32), src, WAVE);
+    return (uint64_t)lo | ((uint64_t)hi << 32);
+}
+
+// Previous (DIR = -1) or next (DIR = +1) element with the same full key for
+// lanes whose adjacent element shares the low key bits but not the key.  The
+// wave's valid lanes [0, last] hold consecutive sorted positions, so the
+// search first walks them with shuffles (all lanes of the wave together, no
+// memory latency); a lane that runs past the wave's edge continues in memory
+// for a few batches on its own, and a lane still unresolved after that (a
+// long run, e.g. a hot key sharing its low bits with another key) is taken
+// over by the whole wave, 64 positions per step.  Those wave steps are
+// charged to the workgroup's budget (*budget, in positions); when it runs
+// out the lane gives up and *overflow is raised, which switches on the
+// passes over the high key bits and a second link.
+template <int DIR>
+__device__ __forceinline__ uint32_t mixed_neighbour(const uint64_t *__restrict__ sk,
+                                                    const uint32_t *__restrict__ st, uint64_t n,
+                                                    uint64_t i, uint64_t k, uint32_t t, bool need,
+                                                    uint32_t res, int lane, int last, int32_t *budget,
+                                                    int32_t *__restrict__ overflow) {
+    for (int d = 2;; ++d) {
+        const int src = lane + DIR * d;
+        const bool inwave = src >= 0 && src <= last;
+        const bool active = need && inwave;
+        if (ballot(active) == 0) break;
+        const int from = inwave ? src : lane;
+        const uint64_t kk = shfl64(k, from);
+        const uint32_t tt = (uint32_t)__shfl((int)t, from, WAVE);
+        if (active) {
+            if (kk == k) {
+                res = tt;
+                need = false;
+            } else if (!same_low(kk, k)) {
+                res = NONE;
+                need = false;
+            }
+        }
+    }
+    int64_t cont = 0;
+    if (need) {
+        // positions i+DIR .. i+DIR*e were examined inside the wave
+        const int e = DIR < 0 ? (lane > 1 ? lane : 1) : (last - lane > 1 ? last - lane : 1);
+        const int64_t from = (int64_t)i + DIR * (e + 1);
+        res = NONE;
+        need = false;
+        if (from >= 0 && (uint64_t)from < n) {
+            uint64_t hit;
+            if (scan_run(sk, n, k, (uint64_t)from, DIR, LINK_SCAN_LIMIT, &hit)) {
+                if (hit != ~0ull) res = st[hit];
+            } else {
+                need = true;
+                cont = from + DIR * (int64_t)LINK_SCAN_LIMIT;
+            }
+        }
+    }
+    for (uint64_t pending = ballot(need); pending; pending &= pending - 1) {
+        const int L = __builtin_ctzll(pending);
+        const uint64_t kL = shfl64(k, L);
+        int64_t pos = (int64_t)shfl64((uint64_t)cont, L);
+        uint32_t found = NONE;
+        for (;;) {
+            int32_t left = 0;
+            if (lane == 0) left = atomicAdd(budget, -WAVE);
+            left = __shfl(left, 0, WAVE);
+            if (left < WAVE) {
+                if (lane == 0) atomicOr(overflow, 1);
+                break;
+            }
+            const int64_t x = pos + DIR * lane;
+            const uint64_t kk = (x >= 0 && (uint64_t)x < n) ? sk[x] : ~kL;
+            const uint64_t hitm = ballot(kk == kL);
+            const uint64_t ev = hitm | ballot(!same_low(kk, kL));
+            if (ev) {
+                const int f = __builtin_ctzll(ev);
+                if ((hitm >> f) & 1) found = st[pos + DIR * f];
+                break;
+            }
+            pos += DIR * WAVE;
+        }
+        if (lane == L) res = found;
+    }
+    return res;
+}
 
 // One workgroup owns a contiguous chunk of the input.  It first counts the
 // chunk's digits, reserves one run per digit in the bucket's output range with
 // a single global atomic (so each bucket cursor sees one atomic per workgroup,
 // not per tile), then streams the chunk tile by tile: LDS counters give each
-// element its slot inside its digit, the tile is staged digit-sorted in LDS,
-// and each digit's part is appended to the workgroup's run.  A chunk spans at
-// most 1024 consecutive buckets (see the plan), so digit = bucket mod 1024
-// names them without collision.
+// element its slot inside its digit, the tile is staged digit-sorted in LDS
+// (one array at a time through a single buffer, which keeps LDS at 32 KB so
+// four workgroups share a CU), and each digit's part is appended to the
+// workgroup's run.  A chunk spans at most 1024 consecutive buckets (see the
+// plan), so digit = bucket mod 1024 names them without collision.
+struct PermLds {
+    uint32_t stage[PERM_TILE];
+    uint32_t cnt[PERM_RADIX];
+    uint32_t lstart[PERM_RADIX];
+    uint32_t cur[PERM_RADIX];
+    uint32_t bucket[PERM_RADIX];
+    uint32_t tmp[PERM_THREADS / WAVE];
+    int32_t budget;   // positions the link may still scan for long mixed runs
+};
+
 template <bool FROM_SORT>
-__global__ __launch_bounds__(PERM_THREADS) void perm_partition_kernel(
-    const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t,
+__device__ __forceinline__ void perm_partition_body(
+    PermLds &L, const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t,
     const uint32_t *__restrict__ in_p, const uint32_t *__restrict__ in_n, uint64_t n, int s,
     uint64_t per_wg, uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t,
-    uint32_t *__restrict__ out_p, uint32_t *__restrict__ out_n, const int32_t *__restrict__ need_high) {
-    __shared__ uint32_t s_t[PERM_TILE], s_p[PERM_TILE], s_n[PERM_TILE];
-    __shared__ uint32_t s_cnt[PERM_RADIX];
-    __shared__ uint32_t s_lstart[PERM_RADIX];
-    __shared__ uint32_t s_cur[PERM_RADIX];
-    __shared__ uint32_t s_bucket[PERM_RADIX];
-    __shared__ uint32_t s_tmp[PERM_THREADS / WAVE];
+    uint32_t *__restrict__ out_p, uint32_t *__restrict__ out_n, bool full, int32_t *__restrict__ overflow) {
+    uint32_t *s_stage = L.stage, *s_cnt = L.cnt, *s_lstart = L.lstart, *s_cur = L.cur, *s_bucket = L.bucket,
+             *s_tmp = L.tmp;
     constexpr int DPT = PERM_RADIX / PERM_THREADS;   // digits per thread
     const int tid = threadIdx.x;
-    const uint64_t lo = (uint64_t)blockIdx.x * per_wg;
-    if (lo >= n) return;
-    const uint64_t hi = lo + per_wg < n ? lo + per_wg : n;
-    const bool full = FROM_SORT && need_high && *need_high != 0;
+    const int lane = tid & (WAVE - 1);
+    // positions fit 32 bits (n < 2^32 - 1); offsets from a tile's base are
+    // compared against what is left, so nothing wraps near the end
+    if ((uint64_t)blockIdx.x * per_wg >= n) return;
+    const uint32_t lo = (uint32_t)((uint64_t)blockIdx.x * per_wg);
+    const uint32_t hi = (uint64_t)lo + per_wg < n ? (uint32_t)(lo + per_wg) : (uint32_t)n;
 
     // ---- count the chunk's digits and reserve one run per digit
     for (int i = tid; i < PERM_RADIX; i += PERM_THREADS) s_cnt[i] = 0;
+    if (tid == 0) L.budget = (int32_t)(2 * (hi - lo) + 4096);
     __syncthreads();
     // eight loads in flight per thread before their LDS updates
-    for (uint64_t i0 = lo + tid; i0 < hi; i0 += 8 * PERM_THREADS) {
+    for (uint32_t b0 = lo; b0 < hi; b0 += 8 * PERM_THREADS) {
+        const uint32_t left = hi - b0;
         uint32_t tt[8];
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            const uint64_t i = i0 + (uint64_t)q * PERM_THREADS;
-            tt[q] = i < hi ? in_t[i] : 0u;
+            const uint32_t o = (uint32_t)(q * PERM_THREADS + tid);
+            tt[q] = o < left ? (in_t + b0)[o] : 0u;
         }
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            if (i0 + (uint64_t)q * PERM_THREADS < hi) {
+            if ((uint32_t)(q * PERM_THREADS + tid) < left) {
                 const uint32_t d = (tt[q] >> s) & (PERM_RADIX - 1);
                 atomicAdd(&s_cnt[d], 1u);
                 s_bucket[d] = tt[q] >> s;   // every writer of digit d writes the same bucket
@@ -364,40 +432,92 @@ __global__ __launch_bounds__(PERM_THREADS) void perm_partition_kernel(
     __syncthreads();
 
     // ---- stream the chunk tile by tile
-    for (uint64_t base = lo; base < hi; base += PERM_TILE) {
+    for (uint32_t base = lo; base < hi; base += PERM_TILE) {
+        const uint32_t left = hi - base;
         for (int i = tid; i < PERM_RADIX; i += PERM_THREADS) s_cnt[i] = 0;
         __syncthreads();
-        uint32_t t[PERM_ITEMS], pv[PERM_ITEMS], nx[PERM_ITEMS], off[PERM_ITEMS];
+        // per-tile base pointers keep the per-lane offsets 32-bit.  Every
+        // load of the tile is issued before the first use, so a tile costs
+        // one memory latency, not one per item.
+        const uint32_t *tb = in_t + base;
+        uint32_t t[PERM_ITEMS], pv[PERM_ITEMS], nx[PERM_ITEMS], pos[PERM_ITEMS];
         bool ok[PERM_ITEMS];
+        if (FROM_SORT) {
+            const uint64_t *kb = sk + base;
+            const int w = tid / WAVE;
+            uint64_t k[PERM_ITEMS];
 #pragma unroll
-        for (int j = 0; j < PERM_ITEMS; ++j) {
-            const uint64_t i = base + (uint64_t)j * PERM_THREADS + tid;
-            ok[j] = i < hi;
-            if (!ok[j]) continue;
-            t[j] = in_t[i];
-            if (FROM_SORT) {
+            for (int j = 0; j < PERM_ITEMS; ++j) {
+                const uint32_t o = (uint32_t)(j * PERM_THREADS + tid);
+                ok[j] = o < left;
+                const uint32_t oc = ok[j] ? o : 0u;
+                t[j] = tb[oc];
+                k[j] = kb[oc];
+            }
+            // the elements just outside each item's wave: lane j loads the
+            // one before item j's first lane, lane 8 + j the one after its
+            // last valid lane
+            uint64_t ek = 0;
+            uint32_t et = 0;
+            {
+                const int j = lane & 7;
+                const uint32_t w0 = (uint32_t)(j * PERM_THREADS + w * WAVE);   // wave's first offset
+                const uint32_t lastj = w0 < left ? (left - 1 - w0 < (uint32_t)(WAVE - 1) ? left - 1 - w0 : WAVE - 1) : 0u;
+                const uint64_t gp = lane < 8 ? (uint64_t)base + w0 - 1 : (uint64_t)base + w0 + lastj + 1;
+                const bool want = lane < 16 && w0 < left && (lane < 8 ? (uint64_t)base + w0 > 0 : gp < n);
+                if (want) {
+                    ek = sk[gp];
+                    et = in_t[gp];
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < PERM_ITEMS; ++j) {
+                const uint32_t o = (uint32_t)(j * PERM_THREADS + tid);
+                const uint64_t i = (uint64_t)base + o;
                 // consecutive lanes hold consecutive sorted positions: the
                 // neighbours' keys and times come from the adjacent lanes
-                // (the wave's first and last lanes load theirs)
-                const uint64_t k = sk[i];
-                const int lane = tid & (WAVE - 1);
-                uint64_t kp = shfl_up64(k), kn = shfl_down64(k);
+                const uint32_t w0 = o - (uint32_t)lane;
+                const int last = w0 < left ? (int)(left - 1 - w0 < (uint32_t)(WAVE - 1) ? left - 1 - w0 : WAVE - 1)
+                                           : -1;
+                uint64_t kp = shfl_up64(k[j]), kn = shfl_down64(k[j]);
                 uint32_t tp = (uint32_t)__shfl_up((int)t[j], 1, WAVE);
                 uint32_t tn = (uint32_t)__shfl_down((int)t[j], 1, WAVE);
-                if (lane == 0 && i > 0) { kp = sk[i - 1]; tp = in_t[i - 1]; }
-                if ((lane == WAVE - 1 || i + 1 >= hi) && i + 1 < n) { kn = sk[i + 1]; tn = in_t[i + 1]; }
-                if (i > 0 && kp == k) pv[j] = tp;
-                else if (i > 0 && !full && same_low(kp, k)) link_prev(sk, in_t, n, i, pv[j]);
-                else pv[j] = NONE;
-                if (i + 1 < n && kn == k) nx[j] = tn;
-                else if (i + 1 < n && !full && same_low(kn, k)) link_next(sk, in_t, n, i, nx[j]);
-                else nx[j] = NONE;
-            } else {
-                pv[j] = in_p[i];
-                nx[j] = in_n[i];
+                const uint64_t ekp = shfl64(ek, j), ekn = shfl64(ek, 8 + j);
+                const uint32_t etp = (uint32_t)__shfl((int)et, j, WAVE);
+                const uint32_t etn = (uint32_t)__shfl((int)et, 8 + j, WAVE);
+                bool mp = false, mn = false;
+                pv[j] = NONE;
+                nx[j] = NONE;
+                if (ok[j]) {
+                    const bool has_next = i + 1 < n;
+                    if (lane == 0) { kp = ekp; tp = etp; }
+                    if (lane == last) { kn = ekn; tn = etn; }
+                    if (i > 0 && kp == k[j]) pv[j] = tp;
+                    else mp = i > 0 && !full && same_low(kp, k[j]);
+                    if (has_next && kn == k[j]) nx[j] = tn;
+                    else mn = has_next && !full && same_low(kn, k[j]);
+                }
+                if (ballot(mp))
+                    pv[j] = mixed_neighbour<-1>(sk, in_t, n, i, k[j], t[j], mp, pv[j], lane, last, &L.budget,
+                                                overflow);
+                if (ballot(mn))
+                    nx[j] = mixed_neighbour<+1>(sk, in_t, n, i, k[j], t[j], mn, nx[j], lane, last, &L.budget,
+                                                overflow);
             }
-            off[j] = atomicAdd(&s_cnt[(t[j] >> s) & (PERM_RADIX - 1)], 1u);
+        } else {
+#pragma unroll
+            for (int j = 0; j < PERM_ITEMS; ++j) {
+                const uint32_t o = (uint32_t)(j * PERM_THREADS + tid);
+                ok[j] = o < left;
+                const uint32_t oc = ok[j] ? o : 0u;
+                t[j] = tb[oc];
+                pv[j] = (in_p + base)[oc];
+                nx[j] = (in_n + base)[oc];
+            }
         }
+#pragma unroll
+        for (int j = 0; j < PERM_ITEMS; ++j)
+            if (ok[j]) pos[j] = atomicAdd(&s_cnt[(t[j] >> s) & (PERM_RADIX - 1)], 1u);
         __syncthreads();
         uint32_t c[DPT], mine = 0, total;
 #pragma unroll
@@ -415,27 +535,67 @@ __global__ __launch_bounds__(PERM_THREADS) void perm_partition_kernel(
 #pragma unroll
         for (int j = 0; j < PERM_ITEMS; ++j) {
             if (!ok[j]) continue;
-            const uint32_t pos = s_lstart[(t[j] >> s) & (PERM_RADIX - 1)] + off[j];
-            s_t[pos] = t[j];
-            s_p[pos] = pv[j];
-            s_n[pos] = nx[j];
+            pos[j] += s_lstart[(t[j] >> s) & (PERM_RADIX - 1)];
+            s_stage[pos[j]] = t[j];
         }
         __syncthreads();
-        for (uint32_t j = tid; j < total; j += PERM_THREADS) {
-            const uint32_t tt = s_t[j];
-            const uint32_t d = (tt >> s) & (PERM_RADIX - 1);
-            const uint32_t dst = s_cur[d] + (j - s_lstart[d]);
-            if (dst < n) {
-                out_t[dst] = tt;
-                out_p[dst] = s_p[j];
-                out_n[dst] = s_n[j];
+        // times out, remembering each slot's destination for prev and next
+        uint32_t dst[PERM_ITEMS];
+#pragma unroll
+        for (int r = 0; r < PERM_ITEMS; ++r) {
+            const uint32_t slot = (uint32_t)(tid + r * PERM_THREADS);
+            dst[r] = ~0u;
+            if (slot < total) {
+                const uint32_t tt = s_stage[slot];
+                const uint32_t d = (tt >> s) & (PERM_RADIX - 1);
+                dst[r] = s_cur[d] + (slot - s_lstart[d]);
+                if (dst[r] < n) out_t[dst[r]] = tt;
             }
         }
         __syncthreads();
 #pragma unroll
+        for (int j = 0; j < PERM_ITEMS; ++j)
+            if (ok[j]) s_stage[pos[j]] = pv[j];
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < PERM_ITEMS; ++r)
+            if (dst[r] < n) out_p[dst[r]] = s_stage[tid + r * PERM_THREADS];
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < PERM_ITEMS; ++j)
+            if (ok[j]) s_stage[pos[j]] = nx[j];
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < PERM_ITEMS; ++r)
+            if (dst[r] < n) out_n[dst[r]] = s_stage[tid + r * PERM_THREADS];
+#pragma unroll
         for (int q = 0; q < DPT; ++q) s_cur[tid * DPT + q] += c[q];
         __syncthreads();
     }
+}
+
+// The link variant holds more state per element (keys and neighbours), so it
+// runs two workgroups per CU; the plain partition runs three.  The first link
+// (over keys sorted by their low 32 bits) raises *flag when a mixed run is too
+// long to scan; the second one runs only then (only_if = flag), over fully
+// sorted keys.
+__global__ __launch_bounds__(PERM_THREADS, 4) void link_partition_kernel(
+    const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t, uint64_t n, int s, uint64_t per_wg,
+    uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t, uint32_t *__restrict__ out_p,
+    uint32_t *__restrict__ out_n, const int32_t *__restrict__ only_if, int32_t *__restrict__ flag) {
+    if (only_if && *only_if == 0) return;
+    __shared__ PermLds L;
+    perm_partition_body<true>(L, sk, in_t, nullptr, nullptr, n, s, per_wg, cursor, out_t, out_p, out_n,
+                              only_if != nullptr, flag);
+}
+
+__global__ __launch_bounds__(PERM_THREADS, 6) void perm_partition_kernel(
+    const uint32_t *__restrict__ in_t, const uint32_t *__restrict__ in_p, const uint32_t *__restrict__ in_n,
+    uint64_t n, int s, uint64_t per_wg, uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t,
+    uint32_t *__restrict__ out_p, uint32_t *__restrict__ out_n) {
+    __shared__ PermLds L;
+    perm_partition_body<false>(L, nullptr, in_t, in_p, in_n, n, s, per_wg, cursor, out_t, out_p, out_n,
+                               true, nullptr);
 }
 
 // cursor[b] = b << s: each bucket's output run starts at its first t
@@ -562,35 +722,20 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
     const int cus = pc::device_cus();
     uint64_t hg = (n + 4095) / 4096;
     if (hg > (uint64_t)cus * 4) hg = (uint64_t)cus * 4;
-    PC_LAUNCH(pc::K_SORT_HIST, pc::sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n, w.hist);
-    PC_LAUNCH(pc::K_SORT_SCAN, pc::sort_scan_kernel, dim3(1), dim3(pc::RADIX), 0, s, w.hist, w.start);
-
-    // passes 0-3 sort by the low 32 key bits; passes 4-7 run only if the
-    // check finds a long mixed run (flag in header word 1)
+    // flag (header word 1): the first link met a mixed run too long to scan,
+    // so the high-byte passes and a second link run
     int32_t *need_high = w.hdr + 1;
-    unsigned long long *mix_work = reinterpret_cast<unsigned long long *>(w.hdr + 2);
-    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(w.hdr + 1), 0u, 3, s)) != PC_OK) return st;
-    const uint64_t *kin = keys;
-    const uint32_t *vin = nullptr;
-    for (int p = 0; p < pc::SORT_PASSES; ++p) {
-        if (p == pc::SORT_PASSES / 2) {
-            uint64_t cg = (n + 255) / 256;
-            if (cg > (uint64_t)cus * 8) cg = (uint64_t)cus * 8;
-            PC_LAUNCH(pc::K_SORT_CHECK, pc::sort_mix_check_kernel, dim3((unsigned)cg), dim3(256), 0, s, kin, n,
-                      (uint64_t)2 * n + 4096, mix_work, need_high);
-        }
-        uint64_t *kout = (p & 1) ? w.k2 : w.k1;
-        uint32_t *vout = (p & 1) ? w.v2 : w.v1;
-        PC_LAUNCH(pc::K_SORT_PASS, pc::sort_pass_kernel, dim3((unsigned)tiles), dim3(pc::SORT_THREADS), 0, s,
-                  kin, vin, kout, vout, n, 8 * p, w.start + p * pc::RADIX, w.status, w.counters + p,
-                  (uint32_t)(p + 1), w.hdr, p >= pc::SORT_PASSES / 2 ? (const int32_t *)need_high : nullptr);
-        kin = kout;
-        vin = vout;
-    }
-    // links + partition back to time order.  The sort left (key, t) in
-    // (k2, v2); triples (t, prev, next) ping-pong between the first sort
-    // buffers (k1 viewed as two u32 arrays, v1) and, once the sorted keys
-    // have been consumed, the second ones (k2 as two u32 arrays, v2).
+    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(need_high), 0u, 1, s)) != PC_OK) return st;
+    PC_LAUNCH(pc::K_SORT_HIST, pc::sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n, 0, w.hist,
+              (const int32_t *)nullptr);
+    PC_LAUNCH(pc::K_SORT_SCAN, pc::sort_scan_kernel, dim3(1), dim3(pc::RADIX), 0, s, w.hist, 0, w.start,
+              (const int32_t *)nullptr);
+
+    // Links + partition back to time order.  The sort leaves (key, t) in
+    // (k2, v2) after four passes and again after eight; triples (t, prev,
+    // next) ping-pong between the first sort buffers (k1 viewed as two u32
+    // arrays, v1) and, once the sorted keys have been consumed, the second
+    // ones (k2 as two u32 arrays, v2).
     const pc::PermPlan pp = pc::plan_perm(n);
     uint32_t *bt[2] = {reinterpret_cast<uint32_t *>(w.k1), reinterpret_cast<uint32_t *>(w.k2)};
     uint32_t *bp[2] = {bt[0] + n, bt[1] + n};
@@ -603,23 +748,43 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
     if (per_wg > (1ull << 20)) per_wg = 1ull << 20;
     if (per_wg < (uint64_t)pc::PERM_TILE) per_wg = pc::PERM_TILE;
     const unsigned ptiles = (unsigned)((n + per_wg - 1) / per_wg);
+    const unsigned cg0 = (unsigned)((pp.buckets[0] + 255) / 256);
+
+    const uint64_t *kin = keys;
+    const uint32_t *vin = nullptr;
+    for (int p = 0; p < pc::SORT_PASSES; ++p) {
+        if (p == pc::SORT_PASSES / 2) {
+            // first link, over keys sorted by their low 32 bits
+            PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg0), dim3(256), 0, s, w.cursor, pp.buckets[0],
+                      pp.s[0]);
+            PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ptiles), dim3(pc::PERM_THREADS), 0, s, kin, vin,
+                      n, pp.s[0], per_wg, w.cursor, bt[0], bp[0], bn[0], (const int32_t *)nullptr, need_high);
+            PC_LAUNCH(pc::K_SORT_HIST, pc::sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n,
+                      pc::SORT_PASSES / 2, w.hist, (const int32_t *)need_high);
+            PC_LAUNCH(pc::K_SORT_SCAN, pc::sort_scan_kernel, dim3(1), dim3(pc::RADIX), 0, s, w.hist,
+                      pc::SORT_PASSES / 2, w.start, (const int32_t *)need_high);
+        }
+        uint64_t *kout = (p & 1) ? w.k2 : w.k1;
+        uint32_t *vout = (p & 1) ? w.v2 : w.v1;
+        PC_LAUNCH(pc::K_SORT_PASS, pc::sort_pass_kernel, dim3((unsigned)tiles), dim3(pc::SORT_THREADS), 0, s,
+                  kin, vin, kout, vout, n, 8 * p, w.start + p * pc::RADIX, w.status, w.counters + p,
+                  (uint32_t)(p + 1), w.hdr, p >= pc::SORT_PASSES / 2 ? (const int32_t *)need_high : nullptr);
+        kin = kout;
+        vin = vout;
+    }
+    // second link, over fully sorted keys, only if the first one gave up
+    PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg0), dim3(256), 0, s, w.cursor, pp.buckets[0], pp.s[0]);
+    PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ptiles), dim3(pc::PERM_THREADS), 0, s, kin, vin, n,
+              pp.s[0], per_wg, w.cursor, bt[0], bp[0], bn[0], (const int32_t *)need_high, (int32_t *)nullptr);
     int cur = 0;
-    for (int i = 0; i < pp.passes; ++i) {
+    for (int i = 1; i < pp.passes; ++i) {
         const unsigned cg = (unsigned)((pp.buckets[i] + 255) / 256);
         PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg), dim3(256), 0, s, w.cursor, pp.buckets[i],
                   pp.s[i]);
-        if (i == 0) {
-            PC_LAUNCH(pc::K_LINK, pc::perm_partition_kernel<true>, dim3(ptiles), dim3(pc::PERM_THREADS), 0, s,
-                      kin, vin, (const uint32_t *)nullptr, (const uint32_t *)nullptr, n, pp.s[i], per_wg,
-                      w.cursor, bt[0], bp[0], bn[0], (const int32_t *)need_high);
-            cur = 0;
-        } else {
-            const int nxt = cur ^ 1;
-            PC_LAUNCH(pc::K_PERM, pc::perm_partition_kernel<false>, dim3(ptiles), dim3(pc::PERM_THREADS), 0,
-                      s, (const uint64_t *)nullptr, bt[cur], bp[cur], bn[cur], n, pp.s[i], per_wg,
-                      w.cursor, bt[nxt], bp[nxt], bn[nxt], (const int32_t *)nullptr);
-            cur = nxt;
-        }
+        const int nxt = cur ^ 1;
+        PC_LAUNCH(pc::K_PERM, pc::perm_partition_kernel, dim3(ptiles), dim3(pc::PERM_THREADS), 0, s, bt[cur],
+                  bp[cur], bn[cur], n, pp.s[i], per_wg, w.cursor, bt[nxt], bp[nxt], bn[nxt]);
+        cur = nxt;
     }
     PC_LAUNCH(pc::K_PERM_LOCAL, pc::perm_local_kernel, dim3((unsigned)((n + 4095) / 4096)), dim3(256), 0, s,
               bt[cur], bp[cur], bn[cur], n, prev, next);

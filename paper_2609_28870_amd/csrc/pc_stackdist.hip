@@ -199,30 +199,36 @@ __device__ __forceinline__ void chunk_masks(bool ok, uint32_t d, int lane, uint6
 }
 
 // Per-tile digit counts (and whether the tile starts a bucket), the input of
-// the segmented scan over tiles.
+// the segmented scan over tiles.  Only counts are needed here, so instead of
+// ranking lanes each run of equal digits in a 64-lane chunk (runs are long at
+// the top levels, where t grows with v) adds its length with one LDS atomic.
 template <bool FIRST>
 __global__ __launch_bounds__(DOM_THREADS) void sd_count_kernel(
     const uint32_t *__restrict__ in_t, uint64_t n, const uint32_t *__restrict__ Zc, int s, int k,
     const uint32_t *__restrict__ tfirst, uint64_t nbuckets, const uint32_t *__restrict__ tile_bucket,
     uint16_t *__restrict__ cnt, uint8_t *__restrict__ seg) {
     __shared__ uint32_t s_cnt[DOM_RADIX];
-    __shared__ uint64_t s_mt[DOM_WAVES][4][16];
     const int tid = threadIdx.x, lane = tid & (WAVE - 1), w = tid / WAVE;
     const uint64_t tile = blockIdx.x;
     const TileLoc L = locate_tile<FIRST>(tile, n, Zc, s + k, tfirst, nbuckets, tile_bucket);
     if (!L.valid) return;
     s_cnt[tid] = 0;
-    __syncthreads();
     uint32_t t[DOM_CHUNKS_PER_WAVE], acc[DOM_CHUNKS_PER_WAVE];
     bool ok[DOM_CHUNKS_PER_WAVE];
     load_tile<FIRST>(L, in_t, nullptr, w, lane, t, acc, ok, false);
+    __syncthreads();
     const uint32_t dmask = (1u << k) - 1u;
 #pragma unroll
     for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
-        const uint32_t d = (t[i] >> s) & dmask;
-        uint64_t eq, lt;
-        chunk_masks(ok[i], d, lane, s_mt[w], eq, lt);
-        if (ok[i] && mbcnt(eq) == 0) atomicAdd(&s_cnt[d], (uint32_t)__popcll(eq));
+        // invalid lanes take digit RADIX (never counted) so they end runs
+        const uint32_t d = ok[i] ? (t[i] >> s) & dmask : (uint32_t)DOM_RADIX;
+        const uint32_t dl = (uint32_t)__shfl_up((int)d, 1, WAVE);
+        const bool head = lane == 0 || dl != d;
+        const uint64_t heads = ballot(head);
+        // next head above this lane (or 64): the run is [lane, next)
+        const uint64_t above = lane == WAVE - 1 ? 0ull : heads & (~0ull << (lane + 1));
+        const uint32_t next = above ? (uint32_t)__builtin_ctzll(above) : (uint32_t)WAVE;
+        if (head && d < (uint32_t)DOM_RADIX) atomicAdd(&s_cnt[d], next - (uint32_t)lane);
     }
     __syncthreads();
     cnt[tile * DOM_RADIX + tid] = (uint16_t)s_cnt[tid];

@@ -170,6 +170,14 @@ def prev_next_use(keys: torch.Tensor, prev: Optional[torch.Tensor] = None,
     return prev, nxt, ws
 
 
+def high_key_passes_ran(ws: torch.Tensor) -> bool:
+    """Whether the last pc_prev_next_use call on this workspace also sorted by
+    the high 32 key bits (workspace word 1, decided on the device).
+    Synchronises the current stream."""
+    torch.cuda.current_stream().synchronize()
+    return bool(int(ws[4:8].view(torch.int32).item()))
+
+
 def stack_distance(prev: torch.Tensor, nxt: torch.Tensor, dist: Optional[torch.Tensor] = None,
                    ws: Optional[torch.Tensor] = None):
     L = lib()
@@ -288,8 +296,7 @@ class Pipeline:
     def high_key_passes_ran(self) -> bool:
         """Whether the last prev/next call also sorted by the high 32 key
         bits (decided on the device; see pc_prev_next_use).  Synchronises."""
-        torch.cuda.current_stream().synchronize()
-        return bool(int(self.ws_pn[4:8].view(torch.int32).item()))
+        return high_key_passes_ran(self.ws_pn)
 
     def status(self) -> dict:
         return {name: workspace_status(ws) for name, ws in

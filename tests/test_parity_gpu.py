@@ -40,10 +40,14 @@ def gpu_hash(trace, B=16, parent=None, root=0):
     return pc.as_u64(keys), pc.as_u32(depth)
 
 
+LAST_HIGH_KEY = [None]   # whether the last gpu_prev_next needed the high key bits
+
+
 def gpu_prev_next(keys_np):
     keys = pc.to_dev_u64(keys_np)
     prev, nxt, ws = pc.prev_next_use(keys)
     assert pc.workspace_status(ws) == 0
+    LAST_HIGH_KEY[0] = pc.high_key_passes_ran(ws)
     return pc.as_u32(prev), pc.as_u32(nxt)
 
 
@@ -194,6 +198,11 @@ def test_small_and_ragged_sizes(n):
 def test_degenerate_streams(kind):
     check_keys_path(stream(kind, 70001, 3), caps=np.array([0, 1, 2, 7, 10000, 10 ** 8], np.uint64),
                     label=kind)
+    # 1000 keys sharing one low-32-bit value are too many to scan, so the
+    # high-bit passes and the second link must have run; short mixed runs
+    # (lowpairs) and a hot key sharing its low bits with a rare one (lowhot)
+    # are resolved by scanning
+    assert LAST_HIGH_KEY[0] == (kind == "lowsame"), kind
 
 
 @pytest.mark.parametrize("n", [(1 << 20) + 12345, (1 << 21) - 1])
