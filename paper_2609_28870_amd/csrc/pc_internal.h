@@ -91,7 +91,8 @@ __device__ __forceinline__ uint32_t mbcnt(uint64_t mask) {
                                      __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-__device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+// wave-wide vote straight from the compare (one VALU compare into an SGPR pair)
+__device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
 
 // Look-back status words carry their own payload (flag + count in one word),
 // so relaxed device-scope atomics suffice: no other memory is published
@@ -127,23 +128,59 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
 // exclusive prefix sum across the 64 lanes of a wave
 __device__ __forceinline__ uint32_t wave_excl_scan(uint32_t v) { return wave_incl_scan(v) - v; }
 
-// Lanes whose `bits`-bit digit equals q (eq) and is smaller than q (lt), for
-// q = this lane's own index, from the per-bit ballots B[0..bits) of the
-// digits (bit b of every valid lane's digit) and the valid-lane mask vm.
-// Walks the bits from the top: a lane is smaller than q at the first bit
-// where it has 0 and q has 1, all higher bits being equal.
+// popcount of (mask & lanes below me) + acc
+__device__ __forceinline__ uint32_t mbcnt_acc(uint64_t mask, uint32_t acc) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, acc));
+}
+
+// Three-input bitwise function (gfx950 v_bitop3): bit i of `table` is the
+// result for (x, y, z) = (i >> 2 & 1, i >> 1 & 1, i & 1).
+template <int TABLE>
+__device__ __forceinline__ uint64_t bitop3(uint64_t x, uint64_t y, uint32_t z) {
+    const uint32_t lo = __builtin_amdgcn_bitop3_b32((uint32_t)x, (uint32_t)y, z, TABLE);
+    const uint32_t hi = __builtin_amdgcn_bitop3_b32((uint32_t)(x >> 32), (uint32_t)(y >> 32), z, TABLE);
+    return ((uint64_t)hi << 32) | lo;
+}
+constexpr int BITOP_X_NOTY_Z = 0x20;    // x & ~y & z
+constexpr int BITOP_X_YEQZ = 0x90;      // x & ~(y ^ z)
+
+// Rank this lane's BITS-bit digit d among the valid lanes vm of the wave,
+// walking the bits from the top: e keeps the lanes whose higher bits equal
+// d's; at a bit where d has 1, the lanes of e with 0 there are smaller.
+// Returns eq = valid lanes with digit d, and *lt = number of valid lanes
+// below this one with a smaller digit.  Per bit: one ballot and six VALU
+// operations, no LDS.
 template <int BITS>
-__device__ __forceinline__ void digit_masks(const uint64_t *B, uint64_t vm, uint32_t q, uint64_t &eq,
-                                            uint64_t &lt) {
-    uint64_t e = vm, l = 0;
+__device__ __forceinline__ uint64_t rank_digit(uint32_t d, uint64_t vm, uint32_t *lt) {
+    uint64_t e = vm;
+    uint32_t c = 0;
 #pragma unroll
     for (int b = BITS - 1; b >= 0; --b) {
-        const bool bit = (q >> b) & 1;
-        if (bit) l |= e & ~B[b];
-        e &= bit ? B[b] : ~B[b];
+        uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)d, b, 1);   // all ones when bit b is set
+        __asm__("" : "+v"(m));   // vote on m itself (one compare), not on a re-derived bit test
+        const uint64_t B = ballot(m != 0);
+        c = mbcnt_acc(bitop3<BITOP_X_NOTY_Z>(e, B, m), c);
+        e = bitop3<BITOP_X_YEQZ>(e, B, m);
     }
-    eq = e;
-    lt = l;
+    // pin the count here: otherwise the compiler sinks the mbcnt chain to the
+    // count's first use and keeps every intermediate mask alive until then
+    __asm__ volatile("" : "+v"(c));
+    *lt = c;
+    return e;
+}
+
+// eq mask only (stable ranking by digit)
+template <int BITS>
+__device__ __forceinline__ uint64_t match_digit(uint32_t d, uint64_t vm) {
+    uint64_t e = vm;
+#pragma unroll
+    for (int b = BITS - 1; b >= 0; --b) {
+        uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)d, b, 1);
+        __asm__("" : "+v"(m));
+        e = bitop3<BITOP_X_YEQZ>(e, ballot(m != 0), m);
+    }
+    return e;
 }
 
 // Block-wide exclusive scan of one value per thread (blockDim.x <= 1024).

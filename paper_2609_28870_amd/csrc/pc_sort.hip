@@ -118,13 +118,7 @@ __global__ __launch_bounds__(SORT_THREADS, 8) void sort_pass_kernel(
 #pragma unroll
     for (int j = 0; j < SORT_ITEMS; ++j) {
         const uint32_t d = (uint32_t)(k[j] >> shift) & 0xFF;
-        uint64_t m = ballot(ok[j]);
-#pragma unroll
-        for (int b = 0; b < 8; ++b) {
-            const bool bit = (d >> b) & 1;
-            const uint64_t B = ballot(ok[j] && bit);
-            m &= bit ? B : ~B;
-        }
+        const uint64_t m = match_digit<8>(d, ballot(ok[j]));
         const uint32_t before = mbcnt(m);
         uint32_t cur = 0;
         if (ok[j]) cur = s_wcnt[w][d];
@@ -222,7 +216,7 @@ constexpr int PERM_THREADS = 512;
 constexpr int PERM_ITEMS = 8;
 constexpr int PERM_TILE = PERM_THREADS * PERM_ITEMS;   // 4096
 constexpr int PERM_RADIX = 1024;
-constexpr int PERM_LOCAL_BITS = 12;
+constexpr int PERM_LOCAL_BITS = 13;
 
 // After the four passes over the low 32 key bits, equal keys are contiguous
 // unless different keys share those bits ("mixed" runs, a few percent of the
@@ -374,7 +368,7 @@ __device__ __forceinline__ uint32_t mixed_neighbour(const uint64_t *__restrict__
 // workgroup's run.  A chunk spans at most 1024 consecutive buckets (see the
 // plan), so digit = bucket mod 1024 names them without collision.
 struct PermLds {
-    uint32_t stage[PERM_TILE];
+    uint64_t stage[PERM_TILE];   // times (as u32), then (prev, next) pairs
     uint32_t cnt[PERM_RADIX];
     uint32_t lstart[PERM_RADIX];
     uint32_t cur[PERM_RADIX];
@@ -386,10 +380,9 @@ struct PermLds {
 template <bool FROM_SORT>
 __device__ __forceinline__ void perm_partition_body(
     PermLds &L, const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t,
-    const uint32_t *__restrict__ in_p, const uint32_t *__restrict__ in_n, uint64_t n, int s,
-    uint64_t per_wg, uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t,
-    uint32_t *__restrict__ out_p, uint32_t *__restrict__ out_n, bool full, int32_t *__restrict__ overflow) {
-    uint32_t *s_stage = L.stage, *s_cnt = L.cnt, *s_lstart = L.lstart, *s_cur = L.cur, *s_bucket = L.bucket,
+    const uint64_t *__restrict__ in_pn, uint64_t n, int s, uint64_t per_wg, uint32_t *__restrict__ cursor,
+    uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn, bool full, int32_t *__restrict__ overflow) {
+    uint32_t *s_stage = reinterpret_cast<uint32_t *>(L.stage), *s_cnt = L.cnt, *s_lstart = L.lstart, *s_cur = L.cur, *s_bucket = L.bucket,
              *s_tmp = L.tmp;
     constexpr int DPT = PERM_RADIX / PERM_THREADS;   // digits per thread
     const int tid = threadIdx.x;
@@ -440,7 +433,8 @@ __device__ __forceinline__ void perm_partition_body(
         // load of the tile is issued before the first use, so a tile costs
         // one memory latency, not one per item.
         const uint32_t *tb = in_t + base;
-        uint32_t t[PERM_ITEMS], pv[PERM_ITEMS], nx[PERM_ITEMS], pos[PERM_ITEMS];
+        uint32_t t[PERM_ITEMS], pos[PERM_ITEMS];
+        uint64_t pn[PERM_ITEMS];   // prev | next << 32
         bool ok[PERM_ITEMS];
         if (FROM_SORT) {
             const uint64_t *kb = sk + base;
@@ -486,23 +480,21 @@ __device__ __forceinline__ void perm_partition_body(
                 const uint32_t etp = (uint32_t)__shfl((int)et, j, WAVE);
                 const uint32_t etn = (uint32_t)__shfl((int)et, 8 + j, WAVE);
                 bool mp = false, mn = false;
-                pv[j] = NONE;
-                nx[j] = NONE;
+                uint32_t pv = NONE, nx = NONE;
                 if (ok[j]) {
                     const bool has_next = i + 1 < n;
                     if (lane == 0) { kp = ekp; tp = etp; }
                     if (lane == last) { kn = ekn; tn = etn; }
-                    if (i > 0 && kp == k[j]) pv[j] = tp;
+                    if (i > 0 && kp == k[j]) pv = tp;
                     else mp = i > 0 && !full && same_low(kp, k[j]);
-                    if (has_next && kn == k[j]) nx[j] = tn;
+                    if (has_next && kn == k[j]) nx = tn;
                     else mn = has_next && !full && same_low(kn, k[j]);
                 }
                 if (ballot(mp))
-                    pv[j] = mixed_neighbour<-1>(sk, in_t, n, i, k[j], t[j], mp, pv[j], lane, last, &L.budget,
-                                                overflow);
+                    pv = mixed_neighbour<-1>(sk, in_t, n, i, k[j], t[j], mp, pv, lane, last, &L.budget, overflow);
                 if (ballot(mn))
-                    nx[j] = mixed_neighbour<+1>(sk, in_t, n, i, k[j], t[j], mn, nx[j], lane, last, &L.budget,
-                                                overflow);
+                    nx = mixed_neighbour<+1>(sk, in_t, n, i, k[j], t[j], mn, nx, lane, last, &L.budget, overflow);
+                pn[j] = (uint64_t)pv | ((uint64_t)nx << 32);
             }
         } else {
 #pragma unroll
@@ -511,8 +503,7 @@ __device__ __forceinline__ void perm_partition_body(
                 ok[j] = o < left;
                 const uint32_t oc = ok[j] ? o : 0u;
                 t[j] = tb[oc];
-                pv[j] = (in_p + base)[oc];
-                nx[j] = (in_n + base)[oc];
+                pn[j] = (in_pn + base)[oc];
             }
         }
 #pragma unroll
@@ -539,7 +530,7 @@ __device__ __forceinline__ void perm_partition_body(
             s_stage[pos[j]] = t[j];
         }
         __syncthreads();
-        // times out, remembering each slot's destination for prev and next
+        // times out, remembering each slot's destination for the (prev, next) pairs
         uint32_t dst[PERM_ITEMS];
 #pragma unroll
         for (int r = 0; r < PERM_ITEMS; ++r) {
@@ -555,19 +546,11 @@ __device__ __forceinline__ void perm_partition_body(
         __syncthreads();
 #pragma unroll
         for (int j = 0; j < PERM_ITEMS; ++j)
-            if (ok[j]) s_stage[pos[j]] = pv[j];
+            if (ok[j]) L.stage[pos[j]] = pn[j];
         __syncthreads();
 #pragma unroll
         for (int r = 0; r < PERM_ITEMS; ++r)
-            if (dst[r] < n) out_p[dst[r]] = s_stage[tid + r * PERM_THREADS];
-        __syncthreads();
-#pragma unroll
-        for (int j = 0; j < PERM_ITEMS; ++j)
-            if (ok[j]) s_stage[pos[j]] = nx[j];
-        __syncthreads();
-#pragma unroll
-        for (int r = 0; r < PERM_ITEMS; ++r)
-            if (dst[r] < n) out_n[dst[r]] = s_stage[tid + r * PERM_THREADS];
+            if (dst[r] < n) out_pn[dst[r]] = L.stage[tid + r * PERM_THREADS];
 #pragma unroll
         for (int q = 0; q < DPT; ++q) s_cur[tid * DPT + q] += c[q];
         __syncthreads();
@@ -581,21 +564,19 @@ __device__ __forceinline__ void perm_partition_body(
 // sorted keys.
 __global__ __launch_bounds__(PERM_THREADS, 4) void link_partition_kernel(
     const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t, uint64_t n, int s, uint64_t per_wg,
-    uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t, uint32_t *__restrict__ out_p,
-    uint32_t *__restrict__ out_n, const int32_t *__restrict__ only_if, int32_t *__restrict__ flag) {
+    uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn,
+    const int32_t *__restrict__ only_if, int32_t *__restrict__ flag) {
     if (only_if && *only_if == 0) return;
     __shared__ PermLds L;
-    perm_partition_body<true>(L, sk, in_t, nullptr, nullptr, n, s, per_wg, cursor, out_t, out_p, out_n,
-                              only_if != nullptr, flag);
+    perm_partition_body<true>(L, sk, in_t, nullptr, n, s, per_wg, cursor, out_t, out_pn, only_if != nullptr,
+                              flag);
 }
 
 __global__ __launch_bounds__(PERM_THREADS, 6) void perm_partition_kernel(
-    const uint32_t *__restrict__ in_t, const uint32_t *__restrict__ in_p, const uint32_t *__restrict__ in_n,
-    uint64_t n, int s, uint64_t per_wg, uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t,
-    uint32_t *__restrict__ out_p, uint32_t *__restrict__ out_n) {
+    const uint32_t *__restrict__ in_t, const uint64_t *__restrict__ in_pn, uint64_t n, int s, uint64_t per_wg,
+    uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn) {
     __shared__ PermLds L;
-    perm_partition_body<false>(L, nullptr, in_t, in_p, in_n, n, s, per_wg, cursor, out_t, out_p, out_n,
-                               true, nullptr);
+    perm_partition_body<false>(L, nullptr, in_t, in_pn, n, s, per_wg, cursor, out_t, out_pn, true, nullptr);
 }
 
 // cursor[b] = b << s: each bucket's output run starts at its first t
@@ -604,46 +585,56 @@ __global__ void perm_cursor_kernel(uint32_t *__restrict__ cursor, uint64_t nb, i
     if (b < nb) cursor[b] = (uint32_t)(b << s);
 }
 
-// every 4096-range of t holds exactly its own triples: place them by t in
-// LDS and write prev / next in time order
-__global__ __launch_bounds__(256) void perm_local_kernel(const uint32_t *__restrict__ in_t,
-                                                         const uint32_t *__restrict__ in_p,
-                                                         const uint32_t *__restrict__ in_n, uint64_t n,
-                                                         uint32_t *__restrict__ prev,
-                                                         uint32_t *__restrict__ next) {
+// every 8192-range of t holds exactly its own triples: place the (prev,
+// next) pairs by t in LDS and write prev / next in time order
+constexpr int LOCAL_THREADS = 512;
+__global__ __launch_bounds__(LOCAL_THREADS) void perm_local_kernel(const uint32_t *__restrict__ in_t,
+                                                                   const uint64_t *__restrict__ in_pn,
+                                                                   uint64_t n, uint32_t *__restrict__ prev,
+                                                                   uint32_t *__restrict__ next) {
     constexpr uint32_t SPAN = 1u << PERM_LOCAL_BITS;
-    __shared__ uint32_t s_p[SPAN], s_n[SPAN];
+    constexpr int PER = SPAN / LOCAL_THREADS;
+    __shared__ uint64_t s_pn[SPAN];
     const uint64_t r0 = (uint64_t)blockIdx.x * SPAN;
     const uint32_t cnt = n - r0 < SPAN ? (uint32_t)(n - r0) : SPAN;
-    for (uint32_t j = threadIdx.x; j < cnt; j += blockDim.x) {
-        const uint32_t tt = in_t[r0 + j];
-        const uint32_t slot = (uint32_t)(tt - r0) & (SPAN - 1);
-        s_p[slot] = in_p[r0 + j];
-        s_n[slot] = in_n[r0 + j];
+    const uint32_t *tb = in_t + r0;
+    const uint64_t *pb = in_pn + r0;
+    uint32_t tt[PER];
+    uint64_t v[PER];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+        const uint32_t j = threadIdx.x + q * LOCAL_THREADS;
+        const uint32_t jc = j < cnt ? j : 0u;
+        tt[q] = tb[jc];
+        v[q] = pb[jc];
     }
+#pragma unroll
+    for (int q = 0; q < PER; ++q)
+        if (threadIdx.x + q * LOCAL_THREADS < cnt) s_pn[(uint32_t)(tt[q] - r0) & (SPAN - 1)] = v[q];
     __syncthreads();
-    for (uint32_t j = threadIdx.x; j < cnt; j += blockDim.x) {
-        prev[r0 + j] = s_p[j];
-        next[r0 + j] = s_n[j];
+    for (uint32_t j = threadIdx.x; j < cnt; j += LOCAL_THREADS) {
+        const uint64_t x = s_pn[j];
+        prev[r0 + j] = (uint32_t)x;
+        next[r0 + j] = (uint32_t)(x >> 32);
     }
 }
 
 struct SortWs {
     int32_t *hdr;
     uint32_t *hist, *start, *counters;
-    uint64_t *k1, *k2;
-    uint32_t *v1, *v2;
+    uint64_t *k1, *k2;   // sort ping-pong; afterwards (prev, next) pairs
+    uint32_t *v1, *v2;   // sort ping-pong; afterwards times t
     uint64_t *status;
     uint32_t *cursor;
     size_t bytes;
 };
 
-// Partition plan for the way back to time order.  The last pass uses
-// 4096-ranges of t.  The first pass has at most 1024 buckets; every later pass
-// splits a bucket into at most 512, so a workgroup chunk (at most 2^20
-// elements, smaller than any earlier bucket of >= 2^21) spans at most two
-// earlier buckets, i.e. at most 1024 consecutive buckets of its own pass, and
-// (bucket mod 1024) names them without collision inside the chunk.
+// Partition plan for the way back to time order.  The last step uses
+// 8192-ranges of t.  Every pass splits into at most 512 buckets, so a
+// workgroup chunk (at most 2^20 elements, smaller than any earlier bucket of
+// >= 2^22) spans at most two earlier buckets, i.e. at most 1024 consecutive
+// buckets of its own pass, and (bucket mod 1024) names them without collision
+// inside the chunk.
 struct PermPlan {
     int passes;
     int s[4];
@@ -658,8 +649,8 @@ static PermPlan plan_perm(uint64_t n) {
     int hi = nbits;   // bits above PERM_LOCAL_BITS still to split
     int cur = nbits;
     int shifts[4], k = 0;
-    // first pass: up to 10 bits; later passes: up to 9 bits
-    int width = 10;
+    // up to 9 bits per pass: longer runs per tile and bucket than 10
+    int width = 9;
     while (cur > PERM_LOCAL_BITS && k < 4) {
         int next_s = cur - width > PERM_LOCAL_BITS ? cur - width : PERM_LOCAL_BITS;
         shifts[k++] = next_s;
@@ -732,14 +723,12 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
               (const int32_t *)nullptr);
 
     // Links + partition back to time order.  The sort leaves (key, t) in
-    // (k2, v2) after four passes and again after eight; triples (t, prev,
-    // next) ping-pong between the first sort buffers (k1 viewed as two u32
-    // arrays, v1) and, once the sorted keys have been consumed, the second
-    // ones (k2 as two u32 arrays, v2).
+    // (k2, v2) after four passes and again after eight; the triples ping-pong
+    // between the first sort buffers ((prev, next) pairs in k1, t in v1) and,
+    // once the sorted keys have been consumed, the second ones (k2, v2).
     const pc::PermPlan pp = pc::plan_perm(n);
-    uint32_t *bt[2] = {reinterpret_cast<uint32_t *>(w.k1), reinterpret_cast<uint32_t *>(w.k2)};
-    uint32_t *bp[2] = {bt[0] + n, bt[1] + n};
-    uint32_t *bn[2] = {w.v1, w.v2};
+    uint32_t *bt[2] = {w.v1, w.v2};
+    uint64_t *bpn[2] = {w.k1, w.k2};
     // chunks of at most 2^20 elements: small enough that a chunk of a later
     // pass spans at most two buckets of the previous one, large enough that
     // each bucket cursor sees few atomics
@@ -758,7 +747,7 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
             PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg0), dim3(256), 0, s, w.cursor, pp.buckets[0],
                       pp.s[0]);
             PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ptiles), dim3(pc::PERM_THREADS), 0, s, kin, vin,
-                      n, pp.s[0], per_wg, w.cursor, bt[0], bp[0], bn[0], (const int32_t *)nullptr, need_high);
+                      n, pp.s[0], per_wg, w.cursor, bt[0], bpn[0], (const int32_t *)nullptr, need_high);
             PC_LAUNCH(pc::K_SORT_HIST, pc::sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n,
                       pc::SORT_PASSES / 2, w.hist, (const int32_t *)need_high);
             PC_LAUNCH(pc::K_SORT_SCAN, pc::sort_scan_kernel, dim3(1), dim3(pc::RADIX), 0, s, w.hist,
@@ -775,7 +764,7 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
     // second link, over fully sorted keys, only if the first one gave up
     PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg0), dim3(256), 0, s, w.cursor, pp.buckets[0], pp.s[0]);
     PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ptiles), dim3(pc::PERM_THREADS), 0, s, kin, vin, n,
-              pp.s[0], per_wg, w.cursor, bt[0], bp[0], bn[0], (const int32_t *)need_high, (int32_t *)nullptr);
+              pp.s[0], per_wg, w.cursor, bt[0], bpn[0], (const int32_t *)need_high, (int32_t *)nullptr);
     int cur = 0;
     for (int i = 1; i < pp.passes; ++i) {
         const unsigned cg = (unsigned)((pp.buckets[i] + 255) / 256);
@@ -783,11 +772,12 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
                   pp.s[i]);
         const int nxt = cur ^ 1;
         PC_LAUNCH(pc::K_PERM, pc::perm_partition_kernel, dim3(ptiles), dim3(pc::PERM_THREADS), 0, s, bt[cur],
-                  bp[cur], bn[cur], n, pp.s[i], per_wg, w.cursor, bt[nxt], bp[nxt], bn[nxt]);
+                  bpn[cur], n, pp.s[i], per_wg, w.cursor, bt[nxt], bpn[nxt]);
         cur = nxt;
     }
-    PC_LAUNCH(pc::K_PERM_LOCAL, pc::perm_local_kernel, dim3((unsigned)((n + 4095) / 4096)), dim3(256), 0, s,
-              bt[cur], bp[cur], bn[cur], n, prev, next);
+    const uint64_t span = 1ull << pc::PERM_LOCAL_BITS;
+    PC_LAUNCH(pc::K_PERM_LOCAL, pc::perm_local_kernel, dim3((unsigned)((n + span - 1) / span)),
+              dim3(pc::LOCAL_THREADS), 0, s, bt[cur], bpn[cur], n, prev, next);
     return PC_OK;
 }
 

@@ -25,9 +25,9 @@
 //   * per level (1-3 levels of 8-bit digits above bit 12), over tiles of 1024
 //     elements: sd_count (per-tile digit counts), a segmented scan of those
 //     counts over the tiles of each bucket (sd_seg: reduce, carry, scan --
-//     no waiting on other workgroups), then sd_dominance_pass: wave ballots
-//     build per-chunk digit masks (two 16-entry nibble tables) giving every
-//     lane the earlier lanes with a smaller / equal digit, a 2-D prefix over
+//     no waiting on other workgroups), then sd_dominance_pass: one ballot
+//     per digit bit gives every lane the earlier lanes of its 64-lane chunk
+//     with a smaller / equal digit, a 2-D prefix over
 //     (chunk, digit) in LDS extends that to the tile, the scanned counts
 //     extend it across tiles, and the tile is written out digit-partitioned
 //     through LDS.
@@ -170,32 +170,6 @@ __device__ __forceinline__ void load_tile(const TileLoc &L, const uint32_t *__re
             acc[i] = (ok[i] && want_acc) ? in_acc[e] : 0u;
         }
     }
-}
-
-// Rank the lanes of one 64-element chunk by digit: eq = lanes with the same
-// digit, lt = lanes with a smaller digit, built from eight ballots through
-// two 16-entry nibble tables in LDS (rows of `mt`, one set per wave).
-__device__ __forceinline__ void chunk_masks(bool ok, uint32_t d, int lane, uint64_t (*mt)[16], uint64_t &eq,
-                                            uint64_t &lt) {
-    const uint64_t vm = ballot(ok);
-    uint64_t B[8];
-#pragma unroll
-    for (int b = 0; b < 8; ++b) B[b] = ballot(ok && ((d >> b) & 1));
-    if (lane < 16) {
-        uint64_t mh, lh, ml, ll;
-        digit_masks<4>(B + 4, vm, (uint32_t)lane, mh, lh);
-        digit_masks<4>(B, vm, (uint32_t)lane, ml, ll);
-        mt[0][lane] = mh;
-        mt[1][lane] = ml;
-        mt[2][lane] = lh;
-        mt[3][lane] = ll;
-    }
-    __builtin_amdgcn_wave_barrier();
-    const uint32_t h = d >> 4, l = d & 15;
-    const uint64_t Mh = mt[0][h], Ml = mt[1][l], Lh = mt[2][h], Ll = mt[3][l];
-    eq = Mh & Ml;
-    lt = Lh | (Mh & Ll);
-    __builtin_amdgcn_wave_barrier();
 }
 
 // Per-tile digit counts (and whether the tile starts a bucket), the input of
@@ -352,7 +326,6 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     __shared__ uint16_t s_pl[DOM_CHUNKS][DOM_RADIX];    // 2-D prefix (earlier chunks, smaller digit)
     __shared__ uint32_t s_st[DOM_TILE];                 // staged t
     __shared__ uint32_t s_sa[DOM_TILE];                 // staged acc
-    __shared__ uint64_t s_mt[DOM_WAVES][4][16];         // nibble mask tables per wave
     __shared__ uint32_t s_lstart[DOM_RADIX];
     __shared__ uint32_t s_gl[DOM_RADIX];
     __shared__ uint32_t s_base[DOM_RADIX];
@@ -381,10 +354,10 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
         const int c = w * DOM_CHUNKS_PER_WAVE + i;
         const uint32_t d = (t[i] >> s) & dmask;
-        uint64_t eq, lt;
-        chunk_masks(ok[i], d, lane, s_mt[w], eq, lt);
+        uint32_t lt;
+        const uint64_t eq = rank_digit<8>(d, ballot(ok[i]), &lt);
         q_ic[i] = ok[i] ? (uint16_t)mbcnt(eq) : 0;
-        l_ic[i] = ok[i] ? (uint16_t)mbcnt(lt) : 0;
+        l_ic[i] = ok[i] ? (uint16_t)lt : 0;
         if (ok[i] && q_ic[i] == 0) s_h[c][d] = (uint16_t)__popcll(eq);
     }
     __syncthreads();
@@ -476,6 +449,7 @@ __global__ __launch_bounds__(LOC_THREADS) void sd_local_kernel(
     const uint64_t r0 = (uint64_t)blockIdx.x * LOCAL_SPAN;
     const uint64_t r1 = r0 + LOCAL_SPAN < n ? r0 + LOCAL_SPAN : n;
     const uint64_t e0 = cnt_lt(r0, Zc), e1 = cnt_lt(r1, Zc);
+    for (int i = tid; i < LOC_CHUNKS * 64 / 2; i += LOC_THREADS) s_work[i] = 0;
 
     // ---- level A: digit = bits 6..11 of t, chunks of 64 in v order
     uint32_t t[LOC_CPW], acc[LOC_CPW];
@@ -488,21 +462,16 @@ __global__ __launch_bounds__(LOC_THREADS) void sd_local_kernel(
         t[i] = ok[i] ? in_t[e] : 0u;
         acc[i] = ok[i] ? in_acc[e] : 0u;
     }
+    __syncthreads();   // chunk histograms zeroed
 #pragma unroll
     for (int i = 0; i < LOC_CPW; ++i) {
         const int c = w * LOC_CPW + i;
         const uint32_t d = (t[i] >> 6) & 63;
-        const uint64_t vm = ballot(ok[i]);
-        uint64_t B[6];
-#pragma unroll
-        for (int b = 0; b < 6; ++b) B[b] = ballot(ok[i] && ((d >> b) & 1));
-        uint64_t m, lmask;   // lanes whose digit equals / is below this lane's index
-        digit_masks<6>(B, vm, (uint32_t)lane, m, lmask);
-        s_h[c][lane] = (uint16_t)__popcll(m);
-        const uint64_t eq = __shfl(m, (int)d, WAVE);
-        const uint64_t lt = __shfl(lmask, (int)d, WAVE);
+        uint32_t lt;
+        const uint64_t eq = rank_digit<6>(d, ballot(ok[i]), &lt);
         qa[i] = ok[i] ? (uint8_t)mbcnt(eq) : 0;
-        la[i] = ok[i] ? (uint8_t)mbcnt(lt) : 0;
+        la[i] = ok[i] ? (uint8_t)lt : 0;
+        if (ok[i] && qa[i] == 0) s_h[c][d] = (uint16_t)__popcll(eq);
     }
     __syncthreads();
     // column prefix: thread (digit d, quarter q) scans 16 chunks, then the
@@ -559,16 +528,10 @@ __global__ __launch_bounds__(LOC_THREADS) void sd_local_kernel(
         const bool okb = (uint32_t)lane < cnt;
         const uint32_t tb = okb ? s_st[base + lane] : 0u;
         const uint32_t ab = okb ? s_sa[base + lane] : 0u;
-        const uint32_t d = tb & 63;
-        const uint64_t vm = ballot(okb);
-        uint64_t B[6];
-#pragma unroll
-        for (int b = 0; b < 6; ++b) B[b] = ballot(okb && ((d >> b) & 1));
-        uint64_t m, lmask;
-        digit_masks<6>(B, vm, (uint32_t)lane, m, lmask);
-        const uint64_t lt = __shfl(lmask, (int)d, WAVE);
+        uint32_t lt;
+        rank_digit<6>(tb & 63, ballot(okb), &lt);
         // slot[] aliases the level-A tables, which are dead after the barrier
-        if (okb) slot[tb & (LOCAL_SPAN - 1)] = ab + mbcnt(lt);
+        if (okb) slot[tb & (LOCAL_SPAN - 1)] = ab + lt;
     }
     __syncthreads();
 
