@@ -40,12 +40,13 @@ namespace pc {
 
 constexpr int LOCAL_BITS = 12;
 constexpr uint32_t LOCAL_SPAN = 1u << LOCAL_BITS;   // 4096
-constexpr int DOM_THREADS = 256;
+constexpr int DOM_THREADS = 512;
 constexpr int DOM_WAVES = DOM_THREADS / WAVE;
 constexpr int DOM_CHUNKS_PER_WAVE = 4;
 constexpr int DOM_CHUNKS = DOM_WAVES * DOM_CHUNKS_PER_WAVE;   // 32
-constexpr int DOM_TILE = DOM_CHUNKS * WAVE;                    // 1024
+constexpr int DOM_TILE = DOM_CHUNKS * WAVE;                    // 2048
 constexpr int DOM_RADIX = 256;
+static_assert(DOM_THREADS == 2 * DOM_RADIX, "the column prefix splits the chunks in two halves");
 constexpr int LOC_THREADS = 256;
 constexpr int LOC_WAVES = LOC_THREADS / WAVE;
 constexpr int LOC_CHUNKS = LOCAL_SPAN / WAVE;                  // 64
@@ -186,7 +187,7 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_count_kernel(
     const uint64_t tile = blockIdx.x;
     const TileLoc L = locate_tile<FIRST>(tile, n, Zc, s + k, tfirst, nbuckets, tile_bucket);
     if (!L.valid) return;
-    s_cnt[tid] = 0;
+    if (tid < DOM_RADIX) s_cnt[tid] = 0;
     uint32_t t[DOM_CHUNKS_PER_WAVE], acc[DOM_CHUNKS_PER_WAVE];
     bool ok[DOM_CHUNKS_PER_WAVE];
     load_tile<FIRST>(L, in_t, nullptr, w, lane, t, acc, ok, false);
@@ -205,7 +206,7 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_count_kernel(
         if (head && d < (uint32_t)DOM_RADIX) atomicAdd(&s_cnt[d], next - (uint32_t)lane);
     }
     __syncthreads();
-    cnt[tile * DOM_RADIX + tid] = (uint16_t)s_cnt[tid];
+    if (tid < DOM_RADIX) cnt[tile * DOM_RADIX + tid] = (uint16_t)s_cnt[tid];
     if (tid == 0) seg[tile] = FIRST ? (tile == 0) : (tile == L.first_tile);
 }
 
@@ -326,8 +327,10 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     __shared__ uint16_t s_pl[DOM_CHUNKS][DOM_RADIX];    // 2-D prefix (earlier chunks, smaller digit)
     __shared__ uint32_t s_st[DOM_TILE];                 // staged t
     __shared__ uint32_t s_sa[DOM_TILE];                 // staged acc
-    __shared__ uint32_t s_lstart[DOM_RADIX];
-    __shared__ uint32_t s_gl[DOM_RADIX];
+    // per-digit tile starts and smaller-digit counts; before that, the two
+    // half sums of the column prefix
+    __shared__ uint32_t s_part[2][DOM_RADIX];
+    uint32_t *s_lstart = s_part[0], *s_gl = s_part[1];
     __shared__ uint32_t s_base[DOM_RADIX];
     __shared__ uint32_t s_tmp[DOM_WAVES];
 
@@ -338,7 +341,8 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     const uint64_t tile = blockIdx.x;
     const TileLoc L = locate_tile<FIRST>(tile, n, Zc, s + k, tfirst, nbuckets, tile_bucket);
     if (!L.valid) return;
-    const uint32_t G = pre[tile * DOM_RADIX + tid];   // same digit, earlier tiles of the bucket
+    // same digit, earlier tiles of the bucket (threads below RADIX own a digit)
+    const uint32_t G = tid < DOM_RADIX ? pre[tile * DOM_RADIX + tid] : 0u;
     {
         uint64_t *z = reinterpret_cast<uint64_t *>(&s_h[0][0]);
         for (int i = tid; i < DOM_CHUNKS * DOM_RADIX / 4; i += DOM_THREADS) z[i] = 0;
@@ -355,25 +359,35 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
         const int c = w * DOM_CHUNKS_PER_WAVE + i;
         const uint32_t d = (t[i] >> s) & dmask;
         uint32_t lt;
-        const uint64_t eq = rank_digit<8>(d, ballot(ok[i]), &lt);
+        // the top level often has few digit bits (8 buckets at 2^31 accesses)
+        const uint64_t eq = k <= 4 ? rank_digit<4>(d, ballot(ok[i]), &lt) : rank_digit<8>(d, ballot(ok[i]), &lt);
         q_ic[i] = ok[i] ? (uint16_t)mbcnt(eq) : 0;
         l_ic[i] = ok[i] ? (uint16_t)lt : 0;
         if (ok[i] && q_ic[i] == 0) s_h[c][d] = (uint16_t)__popcll(eq);
     }
     __syncthreads();
 
-    // ---- column prefix over chunks (thread = digit) and tile totals; all
-    // loads are issued before any store so they pipeline
+    // ---- column prefix over chunks (thread = digit, two halves of the
+    // chunks) and tile totals; all loads are issued before any store
     uint32_t tot = 0;
     {
-        const int d = tid;
-        uint16_t h[DOM_CHUNKS];
+        constexpr int HALF = DOM_CHUNKS / 2;
+        const int d = tid & (DOM_RADIX - 1), c0 = (tid / DOM_RADIX) * HALF;
+        uint16_t h[HALF];
+        uint32_t sum = 0;
 #pragma unroll
-        for (int c = 0; c < DOM_CHUNKS; ++c) h[c] = s_h[c][d];
+        for (int c = 0; c < HALF; ++c) {
+            h[c] = s_h[c0 + c][d];
+            sum += h[c];
+        }
+        s_part[tid / DOM_RADIX][d] = sum;
+        __syncthreads();
+        uint32_t run = c0 ? s_part[0][d] : 0u;
+        tot = tid < DOM_RADIX ? s_part[0][d] + s_part[1][d] : 0u;
 #pragma unroll
-        for (int c = 0; c < DOM_CHUNKS; ++c) {
-            s_h[c][d] = (uint16_t)tot;
-            tot += h[c];
+        for (int c = 0; c < HALF; ++c) {
+            s_h[c0 + c][d] = (uint16_t)run;
+            run += h[c];
         }
     }
     __syncthreads();
@@ -391,7 +405,7 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     const uint32_t lst = block_excl_scan(tot, s_tmp, &n_valid);
     uint32_t gsum;
     const uint32_t GL = block_excl_scan(G, s_tmp, &gsum);   // smaller digit, earlier tiles
-    {
+    if (tid < DOM_RADIX) {
         const uint64_t X = ((L.bucket << k) + (uint64_t)tid) << s;
         const uint64_t sub = cnt_lt(X < n ? X : n, Zc);
         s_lstart[tid] = lst;
