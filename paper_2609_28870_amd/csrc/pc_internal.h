@@ -125,6 +125,18 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
     return x;
 }
 
+// Inclusive prefix OR across the 64 lanes of a wave (same DPP pattern as the
+// sum above; lanes shifted in from outside a row contribute 0).
+__device__ __forceinline__ uint32_t wave_incl_or(uint32_t x) {
+    x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false);   // row_shr:1
+    x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false);   // row_shr:2
+    x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false);   // row_shr:4
+    x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false);   // row_shr:8
+    x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);   // row_bcast:15
+    x |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);   // row_bcast:31
+    return x;
+}
+
 // exclusive prefix sum across the 64 lanes of a wave
 __device__ __forceinline__ uint32_t wave_excl_scan(uint32_t v) { return wave_incl_scan(v) - v; }
 
@@ -153,15 +165,22 @@ constexpr int BITOP_X_YEQZ = 0x90;      // x & ~(y ^ z)
 // operations, no LDS.
 template <int BITS>
 __device__ __forceinline__ uint64_t rank_digit(uint32_t d, uint64_t vm, uint32_t *lt) {
+    // all votes first: the mask chain then never waits on a compare that has
+    // just written its SGPR pair
+    uint32_t m[BITS];
+    uint64_t B[BITS];
+#pragma unroll
+    for (int b = 0; b < BITS; ++b) {
+        m[b] = (uint32_t)__builtin_amdgcn_sbfe((int)d, b, 1);   // all ones when bit b is set
+        __asm__("" : "+v"(m[b]));   // vote on m itself (one compare), not on a re-derived bit test
+        B[b] = ballot(m[b] != 0);
+    }
     uint64_t e = vm;
     uint32_t c = 0;
 #pragma unroll
     for (int b = BITS - 1; b >= 0; --b) {
-        uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)d, b, 1);   // all ones when bit b is set
-        __asm__("" : "+v"(m));   // vote on m itself (one compare), not on a re-derived bit test
-        const uint64_t B = ballot(m != 0);
-        c = mbcnt_acc(bitop3<BITOP_X_NOTY_Z>(e, B, m), c);
-        e = bitop3<BITOP_X_YEQZ>(e, B, m);
+        c = mbcnt_acc(bitop3<BITOP_X_NOTY_Z>(e, B[b], m[b]), c);
+        e = bitop3<BITOP_X_YEQZ>(e, B[b], m[b]);
     }
     // pin the count here: otherwise the compiler sinks the mbcnt chain to the
     // count's first use and keeps every intermediate mask alive until then
@@ -173,14 +192,30 @@ __device__ __forceinline__ uint64_t rank_digit(uint32_t d, uint64_t vm, uint32_t
 // eq mask only (stable ranking by digit)
 template <int BITS>
 __device__ __forceinline__ uint64_t match_digit(uint32_t d, uint64_t vm) {
+    uint32_t m[BITS];
+    uint64_t B[BITS];
+#pragma unroll
+    for (int b = 0; b < BITS; ++b) {
+        m[b] = (uint32_t)__builtin_amdgcn_sbfe((int)d, b, 1);
+        __asm__("" : "+v"(m[b]));
+        B[b] = ballot(m[b] != 0);
+    }
     uint64_t e = vm;
 #pragma unroll
-    for (int b = BITS - 1; b >= 0; --b) {
-        uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)d, b, 1);
-        __asm__("" : "+v"(m));
-        e = bitop3<BITOP_X_YEQZ>(e, ballot(m != 0), m);
-    }
+    for (int b = BITS - 1; b >= 0; --b) e = bitop3<BITOP_X_YEQZ>(e, B[b], m[b]);
     return e;
+}
+
+// For 6-bit digits that are distinct across the valid lanes: the number of
+// valid lanes below this one with a smaller digit.  The prefix OR of the
+// one-hot digits is the set of digits seen in lower lanes (distinctness keeps
+// this lane's own bit out of it once removed), so no per-bit ranking is
+// needed.
+__device__ __forceinline__ uint32_t count_smaller_distinct6(uint32_t d, bool ok) {
+    const uint64_t one = ok ? 1ull << d : 0ull;
+    const uint32_t lo = wave_incl_or((uint32_t)one), hi = wave_incl_or((uint32_t)(one >> 32));
+    const uint64_t seen = (((uint64_t)hi << 32) | lo) ^ one;
+    return (uint32_t)__popcll(seen & (one - 1));
 }
 
 // Block-wide exclusive scan of one value per thread (blockDim.x <= 1024).

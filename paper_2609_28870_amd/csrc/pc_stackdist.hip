@@ -47,10 +47,11 @@ constexpr int DOM_CHUNKS = DOM_WAVES * DOM_CHUNKS_PER_WAVE;   // 32
 constexpr int DOM_TILE = DOM_CHUNKS * WAVE;                    // 2048
 constexpr int DOM_RADIX = 256;
 static_assert(DOM_THREADS == 2 * DOM_RADIX, "the column prefix splits the chunks in two halves");
-constexpr int LOC_THREADS = 256;
+constexpr int LOC_THREADS = 512;
 constexpr int LOC_WAVES = LOC_THREADS / WAVE;
 constexpr int LOC_CHUNKS = LOCAL_SPAN / WAVE;                  // 64
-constexpr int LOC_CPW = LOC_CHUNKS / LOC_WAVES;                // 16
+constexpr int LOC_CPW = LOC_CHUNKS / LOC_WAVES;                // 8
+constexpr int LOC_PARTS = LOC_THREADS / 64;                    // column-prefix parts per digit
 constexpr int SCAN_THREADS = 1024;
 
 // number of non-cold accesses t < X (X a multiple of 4096, or X = n)
@@ -441,21 +442,21 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     }
 }
 
-// Last 12 bits, one workgroup per 4096-range of t, then D in t order.
-__global__ __launch_bounds__(LOC_THREADS) void sd_local_kernel(
+// Last 12 bits, one workgroup per 4096-range of t, then D in t order.  The
+// level-A counts go straight into a slot per t (acc included), so only the
+// six low bits of t are staged for level B, and the prev values needed at the
+// end are loaded up front; LDS stays under 40 KB (four workgroups per CU).
+__global__ __launch_bounds__(LOC_THREADS, 6) void sd_local_kernel(
     const uint32_t *__restrict__ in_t, const uint32_t *__restrict__ in_acc,
     const uint32_t *__restrict__ prev, uint64_t n, const uint32_t *__restrict__ Zc,
     uint32_t *__restrict__ dist) {
-    __shared__ uint32_t s_st[LOCAL_SPAN];
-    __shared__ uint32_t s_sa[LOCAL_SPAN];
-    __shared__ uint32_t s_work[LOCAL_SPAN];   // [64][64] u16 tables, then the slot array
-    __shared__ uint32_t s_tot[64];
-    __shared__ uint32_t s_lstart[64];
-    __shared__ uint32_t s_part[4][64];
+    __shared__ uint32_t slot[LOCAL_SPAN];           // by t: acc + counts; first the column-prefix sums
+    __shared__ uint16_t s_h[LOC_CHUNKS][64];        // chunk histograms -> column prefix
+    __shared__ uint16_t s_pl[LOC_CHUNKS][64];       // 2-D prefix (earlier chunks, smaller digit)
+    __shared__ uint8_t s_low[LOCAL_SPAN];           // bits 0..5 of t, grouped by bits 6..11
+    __shared__ uint32_t s_lstart[65];
     __shared__ uint32_t s_tmp[LOC_WAVES];
-    uint16_t(*s_h)[64] = reinterpret_cast<uint16_t(*)[64]>(&s_work[0]);
-    uint16_t(*s_pl)[64] = reinterpret_cast<uint16_t(*)[64]>(&s_work[LOCAL_SPAN / 2]);
-    uint32_t *slot = s_work;
+    uint32_t(*s_part)[64] = reinterpret_cast<uint32_t(*)[64]>(slot);   // [LOC_PARTS][64]
 
     const int tid = threadIdx.x;
     const int lane = tid & (WAVE - 1);
@@ -463,20 +464,31 @@ __global__ __launch_bounds__(LOC_THREADS) void sd_local_kernel(
     const uint64_t r0 = (uint64_t)blockIdx.x * LOCAL_SPAN;
     const uint64_t r1 = r0 + LOCAL_SPAN < n ? r0 + LOCAL_SPAN : n;
     const uint64_t e0 = cnt_lt(r0, Zc), e1 = cnt_lt(r1, Zc);
-    for (int i = tid; i < LOC_CHUNKS * 64 / 2; i += LOC_THREADS) s_work[i] = 0;
+    for (int i = tid; i < LOC_CHUNKS * 64 / 2; i += LOC_THREADS) reinterpret_cast<uint32_t *>(&s_h[0][0])[i] = 0;
 
-    // ---- level A: digit = bits 6..11 of t, chunks of 64 in v order
-    uint32_t t[LOC_CPW], acc[LOC_CPW];
-    uint8_t qa[LOC_CPW], la[LOC_CPW];
+    // ---- loads: the range's elements (v order) and its prev values (t order)
+    constexpr int PER = LOCAL_SPAN / LOC_THREADS;   // 8
+    // (32-bit offsets from per-range base pointers)
+    uint32_t t[LOC_CPW], acc[LOC_CPW], p[PER];
     bool ok[LOC_CPW];
+    const uint32_t ne = (uint32_t)(e1 - e0), nt = (uint32_t)(r1 - r0);
+    const uint32_t *tb = in_t + e0, *ab = in_acc + e0, *pb = prev + r0;
 #pragma unroll
     for (int i = 0; i < LOC_CPW; ++i) {
-        const uint64_t e = e0 + (uint64_t)(w * LOC_CPW + i) * WAVE + lane;
-        ok[i] = e < e1;
-        t[i] = ok[i] ? in_t[e] : 0u;
-        acc[i] = ok[i] ? in_acc[e] : 0u;
+        const uint32_t o = (uint32_t)((w * LOC_CPW + i) * WAVE + lane);
+        ok[i] = o < ne;
+        const uint32_t oc = ok[i] ? o : 0u;
+        t[i] = tb[oc];
+        acc[i] = ab[oc];
     }
+    const uint32_t tofs = (uint32_t)tid * PER;
+    const uint64_t tbase = r0 + tofs;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) p[j] = pb[tofs + j < nt ? tofs + j : 0u];
     __syncthreads();   // chunk histograms zeroed
+
+    // ---- level A: digit = bits 6..11 of t, chunks of 64 in v order
+    uint8_t qa[LOC_CPW], la[LOC_CPW];
 #pragma unroll
     for (int i = 0; i < LOC_CPW; ++i) {
         const int c = w * LOC_CPW + i;
@@ -488,78 +500,67 @@ __global__ __launch_bounds__(LOC_THREADS) void sd_local_kernel(
         if (ok[i] && qa[i] == 0) s_h[c][d] = (uint16_t)__popcll(eq);
     }
     __syncthreads();
-    // column prefix: thread (digit d, quarter q) scans 16 chunks, then the
-    // four quarter sums are combined
+    // column prefix: thread (digit d, part q) scans LOC_CHUNKS / LOC_PARTS
+    // chunks, then the part sums are combined
     {
+        constexpr int CP = LOC_CHUNKS / LOC_PARTS;
         const int d = tid & 63, q = tid >> 6;
-        uint16_t h[LOC_CHUNKS / 4];
+        uint16_t h[CP];
         uint32_t sum = 0;
 #pragma unroll
-        for (int c = 0; c < LOC_CHUNKS / 4; ++c) {
-            h[c] = s_h[q * (LOC_CHUNKS / 4) + c][d];
+        for (int c = 0; c < CP; ++c) {
+            h[c] = s_h[q * CP + c][d];
             sum += h[c];
         }
         s_part[q][d] = sum;
         __syncthreads();
         uint32_t run = 0, tot = 0;
 #pragma unroll
-        for (int x = 0; x < 4; ++x) {
+        for (int x = 0; x < LOC_PARTS; ++x) {
             const uint32_t v = s_part[x][d];
             if (x < q) run += v;
             tot += v;
         }
 #pragma unroll
-        for (int c = 0; c < LOC_CHUNKS / 4; ++c) {
-            s_h[q * (LOC_CHUNKS / 4) + c][d] = (uint16_t)run;
+        for (int c = 0; c < CP; ++c) {
+            s_h[q * CP + c][d] = (uint16_t)run;
             run += h[c];
         }
         if (q == 0) {
-            s_tot[d] = tot;
-            s_lstart[d] = wave_excl_scan(tot);
+            const uint32_t incl = wave_incl_scan(tot);
+            s_lstart[d] = incl - tot;
+            if (d == 63) s_lstart[64] = incl;
         }
     }
     __syncthreads();
-    for (int c = w * LOC_CPW; c < (w + 1) * LOC_CPW; ++c) {
-        s_pl[c][lane] = (uint16_t)wave_excl_scan(s_h[c][lane]);
-    }
+    for (int c = w * LOC_CPW; c < (w + 1) * LOC_CPW; ++c) s_pl[c][lane] = (uint16_t)wave_excl_scan(s_h[c][lane]);
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < LOC_CPW; ++i) {
         if (ok[i]) {
             const int c = w * LOC_CPW + i;
             const uint32_t d = (t[i] >> 6) & 63;
-            const uint32_t j = s_lstart[d] + s_h[c][d] + qa[i];
-            s_st[j] = t[i];
-            s_sa[j] = acc[i] + s_pl[c][d] + la[i];
+            s_low[s_lstart[d] + s_h[c][d] + qa[i]] = (uint8_t)(t[i] & 63);
+            slot[t[i] & (LOCAL_SPAN - 1)] = acc[i] + s_pl[c][d] + la[i];
         }
     }
     __syncthreads();
 
-    // ---- level B: bits 0..5 inside each 64-range (at most 64 elements)
+    // ---- level B: bits 0..5 inside each 64-range (at most 64 elements,
+    // all with different t, so their six low bits are distinct)
     for (int g = w; g < 64; g += LOC_WAVES) {
-        const uint32_t cnt = s_tot[g];
         const uint32_t base = s_lstart[g];
-        const bool okb = (uint32_t)lane < cnt;
-        const uint32_t tb = okb ? s_st[base + lane] : 0u;
-        const uint32_t ab = okb ? s_sa[base + lane] : 0u;
-        uint32_t lt;
-        rank_digit<6>(tb & 63, ballot(okb), &lt);
-        // slot[] aliases the level-A tables, which are dead after the barrier
-        if (okb) slot[tb & (LOCAL_SPAN - 1)] = ab + lt;
+        const bool okb = (uint32_t)lane < s_lstart[g + 1] - base;
+        const uint32_t lb = okb ? s_low[base + lane] : 0u;
+        const uint32_t lt = count_smaller_distinct6(lb, okb);
+        if (okb) slot[g * 64 + lb] += lt;
     }
     __syncthreads();
 
     // ---- D in t order: Z(t) from a block scan of cold flags
-    constexpr int PER = LOCAL_SPAN / LOC_THREADS;   // 16
-    const uint64_t tbase = r0 + (uint64_t)tid * PER;
-    uint32_t p[PER];
     uint32_t cold = 0;
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const uint64_t tt = tbase + j;
-        p[j] = tt < n ? prev[tt] : 0u;
-        cold += (tt < n && p[j] == NONE) ? 1u : 0u;
-    }
+    for (int j = 0; j < PER; ++j) cold += (tbase + j < n && p[j] == NONE) ? 1u : 0u;
     uint32_t allcold;
     uint32_t z = Zc[blockIdx.x] + block_excl_scan(cold, s_tmp, &allcold);
 #pragma unroll
