@@ -277,61 +277,39 @@ __device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
     return (uint64_t)lo | ((uint64_t)hi << 32);
 }
 
-// Previous (DIR = -1) or next (DIR = +1) element with the same full key for
-// lanes whose adjacent element shares the low key bits but not the key.  The
-// wave's valid lanes [0, last] hold consecutive sorted positions, so the
-// search first walks them with shuffles (all lanes of the wave together, no
-// memory latency); a lane that runs past the wave's edge continues in memory
-// for a few batches on its own, and a lane still unresolved after that (a
-// long run, e.g. a hot key sharing its low bits with another key) is taken
-// over by the whole wave, 64 positions per step.  Those wave steps are
-// charged to the workgroup's budget (*budget, in positions); when it runs
-// out the lane gives up and *overflow is raised, which switches on the
-// passes over the high key bits and a second link.
-template <int DIR>
-__device__ __forceinline__ uint32_t mixed_neighbour(const uint64_t *__restrict__ sk,
-                                                    const uint32_t *__restrict__ st, uint64_t n,
-                                                    uint64_t i, uint64_t k, uint32_t t, bool need,
-                                                    uint32_t res, int lane, int last, int32_t *budget,
-                                                    int32_t *__restrict__ overflow) {
-    for (int d = 2;; ++d) {
-        const int src = lane + DIR * d;
-        const bool inwave = src >= 0 && src <= last;
-        const bool active = need && inwave;
-        if (ballot(active) == 0) break;
-        const int from = inwave ? src : lane;
-        const uint64_t kk = shfl64(k, from);
-        const uint32_t tt = (uint32_t)__shfl((int)t, from, WAVE);
-        if (active) {
-            if (kk == k) {
-                res = tt;
-                need = false;
-            } else if (!same_low(kk, k)) {
-                res = NONE;
-                need = false;
-            }
-        }
-    }
+// Previous (dir = -1) or next (dir = +1) element with the same full key as
+// sorted position i, whose adjacent element shares the low key bits but not
+// the key.  Lanes resolve such requests independently: each scans a few
+// batches on its own; a lane still unresolved after that (a long run, e.g. a
+// hot key sharing its low bits with another key) is taken over by the whole
+// wave, 64 positions per step.  The wave steps are charged to the
+// workgroup's budget (*budget, in positions); when it runs out the lane gives
+// up and *overflow is raised, which switches on the passes over the high key
+// bits and a second link.  All lanes of the wave must call this together.
+__device__ __forceinline__ uint32_t resolve_mixed(const uint64_t *__restrict__ sk, const uint32_t *__restrict__ st,
+                                                  uint64_t n, bool active, uint64_t i, int dir, int lane,
+                                                  int32_t *budget, int32_t *__restrict__ overflow) {
+    uint32_t res = NONE;
+    uint64_t k = 0;
     int64_t cont = 0;
-    if (need) {
-        // positions i+DIR .. i+DIR*e were examined inside the wave
-        const int e = DIR < 0 ? (lane > 1 ? lane : 1) : (last - lane > 1 ? last - lane : 1);
-        const int64_t from = (int64_t)i + DIR * (e + 1);
-        res = NONE;
-        need = false;
+    bool need = false;
+    if (active) {
+        k = sk[i];
+        const int64_t from = (int64_t)i + 2 * dir;   // i + dir is the known different key
         if (from >= 0 && (uint64_t)from < n) {
             uint64_t hit;
-            if (scan_run(sk, n, k, (uint64_t)from, DIR, LINK_SCAN_LIMIT, &hit)) {
+            if (scan_run(sk, n, k, (uint64_t)from, dir, LINK_SCAN_LIMIT, &hit)) {
                 if (hit != ~0ull) res = st[hit];
             } else {
                 need = true;
-                cont = from + DIR * (int64_t)LINK_SCAN_LIMIT;
+                cont = from + dir * (int64_t)LINK_SCAN_LIMIT;
             }
         }
     }
     for (uint64_t pending = ballot(need); pending; pending &= pending - 1) {
         const int L = __builtin_ctzll(pending);
         const uint64_t kL = shfl64(k, L);
+        const int dL = __shfl(dir, L, WAVE);
         int64_t pos = (int64_t)shfl64((uint64_t)cont, L);
         uint32_t found = NONE;
         for (;;) {
@@ -342,16 +320,16 @@ __device__ __forceinline__ uint32_t mixed_neighbour(const uint64_t *__restrict__
                 if (lane == 0) atomicOr(overflow, 1);
                 break;
             }
-            const int64_t x = pos + DIR * lane;
+            const int64_t x = pos + dL * lane;
             const uint64_t kk = (x >= 0 && (uint64_t)x < n) ? sk[x] : ~kL;
             const uint64_t hitm = ballot(kk == kL);
             const uint64_t ev = hitm | ballot(!same_low(kk, kL));
             if (ev) {
                 const int f = __builtin_ctzll(ev);
-                if ((hitm >> f) & 1) found = st[pos + DIR * f];
+                if ((hitm >> f) & 1) found = st[pos + dL * f];
                 break;
             }
-            pos += DIR * WAVE;
+            pos += dL * WAVE;
         }
         if (lane == L) res = found;
     }
@@ -375,6 +353,7 @@ struct PermLds {
     uint32_t bucket[PERM_RADIX];
     uint32_t tmp[PERM_THREADS / WAVE];
     int32_t budget;   // positions the link may still scan for long mixed runs
+    uint32_t nmixed;  // mixed-run requests of the current tile (the list lives in `stage`)
 };
 
 template <bool FROM_SORT>
@@ -382,20 +361,19 @@ __device__ __forceinline__ void perm_partition_body(
     PermLds &L, const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t,
     const uint64_t *__restrict__ in_pn, uint64_t n, int s, uint64_t per_wg, uint32_t *__restrict__ cursor,
     uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn, bool full, int32_t *__restrict__ overflow) {
-    uint32_t *s_stage = reinterpret_cast<uint32_t *>(L.stage), *s_cnt = L.cnt, *s_lstart = L.lstart, *s_cur = L.cur, *s_bucket = L.bucket,
-             *s_tmp = L.tmp;
+    uint32_t *s_stage = reinterpret_cast<uint32_t *>(L.stage), *s_cnt = L.cnt, *s_lstart = L.lstart,
+             *s_cur = L.cur, *s_bucket = L.bucket, *s_tmp = L.tmp;
     constexpr int DPT = PERM_RADIX / PERM_THREADS;   // digits per thread
-    const int tid = threadIdx.x;
-    const int lane = tid & (WAVE - 1);
     // positions fit 32 bits (n < 2^32 - 1); offsets from a tile's base are
     // compared against what is left, so nothing wraps near the end
     if ((uint64_t)blockIdx.x * per_wg >= n) return;
+    const int tid0 = threadIdx.x;   // the tile loop below takes its own copy
     const uint32_t lo = (uint32_t)((uint64_t)blockIdx.x * per_wg);
     const uint32_t hi = (uint64_t)lo + per_wg < n ? (uint32_t)(lo + per_wg) : (uint32_t)n;
 
     // ---- count the chunk's digits and reserve one run per digit
-    for (int i = tid; i < PERM_RADIX; i += PERM_THREADS) s_cnt[i] = 0;
-    if (tid == 0) L.budget = (int32_t)(2 * (hi - lo) + 4096);
+    for (int i = tid0; i < PERM_RADIX; i += PERM_THREADS) s_cnt[i] = 0;
+    if (tid0 == 0) L.budget = (int32_t)(2 * (hi - lo) + 4096);
     __syncthreads();
     // eight loads in flight per thread before their LDS updates
     for (uint32_t b0 = lo; b0 < hi; b0 += 8 * PERM_THREADS) {
@@ -403,12 +381,12 @@ __device__ __forceinline__ void perm_partition_body(
         uint32_t tt[8];
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            const uint32_t o = (uint32_t)(q * PERM_THREADS + tid);
+            const uint32_t o = (uint32_t)(q * PERM_THREADS + tid0);
             tt[q] = o < left ? (in_t + b0)[o] : 0u;
         }
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            if ((uint32_t)(q * PERM_THREADS + tid) < left) {
+            if ((uint32_t)(q * PERM_THREADS + tid0) < left) {
                 const uint32_t d = (tt[q] >> s) & (PERM_RADIX - 1);
                 atomicAdd(&s_cnt[d], 1u);
                 s_bucket[d] = tt[q] >> s;   // every writer of digit d writes the same bucket
@@ -418,7 +396,7 @@ __device__ __forceinline__ void perm_partition_body(
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < DPT; ++q) {
-        const int d = tid * DPT + q;
+        const int d = tid0 * DPT + q;
         const uint32_t c = s_cnt[d];
         if (c) s_cur[d] = atomicAdd(&cursor[s_bucket[d]], c);
     }
@@ -427,7 +405,13 @@ __device__ __forceinline__ void perm_partition_body(
     // ---- stream the chunk tile by tile
     for (uint32_t base = lo; base < hi; base += PERM_TILE) {
         const uint32_t left = hi - base;
+        // an opaque copy of the thread index: values derived from it are
+        // recomputed per tile instead of being held (and spilled) across the loop
+        int tid = threadIdx.x;
+        __asm__ volatile("" : "+v"(tid));
+        const int lane = tid & (WAVE - 1);
         for (int i = tid; i < PERM_RADIX; i += PERM_THREADS) s_cnt[i] = 0;
+        if (tid == 0) L.nmixed = 0;
         __syncthreads();
         // per-tile base pointers keep the per-lane offsets 32-bit.  Every
         // load of the tile is issued before the first use, so a tile costs
@@ -464,6 +448,11 @@ __device__ __forceinline__ void perm_partition_body(
                     et = in_t[gp];
                 }
             }
+            // fast links from neighbours; a lane whose neighbour shares the
+            // low bits but not the key appends a request (offset, direction)
+            // to the tile's list, resolved below by the whole workgroup
+            uint32_t *mlist = reinterpret_cast<uint32_t *>(L.stage);   // 2 * PERM_TILE entries
+            uint32_t mixbits = 0;   // bit 2j: item j's prev is in the list, bit 2j+1: its next
 #pragma unroll
             for (int j = 0; j < PERM_ITEMS; ++j) {
                 const uint32_t o = (uint32_t)(j * PERM_THREADS + tid);
@@ -490,11 +479,49 @@ __device__ __forceinline__ void perm_partition_body(
                     if (has_next && kn == k[j]) nx = tn;
                     else mn = has_next && !full && same_low(kn, k[j]);
                 }
-                if (ballot(mp))
-                    pv = mixed_neighbour<-1>(sk, in_t, n, i, k[j], t[j], mp, pv, lane, last, &L.budget, overflow);
-                if (ballot(mn))
-                    nx = mixed_neighbour<+1>(sk, in_t, n, i, k[j], t[j], mn, nx, lane, last, &L.budget, overflow);
+                const uint64_t mpm = ballot(mp), mnm = ballot(mn);
+                if (mpm | mnm) {
+                    const uint32_t cnt = (uint32_t)__popcll(mpm) + (uint32_t)__popcll(mnm);
+                    uint32_t e0 = 0;
+                    if (lane == 0) e0 = atomicAdd(&L.nmixed, cnt);
+                    e0 = (uint32_t)__shfl((int)e0, 0, WAVE);
+                    if (mp) {
+                        const uint32_t e = e0 + mbcnt(mpm);
+                        mlist[e] = o << 1;
+                        pv = e;
+                        mixbits |= 1u << (2 * j);
+                    }
+                    if (mn) {
+                        const uint32_t e = e0 + (uint32_t)__popcll(mpm) + mbcnt(mnm);
+                        mlist[e] = (o << 1) | 1u;
+                        nx = e;
+                        mixbits |= 2u << (2 * j);
+                    }
+                }
                 pn[j] = (uint64_t)pv | ((uint64_t)nx << 32);
+            }
+            __syncthreads();
+            const uint32_t nm = L.nmixed;
+            if (nm) {
+                // resolve the list in place (entry -> time of the neighbour)
+                for (uint32_t e0 = 0; e0 < nm; e0 += PERM_THREADS) {
+                    const uint32_t e = e0 + tid;
+                    const bool act = e < nm;
+                    const uint32_t code = act ? mlist[e] : 0u;
+                    const uint32_t res = resolve_mixed(sk, in_t, n, act, (uint64_t)base + (code >> 1),
+                                                       (code & 1) ? 1 : -1, lane, &L.budget, overflow);
+                    if (act) mlist[e] = res;
+                }
+                __syncthreads();
+#pragma unroll
+                for (int j = 0; j < PERM_ITEMS; ++j) {
+                    if (mixbits & (3u << (2 * j))) {
+                        uint32_t pv = (uint32_t)pn[j], nx = (uint32_t)(pn[j] >> 32);
+                        if (mixbits & (1u << (2 * j))) pv = mlist[pv];
+                        if (mixbits & (2u << (2 * j))) nx = mlist[nx];
+                        pn[j] = (uint64_t)pv | ((uint64_t)nx << 32);
+                    }
+                }
             }
         } else {
 #pragma unroll
