@@ -17,7 +17,7 @@
 //     into digit bases;
 //   * each of the eight sort passes is a single "onesweep" kernel: a
 //     workgroup takes the next tile from an atomic counter (so every tile it
-//     waits on is already running), ranks its 4096 elements by digit with
+//     waits on is already running), ranks its 8192 elements by digit with
 //     wave ballots (stable: lanes in order, waves in order), publishes its
 //     per-digit counts and reads its predecessors' with a decoupled
 //     look-back, then writes the tile out through LDS so each digit run is a
@@ -33,8 +33,8 @@ namespace pc {
 constexpr int RADIX = 256;
 constexpr int SORT_THREADS = 512;
 constexpr int SORT_WAVES = SORT_THREADS / WAVE;
-constexpr int SORT_ITEMS = 8;
-constexpr int SORT_TILE = SORT_THREADS * SORT_ITEMS;   // 4096
+constexpr int SORT_ITEMS = 16;
+constexpr int SORT_TILE = SORT_THREADS * SORT_ITEMS;   // 8192
 constexpr int SORT_PASSES = 8;
 constexpr uint64_t FLAG_AGG = 1ull << 32;
 constexpr uint64_t FLAG_INC = 1ull << 33;
@@ -76,16 +76,18 @@ __global__ __launch_bounds__(RADIX) void sort_scan_kernel(const uint32_t *__rest
     }
 }
 
-__global__ __launch_bounds__(SORT_THREADS, 8) void sort_pass_kernel(
+__global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_kernel(
     const uint64_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
     uint64_t *__restrict__ keys_out, uint32_t *__restrict__ vals_out, uint64_t n, int shift,
     const uint32_t *__restrict__ start, uint64_t *__restrict__ status, uint32_t *__restrict__ counter,
     uint32_t epoch, int32_t *__restrict__ err, const int32_t *__restrict__ only_if) {
     // passes over the high key bits run only when the link step needs them
     if (only_if && *only_if == 0) return;
-    // LDS is kept under 40 KB so four workgroups share a CU: the tile is
-    // staged twice through one buffer (keys, then values) and the per-wave
-    // digit counters are 16-bit (a tile holds at most 4096 elements)
+    // Large tiles make each digit's run in the output long (about 32
+    // elements of 8192), so the scattered writes are mostly whole lines; the
+    // tile is staged twice through one buffer (keys, then values) and the
+    // per-wave digit counters are 16-bit (a tile holds at most 8192
+    // elements), which keeps two workgroups on a CU
     __shared__ uint64_t s_stage[SORT_TILE];
     __shared__ uint16_t s_wcnt[SORT_WAVES][RADIX];
     __shared__ uint32_t s_lstart[RADIX];
@@ -212,9 +214,12 @@ __global__ __launch_bounds__(SORT_THREADS, 8) void sort_pass_kernel(
 // pass therefore reserves its output runs with one global atomic per
 // (workgroup, digit) instead of a look-back, stages each tile digit-sorted
 // in LDS and writes each run contiguously.
-constexpr int PERM_THREADS = 512;
-constexpr int PERM_ITEMS = 8;
-constexpr int PERM_TILE = PERM_THREADS * PERM_ITEMS;   // 4096
+constexpr int LINK_THREADS = 512;
+constexpr int LINK_ITEMS = 8;                          // link: 4096-element tiles
+constexpr int LINK_TILE = LINK_THREADS * LINK_ITEMS;
+constexpr int PART_THREADS = 512;
+constexpr int PART_ITEMS = 16;                         // plain partition: 8192-element tiles
+constexpr int PERM_TILE = PART_THREADS * PART_ITEMS;   // the larger tile
 constexpr int PERM_RADIX = 1024;
 constexpr int PERM_LOCAL_BITS = 13;
 
@@ -341,28 +346,29 @@ __device__ __forceinline__ uint32_t resolve_mixed(const uint64_t *__restrict__ s
 // a single global atomic (so each bucket cursor sees one atomic per workgroup,
 // not per tile), then streams the chunk tile by tile: LDS counters give each
 // element its slot inside its digit, the tile is staged digit-sorted in LDS
-// (one array at a time through a single buffer, which keeps LDS at 32 KB so
-// four workgroups share a CU), and each digit's part is appended to the
-// workgroup's run.  A chunk spans at most 1024 consecutive buckets (see the
+// (times, then (prev, next) pairs, through a single buffer), and each
+// digit's part is appended to the workgroup's run.  Longer tiles give longer
+// runs per digit, hence fewer partially written lines; the link keeps 4096
+// because it holds keys and neighbours per element.  A chunk spans at most 1024 consecutive buckets (see the
 // plan), so digit = bucket mod 1024 names them without collision.
+template <int TILE, int THREADS>
 struct PermLds {
-    uint64_t stage[PERM_TILE];   // times (as u32), then (prev, next) pairs
+    uint64_t stage[TILE];   // bucket names while counting; per tile: times (as u32), then (prev, next) pairs
     uint32_t cnt[PERM_RADIX];
     uint32_t lstart[PERM_RADIX];
     uint32_t cur[PERM_RADIX];
-    uint32_t bucket[PERM_RADIX];
-    uint32_t tmp[PERM_THREADS / WAVE];
+    uint32_t tmp[THREADS / WAVE];
     int32_t budget;   // positions the link may still scan for long mixed runs
     uint32_t nmixed;  // mixed-run requests of the current tile (the list lives in `stage`)
 };
 
-template <bool FROM_SORT>
+template <bool FROM_SORT, int PERM_THREADS, int ITEMS>
 __device__ __forceinline__ void perm_partition_body(
-    PermLds &L, const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t,
+    PermLds<PERM_THREADS * ITEMS, PERM_THREADS> &L, const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t,
     const uint64_t *__restrict__ in_pn, uint64_t n, int s, uint64_t per_wg, uint32_t *__restrict__ cursor,
     uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn, bool full, int32_t *__restrict__ overflow) {
     uint32_t *s_stage = reinterpret_cast<uint32_t *>(L.stage), *s_cnt = L.cnt, *s_lstart = L.lstart,
-             *s_cur = L.cur, *s_bucket = L.bucket, *s_tmp = L.tmp;
+             *s_cur = L.cur, *s_bucket = reinterpret_cast<uint32_t *>(L.stage), *s_tmp = L.tmp;
     constexpr int DPT = PERM_RADIX / PERM_THREADS;   // digits per thread
     // positions fit 32 bits (n < 2^32 - 1); offsets from a tile's base are
     // compared against what is left, so nothing wraps near the end
@@ -403,7 +409,8 @@ __device__ __forceinline__ void perm_partition_body(
     __syncthreads();
 
     // ---- stream the chunk tile by tile
-    for (uint32_t base = lo; base < hi; base += PERM_TILE) {
+    constexpr int TILE = PERM_THREADS * ITEMS;
+    for (uint32_t base = lo; base < hi; base += TILE) {
         const uint32_t left = hi - base;
         // an opaque copy of the thread index: values derived from it are
         // recomputed per tile instead of being held (and spilled) across the loop
@@ -417,15 +424,15 @@ __device__ __forceinline__ void perm_partition_body(
         // load of the tile is issued before the first use, so a tile costs
         // one memory latency, not one per item.
         const uint32_t *tb = in_t + base;
-        uint32_t t[PERM_ITEMS], pos[PERM_ITEMS];
-        uint64_t pn[PERM_ITEMS];   // prev | next << 32
-        bool ok[PERM_ITEMS];
+        uint32_t t[ITEMS], pos[ITEMS];
+        uint64_t pn[ITEMS];   // prev | next << 32
+        bool ok[ITEMS];
         if (FROM_SORT) {
             const uint64_t *kb = sk + base;
             const int w = tid / WAVE;
-            uint64_t k[PERM_ITEMS];
+            uint64_t k[ITEMS];
 #pragma unroll
-            for (int j = 0; j < PERM_ITEMS; ++j) {
+            for (int j = 0; j < ITEMS; ++j) {
                 const uint32_t o = (uint32_t)(j * PERM_THREADS + tid);
                 ok[j] = o < left;
                 const uint32_t oc = ok[j] ? o : 0u;
@@ -451,10 +458,10 @@ __device__ __forceinline__ void perm_partition_body(
             // fast links from neighbours; a lane whose neighbour shares the
             // low bits but not the key appends a request (offset, direction)
             // to the tile's list, resolved below by the whole workgroup
-            uint32_t *mlist = reinterpret_cast<uint32_t *>(L.stage);   // 2 * PERM_TILE entries
+            uint32_t *mlist = reinterpret_cast<uint32_t *>(L.stage);   // 2 * TILE entries
             uint32_t mixbits = 0;   // bit 2j: item j's prev is in the list, bit 2j+1: its next
 #pragma unroll
-            for (int j = 0; j < PERM_ITEMS; ++j) {
+            for (int j = 0; j < ITEMS; ++j) {
                 const uint32_t o = (uint32_t)(j * PERM_THREADS + tid);
                 const uint64_t i = (uint64_t)base + o;
                 // consecutive lanes hold consecutive sorted positions: the
@@ -514,7 +521,7 @@ __device__ __forceinline__ void perm_partition_body(
                 }
                 __syncthreads();
 #pragma unroll
-                for (int j = 0; j < PERM_ITEMS; ++j) {
+                for (int j = 0; j < ITEMS; ++j) {
                     if (mixbits & (3u << (2 * j))) {
                         uint32_t pv = (uint32_t)pn[j], nx = (uint32_t)(pn[j] >> 32);
                         if (mixbits & (1u << (2 * j))) pv = mlist[pv];
@@ -525,7 +532,7 @@ __device__ __forceinline__ void perm_partition_body(
             }
         } else {
 #pragma unroll
-            for (int j = 0; j < PERM_ITEMS; ++j) {
+            for (int j = 0; j < ITEMS; ++j) {
                 const uint32_t o = (uint32_t)(j * PERM_THREADS + tid);
                 ok[j] = o < left;
                 const uint32_t oc = ok[j] ? o : 0u;
@@ -534,7 +541,7 @@ __device__ __forceinline__ void perm_partition_body(
             }
         }
 #pragma unroll
-        for (int j = 0; j < PERM_ITEMS; ++j)
+        for (int j = 0; j < ITEMS; ++j)
             if (ok[j]) pos[j] = atomicAdd(&s_cnt[(t[j] >> s) & (PERM_RADIX - 1)], 1u);
         __syncthreads();
         uint32_t c[DPT], mine = 0, total;
@@ -551,16 +558,16 @@ __device__ __forceinline__ void perm_partition_body(
         }
         __syncthreads();
 #pragma unroll
-        for (int j = 0; j < PERM_ITEMS; ++j) {
+        for (int j = 0; j < ITEMS; ++j) {
             if (!ok[j]) continue;
             pos[j] += s_lstart[(t[j] >> s) & (PERM_RADIX - 1)];
             s_stage[pos[j]] = t[j];
         }
         __syncthreads();
         // times out, remembering each slot's destination for the (prev, next) pairs
-        uint32_t dst[PERM_ITEMS];
+        uint32_t dst[ITEMS];
 #pragma unroll
-        for (int r = 0; r < PERM_ITEMS; ++r) {
+        for (int r = 0; r < ITEMS; ++r) {
             const uint32_t slot = (uint32_t)(tid + r * PERM_THREADS);
             dst[r] = ~0u;
             if (slot < total) {
@@ -572,11 +579,11 @@ __device__ __forceinline__ void perm_partition_body(
         }
         __syncthreads();
 #pragma unroll
-        for (int j = 0; j < PERM_ITEMS; ++j)
+        for (int j = 0; j < ITEMS; ++j)
             if (ok[j]) L.stage[pos[j]] = pn[j];
         __syncthreads();
 #pragma unroll
-        for (int r = 0; r < PERM_ITEMS; ++r)
+        for (int r = 0; r < ITEMS; ++r)
             if (dst[r] < n) out_pn[dst[r]] = L.stage[tid + r * PERM_THREADS];
 #pragma unroll
         for (int q = 0; q < DPT; ++q) s_cur[tid * DPT + q] += c[q];
@@ -589,21 +596,21 @@ __device__ __forceinline__ void perm_partition_body(
 // (over keys sorted by their low 32 bits) raises *flag when a mixed run is too
 // long to scan; the second one runs only then (only_if = flag), over fully
 // sorted keys.
-__global__ __launch_bounds__(PERM_THREADS, 4) void link_partition_kernel(
+__global__ __launch_bounds__(LINK_THREADS, 4) void link_partition_kernel(
     const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t, uint64_t n, int s, uint64_t per_wg,
     uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn,
     const int32_t *__restrict__ only_if, int32_t *__restrict__ flag) {
     if (only_if && *only_if == 0) return;
-    __shared__ PermLds L;
-    perm_partition_body<true>(L, sk, in_t, nullptr, n, s, per_wg, cursor, out_t, out_pn, only_if != nullptr,
+    __shared__ PermLds<LINK_TILE, LINK_THREADS> L;
+    perm_partition_body<true, LINK_THREADS, LINK_ITEMS>(L, sk, in_t, nullptr, n, s, per_wg, cursor, out_t, out_pn, only_if != nullptr,
                               flag);
 }
 
-__global__ __launch_bounds__(PERM_THREADS, 6) void perm_partition_kernel(
+__global__ __launch_bounds__(PART_THREADS, 4) void perm_partition_kernel(
     const uint32_t *__restrict__ in_t, const uint64_t *__restrict__ in_pn, uint64_t n, int s, uint64_t per_wg,
     uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn) {
-    __shared__ PermLds L;
-    perm_partition_body<false>(L, nullptr, in_t, in_pn, n, s, per_wg, cursor, out_t, out_pn, true, nullptr);
+    __shared__ PermLds<PERM_TILE, PART_THREADS> L;
+    perm_partition_body<false, PART_THREADS, PART_ITEMS>(L, nullptr, in_t, in_pn, n, s, per_wg, cursor, out_t, out_pn, true, nullptr);
 }
 
 // cursor[b] = b << s: each bucket's output run starts at its first t
@@ -773,7 +780,7 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
             // first link, over keys sorted by their low 32 bits
             PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg0), dim3(256), 0, s, w.cursor, pp.buckets[0],
                       pp.s[0]);
-            PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ptiles), dim3(pc::PERM_THREADS), 0, s, kin, vin,
+            PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ptiles), dim3(pc::LINK_THREADS), 0, s, kin, vin,
                       n, pp.s[0], per_wg, w.cursor, bt[0], bpn[0], (const int32_t *)nullptr, need_high);
             PC_LAUNCH(pc::K_SORT_HIST, pc::sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n,
                       pc::SORT_PASSES / 2, w.hist, (const int32_t *)need_high);
@@ -790,7 +797,7 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
     }
     // second link, over fully sorted keys, only if the first one gave up
     PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg0), dim3(256), 0, s, w.cursor, pp.buckets[0], pp.s[0]);
-    PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ptiles), dim3(pc::PERM_THREADS), 0, s, kin, vin, n,
+    PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ptiles), dim3(pc::LINK_THREADS), 0, s, kin, vin, n,
               pp.s[0], per_wg, w.cursor, bt[0], bpn[0], (const int32_t *)need_high, (int32_t *)nullptr);
     int cur = 0;
     for (int i = 1; i < pp.passes; ++i) {
@@ -798,7 +805,7 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
         PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg), dim3(256), 0, s, w.cursor, pp.buckets[i],
                   pp.s[i]);
         const int nxt = cur ^ 1;
-        PC_LAUNCH(pc::K_PERM, pc::perm_partition_kernel, dim3(ptiles), dim3(pc::PERM_THREADS), 0, s, bt[cur],
+        PC_LAUNCH(pc::K_PERM, pc::perm_partition_kernel, dim3(ptiles), dim3(pc::PART_THREADS), 0, s, bt[cur],
                   bpn[cur], n, pp.s[i], per_wg, w.cursor, bt[nxt], bpn[nxt]);
         cur = nxt;
     }
