@@ -43,6 +43,62 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+# HIP kernel behind each timed kernel id (for the committed counter summary)
+HIP_KERNEL = {"sort_onesweep_pass": "pc::sort_pass_kernel", "link_partition": "pc::link_partition_kernel",
+              "perm_partition": "pc::perm_partition_kernel", "hash_digest": "pc::hash_digest_kernel",
+              "hash_chain": "pc::hash_chain_kernel", "sd_local_finish": "pc::sd_local_kernel",
+              "perm_local": "pc::perm_local_kernel", "mrc_hist": "pc::mrc_hist_kernel"}
+PROFILE = os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9.md")
+
+
+def source_sha256():
+    """Hash of the library sources and header, as recorded with the counters."""
+    import hashlib
+    h = hashlib.sha256()
+    src = os.path.join(ROOT, "paper_2609_28870_amd", "csrc")
+    for f in sorted(os.listdir(src)):
+        with open(os.path.join(src, f), "rb") as fh:
+            h.update(fh.read())
+    with open(os.path.join(ROOT, "include", "pc.h"), "rb") as fh:
+        h.update(fh.read())
+    return h.hexdigest()
+
+
+def _profile_blob():
+    try:
+        text = open(PROFILE).read()
+        blob = json.loads(text[text.index("```json") + 7:text.rindex("```")])
+    except (OSError, ValueError):
+        return None
+    return blob if blob.get("source_sha256") == source_sha256() else None
+
+
+def measured_stage_bytes(stage_of):
+    """Measured HBM bytes per pipeline run of each stage (sum over its
+    kernels' working launches) from the committed counter summary, or None
+    when the library has changed since."""
+    blob = _profile_blob()
+    if blob is None:
+        return None
+    out = {}
+    for e in blob["kernels"].values():
+        st = stage_of(e["id"])
+        out[st] = out.get(st, 0.0) + (e["read_bytes"] + e["write_bytes"]) * e["launches_per_run"]
+    return out
+
+
+def measured_traffic(kernel_id):
+    """HBM bytes per working launch of a kernel from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary (calibrated on a plain copy), or None when
+    the library has changed since those counters were taken."""
+    blob = _profile_blob()
+    entry = blob["kernels"].get(HIP_KERNEL.get(kernel_id, "")) if blob else None
+    if entry is None:
+        return None
+    return {"read_bytes": entry["read_bytes"], "write_bytes": entry["write_bytes"],
+            "profiled_avg_ms": entry["avg_ms"], "source": os.path.relpath(PROFILE, ROOT)}
+
+
 def cpu_baseline(trace, caps, alpha, beta, budget_accesses):
     """The oracle (plain C, one thread) over the first requests of the same
     trace: hash, prev/next, next-use histogram and one LRU simulation per
@@ -162,19 +218,30 @@ def main():
     roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None}
     roof["kernel"] = dom
-    roof["traffic"] = None
+    mt = measured_traffic(dom)
+    roof["traffic"] = mt["read_bytes"] + mt["write_bytes"] if mt else None
+    if mt:
+        mt["GBps_at_this_run"] = round(roof["traffic"] / (d["avg_working_launch_ms"] / 1e3) / 1e9, 1)
+    roof["traffic_detail"] = mt
     stage_of = {"hash_digest": "hash", "hash_chain": "hash", "sort_digit_hist": "prev_next",
                 "sort_digit_scan": "prev_next", "sort_onesweep_pass": "prev_next",
                 "link_partition": "prev_next",
                 "perm_partition": "prev_next", "perm_local": "prev_next", "mrc_hist": "mrc",
                 "mrc_cost": "mrc"}
     stage_bytes = {"hash": 4 * B + 8 + 4, "prev_next": 16, "stack_distance": 8, "mrc": 12}
+
+    def stage_name(kid):
+        return stage_of.get(kid, "stack_distance" if kid.startswith("sd_") else "other")
+
     stages = {}
     for name, e in kernels.items():
-        st_name = stage_of.get(name, "stack_distance" if name.startswith("sd_") else "other")
+        st_name = stage_name(name)
         stages[st_name] = stages.get(st_name, 0.0) + e["ms_per_step"]
+    measured = measured_stage_bytes(stage_name)
     stages = {k: {"ms_per_step": round(v, 3),
-                  "algo_GBps": round(stage_bytes[k] * n_blocks / v / 1e6, 1) if k in stage_bytes else None}
+                  "algo_GBps": round(stage_bytes[k] * n_blocks / v / 1e6, 1) if k in stage_bytes else None,
+                  # counter-measured bytes (committed summary) over this run's time
+                  "measured_GBps": round(measured[k] / v / 1e6, 1) if measured and k in measured else None}
               for k, v in stages.items()}
 
     # the curves themselves (exact integers -> float64 ratios)
