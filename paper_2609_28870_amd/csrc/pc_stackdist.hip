@@ -21,7 +21,7 @@
 //
 // Buckets are ranges of t, so their sizes are known in advance from the
 // per-4096 prefix of cold counts: #non-cold t < X = X - Z(X).
-//   * sd_cold_count + sd_scan      -> Z at every multiple of 4096
+//   * sd_cold_count + a three-step scan -> Z at every multiple of 4096
 //   * per level (1-3 levels of 8-bit digits above bit 12), over tiles of 1024
 //     elements: sd_count (per-tile digit counts), a segmented scan of those
 //     counts over the tiles of each bucket (sd_seg: reduce, carry, scan --
@@ -91,6 +91,43 @@ __global__ __launch_bounds__(SCAN_THREADS) void sd_scan_kernel(const uint32_t *_
         run += x;
     }
     if (threadIdx.x == 0) out[m] = total;
+}
+
+// Exclusive scan of m values over many workgroups (the per-4096 cold counts
+// number n / 4096): block sums, one workgroup scans the sums, every block
+// scans itself on top of its offset.  out[m] = total.
+constexpr int SCAN_BLOCK = SCAN_THREADS * 4;
+__global__ __launch_bounds__(SCAN_THREADS) void sd_scan_reduce_kernel(const uint32_t *__restrict__ in, uint64_t m,
+                                                                      uint32_t *__restrict__ part) {
+    __shared__ uint32_t tmp[SCAN_THREADS / WAVE];
+    const uint64_t i0 = (uint64_t)blockIdx.x * SCAN_BLOCK + (uint64_t)threadIdx.x * 4;
+    uint32_t x = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) x += i0 + q < m ? in[i0 + q] : 0u;
+    uint32_t total;
+    block_excl_scan(x, tmp, &total);
+    if (threadIdx.x == 0) part[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(SCAN_THREADS) void sd_scan_apply_kernel(const uint32_t *__restrict__ in, uint64_t m,
+                                                                     const uint32_t *__restrict__ part_ex,
+                                                                     uint64_t nblocks, uint32_t *__restrict__ out) {
+    __shared__ uint32_t tmp[SCAN_THREADS / WAVE];
+    const uint64_t i0 = (uint64_t)blockIdx.x * SCAN_BLOCK + (uint64_t)threadIdx.x * 4;
+    uint32_t v[4], x = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        v[q] = i0 + q < m ? in[i0 + q] : 0u;
+        x += v[q];
+    }
+    uint32_t total;
+    uint32_t run = part_ex[blockIdx.x] + block_excl_scan(x, tmp, &total);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        if (i0 + q < m) out[i0 + q] = run;
+        run += v[q];
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) out[m] = part_ex[nblocks];
 }
 
 // tiles per bucket of a dominance pass (bucket = t >> S)
@@ -252,31 +289,48 @@ __global__ __launch_bounds__(DOM_RADIX) void sd_seg_reduce_kernel(const uint16_t
     if (d == 0) ghas[blockIdx.x] = has;
 }
 
-// B: carry into every group (one workgroup, thread = digit)
-__global__ __launch_bounds__(DOM_RADIX) void sd_seg_carry_kernel(const uint32_t *__restrict__ gsum,
-                                                                 const uint8_t *__restrict__ ghas,
-                                                                 const uint32_t *tfirst_end, uint64_t fixed,
-                                                                 uint32_t *__restrict__ gin) {
+// B: carry into every group: per digit (one workgroup each), a segmented
+// scan over the groups where a group holding a bucket start restarts the
+// sum.  Inside a wave: the plain prefix sum minus the sum before the last
+// start at or below the lane (found with a ballot); across the waves of a
+// 1024-group chunk and across chunks: a short serial carry.
+constexpr int CARRY_THREADS = 1024;
+__global__ __launch_bounds__(CARRY_THREADS) void sd_seg_carry_kernel(const uint32_t *__restrict__ gsum,
+                                                                     const uint8_t *__restrict__ ghas,
+                                                                     const uint32_t *tfirst_end, uint64_t fixed,
+                                                                     uint32_t *__restrict__ gin) {
+    __shared__ uint32_t s_val[CARRY_THREADS / WAVE];
+    __shared__ uint32_t s_has[CARRY_THREADS / WAVE];
     const uint64_t rows = total_tiles(tfirst_end, fixed);
     const uint64_t groups = (rows + SEG_GROUP - 1) / SEG_GROUP;
-    const int d = threadIdx.x;
-    uint32_t carry = 0;
-    for (uint64_t g = 0; g < groups; g += SEG_BATCH) {
-        uint32_t v[SEG_BATCH];
-        bool h[SEG_BATCH];
-#pragma unroll
-        for (int q = 0; q < SEG_BATCH; ++q) {
-            const bool in = g + q < groups;
-            v[q] = in ? gsum[(g + q) * DOM_RADIX + d] : 0u;
-            h[q] = in && ghas[g + q];
+    const int d = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & (WAVE - 1), w = tid / WAVE;
+    uint32_t carry = 0;   // carry into the current chunk
+    for (uint64_t g0 = 0; g0 < groups; g0 += CARRY_THREADS) {
+        const uint64_t g = g0 + tid;
+        const bool in = g < groups;
+        const bool f = in && ghas[g];
+        const uint32_t v = in ? gsum[g * DOM_RADIX + d] : 0u;
+        const uint32_t S = wave_incl_scan(v);
+        const uint64_t fm = ballot(f);
+        const uint64_t le = fm & (lane == WAVE - 1 ? ~0ull : ((2ull << lane) - 1));   // starts at or below me
+        const int last = le ? 63 - __builtin_clzll(le) : -1;
+        const uint32_t before = (uint32_t)__shfl((int)S, last > 0 ? last - 1 : 0, WAVE);
+        const uint32_t seg = last > 0 ? S - before : S;   // sum since the last start (or since lane 0)
+        if (lane == WAVE - 1) {
+            s_val[w] = seg;
+            s_has[w] = fm != 0;
         }
-#pragma unroll
-        for (int q = 0; q < SEG_BATCH; ++q) {
-            if (g + q < groups) {
-                gin[(g + q) * DOM_RADIX + d] = carry;
-                carry = h[q] ? v[q] : carry + v[q];
-            }
-        }
+        __syncthreads();
+        uint32_t cin = carry;   // carry into this wave
+        for (int x = 0; x < w; ++x) cin = s_has[x] ? s_val[x] : cin + s_val[x];
+        uint32_t chunk_out = cin;
+        for (int x = w; x < CARRY_THREADS / WAVE; ++x) chunk_out = s_has[x] ? s_val[x] : chunk_out + s_val[x];
+        const uint32_t incl = last >= 0 ? seg : cin + seg;   // carry after group g
+        const uint32_t prev = (uint32_t)__shfl_up((int)incl, 1, WAVE);
+        if (in) gin[g * DOM_RADIX + d] = lane == 0 ? cin : prev;
+        carry = chunk_out;
+        __syncthreads();
     }
 }
 
@@ -615,7 +669,7 @@ static SdPlan plan_sd(uint64_t n) {
 
 struct SdWs {
     int32_t *hdr;
-    uint32_t *cold, *Zc, *tcount, *tfirst;
+    uint32_t *cold, *Zc, *tcount, *tfirst, *part, *part_ex;
     uint32_t *at, *aa, *bt, *ba;
     uint16_t *cnt;
     uint8_t *seg, *ghas;
@@ -631,6 +685,9 @@ static SdWs carve_sd(void *ws, uint64_t n, const SdPlan &p) {
     w.hdr = c.take<int32_t>(WS_HEADER / sizeof(int32_t));
     w.cold = c.take<uint32_t>(nchunks + 1);
     w.Zc = c.take<uint32_t>(nchunks + 2);
+    const uint64_t nblocks = (nchunks + SCAN_BLOCK - 1) / SCAN_BLOCK;
+    w.part = c.take<uint32_t>(nblocks + 1);
+    w.part_ex = c.take<uint32_t>(nblocks + 2);
     w.tcount = c.take<uint32_t>(p.max_buckets + 1);
     w.tfirst = c.take<uint32_t>(p.max_buckets + 2);
     w.at = c.take<uint32_t>(n);
@@ -672,8 +729,13 @@ pc_status pc_stack_distance(const uint32_t *prev, const uint32_t *next, uint64_t
     const uint64_t nchunks = (n + pc::LOCAL_SPAN - 1) / pc::LOCAL_SPAN;
     PC_LAUNCH(pc::K_SD_COLD, pc::sd_cold_count_kernel, dim3((unsigned)nchunks), dim3(256), 0, s, prev, n,
               w.cold);
-    PC_LAUNCH(pc::K_SD_SCAN, pc::sd_scan_kernel, dim3(1), dim3(pc::SCAN_THREADS), 0, s, w.cold, nchunks,
-              w.Zc);
+    const uint64_t nblocks = (nchunks + pc::SCAN_BLOCK - 1) / pc::SCAN_BLOCK;
+    PC_LAUNCH(pc::K_SD_SCAN, pc::sd_scan_reduce_kernel, dim3((unsigned)nblocks), dim3(pc::SCAN_THREADS), 0, s,
+              w.cold, nchunks, w.part);
+    PC_LAUNCH(pc::K_SD_SCAN, pc::sd_scan_kernel, dim3(1), dim3(pc::SCAN_THREADS), 0, s, w.part, nblocks,
+              w.part_ex);
+    PC_LAUNCH(pc::K_SD_SCAN, pc::sd_scan_apply_kernel, dim3((unsigned)nblocks), dim3(pc::SCAN_THREADS), 0, s,
+              w.cold, nchunks, w.part_ex, nblocks, w.Zc);
 
     uint32_t *src_t = nullptr, *src_a = nullptr;
     for (int i = 0; i < p.passes; ++i) {
@@ -701,8 +763,8 @@ pc_status pc_stack_distance(const uint32_t *prev, const uint32_t *next, uint64_t
         const uint32_t *tend = i == 0 ? nullptr : w.tfirst + p.nbuckets[i];
         PC_LAUNCH(pc::K_SD_SEG, pc::sd_seg_reduce_kernel, dim3(groups), dim3(pc::DOM_RADIX), 0, s, w.cnt, w.seg,
                   tend, fixed, w.gsum, w.ghas);
-        PC_LAUNCH(pc::K_SD_SEG, pc::sd_seg_carry_kernel, dim3(1), dim3(pc::DOM_RADIX), 0, s, w.gsum, w.ghas, tend,
-                  fixed, w.gin);
+        PC_LAUNCH(pc::K_SD_SEG, pc::sd_seg_carry_kernel, dim3(pc::DOM_RADIX), dim3(pc::CARRY_THREADS), 0, s,
+                  w.gsum, w.ghas, tend, fixed, w.gin);
         PC_LAUNCH(pc::K_SD_SEG, pc::sd_seg_scan_kernel, dim3(groups), dim3(pc::DOM_RADIX), 0, s, w.cnt, w.seg,
                   tend, fixed, w.gin, w.pre);
         if (i == 0) {
