@@ -25,6 +25,12 @@ Each function states the definition it computes and the passage of the paper
   (Sec. 5.2 "Compute-awareness"); uniform cost gives the hit ratio back.
 * ``belady``: demand-paging MIN per capacity (the offline ceiling, Sec. 3.2).
 * ``nextuse_hist``: histogram of next-use gaps ``next(t) - t``.
+* ``stack_distance_req_walk`` / ``stack_distance_req_bit`` / ``lru_req`` /
+  ``mrc_bins_req``: the same under request-level residency, the paper's
+  simulator semantics (Sec. 3.1 "Simulator": all blocks of a request resident
+  at once, room made ahead of time); readings: hits decided on arrival, the
+  request's deepest block least recent afterwards, capacities below the
+  largest request infeasible (Sec. 3.1 "Cache-size regimes").
 """
 from __future__ import annotations
 
@@ -69,6 +75,13 @@ def lib():
         L.orc_lru_sim.restype = ctypes.c_int
         L.orc_lru_sim.argtypes = [_u32p, _u32p, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64,
                                   _u64p, _u64p, _u8p]
+        L.orc_stack_distance_req_walk.restype = ctypes.c_int
+        L.orc_stack_distance_req_walk.argtypes = [_u32p, _u64p, ctypes.c_uint64, ctypes.c_uint64, _u32p]
+        L.orc_stack_distance_req_bit.restype = ctypes.c_int
+        L.orc_stack_distance_req_bit.argtypes = [_u32p, _u64p, ctypes.c_uint64, ctypes.c_uint64, _u32p]
+        L.orc_lru_sim_req.restype = ctypes.c_int
+        L.orc_lru_sim_req.argtypes = [_u32p, _u32p, _u64p, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64,
+                                      _u64p, _u64p, _u8p]
         L.orc_belady_sim.restype = ctypes.c_int
         L.orc_belady_sim.argtypes = [_u32p, _u32p, ctypes.c_uint64, ctypes.c_uint64,
                                      ctypes.c_uint64, _u64p, _u8p]
@@ -248,3 +261,104 @@ def nextuse_hist(nxt, caps):
         hist[i] = int(bc[i])
     hist[caps.size] += int(none.sum())
     return hist
+
+
+# ------------------------------------------------------------ request level
+
+def _req(blk_off):
+    blk_off = _c(blk_off, np.uint64)
+    return blk_off, blk_off.size - 1
+
+
+def stack_distance_req_walk(keys, blk_off, ids=None):
+    """Request-level distance of every access (depth order within each
+    request) by walking the recency list: distinct blocks above the block
+    when its request arrives; NONE if never used before."""
+    if ids is None:
+        ids = key_ids(keys)
+    id_, n_ids = ids
+    bo, ns = _req(blk_off)
+    d = np.empty(id_.size, np.uint32)
+    rc = lib().orc_stack_distance_req_walk(_p(id_, _u32p), _p(bo, _u64p), ns, n_ids, _p(d, _u32p))
+    if rc == -2:
+        raise ValueError("a key repeats inside one request")
+    assert rc == 0
+    return d
+
+
+def stack_distance_req_bit(keys, blk_off, ids=None):
+    """Same, with a Fenwick tree over last-use marks in recency time."""
+    if ids is None:
+        ids = key_ids(keys)
+    id_, n_ids = ids
+    bo, ns = _req(blk_off)
+    d = np.empty(id_.size, np.uint32)
+    assert lib().orc_stack_distance_req_bit(_p(id_, _u32p), _p(bo, _u64p), ns, n_ids, _p(d, _u32p)) == 0
+    return d
+
+
+def lru_req(keys, blk_off, caps, depth=None, ids=None, flags=False):
+    """Per capacity: (hits, depth sum over hits[, flags]) of a request-level
+    LRU cache, or None where the capacity is below the largest request."""
+    if ids is None:
+        ids = key_ids(keys)
+    id_, n_ids = ids
+    bo, ns = _req(blk_off)
+    dep = _c(depth, np.uint32) if depth is not None else None
+    out = []
+    for c in caps:
+        h = ctypes.c_uint64(0)
+        dh = ctypes.c_uint64(0)
+        fl = np.empty(id_.size, np.uint8) if flags else None
+        rc = lib().orc_lru_sim_req(_p(id_, _u32p), _p(dep, _u32p) if dep is not None else None, _p(bo, _u64p),
+                                   ns, n_ids, int(c), ctypes.byref(h), ctypes.byref(dh),
+                                   _p(fl, _u8p) if fl is not None else None)
+        if rc == -3:
+            out.append(None)
+            continue
+        assert rc == 0
+        out.append((h.value, dh.value, fl) if flags else (h.value, dh.value))
+    return out
+
+
+def max_request_blocks(blk_off):
+    bo = np.asarray(blk_off, np.uint64)
+    return int((bo[1:] - bo[:-1]).max()) if bo.size > 1 else 0
+
+
+def mrc_bins_req(keys, blk_off, caps, depth=None, alpha=1, beta=0, ids=None):
+    """Bins over the capacity edges from one request-level simulation per
+    capacity.  Only feasible edges (>= the largest request) are simulated;
+    the bins of infeasible edges hold the accesses whose request-level
+    distance lies below them, which is what the GPU reports for them, so
+    they are filled from the walk instead and flagged by the caller."""
+    keys = _c(keys, np.uint64)
+    n = keys.size
+    if depth is None:
+        depth = np.zeros(n, np.uint32)
+    caps = [int(c) for c in caps]
+    mx = max_request_blocks(blk_off)
+    feas = [c >= mx and c > 0 for c in caps]
+    sim = lru_req(keys, blk_off, [c for c, f in zip(caps, feas) if f], depth, ids)
+    it = iter(sim)
+    res = []
+    d = None
+    for c, f in zip(caps, feas):
+        if f:
+            res.append(next(it))
+        else:
+            if d is None:
+                d = stack_distance_req_walk(keys, blk_off, ids).astype(np.int64)
+                d[d == NONE] = -1
+            hit = (d >= 0) & (d < c)
+            res.append((int(hit.sum()), int(np.asarray(depth, np.uint64)[hit].sum())))
+    count, dsum = [], []
+    ph, pd = 0, 0
+    for h, dh in res:
+        count.append(h - ph)
+        dsum.append(dh - pd)
+        ph, pd = h, dh
+    count.append(n - ph)
+    dsum.append(int(np.asarray(depth, np.uint64).sum(dtype=np.uint64)) - pd)
+    cost = [alpha * c + beta * d for c, d in zip(count, dsum)]
+    return count, dsum, cost, feas

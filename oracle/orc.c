@@ -260,6 +260,158 @@ int orc_lru_sim(const uint32_t *id, const uint32_t *depth, uint64_t n, uint64_t 
 }
 
 /* ------------------------------------------------------------------ */
+/* Request-level residency (Sec. 3.1 "Simulator"): every block of a     */
+/* request must be resident at once during its prefill, so the cache    */
+/* evicts ahead of time (least recently used first, never a block of    */
+/* the request in flight) to make room for the request's misses.        */
+/* Readings: hits are decided on arrival, before any eviction for the   */
+/* request; afterwards all its blocks are the most recent, the deepest  */
+/* one least recent of them (the order a serving engine frees a         */
+/* request's blocks in); keys inside one request must be distinct       */
+/* (true for chained prefix hashes).  A capacity below the largest      */
+/* request is infeasible.  Requests are given by blk_off[0..n_seqs]:    */
+/* request r holds accesses [blk_off[r], blk_off[r+1]) in depth order.  */
+/* ------------------------------------------------------------------ */
+
+/* Exact request-level distance by walking the MRU list: for every block of
+ * request r, the number of distinct blocks above it in the recency list as
+ * it stands when r arrives (ORC_NONE if never used before).  Returns -2 if a
+ * key repeats inside a request. */
+int orc_stack_distance_req_walk(const uint32_t *id, const uint64_t *blk_off, uint64_t n_seqs,
+                                uint64_t n_ids, uint32_t *dist)
+{
+    uint32_t *nx = (uint32_t *)malloc((n_ids + 1) * sizeof(uint32_t));
+    uint32_t *pv = (uint32_t *)malloc((n_ids + 1) * sizeof(uint32_t));
+    uint8_t *seen = (uint8_t *)calloc(n_ids + 1, 1);
+    uint64_t *stamp = (uint64_t *)calloc(n_ids + 1, sizeof(uint64_t));
+    if (!nx || !pv || !seen || !stamp) { free(nx); free(pv); free(seen); free(stamp); return -1; }
+    uint32_t head = ORC_NONE;
+    for (uint64_t r = 0; r < n_seqs; r++) {
+        uint64_t a = blk_off[r], b = blk_off[r + 1];
+        for (uint64_t t = a; t < b; t++) {
+            uint32_t u = id[t];
+            if (stamp[u] == r + 1) { free(nx); free(pv); free(seen); free(stamp); return -2; }
+            stamp[u] = r + 1;
+            if (!seen[u]) {
+                dist[t] = ORC_NONE;
+            } else {
+                uint32_t d = 0, x = head;
+                while (x != u) { x = nx[x]; d++; }
+                dist[t] = d;
+            }
+        }
+        /* make the request's blocks the most recent: deepest first, so the
+         * shallowest ends on top */
+        for (uint64_t t = b; t > a; t--) {
+            uint32_t u = id[t - 1];
+            if (seen[u]) {
+                if (pv[u] != ORC_NONE) nx[pv[u]] = nx[u]; else head = nx[u];
+                if (nx[u] != ORC_NONE) pv[nx[u]] = pv[u];
+            }
+            seen[u] = 1;
+            pv[u] = ORC_NONE;
+            nx[u] = head;
+            if (head != ORC_NONE) pv[head] = u;
+            head = u;
+        }
+    }
+    free(nx); free(pv); free(seen); free(stamp);
+    return 0;
+}
+
+/* Second exact method: a mark at each key's last use in "recency time",
+ * where request r occupies [blk_off[r], blk_off[r+1]) with its deepest block
+ * first.  The distance of a block of r is the number of marks strictly
+ * between its last use and the start of r, read before r places its own
+ * marks (Bennett & Kruskal 1975, queried at the request start). */
+int orc_stack_distance_req_bit(const uint32_t *id, const uint64_t *blk_off, uint64_t n_seqs, uint64_t n_ids,
+                               uint32_t *dist)
+{
+    uint64_t n = blk_off[n_seqs];
+    int32_t *bit = (int32_t *)calloc(n + 1, sizeof(int32_t));
+    uint32_t *last = (uint32_t *)malloc((n_ids + 1) * sizeof(uint32_t));
+    if (!bit || !last) { free(bit); free(last); return -1; }
+    for (uint64_t i = 0; i <= n_ids; i++) last[i] = ORC_NONE;
+    for (uint64_t r = 0; r < n_seqs; r++) {
+        uint64_t a = blk_off[r], b = blk_off[r + 1];
+        for (uint64_t t = a; t < b; t++) {
+            uint32_t p = last[id[t]];
+            dist[t] = p == ORC_NONE ? ORC_NONE : (uint32_t)(bit_sum(bit, a) - bit_sum(bit, (uint64_t)p + 1));
+        }
+        for (uint64_t t = a; t < b; t++) {
+            uint32_t u = id[t];
+            uint64_t when = a + (b - 1 - t);   /* deepest block first */
+            if (last[u] != ORC_NONE) bit_add(bit, n, last[u], -1);
+            bit_add(bit, n, when, +1);
+            last[u] = (uint32_t)when;
+        }
+    }
+    free(bit); free(last);
+    return 0;
+}
+
+/* One request-level LRU cache of `cap` blocks: hits decided on arrival;
+ * then least recently used blocks that are not part of the request are
+ * evicted until the request's misses fit; the misses are inserted and the
+ * request's blocks become the most recent (deepest least recent).  Returns
+ * -3 if a request has more blocks than cap (infeasible capacity). */
+int orc_lru_sim_req(const uint32_t *id, const uint32_t *depth, const uint64_t *blk_off, uint64_t n_seqs,
+                    uint64_t n_ids, uint64_t cap, uint64_t *hits_out, uint64_t *depth_hits_out,
+                    uint8_t *hit_flag)
+{
+    uint32_t *nx = (uint32_t *)malloc((n_ids + 1) * sizeof(uint32_t));
+    uint32_t *pv = (uint32_t *)malloc((n_ids + 1) * sizeof(uint32_t));
+    uint8_t *in = (uint8_t *)calloc(n_ids + 1, 1);
+    uint64_t *pin = (uint64_t *)calloc(n_ids + 1, sizeof(uint64_t));
+    if (!nx || !pv || !in || !pin) { free(nx); free(pv); free(in); free(pin); return -1; }
+    uint32_t head = ORC_NONE, tail = ORC_NONE;
+    uint64_t size = 0, hits = 0, dh = 0;
+    int rc = 0;
+    for (uint64_t r = 0; r < n_seqs && rc == 0; r++) {
+        uint64_t a = blk_off[r], b = blk_off[r + 1], misses = 0;
+        if (b - a > cap) { rc = -3; break; }
+        for (uint64_t t = a; t < b; t++) {
+            uint32_t u = id[t];
+            pin[u] = r + 1;
+            int h = in[u];
+            if (h) { hits++; if (depth) dh += depth[t]; } else misses++;
+            if (hit_flag) hit_flag[t] = (uint8_t)h;
+        }
+        /* proactive eviction: walk from the least recent end, skipping
+         * blocks of the request in flight */
+        uint32_t x = tail;
+        while (size + misses > cap) {
+            while (pin[x] == r + 1) x = pv[x];
+            uint32_t y = pv[x];
+            if (pv[x] != ORC_NONE) nx[pv[x]] = nx[x]; else head = nx[x];
+            if (nx[x] != ORC_NONE) pv[nx[x]] = pv[x]; else tail = pv[x];
+            in[x] = 0;
+            size--;
+            x = y;
+        }
+        /* the request's blocks to the front, deepest first */
+        for (uint64_t t = b; t > a; t--) {
+            uint32_t u = id[t - 1];
+            if (in[u]) {
+                if (pv[u] != ORC_NONE) nx[pv[u]] = nx[u]; else head = nx[u];
+                if (nx[u] != ORC_NONE) pv[nx[u]] = pv[u]; else tail = pv[u];
+            } else {
+                in[u] = 1;
+                size++;
+            }
+            pv[u] = ORC_NONE;
+            nx[u] = head;
+            if (head != ORC_NONE) pv[head] = u; else tail = u;
+            head = u;
+        }
+    }
+    *hits_out = hits;
+    if (depth_hits_out) *depth_hits_out = dh;
+    free(nx); free(pv); free(in); free(pin);
+    return rc;
+}
+
+/* ------------------------------------------------------------------ */
 /* Belady's MIN (Sec. 3.2: offline ceiling), demand paging: every      */
 /* accessed block is inserted; on overflow evict the resident block    */
 /* whose next use is farthest away (never reused = farthest).          */

@@ -306,3 +306,109 @@ def test_nextuse_histogram_brute_force():
                 gap = int(nxt[t]) - t
                 want[sum(1 for c in caps if c <= gap)] += 1
         assert oracle.nextuse_hist(nxt, caps) == want
+
+
+# --------------------------------------------------- request-level residency
+
+def _request_golden():
+    for row in read_golden("request_residency_examples.txt"):
+        bars = [i for i, x in enumerate(row) if x == "|"]
+        names, reqs, cur = {}, [], []
+        for x in row[1:bars[0]]:
+            if x == "/":
+                reqs.append(cur)
+                cur = []
+            else:
+                cur.append(names.setdefault(x, len(names) + 7))
+        reqs.append(cur)
+        keys = np.array([k for r in reqs for k in r], np.uint64)
+        blk_off = np.concatenate([[0], np.cumsum([len(r) for r in reqs])]).astype(np.uint64)
+        want = [NONE if v == "-" else int(v) for v in row[bars[0] + 1:bars[1]]]
+        hits = {int(c): int(h) for c, h in (x.split(":") for x in row[bars[1] + 1:])}
+        yield row[0], keys, blk_off, want, hits
+
+
+def test_request_level_hand_worked_examples():
+    for name, keys, blk_off, want, hits in _request_golden():
+        assert list(oracle.stack_distance_req_walk(keys, blk_off)) == want, name
+        assert list(oracle.stack_distance_req_bit(keys, blk_off)) == want, name
+        caps = sorted(hits)
+        got = oracle.lru_req(keys, blk_off, caps)
+        assert [g[0] for g in got] == [hits[c] for c in caps], name
+
+
+def random_requests(count, seed):
+    """Small multi-turn traces: sessions re-send and extend their context,
+    some start from shared prompts, some reset; keys are distinct inside a
+    request (as chained prefix hashes are)."""
+    rng = np.random.default_rng(seed)
+    for _ in range(count):
+        n_sess = int(rng.integers(1, 6))
+        ctx = {s: [] for s in range(n_sess)}
+        shared = {p: [1000 * (p + 1) + d for d in range(int(rng.integers(1, 4)))] for p in range(3)}
+        reqs, nxt = [], 1
+        for _r in range(int(rng.integers(1, 30))):
+            s = int(rng.integers(n_sess))
+            if not ctx[s] and rng.random() < 0.3:
+                ctx[s] = list(shared[int(rng.integers(3))])
+            grow = int(rng.integers(0, 5))
+            ctx[s] = ctx[s] + list(range(nxt, nxt + grow))
+            nxt += grow
+            if rng.random() < 0.1:
+                ctx[s] = []
+            if ctx[s]:
+                reqs.append(list(ctx[s]))
+        if not reqs:
+            continue
+        keys = np.array([k for r in reqs for k in r], np.uint64)
+        blk_off = np.concatenate([[0], np.cumsum([len(r) for r in reqs])]).astype(np.uint64)
+        yield keys, blk_off
+
+
+def test_request_level_walk_fenwick_and_simulation_agree():
+    """Two exact distance methods agree, and the pinned-request cache hits
+    exactly when D_req < c at every feasible capacity (so request-level LRU
+    is a stack algorithm there, with inclusion)."""
+    for keys, blk_off in random_requests(150, seed=21):
+        d = oracle.stack_distance_req_walk(keys, blk_off)
+        assert np.array_equal(d, oracle.stack_distance_req_bit(keys, blk_off))
+        mx = oracle.max_request_blocks(blk_off)
+        caps = list(range(max(mx, 1), mx + 10))
+        prev_flags = None
+        for c, res in zip(caps, oracle.lru_req(keys, blk_off, caps, flags=True)):
+            h, _, fl = res
+            want = (d != NONE) & (d < c)
+            assert np.array_equal(fl.astype(bool), want), c
+            assert h == int(want.sum())
+            if prev_flags is not None:
+                assert np.all(fl >= prev_flags)   # inclusion
+            prev_flags = fl
+        if mx > 1:
+            assert oracle.lru_req(keys, blk_off, [mx - 1])[0] is None   # infeasible
+
+
+def test_request_level_equals_per_access_for_single_block_requests():
+    for keys in random_streams(60, seed=8):
+        blk_off = np.arange(keys.size + 1, dtype=np.uint64)
+        assert np.array_equal(oracle.stack_distance_req_walk(keys, blk_off), oracle.stack_distance_walk(keys))
+
+
+def test_request_level_identity_in_recency_order():
+    """In recency order (each request's blocks deepest first), the request
+    distance equals the per-access distance minus the earlier accesses of the
+    same request whose previous use is older (cold ones included):
+    D_req(t) = D(t) - #{j in [s(t), t) : prev(j) + 1 < prev(t) + 1}."""
+    for keys, blk_off in random_requests(120, seed=5):
+        bo = blk_off.astype(np.int64)
+        order = np.concatenate([np.arange(bo[r + 1] - 1, bo[r] - 1, -1) for r in range(bo.size - 1)])
+        kp = keys[order]
+        p, _ = oracle.prev_next(kp)
+        d = oracle.stack_distance_walk(kp)
+        v = np.where(p == NONE, 0, p.astype(np.int64) + 1)
+        want_p = np.empty(kp.size, np.int64)
+        for r in range(bo.size - 1):
+            for t in range(bo[r], bo[r + 1]):
+                want_p[t] = -1 if p[t] == NONE else int(d[t]) - int((v[bo[r]:t] < v[t]).sum())
+        got = oracle.stack_distance_req_walk(keys, blk_off).astype(np.int64)
+        got[got == NONE] = -1
+        assert np.array_equal(got[order], want_p)
