@@ -36,6 +36,8 @@ ALGO_BYTES = {
     "sd_dominance_pass": lambda B: 8 + 8,         # (t, acc) in and out
     "sd_local_finish": lambda B: 8 + 4 + 4,       # (t, acc), prev in; dist out
     "mrc_hist": lambda B: 12,                     # dist, depth, next in
+    "request_order": lambda B: 12 + 12,           # key, depth in; reversed copies out
+    "sd_local_request": lambda B: 8 + 8 + 4,      # (t, acc), prev, per-access dist in; dist_req out
 }
 
 
@@ -99,10 +101,12 @@ def measured_traffic(kernel_id):
             "profiled_avg_ms": entry["avg_ms"], "source": os.path.relpath(PROFILE, ROOT)}
 
 
-def cpu_baseline(trace, caps, alpha, beta, budget_accesses):
+def cpu_baseline(trace, caps, alpha, beta, budget_accesses, request=False):
     """The oracle (plain C, one thread) over the first requests of the same
     trace: hash, prev/next, next-use histogram and one LRU simulation per
-    capacity edge -- the same outputs as one GPU step."""
+    capacity edge -- the same outputs as one GPU step.  In request mode:
+    hash and the request-level bins (one pinned-request simulation per
+    feasible edge, the recency-list walk for the others)."""
     import oracle
     import pcgen
     nb = (trace.tok_len // np.uint32(trace.block_size)).astype(np.int64)
@@ -112,13 +116,18 @@ def cpu_baseline(trace, caps, alpha, beta, budget_accesses):
     t0 = time.perf_counter()
     keys, depth = oracle.hash_trace(sub)
     ids = oracle.key_ids(keys)
-    _, nxt = oracle.prev_next(keys, ids)
-    oracle.nextuse_hist(nxt, caps)
-    oracle.mrc_bins(keys, caps, depth, alpha, beta, ids)
+    if request:
+        oracle.mrc_bins_req(keys, sub.blk_off(), caps, depth, alpha, beta, ids)
+        what = "request-level bins"
+    else:
+        _, nxt = oracle.prev_next(keys, ids)
+        oracle.nextuse_hist(nxt, caps)
+        oracle.mrc_bins(keys, caps, depth, alpha, beta, ids)
+        what = "prev/next + %d per-capacity LRU simulations" % len(caps)
     dt = time.perf_counter() - t0
     return {"value": keys.size / dt, "unit": "block-accesses/s", "cores": 1, "kind": "oracle",
-            "sample": "first %d requests (%d block accesses) of the same trace; hash + prev/next + "
-                      "%d per-capacity LRU simulations; %.1f s" % (r, keys.size, len(caps), dt)}
+            "sample": "first %d requests (%d block accesses) of the same trace; hash + %s; %.1f s" % (
+                r, keys.size, what, dt)}
 
 
 def main():
@@ -129,8 +138,11 @@ def main():
     ap.add_argument("--workload", default="full", choices=["tiny", "chat", "agent", "full"])
     ap.add_argument("--sessions", type=int, default=None, help="override the session count")
     ap.add_argument("--block-size", type=int, default=16)
-    ap.add_argument("--cpu-sample", type=int, default=20_000_000,
-                    help="block accesses in the oracle's timed sample (0 = skip)")
+    ap.add_argument("--residency", default="access", choices=["access", "request"],
+                    help="per-access LRU (default) or request-level residency (whole request pinned)")
+    ap.add_argument("--cpu-sample", type=int, default=None,
+                    help="block accesses in the oracle's timed sample (0 = skip; default 2e7, "
+                         "4e5 with --residency request)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 4 GiB device copy (for rocprof counter calibration)")
     args = ap.parse_args()
@@ -155,8 +167,9 @@ def main():
     alpha, beta = 2 * B * P_LIN, 2 * B * B
     up = pc.upload_trace(trace, B)
     caps = pc.to_dev_u64(caps_np)
+    request = args.residency == "request"
     pipe = pc.Pipeline(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
-                       caps, B, alpha, beta)
+                       caps, B, alpha, beta, residency=args.residency)
     torch.cuda.synchronize()
     log("inputs resident in HBM; device memory in use %.1f GB" % (torch.cuda.memory_allocated() / 1e9))
 
@@ -207,7 +220,7 @@ def main():
         entry = {"launches_per_step": launches // args.steps, "working_launches_per_step": wl,
                  "ms_per_step": round(per_step, 4)}
         if name in ALGO_BYTES:
-            per_launch = ALGO_BYTES[name](B) * n_blocks
+            per_launch = (8 if request and name == "mrc_hist" else ALGO_BYTES[name](B)) * n_blocks
             entry["algo_bytes_per_launch"] = per_launch
             entry["avg_working_launch_ms"] = round(per_step / wl, 4)
             entry["algo_GBps"] = round(per_launch * wl / per_step / 1e6, 1)
@@ -227,8 +240,10 @@ def main():
                 "sort_digit_scan": "prev_next", "sort_onesweep_pass": "prev_next",
                 "link_partition": "prev_next",
                 "perm_partition": "prev_next", "perm_local": "prev_next", "mrc_hist": "mrc",
-                "mrc_cost": "mrc"}
-    stage_bytes = {"hash": 4 * B + 8 + 4, "prev_next": 16, "stack_distance": 8, "mrc": 12}
+                "mrc_cost": "mrc", "request_order": "request_order", "request_keys": "request_distance",
+                "request_sort": "request_distance", "sd_local_request": "request_distance"}
+    stage_bytes = {"hash": 4 * B + 8 + 4, "prev_next": 16, "stack_distance": 8, "mrc": 8 if request else 12,
+                   "request_order": 24, "request_distance": 16}
 
     def stage_name(kid):
         return stage_of.get(kid, "stack_distance" if kid.startswith("sd_") else "other")
@@ -247,13 +262,17 @@ def main():
     # the curves themselves (exact integers -> float64 ratios)
     bins = pc.bins_to_host(pipe.bins)
     hr, csr = pc.curves(bins["count"], bins["cost"])
+    # request-level bins hold only at capacities that fit the largest request
+    min_cap = int((trace.tok_len // np.uint32(B)).max()) if request else 0
     cb = None
-    if args.cpu_sample > 0:
-        log("timing the CPU oracle on a %d-access sample" % args.cpu_sample)
-        cb = cpu_baseline(trace, caps_np, alpha, beta, args.cpu_sample)
+    sample = args.cpu_sample if args.cpu_sample is not None else (400_000 if request else 20_000_000)
+    if sample > 0:
+        log("timing the CPU oracle on a %d-access sample" % sample)
+        cb = cpu_baseline(trace, caps_np, alpha, beta, sample, request)
 
     out = {
         "metric": "KV-block accesses/sec for hash+stack-distance+MRC; achieved HBM GB/s",
+        "residency": args.residency,
         "value": value,
         "unit": "block-accesses/s",
         "n_gpus": 1,
@@ -274,6 +293,8 @@ def main():
             "processed_tokens": trace.processed_tokens(),
             "capacities": int(caps_np.size),
             "cost_model": "2*B*(P_lin + B*depth), P_lin=3e9",
+            "residency": "per-access LRU" if not request else
+                         "request-level (whole request resident; bins valid from %d blocks)" % min_cap,
             "parallelism": "single GPU",
         },
         "roofline": roof,
@@ -281,7 +302,7 @@ def main():
         "kernels": kernels,
         "stages": stages,
         "high_key_sort_passes": high,
-        "curves_at": {str(int(c)): [round(h, 6), round(s, 6)]
+        "curves_at": {str(int(c)): [round(h, 6), round(s, 6)] if int(c) >= min_cap else None
                       for c, h, s in zip(caps_np, hr, csr) if int(c) in pcgen.GIB_BLOCKS.values()},
     }
     print(json.dumps(out), flush=True)

@@ -125,6 +125,47 @@ pc_status pc_stack_distance(const uint32_t *prev, const uint32_t *next, uint64_t
                             uint32_t *dist, void *ws, size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
+ * Request-level residency (Sec. 3.1 "Simulator": every block of a request
+ * must be resident at once during its prefill, so room is made ahead of time
+ * by evicting least recently used blocks that are not part of the request).
+ * Readings: a block hits if it is resident when its request arrives;
+ * afterwards the request's blocks are the most recent, its deepest block the
+ * least recent of them.  For a capacity c of at least the largest request's
+ * block count this cache is a stack algorithm too: a block hits exactly when
+ * dist_req < c, where dist_req counts the distinct blocks above it in the
+ * recency list when its request arrives.  Capacities below the largest
+ * request cannot hold that request (Sec. 3.1 "Cache-size regimes") and are
+ * the caller's to exclude.  Keys inside one request must be distinct (chained
+ * prefix hashes are); otherwise the results are unspecified (memory-safe).
+ *
+ * Pipeline: pc_request_order puts each request's accesses in that recency
+ * order (deepest block first); pc_prev_next_use and pc_stack_distance run
+ * unchanged on the reordered keys; pc_stack_distance_req turns their outputs
+ * into dist_req (same order).  All arrays of one pipeline share that order.
+ * ------------------------------------------------------------------------ */
+
+/* Each request's accesses in reverse: keys_out[blk_off[r+1]-1-j] =
+ * keys[blk_off[r]+j] (and the same for depth when given).  blk_off is the
+ * uint64[n_seqs+1] request table of pc_hash_blocks (blk_off[n_seqs] = n).
+ * Outputs must not alias inputs.  A request with blk_off[r] > blk_off[r+1]
+ * or past n is skipped and the workspace status is set to 2. */
+size_t pc_request_order_ws(void);
+pc_status pc_request_order(const uint64_t *keys, const uint32_t *depth, const uint64_t *blk_off,
+                           uint32_t n_seqs, uint64_t n, uint64_t *keys_out, uint32_t *depth_out,
+                           void *ws, size_t ws_bytes, void *stream);
+
+/* dist_req from prev, next and dist of the reordered accesses (all uint32[n],
+ * recency order) and the request table.  With t in request r, s = blk_off[r]:
+ *   dist_req[t] = dist[t] - #{ j in [s, t) : prev(j) + 1 < prev(t) + 1 }
+ * (cold j count as prev + 1 = 0), PC_NONE when prev(t) = PC_NONE.  A layout
+ * with blk_off[0] != 0, blk_off[n_seqs] != n or a decreasing step sets the
+ * workspace status to 2 (results unspecified). */
+size_t pc_stack_distance_req_ws(uint64_t n, uint32_t n_seqs);
+pc_status pc_stack_distance_req(const uint32_t *prev, const uint32_t *next, const uint32_t *dist,
+                                const uint64_t *blk_off, uint32_t n_seqs, uint64_t n, uint32_t *dist_req,
+                                void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
  * Hit-ratio and compute-savings histograms over capacity edges.
  *
  * Paper: block hit ratio counts every access, compulsory misses included

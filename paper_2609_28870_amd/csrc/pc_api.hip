@@ -6,11 +6,35 @@
 
 namespace pc {
 
-static const char *kKernelNames[K_COUNT] = {
-    "fill_u32",         "hash_digest",   "hash_chain",      "sort_digit_hist",   "sort_digit_scan",
-    "sort_onesweep_pass", "link_partition", "perm_partition", "perm_local",        "sd_cold_count",
-    "sd_scan",          "sd_tile_map",   "sd_count",        "sd_seg_scan",       "sd_dominance_pass",
-    "sd_local_finish",  "mrc_hist",      "mrc_cost"};
+// one case per kernel id (a missing one is a -Wswitch warning)
+static const char *kernel_name(KernelId k) {
+    switch (k) {
+    case K_FILL32: return "fill_u32";
+    case K_HASH_DIGEST: return "hash_digest";
+    case K_HASH: return "hash_chain";
+    case K_SORT_HIST: return "sort_digit_hist";
+    case K_SORT_SCAN: return "sort_digit_scan";
+    case K_SORT_PASS: return "sort_onesweep_pass";
+    case K_LINK: return "link_partition";
+    case K_PERM: return "perm_partition";
+    case K_PERM_LOCAL: return "perm_local";
+    case K_SD_COLD: return "sd_cold_count";
+    case K_SD_SCAN: return "sd_scan";
+    case K_SD_TILES: return "sd_tile_map";
+    case K_SD_COUNT: return "sd_count";
+    case K_SD_SEG: return "sd_seg_scan";
+    case K_SD_PASS: return "sd_dominance_pass";
+    case K_SD_LOCAL: return "sd_local_finish";
+    case K_MRC_HIST: return "mrc_hist";
+    case K_MRC_COST: return "mrc_cost";
+    case K_REQ_ORDER: return "request_order";
+    case K_REQ_KEYS: return "request_keys";
+    case K_SD_LOCAL_REQ: return "sd_local_request";
+    case K_REQ_SORT: return "request_sort";
+    case K_COUNT: break;
+    }
+    return "";
+}
 
 struct ProfEvent {
     int kid;
@@ -107,7 +131,7 @@ void pc_prof_enable(int on) { pc::g_prof = on != 0; }
 int pc_prof_kernel_count(void) { return pc::K_COUNT; }
 
 const char *pc_prof_kernel_name(int i) {
-    return (i >= 0 && i < pc::K_COUNT) ? pc::kKernelNames[i] : "";
+    return (i >= 0 && i < pc::K_COUNT) ? pc::kernel_name((pc::KernelId)i) : "";
 }
 
 pc_status pc_prof_read(uint64_t *launches, double *total_ms, int n) {

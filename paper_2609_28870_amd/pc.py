@@ -21,6 +21,7 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "_lib", "libpc.so")
 NONE = 0xFFFFFFFF
+HEADER = 256   # bytes of status header at the start of every workspace
 
 _lib = None
 
@@ -59,6 +60,14 @@ def lib():
     L.pc_stack_distance_ws.argtypes = [_u64]
     L.pc_stack_distance.restype = _st
     L.pc_stack_distance.argtypes = [_vp, _vp, _u64, _vp, _vp, _sz, _vp]
+    L.pc_request_order_ws.restype = _sz
+    L.pc_request_order_ws.argtypes = []
+    L.pc_request_order.restype = _st
+    L.pc_request_order.argtypes = [_vp, _vp, _vp, _u32, _u64, _vp, _vp, _vp, _sz, _vp]
+    L.pc_stack_distance_req_ws.restype = _sz
+    L.pc_stack_distance_req_ws.argtypes = [_u64, _u32]
+    L.pc_stack_distance_req.restype = _st
+    L.pc_stack_distance_req.argtypes = [_vp, _vp, _vp, _vp, _u32, _u64, _vp, _vp, _sz, _vp]
     L.pc_mrc_weighted_ws.restype = _sz
     L.pc_mrc_weighted_ws.argtypes = [_u64, _u32]
     L.pc_mrc_weighted.restype = _st
@@ -190,11 +199,49 @@ def stack_distance(prev: torch.Tensor, nxt: torch.Tensor, dist: Optional[torch.T
     return dist, ws
 
 
+def request_order(keys: torch.Tensor, blk_off: torch.Tensor, depth: Optional[torch.Tensor] = None,
+                  keys_out: Optional[torch.Tensor] = None, depth_out: Optional[torch.Tensor] = None,
+                  ws: Optional[torch.Tensor] = None):
+    """pc_request_order: every request's accesses reversed (deepest block
+    first), the recency order of request-level residency."""
+    L = lib()
+    n = keys.numel()
+    n_seqs = blk_off.numel() - 1
+    dev = _dev()
+    if keys_out is None:
+        keys_out = torch.empty(n, dtype=torch.int64, device=dev)
+    if depth is not None and depth_out is None:
+        depth_out = torch.empty(n, dtype=torch.int32, device=dev)
+    if ws is None:
+        ws = workspace(L.pc_request_order_ws())
+    check(L.pc_request_order(_ptr(keys), _ptr(depth), _ptr(blk_off), n_seqs, n, _ptr(keys_out),
+                             _ptr(depth_out) if depth is not None else None, _ptr(ws), ws.numel(),
+                             _stream()))
+    return keys_out, depth_out, ws
+
+
+def stack_distance_req(prev: torch.Tensor, nxt: torch.Tensor, dist: torch.Tensor, blk_off: torch.Tensor,
+                       dist_req: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
+    """pc_stack_distance_req: request-level stack distances from prev, next
+    and dist of the request-ordered accesses."""
+    L = lib()
+    n = prev.numel()
+    n_seqs = blk_off.numel() - 1
+    if dist_req is None:
+        dist_req = torch.empty(n, dtype=torch.int32, device=_dev())
+    if ws is None:
+        ws = workspace(L.pc_stack_distance_req_ws(n, n_seqs))
+    check(L.pc_stack_distance_req(_ptr(prev), _ptr(nxt), _ptr(dist), _ptr(blk_off), n_seqs, n,
+                                  _ptr(dist_req), _ptr(ws), ws.numel(), _stream()))
+    return dist_req, ws
+
+
 def mrc_weighted(dist: torch.Tensor, caps: torch.Tensor, depth: Optional[torch.Tensor] = None,
                  nxt: Optional[torch.Tensor] = None, alpha: int = 1, beta: int = 0,
                  out: Optional[dict] = None, ws: Optional[torch.Tensor] = None):
     """pc_mrc_weighted: per-bin count, depthsum, cost (lo/hi) and next-use
-    histogram as int64 tensors of n_caps+1 entries (uint64 bit patterns)."""
+    histogram as int64 tensors of n_caps+1 entries (uint64 bit patterns);
+    the next-use histogram is all zero when ``nxt`` is None."""
     L = lib()
     n = dist.numel()
     k = caps.numel()
@@ -207,7 +254,7 @@ def mrc_weighted(dist: torch.Tensor, caps: torch.Tensor, depth: Optional[torch.T
     check(L.pc_mrc_weighted(_ptr(dist), _ptr(depth), _ptr(nxt), n, _ptr(caps), k,
                             alpha & (2 ** 64 - 1), beta & (2 ** 64 - 1), _ptr(out["count"]),
                             _ptr(out["depthsum"]), _ptr(out["cost_lo"]), _ptr(out["cost_hi"]),
-                            _ptr(out["nextuse"]) if nxt is not None else None, _ptr(ws), ws.numel(),
+                            _ptr(out["nextuse"]), _ptr(ws), ws.numel(),
                             _stream()))
     return out, ws
 
@@ -259,10 +306,21 @@ def prof_read() -> dict:
 
 class Pipeline:
     """All four stages over one trace with buffers and workspaces allocated
-    once; ``run()`` enqueues hash -> prev/next -> stack distance -> bins."""
+    once; ``run()`` enqueues hash -> prev/next -> stack distance -> bins.
+
+    ``residency="access"`` bins the per-access LRU stack distance.
+    ``residency="request"`` (every block of a request resident at once,
+    Sec. 3.1) first puts each request's accesses in recency order (deepest
+    block first), runs prev/next and the stack distance on that order, turns
+    the result into the request-level distance and bins that, with depth in
+    the same order; the next-use histogram is not taken in that mode.  Its
+    bins are valid at capacities of at least the largest request."""
 
     def __init__(self, tokens, tok_start, tok_len, blk_off, n_blocks: int, caps,
-                 block_size: int = 16, alpha: int = 1, beta: int = 0, with_nextuse: bool = True):
+                 block_size: int = 16, alpha: int = 1, beta: int = 0, with_nextuse: bool = True,
+                 residency: str = "access"):
+        if residency not in ("access", "request"):
+            raise PcError("residency must be 'access' or 'request'")
         L = lib()
         dev = _dev()
         self.tokens, self.tok_start, self.tok_len, self.blk_off = tokens, tok_start, tok_len, blk_off
@@ -270,8 +328,11 @@ class Pipeline:
         self.B = block_size
         self.caps = caps
         self.alpha, self.beta = alpha, beta
-        self.with_nextuse = with_nextuse
+        self.residency = residency
+        self.request = residency == "request"
+        self.with_nextuse = with_nextuse and not self.request
         n = self.n
+        n_seqs = tok_len.numel()
         self.keys = torch.empty(n, dtype=torch.int64, device=dev)
         self.depth = torch.empty(n, dtype=torch.int32, device=dev)
         self.prev = torch.empty(n, dtype=torch.int32, device=dev)
@@ -280,18 +341,40 @@ class Pipeline:
         k = caps.numel()
         self.bins = {name: torch.empty(k + 1, dtype=torch.int64, device=dev)
                      for name in ("count", "depthsum", "cost_lo", "cost_hi", "nextuse")}
-        self.ws_hash = workspace(L.pc_hash_blocks_ws(tok_len.numel()))
+        self.ws_hash = workspace(L.pc_hash_blocks_ws(n_seqs))
         self.ws_pn = workspace(L.pc_prev_next_use_ws(n))
         self.ws_sd = workspace(L.pc_stack_distance_ws(n))
+        if self.request:
+            self.keys_r = torch.empty(n, dtype=torch.int64, device=dev)
+            self.depth_r = torch.empty(n, dtype=torch.int32, device=dev)
+            self.dist_req = torch.empty(n, dtype=torch.int32, device=dev)
+            self.ws_ro = workspace(L.pc_request_order_ws())
+            # The request-level call runs after prev/next on the same stream,
+            # so it reuses the prev/next workspace, shifted by one header so
+            # that both status headers survive the run.
+            req = L.pc_stack_distance_req_ws(n, n_seqs) + HEADER
+            if req > self.ws_pn.numel():
+                self.ws_pn = workspace(req)
+            self.ws_req = self.ws_pn[HEADER:]
         self.ws_mrc = workspace(L.pc_mrc_weighted_ws(n, k))
 
     def run(self):
         hash_blocks(self.tokens, self.tok_start, self.tok_len, self.blk_off, self.n, self.B,
                     keys=self.keys, depth=self.depth, ws=self.ws_hash)
-        prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn)
+        if not self.request:
+            prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn)
+            stack_distance(self.prev, self.next, self.dist, ws=self.ws_sd)
+            mrc_weighted(self.dist, self.caps, self.depth, self.next if self.with_nextuse else None,
+                         self.alpha, self.beta, out=self.bins, ws=self.ws_mrc)
+            return
+        request_order(self.keys, self.blk_off, self.depth, keys_out=self.keys_r, depth_out=self.depth_r,
+                      ws=self.ws_ro)
+        prev_next_use(self.keys_r, self.prev, self.next, ws=self.ws_pn)
         stack_distance(self.prev, self.next, self.dist, ws=self.ws_sd)
-        mrc_weighted(self.dist, self.caps, self.depth, self.next if self.with_nextuse else None,
-                     self.alpha, self.beta, out=self.bins, ws=self.ws_mrc)
+        stack_distance_req(self.prev, self.next, self.dist, self.blk_off, dist_req=self.dist_req,
+                           ws=self.ws_req)
+        mrc_weighted(self.dist_req, self.caps, self.depth_r, None, self.alpha, self.beta,
+                     out=self.bins, ws=self.ws_mrc)
 
     def high_key_passes_ran(self) -> bool:
         """Whether the last prev/next call also sorted by the high 32 key
@@ -299,9 +382,12 @@ class Pipeline:
         return high_key_passes_ran(self.ws_pn)
 
     def status(self) -> dict:
-        return {name: workspace_status(ws) for name, ws in
-                (("hash", self.ws_hash), ("prev_next", self.ws_pn), ("stack_distance", self.ws_sd),
-                 ("mrc", self.ws_mrc))}
+        stages = [("hash", self.ws_hash), ("prev_next", self.ws_pn), ("stack_distance", self.ws_sd),
+                  ("mrc", self.ws_mrc)]
+        if self.request:
+            stages.insert(1, ("request_order", self.ws_ro))
+            stages.append(("stack_distance_req", self.ws_req))
+        return {name: workspace_status(ws) for name, ws in stages}
 
 
 def upload_trace(trace, block_size: Optional[int] = None):

@@ -1,6 +1,7 @@
 import os
 import sys
 
+import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -24,3 +25,26 @@ def read_golden(name):
             if line:
                 rows.append(line.split())
     return rows
+
+
+NONE = 0xFFFFFFFF
+
+
+def request_golden():
+    """(name, keys, blk_off, D_req per access, {capacity: hits}) per row of the
+    hand-worked request-level fixture; blocks named in a row get small ids."""
+    for row in read_golden("request_residency_examples.txt"):
+        bars = [i for i, x in enumerate(row) if x == "|"]
+        names, reqs, cur = {}, [], []
+        for x in row[1:bars[0]]:
+            if x == "/":
+                reqs.append(cur)
+                cur = []
+            else:
+                cur.append(names.setdefault(x, len(names) + 7))
+        reqs.append(cur)
+        keys = np.array([k for r in reqs for k in r], np.uint64)
+        blk_off = np.concatenate([[0], np.cumsum([len(r) for r in reqs])]).astype(np.uint64)
+        want = [NONE if v == "-" else int(v) for v in row[bars[0] + 1:bars[1]]]
+        hits = {int(c): int(h) for c, h in (x.split(":") for x in row[bars[1] + 1:])}
+        yield row[0], keys, blk_off, want, hits

@@ -82,6 +82,38 @@ def test_stack_distance_rejects_bad_arguments(L):
     assert L.pc_stack_distance(FAKE, FAKE, n, FAKE, FAKE, ws - 1, None) == -3
 
 
+def test_request_order_rejects_bad_arguments(L):
+    ws = L.pc_request_order_ws()
+    assert ws >= 256
+    call = lambda keys=FAKE, depth=None, bo=FAKE, ns=4, n=10, ko=ctypes.c_void_p(0x2000), do=None, w=FAKE, \
+        wsz=ws: L.pc_request_order(keys, depth, bo, ns, n, ko, do, w, wsz, None)
+    assert call(n=0xFFFFFFFF) == -2
+    assert call(keys=None) == -1
+    assert call(bo=None) == -1
+    assert call(ko=None) == -1
+    assert call(depth=FAKE) == -1                     # depth without depth_out
+    assert call(ko=FAKE) == -1                        # output aliases input
+    assert call(depth=FAKE, do=FAKE) == -1
+    assert call(w=None) == -3
+    assert call(wsz=ws - 1) == -3
+
+
+def test_stack_distance_req_rejects_bad_arguments(L):
+    n = 5000
+    ws = L.pc_stack_distance_req_ws(n, 40)
+    assert ws > L.pc_stack_distance_ws(n)
+    assert L.pc_stack_distance_req_ws(10 ** 6, 40) > ws
+    call = lambda prev=FAKE, ns=40, n=n, out=FAKE, w=FAKE, wsz=ws: L.pc_stack_distance_req(
+        prev, FAKE, FAKE, FAKE, ns, n, out, w, wsz, None)
+    assert call(n=0xFFFFFFFF) == -2
+    assert call(ns=0x80000000) == -2
+    assert call(prev=None) == -1
+    assert call(out=None) == -1
+    assert call(ns=0) == -1
+    assert call(w=None) == -3
+    assert call(wsz=ws - 1) == -3
+
+
 def test_mrc_rejects_bad_arguments(L):
     ws = L.pc_mrc_weighted_ws(10, 4)
     ok = lambda **kw: dict(dict(dist=FAKE, depth=None, nxt=None, n=10, caps=FAKE, k=4, a=1, b=0,
@@ -107,4 +139,6 @@ def test_profiling_table(L):
     n = L.pc_prof_kernel_count()
     names = [L.pc_prof_kernel_name(i).decode() for i in range(n)]
     assert "hash_chain" in names and "sd_dominance_pass" in names and "mrc_hist" in names
+    assert all(names) and len(set(names)) == n
+    assert names[-1] == "request_sort"
     assert pc.prof_read() is not None

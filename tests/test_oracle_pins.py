@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 import oracle
-from conftest import read_golden
+from conftest import read_golden, request_golden
 
 NONE = oracle.NONE
 G = 0x9E3779B97F4A7C15
@@ -310,26 +310,8 @@ def test_nextuse_histogram_brute_force():
 
 # --------------------------------------------------- request-level residency
 
-def _request_golden():
-    for row in read_golden("request_residency_examples.txt"):
-        bars = [i for i, x in enumerate(row) if x == "|"]
-        names, reqs, cur = {}, [], []
-        for x in row[1:bars[0]]:
-            if x == "/":
-                reqs.append(cur)
-                cur = []
-            else:
-                cur.append(names.setdefault(x, len(names) + 7))
-        reqs.append(cur)
-        keys = np.array([k for r in reqs for k in r], np.uint64)
-        blk_off = np.concatenate([[0], np.cumsum([len(r) for r in reqs])]).astype(np.uint64)
-        want = [NONE if v == "-" else int(v) for v in row[bars[0] + 1:bars[1]]]
-        hits = {int(c): int(h) for c, h in (x.split(":") for x in row[bars[1] + 1:])}
-        yield row[0], keys, blk_off, want, hits
-
-
 def test_request_level_hand_worked_examples():
-    for name, keys, blk_off, want, hits in _request_golden():
+    for name, keys, blk_off, want, hits in request_golden():
         assert list(oracle.stack_distance_req_walk(keys, blk_off)) == want, name
         assert list(oracle.stack_distance_req_bit(keys, blk_off)) == want, name
         caps = sorted(hits)
