@@ -37,7 +37,7 @@ ALGO_BYTES = {
     "sd_local_finish": lambda B: 8 + 4 + 4,       # (t, acc), prev in; dist out
     "mrc_hist": lambda B: 12,                     # dist, depth, next in
     "request_order": lambda B: 12 + 12,           # key, depth in; reversed copies out
-    "sd_local_request": lambda B: 8 + 8 + 4,      # (t, acc), prev, per-access dist in; dist_req out
+    "request_distance": lambda B: 4 + 4 + 4,      # prev, per-access dist in; dist_req out
 }
 
 
@@ -240,10 +240,9 @@ def main():
                 "sort_digit_scan": "prev_next", "sort_onesweep_pass": "prev_next",
                 "link_partition": "prev_next",
                 "perm_partition": "prev_next", "perm_local": "prev_next", "mrc_hist": "mrc",
-                "mrc_cost": "mrc", "request_order": "request_order", "request_keys": "request_distance",
-                "request_sort": "request_distance", "sd_local_request": "request_distance"}
+                "mrc_cost": "mrc", "request_order": "request_order", "request_distance": "request_distance"}
     stage_bytes = {"hash": 4 * B + 8 + 4, "prev_next": 16, "stack_distance": 8, "mrc": 8 if request else 12,
-                   "request_order": 24, "request_distance": 16}
+                   "request_order": 24, "request_distance": 12}
 
     def stage_name(kid):
         return stage_of.get(kid, "stack_distance" if kid.startswith("sd_") else "other")

@@ -154,16 +154,23 @@ pc_status pc_request_order(const uint64_t *keys, const uint32_t *depth, const ui
                            uint32_t n_seqs, uint64_t n, uint64_t *keys_out, uint32_t *depth_out,
                            void *ws, size_t ws_bytes, void *stream);
 
-/* dist_req from prev, next and dist of the reordered accesses (all uint32[n],
- * recency order) and the request table.  With t in request r, s = blk_off[r]:
- *   dist_req[t] = dist[t] - #{ j in [s, t) : prev(j) + 1 < prev(t) + 1 }
- * (cold j count as prev + 1 = 0), PC_NONE when prev(t) = PC_NONE.  A layout
- * with blk_off[0] != 0, blk_off[n_seqs] != n or a decreasing step sets the
- * workspace status to 2 (results unspecified). */
-size_t pc_stack_distance_req_ws(uint64_t n, uint32_t n_seqs);
-pc_status pc_stack_distance_req(const uint32_t *prev, const uint32_t *next, const uint32_t *dist,
-                                const uint64_t *blk_off, uint32_t n_seqs, uint64_t n, uint32_t *dist_req,
-                                void *ws, size_t ws_bytes, void *stream);
+/* dist_req from prev and dist of the reordered accesses (uint32[n] each,
+ * recency order, as pc_prev_next_use and pc_stack_distance give them) and
+ * the request table.  With v = prev + 1 (0 for a cold access) and t in
+ * request r, s = blk_off[r]:
+ *   dist_req[t] = dist[t] - #{ j in [s, t) : v(j) < v(t) },
+ * PC_NONE when prev[t] = PC_NONE.  The blocks above t's block when its
+ * request arrives are the distinct blocks used between prev[t] and s; the
+ * per-access distance also counts the request's accesses in [s, t) whose
+ * blocks were not among them, which are those with v(j) < v(t).  Chained
+ * prefix keys make the count t - s (one pass over prev and dist); other key
+ * streams are counted directly where they break that order (slower, same
+ * result).  blk_off[0] != 0, blk_off[n_seqs] != n or a decreasing step sets
+ * the workspace status to 2 (results unspecified, memory-safe). */
+size_t pc_stack_distance_req_ws(void);
+pc_status pc_stack_distance_req(const uint32_t *prev, const uint32_t *dist, const uint64_t *blk_off,
+                                uint32_t n_seqs, uint64_t n, uint32_t *dist_req, void *ws,
+                                size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
  * Hit-ratio and compute-savings histograms over capacity edges.

@@ -28,9 +28,7 @@ static const char *kernel_name(KernelId k) {
     case K_MRC_HIST: return "mrc_hist";
     case K_MRC_COST: return "mrc_cost";
     case K_REQ_ORDER: return "request_order";
-    case K_REQ_KEYS: return "request_keys";
-    case K_SD_LOCAL_REQ: return "sd_local_request";
-    case K_REQ_SORT: return "request_sort";
+    case K_REQ_DIST: return "request_distance";
     case K_COUNT: break;
     }
     return "";

@@ -57,9 +57,7 @@ enum KernelId {
     K_MRC_HIST,
     K_MRC_COST,
     K_REQ_ORDER,
-    K_REQ_KEYS,
-    K_SD_LOCAL_REQ,
-    K_REQ_SORT,
+    K_REQ_DIST,
     K_COUNT
 };
 
@@ -82,19 +80,6 @@ int device_cus();
 // fill a uint32 array with a value on a stream (used instead of memset so the
 // same code stays valid under graph capture)
 pc_status fill_u32(uint32_t *p, uint32_t value, size_t count, hipStream_t s);
-
-// Stable LSD sort of n (key, value) pairs by the low 8 * passes key bits
-// (1 <= passes <= 4) with the onesweep passes of pc_prev_next_use, for
-// callers inside the library.  All buffers are the caller's: k1, k2
-// (uint64[n]), v1, v2 (uint32[n]), status (uint64[sort_status_words(n)]),
-// hist, start (uint32[8 * 256]), counters (uint32[8]); err is the workspace
-// header word that records look-back timeouts.  vals_in may be null (value =
-// index).  The sorted pairs end in (k1, v1) after an odd number of passes,
-// in (k2, v2) after an even one.
-size_t sort_status_words(uint64_t n);
-pc_status sort_pairs_low(const uint64_t *keys_in, const uint32_t *vals_in, uint64_t n, int passes, uint64_t *k1,
-                         uint64_t *k2, uint32_t *v1, uint32_t *v2, uint64_t *status, uint32_t *hist,
-                         uint32_t *start, uint32_t *counters, int32_t *err, hipStream_t s);
 
 // ------------------------------------------------------------ device helpers
 __device__ __forceinline__ uint64_t lanemask_lt() {

@@ -721,37 +721,6 @@ static SortWs carve_sort(void *ws, uint64_t n) {
     return w;
 }
 
-size_t sort_status_words(uint64_t n) { return ((n + SORT_TILE - 1) / SORT_TILE) * RADIX; }
-
-pc_status sort_pairs_low(const uint64_t *keys_in, const uint32_t *vals_in, uint64_t n, int passes, uint64_t *k1,
-                         uint64_t *k2, uint32_t *v1, uint32_t *v2, uint64_t *status, uint32_t *hist,
-                         uint32_t *start, uint32_t *counters, int32_t *err, hipStream_t s) {
-    if (passes < 1 || passes > SORT_PASSES / 2 || n == 0) return PC_ERR_INVALID;
-    const uint64_t tiles = (n + SORT_TILE - 1) / SORT_TILE;
-    pc_status st;
-    if ((st = fill_u32(hist, 0u, SORT_PASSES * RADIX, s)) != PC_OK) return st;
-    if ((st = fill_u32(counters, 0u, SORT_PASSES, s)) != PC_OK) return st;
-    if ((st = fill_u32(reinterpret_cast<uint32_t *>(status), 0u, tiles * RADIX * 2, s)) != PC_OK) return st;
-    const int cus = device_cus();
-    uint64_t hg = (n + 4095) / 4096;
-    if (hg > (uint64_t)cus * 4) hg = (uint64_t)cus * 4;
-    PC_LAUNCH(K_REQ_SORT, sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys_in, n, 0, hist,
-              (const int32_t *)nullptr);
-    PC_LAUNCH(K_REQ_SORT, sort_scan_kernel, dim3(1), dim3(RADIX), 0, s, hist, 0, start, (const int32_t *)nullptr);
-    const uint64_t *kin = keys_in;
-    const uint32_t *vin = vals_in;
-    for (int p = 0; p < passes; ++p) {
-        uint64_t *kout = (p & 1) ? k2 : k1;
-        uint32_t *vout = (p & 1) ? v2 : v1;
-        PC_LAUNCH(K_REQ_SORT, sort_pass_kernel, dim3((unsigned)tiles), dim3(SORT_THREADS), 0, s, kin, vin, kout,
-                  vout, n, 8 * p, start + p * RADIX, status, counters + p, (uint32_t)(p + 1), err,
-                  (const int32_t *)nullptr);
-        kin = kout;
-        vin = vout;
-    }
-    return PC_OK;
-}
-
 }  // namespace pc
 
 extern "C" {

@@ -500,38 +500,10 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
 // level-A counts go straight into a slot per t (acc included), so only the
 // six low bits of t are staged for level B, and the prev values needed at the
 // end are loaded up front; LDS stays under 40 KB (four workgroups per CU).
-// In request mode (REQ) the count is taken over the elements in (request, v)
-// order, and the output combines it with the per-access distance dpa:
-// D_req(t) = dpa(t) - count(t) + s(t) - Z(t), s(t) = first access of t's
-// request (found through the page table req_page and blk_off).
-__device__ __forceinline__ uint32_t req_find(const uint64_t *__restrict__ blk_off, uint32_t lo, uint32_t hi,
-                                             uint64_t t) {
-    // largest r in [lo, hi] with blk_off[r] <= t
-    while (lo < hi) {
-        const uint32_t mid = lo + (hi - lo + 1) / 2;
-        if (blk_off[mid] <= t) lo = mid;
-        else hi = mid - 1;
-    }
-    return lo;
-}
-
-// requests that can contain positions of page p (a 4096-range)
-__device__ __forceinline__ void req_page_range(const uint32_t *__restrict__ req_page, uint64_t pages, uint32_t n_seqs,
-                                               uint64_t p, uint32_t *lo, uint32_t *hi) {
-    uint32_t a = req_page[p];
-    uint32_t b = p + 1 < pages ? req_page[p + 1] : n_seqs - 1;
-    a = a < n_seqs ? a : n_seqs - 1;   // clamps keep inconsistent layouts in bounds
-    b = b < n_seqs ? b : n_seqs - 1;
-    *lo = a;
-    *hi = b > a ? b : a;
-}
-
-template <bool REQ>
 __global__ __launch_bounds__(LOC_THREADS, 6) void sd_local_kernel(
     const uint32_t *__restrict__ in_t, const uint32_t *__restrict__ in_acc,
     const uint32_t *__restrict__ prev, uint64_t n, const uint32_t *__restrict__ Zc,
-    uint32_t *__restrict__ dist, const uint32_t *__restrict__ dpa, const uint64_t *__restrict__ blk_off,
-    uint32_t n_seqs, const uint32_t *__restrict__ req_page) {
+    uint32_t *__restrict__ dist) {
     __shared__ uint32_t slot[LOCAL_SPAN];           // by t: acc + counts; first the column-prefix sums
     __shared__ uint16_t s_h[LOC_CHUNKS][64];        // chunk histograms -> column prefix
     __shared__ uint16_t s_pl[LOC_CHUNKS][64];       // 2-D prefix (earlier chunks, smaller digit)
@@ -645,74 +617,89 @@ __global__ __launch_bounds__(LOC_THREADS, 6) void sd_local_kernel(
     for (int j = 0; j < PER; ++j) cold += (tbase + j < n && p[j] == NONE) ? 1u : 0u;
     uint32_t allcold;
     uint32_t z = Zc[blockIdx.x] + block_excl_scan(cold, s_tmp, &allcold);
-    if (!REQ) {
 #pragma unroll
-        for (int j = 0; j < PER; ++j) {
-            const uint64_t tt = tbase + j;
-            if (tt < n) {
-                if (p[j] == NONE) {
-                    dist[tt] = NONE;
-                    ++z;
-                } else {
-                    dist[tt] = z + slot[tt - r0] - (p[j] + 1u);
-                }
-            }
-        }
-    } else {
-        uint32_t lo, hi;
-        req_page_range(req_page, (n + LOCAL_SPAN - 1) / LOCAL_SPAN, n_seqs, blockIdx.x, &lo, &hi);
-        uint32_t r = req_find(blk_off, lo, hi, tbase);
-#pragma unroll
-        for (int j = 0; j < PER; ++j) {
-            const uint64_t tt = tbase + j;
-            if (tt < n) {
-                while (r < hi && blk_off[r + 1] <= tt) ++r;
-                if (p[j] == NONE) {
-                    dist[tt] = NONE;
-                    ++z;
-                } else {
-                    dist[tt] = dpa[tt] - slot[tt - r0] + (uint32_t)blk_off[r] - z;
-                }
+    for (int j = 0; j < PER; ++j) {
+        const uint64_t tt = tbase + j;
+        if (tt < n) {
+            if (p[j] == NONE) {
+                dist[tt] = NONE;
+                ++z;
+            } else {
+                dist[tt] = z + slot[tt - r0] - (p[j] + 1u);
             }
         }
     }
 }
 
-// ---- request-level residency helpers -------------------------------------
-// req_page[p] = the request holding position p * 4096; also checks the layout
-// (blk_off[0] = 0, non-decreasing, blk_off[n_seqs] = n).
-__global__ void req_page_kernel(const uint64_t *__restrict__ blk_off, uint32_t n_seqs, uint64_t n,
-                                uint32_t *__restrict__ req_page, int32_t *__restrict__ err) {
-    const uint64_t r = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (r == 0 && (blk_off[0] != 0 || blk_off[n_seqs] != n)) atomicOr(err, DEV_ERR_BAD_LAYOUT);
-    if (r >= n_seqs) return;
-    const uint64_t a = blk_off[r], b = blk_off[r + 1];
-    if (a > b || b > n) {
-        atomicOr(err, DEV_ERR_BAD_LAYOUT);
-        return;
-    }
-    for (uint64_t pg = (a + LOCAL_SPAN - 1) / LOCAL_SPAN; pg * LOCAL_SPAN < b; ++pg) req_page[pg] = (uint32_t)r;
+// ---- request-level residency --------------------------------------------
+// Inclusive prefix max across the 64 lanes of a wave (the DPP pattern of
+// wave_incl_scan; lanes shifted in from outside a row contribute 0).
+__device__ __forceinline__ uint32_t wave_incl_max(uint32_t x) {
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false));   // row_shr:1
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false));   // row_shr:2
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false));   // row_shr:4
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false));   // row_shr:8
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false));   // row_bcast:15
+    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false));   // row_bcast:31
+    return x;
 }
 
-// Sort input for the request-order count: element i (in v order, i.e. the
-// access whose previous use is i) is t = next[i]; its key is t's request
-// (accesses never reused get key n_seqs and sort last).
-__global__ __launch_bounds__(256) void req_keys_kernel(const uint32_t *__restrict__ next, uint64_t n,
+// Request-level distance from the per-access distance of the request-ordered
+// stream.  With v = prev + 1 (0 for a cold access) and t in request [s, e):
+//     dist_req(t) = dist(t) - #{ j in [s, t) : v(j) < v(t) }.
+// When v(t) exceeds every earlier v of its request the count is t - s.  That
+// is always so for chained prefix keys: a block's last use is no later than
+// the last use of any shallower block of its chain, and each request lists
+// its shallower blocks after its deeper ones.  Other key streams take a
+// direct count over [s, t) for the accesses that break the order.
+// One wave per request (grid-stride), REQ_ITEMS x 64 accesses per step.
+constexpr int REQ_ITEMS = 8;
+
+__global__ __launch_bounds__(256) void req_dist_kernel(const uint32_t *__restrict__ prev,
+                                                       const uint32_t *__restrict__ dist,
                                                        const uint64_t *__restrict__ blk_off, uint32_t n_seqs,
-                                                       const uint32_t *__restrict__ req_page,
-                                                       uint64_t *__restrict__ key, uint32_t *__restrict__ val) {
-    const uint64_t pages = (n + LOCAL_SPAN - 1) / LOCAL_SPAN;
-    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-        const uint32_t t = next[i];
-        uint64_t k = n_seqs;
-        if (t != NONE && (uint64_t)t < n) {
-            uint32_t lo, hi;
-            req_page_range(req_page, pages, n_seqs, (uint64_t)t / LOCAL_SPAN, &lo, &hi);
-            k = req_find(blk_off, lo, hi, t);
+                                                       uint64_t n, uint32_t *__restrict__ dist_req,
+                                                       int32_t *__restrict__ err) {
+    const int lane = threadIdx.x & (WAVE - 1);
+    const uint32_t waves = gridDim.x * (blockDim.x / WAVE);
+    const uint32_t w0 = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / WAVE) + threadIdx.x / WAVE);
+    if (w0 == 0 && lane == 0 && (blk_off[0] != 0 || blk_off[n_seqs] != n)) atomicOr(err, DEV_ERR_BAD_LAYOUT);
+    for (uint32_t r = w0; r < n_seqs; r += waves) {
+        const uint64_t s = blk_off[r], e = blk_off[r + 1];
+        if (s > e || e > n) {
+            if (lane == 0) atomicOr(err, DEV_ERR_BAD_LAYOUT);
+            continue;
         }
-        key[i] = k;
-        val[i] = t;
+        uint32_t carry = 0;   // max v over the request's accesses before this step
+        for (uint64_t base = s; base < e; base += REQ_ITEMS * WAVE) {
+            uint32_t v[REQ_ITEMS], d[REQ_ITEMS];
+#pragma unroll
+            for (int i = 0; i < REQ_ITEMS; ++i) {
+                const uint64_t t = base + i * WAVE + lane;
+                const bool ok = t < e;
+                v[i] = ok ? prev[t] + 1u : 0u;
+                d[i] = ok ? dist[t] : 0u;
+            }
+#pragma unroll
+            for (int i = 0; i < REQ_ITEMS; ++i) {
+                const uint64_t t = base + i * WAVE + lane;
+                // v(t) is above every earlier v iff it is the prefix max and
+                // above the carry (earlier non-zero v are distinct from it)
+                const uint32_t incl = wave_incl_max(v[i]);
+                const bool top = v[i] == incl && v[i] > carry;
+                carry = max(carry, (uint32_t)__builtin_amdgcn_readlane((int)incl, WAVE - 1));
+                if (t >= e) continue;
+                if (v[i] == 0u) {
+                    dist_req[t] = NONE;
+                } else if (top) {
+                    dist_req[t] = d[i] - (uint32_t)(t - s);
+                } else {
+                    uint32_t c = 0;
+                    for (uint64_t j = s; j < t; ++j) c += (prev[j] + 1u < v[i]) ? 1u : 0u;
+                    dist_req[t] = d[i] - c;
+                }
+            }
+        }
     }
 }
 
@@ -776,12 +763,6 @@ static SdPlan plan_sd(uint64_t n) {
     return p;
 }
 
-struct ReqWs {
-    uint64_t *k1, *k2;
-    uint32_t *v1, *v2;
-    uint64_t *status;
-    uint32_t *hist, *start, *counters, *req_page;
-};
 
 struct SdWs {
     int32_t *hdr;
@@ -793,9 +774,8 @@ struct SdWs {
     size_t bytes;
 };
 
-// Workspace of one call.  In request mode the level buffers (t, acc) x 2
-// live inside the sort's key buffers, which are free once the sort is done.
-static SdWs carve_sd(void *ws, uint64_t n, const SdPlan &p, bool req = false, ReqWs *rq = nullptr) {
+// workspace of one call
+static SdWs carve_sd(void *ws, uint64_t n, const SdPlan &p) {
     Carver c{(char *)ws, 0};
     SdWs w;
     const uint64_t nchunks = (n + LOCAL_SPAN - 1) / LOCAL_SPAN;
@@ -808,12 +788,10 @@ static SdWs carve_sd(void *ws, uint64_t n, const SdPlan &p, bool req = false, Re
     w.part_ex = c.take<uint32_t>(nblocks + 2);
     w.tcount = c.take<uint32_t>(p.max_buckets + 1);
     w.tfirst = c.take<uint32_t>(p.max_buckets + 2);
-    if (!req) {
-        w.at = c.take<uint32_t>(n);
-        w.aa = c.take<uint32_t>(n);
-        w.bt = c.take<uint32_t>(n);
-        w.ba = c.take<uint32_t>(n);
-    }
+    w.at = c.take<uint32_t>(n);
+    w.aa = c.take<uint32_t>(n);
+    w.bt = c.take<uint32_t>(n);
+    w.ba = c.take<uint32_t>(n);
     w.cnt = c.take<uint16_t>(p.max_grid * DOM_RADIX);
     w.seg = c.take<uint8_t>(p.max_grid);
     w.ghas = c.take<uint8_t>(groups);
@@ -821,23 +799,6 @@ static SdWs carve_sd(void *ws, uint64_t n, const SdPlan &p, bool req = false, Re
     w.gin = c.take<uint32_t>(groups * DOM_RADIX);
     w.pre = c.take<uint32_t>(p.max_grid * DOM_RADIX);
     w.tile_bucket = c.take<uint32_t>(p.max_grid);
-    if (req) {
-        ReqWs r;
-        r.k1 = c.take<uint64_t>(n);
-        r.k2 = c.take<uint64_t>(n);
-        r.v1 = c.take<uint32_t>(n);
-        r.v2 = c.take<uint32_t>(n);
-        r.status = c.take<uint64_t>(sort_status_words(n));
-        r.hist = c.take<uint32_t>(8 * 256);
-        r.start = c.take<uint32_t>(8 * 256);
-        r.counters = c.take<uint32_t>(8);
-        r.req_page = c.take<uint32_t>(nchunks + 2);
-        w.at = reinterpret_cast<uint32_t *>(r.k1);
-        w.aa = w.at ? w.at + n : nullptr;
-        w.bt = reinterpret_cast<uint32_t *>(r.k2);
-        w.ba = w.bt ? w.bt + n : nullptr;
-        if (rq) *rq = r;
-    }
     w.bytes = c.off;
     return w;
 }
@@ -929,9 +890,8 @@ pc_status pc_stack_distance(const uint32_t *prev, const uint32_t *next, uint64_t
     uint32_t *lt, *la;
     if ((st = pc::sd_levels(next, n, p, w, s, &lt, &la)) != PC_OK) return st;
     const uint64_t nchunks = (n + pc::LOCAL_SPAN - 1) / pc::LOCAL_SPAN;
-    PC_LAUNCH(pc::K_SD_LOCAL, pc::sd_local_kernel<false>, dim3((unsigned)nchunks), dim3(pc::LOC_THREADS), 0, s,
-              lt, la, prev, n, w.Zc, dist, (const uint32_t *)nullptr, (const uint64_t *)nullptr, 0u,
-              (const uint32_t *)nullptr);
+    PC_LAUNCH(pc::K_SD_LOCAL, pc::sd_local_kernel, dim3((unsigned)nchunks), dim3(pc::LOC_THREADS), 0, s, lt, la,
+              prev, n, w.Zc, dist);
     return PC_OK;
 }
 
@@ -958,54 +918,24 @@ pc_status pc_request_order(const uint64_t *keys, const uint32_t *depth, const ui
     return PC_OK;
 }
 
-// bytes of the request key (0 .. n_seqs) the sort has to look at
-static int sort_passes_for(uint32_t n_seqs) {
-    int bits = 0;
-    while (bits < 32 && ((uint64_t)1 << bits) <= (uint64_t)n_seqs) ++bits;
-    return bits <= 8 ? 1 : (bits + 7) / 8;
-}
+size_t pc_stack_distance_req_ws(void) { return pc::WS_HEADER; }
 
-size_t pc_stack_distance_req_ws(uint64_t n, uint32_t n_seqs) {
-    (void)n_seqs;
-    const pc::SdPlan p = pc::plan_sd(n);
-    return pc::carve_sd(nullptr, n, p, true).bytes;
-}
-
-pc_status pc_stack_distance_req(const uint32_t *prev, const uint32_t *next, const uint32_t *dist,
-                                const uint64_t *blk_off, uint32_t n_seqs, uint64_t n, uint32_t *dist_req, void *ws,
-                                size_t ws_bytes, void *stream) {
+pc_status pc_stack_distance_req(const uint32_t *prev, const uint32_t *dist, const uint64_t *blk_off, uint32_t n_seqs,
+                                uint64_t n, uint32_t *dist_req, void *ws, size_t ws_bytes, void *stream) {
     if (n >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
-    if (n > 0 && (!prev || !next || !dist || !dist_req || !blk_off || n_seqs == 0)) return PC_ERR_INVALID;
+    if (n > 0 && (!prev || !dist || !dist_req || !blk_off || n_seqs == 0)) return PC_ERR_INVALID;
     if (n_seqs >= 0x80000000u) return PC_ERR_TOO_LARGE;
     if (!ws) return PC_ERR_WORKSPACE;
-    if (ws_bytes < pc_stack_distance_req_ws(n, n_seqs)) return PC_ERR_WORKSPACE;
+    if (ws_bytes < pc_stack_distance_req_ws()) return PC_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
-    const pc::SdPlan p = pc::plan_sd(n);
-    pc::ReqWs r;
-    pc::SdWs w = pc::carve_sd(ws, n, p, true, &r);
-    pc_status st = pc::fill_u32(reinterpret_cast<uint32_t *>(w.hdr), 0u, 1, s);
+    int32_t *hdr = reinterpret_cast<int32_t *>(ws);
+    pc_status st = pc::fill_u32(reinterpret_cast<uint32_t *>(hdr), 0u, 1, s);
     if (st != PC_OK || n == 0) return st;
-    const uint64_t pages = (n + pc::LOCAL_SPAN - 1) / pc::LOCAL_SPAN;
-    if ((st = pc::fill_u32(r.req_page, 0u, pages + 1, s)) != PC_OK) return st;
-    PC_LAUNCH(pc::K_REQ_KEYS, pc::req_page_kernel, dim3((unsigned)(((uint64_t)n_seqs + 255) / 256)), dim3(256), 0,
-              s, blk_off, n_seqs, n, r.req_page, w.hdr);
-    // the accesses in v order (next[] read in index order) keyed by their
-    // request, then stably sorted by it: (request, v) order
     const int cus = pc::device_cus();
-    uint64_t kg = (n + 255) / 256;
-    if (kg > (uint64_t)cus * 16) kg = (uint64_t)cus * 16;
-    PC_LAUNCH(pc::K_REQ_KEYS, pc::req_keys_kernel, dim3((unsigned)kg), dim3(256), 0, s, next, n, blk_off, n_seqs,
-              r.req_page, r.k2, r.v2);
-    const int passes = sort_passes_for(n_seqs);
-    if ((st = pc::sort_pairs_low(r.k2, r.v2, n, passes, r.k1, r.k2, r.v1, r.v2, r.status, r.hist, r.start,
-                                 r.counters, w.hdr, s)) != PC_OK)
-        return st;
-    const uint32_t *sorted = (passes & 1) ? r.v1 : r.v2;
-    if ((st = pc::sd_cold_prefix(prev, n, w, s)) != PC_OK) return st;
-    uint32_t *lt, *la;
-    if ((st = pc::sd_levels(sorted, n, p, w, s, &lt, &la)) != PC_OK) return st;
-    PC_LAUNCH(pc::K_SD_LOCAL_REQ, pc::sd_local_kernel<true>, dim3((unsigned)pages), dim3(pc::LOC_THREADS), 0, s, lt,
-              la, prev, n, w.Zc, dist_req, dist, blk_off, n_seqs, r.req_page);
+    uint64_t grid = ((uint64_t)n_seqs + 3) / 4;
+    if (grid > (uint64_t)cus * 16) grid = (uint64_t)cus * 16;
+    PC_LAUNCH(pc::K_REQ_DIST, pc::req_dist_kernel, dim3((unsigned)grid), dim3(256), 0, s, prev, dist, blk_off, n_seqs,
+              n, dist_req, hdr);
     return PC_OK;
 }
 

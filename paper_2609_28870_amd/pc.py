@@ -21,7 +21,6 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "_lib", "libpc.so")
 NONE = 0xFFFFFFFF
-HEADER = 256   # bytes of status header at the start of every workspace
 
 _lib = None
 
@@ -65,9 +64,9 @@ def lib():
     L.pc_request_order.restype = _st
     L.pc_request_order.argtypes = [_vp, _vp, _vp, _u32, _u64, _vp, _vp, _vp, _sz, _vp]
     L.pc_stack_distance_req_ws.restype = _sz
-    L.pc_stack_distance_req_ws.argtypes = [_u64, _u32]
+    L.pc_stack_distance_req_ws.argtypes = []
     L.pc_stack_distance_req.restype = _st
-    L.pc_stack_distance_req.argtypes = [_vp, _vp, _vp, _vp, _u32, _u64, _vp, _vp, _sz, _vp]
+    L.pc_stack_distance_req.argtypes = [_vp, _vp, _vp, _u32, _u64, _vp, _vp, _sz, _vp]
     L.pc_mrc_weighted_ws.restype = _sz
     L.pc_mrc_weighted_ws.argtypes = [_u64, _u32]
     L.pc_mrc_weighted.restype = _st
@@ -220,18 +219,18 @@ def request_order(keys: torch.Tensor, blk_off: torch.Tensor, depth: Optional[tor
     return keys_out, depth_out, ws
 
 
-def stack_distance_req(prev: torch.Tensor, nxt: torch.Tensor, dist: torch.Tensor, blk_off: torch.Tensor,
+def stack_distance_req(prev: torch.Tensor, dist: torch.Tensor, blk_off: torch.Tensor,
                        dist_req: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
-    """pc_stack_distance_req: request-level stack distances from prev, next
-    and dist of the request-ordered accesses."""
+    """pc_stack_distance_req: request-level stack distances from prev and
+    dist of the request-ordered accesses."""
     L = lib()
     n = prev.numel()
     n_seqs = blk_off.numel() - 1
     if dist_req is None:
         dist_req = torch.empty(n, dtype=torch.int32, device=_dev())
     if ws is None:
-        ws = workspace(L.pc_stack_distance_req_ws(n, n_seqs))
-    check(L.pc_stack_distance_req(_ptr(prev), _ptr(nxt), _ptr(dist), _ptr(blk_off), n_seqs, n,
+        ws = workspace(L.pc_stack_distance_req_ws())
+    check(L.pc_stack_distance_req(_ptr(prev), _ptr(dist), _ptr(blk_off), n_seqs, n,
                                   _ptr(dist_req), _ptr(ws), ws.numel(), _stream()))
     return dist_req, ws
 
@@ -332,7 +331,6 @@ class Pipeline:
         self.request = residency == "request"
         self.with_nextuse = with_nextuse and not self.request
         n = self.n
-        n_seqs = tok_len.numel()
         self.keys = torch.empty(n, dtype=torch.int64, device=dev)
         self.depth = torch.empty(n, dtype=torch.int32, device=dev)
         self.prev = torch.empty(n, dtype=torch.int32, device=dev)
@@ -341,7 +339,7 @@ class Pipeline:
         k = caps.numel()
         self.bins = {name: torch.empty(k + 1, dtype=torch.int64, device=dev)
                      for name in ("count", "depthsum", "cost_lo", "cost_hi", "nextuse")}
-        self.ws_hash = workspace(L.pc_hash_blocks_ws(n_seqs))
+        self.ws_hash = workspace(L.pc_hash_blocks_ws(tok_len.numel()))
         self.ws_pn = workspace(L.pc_prev_next_use_ws(n))
         self.ws_sd = workspace(L.pc_stack_distance_ws(n))
         if self.request:
@@ -349,13 +347,7 @@ class Pipeline:
             self.depth_r = torch.empty(n, dtype=torch.int32, device=dev)
             self.dist_req = torch.empty(n, dtype=torch.int32, device=dev)
             self.ws_ro = workspace(L.pc_request_order_ws())
-            # The request-level call runs after prev/next on the same stream,
-            # so it reuses the prev/next workspace, shifted by one header so
-            # that both status headers survive the run.
-            req = L.pc_stack_distance_req_ws(n, n_seqs) + HEADER
-            if req > self.ws_pn.numel():
-                self.ws_pn = workspace(req)
-            self.ws_req = self.ws_pn[HEADER:]
+            self.ws_req = workspace(L.pc_stack_distance_req_ws())
         self.ws_mrc = workspace(L.pc_mrc_weighted_ws(n, k))
 
     def run(self):
@@ -371,8 +363,7 @@ class Pipeline:
                       ws=self.ws_ro)
         prev_next_use(self.keys_r, self.prev, self.next, ws=self.ws_pn)
         stack_distance(self.prev, self.next, self.dist, ws=self.ws_sd)
-        stack_distance_req(self.prev, self.next, self.dist, self.blk_off, dist_req=self.dist_req,
-                           ws=self.ws_req)
+        stack_distance_req(self.prev, self.dist, self.blk_off, dist_req=self.dist_req, ws=self.ws_req)
         mrc_weighted(self.dist_req, self.caps, self.depth_r, None, self.alpha, self.beta,
                      out=self.bins, ws=self.ws_mrc)
 

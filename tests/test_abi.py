@@ -100,11 +100,10 @@ def test_request_order_rejects_bad_arguments(L):
 
 def test_stack_distance_req_rejects_bad_arguments(L):
     n = 5000
-    ws = L.pc_stack_distance_req_ws(n, 40)
-    assert ws > L.pc_stack_distance_ws(n)
-    assert L.pc_stack_distance_req_ws(10 ** 6, 40) > ws
+    ws = L.pc_stack_distance_req_ws()
+    assert ws >= 256
     call = lambda prev=FAKE, ns=40, n=n, out=FAKE, w=FAKE, wsz=ws: L.pc_stack_distance_req(
-        prev, FAKE, FAKE, FAKE, ns, n, out, w, wsz, None)
+        prev, FAKE, FAKE, ns, n, out, w, wsz, None)
     assert call(n=0xFFFFFFFF) == -2
     assert call(ns=0x80000000) == -2
     assert call(prev=None) == -1
@@ -140,5 +139,5 @@ def test_profiling_table(L):
     names = [L.pc_prof_kernel_name(i).decode() for i in range(n)]
     assert "hash_chain" in names and "sd_dominance_pass" in names and "mrc_hist" in names
     assert all(names) and len(set(names)) == n
-    assert names[-1] == "request_sort"
+    assert names[-1] == "request_distance"
     assert pc.prof_read() is not None

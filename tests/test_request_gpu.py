@@ -56,7 +56,7 @@ def gpu_request_path(keys, blk_off, depth=None):
     assert pc.workspace_status(ws) == 0
     dist, ws = pc.stack_distance(prev, nxt)
     assert pc.workspace_status(ws) == 0
-    dreq, ws = pc.stack_distance_req(prev, nxt, dist, bo)
+    dreq, ws = pc.stack_distance_req(prev, dist, bo)
     assert pc.workspace_status(ws) == 0
     out = dict(keys_r=pc.as_u64(kr), prev=pc.as_u32(prev), next=pc.as_u32(nxt), dist=pc.as_u32(dist),
                dist_req=pc.as_u32(dreq))
@@ -189,6 +189,19 @@ def test_repeated_request_reuses_from_the_top():
     assert np.array_equal(got[m:], np.arange(m, dtype=np.uint32))
 
 
+def test_scrambled_reuse_takes_the_direct_count():
+    """Keys that are not prefix chains: later requests re-read earlier blocks
+    in shuffled order, so their previous uses are out of order inside the
+    request and the kernel counts them directly (large requests included)."""
+    rng = np.random.default_rng(21)
+    pool = np.arange(1, 20001, dtype=np.uint64) * np.uint64(0x9E3779B1)
+    reqs = [pool[:6000], rng.permutation(pool[:6000]), pool[3000:9000],
+            rng.permutation(pool[:12000])[:7000], rng.permutation(pool[5000:20000])]
+    keys = np.concatenate(reqs)
+    bo = np.concatenate([[0], np.cumsum([r.size for r in reqs])]).astype(np.uint64)
+    check_request_path(keys, bo, label="scrambled", exact_walk=False)
+
+
 @pytest.mark.parametrize("n", [0, 1, 2, 4095, 4096, 4097, 8193])
 def test_ragged_sizes(n):
     keys = pcgen.random_keys(max(n, 1), max(n // 4, 1), n)[:n]
@@ -217,7 +230,7 @@ def test_bad_layout_is_reported():
     prev, nxt, _ = pc.prev_next_use(pc.to_dev_u64(keys))
     dist, _ = pc.stack_distance(prev, nxt)
     for bo in ([0, 50, 99], [0, 60, 40, 100], [1, 50, 100]):
-        _, ws = pc.stack_distance_req(prev, nxt, dist, pc.to_dev_u64(np.array(bo, np.uint64)))
+        _, ws = pc.stack_distance_req(prev, dist, pc.to_dev_u64(np.array(bo, np.uint64)))
         assert pc.workspace_status(ws) == 2, bo
     _, _, ws = pc.request_order(pc.to_dev_u64(keys), pc.to_dev_u64(np.array([0, 60, 40, 100], np.uint64)))
     assert pc.workspace_status(ws) == 2
