@@ -49,8 +49,11 @@ def log(*a):
 HIP_KERNEL = {"sort_onesweep_pass": "pc::sort_pass_kernel", "link_partition": "pc::link_partition_kernel",
               "perm_partition": "pc::perm_partition_kernel", "hash_digest": "pc::hash_digest_kernel",
               "hash_chain": "pc::hash_chain_kernel", "sd_local_finish": "pc::sd_local_kernel",
-              "perm_local": "pc::perm_local_kernel", "mrc_hist": "pc::mrc_hist_kernel"}
-PROFILE = os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9.md")
+              "perm_local": "pc::perm_local_kernel", "mrc_hist": "pc::mrc_hist_kernel",
+              "request_order": "pc::req_order_kernel", "request_distance": "pc::req_dist_kernel"}
+PROFILES = {"access": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9.md"),
+            "request": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_request.md")}
+PROFILE = PROFILES["access"]
 
 
 def source_sha256():
@@ -141,8 +144,8 @@ def main():
     ap.add_argument("--residency", default="access", choices=["access", "request"],
                     help="per-access LRU (default) or request-level residency (whole request pinned)")
     ap.add_argument("--cpu-sample", type=int, default=None,
-                    help="block accesses in the oracle's timed sample (0 = skip; default 2e7, "
-                         "4e5 with --residency request)")
+                    help="block accesses in the oracle's timed sample (0 = skip; default 1e8, "
+                         "1e6 with --residency request)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 4 GiB device copy (for rocprof counter calibration)")
     args = ap.parse_args()
@@ -168,6 +171,8 @@ def main():
     up = pc.upload_trace(trace, B)
     caps = pc.to_dev_u64(caps_np)
     request = args.residency == "request"
+    global PROFILE
+    PROFILE = PROFILES[args.residency]
     pipe = pc.Pipeline(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
                        caps, B, alpha, beta, residency=args.residency)
     torch.cuda.synchronize()
@@ -264,7 +269,7 @@ def main():
     # request-level bins hold only at capacities that fit the largest request
     min_cap = int((trace.tok_len // np.uint32(B)).max()) if request else 0
     cb = None
-    sample = args.cpu_sample if args.cpu_sample is not None else (400_000 if request else 20_000_000)
+    sample = args.cpu_sample if args.cpu_sample is not None else (1_000_000 if request else 100_000_000)
     if sample > 0:
         log("timing the CPU oracle on a %d-access sample" % sample)
         cb = cpu_baseline(trace, caps_np, alpha, beta, sample, request)
