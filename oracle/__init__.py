@@ -31,6 +31,12 @@ Each function states the definition it computes and the passage of the paper
   at once, room made ahead of time); readings: hits decided on arrival, the
   request's deepest block least recent afterwards, capacities below the
   largest request infeasible (Sec. 3.1 "Cache-size regimes").
+* ``stack_distance_session_walk`` / ``lru_session`` / ``mrc_bins_session``:
+  session-level eviction (Sec. 5.3 "Block-Level vs. Session-Level
+  Eviction": whole sessions evicted at once); readings: a session's
+  footprint is its largest request so far, sessions are kept in LRU order
+  and evicted whole from the least recent end, and a block hits if the
+  session that last used it is resident when the request arrives.
 """
 from __future__ import annotations
 
@@ -79,6 +85,12 @@ def lib():
         L.orc_stack_distance_req_walk.argtypes = [_u32p, _u64p, ctypes.c_uint64, ctypes.c_uint64, _u32p]
         L.orc_stack_distance_req_bit.restype = ctypes.c_int
         L.orc_stack_distance_req_bit.argtypes = [_u32p, _u64p, ctypes.c_uint64, ctypes.c_uint64, _u32p]
+        L.orc_session_sim.restype = ctypes.c_int
+        L.orc_session_sim.argtypes = [_u32p, _u32p, _u64p, _u32p, ctypes.c_uint64, ctypes.c_uint64,
+                                      ctypes.c_uint64, ctypes.c_uint64, _u64p, _u64p, _u8p]
+        L.orc_stack_distance_session_walk.restype = ctypes.c_int
+        L.orc_stack_distance_session_walk.argtypes = [_u32p, _u64p, _u32p, ctypes.c_uint64, ctypes.c_uint64,
+                                                      ctypes.c_uint64, _u32p]
         L.orc_lru_sim_req.restype = ctypes.c_int
         L.orc_lru_sim_req.argtypes = [_u32p, _u32p, _u64p, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64,
                                       _u64p, _u64p, _u8p]
@@ -362,3 +374,65 @@ def mrc_bins_req(keys, blk_off, caps, depth=None, alpha=1, beta=0, ids=None):
     dsum.append(int(np.asarray(depth, np.uint64).sum(dtype=np.uint64)) - pd)
     cost = [alpha * c + beta * d for c, d in zip(count, dsum)]
     return count, dsum, cost, feas
+
+
+def _sess(sess, n_seqs):
+    sess = _c(sess, np.uint32)
+    assert sess.size == n_seqs
+    return sess, (int(sess.max()) + 1 if sess.size else 0)
+
+
+def stack_distance_session_walk(keys, blk_off, sess, ids=None):
+    """Session-level distance of every access by walking the session recency
+    list: footprints of the session that last used the block and of every
+    session above it, less one; NONE if the block was never used before."""
+    if ids is None:
+        ids = key_ids(keys)
+    id_, n_ids = ids
+    bo, ns = _req(blk_off)
+    sv, n_sess = _sess(sess, ns)
+    d = np.empty(id_.size, np.uint32)
+    assert lib().orc_stack_distance_session_walk(_p(id_, _u32p), _p(bo, _u64p), _p(sv, _u32p), ns, n_ids,
+                                                 n_sess, _p(d, _u32p)) == 0
+    return d
+
+
+def lru_session(keys, blk_off, sess, caps, depth=None, ids=None, flags=False):
+    """Per capacity: (hits, depth sum over hits[, flags]) of a session-level
+    LRU cache simulated literally."""
+    if ids is None:
+        ids = key_ids(keys)
+    id_, n_ids = ids
+    bo, ns = _req(blk_off)
+    sv, n_sess = _sess(sess, ns)
+    dep = _c(depth, np.uint32) if depth is not None else None
+    out = []
+    for c in caps:
+        h = ctypes.c_uint64(0)
+        dh = ctypes.c_uint64(0)
+        fl = np.empty(id_.size, np.uint8) if flags else None
+        assert lib().orc_session_sim(_p(id_, _u32p), _p(dep, _u32p) if dep is not None else None, _p(bo, _u64p),
+                                     _p(sv, _u32p), ns, n_ids, n_sess, int(c), ctypes.byref(h), ctypes.byref(dh),
+                                     _p(fl, _u8p) if fl is not None else None) == 0
+        out.append((h.value, dh.value, fl) if flags else (h.value, dh.value))
+    return out
+
+
+def mrc_bins_session(keys, blk_off, sess, caps, depth=None, alpha=1, beta=0, ids=None):
+    """Bins over the capacity edges from one session-level simulation per
+    capacity (same layout as ``mrc_bins``)."""
+    keys = _c(keys, np.uint64)
+    n = keys.size
+    if depth is None:
+        depth = np.zeros(n, np.uint32)
+    res = lru_session(keys, blk_off, sess, caps, depth, ids)
+    count, dsum = [], []
+    ph, pd = 0, 0
+    for h, dh in res:
+        count.append(h - ph)
+        dsum.append(dh - pd)
+        ph, pd = h, dh
+    count.append(n - ph)
+    dsum.append(int(np.asarray(depth, np.uint64).sum(dtype=np.uint64)) - pd)
+    cost = [alpha * c + beta * d for c, d in zip(count, dsum)]
+    return count, dsum, cost

@@ -485,3 +485,118 @@ int orc_belady_sim(const uint32_t *id, const uint32_t *next, uint64_t n, uint64_
     free(h); free(cur); free(in);
     return 0;
 }
+
+/* ------------------------------------------------------------------ */
+/* Session-level eviction (Sec. 5.3 "Block-Level vs. Session-Level      */
+/* Eviction"): whole sessions are the unit of eviction.  Readings:      */
+/*  - a session's footprint after one of its requests is the largest   */
+/*    block count among its requests so far (append-only context);     */
+/*  - the cache keeps resident sessions in recency order of their      */
+/*    latest request; after each request its session moves to the     */
+/*    front with its new footprint, then whole sessions are evicted    */
+/*    from the least recent end while the resident footprints exceed   */
+/*    the capacity (the arriving session last of all);                 */
+/*  - a block hits if the session that made the previous access of the */
+/*    same block is resident when the request arrives.                 */
+/* Requests are blk_off[0..n_seqs] as above; sess[r] < n_sess is the   */
+/* session of request r.                                               */
+/* ------------------------------------------------------------------ */
+
+/* One session-level LRU cache of `cap` blocks, simulated literally. */
+int orc_session_sim(const uint32_t *id, const uint32_t *depth, const uint64_t *blk_off, const uint32_t *sess,
+                    uint64_t n_seqs, uint64_t n_ids, uint64_t n_sess, uint64_t cap, uint64_t *hits_out,
+                    uint64_t *depth_hits_out, uint8_t *hit_flag)
+{
+    uint32_t *last = (uint32_t *)malloc((n_ids + 1) * sizeof(uint32_t));   /* session of the last access */
+    uint32_t *nx = (uint32_t *)malloc((n_sess + 1) * sizeof(uint32_t));
+    uint32_t *pv = (uint32_t *)malloc((n_sess + 1) * sizeof(uint32_t));
+    uint64_t *fp = (uint64_t *)calloc(n_sess + 1, sizeof(uint64_t));
+    uint8_t *in = (uint8_t *)calloc(n_sess + 1, 1);
+    if (!last || !nx || !pv || !fp || !in) { free(last); free(nx); free(pv); free(fp); free(in); return -1; }
+    for (uint64_t i = 0; i <= n_ids; i++) last[i] = ORC_NONE;
+    uint32_t head = ORC_NONE, tail = ORC_NONE;
+    uint64_t total = 0, hits = 0, dh = 0;
+    for (uint64_t r = 0; r < n_seqs; r++) {
+        uint64_t a = blk_off[r], b = blk_off[r + 1];
+        uint32_t s = sess[r];
+        for (uint64_t t = a; t < b; t++) {
+            uint32_t q = last[id[t]];
+            int h = q != ORC_NONE && in[q];
+            if (h) { hits++; if (depth) dh += depth[t]; }
+            if (hit_flag) hit_flag[t] = (uint8_t)h;
+        }
+        for (uint64_t t = a; t < b; t++) last[id[t]] = s;
+        /* the session to the front with its new footprint */
+        if (in[s]) {
+            if (pv[s] != ORC_NONE) nx[pv[s]] = nx[s]; else head = nx[s];
+            if (nx[s] != ORC_NONE) pv[nx[s]] = pv[s]; else tail = pv[s];
+            total -= fp[s];
+        }
+        if (b - a > fp[s]) fp[s] = b - a;
+        in[s] = 1;
+        total += fp[s];
+        pv[s] = ORC_NONE;
+        nx[s] = head;
+        if (head != ORC_NONE) pv[head] = s; else tail = s;
+        head = s;
+        /* whole sessions out from the least recent end */
+        while (total > cap) {
+            uint32_t x = tail;
+            tail = pv[x];
+            if (tail != ORC_NONE) nx[tail] = ORC_NONE; else head = ORC_NONE;
+            in[x] = 0;
+            total -= fp[x];
+        }
+    }
+    *hits_out = hits;
+    if (depth_hits_out) *depth_hits_out = dh;
+    free(last); free(nx); free(pv); free(fp); free(in);
+    return 0;
+}
+
+/* Session-level distance of every access by walking the session recency
+ * list as it stands when the request arrives: with q the session of the
+ * block's previous access, the footprints of q and of every session above
+ * it, summed, less one (so the block hits at capacity c iff distance < c);
+ * ORC_NONE if the block was never used before. */
+int orc_stack_distance_session_walk(const uint32_t *id, const uint64_t *blk_off, const uint32_t *sess,
+                                    uint64_t n_seqs, uint64_t n_ids, uint64_t n_sess, uint32_t *dist)
+{
+    uint32_t *last = (uint32_t *)malloc((n_ids + 1) * sizeof(uint32_t));
+    uint32_t *nx = (uint32_t *)malloc((n_sess + 1) * sizeof(uint32_t));
+    uint32_t *pv = (uint32_t *)malloc((n_sess + 1) * sizeof(uint32_t));
+    uint64_t *fp = (uint64_t *)calloc(n_sess + 1, sizeof(uint64_t));
+    uint8_t *seen = (uint8_t *)calloc(n_sess + 1, 1);
+    if (!last || !nx || !pv || !fp || !seen) { free(last); free(nx); free(pv); free(fp); free(seen); return -1; }
+    for (uint64_t i = 0; i <= n_ids; i++) last[i] = ORC_NONE;
+    uint32_t head = ORC_NONE;
+    for (uint64_t r = 0; r < n_seqs; r++) {
+        uint64_t a = blk_off[r], b = blk_off[r + 1];
+        uint32_t s = sess[r];
+        for (uint64_t t = a; t < b; t++) {
+            uint32_t q = last[id[t]];
+            if (q == ORC_NONE) { dist[t] = ORC_NONE; continue; }
+            uint64_t sum = 0;
+            uint32_t x = head;
+            for (;;) {
+                sum += fp[x];
+                if (x == q) break;
+                x = nx[x];
+            }
+            dist[t] = (uint32_t)(sum - 1);   /* sum <= number of accesses < 2^32 */
+        }
+        for (uint64_t t = a; t < b; t++) last[id[t]] = s;
+        if (seen[s]) {
+            if (pv[s] != ORC_NONE) nx[pv[s]] = nx[s]; else head = nx[s];
+            if (nx[s] != ORC_NONE) pv[nx[s]] = pv[s];
+        }
+        seen[s] = 1;
+        if (b - a > fp[s]) fp[s] = b - a;
+        pv[s] = ORC_NONE;
+        nx[s] = head;
+        if (head != ORC_NONE) pv[head] = s;
+        head = s;
+    }
+    free(last); free(nx); free(pv); free(fp); free(seen);
+    return 0;
+}

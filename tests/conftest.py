@@ -48,3 +48,22 @@ def request_golden():
         want = [NONE if v == "-" else int(v) for v in row[bars[0] + 1:bars[1]]]
         hits = {int(c): int(h) for c, h in (x.split(":") for x in row[bars[1] + 1:])}
         yield row[0], keys, blk_off, want, hits
+
+
+def session_golden():
+    """(name, keys, blk_off, session per request, D per access, {capacity:
+    hits}) per row of the hand-worked session-level fixture."""
+    for row in read_golden("session_level_examples.txt"):
+        bars = [i for i, x in enumerate(row) if x == "|"]
+        names, snames, reqs, sess = {}, {}, [], []
+        for x in row[1:bars[0]]:
+            if x.endswith(":"):
+                reqs.append([])
+                sess.append(snames.setdefault(x[:-1], len(snames)))
+            elif x != "/":
+                reqs[-1].append(names.setdefault(x, len(names) + 7))
+        keys = np.array([k for r in reqs for k in r], np.uint64)
+        blk_off = np.concatenate([[0], np.cumsum([len(r) for r in reqs])]).astype(np.uint64)
+        want = [NONE if v == "-" else int(v) for v in row[bars[0] + 1:bars[1]]]
+        hits = {int(c): int(h) for c, h in (x.split(":") for x in row[bars[1] + 1:])}
+        yield row[0], keys, blk_off, np.array(sess, np.uint32), want, hits

@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 import oracle
-from conftest import read_golden, request_golden
+from conftest import read_golden, request_golden, session_golden
 
 NONE = oracle.NONE
 G = 0x9E3779B97F4A7C15
@@ -394,3 +394,83 @@ def test_request_level_identity_in_recency_order():
         got = oracle.stack_distance_req_walk(keys, blk_off).astype(np.int64)
         got[got == NONE] = -1
         assert np.array_equal(got[order], want_p)
+
+
+# ------------------------------------------------------- session level
+
+def test_session_level_hand_worked_examples():
+    for name, keys, blk_off, sess, want, hits in session_golden():
+        assert list(oracle.stack_distance_session_walk(keys, blk_off, sess)) == want, name
+        caps = sorted(hits)
+        got = oracle.lru_session(keys, blk_off, sess, caps)
+        assert [g[0] for g in got] == [hits[c] for c in caps], name
+
+
+def random_sessions(count, seed, append_only=True):
+    """Multi-turn sessions (append-only contexts, some starting from shared
+    prompts), or arbitrary requests tagged with sessions; keys distinct
+    inside a request."""
+    rng = np.random.default_rng(seed)
+    for _ in range(count):
+        n_sess = int(rng.integers(1, 7))
+        ctx = {s: [] for s in range(n_sess)}
+        shared = {p: [1000 * (p + 1) + d for d in range(int(rng.integers(1, 4)))] for p in range(2)}
+        reqs, sess, nxt = [], [], 1
+        for _r in range(int(rng.integers(1, 30))):
+            s = int(rng.integers(n_sess))
+            if append_only:
+                if not ctx[s] and rng.random() < 0.4:
+                    ctx[s] = list(shared[int(rng.integers(2))])
+                grow = int(rng.integers(0, 4))
+                ctx[s] = ctx[s] + list(range(nxt, nxt + grow))
+                nxt += grow
+                req = list(ctx[s])
+            else:
+                req = list(rng.choice(40, size=int(rng.integers(0, 6)), replace=False) + 1)
+            reqs.append(req)
+            sess.append(s)
+        keys = np.array([k for r in reqs for k in r], np.uint64)
+        if keys.size == 0:
+            continue
+        blk_off = np.concatenate([[0], np.cumsum([len(r) for r in reqs])]).astype(np.uint64)
+        yield keys, blk_off, np.array(sess, np.uint32)
+
+
+@pytest.mark.parametrize("append_only", [True, False])
+def test_session_level_simulation_hits_iff_distance_below_capacity(append_only):
+    """Session-level LRU is a stack algorithm: the literal simulation hits
+    exactly where the walked distance is below the capacity, per access and
+    at every capacity (so inclusion holds)."""
+    for keys, blk_off, sess in random_sessions(60, 31 if append_only else 32, append_only):
+        d = oracle.stack_distance_session_walk(keys, blk_off, sess).astype(np.int64)
+        caps = [0, 1, 2, 3, 4, 6, 9, 13, 20, 40, 1000]
+        res = oracle.lru_session(keys, blk_off, sess, caps, flags=True)
+        prev = None
+        for c, (h, _, fl) in zip(caps, res):
+            want = (d != NONE) & (d < c)
+            assert np.array_equal(fl.astype(bool), want), c
+            assert h == int(want.sum())
+            if prev is not None:
+                assert np.all(fl >= prev)
+            prev = fl
+
+
+def test_session_level_one_block_sessions_reduce_to_block_lru():
+    """Every request one block and every session one key: sessions are
+    blocks of size one, so session-level LRU is per-access LRU."""
+    rng = np.random.default_rng(5)
+    for _ in range(30):
+        sess = rng.integers(0, int(rng.integers(1, 12)), size=int(rng.integers(1, 80))).astype(np.uint32)
+        keys = sess.astype(np.uint64) * np.uint64(977) + np.uint64(3)
+        blk_off = np.arange(sess.size + 1, dtype=np.uint64)
+        assert np.array_equal(oracle.stack_distance_session_walk(keys, blk_off, sess),
+                              oracle.stack_distance_walk(keys))
+
+
+def test_session_level_everything_fits():
+    """With room for every session's footprint, each block that was used
+    before hits."""
+    for keys, blk_off, sess in random_sessions(20, 33):
+        p, _ = oracle.prev_next(keys)
+        (h, _), = oracle.lru_session(keys, blk_off, sess, [int(keys.size) + 1])
+        assert h == int((p != NONE).sum())
