@@ -50,9 +50,11 @@ HIP_KERNEL = {"sort_onesweep_pass": "pc::sort_pass_kernel", "link_partition": "p
               "perm_partition": "pc::perm_partition_kernel", "hash_digest": "pc::hash_digest_kernel",
               "hash_chain": "pc::hash_chain_kernel", "sd_local_finish": "pc::sd_local_kernel",
               "perm_local": "pc::perm_local_kernel", "mrc_hist": "pc::mrc_hist_kernel",
-              "request_order": "pc::req_order_kernel", "request_distance": "pc::req_dist_kernel"}
+              "request_order": "pc::req_order_kernel", "request_distance": "pc::req_dist_kernel",
+              "session_distance": "pc::sess_dist_kernel"}
 PROFILES = {"access": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9.md"),
-            "request": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_request.md")}
+            "request": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_request.md"),
+            "session": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_session.md")}
 PROFILE = PROFILES["access"]
 
 
@@ -119,7 +121,10 @@ def cpu_baseline(trace, caps, alpha, beta, budget_accesses, request=False):
     t0 = time.perf_counter()
     keys, depth = oracle.hash_trace(sub)
     ids = oracle.key_ids(keys)
-    if request:
+    if request == "session":
+        oracle.mrc_bins_session(keys, sub.blk_off(), sub.session.astype(np.uint32), caps, depth, alpha, beta, ids)
+        what = "prev/next + session-level bins (%d per-capacity session LRU simulations)" % len(caps)
+    elif request:
         oracle.mrc_bins_req(keys, sub.blk_off(), caps, depth, alpha, beta, ids)
         what = "request-level bins"
     else:
@@ -141,8 +146,9 @@ def main():
     ap.add_argument("--workload", default="full", choices=["tiny", "chat", "agent", "full"])
     ap.add_argument("--sessions", type=int, default=None, help="override the session count")
     ap.add_argument("--block-size", type=int, default=16)
-    ap.add_argument("--residency", default="access", choices=["access", "request"],
-                    help="per-access LRU (default) or request-level residency (whole request pinned)")
+    ap.add_argument("--residency", default="access", choices=["access", "request", "session"],
+                    help="per-access LRU (default), request-level residency (whole request pinned) "
+                         "or session-level eviction (whole sessions evicted)")
     ap.add_argument("--cpu-sample", type=int, default=None,
                     help="block accesses in the oracle's timed sample (0 = skip; default 1e8, "
                          "1e6 with --residency request)")
@@ -171,10 +177,11 @@ def main():
     up = pc.upload_trace(trace, B)
     caps = pc.to_dev_u64(caps_np)
     request = args.residency == "request"
+    session_mode = args.residency == "session"
     global PROFILE
     PROFILE = PROFILES[args.residency]
     pipe = pc.Pipeline(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
-                       caps, B, alpha, beta, residency=args.residency)
+                       caps, B, alpha, beta, residency=args.residency, session=up["session"])
     torch.cuda.synchronize()
     log("inputs resident in HBM; device memory in use %.1f GB" % (torch.cuda.memory_allocated() / 1e9))
 
@@ -225,7 +232,7 @@ def main():
         entry = {"launches_per_step": launches // args.steps, "working_launches_per_step": wl,
                  "ms_per_step": round(per_step, 4)}
         if name in ALGO_BYTES:
-            per_launch = (8 if request and name == "mrc_hist" else ALGO_BYTES[name](B)) * n_blocks
+            per_launch = (8 if (request or session_mode) and name == "mrc_hist" else ALGO_BYTES[name](B)) * n_blocks
             entry["algo_bytes_per_launch"] = per_launch
             entry["avg_working_launch_ms"] = round(per_step / wl, 4)
             entry["algo_GBps"] = round(per_launch * wl / per_step / 1e6, 1)
@@ -245,9 +252,11 @@ def main():
                 "sort_digit_scan": "prev_next", "sort_onesweep_pass": "prev_next",
                 "link_partition": "prev_next",
                 "perm_partition": "prev_next", "perm_local": "prev_next", "mrc_hist": "mrc",
-                "mrc_cost": "mrc", "request_order": "request_order", "request_distance": "request_distance"}
-    stage_bytes = {"hash": 4 * B + 8 + 4, "prev_next": 16, "stack_distance": 8, "mrc": 8 if request else 12,
-                   "request_order": 24, "request_distance": 12}
+                "mrc_cost": "mrc", "request_order": "request_order", "request_distance": "request_distance",
+                "session_requests": "session_distance", "session_distance": "session_distance"}
+    stage_bytes = {"hash": 4 * B + 8 + 4, "prev_next": 16, "stack_distance": 8,
+                   "mrc": 8 if request or session_mode else 12, "request_order": 24, "request_distance": 12,
+                   "session_distance": 8}
 
     def stage_name(kid):
         return stage_of.get(kid, "stack_distance" if kid.startswith("sd_") else "other")
@@ -272,7 +281,7 @@ def main():
     sample = args.cpu_sample if args.cpu_sample is not None else (1_000_000 if request else 100_000_000)
     if sample > 0:
         log("timing the CPU oracle on a %d-access sample" % sample)
-        cb = cpu_baseline(trace, caps_np, alpha, beta, sample, request)
+        cb = cpu_baseline(trace, caps_np, alpha, beta, sample, "session" if session_mode else request)
 
     out = {
         "metric": "KV-block accesses/sec for hash+stack-distance+MRC; achieved HBM GB/s",
@@ -297,8 +306,9 @@ def main():
             "processed_tokens": trace.processed_tokens(),
             "capacities": int(caps_np.size),
             "cost_model": "2*B*(P_lin + B*depth), P_lin=3e9",
-            "residency": "per-access LRU" if not request else
-                         "request-level (whole request resident; bins valid from %d blocks)" % min_cap,
+            "residency": ("request-level (whole request resident; bins valid from %d blocks)" % min_cap
+                          if request else "session-level (whole sessions evicted)" if session_mode
+                          else "per-access LRU"),
             "parallelism": "single GPU",
         },
         "roofline": roof,

@@ -173,6 +173,33 @@ pc_status pc_stack_distance_req(const uint32_t *prev, const uint32_t *dist, cons
                                 size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
+ * Session-level eviction (Sec. 5.3 "Block-Level vs. Session-Level Eviction":
+ * whole sessions are evicted at once, trading hit ratio at small capacities
+ * for far less metadata).  Readings: a session's footprint after one of its
+ * requests is the largest block count among its requests so far; resident
+ * sessions are kept in recency order of their latest request and evicted
+ * whole from the least recent end while their footprints exceed the
+ * capacity (the arriving session last); a block hits if the session that
+ * made its previous access is resident when the request arrives.  Footprints
+ * only grow, so this is a stack algorithm: a block hits at capacity c
+ * exactly when dist_sess < c, where dist_sess is the footprint of that
+ * session plus the latest footprints of all sessions active since its
+ * latest request, less one.  Keys inside one request must be distinct;
+ * otherwise results are unspecified (memory-safe).
+ *
+ *   prev     uint32[n] from pc_prev_next_use over the keys in request order
+ *   blk_off  uint64[n_seqs+1] request table (blk_off[n_seqs] = n)
+ *   session  uint32[n_seqs] session of each request (any ids)
+ *   dist_sess uint32[n] out, PC_NONE where prev is PC_NONE
+ * A bad request table sets the workspace status to 2; a look-back timeout
+ * in the request-level linking sets 1.
+ * ------------------------------------------------------------------------ */
+size_t pc_stack_distance_session_ws(uint64_t n, uint32_t n_seqs);
+pc_status pc_stack_distance_session(const uint32_t *prev, const uint64_t *blk_off, const uint32_t *session,
+                                    uint32_t n_seqs, uint64_t n, uint32_t *dist_sess, void *ws,
+                                    size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
  * Hit-ratio and compute-savings histograms over capacity edges.
  *
  * Paper: block hit ratio counts every access, compulsory misses included

@@ -29,6 +29,8 @@ static const char *kernel_name(KernelId k) {
     case K_MRC_COST: return "mrc_cost";
     case K_REQ_ORDER: return "request_order";
     case K_REQ_DIST: return "request_distance";
+    case K_SESS_REQ: return "session_requests";
+    case K_SESS_DIST: return "session_distance";
     case K_COUNT: break;
     }
     return "";

@@ -58,6 +58,8 @@ enum KernelId {
     K_MRC_COST,
     K_REQ_ORDER,
     K_REQ_DIST,
+    K_SESS_REQ,
+    K_SESS_DIST,
     K_COUNT
 };
 

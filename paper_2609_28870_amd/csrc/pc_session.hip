@@ -1,0 +1,219 @@
+// Session-level eviction (Sec. 5.3 "Block-Level vs. Session-Level Eviction":
+// whole sessions are evicted at once) as a size-weighted stack distance.
+//
+// Readings (the paper gives no simulator detail for this mode):
+//   - a session's footprint after one of its requests is the largest block
+//     count among its requests so far (contexts are append-only, Sec. 2.3);
+//   - resident sessions are kept in recency order of their latest request
+//     and evicted whole from the least recent end while the resident
+//     footprints exceed the capacity;
+//   - a block hits if the session that made its previous access is resident
+//     when the request arrives.
+// Footprints only grow and sessions only join the top of the list, so the
+// footprint held above a session only grows until its next request: q is
+// resident at request tau iff w(lq) + W(lq, tau) <= c, where lq is q's latest
+// request before tau, w the footprint after a request, and
+//     W(a, tau) = sum of w(i) over requests i in (a, tau) whose session's next
+//                 request is tau or later
+// (the latest footprint of every other session active since a).  The
+// distance of a block is w(lq) - 1 + W(lq, tau), a hit at c iff it is < c.
+#include "pc_internal.h"
+
+namespace pc {
+
+// largest r in [lo, hi] with blk_off[r] <= t
+__device__ __forceinline__ uint32_t sess_req_find(const uint64_t *__restrict__ blk_off, uint32_t lo, uint32_t hi,
+                                                  uint64_t t) {
+    while (lo < hi) {
+        const uint32_t mid = lo + (hi - lo + 1) / 2;
+        if (blk_off[mid] <= t) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+constexpr int PAGE_BITS = 12;   // the request table is paged by 4096 positions
+
+// req_page[p] = the request holding position p << PAGE_BITS; also checks the
+// layout (blk_off[0] = 0, non-decreasing, blk_off[n_seqs] = n).
+__global__ void sess_page_kernel(const uint64_t *__restrict__ blk_off, uint32_t n_seqs, uint64_t n,
+                                 uint32_t *__restrict__ req_page, int32_t *__restrict__ err) {
+    const uint64_t r = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r == 0 && (blk_off[0] != 0 || blk_off[n_seqs] != n)) atomicOr(err, DEV_ERR_BAD_LAYOUT);
+    if (r >= n_seqs) return;
+    const uint64_t a = blk_off[r], b = blk_off[r + 1];
+    if (a > b || b > n) {
+        atomicOr(err, DEV_ERR_BAD_LAYOUT);
+        return;
+    }
+    for (uint64_t pg = (a + (1u << PAGE_BITS) - 1) >> PAGE_BITS; (pg << PAGE_BITS) < b; ++pg)
+        req_page[pg] = (uint32_t)r;
+}
+
+// request-level keys for linking the requests of each session
+__global__ void sess_keys_kernel(const uint32_t *__restrict__ sess, uint32_t n_seqs, uint64_t *__restrict__ keys) {
+    const uint32_t r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r < n_seqs) keys[r] = sess[r];
+}
+
+// Footprint after every request: a running max of block counts along each
+// session's requests, walked from its first request (one lane per session).
+__global__ void sess_footprint_kernel(const uint32_t *__restrict__ prev_s, const uint32_t *__restrict__ next_s,
+                                      const uint64_t *__restrict__ blk_off, uint32_t n_seqs, uint64_t n,
+                                      uint32_t *__restrict__ w, int32_t *__restrict__ err) {
+    const uint32_t stride = gridDim.x * blockDim.x;
+    for (uint32_t r = blockIdx.x * blockDim.x + threadIdx.x; r < n_seqs; r += stride) {
+        if (prev_s[r] != NONE) continue;
+        uint64_t cur = 0;
+        uint32_t x = r;
+        for (;;) {
+            const uint64_t a = blk_off[x], b = blk_off[x + 1];
+            const uint64_t m = (a <= b && b <= n) ? b - a : 0;   // a bad layout is reported elsewhere
+            cur = m > cur ? m : cur;
+            w[x] = (uint32_t)cur;
+            const uint32_t y = next_s[x];
+            if (y == NONE) break;
+            if (y <= x || y >= n_seqs) {   // links run forward; anything else is not ours
+                atomicOr(err, DEV_ERR_BAD_LAYOUT);
+                break;
+            }
+            x = y;
+        }
+    }
+}
+
+// Distance of every access: one wave per request tau, 64 accesses per step.
+// Each access finds the request j of its previous use (page table, then a
+// short search), advances to lq, the latest request of j's session before tau,
+// and takes w(lq) - 1 + W(lq, tau).  W is summed by the whole wave over the
+// requests between lq and tau, once per distinct lq in the step (the last one
+// is kept across steps: a request's blocks mostly share one or two).
+__global__ __launch_bounds__(256) void sess_dist_kernel(const uint32_t *__restrict__ prev,
+                                                        const uint64_t *__restrict__ blk_off, uint32_t n_seqs,
+                                                        uint64_t n, const uint32_t *__restrict__ req_page,
+                                                        const uint32_t *__restrict__ next_s,
+                                                        const uint32_t *__restrict__ w,
+                                                        uint32_t *__restrict__ dist) {
+    const int lane = threadIdx.x & (WAVE - 1);
+    const uint32_t waves = gridDim.x * (blockDim.x / WAVE);
+    const uint32_t w0 = __builtin_amdgcn_readfirstlane(blockIdx.x * (blockDim.x / WAVE) + threadIdx.x / WAVE);
+    const uint64_t pages = (n + (1u << PAGE_BITS) - 1) >> PAGE_BITS;
+    for (uint32_t tau = w0; tau < n_seqs; tau += waves) {
+        const uint64_t s = blk_off[tau], e = blk_off[tau + 1];
+        if (s > e || e > n) continue;   // reported by the page kernel
+        uint32_t memo_a = NONE, memo_w = 0;
+        for (uint64_t base = s; base < e; base += WAVE) {
+            const uint64_t t = base + lane;
+            const uint32_t p = t < e ? prev[t] : NONE;
+            uint32_t lq = NONE;
+            if (p != NONE && (uint64_t)p < n) {
+                const uint64_t pg = (uint64_t)p >> PAGE_BITS;
+                uint32_t lo = req_page[pg];
+                uint32_t hi = pg + 1 < pages ? req_page[pg + 1] : n_seqs - 1;
+                lo = lo < n_seqs ? lo : n_seqs - 1;   // clamps keep bad layouts in bounds
+                hi = hi < n_seqs ? hi : n_seqs - 1;
+                hi = hi > lo ? hi : lo;
+                uint32_t x = sess_req_find(blk_off, lo, hi, p);
+                // a previous use lies in an earlier request; advance along the
+                // session while its next request is still before tau
+                if (x < tau) {
+                    for (uint32_t y = next_s[x]; y < tau && y > x; y = next_s[x]) x = y;
+                    lq = x;
+                }
+            }
+            uint32_t wv = 0;
+            bool need = lq != NONE;
+            if (need && lq == memo_a) {
+                wv = memo_w;
+                need = false;
+            }
+            for (uint64_t m = ballot(need); m != 0; m = ballot(need)) {
+                const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)lq, (int)__builtin_ctzll(m));
+                uint32_t sum = 0;
+                for (uint32_t i = a + 1 + lane; i < tau; i += WAVE) {
+                    const uint32_t y = next_s[i];
+                    sum += (y >= tau) ? w[i] : 0u;   // none (no next request) is above tau
+                }
+                const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(sum), WAVE - 1);
+                if (need && lq == a) {
+                    wv = tot;
+                    need = false;
+                }
+                memo_a = a;
+                memo_w = tot;
+            }
+            if (t < e) dist[t] = lq == NONE ? NONE : w[lq] - 1u + wv;
+        }
+    }
+}
+
+// fold a nested call's status word into the caller's
+__global__ void sess_status_kernel(int32_t *__restrict__ hdr, const int32_t *__restrict__ sub) {
+    if (threadIdx.x == 0 && sub[0] != 0) atomicOr(hdr, sub[0]);
+}
+
+struct SessWs {
+    int32_t *hdr;
+    uint64_t *skeys;
+    uint32_t *prev_s, *next_s, *w, *req_page;
+    void *pn_ws;
+    size_t pn_bytes;
+    size_t bytes;
+};
+
+static SessWs carve_sess(void *ws, uint64_t n, uint32_t n_seqs) {
+    Carver c{(char *)ws, 0};
+    SessWs s;
+    s.hdr = c.take<int32_t>(WS_HEADER / sizeof(int32_t));
+    s.skeys = c.take<uint64_t>(n_seqs);
+    s.prev_s = c.take<uint32_t>(n_seqs);
+    s.next_s = c.take<uint32_t>(n_seqs);
+    s.w = c.take<uint32_t>(n_seqs);
+    s.req_page = c.take<uint32_t>(((n + (1u << PAGE_BITS) - 1) >> PAGE_BITS) + 2);
+    s.pn_bytes = pc_prev_next_use_ws(n_seqs);
+    s.pn_ws = c.take<char>(s.pn_bytes);
+    s.bytes = c.off;
+    return s;
+}
+
+}  // namespace pc
+
+extern "C" {
+
+size_t pc_stack_distance_session_ws(uint64_t n, uint32_t n_seqs) { return pc::carve_sess(nullptr, n, n_seqs).bytes; }
+
+pc_status pc_stack_distance_session(const uint32_t *prev, const uint64_t *blk_off, const uint32_t *session,
+                                    uint32_t n_seqs, uint64_t n, uint32_t *dist_sess, void *ws, size_t ws_bytes,
+                                    void *stream) {
+    if (n >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
+    if (n_seqs >= 0x80000000u) return PC_ERR_TOO_LARGE;
+    if (n > 0 && (!prev || !blk_off || !session || !dist_sess || n_seqs == 0)) return PC_ERR_INVALID;
+    if (!ws) return PC_ERR_WORKSPACE;
+    if (ws_bytes < pc_stack_distance_session_ws(n, n_seqs)) return PC_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    pc::SessWs w = pc::carve_sess(ws, n, n_seqs);
+    pc_status st = pc::fill_u32(reinterpret_cast<uint32_t *>(w.hdr), 0u, 1, s);
+    if (st != PC_OK || n == 0) return st;
+    const uint64_t pages = (n + (1u << pc::PAGE_BITS) - 1) >> pc::PAGE_BITS;
+    if ((st = pc::fill_u32(w.req_page, 0u, pages + 1, s)) != PC_OK) return st;
+    const unsigned rgrid = (unsigned)(((uint64_t)n_seqs + 255) / 256);
+    PC_LAUNCH(pc::K_SESS_REQ, pc::sess_page_kernel, dim3(rgrid), dim3(256), 0, s, blk_off, n_seqs, n, w.req_page,
+              w.hdr);
+    // the requests of each session, linked like blocks of one key
+    PC_LAUNCH(pc::K_SESS_REQ, pc::sess_keys_kernel, dim3(rgrid), dim3(256), 0, s, session, n_seqs, w.skeys);
+    if ((st = pc_prev_next_use(w.skeys, n_seqs, w.prev_s, w.next_s, w.pn_ws, w.pn_bytes, stream)) != PC_OK)
+        return st;
+    PC_LAUNCH(pc::K_SESS_REQ, pc::sess_status_kernel, dim3(1), dim3(64), 0, s, w.hdr,
+              reinterpret_cast<const int32_t *>(w.pn_ws));
+    const int cus = pc::device_cus();
+    unsigned fgrid = rgrid < (unsigned)cus * 4 ? rgrid : (unsigned)cus * 4;
+    PC_LAUNCH(pc::K_SESS_REQ, pc::sess_footprint_kernel, dim3(fgrid), dim3(256), 0, s, w.prev_s, w.next_s, blk_off,
+              n_seqs, n, w.w, w.hdr);
+    uint64_t grid = ((uint64_t)n_seqs + 3) / 4;
+    if (grid > (uint64_t)cus * 16) grid = (uint64_t)cus * 16;
+    PC_LAUNCH(pc::K_SESS_DIST, pc::sess_dist_kernel, dim3((unsigned)grid), dim3(256), 0, s, prev, blk_off, n_seqs, n,
+              w.req_page, w.next_s, w.w, dist_sess);
+    return PC_OK;
+}
+
+}  // extern "C"

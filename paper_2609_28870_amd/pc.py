@@ -67,6 +67,10 @@ def lib():
     L.pc_stack_distance_req_ws.argtypes = []
     L.pc_stack_distance_req.restype = _st
     L.pc_stack_distance_req.argtypes = [_vp, _vp, _vp, _u32, _u64, _vp, _vp, _sz, _vp]
+    L.pc_stack_distance_session_ws.restype = _sz
+    L.pc_stack_distance_session_ws.argtypes = [_u64, _u32]
+    L.pc_stack_distance_session.restype = _st
+    L.pc_stack_distance_session.argtypes = [_vp, _vp, _vp, _u32, _u64, _vp, _vp, _sz, _vp]
     L.pc_mrc_weighted_ws.restype = _sz
     L.pc_mrc_weighted_ws.argtypes = [_u64, _u32]
     L.pc_mrc_weighted.restype = _st
@@ -235,6 +239,24 @@ def stack_distance_req(prev: torch.Tensor, dist: torch.Tensor, blk_off: torch.Te
     return dist_req, ws
 
 
+def stack_distance_session(prev: torch.Tensor, blk_off: torch.Tensor, session: torch.Tensor,
+                           dist_sess: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
+    """pc_stack_distance_session: session-level distances from prev (request
+    order), the request table and the session of every request."""
+    L = lib()
+    n = prev.numel()
+    n_seqs = blk_off.numel() - 1
+    if session.numel() != n_seqs:
+        raise PcError("one session id per request expected")
+    if dist_sess is None:
+        dist_sess = torch.empty(n, dtype=torch.int32, device=_dev())
+    if ws is None:
+        ws = workspace(L.pc_stack_distance_session_ws(n, n_seqs))
+    check(L.pc_stack_distance_session(_ptr(prev), _ptr(blk_off), _ptr(session), n_seqs, n, _ptr(dist_sess),
+                                      _ptr(ws), ws.numel(), _stream()))
+    return dist_sess, ws
+
+
 def mrc_weighted(dist: torch.Tensor, caps: torch.Tensor, depth: Optional[torch.Tensor] = None,
                  nxt: Optional[torch.Tensor] = None, alpha: int = 1, beta: int = 0,
                  out: Optional[dict] = None, ws: Optional[torch.Tensor] = None):
@@ -308,6 +330,9 @@ class Pipeline:
     once; ``run()`` enqueues hash -> prev/next -> stack distance -> bins.
 
     ``residency="access"`` bins the per-access LRU stack distance.
+    ``residency="session"`` (whole sessions evicted at once, Sec. 5.3) bins
+    the session-level distance instead; it needs ``session``, the session of
+    every request, and takes no next-use histogram.
     ``residency="request"`` (every block of a request resident at once,
     Sec. 3.1) first puts each request's accesses in recency order (deepest
     block first), runs prev/next and the stack distance on that order, turns
@@ -317,9 +342,11 @@ class Pipeline:
 
     def __init__(self, tokens, tok_start, tok_len, blk_off, n_blocks: int, caps,
                  block_size: int = 16, alpha: int = 1, beta: int = 0, with_nextuse: bool = True,
-                 residency: str = "access"):
-        if residency not in ("access", "request"):
-            raise PcError("residency must be 'access' or 'request'")
+                 residency: str = "access", session: Optional[torch.Tensor] = None):
+        if residency not in ("access", "request", "session"):
+            raise PcError("residency must be 'access', 'request' or 'session'")
+        if residency == "session" and session is None:
+            raise PcError("session-level residency needs the session of every request")
         L = lib()
         dev = _dev()
         self.tokens, self.tok_start, self.tok_len, self.blk_off = tokens, tok_start, tok_len, blk_off
@@ -329,7 +356,8 @@ class Pipeline:
         self.alpha, self.beta = alpha, beta
         self.residency = residency
         self.request = residency == "request"
-        self.with_nextuse = with_nextuse and not self.request
+        self.session = session
+        self.with_nextuse = with_nextuse and residency == "access"
         n = self.n
         self.keys = torch.empty(n, dtype=torch.int64, device=dev)
         self.depth = torch.empty(n, dtype=torch.int32, device=dev)
@@ -341,7 +369,10 @@ class Pipeline:
                      for name in ("count", "depthsum", "cost_lo", "cost_hi", "nextuse")}
         self.ws_hash = workspace(L.pc_hash_blocks_ws(tok_len.numel()))
         self.ws_pn = workspace(L.pc_prev_next_use_ws(n))
-        self.ws_sd = workspace(L.pc_stack_distance_ws(n))
+        if residency == "session":
+            self.ws_sd = workspace(L.pc_stack_distance_session_ws(n, tok_len.numel()))
+        else:
+            self.ws_sd = workspace(L.pc_stack_distance_ws(n))
         if self.request:
             self.keys_r = torch.empty(n, dtype=torch.int64, device=dev)
             self.depth_r = torch.empty(n, dtype=torch.int32, device=dev)
@@ -353,6 +384,12 @@ class Pipeline:
     def run(self):
         hash_blocks(self.tokens, self.tok_start, self.tok_len, self.blk_off, self.n, self.B,
                     keys=self.keys, depth=self.depth, ws=self.ws_hash)
+        if self.residency == "session":
+            prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn)
+            stack_distance_session(self.prev, self.blk_off, self.session, dist_sess=self.dist, ws=self.ws_sd)
+            mrc_weighted(self.dist, self.caps, self.depth, None, self.alpha, self.beta, out=self.bins,
+                         ws=self.ws_mrc)
+            return
         if not self.request:
             prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn)
             stack_distance(self.prev, self.next, self.dist, ws=self.ws_sd)
@@ -388,4 +425,5 @@ def upload_trace(trace, block_size: Optional[int] = None):
     dev = _dev()
     return dict(tokens=torch.from_numpy(trace.tokens).to(dev),
                 tok_start=to_dev_u64(trace.tok_start), tok_len=to_dev_u32(trace.tok_len),
-                blk_off=to_dev_u64(off), n_blocks=int(off[-1]), block_size=B)
+                blk_off=to_dev_u64(off), n_blocks=int(off[-1]), block_size=B,
+                session=to_dev_u32(trace.session.astype(np.uint32)))

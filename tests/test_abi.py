@@ -113,6 +113,24 @@ def test_stack_distance_req_rejects_bad_arguments(L):
     assert call(wsz=ws - 1) == -3
 
 
+def test_stack_distance_session_rejects_bad_arguments(L):
+    n = 5000
+    ws = L.pc_stack_distance_session_ws(n, 40)
+    assert ws >= L.pc_prev_next_use_ws(40)
+    assert L.pc_stack_distance_session_ws(10 ** 8, 40) > ws
+    call = lambda prev=FAKE, bo=FAKE, sess=FAKE, ns=40, n=n, out=FAKE, w=FAKE, wsz=ws: \
+        L.pc_stack_distance_session(prev, bo, sess, ns, n, out, w, wsz, None)
+    assert call(n=0xFFFFFFFF) == -2
+    assert call(ns=0x80000000) == -2
+    assert call(prev=None) == -1
+    assert call(bo=None) == -1
+    assert call(sess=None) == -1
+    assert call(out=None) == -1
+    assert call(ns=0) == -1
+    assert call(w=None) == -3
+    assert call(wsz=ws - 1) == -3
+
+
 def test_mrc_rejects_bad_arguments(L):
     ws = L.pc_mrc_weighted_ws(10, 4)
     ok = lambda **kw: dict(dict(dist=FAKE, depth=None, nxt=None, n=10, caps=FAKE, k=4, a=1, b=0,
@@ -139,5 +157,5 @@ def test_profiling_table(L):
     names = [L.pc_prof_kernel_name(i).decode() for i in range(n)]
     assert "hash_chain" in names and "sd_dominance_pass" in names and "mrc_hist" in names
     assert all(names) and len(set(names)) == n
-    assert names[-1] == "request_distance"
+    assert names[-1] == "session_distance"
     assert pc.prof_read() is not None
