@@ -82,12 +82,17 @@ __global__ void sess_footprint_kernel(const uint32_t *__restrict__ prev_s, const
     }
 }
 
-// Distance of every access: one wave per request tau, 64 accesses per step.
-// Each access finds the request j of its previous use (page table, then a
-// short search), advances to lq, the latest request of j's session before tau,
-// and takes w(lq) - 1 + W(lq, tau).  W is summed by the whole wave over the
-// requests between lq and tau, once per distinct lq in the step (the last one
-// is kept across steps: a request's blocks mostly share one or two).
+// Distance of every access: one wave per request tau, SESS_ITEMS accesses per
+// lane and step (64 apart, so loads and stores stay coalesced).  Each access
+// finds the request j of its
+// previous use (page table, then a short search; a lane keeps the last j it
+// found, since consecutive blocks of a request were mostly last used by the
+// same request), advances to lq, the latest request of j's session before
+// tau, and takes w(lq) - 1 + W(lq, tau).  W is summed by the whole wave over
+// the requests between lq and tau, once per distinct lq (the last one is kept
+// across steps: a request's blocks mostly share one or two).
+constexpr int SESS_ITEMS = 8;
+
 __global__ __launch_bounds__(256) void sess_dist_kernel(const uint32_t *__restrict__ prev,
                                                         const uint64_t *__restrict__ blk_off, uint32_t n_seqs,
                                                         uint64_t n, const uint32_t *__restrict__ req_page,
@@ -102,47 +107,66 @@ __global__ __launch_bounds__(256) void sess_dist_kernel(const uint32_t *__restri
         const uint64_t s = blk_off[tau], e = blk_off[tau + 1];
         if (s > e || e > n) continue;   // reported by the page kernel
         uint32_t memo_a = NONE, memo_w = 0;
-        for (uint64_t base = s; base < e; base += WAVE) {
-            const uint64_t t = base + lane;
-            const uint32_t p = t < e ? prev[t] : NONE;
-            uint32_t lq = NONE;
-            if (p != NONE && (uint64_t)p < n) {
-                const uint64_t pg = (uint64_t)p >> PAGE_BITS;
-                uint32_t lo = req_page[pg];
-                uint32_t hi = pg + 1 < pages ? req_page[pg + 1] : n_seqs - 1;
-                lo = lo < n_seqs ? lo : n_seqs - 1;   // clamps keep bad layouts in bounds
-                hi = hi < n_seqs ? hi : n_seqs - 1;
-                hi = hi > lo ? hi : lo;
-                uint32_t x = sess_req_find(blk_off, lo, hi, p);
-                // a previous use lies in an earlier request; advance along the
-                // session while its next request is still before tau
-                if (x < tau) {
-                    for (uint32_t y = next_s[x]; y < tau && y > x; y = next_s[x]) x = y;
-                    lq = x;
+        // the lane's last source request: positions [src_lo, src_hi) -> lq, w(lq)
+        uint64_t src_lo = 1, src_hi = 0;
+        uint32_t src_lq = NONE, src_w = 0;
+        for (uint64_t base = s; base < e; base += SESS_ITEMS * WAVE) {
+            const uint64_t t0 = base + lane;
+            uint32_t p[SESS_ITEMS], lq[SESS_ITEMS], wl[SESS_ITEMS];
+#pragma unroll
+            for (int k = 0; k < SESS_ITEMS; ++k) p[k] = t0 + k * WAVE < e ? prev[t0 + k * WAVE] : NONE;
+#pragma unroll
+            for (int k = 0; k < SESS_ITEMS; ++k) {
+                lq[k] = NONE;
+                wl[k] = 0;
+                if (p[k] == NONE || (uint64_t)p[k] >= n) continue;
+                if ((uint64_t)p[k] < src_lo || (uint64_t)p[k] >= src_hi) {
+                    const uint64_t pg = (uint64_t)p[k] >> PAGE_BITS;
+                    uint32_t lo = req_page[pg];
+                    uint32_t hi = pg + 1 < pages ? req_page[pg + 1] : n_seqs - 1;
+                    lo = lo < n_seqs ? lo : n_seqs - 1;   // clamps keep bad layouts in bounds
+                    hi = hi < n_seqs ? hi : n_seqs - 1;
+                    hi = hi > lo ? hi : lo;
+                    uint32_t x = sess_req_find(blk_off, lo, hi, p[k]);
+                    src_lo = blk_off[x];
+                    src_hi = blk_off[x + 1];
+                    src_lq = NONE;
+                    // a previous use lies in an earlier request; advance along
+                    // the session while its next request is still before tau
+                    if (x < tau) {
+                        for (uint32_t y = next_s[x]; y < tau && y > x; y = next_s[x]) x = y;
+                        src_lq = x;
+                        src_w = w[x];
+                    }
                 }
+                lq[k] = src_lq;
+                wl[k] = src_w;
             }
-            uint32_t wv = 0;
-            bool need = lq != NONE;
-            if (need && lq == memo_a) {
-                wv = memo_w;
-                need = false;
-            }
-            for (uint64_t m = ballot(need); m != 0; m = ballot(need)) {
-                const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)lq, (int)__builtin_ctzll(m));
-                uint32_t sum = 0;
-                for (uint32_t i = a + 1 + lane; i < tau; i += WAVE) {
-                    const uint32_t y = next_s[i];
-                    sum += (y >= tau) ? w[i] : 0u;   // none (no next request) is above tau
-                }
-                const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(sum), WAVE - 1);
-                if (need && lq == a) {
-                    wv = tot;
+#pragma unroll
+            for (int k = 0; k < SESS_ITEMS; ++k) {
+                uint32_t wv = 0;
+                bool need = lq[k] != NONE;
+                if (need && lq[k] == memo_a) {
+                    wv = memo_w;
                     need = false;
                 }
-                memo_a = a;
-                memo_w = tot;
+                for (uint64_t m = ballot(need); m != 0; m = ballot(need)) {
+                    const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)lq[k], (int)__builtin_ctzll(m));
+                    uint32_t sum = 0;
+                    for (uint32_t i = a + 1 + lane; i < tau; i += WAVE) {
+                        const uint32_t y = next_s[i];
+                        sum += (y >= tau) ? w[i] : 0u;   // none (no next request) is above tau
+                    }
+                    const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(sum), WAVE - 1);
+                    if (need && lq[k] == a) {
+                        wv = tot;
+                        need = false;
+                    }
+                    memo_a = a;
+                    memo_w = tot;
+                }
+                if (t0 + k * WAVE < e) dist[t0 + k * WAVE] = lq[k] == NONE ? NONE : wl[k] - 1u + wv;
             }
-            if (t < e) dist[t] = lq == NONE ? NONE : w[lq] - 1u + wv;
         }
     }
 }
