@@ -436,3 +436,114 @@ def mrc_bins_session(keys, blk_off, sess, caps, depth=None, alpha=1, beta=0, ids
     dsum.append(int(np.asarray(depth, np.uint64).sum(dtype=np.uint64)) - pd)
     cost = [alpha * c + beta * d for c, d in zip(count, dsum)]
     return count, dsum, cost
+
+
+# ------------------------------------------------------------- f4 profiles
+# Workload characterisation (Sec. 4): reuse intervals in time (Sec. 4.2),
+# block lifetimes (Sec. 4.1), access frequency and the chance of a further
+# reuse after k accesses (Sec. 4.3), per-session footprints, turns, duration
+# and inter-request gaps (Sec. 4.5, Sec. 4.1, Sec. 2.3).  Times are request
+# timestamps in microseconds; a block's accesses take their request's time.
+# Histograms use the capacity-bin convention: bin k < K holds values in
+# [edges[k-1], edges[k]) (edges[-1] = 0), bin K holds values >= edges[K-1].
+
+def _bins(x, edges):
+    return np.searchsorted(np.asarray(edges, np.uint64), np.asarray(x, np.uint64), side="right")
+
+
+def _hist(x, edges):
+    return [int(v) for v in np.bincount(_bins(x, edges), minlength=len(edges) + 1)]
+
+
+def access_times(blk_off, ts_us):
+    """Timestamp of every access: its request's."""
+    bo = np.asarray(blk_off, np.int64)
+    return np.repeat(np.asarray(ts_us, np.uint64), np.diff(bo))
+
+
+def reuse_profile(keys, blk_off, ts_us, edges, freq_max):
+    """Per-block and per-reuse statistics of an access stream.
+
+    interval: histogram over reuses t (prev(t) exists) of ts(t) - ts(prev t);
+    lifetime: histogram over blocks of ts(last access) - ts(first access);
+    freq: blocks by number of accesses f, bin min(f, freq_max) (bin 0 empty);
+    life_by_class: lifetime histogram per frequency class floor(log2 f)
+    (32 classes, flattened class-major)."""
+    keys = _c(keys, np.uint64)
+    ids, n_ids = key_ids(keys)
+    prev, _ = prev_next(keys, (ids, n_ids))
+    ts = access_times(blk_off, ts_us)
+    has = prev != NONE
+    interval = ts[has] - ts[prev[has]]
+    order = np.arange(keys.size)
+    first = np.full(n_ids, keys.size, np.int64)
+    np.minimum.at(first, ids, order)
+    last = np.full(n_ids, -1, np.int64)
+    np.maximum.at(last, ids, order)
+    count = np.bincount(ids, minlength=n_ids)
+    life = ts[last] - ts[first]
+    cls = np.floor(np.log2(count)).astype(np.int64)
+    k = len(edges) + 1
+    lb = np.zeros(32 * k, np.int64)
+    np.add.at(lb, cls * k + _bins(life, edges), 1)
+    return {"interval": _hist(interval, edges), "lifetime": _hist(life, edges),
+            "freq": [int(v) for v in np.bincount(np.minimum(count, freq_max), minlength=freq_max + 1)],
+            "life_by_class": [int(v) for v in lb]}
+
+
+def reuse_probability(freq):
+    """P(a block is accessed again | it has been accessed k times) for
+    k = 1 .. len(freq) - 2, from the frequency histogram (exact below the
+    tail bin): blocks with f >= k+1 over blocks with f >= k."""
+    f = np.asarray(freq, np.int64)
+    at_least = np.cumsum(f[::-1])[::-1]          # blocks with f >= k (tail bin counts as >= F)
+    return [float(at_least[k + 1]) / float(at_least[k]) if at_least[k] else 0.0 for k in range(1, f.size - 1)]
+
+
+def session_profile(blk_off, sess, ts_us, edges, fp_max, rq_max):
+    """Per-session statistics from the request table.
+
+    footprint: sessions by footprint, the largest request's block count
+    (append-only contexts), bin min(fp, fp_max); requests: sessions by
+    number of requests, bin min(count, rq_max); duration: histogram of
+    ts(last request) - ts(first request); gap: histogram over requests with
+    an earlier request of the same session of the time since that one."""
+    bo = np.asarray(blk_off, np.int64)
+    m = np.diff(bo)
+    sess = np.asarray(sess, np.int64)
+    ts = np.asarray(ts_us, np.uint64)
+    fp, cnt, t0, t1, last = {}, {}, {}, {}, {}
+    gaps = []
+    for r in range(sess.size):
+        s = int(sess[r])
+        fp[s] = max(fp.get(s, 0), int(m[r]))
+        cnt[s] = cnt.get(s, 0) + 1
+        t0.setdefault(s, int(ts[r]))
+        t1[s] = int(ts[r])
+        if s in last:
+            gaps.append(int(ts[r]) - last[s])
+        last[s] = int(ts[r])
+    ss = sorted(fp)
+    return {"footprint": [int(v) for v in np.bincount(np.minimum([fp[s] for s in ss], fp_max),
+                                                      minlength=fp_max + 1)],
+            "requests": [int(v) for v in np.bincount(np.minimum([cnt[s] for s in ss], rq_max),
+                                                     minlength=rq_max + 1)],
+            "duration": _hist([t1[s] - t0[s] for s in ss], edges),
+            "gap": _hist(gaps, edges)}
+
+
+def lorenz_top_share(footprint_hist, frac):
+    """Share of all footprint blocks held by the largest ceil(frac * S)
+    sessions, from an exact footprint histogram (no tail sessions)."""
+    h = np.asarray(footprint_hist, np.int64)
+    total_s = int(h.sum())
+    total_b = int((h * np.arange(h.size)).sum())
+    want = int(np.ceil(frac * total_s))
+    got_s = got_b = 0
+    for v in range(h.size - 1, -1, -1):
+        take = min(int(h[v]), want - got_s)
+        got_s += take
+        got_b += take * v
+        if got_s == want:
+            break
+    return got_b / total_b if total_b else 0.0

@@ -67,3 +67,17 @@ def session_golden():
         want = [NONE if v == "-" else int(v) for v in row[bars[0] + 1:bars[1]]]
         hits = {int(c): int(h) for c, h in (x.split(":") for x in row[bars[1] + 1:])}
         yield row[0], keys, blk_off, np.array(sess, np.uint32), want, hits
+
+
+def characterization_golden():
+    """The hand-worked characterisation fixture: the trace (keys, blk_off,
+    session, ts_us) and a dict of expected rows."""
+    rows = read_golden("characterization_example.txt")
+    reqs = [r for r in rows if r[0] == "request"]
+    want = {r[0]: [int(x) for x in r[1:]] for r in rows if r[0] != "request"}
+    snames = {}
+    sess = np.array([snames.setdefault(r[1], len(snames)) for r in reqs], np.uint32)
+    ts = np.array([int(r[2]) for r in reqs], np.uint64)
+    keys = np.array([int(x) for r in reqs for x in r[3:]], np.uint64)
+    blk_off = np.concatenate([[0], np.cumsum([len(r) - 3 for r in reqs])]).astype(np.uint64)
+    return keys, blk_off, sess, ts, want

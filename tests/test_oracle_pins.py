@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 import oracle
-from conftest import read_golden, request_golden, session_golden
+from conftest import characterization_golden, read_golden, request_golden, session_golden
 
 NONE = oracle.NONE
 G = 0x9E3779B97F4A7C15
@@ -474,3 +474,70 @@ def test_session_level_everything_fits():
         p, _ = oracle.prev_next(keys)
         (h, _), = oracle.lru_session(keys, blk_off, sess, [int(keys.size) + 1])
         assert h == int((p != NONE).sum())
+
+
+# ------------------------------------------------------- characterisation
+
+def test_characterization_hand_worked_example():
+    keys, blk_off, sess, ts, want = characterization_golden()
+    edges = want["edges"]
+    rp = oracle.reuse_profile(keys, blk_off, ts, edges, want["freq_max"][0])
+    assert rp["interval"] == want["interval"]
+    assert rp["lifetime"] == want["lifetime"]
+    assert rp["freq"] == want["freq"]
+    k = len(edges) + 1
+    assert rp["life_by_class"][:k] == want["class0"] and rp["life_by_class"][k:2 * k] == want["class1"]
+    assert not any(rp["life_by_class"][2 * k:])
+    sp = oracle.session_profile(blk_off, sess, ts, edges, want["footprint_max"][0], want["requests_max"][0])
+    for name in ("footprint", "requests", "duration", "gap"):
+        assert sp[name] == want[name], name
+
+
+def _timed_sessions(seed):
+    for keys, blk_off, sess in random_sessions(30, seed):
+        rng = np.random.default_rng(seed)
+        ts = np.cumsum(rng.integers(0, 50, size=sess.size)).astype(np.uint64)
+        yield keys, blk_off, sess, ts
+
+
+def test_characterization_invariants_and_brute_force():
+    edges = [1, 3, 10, 30, 100, 300]
+    for keys, blk_off, sess, ts in _timed_sessions(51):
+        n = keys.size
+        rp = oracle.reuse_profile(keys, blk_off, ts, edges, 1000)
+        at = oracle.access_times(blk_off, ts)
+        # brute force per block: its accesses in order
+        acc = {}
+        for t, k in enumerate(keys.tolist()):
+            acc.setdefault(k, []).append(t)
+        assert sum(rp["freq"]) == len(acc)
+        assert sum(f * c for f, c in enumerate(rp["freq"])) == n
+        assert sum(rp["interval"]) == n - len(acc)
+        ivals = [int(at[b]) - int(at[a]) for ts_ in acc.values() for a, b in zip(ts_, ts_[1:])]
+        assert rp["interval"] == [int(v) for v in np.bincount(np.searchsorted(edges, ivals, side="right"),
+                                                             minlength=len(edges) + 1)]
+        lives = [int(at[v[-1]]) - int(at[v[0]]) for v in acc.values()]
+        assert rp["lifetime"] == [int(v) for v in np.bincount(np.searchsorted(edges, lives, side="right"),
+                                                             minlength=len(edges) + 1)]
+        # further-reuse probability after k accesses, counted access by access
+        p = oracle.reuse_probability(rp["freq"])
+        for k in range(1, 6):
+            kth = [len(v) > k for v in acc.values() if len(v) >= k]
+            if kth:
+                assert p[k - 1] == sum(kth) / len(kth)
+        sp = oracle.session_profile(blk_off, sess, ts, edges, 1000, 1000)
+        # append-only sessions: the footprint is the number of distinct blocks
+        bo = blk_off.astype(np.int64)
+        held = {}
+        for r, s in enumerate(sess.tolist()):
+            held.setdefault(s, set()).update(keys[bo[r]:bo[r + 1]].tolist())
+        assert sp["footprint"] == [int(v) for v in np.bincount([len(h) for h in held.values()], minlength=1001)]
+        assert sum(sp["gap"]) == sess.size - len(held)
+
+
+def test_lorenz_top_share_closed_forms():
+    # one session with 10 blocks and nine with 1: the top 10% hold 10/19
+    h = [0, 9] + [0] * 8 + [1]
+    assert oracle.lorenz_top_share(h, 0.1) == 10 / 19
+    assert oracle.lorenz_top_share(h, 1.0) == 1.0
+    assert oracle.lorenz_top_share([0, 0, 0, 5], 0.4) == 0.4   # equal footprints: share = fraction
