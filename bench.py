@@ -12,6 +12,7 @@ of the dominant kernel and the CPU oracle timed on a bounded sample.
 """
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -38,6 +39,9 @@ ALGO_BYTES = {
     "mrc_hist": lambda B: 12,                     # dist, depth, next in
     "request_order": lambda B: 12 + 12,           # key, depth in; reversed copies out
     "request_distance": lambda B: 4 + 4 + 4,      # prev, per-access dist in; dist_req out
+    "session_distance": lambda B: 4 + 4,          # prev in; dist_sess out
+    "reuse_profile_pack": lambda B: 4 + 8,        # next in; (next, request) out
+    "reuse_profile_walk": lambda B: 4 + 8,        # prev (chain starts) and one (next, request) per step in
 }
 
 
@@ -106,6 +110,58 @@ def measured_traffic(kernel_id):
             "profiled_avg_ms": entry["avg_ms"], "source": os.path.relpath(PROFILE, ROOT)}
 
 
+# time edges of the characterisation histograms (microseconds): 1-2-5 steps
+# from 1 us to 1e11 us (~28 hours)
+PROFILE_EDGES_US = sorted(m * 10 ** e for e in range(0, 11) for m in (1, 2, 5)) + [10 ** 11]
+
+
+def _quantile(hist, edges, q):
+    """Upper edge of the bin holding the q-quantile of a histogram."""
+    total = sum(hist)
+    if total == 0:
+        return None
+    run = 0
+    for k, c in enumerate(hist):
+        run += c
+        if run >= q * total:
+            return edges[k] if k < len(edges) else float("inf")
+    return float("inf")
+
+
+def profile_summary(rp, sp):
+    """A few headline figures from the characterisation histograms (host
+    arithmetic on exact integer bins)."""
+    e = PROFILE_EDGES_US
+    f = rp["freq"]
+    at_least = [sum(f[k:]) for k in range(len(f))]
+    fp = sp["footprint"]
+    n_sess = sum(fp)
+    blocks = sum(v * c for v, c in enumerate(fp))
+
+    def top_share(frac):
+        want = math.ceil(frac * n_sess - 1e-9)   # the largest ceil(frac * sessions) sessions
+        got_s = got_b = 0
+        for v in range(len(fp) - 1, -1, -1):
+            take = min(fp[v], want - got_s)
+            got_s += take
+            got_b += take * v
+            if got_s >= want:
+                break
+        return round(got_b / blocks, 4) if blocks else None
+
+    return {"reuse_interval_us_p50_upper": _quantile(rp["interval"], e, 0.5),
+            "reuse_interval_us_p99_upper": _quantile(rp["interval"], e, 0.99),
+            "lifetime_us_p50_upper": _quantile(rp["lifetime"], e, 0.5),
+            "one_access_blocks": round(f[1] / at_least[1], 4) if at_least[1] else None,
+            "p_reuse_after_1": round(at_least[2] / at_least[1], 4) if at_least[1] else None,
+            "p_reuse_after_2": round(at_least[3] / at_least[2], 4) if at_least[2] else None,
+            "sessions": n_sess,
+            "footprint_top10pct_share": top_share(0.1),
+            "footprint_top1pct_share": top_share(0.01),
+            "session_duration_us_p50_upper": _quantile(sp["duration"], e, 0.5),
+            "intra_session_gap_us_p50_upper": _quantile(sp["gap"], e, 0.5)}
+
+
 def cpu_baseline(trace, caps, alpha, beta, budget_accesses, request=False):
     """The oracle (plain C, one thread) over the first requests of the same
     trace: hash, prev/next, next-use histogram and one LRU simulation per
@@ -121,7 +177,13 @@ def cpu_baseline(trace, caps, alpha, beta, budget_accesses, request=False):
     t0 = time.perf_counter()
     keys, depth = oracle.hash_trace(sub)
     ids = oracle.key_ids(keys)
-    if request == "session":
+    if request == "profile":
+        bo = sub.blk_off()
+        ts = sub.ts_us.astype(np.uint64)
+        oracle.reuse_profile(keys, bo, ts, PROFILE_EDGES_US, 2048)
+        oracle.session_profile(bo, sub.session, ts, PROFILE_EDGES_US, 1 << 16, 2048)
+        what = "reuse and session profiles"
+    elif request == "session":
         oracle.mrc_bins_session(keys, sub.blk_off(), sub.session.astype(np.uint32), caps, depth, alpha, beta, ids)
         what = "prev/next + session-level bins (%d per-capacity session LRU simulations)" % len(caps)
     elif request:
@@ -149,6 +211,9 @@ def main():
     ap.add_argument("--residency", default="access", choices=["access", "request", "session"],
                     help="per-access LRU (default), request-level residency (whole request pinned) "
                          "or session-level eviction (whole sessions evicted)")
+    ap.add_argument("--profile", action="store_true",
+                    help="time the workload characterisation instead (hash, prev/next, reuse and session "
+                         "profiles)")
     ap.add_argument("--cpu-sample", type=int, default=None,
                     help="block accesses in the oracle's timed sample (0 = skip; default 1e8, "
                          "1e6 with --residency request)")
@@ -180,8 +245,13 @@ def main():
     session_mode = args.residency == "session"
     global PROFILE
     PROFILE = PROFILES[args.residency]
-    pipe = pc.Pipeline(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
-                       caps, B, alpha, beta, residency=args.residency, session=up["session"])
+    if args.profile:
+        prof_edges = pc.to_dev_u64(np.array(PROFILE_EDGES_US, np.uint64))
+        pipe = pc.Profiler(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
+                           up["session"], up["ts_us"], prof_edges, B)
+    else:
+        pipe = pc.Pipeline(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
+                           caps, B, alpha, beta, residency=args.residency, session=up["session"])
     torch.cuda.synchronize()
     log("inputs resident in HBM; device memory in use %.1f GB" % (torch.cuda.memory_allocated() / 1e9))
 
@@ -220,7 +290,7 @@ def main():
     value = n_blocks / (ms_step / 1e3)
     # the four high-key sort passes exit at once unless the first link
     # asked for them; count only passes that moved data
-    high = pipe.high_key_passes_ran()
+    high = pipe.high_key_passes_ran() if not args.profile else pc.high_key_passes_ran(pipe.ws_pn)
     work_launches = {"sort_onesweep_pass": 8 if high else 4, "link_partition": 2 if high else 1,
                      "sort_digit_hist": 2 if high else 1}
     kernels = {}
@@ -253,10 +323,13 @@ def main():
                 "link_partition": "prev_next",
                 "perm_partition": "prev_next", "perm_local": "prev_next", "mrc_hist": "mrc",
                 "mrc_cost": "mrc", "request_order": "request_order", "request_distance": "request_distance",
-                "session_requests": "session_distance", "session_distance": "session_distance"}
+                "session_requests": "session_profile" if args.profile else "session_distance",
+                "session_distance": "session_distance",
+                "reuse_profile_pack": "reuse_profile", "reuse_profile_walk": "reuse_profile",
+                "session_profile": "session_profile"}
     stage_bytes = {"hash": 4 * B + 8 + 4, "prev_next": 16, "stack_distance": 8,
                    "mrc": 8 if request or session_mode else 12, "request_order": 24, "request_distance": 12,
-                   "session_distance": 8}
+                   "session_distance": 8, "reuse_profile": 24}
 
     def stage_name(kid):
         return stage_of.get(kid, "stack_distance" if kid.startswith("sd_") else "other")
@@ -272,16 +345,21 @@ def main():
                   "measured_GBps": round(measured[k] / v / 1e6, 1) if measured and k in measured else None}
               for k, v in stages.items()}
 
-    # the curves themselves (exact integers -> float64 ratios)
-    bins = pc.bins_to_host(pipe.bins)
-    hr, csr = pc.curves(bins["count"], bins["cost"])
     # request-level bins hold only at capacities that fit the largest request
     min_cap = int((trace.tok_len // np.uint32(B)).max()) if request else 0
+    summary = None
+    if args.profile:
+        summary = profile_summary(pc.hists_to_host(pipe.reuse), pc.hists_to_host(pipe.sessions))
+    else:
+        # the curves themselves (exact integers -> float64 ratios)
+        bins = pc.bins_to_host(pipe.bins)
+        hr, csr = pc.curves(bins["count"], bins["cost"])
     cb = None
     sample = args.cpu_sample if args.cpu_sample is not None else (1_000_000 if request else 100_000_000)
     if sample > 0:
         log("timing the CPU oracle on a %d-access sample" % sample)
-        cb = cpu_baseline(trace, caps_np, alpha, beta, sample, "session" if session_mode else request)
+        kind = "profile" if args.profile else "session" if session_mode else request
+        cb = cpu_baseline(trace, caps_np, alpha, beta, sample, kind)
 
     out = {
         "metric": "KV-block accesses/sec for hash+stack-distance+MRC; achieved HBM GB/s",
@@ -316,9 +394,16 @@ def main():
         "kernels": kernels,
         "stages": stages,
         "high_key_sort_passes": high,
-        "curves_at": {str(int(c)): [round(h, 6), round(s, 6)] if int(c) >= min_cap else None
-                      for c, h, s in zip(caps_np, hr, csr) if int(c) in pcgen.GIB_BLOCKS.values()},
     }
+    if args.profile:
+        out["metric"] = "KV-block accesses/sec for hash+prev/next+workload characterisation; achieved HBM GB/s"
+        out["residency"] = None
+        out["config"]["residency"] = None
+        out["config"]["analysis"] = "reuse intervals, lifetimes, frequencies, session footprints (Sec. 4)"
+        out["characterisation"] = summary
+    else:
+        out["curves_at"] = {str(int(c)): [round(h, 6), round(s, 6)] if int(c) >= min_cap else None
+                            for c, h, s in zip(caps_np, hr, csr) if int(c) in pcgen.GIB_BLOCKS.values()}
     print(json.dumps(out), flush=True)
 
 

@@ -44,6 +44,10 @@ typedef enum {
 
 #define PC_NONE 0xFFFFFFFFu
 #define PC_MAX_CAPS 1024u
+#define PC_MAX_PROFILE_EDGES 128u  /* time-histogram edges of the profiles */
+#define PC_MAX_FREQ 2048u          /* largest exact frequency / request-count bin */
+#define PC_FREQ_CLASSES 32u        /* frequency classes floor(log2 f) */
+#define PC_MAX_FOOTPRINT (1u << 24) /* largest exact footprint bin */
 
 /* Human-readable name of a status code (static storage). */
 const char *pc_status_string(pc_status s);
@@ -198,6 +202,53 @@ size_t pc_stack_distance_session_ws(uint64_t n, uint32_t n_seqs);
 pc_status pc_stack_distance_session(const uint32_t *prev, const uint64_t *blk_off, const uint32_t *session,
                                     uint32_t n_seqs, uint64_t n, uint32_t *dist_sess, void *ws,
                                     size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Workload characterisation (Sec. 4) from the index arrays.  Times are
+ * request timestamps in microseconds (uint64[n_seqs], non-decreasing; a
+ * block access takes its request's time).  Time histograms use the bin
+ * convention of pc_mrc_weighted: bin k < K holds values v with
+ * edges[k-1] <= v < edges[k] (edges[-1] = 0), bin K holds v >= edges[K-1];
+ * 1 <= K = n_edges <= PC_MAX_PROFILE_EDGES, edges non-decreasing (checked on
+ * the device: status 3).  Every output is zeroed on `stream`, then
+ * accumulated; a bad request table sets status 2.
+ * ------------------------------------------------------------------------ */
+
+/* Per reuse and per block, from prev/next (pc_prev_next_use) in request
+ * order:
+ *   interval[K+1]      reuses t (prev exists) by ts(t) - ts(prev t)
+ *                      (Sec. 4.2 reuse intervals)
+ *   lifetime[K+1]      blocks by ts(last access) - ts(first access), 0 for a
+ *                      block used once (Sec. 4.1 lifetimes)
+ *   freq[freq_max+1]   blocks by access count f, bin min(f, freq_max), bin 0
+ *                      empty; with it the chance of a further access after k
+ *                      accesses is #(f >= k+1) / #(f >= k) (Sec. 4.3)
+ *   life_by_class[PC_FREQ_CLASSES * (K+1)]  lifetime histogram per frequency
+ *                      class floor(log2 f), class-major (Sec. 4.3, lifetime
+ *                      against frequency)
+ * 1 <= freq_max <= PC_MAX_FREQ. */
+size_t pc_reuse_profile_ws(uint64_t n);
+pc_status pc_reuse_profile(const uint32_t *prev, const uint32_t *next, const uint64_t *blk_off,
+                           const uint64_t *ts_us, uint32_t n_seqs, uint64_t n, const uint64_t *edges,
+                           uint32_t n_edges, uint32_t freq_max, uint64_t *interval, uint64_t *lifetime,
+                           uint64_t *freq, uint64_t *life_by_class, void *ws, size_t ws_bytes, void *stream);
+
+/* Per session, from the request table and the session of every request:
+ *   footprint[fp_max+1]  sessions by footprint, the largest request's block
+ *                        count (contexts are append-only), bin min(fp, fp_max)
+ *                        (Sec. 4.5; its CCDF and Lorenz curve follow)
+ *   requests[rq_max+1]   sessions by number of requests, bin min(count, rq_max)
+ *                        (Sec. 4.3 requests per session)
+ *   duration[K+1]        sessions by ts(last request) - ts(first request)
+ *                        (Sec. 4.1 session duration)
+ *   gap[K+1]             requests with an earlier request of the same session
+ *                        by the time since it (Sec. 4.2 inter-request time)
+ * 1 <= rq_max <= PC_MAX_FREQ, 1 <= fp_max <= PC_MAX_FOOTPRINT. */
+size_t pc_session_profile_ws(uint32_t n_seqs);
+pc_status pc_session_profile(const uint64_t *blk_off, const uint32_t *session, const uint64_t *ts_us,
+                             uint32_t n_seqs, uint64_t n, const uint64_t *edges, uint32_t n_edges,
+                             uint32_t fp_max, uint32_t rq_max, uint64_t *footprint, uint64_t *requests,
+                             uint64_t *duration, uint64_t *gap, void *ws, size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
  * Hit-ratio and compute-savings histograms over capacity edges.

@@ -31,6 +31,9 @@ static const char *kernel_name(KernelId k) {
     case K_REQ_DIST: return "request_distance";
     case K_SESS_REQ: return "session_requests";
     case K_SESS_DIST: return "session_distance";
+    case K_SESS_PROFILE: return "session_profile";
+    case K_PROF_PACK: return "reuse_profile_pack";
+    case K_PROF_WALK: return "reuse_profile_walk";
     case K_COUNT: break;
     }
     return "";

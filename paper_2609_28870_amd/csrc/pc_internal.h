@@ -60,6 +60,9 @@ enum KernelId {
     K_REQ_DIST,
     K_SESS_REQ,
     K_SESS_DIST,
+    K_SESS_PROFILE,
+    K_PROF_PACK,
+    K_PROF_WALK,
     K_COUNT
 };
 

@@ -176,12 +176,38 @@ __global__ void sess_status_kernel(int32_t *__restrict__ hdr, const int32_t *__r
     if (threadIdx.x == 0 && sub[0] != 0) atomicOr(hdr, sub[0]);
 }
 
-struct SessWs {
-    int32_t *hdr;
+// The requests of each session, linked like the accesses of one key: the
+// session ids go through pc_prev_next_use (1 per request).
+struct SessLinks {
     uint64_t *skeys;
-    uint32_t *prev_s, *next_s, *w, *req_page;
+    uint32_t *prev_s, *next_s;
     void *pn_ws;
     size_t pn_bytes;
+};
+
+static void take_links(Carver &c, uint32_t n_seqs, SessLinks &l) {
+    l.skeys = c.take<uint64_t>(n_seqs);
+    l.prev_s = c.take<uint32_t>(n_seqs);
+    l.next_s = c.take<uint32_t>(n_seqs);
+    l.pn_bytes = pc_prev_next_use_ws(n_seqs);
+    l.pn_ws = c.take<char>(l.pn_bytes);
+}
+
+static pc_status link_sessions(const uint32_t *session, uint32_t n_seqs, const SessLinks &l, int32_t *hdr,
+                               hipStream_t s) {
+    const unsigned rgrid = (unsigned)(((uint64_t)n_seqs + 255) / 256);
+    PC_LAUNCH(K_SESS_REQ, sess_keys_kernel, dim3(rgrid), dim3(256), 0, s, session, n_seqs, l.skeys);
+    pc_status st = pc_prev_next_use(l.skeys, n_seqs, l.prev_s, l.next_s, l.pn_ws, l.pn_bytes, s);
+    if (st != PC_OK) return st;
+    PC_LAUNCH(K_SESS_REQ, sess_status_kernel, dim3(1), dim3(64), 0, s, hdr,
+              reinterpret_cast<const int32_t *>(l.pn_ws));
+    return PC_OK;
+}
+
+struct SessWs {
+    int32_t *hdr;
+    SessLinks l;
+    uint32_t *w, *req_page;
     size_t bytes;
 };
 
@@ -189,15 +215,86 @@ static SessWs carve_sess(void *ws, uint64_t n, uint32_t n_seqs) {
     Carver c{(char *)ws, 0};
     SessWs s;
     s.hdr = c.take<int32_t>(WS_HEADER / sizeof(int32_t));
-    s.skeys = c.take<uint64_t>(n_seqs);
-    s.prev_s = c.take<uint32_t>(n_seqs);
-    s.next_s = c.take<uint32_t>(n_seqs);
+    take_links(c, n_seqs, s.l);
     s.w = c.take<uint32_t>(n_seqs);
     s.req_page = c.take<uint32_t>(((n + (1u << PAGE_BITS) - 1) >> PAGE_BITS) + 2);
-    s.pn_bytes = pc_prev_next_use_ws(n_seqs);
-    s.pn_ws = c.take<char>(s.pn_bytes);
     s.bytes = c.off;
     return s;
+}
+
+// Per-session statistics (Sec. 4.5 footprints, Sec. 4.1 session duration,
+// Sec. 4.3 requests per session, Sec. 2.3 gaps between a session's
+// requests): one lane per session walks its requests from the first.
+// Footprint = largest request (append-only contexts).  Small histograms
+// accumulate in LDS; the footprint histogram, whose range is the largest
+// request, is added to globally.
+__global__ __launch_bounds__(256) void sess_profile_kernel(
+    const uint32_t *__restrict__ prev_s, const uint32_t *__restrict__ next_s, const uint64_t *__restrict__ blk_off,
+    const uint64_t *__restrict__ ts_us, uint32_t n_seqs, uint64_t n, const uint64_t *__restrict__ edges,
+    uint32_t n_edges, uint32_t fp_max, uint32_t rq_max, uint64_t *__restrict__ footprint,
+    uint64_t *__restrict__ requests, uint64_t *__restrict__ duration, uint64_t *__restrict__ gap,
+    int32_t *__restrict__ err) {
+    __shared__ uint64_t s_edges[PC_MAX_PROFILE_EDGES];
+    __shared__ uint32_t s_dur[PC_MAX_PROFILE_EDGES + 1];
+    __shared__ uint32_t s_gap[PC_MAX_PROFILE_EDGES + 1];
+    __shared__ uint32_t s_req[PC_MAX_FREQ + 1];
+    const int tid = threadIdx.x;
+    const uint32_t kb = n_edges + 1;
+    for (uint32_t i = tid; i < n_edges; i += blockDim.x) {
+        s_edges[i] = edges[i];
+        if (blockIdx.x == 0 && i + 1 < n_edges && edges[i] > edges[i + 1]) atomicOr(err, DEV_ERR_BAD_CAPS);
+    }
+    for (uint32_t i = tid; i < kb; i += blockDim.x) s_dur[i] = s_gap[i] = 0;
+    for (uint32_t i = tid; i <= rq_max; i += blockDim.x) s_req[i] = 0;
+    __syncthreads();
+    const uint32_t stride = gridDim.x * blockDim.x;
+    for (uint32_t r = blockIdx.x * blockDim.x + tid; r < n_seqs; r += stride) {
+        if (prev_s[r] != NONE) continue;
+        uint64_t fp = 0, cnt = 0;
+        const uint64_t t0 = ts_us[r];
+        uint64_t t1 = t0;
+        uint32_t x = r;
+        for (;;) {
+            const uint64_t a = blk_off[x], b = blk_off[x + 1];
+            const uint64_t m = (a <= b && b <= n) ? b - a : 0;   // a bad layout is reported elsewhere
+            fp = m > fp ? m : fp;
+            const uint64_t tx = ts_us[x];
+            if (cnt > 0) {
+                uint32_t lo = 0, hi = n_edges;   // number of edges <= the gap
+                while (lo < hi) {
+                    const uint32_t mid = (lo + hi) >> 1;
+                    if (s_edges[mid] <= tx - t1) lo = mid + 1;
+                    else hi = mid;
+                }
+                atomicAdd(&s_gap[lo], 1u);
+            }
+            t1 = tx;
+            ++cnt;
+            const uint32_t y = next_s[x];
+            if (y == NONE) break;
+            if (y <= x || y >= n_seqs) {
+                atomicOr(err, DEV_ERR_BAD_LAYOUT);
+                break;
+            }
+            x = y;
+        }
+        uint32_t lo = 0, hi = n_edges;
+        while (lo < hi) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if (s_edges[mid] <= t1 - t0) lo = mid + 1;
+            else hi = mid;
+        }
+        atomicAdd(&s_dur[lo], 1u);
+        atomicAdd(&s_req[cnt < rq_max ? cnt : rq_max], 1u);
+        atomicAdd((unsigned long long *)&footprint[fp < fp_max ? fp : fp_max], 1ull);
+    }
+    __syncthreads();
+    for (uint32_t i = tid; i < kb; i += blockDim.x) {
+        if (s_dur[i]) atomicAdd((unsigned long long *)&duration[i], (unsigned long long)s_dur[i]);
+        if (s_gap[i]) atomicAdd((unsigned long long *)&gap[i], (unsigned long long)s_gap[i]);
+    }
+    for (uint32_t i = tid; i <= rq_max; i += blockDim.x)
+        if (s_req[i]) atomicAdd((unsigned long long *)&requests[i], (unsigned long long)s_req[i]);
 }
 
 }  // namespace pc
@@ -223,20 +320,60 @@ pc_status pc_stack_distance_session(const uint32_t *prev, const uint64_t *blk_of
     const unsigned rgrid = (unsigned)(((uint64_t)n_seqs + 255) / 256);
     PC_LAUNCH(pc::K_SESS_REQ, pc::sess_page_kernel, dim3(rgrid), dim3(256), 0, s, blk_off, n_seqs, n, w.req_page,
               w.hdr);
-    // the requests of each session, linked like blocks of one key
-    PC_LAUNCH(pc::K_SESS_REQ, pc::sess_keys_kernel, dim3(rgrid), dim3(256), 0, s, session, n_seqs, w.skeys);
-    if ((st = pc_prev_next_use(w.skeys, n_seqs, w.prev_s, w.next_s, w.pn_ws, w.pn_bytes, stream)) != PC_OK)
-        return st;
-    PC_LAUNCH(pc::K_SESS_REQ, pc::sess_status_kernel, dim3(1), dim3(64), 0, s, w.hdr,
-              reinterpret_cast<const int32_t *>(w.pn_ws));
+    if ((st = pc::link_sessions(session, n_seqs, w.l, w.hdr, s)) != PC_OK) return st;
     const int cus = pc::device_cus();
     unsigned fgrid = rgrid < (unsigned)cus * 4 ? rgrid : (unsigned)cus * 4;
-    PC_LAUNCH(pc::K_SESS_REQ, pc::sess_footprint_kernel, dim3(fgrid), dim3(256), 0, s, w.prev_s, w.next_s, blk_off,
-              n_seqs, n, w.w, w.hdr);
+    PC_LAUNCH(pc::K_SESS_REQ, pc::sess_footprint_kernel, dim3(fgrid), dim3(256), 0, s, w.l.prev_s, w.l.next_s,
+              blk_off, n_seqs, n, w.w, w.hdr);
     uint64_t grid = ((uint64_t)n_seqs + 3) / 4;
     if (grid > (uint64_t)cus * 16) grid = (uint64_t)cus * 16;
     PC_LAUNCH(pc::K_SESS_DIST, pc::sess_dist_kernel, dim3((unsigned)grid), dim3(256), 0, s, prev, blk_off, n_seqs, n,
-              w.req_page, w.next_s, w.w, dist_sess);
+              w.req_page, w.l.next_s, w.w, dist_sess);
+    return PC_OK;
+}
+
+size_t pc_session_profile_ws(uint32_t n_seqs) {
+    pc::Carver c{nullptr, 0};
+    c.take<int32_t>(pc::WS_HEADER / sizeof(int32_t));
+    pc::SessLinks l;
+    pc::take_links(c, n_seqs, l);
+    return c.off;
+}
+
+pc_status pc_session_profile(const uint64_t *blk_off, const uint32_t *session, const uint64_t *ts_us, uint32_t n_seqs,
+                             uint64_t n, const uint64_t *edges, uint32_t n_edges, uint32_t fp_max, uint32_t rq_max,
+                             uint64_t *footprint, uint64_t *requests, uint64_t *duration, uint64_t *gap, void *ws,
+                             size_t ws_bytes, void *stream) {
+    if (n >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
+    if (n_seqs >= 0x80000000u) return PC_ERR_TOO_LARGE;
+    if (n_edges < 1 || n_edges > PC_MAX_PROFILE_EDGES || rq_max < 1 || rq_max > PC_MAX_FREQ || fp_max < 1 ||
+        fp_max > PC_MAX_FOOTPRINT)
+        return PC_ERR_INVALID;
+    if (!edges || !footprint || !requests || !duration || !gap) return PC_ERR_INVALID;
+    if (n_seqs > 0 && (!blk_off || !session || !ts_us)) return PC_ERR_INVALID;
+    if (!ws) return PC_ERR_WORKSPACE;
+    if (ws_bytes < pc_session_profile_ws(n_seqs)) return PC_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    pc::Carver c{(char *)ws, 0};
+    int32_t *hdr = c.take<int32_t>(pc::WS_HEADER / sizeof(int32_t));
+    pc::SessLinks l;
+    pc::take_links(c, n_seqs, l);
+    pc_status st = pc::fill_u32(reinterpret_cast<uint32_t *>(hdr), 0u, 1, s);
+    if (st != PC_OK) return st;
+    const size_t kb = (size_t)n_edges + 1;
+    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(footprint), 0u, 2 * ((size_t)fp_max + 1), s)) != PC_OK)
+        return st;
+    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(requests), 0u, 2 * ((size_t)rq_max + 1), s)) != PC_OK)
+        return st;
+    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(duration), 0u, 2 * kb, s)) != PC_OK) return st;
+    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(gap), 0u, 2 * kb, s)) != PC_OK) return st;
+    if (n_seqs == 0) return PC_OK;
+    if ((st = pc::link_sessions(session, n_seqs, l, hdr, s)) != PC_OK) return st;
+    const int cus = pc::device_cus();
+    unsigned grid = (unsigned)(((uint64_t)n_seqs + 255) / 256);
+    if (grid > (unsigned)cus * 4) grid = (unsigned)cus * 4;
+    PC_LAUNCH(pc::K_SESS_PROFILE, pc::sess_profile_kernel, dim3(grid), dim3(256), 0, s, l.prev_s, l.next_s, blk_off,
+              ts_us, n_seqs, n, edges, n_edges, fp_max, rq_max, footprint, requests, duration, gap, hdr);
     return PC_OK;
 }
 

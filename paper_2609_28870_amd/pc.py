@@ -71,6 +71,16 @@ def lib():
     L.pc_stack_distance_session_ws.argtypes = [_u64, _u32]
     L.pc_stack_distance_session.restype = _st
     L.pc_stack_distance_session.argtypes = [_vp, _vp, _vp, _u32, _u64, _vp, _vp, _sz, _vp]
+    L.pc_reuse_profile_ws.restype = _sz
+    L.pc_reuse_profile_ws.argtypes = [_u64]
+    L.pc_reuse_profile.restype = _st
+    L.pc_reuse_profile.argtypes = [_vp, _vp, _vp, _vp, _u32, _u64, _vp, _u32, _u32, _vp, _vp, _vp, _vp, _vp,
+                                   _sz, _vp]
+    L.pc_session_profile_ws.restype = _sz
+    L.pc_session_profile_ws.argtypes = [_u32]
+    L.pc_session_profile.restype = _st
+    L.pc_session_profile.argtypes = [_vp, _vp, _vp, _u32, _u64, _vp, _u32, _u32, _u32, _vp, _vp, _vp, _vp, _vp,
+                                     _sz, _vp]
     L.pc_mrc_weighted_ws.restype = _sz
     L.pc_mrc_weighted_ws.argtypes = [_u64, _u32]
     L.pc_mrc_weighted.restype = _st
@@ -257,6 +267,58 @@ def stack_distance_session(prev: torch.Tensor, blk_off: torch.Tensor, session: t
     return dist_sess, ws
 
 
+FREQ_CLASSES = 32
+
+
+def reuse_profile(prev: torch.Tensor, nxt: torch.Tensor, blk_off: torch.Tensor, ts_us: torch.Tensor,
+                  edges: torch.Tensor, freq_max: int, out: Optional[dict] = None, ws: Optional[torch.Tensor] = None):
+    """pc_reuse_profile: reuse-interval, lifetime, frequency and
+    lifetime-by-frequency-class histograms (int64 tensors of uint64)."""
+    L = lib()
+    n = prev.numel()
+    n_seqs = blk_off.numel() - 1
+    k = edges.numel()
+    dev = _dev()
+    if out is None:
+        out = {"interval": torch.empty(k + 1, dtype=torch.int64, device=dev),
+               "lifetime": torch.empty(k + 1, dtype=torch.int64, device=dev),
+               "freq": torch.empty(freq_max + 1, dtype=torch.int64, device=dev),
+               "life_by_class": torch.empty(FREQ_CLASSES * (k + 1), dtype=torch.int64, device=dev)}
+    if ws is None:
+        ws = workspace(L.pc_reuse_profile_ws(n))
+    check(L.pc_reuse_profile(_ptr(prev), _ptr(nxt), _ptr(blk_off), _ptr(ts_us), n_seqs, n, _ptr(edges), k,
+                             freq_max, _ptr(out["interval"]), _ptr(out["lifetime"]), _ptr(out["freq"]),
+                             _ptr(out["life_by_class"]), _ptr(ws), ws.numel(), _stream()))
+    return out, ws
+
+
+def session_profile(blk_off: torch.Tensor, session: torch.Tensor, ts_us: torch.Tensor, n: int,
+                    edges: torch.Tensor, fp_max: int, rq_max: int, out: Optional[dict] = None,
+                    ws: Optional[torch.Tensor] = None):
+    """pc_session_profile: footprint, request-count, duration and gap
+    histograms over sessions (int64 tensors of uint64)."""
+    L = lib()
+    n_seqs = blk_off.numel() - 1
+    k = edges.numel()
+    dev = _dev()
+    if out is None:
+        out = {"footprint": torch.empty(fp_max + 1, dtype=torch.int64, device=dev),
+               "requests": torch.empty(rq_max + 1, dtype=torch.int64, device=dev),
+               "duration": torch.empty(k + 1, dtype=torch.int64, device=dev),
+               "gap": torch.empty(k + 1, dtype=torch.int64, device=dev)}
+    if ws is None:
+        ws = workspace(L.pc_session_profile_ws(n_seqs))
+    check(L.pc_session_profile(_ptr(blk_off), _ptr(session), _ptr(ts_us), n_seqs, n, _ptr(edges), k, fp_max,
+                               rq_max, _ptr(out["footprint"]), _ptr(out["requests"]), _ptr(out["duration"]),
+                               _ptr(out["gap"]), _ptr(ws), ws.numel(), _stream()))
+    return out, ws
+
+
+def hists_to_host(out: dict) -> dict:
+    """Device histograms -> lists of python ints."""
+    return {name: [int(x) for x in as_u64(t).tolist()] for name, t in out.items()}
+
+
 def mrc_weighted(dist: torch.Tensor, caps: torch.Tensor, depth: Optional[torch.Tensor] = None,
                  nxt: Optional[torch.Tensor] = None, alpha: int = 1, beta: int = 0,
                  out: Optional[dict] = None, ws: Optional[torch.Tensor] = None):
@@ -418,6 +480,53 @@ class Pipeline:
         return {name: workspace_status(ws) for name, ws in stages}
 
 
+class Profiler:
+    """Workload characterisation over one trace (Sec. 4): hash -> prev/next
+    -> reuse profile (intervals, lifetimes, frequencies) and session profile
+    (footprints, requests, durations, gaps), buffers allocated once."""
+
+    def __init__(self, tokens, tok_start, tok_len, blk_off, n_blocks: int, session, ts_us, edges,
+                 block_size: int = 16, freq_max: int = 2048, fp_max: int = 1 << 16, rq_max: int = 2048):
+        L = lib()
+        dev = _dev()
+        self.tokens, self.tok_start, self.tok_len, self.blk_off = tokens, tok_start, tok_len, blk_off
+        self.session, self.ts_us, self.edges = session, ts_us, edges
+        self.n = int(n_blocks)
+        self.B = block_size
+        self.freq_max, self.fp_max, self.rq_max = freq_max, fp_max, rq_max
+        n = self.n
+        self.keys = torch.empty(n, dtype=torch.int64, device=dev)
+        self.prev = torch.empty(n, dtype=torch.int32, device=dev)
+        self.next = torch.empty(n, dtype=torch.int32, device=dev)
+        self.ws_hash = workspace(L.pc_hash_blocks_ws(tok_len.numel()))
+        self.ws_pn = workspace(L.pc_prev_next_use_ws(n))
+        self.ws_rp = workspace(L.pc_reuse_profile_ws(n))
+        self.ws_sp = workspace(L.pc_session_profile_ws(tok_len.numel()))
+        k = edges.numel()
+        self.reuse = {"interval": torch.empty(k + 1, dtype=torch.int64, device=dev),
+                      "lifetime": torch.empty(k + 1, dtype=torch.int64, device=dev),
+                      "freq": torch.empty(freq_max + 1, dtype=torch.int64, device=dev),
+                      "life_by_class": torch.empty(FREQ_CLASSES * (k + 1), dtype=torch.int64, device=dev)}
+        self.sessions = {"footprint": torch.empty(fp_max + 1, dtype=torch.int64, device=dev),
+                         "requests": torch.empty(rq_max + 1, dtype=torch.int64, device=dev),
+                         "duration": torch.empty(k + 1, dtype=torch.int64, device=dev),
+                         "gap": torch.empty(k + 1, dtype=torch.int64, device=dev)}
+
+    def run(self):
+        hash_blocks(self.tokens, self.tok_start, self.tok_len, self.blk_off, self.n, self.B,
+                    want_depth=False, keys=self.keys, ws=self.ws_hash)
+        prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn)
+        reuse_profile(self.prev, self.next, self.blk_off, self.ts_us, self.edges, self.freq_max,
+                      out=self.reuse, ws=self.ws_rp)
+        session_profile(self.blk_off, self.session, self.ts_us, self.n, self.edges, self.fp_max, self.rq_max,
+                        out=self.sessions, ws=self.ws_sp)
+
+    def status(self) -> dict:
+        return {name: workspace_status(ws) for name, ws in
+                (("hash", self.ws_hash), ("prev_next", self.ws_pn), ("reuse_profile", self.ws_rp),
+                 ("session_profile", self.ws_sp))}
+
+
 def upload_trace(trace, block_size: Optional[int] = None):
     """Copy a pcgen.Trace's arrays to the GPU (input preparation, untimed)."""
     B = block_size or trace.block_size
@@ -426,4 +535,5 @@ def upload_trace(trace, block_size: Optional[int] = None):
     return dict(tokens=torch.from_numpy(trace.tokens).to(dev),
                 tok_start=to_dev_u64(trace.tok_start), tok_len=to_dev_u32(trace.tok_len),
                 blk_off=to_dev_u64(off), n_blocks=int(off[-1]), block_size=B,
-                session=to_dev_u32(trace.session.astype(np.uint32)))
+                session=to_dev_u32(trace.session.astype(np.uint32)),
+                ts_us=to_dev_u64(trace.ts_us.astype(np.uint64)))

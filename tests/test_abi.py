@@ -131,6 +131,37 @@ def test_stack_distance_session_rejects_bad_arguments(L):
     assert call(wsz=ws - 1) == -3
 
 
+def test_profiles_reject_bad_arguments(L):
+    n = 5000
+    ws = L.pc_reuse_profile_ws(n)
+    assert ws >= 8 * n
+    rp = lambda prev=FAKE, ns=40, n=n, k=4, fm=16, out=FAKE, w=FAKE, wsz=ws: L.pc_reuse_profile(
+        prev, FAKE, FAKE, FAKE, ns, n, FAKE, k, fm, out, FAKE, FAKE, FAKE, w, wsz, None)
+    assert rp(n=0xFFFFFFFF) == -2
+    assert rp(ns=0x80000000) == -2
+    assert rp(k=0) == -1
+    assert rp(k=129) == -1
+    assert rp(fm=0) == -1
+    assert rp(fm=2049) == -1
+    assert rp(prev=None) == -1
+    assert rp(out=None) == -1
+    assert rp(ns=0) == -1
+    assert rp(w=None) == -3
+    assert rp(wsz=ws - 1) == -3
+    ws = L.pc_session_profile_ws(40)
+    sp = lambda bo=FAKE, ns=40, k=4, fp=16, rq=16, out=FAKE, w=FAKE, wsz=ws: L.pc_session_profile(
+        bo, FAKE, FAKE, ns, n, FAKE, k, fp, rq, out, FAKE, FAKE, FAKE, w, wsz, None)
+    assert sp(ns=0x80000000) == -2
+    assert sp(k=0) == -1
+    assert sp(rq=2049) == -1
+    assert sp(fp=0) == -1
+    assert sp(fp=(1 << 24) + 1) == -1
+    assert sp(bo=None) == -1
+    assert sp(out=None) == -1
+    assert sp(w=None) == -3
+    assert sp(wsz=ws - 1) == -3
+
+
 def test_mrc_rejects_bad_arguments(L):
     ws = L.pc_mrc_weighted_ws(10, 4)
     ok = lambda **kw: dict(dict(dist=FAKE, depth=None, nxt=None, n=10, caps=FAKE, k=4, a=1, b=0,
@@ -157,5 +188,5 @@ def test_profiling_table(L):
     names = [L.pc_prof_kernel_name(i).decode() for i in range(n)]
     assert "hash_chain" in names and "sd_dominance_pass" in names and "mrc_hist" in names
     assert all(names) and len(set(names)) == n
-    assert names[-1] == "session_distance"
+    assert names[-1] == "reuse_profile_walk"
     assert pc.prof_read() is not None
