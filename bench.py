@@ -28,8 +28,7 @@ P_LIN = 3_000_000_000          # FLOPs per token, linear part (agent cost model)
 # algorithmic bytes per element for each kernel (inputs it must read and
 # outputs it must write, once each)
 ALGO_BYTES = {
-    "hash_digest": lambda B: 4 * B + 8,           # tokens in, digest out
-    "hash_chain": lambda B: 8 + 8 + 4,            # digest in, key and depth out
+    "hash_blocks": lambda B: 4 * B + 8 + 4,       # tokens in, key and depth out
     "sort_onesweep_pass": lambda B: 12 + 12,      # (key, t) in and out
     "link_partition": lambda B: 12 + 12,          # sorted (key, t) in, (t, prev, next) out
     "perm_partition": lambda B: 12 + 12,          # (t, prev, next) in and out
@@ -51,8 +50,8 @@ def log(*a):
 
 # HIP kernel behind each timed kernel id (for the committed counter summary)
 HIP_KERNEL = {"sort_onesweep_pass": "pc::sort_pass_kernel", "link_partition": "pc::link_partition_kernel",
-              "perm_partition": "pc::perm_partition_kernel", "hash_digest": "pc::hash_digest_kernel",
-              "hash_chain": "pc::hash_chain_kernel", "sd_local_finish": "pc::sd_local_kernel",
+              "perm_partition": "pc::perm_partition_kernel", "hash_blocks": "pc::hash_fused_kernel",
+              "sd_local_finish": "pc::sd_local_kernel",
               "perm_local": "pc::perm_local_kernel", "mrc_hist": "pc::mrc_hist_kernel",
               "request_order": "pc::req_order_kernel", "request_distance": "pc::req_dist_kernel",
               "session_distance": "pc::sess_dist_kernel"}
@@ -318,7 +317,7 @@ def main():
     if mt:
         mt["GBps_at_this_run"] = round(roof["traffic"] / (d["avg_working_launch_ms"] / 1e3) / 1e9, 1)
     roof["traffic_detail"] = mt
-    stage_of = {"hash_digest": "hash", "hash_chain": "hash", "sort_digit_hist": "prev_next",
+    stage_of = {"hash_blocks": "hash", "sort_digit_hist": "prev_next",
                 "sort_digit_scan": "prev_next", "sort_onesweep_pass": "prev_next",
                 "link_partition": "prev_next",
                 "perm_partition": "prev_next", "perm_local": "prev_next", "mrc_hist": "mrc",

@@ -10,8 +10,7 @@ namespace pc {
 static const char *kernel_name(KernelId k) {
     switch (k) {
     case K_FILL32: return "fill_u32";
-    case K_HASH_DIGEST: return "hash_digest";
-    case K_HASH: return "hash_chain";
+    case K_HASH: return "hash_blocks";
     case K_SORT_HIST: return "sort_digit_hist";
     case K_SORT_SCAN: return "sort_digit_scan";
     case K_SORT_PASS: return "sort_onesweep_pass";

@@ -6,16 +6,17 @@
 // as a step S(x, w) = mix64((x ^ w) + gamma), folded over the block's
 // token-pair words from 0 (the digest) and chained block to block.
 //
-// GPU mapping, two phases.  (1) Digests are independent per block: one wave
-// takes one request and lane j hashes block j, so a wave reads 4 KiB of
-// tokens in one coalesced sweep and writes 64 digests contiguously.  (2) The
-// chain is serial inside a request: one lane owns one request and walks its
-// digests in place; the digests move between HBM and an LDS tile one request
-// at a time (coalesced 512-byte accesses) and are chained from LDS.  A wave
-// refills lanes from a global request counter as their requests end, so long
-// and short requests mix without idle lanes.  Per 16-token block the
-// work is nine splitmix steps (two 64x64 multiplies each) and 64 bytes of
-// tokens read.
+// GPU mapping: one kernel.  The chain is serial inside a request, so a lane
+// owns a request and walks it in rounds of up to 32 blocks; the digests of a
+// round are independent, so the whole wave computes them first (32 lanes per
+// request, one block each, token loads of several requests in flight), puts
+// them in an LDS tile with one row per request, and each lane then chains its
+// own row.  Keys and depths leave one request at a time (coalesced).  Lanes
+// whose request ended take the next one from a global counter, so long and
+// short requests mix without idle lanes.  Per 16-token block the work is nine
+// splitmix steps (two 64x64 multiplies each), 64 token bytes in and 12 bytes
+// out; the steps are what bounds it (the multiplies issue at a quarter of the
+// VALU rate).
 #include "pc_internal.h"
 
 namespace pc {
@@ -34,22 +35,6 @@ __device__ __forceinline__ uint64_t word(uint32_t a, uint32_t b) {
     return (uint64_t)a | ((uint64_t)b << 32);
 }
 
-// digest of one 16-token block at a 16-byte aligned address
-__device__ __forceinline__ uint64_t digest16(const int32_t *p) {
-    const uint4 *q = reinterpret_cast<const uint4 *>(p);
-    uint4 a = q[0], b = q[1], c = q[2], d = q[3];
-    uint64_t h = 0;
-    h = hstep(h, word(a.x, a.y));
-    h = hstep(h, word(a.z, a.w));
-    h = hstep(h, word(b.x, b.y));
-    h = hstep(h, word(b.z, b.w));
-    h = hstep(h, word(c.x, c.y));
-    h = hstep(h, word(c.z, c.w));
-    h = hstep(h, word(d.x, d.y));
-    h = hstep(h, word(d.z, d.w));
-    return h;
-}
-
 // any even block size, any 4-byte alignment
 __device__ __forceinline__ uint64_t digest_any(const int32_t *p, uint32_t B) {
     uint64_t h = 0;
@@ -57,78 +42,58 @@ __device__ __forceinline__ uint64_t digest_any(const int32_t *p, uint32_t B) {
     return h;
 }
 
-constexpr int HASH_THREADS = 256;
-
 // true when every token and block of request r lies inside the arrays
 __device__ __forceinline__ bool request_in_bounds(uint64_t st, uint32_t len, uint32_t nb, uint64_t out,
                                                   uint64_t n_tokens, uint64_t n_blocks) {
     return st <= n_tokens && len <= n_tokens - st && out <= n_blocks && nb <= n_blocks - out;
 }
 
-// Phase 1: digests.  One wave per request, lane = block: a wave reads 64
-// consecutive 64-byte token blocks (4 KiB, fully coalesced) and writes 64
-// consecutive 8-byte digests into the key array.  Requests come from an
-// atomic counter so long and short requests balance across waves.
-__global__ __launch_bounds__(HASH_THREADS) void hash_digest_kernel(
-    const int32_t *__restrict__ tokens, uint64_t n_tokens, const uint64_t *__restrict__ tok_start,
-    const uint32_t *__restrict__ tok_len, uint32_t n_seqs, uint32_t B,
-    const uint64_t *__restrict__ blk_off, uint64_t n_blocks, uint64_t *__restrict__ keys,
-    uint32_t *__restrict__ counter, int32_t *__restrict__ err) {
-    const int lane = threadIdx.x & (WAVE - 1);
-    while (true) {
-        uint32_t r = 0;
-        if (lane == 0) r = atomicAdd(counter, 1u);
-        r = __shfl(r, 0, WAVE);
-        if (r >= n_seqs) break;
-        const uint32_t len = tok_len[r];
-        const uint64_t st = tok_start[r];
-        const uint32_t nb = len / B;
-        const uint64_t out = blk_off[r];
-        if (!request_in_bounds(st, len, nb, out, n_tokens, n_blocks)) {
-            if (lane == 0) atomicOr(err, DEV_ERR_BAD_LAYOUT);
-            continue;
-        }
-        const int32_t *tp = tokens + st;
-        const bool fast = (B == 16) && ((reinterpret_cast<uintptr_t>(tp) & 15) == 0);
-        for (uint32_t j = lane; j < nb; j += WAVE) {
-            const int32_t *p = tp + (uint64_t)j * B;
-            keys[out + j] = fast ? digest16(p) : digest_any(p, B);
-        }
-    }
-}
-
-// Phase 2: the chain, serial inside a request.  A wave owns up to 64
-// requests (one per lane) and advances all of them by up to 32 blocks per
-// round.  Memory moves per request, not per lane: for each of its requests
-// the wave loads the next 32 digests with one coalesced 256-byte access into
-// an LDS tile (row = request, padded against bank conflicts), every lane then
-// chains its own row in LDS, and the keys (and depths) go back the same way.
-// Lanes whose request ended take the next one from an atomic counter at the
-// start of the round.
 __device__ __forceinline__ uint64_t readlane64(uint64_t v, int i) {
     const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, i);
     const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), i);
     return (uint64_t)lo | ((uint64_t)hi << 32);
 }
 
-constexpr int CHAIN_THREADS = 128;                       // two waves per workgroup
-constexpr int CHAIN_WAVES = CHAIN_THREADS / WAVE;
-constexpr int CHAIN_SPAN = 32;                           // blocks per request per round
-constexpr int CHAIN_ROW = CHAIN_SPAN + 1;                // padded LDS row
-constexpr int GATHER_BATCH = 16;                         // requests per load round
+constexpr int GATHER_BATCH = 16;                         // requests per store round
 
-__global__ __launch_bounds__(CHAIN_THREADS) void hash_chain_kernel(
-    const uint32_t *__restrict__ tok_len, uint32_t n_seqs, uint32_t B,
-    const uint64_t *__restrict__ parent, uint64_t root, const uint64_t *__restrict__ blk_off,
-    uint64_t n_blocks, uint64_t *__restrict__ keys, uint32_t *__restrict__ depth,
-    uint32_t *__restrict__ counter) {
-    __shared__ uint64_t s_tile[CHAIN_WAVES][WAVE * CHAIN_ROW];
+// Both phases in one kernel: the chain kernel's lane-per-request rounds,
+// with each round's digests computed in place of being read back from HBM.
+// A sweep gives each request of FUSE_ROWS rows a group of FUSE_SPAN lanes
+// (lane j of the group hashes block j of the round) and writes the digests
+// into the LDS tile; the token loads of FUSE_SWEEPS sweeps are issued
+// together.  The digests never touch HBM: a block costs its token bytes in and
+// its key and depth out.
+constexpr int FUSE_THREADS = 128;
+constexpr int FUSE_WAVES = FUSE_THREADS / WAVE;
+constexpr int FUSE_SPAN = 32;               // blocks per request per round
+constexpr int FUSE_ROWS = WAVE / FUSE_SPAN; // requests per sweep
+constexpr int FUSE_ROW = FUSE_SPAN + 1;     // padded LDS row
+constexpr int FUSE_SWEEPS = 4;              // sweeps whose loads are in flight together
+
+__device__ __forceinline__ uint64_t digest16_words(const uint4 (&q)[4]) {
+    uint64_t h = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        h = hstep(h, word(q[i].x, q[i].y));
+        h = hstep(h, word(q[i].z, q[i].w));
+    }
+    return h;
+}
+
+__global__ __launch_bounds__(FUSE_THREADS) void hash_fused_kernel(
+    const int32_t *__restrict__ tokens, uint64_t n_tokens, const uint64_t *__restrict__ tok_start,
+    const uint32_t *__restrict__ tok_len, uint32_t n_seqs, uint32_t B, const uint64_t *__restrict__ parent,
+    uint64_t root, const uint64_t *__restrict__ blk_off, uint64_t n_blocks, uint64_t *__restrict__ keys,
+    uint32_t *__restrict__ depth, uint32_t *__restrict__ counter, int32_t *__restrict__ err) {
+    __shared__ uint64_t s_tile[FUSE_WAVES][WAVE * FUSE_ROW];
     const int lane = threadIdx.x & (WAVE - 1);
     const int w = threadIdx.x / WAVE;
+    const int grp = lane / FUSE_SPAN;
+    const uint32_t jj = (uint32_t)(lane & (FUSE_SPAN - 1));
     uint64_t *tile = s_tile[w];
     bool done = false, busy = false;
-    uint32_t b = 0, nb = 0;
-    uint64_t key = 0, out = 0;
+    uint32_t b = 0, nb = 0, fast = 0;
+    uint64_t key = 0, out = 0, st = 0;
     while (true) {
         const bool need = !done && !busy;
         const uint64_t needmask = ballot(need);
@@ -142,12 +107,18 @@ __global__ __launch_bounds__(CHAIN_THREADS) void hash_chain_kernel(
                 if (r >= n_seqs) {
                     done = true;
                 } else {
-                    nb = tok_len[r] / B;
+                    const uint32_t len = tok_len[r];
+                    st = tok_start[r];
+                    nb = len / B;
                     out = blk_off[r];
                     b = 0;
                     key = parent ? parent[r] : root;
-                    // phase 1 wrote digests only for in-bounds requests
-                    busy = nb > 0 && out <= n_blocks && nb <= n_blocks - out;
+                    fast = (B == 16 && (reinterpret_cast<uintptr_t>(tokens + st) & 15) == 0) ? 1u : 0u;
+                    if (request_in_bounds(st, len, nb, out, n_tokens, n_blocks)) {
+                        busy = nb > 0;
+                    } else {
+                        atomicOr(err, DEV_ERR_BAD_LAYOUT);
+                    }
                 }
             }
         }
@@ -156,50 +127,68 @@ __global__ __launch_bounds__(CHAIN_THREADS) void hash_chain_kernel(
             if (ballot(!done) == 0) break;
             continue;
         }
-        const uint32_t m = busy ? (nb - b < (uint32_t)CHAIN_SPAN ? nb - b : (uint32_t)CHAIN_SPAN) : 0u;
-        const uint64_t pos = out + b;
-        // gather: row i <- the next m_i digests of lane i's request.  Loads
-        // for GATHER_BATCH requests are issued before their LDS stores, so a
-        // round waits for a few memory latencies instead of one per request.
+        const uint32_t m = busy ? (nb - b < (uint32_t)FUSE_SPAN ? nb - b : (uint32_t)FUSE_SPAN) : 0u;
+        // ---- digests of the round's blocks into the tile
         {
             uint64_t act = active;
             while (act) {
-                int ids[GATHER_BATCH];
-                uint64_t v[GATHER_BATCH];
+                int row[FUSE_SWEEPS];
+                bool ok[FUSE_SWEEPS], fr[FUSE_SWEEPS];
+                uint64_t addr[FUSE_SWEEPS];
+                uint4 tk[FUSE_SWEEPS][4];
 #pragma unroll
-                for (int q = 0; q < GATHER_BATCH; ++q) {
-                    ids[q] = -1;
-                    v[q] = 0;
-                    if (act) {
-                        const int i = __ffsll((unsigned long long)act) - 1;   // wave-uniform
-                        act &= act - 1;
-                        ids[q] = i;
-                        const uint32_t mi = (uint32_t)__builtin_amdgcn_readlane((int)m, i);
-                        const uint64_t pi = readlane64(pos, i);
-                        if ((uint32_t)lane < mi) v[q] = keys[pi + lane];
+                for (int q = 0; q < FUSE_SWEEPS; ++q) {
+                    // the next FUSE_ROWS requests (wave-uniform); this lane's is number grp
+                    int r = -1;
+#pragma unroll
+                    for (int g = 0; g < FUSE_ROWS; ++g) {
+                        int rg = -1;
+                        if (act) {
+                            rg = __ffsll((unsigned long long)act) - 1;
+                            act &= act - 1;
+                        }
+                        if (g == grp) r = rg;
+                    }
+                    const int src = r >= 0 ? r : 0;
+                    const uint32_t mr = (uint32_t)__shfl((int)m, src, WAVE);
+                    const uint32_t br = (uint32_t)__shfl((int)b, src, WAVE);
+                    const uint32_t fq = (uint32_t)__shfl((int)fast, src, WAVE);
+                    const uint64_t sr = (uint64_t)(uint32_t)__shfl((int)(uint32_t)st, src, WAVE) |
+                                        ((uint64_t)(uint32_t)__shfl((int)(uint32_t)(st >> 32), src, WAVE) << 32);
+                    row[q] = src;
+                    ok[q] = r >= 0 && jj < mr;
+                    fr[q] = fq != 0;
+                    addr[q] = sr + (uint64_t)(br + jj) * B;
+                    if (ok[q] && fr[q]) {
+                        const uint4 *p = reinterpret_cast<const uint4 *>(tokens + addr[q]);
+                        tk[q][0] = p[0];
+                        tk[q][1] = p[1];
+                        tk[q][2] = p[2];
+                        tk[q][3] = p[3];
                     }
                 }
 #pragma unroll
-                for (int q = 0; q < GATHER_BATCH; ++q) {
-                    if (ids[q] >= 0) {
-                        const uint32_t mi = (uint32_t)__builtin_amdgcn_readlane((int)m, ids[q]);
-                        if ((uint32_t)lane < mi) tile[ids[q] * CHAIN_ROW + lane] = v[q];
+                for (int q = 0; q < FUSE_SWEEPS; ++q) {
+                    if (ok[q]) {
+                        const uint64_t d = fr[q] ? digest16_words(tk[q]) : digest_any(tokens + addr[q], B);
+                        tile[row[q] * FUSE_ROW + jj] = d;
                     }
                 }
             }
         }
         __builtin_amdgcn_wave_barrier();
+        // ---- the chain, one request per lane, from LDS
         if (busy) {
-            uint64_t *row = tile + lane * CHAIN_ROW;
-            for (uint32_t j = 0; j < m; ++j) {
-                key = hstep(key, row[j]);
-                row[j] = key;
+            uint64_t *rowp = tile + lane * FUSE_ROW;
+            for (uint32_t q = 0; q < m; ++q) {
+                key = hstep(key, rowp[q]);
+                rowp[q] = key;
             }
         }
         __builtin_amdgcn_wave_barrier();
-        // scatter back: keys and depths of row i, coalesced (LDS reads for a
-        // batch of requests first, then their stores)
+        // ---- keys and depths of row i back, coalesced per request
         {
+            const uint64_t pos = out + b;
             uint64_t act = active;
             while (act) {
                 int ids[GATHER_BATCH];
@@ -212,7 +201,7 @@ __global__ __launch_bounds__(CHAIN_THREADS) void hash_chain_kernel(
                         const int i = __ffsll((unsigned long long)act) - 1;
                         act &= act - 1;
                         ids[q] = i;
-                        v[q] = tile[i * CHAIN_ROW + (lane < CHAIN_SPAN ? lane : 0)];
+                        v[q] = tile[i * FUSE_ROW + (lane < FUSE_SPAN ? lane : 0)];
                     }
                 }
 #pragma unroll
@@ -271,20 +260,13 @@ pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_
     if (st != PC_OK) return st;
 
     const int cus = pc::device_cus();
-    // persistent grids: a few workgroups per CU, work handed out by counters
-    uint64_t want = ((uint64_t)n_seqs * pc::WAVE + pc::HASH_THREADS - 1) / pc::HASH_THREADS;
+    // persistent grid: a few workgroups per CU, requests handed out by a counter
+    uint64_t want = ((uint64_t)n_seqs + pc::FUSE_THREADS - 1) / pc::FUSE_THREADS;
     uint64_t cap = (uint64_t)cus * 8;
     unsigned grid = (unsigned)(want < cap ? want : cap);
     if (grid == 0) grid = 1;
-    PC_LAUNCH(pc::K_HASH_DIGEST, pc::hash_digest_kernel, dim3(grid), dim3(pc::HASH_THREADS), 0, s,
-              tokens, n_tokens, tok_start, tok_len, n_seqs, block_size, blk_off, n_blocks, keys,
-              counters, hdr);
-    want = ((uint64_t)n_seqs + pc::CHAIN_THREADS - 1) / pc::CHAIN_THREADS;
-    cap = (uint64_t)cus * 8;
-    grid = (unsigned)(want < cap ? want : cap);
-    if (grid == 0) grid = 1;
-    PC_LAUNCH(pc::K_HASH, pc::hash_chain_kernel, dim3(grid), dim3(pc::CHAIN_THREADS), 0, s, tok_len,
-              n_seqs, block_size, parent, root, blk_off, n_blocks, keys, depth, counters + 1);
+    PC_LAUNCH(pc::K_HASH, pc::hash_fused_kernel, dim3(grid), dim3(pc::FUSE_THREADS), 0, s, tokens, n_tokens,
+              tok_start, tok_len, n_seqs, block_size, parent, root, blk_off, n_blocks, keys, depth, counters, hdr);
     return PC_OK;
 }
 

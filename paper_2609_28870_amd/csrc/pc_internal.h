@@ -39,7 +39,6 @@ constexpr int32_t DEV_ERR_BAD_CAPS = 3;
 // ------------------------------------------------------------ kernel launches
 enum KernelId {
     K_FILL32 = 0,
-    K_HASH_DIGEST,
     K_HASH,
     K_SORT_HIST,
     K_SORT_SCAN,

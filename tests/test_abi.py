@@ -186,7 +186,7 @@ def test_workspace_status_rejects_null(L):
 def test_profiling_table(L):
     n = L.pc_prof_kernel_count()
     names = [L.pc_prof_kernel_name(i).decode() for i in range(n)]
-    assert "hash_chain" in names and "sd_dominance_pass" in names and "mrc_hist" in names
+    assert "hash_blocks" in names and "sd_dominance_pass" in names and "mrc_hist" in names
     assert all(names) and len(set(names)) == n
     assert names[-1] == "reuse_profile_walk"
     assert pc.prof_read() is not None
