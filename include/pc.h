@@ -82,6 +82,10 @@ int pc_version(void);
  *                               blk_off[n_seqs] must equal n_blocks
  *   keys       uint64[n_blocks] output
  *   depth      uint32[n_blocks] output block index b inside its request, or NULL
+ *   key_hist   uint32[4 * 256] output, or NULL: key_hist[256 p + d] counts the
+ *              keys written whose byte p (bits 8p .. 8p+7) is d, p = 0..3.
+ *              Zeroed by the call.  Handing it to pc_prev_next_use spares that
+ *              call a full read of the keys.
  * A request whose tokens run past n_tokens, or whose blocks run past
  * n_blocks, is skipped and the workspace status (pc_workspace_status) is set
  * to 2; nothing is read or written out of bounds.
@@ -90,7 +94,7 @@ size_t pc_hash_blocks_ws(uint32_t n_seqs);
 pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_t *tok_start,
                          const uint32_t *tok_len, uint32_t n_seqs, uint32_t block_size,
                          const uint64_t *parent, uint64_t root, const uint64_t *blk_off,
-                         uint64_t n_blocks, uint64_t *keys, uint32_t *depth,
+                         uint64_t n_blocks, uint64_t *keys, uint32_t *depth, uint32_t *key_hist,
                          void *ws, size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
@@ -102,7 +106,13 @@ pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_
  * (Sec. 3.2 "Belady's optimum"; Sec. 5.2 "BeladyCompute", time until next
  * access); prev == PC_NONE marks a compulsory miss (Sec. 4.6).
  *
- *   keys  uint64[n]; prev, next uint32[n] outputs.
+ *   keys      uint64[n]; prev, next uint32[n] outputs.
+ *   key_hist  uint32[4 * 256] or NULL: the byte histograms of the low four key
+ *             bytes as pc_hash_blocks counts them, for exactly these keys; NULL
+ *             counts them here (one more read of the keys).  A histogram whose
+ *             rows do not each sum to n sets the workspace status to 4; one
+ *             that sums right but does not match the keys gives unspecified
+ *             outputs (never an access out of bounds).
  * Keys are grouped by their low 32 bits first; only when many different keys
  * share those bits does the call also sort by the high 32 bits.  Once the
  * stream has completed, 32-bit word 1 of the workspace tells which happened
@@ -110,7 +120,7 @@ pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_
  * ------------------------------------------------------------------------ */
 size_t pc_prev_next_use_ws(uint64_t n);
 pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uint32_t *next,
-                           void *ws, size_t ws_bytes, void *stream);
+                           const uint32_t *key_hist, void *ws, size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
  * Exact LRU stack distance of every access.
@@ -292,7 +302,9 @@ pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uin
  *      bounded spin (outputs undefined);
  *   2  pc_hash_blocks: a request's tokens or blocks fall outside the arrays
  *      (that request was skipped);
- *   3  pc_mrc_weighted: caps not non-decreasing (bins undefined).
+ *   3  pc_mrc_weighted and the profiles: edges not non-decreasing (bins
+ *      undefined);
+ *   4  pc_prev_next_use: a given key histogram does not sum to n.
  * This call copies the code of workspace `ws` to *code_out after
  * synchronising `stream` (the only synchronising call in the library).
  * ------------------------------------------------------------------------ */

@@ -84,8 +84,12 @@ __global__ __launch_bounds__(FUSE_THREADS) void hash_fused_kernel(
     const int32_t *__restrict__ tokens, uint64_t n_tokens, const uint64_t *__restrict__ tok_start,
     const uint32_t *__restrict__ tok_len, uint32_t n_seqs, uint32_t B, const uint64_t *__restrict__ parent,
     uint64_t root, const uint64_t *__restrict__ blk_off, uint64_t n_blocks, uint64_t *__restrict__ keys,
-    uint32_t *__restrict__ depth, uint32_t *__restrict__ counter, int32_t *__restrict__ err) {
+    uint32_t *__restrict__ depth, uint32_t *__restrict__ key_hist, uint32_t *__restrict__ counter,
+    int32_t *__restrict__ err) {
     __shared__ uint64_t s_tile[FUSE_WAVES][WAVE * FUSE_ROW];
+    __shared__ uint32_t s_hist[4 * 256];   // byte histograms of the keys written
+    for (int i = threadIdx.x; i < 4 * 256; i += FUSE_THREADS) s_hist[i] = 0;
+    __syncthreads();
     const int lane = threadIdx.x & (WAVE - 1);
     const int w = threadIdx.x / WAVE;
     const int grp = lane / FUSE_SPAN;
@@ -214,6 +218,11 @@ __global__ __launch_bounds__(FUSE_THREADS) void hash_fused_kernel(
                         if ((uint32_t)lane < mi) {
                             keys[pi + lane] = v[q];
                             if (depth) depth[pi + lane] = bi + lane;
+                            if (key_hist) {
+                                const uint32_t lo = (uint32_t)v[q];
+#pragma unroll
+                                for (int p = 0; p < 4; ++p) atomicAdd(&s_hist[256 * p + ((lo >> (8 * p)) & 0xFF)], 1u);
+                            }
                         }
                     }
                 }
@@ -224,6 +233,11 @@ __global__ __launch_bounds__(FUSE_THREADS) void hash_fused_kernel(
             b += m;
             busy = b < nb;
         }
+    }
+    if (key_hist) {
+        __syncthreads();
+        for (int i = threadIdx.x; i < 4 * 256; i += FUSE_THREADS)
+            if (s_hist[i]) atomicAdd(&key_hist[i], s_hist[i]);
     }
 }
 
@@ -240,7 +254,7 @@ pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_
                          const uint32_t *tok_len,
                          uint32_t n_seqs, uint32_t block_size, const uint64_t *parent, uint64_t root,
                          const uint64_t *blk_off, uint64_t n_blocks, uint64_t *keys, uint32_t *depth,
-                         void *ws, size_t ws_bytes, void *stream) {
+                         uint32_t *key_hist, void *ws, size_t ws_bytes, void *stream) {
     if (block_size < 2 || block_size > 1024 || (block_size & 1)) return PC_ERR_INVALID;
     if (n_seqs >= 0x80000000u) return PC_ERR_TOO_LARGE;
     if (n_blocks >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
@@ -249,6 +263,10 @@ pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_
     if (!ws) return PC_ERR_WORKSPACE;
     if (ws_bytes < pc_hash_blocks_ws(n_seqs)) return PC_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
+    if (key_hist) {
+        const pc_status hs = pc::fill_u32(key_hist, 0u, 4 * 256, s);
+        if (hs != PC_OK) return hs;
+    }
     if (n_seqs == 0 || n_blocks == 0) return PC_OK;
 
     pc::Carver c{(char *)ws, 0};
@@ -266,7 +284,8 @@ pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_
     unsigned grid = (unsigned)(want < cap ? want : cap);
     if (grid == 0) grid = 1;
     PC_LAUNCH(pc::K_HASH, pc::hash_fused_kernel, dim3(grid), dim3(pc::FUSE_THREADS), 0, s, tokens, n_tokens,
-              tok_start, tok_len, n_seqs, block_size, parent, root, blk_off, n_blocks, keys, depth, counters, hdr);
+              tok_start, tok_len, n_seqs, block_size, parent, root, blk_off, n_blocks, keys, depth, key_hist,
+              counters, hdr);
     return PC_OK;
 }
 

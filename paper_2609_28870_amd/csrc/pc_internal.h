@@ -35,6 +35,7 @@ struct Carver {
 constexpr int32_t DEV_ERR_LOOKBACK_TIMEOUT = 1;
 constexpr int32_t DEV_ERR_BAD_LAYOUT = 2;
 constexpr int32_t DEV_ERR_BAD_CAPS = 3;
+constexpr int32_t DEV_ERR_BAD_HIST = 4;
 
 // ------------------------------------------------------------ kernel launches
 enum KernelId {

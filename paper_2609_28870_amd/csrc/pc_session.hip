@@ -197,7 +197,7 @@ static pc_status link_sessions(const uint32_t *session, uint32_t n_seqs, const S
                                hipStream_t s) {
     const unsigned rgrid = (unsigned)(((uint64_t)n_seqs + 255) / 256);
     PC_LAUNCH(K_SESS_REQ, sess_keys_kernel, dim3(rgrid), dim3(256), 0, s, session, n_seqs, l.skeys);
-    pc_status st = pc_prev_next_use(l.skeys, n_seqs, l.prev_s, l.next_s, l.pn_ws, l.pn_bytes, s);
+    pc_status st = pc_prev_next_use(l.skeys, n_seqs, l.prev_s, l.next_s, nullptr, l.pn_ws, l.pn_bytes, s);
     if (st != PC_OK) return st;
     PC_LAUNCH(K_SESS_REQ, sess_status_kernel, dim3(1), dim3(64), 0, s, hdr,
               reinterpret_cast<const int32_t *>(l.pn_ws));

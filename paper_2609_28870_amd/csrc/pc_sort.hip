@@ -63,16 +63,20 @@ __global__ __launch_bounds__(256) void sort_hist_kernel(const uint64_t *__restri
     }
 }
 
-// exclusive scan of each pass's 256-bin histogram -> digit bases
+// exclusive scan of each pass's 256-bin histogram -> digit bases; hist
+// holds the group's rows (p0 .. p0+3) at rows 0..3; a row that does not sum
+// to n (a histogram handed in by the caller) is reported
 __global__ __launch_bounds__(RADIX) void sort_scan_kernel(const uint32_t *__restrict__ hist, int p0,
-                                                          uint32_t *__restrict__ start,
+                                                          uint32_t *__restrict__ start, uint64_t n,
+                                                          int32_t *__restrict__ err,
                                                           const int32_t *__restrict__ only_if) {
     if (only_if && *only_if == 0) return;
     __shared__ uint32_t tmp[RADIX / WAVE];
-    for (int p = p0; p < p0 + HIST_DIGITS; ++p) {
+    for (int p = 0; p < HIST_DIGITS; ++p) {
         uint32_t total;
         const uint32_t e = block_excl_scan(hist[p * RADIX + threadIdx.x], tmp, &total);
-        start[p * RADIX + threadIdx.x] = e;
+        start[(p0 + p) * RADIX + threadIdx.x] = e;
+        if (threadIdx.x == 0 && (uint64_t)total != n) atomicOr(err, DEV_ERR_BAD_HIST);
     }
 }
 
@@ -176,20 +180,27 @@ __global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_kernel(
             st_status64(mine, ep | FLAG_INC | (uint32_t)(excl + cnt));
         }
         s_gbase[tid] = start[tid] + excl - lst;
+        // the last tile holds every digit's total: it must fill the digit's
+        // range exactly (a caller's histogram that does not match the keys)
+        if ((uint64_t)(tile + 1) * SORT_TILE >= n) {
+            const uint32_t hi = tid + 1 < RADIX ? start[tid + 1] : (uint32_t)n;
+            if (start[tid] + excl + cnt != hi) atomicOr(err, DEV_ERR_BAD_HIST);
+        }
     }
     __syncthreads();
     const uint64_t left = n - base;
     const uint32_t n_tile = left < (uint64_t)SORT_TILE ? (uint32_t)left : (uint32_t)SORT_TILE;
-    // keys out, remembering each slot's destination for the values
+    // keys out, remembering each slot's destination for the values (a
+    // histogram that does not match the keys cannot send a write outside)
     uint32_t dst[SORT_ITEMS];
 #pragma unroll
     for (int r = 0; r < SORT_ITEMS; ++r) {
         const uint32_t i = (uint32_t)(tid + r * SORT_THREADS);
-        dst[r] = 0;
+        dst[r] = NONE;
         if (i < n_tile) {
             const uint64_t kk = s_stage[i];
             dst[r] = s_gbase[(uint32_t)(kk >> shift) & 0xFF] + i;
-            keys_out[dst[r]] = kk;
+            if (dst[r] < n) keys_out[dst[r]] = kk;
         }
     }
     __syncthreads();
@@ -201,7 +212,7 @@ __global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_kernel(
 #pragma unroll
     for (int r = 0; r < SORT_ITEMS; ++r) {
         const uint32_t i = (uint32_t)(tid + r * SORT_THREADS);
-        if (i < n_tile) vals_out[dst[r]] = s_val[i];
+        if (i < n_tile && dst[r] < n) vals_out[dst[r]] = s_val[i];
     }
 }
 
@@ -392,7 +403,9 @@ __device__ __forceinline__ void perm_partition_body(
         }
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            if ((uint32_t)(q * PERM_THREADS + tid0) < left) {
+            // (a time outside [0, n) can only come from inconsistent input;
+            // it reserves nothing and its element is not written)
+            if ((uint32_t)(q * PERM_THREADS + tid0) < left && tt[q] < n) {
                 const uint32_t d = (tt[q] >> s) & (PERM_RADIX - 1);
                 atomicAdd(&s_cnt[d], 1u);
                 s_bucket[d] = tt[q] >> s;   // every writer of digit d writes the same bucket
@@ -728,7 +741,7 @@ extern "C" {
 size_t pc_prev_next_use_ws(uint64_t n) { return pc::carve_sort(nullptr, n).bytes; }
 
 pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uint32_t *next,
-                           void *ws, size_t ws_bytes, void *stream) {
+                           const uint32_t *key_hist, void *ws, size_t ws_bytes, void *stream) {
     if (n >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
     if (n > 0 && (!keys || !prev || !next)) return PC_ERR_INVALID;
     if (!ws) return PC_ERR_WORKSPACE;
@@ -751,10 +764,12 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
     // so the high-byte passes and a second link run
     int32_t *need_high = w.hdr + 1;
     if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(need_high), 0u, 1, s)) != PC_OK) return st;
-    PC_LAUNCH(pc::K_SORT_HIST, pc::sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n, 0, w.hist,
-              (const int32_t *)nullptr);
-    PC_LAUNCH(pc::K_SORT_SCAN, pc::sort_scan_kernel, dim3(1), dim3(pc::RADIX), 0, s, w.hist, 0, w.start,
-              (const int32_t *)nullptr);
+    // the low bytes' histograms: handed in by the hash, or counted here
+    if (!key_hist)
+        PC_LAUNCH(pc::K_SORT_HIST, pc::sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n, 0, w.hist,
+                  (const int32_t *)nullptr);
+    PC_LAUNCH(pc::K_SORT_SCAN, pc::sort_scan_kernel, dim3(1), dim3(pc::RADIX), 0, s, key_hist ? key_hist : w.hist,
+              0, w.start, n, w.hdr, (const int32_t *)nullptr);
 
     // Links + partition back to time order.  The sort leaves (key, t) in
     // (k2, v2) after four passes and again after eight; the triples ping-pong
@@ -784,8 +799,9 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
                       n, pp.s[0], per_wg, w.cursor, bt[0], bpn[0], (const int32_t *)nullptr, need_high);
             PC_LAUNCH(pc::K_SORT_HIST, pc::sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n,
                       pc::SORT_PASSES / 2, w.hist, (const int32_t *)need_high);
-            PC_LAUNCH(pc::K_SORT_SCAN, pc::sort_scan_kernel, dim3(1), dim3(pc::RADIX), 0, s, w.hist,
-                      pc::SORT_PASSES / 2, w.start, (const int32_t *)need_high);
+            PC_LAUNCH(pc::K_SORT_SCAN, pc::sort_scan_kernel, dim3(1), dim3(pc::RADIX), 0, s,
+                      w.hist + pc::SORT_PASSES / 2 * pc::RADIX, pc::SORT_PASSES / 2, w.start, n, w.hdr,
+                      (const int32_t *)need_high);
         }
         uint64_t *kout = (p & 1) ? w.k2 : w.k1;
         uint32_t *vout = (p & 1) ? w.v2 : w.v1;

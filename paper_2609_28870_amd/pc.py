@@ -50,11 +50,11 @@ def lib():
     L.pc_hash_blocks_ws.argtypes = [_u32]
     L.pc_hash_blocks.restype = _st
     L.pc_hash_blocks.argtypes = [_vp, _u64, _vp, _vp, _u32, _u32, _vp, _u64, _vp, _u64, _vp, _vp,
-                                 _vp, _sz, _vp]
+                                 _vp, _vp, _sz, _vp]
     L.pc_prev_next_use_ws.restype = _sz
     L.pc_prev_next_use_ws.argtypes = [_u64]
     L.pc_prev_next_use.restype = _st
-    L.pc_prev_next_use.argtypes = [_vp, _u64, _vp, _vp, _vp, _sz, _vp]
+    L.pc_prev_next_use.argtypes = [_vp, _u64, _vp, _vp, _vp, _vp, _sz, _vp]
     L.pc_stack_distance_ws.restype = _sz
     L.pc_stack_distance_ws.argtypes = [_u64]
     L.pc_stack_distance.restype = _st
@@ -159,8 +159,10 @@ def hash_blocks(tokens: torch.Tensor, tok_start: torch.Tensor, tok_len: torch.Te
                 blk_off: torch.Tensor, n_blocks: int, block_size: int = 16,
                 parent: Optional[torch.Tensor] = None, root: int = 0, want_depth: bool = True,
                 keys: Optional[torch.Tensor] = None, depth: Optional[torch.Tensor] = None,
-                ws: Optional[torch.Tensor] = None):
-    """pc_hash_blocks: keys (int64 bits of uint64) and depth (int32 bits)."""
+                ws: Optional[torch.Tensor] = None, key_hist: Optional[torch.Tensor] = None):
+    """pc_hash_blocks: keys (int64 bits of uint64) and depth (int32 bits);
+    with ``key_hist`` (int32[1024]) also the byte histograms of the keys'
+    low four bytes, which prev_next_use can take instead of counting them."""
     L = lib()
     dev = _dev()
     n_seqs = tok_len.numel()
@@ -172,13 +174,14 @@ def hash_blocks(tokens: torch.Tensor, tok_start: torch.Tensor, tok_len: torch.Te
         ws = workspace(L.pc_hash_blocks_ws(n_seqs))
     check(L.pc_hash_blocks(_ptr(tokens), tokens.numel(), _ptr(tok_start), _ptr(tok_len), n_seqs,
                            block_size, _ptr(parent), root & (2 ** 64 - 1), _ptr(blk_off), n_blocks,
-                           _ptr(keys), _ptr(depth) if want_depth else None, _ptr(ws), ws.numel(),
-                           _stream()))
+                           _ptr(keys), _ptr(depth) if want_depth else None, _ptr(key_hist), _ptr(ws),
+                           ws.numel(), _stream()))
     return keys, (depth if want_depth else None), ws
 
 
 def prev_next_use(keys: torch.Tensor, prev: Optional[torch.Tensor] = None,
-                  nxt: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None):
+                  nxt: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                  key_hist: Optional[torch.Tensor] = None):
     L = lib()
     n = keys.numel()
     dev = _dev()
@@ -188,7 +191,8 @@ def prev_next_use(keys: torch.Tensor, prev: Optional[torch.Tensor] = None,
         nxt = torch.empty(n, dtype=torch.int32, device=dev)
     if ws is None:
         ws = workspace(L.pc_prev_next_use_ws(n))
-    check(L.pc_prev_next_use(_ptr(keys), n, _ptr(prev), _ptr(nxt), _ptr(ws), ws.numel(), _stream()))
+    check(L.pc_prev_next_use(_ptr(keys), n, _ptr(prev), _ptr(nxt), _ptr(key_hist), _ptr(ws), ws.numel(),
+                             _stream()))
     return prev, nxt, ws
 
 
@@ -422,6 +426,7 @@ class Pipeline:
         self.with_nextuse = with_nextuse and residency == "access"
         n = self.n
         self.keys = torch.empty(n, dtype=torch.int64, device=dev)
+        self.key_hist = torch.empty(4 * 256, dtype=torch.int32, device=dev)
         self.depth = torch.empty(n, dtype=torch.int32, device=dev)
         self.prev = torch.empty(n, dtype=torch.int32, device=dev)
         self.next = torch.empty(n, dtype=torch.int32, device=dev)
@@ -445,22 +450,23 @@ class Pipeline:
 
     def run(self):
         hash_blocks(self.tokens, self.tok_start, self.tok_len, self.blk_off, self.n, self.B,
-                    keys=self.keys, depth=self.depth, ws=self.ws_hash)
+                    keys=self.keys, depth=self.depth, ws=self.ws_hash, key_hist=self.key_hist)
         if self.residency == "session":
-            prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn)
+            prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
             stack_distance_session(self.prev, self.blk_off, self.session, dist_sess=self.dist, ws=self.ws_sd)
             mrc_weighted(self.dist, self.caps, self.depth, None, self.alpha, self.beta, out=self.bins,
                          ws=self.ws_mrc)
             return
         if not self.request:
-            prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn)
+            prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
             stack_distance(self.prev, self.next, self.dist, ws=self.ws_sd)
             mrc_weighted(self.dist, self.caps, self.depth, self.next if self.with_nextuse else None,
                          self.alpha, self.beta, out=self.bins, ws=self.ws_mrc)
             return
         request_order(self.keys, self.blk_off, self.depth, keys_out=self.keys_r, depth_out=self.depth_r,
                       ws=self.ws_ro)
-        prev_next_use(self.keys_r, self.prev, self.next, ws=self.ws_pn)
+        # the reordered keys are a permutation of the hashed ones: same histogram
+        prev_next_use(self.keys_r, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
         stack_distance(self.prev, self.next, self.dist, ws=self.ws_sd)
         stack_distance_req(self.prev, self.dist, self.blk_off, dist_req=self.dist_req, ws=self.ws_req)
         mrc_weighted(self.dist_req, self.caps, self.depth_r, None, self.alpha, self.beta,
@@ -496,6 +502,7 @@ class Profiler:
         self.freq_max, self.fp_max, self.rq_max = freq_max, fp_max, rq_max
         n = self.n
         self.keys = torch.empty(n, dtype=torch.int64, device=dev)
+        self.key_hist = torch.empty(4 * 256, dtype=torch.int32, device=dev)
         self.prev = torch.empty(n, dtype=torch.int32, device=dev)
         self.next = torch.empty(n, dtype=torch.int32, device=dev)
         self.ws_hash = workspace(L.pc_hash_blocks_ws(tok_len.numel()))
@@ -514,8 +521,8 @@ class Profiler:
 
     def run(self):
         hash_blocks(self.tokens, self.tok_start, self.tok_len, self.blk_off, self.n, self.B,
-                    want_depth=False, keys=self.keys, ws=self.ws_hash)
-        prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn)
+                    want_depth=False, keys=self.keys, ws=self.ws_hash, key_hist=self.key_hist)
+        prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
         reuse_profile(self.prev, self.next, self.blk_off, self.ts_us, self.edges, self.freq_max,
                       out=self.reuse, ws=self.ws_rp)
         session_profile(self.blk_off, self.session, self.ts_us, self.n, self.edges, self.fp_max, self.rq_max,

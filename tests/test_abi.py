@@ -52,7 +52,7 @@ FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails va
 def test_hash_rejects_bad_arguments(L):
     ws = L.pc_hash_blocks_ws(4)
     args = lambda B=16, n_seqs=4, nb=100, wsz=ws, tokens=FAKE, w=FAKE: (
-        tokens, 1000, FAKE, FAKE, n_seqs, B, None, 0, FAKE, nb, FAKE, None, w, wsz, None)
+        tokens, 1000, FAKE, FAKE, n_seqs, B, None, 0, FAKE, nb, FAKE, None, None, w, wsz, None)
     assert L.pc_hash_blocks(*args(B=15)) == -1
     assert L.pc_hash_blocks(*args(B=0)) == -1
     assert L.pc_hash_blocks(*args(B=2048)) == -1
@@ -66,11 +66,11 @@ def test_hash_rejects_bad_arguments(L):
 def test_prev_next_rejects_bad_arguments(L):
     n = 1000
     ws = L.pc_prev_next_use_ws(n)
-    assert L.pc_prev_next_use(FAKE, 0xFFFFFFFF, FAKE, FAKE, FAKE, 1 << 40, None) == -2
-    assert L.pc_prev_next_use(None, n, FAKE, FAKE, FAKE, ws, None) == -1
-    assert L.pc_prev_next_use(FAKE, n, FAKE, None, FAKE, ws, None) == -1
-    assert L.pc_prev_next_use(FAKE, n, FAKE, FAKE, None, ws, None) == -3
-    assert L.pc_prev_next_use(FAKE, n, FAKE, FAKE, FAKE, ws - 1, None) == -3
+    assert L.pc_prev_next_use(FAKE, 0xFFFFFFFF, FAKE, FAKE, None, FAKE, 1 << 40, None) == -2
+    assert L.pc_prev_next_use(None, n, FAKE, FAKE, None, FAKE, ws, None) == -1
+    assert L.pc_prev_next_use(FAKE, n, FAKE, None, None, FAKE, ws, None) == -1
+    assert L.pc_prev_next_use(FAKE, n, FAKE, FAKE, None, None, ws, None) == -3
+    assert L.pc_prev_next_use(FAKE, n, FAKE, FAKE, None, FAKE, ws - 1, None) == -3
 
 
 def test_stack_distance_rejects_bad_arguments(L):

@@ -126,6 +126,49 @@ def test_hash_unaligned_views_parent_and_root():
     assert np.array_equal(gk, ok)
 
 
+def low_byte_hist(keys):
+    k = np.asarray(keys, np.uint64)
+    return np.concatenate([np.bincount(((k >> np.uint64(8 * p)) & np.uint64(0xFF)).astype(np.int64),
+                                       minlength=256) for p in range(4)])
+
+
+def test_hash_counts_the_key_byte_histogram():
+    tr = pcgen.make_trace("tiny")
+    keys, _ = oracle.hash_trace(tr)
+    up = pc.upload_trace(tr, 16)
+    hist = torch.empty(1024, dtype=torch.int32, device="cuda")
+    gk, _, ws = pc.hash_blocks(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"], 16,
+                               key_hist=hist)
+    assert pc.workspace_status(ws) == 0
+    assert np.array_equal(pc.as_u64(gk), keys)
+    assert np.array_equal(pc.as_u32(hist).astype(np.int64), low_byte_hist(keys))
+
+
+@pytest.mark.parametrize("kind", ["mixed", "lowsame"])
+def test_prev_next_with_a_given_histogram(kind):
+    keys = stream(kind, 70001, 5)
+    hist = pc.to_dev_u32(low_byte_hist(keys).astype(np.uint32))
+    prev, nxt, ws = pc.prev_next_use(pc.to_dev_u64(keys), key_hist=hist)
+    assert pc.workspace_status(ws) == 0
+    op, on = oracle.prev_next(keys)
+    assert np.array_equal(pc.as_u32(prev), op) and np.array_equal(pc.as_u32(nxt), on)
+
+
+def test_prev_next_reports_a_wrong_histogram():
+    keys = stream("mixed", 20000, 6)
+    h = low_byte_hist(keys)
+    short = h.copy()
+    short[3] -= 1                       # a row that does not sum to n
+    _, _, ws = pc.prev_next_use(pc.to_dev_u64(keys), key_hist=pc.to_dev_u32(short.astype(np.uint32)))
+    assert pc.workspace_status(ws) == 4
+    moved = h.copy()
+    d = int(np.nonzero(moved[:256])[0][0])
+    moved[d] -= 1
+    moved[(d + 1) % 256] += 1           # sums to n, but not these keys' counts
+    _, _, ws = pc.prev_next_use(pc.to_dev_u64(keys), key_hist=pc.to_dev_u32(moved.astype(np.uint32)))
+    assert pc.workspace_status(ws) == 4
+
+
 def test_tiny_trace_every_stage():
     tr = pcgen.make_trace("tiny")
     keys, depth = oracle.hash_trace(tr)
