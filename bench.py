@@ -54,10 +54,12 @@ HIP_KERNEL = {"sort_onesweep_pass": "pc::sort_pass_kernel", "link_partition": "p
               "sd_local_finish": "pc::sd_local_kernel",
               "perm_local": "pc::perm_local_kernel", "mrc_hist": "pc::mrc_hist_kernel",
               "request_order": "pc::req_order_kernel", "request_distance": "pc::req_dist_kernel",
-              "session_distance": "pc::sess_dist_kernel"}
+              "session_distance": "pc::sess_dist_kernel", "reuse_profile_walk": "pc::prof_walk_kernel",
+              "reuse_profile_pack": "pc::prof_pack_kernel"}
 PROFILES = {"access": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9.md"),
             "request": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_request.md"),
-            "session": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_session.md")}
+            "session": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_session.md"),
+            "profile": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_profile.md")}
 PROFILE = PROFILES["access"]
 
 
@@ -243,7 +245,7 @@ def main():
     request = args.residency == "request"
     session_mode = args.residency == "session"
     global PROFILE
-    PROFILE = PROFILES[args.residency]
+    PROFILE = PROFILES["profile" if args.profile else args.residency]
     if args.profile:
         prof_edges = pc.to_dev_u64(np.array(PROFILE_EDGES_US, np.uint64))
         pipe = pc.Profiler(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
