@@ -56,15 +56,18 @@ __global__ __launch_bounds__(PROF_THREADS) void prof_walk_kernel(
     uint32_t n_seqs, uint64_t n, const uint64_t *__restrict__ edges, uint32_t n_edges, uint32_t freq_max,
     uint64_t *__restrict__ interval, uint64_t *__restrict__ lifetime, uint64_t *__restrict__ freq,
     uint64_t *__restrict__ life_by_class, int32_t *__restrict__ err) {
-    __shared__ uint64_t s_edges[PC_MAX_PROFILE_EDGES];
-    __shared__ uint32_t s_ival[PC_MAX_PROFILE_EDGES + 1];
-    __shared__ uint32_t s_class[PC_FREQ_CLASSES * (PC_MAX_PROFILE_EDGES + 1)];
-    __shared__ uint32_t s_freq[PC_MAX_FREQ + 1];
+    // LDS sized by the call (edges, bins, frequency bins): smaller
+    // histograms leave room for more waves, and the walk is latency-bound
+    extern __shared__ uint64_t smem[];
     __shared__ uint32_t s_queue[PROF_WAVES][PROF_QUEUE];
     const int tid = threadIdx.x;
     const int lane = tid & (WAVE - 1);
     const int wv = tid / WAVE;
     const uint32_t kb = n_edges + 1;
+    uint64_t *s_edges = smem;                                               // n_edges
+    uint32_t *s_ival = reinterpret_cast<uint32_t *>(s_edges + n_edges);     // kb
+    uint32_t *s_class = s_ival + kb;                                        // classes * kb
+    uint32_t *s_freq = s_class + PC_FREQ_CLASSES * kb;                      // freq_max + 1
     for (uint32_t i = tid; i < n_edges; i += PROF_THREADS) {
         s_edges[i] = edges[i];
         if (blockIdx.x == 0 && i + 1 < n_edges && edges[i] > edges[i + 1]) atomicOr(err, DEV_ERR_BAD_CAPS);
@@ -197,8 +200,9 @@ pc_status pc_reuse_profile(const uint32_t *prev, const uint32_t *next, const uin
               w.packed, w.hdr);
     const uint64_t chunks = (n + pc::WAVE - 1) / pc::WAVE;
     uint64_t grid = (chunks + pc::PROF_WAVES - 1) / pc::PROF_WAVES;
-    if (grid > (uint64_t)cus * 8) grid = (uint64_t)cus * 8;
-    PC_LAUNCH(pc::K_PROF_WALK, pc::prof_walk_kernel, dim3((unsigned)grid), dim3(pc::PROF_THREADS), 0, s, prev,
+    if (grid > (uint64_t)cus * 7) grid = (uint64_t)cus * 7;   // about one resident round
+    const size_t shmem = (size_t)n_edges * 8 + (kb + (size_t)PC_FREQ_CLASSES * kb + freq_max + 1) * 4;
+    PC_LAUNCH(pc::K_PROF_WALK, pc::prof_walk_kernel, dim3((unsigned)grid), dim3(pc::PROF_THREADS), shmem, s, prev,
               w.packed, ts_us, n_seqs, n, edges, n_edges, freq_max, interval, lifetime, freq, life_by_class, w.hdr);
     return PC_OK;
 }
