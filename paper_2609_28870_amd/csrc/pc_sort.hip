@@ -277,15 +277,24 @@ __device__ __forceinline__ bool scan_run(const uint64_t *__restrict__ sk, uint64
     return false;
 }
 
-__device__ __forceinline__ uint64_t shfl_up64(uint64_t v) {
-    const uint32_t lo = (uint32_t)__shfl_up((int)(uint32_t)v, 1, WAVE);
-    const uint32_t hi = (uint32_t)__shfl_up((int)(uint32_t)(v >> 32), 1, WAVE);
-    return (uint64_t)lo | ((uint64_t)hi << 32);
+// lane i receives lane i - 1's value (from_lower) or lane i + 1's
+// (from_upper) with one DPP move across the whole wave (wave_shr:1 /
+// wave_shl:1); the lane without a source keeps its own value
+__device__ __forceinline__ uint32_t from_lower(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x138, 0xf, 0xf, false);
 }
-__device__ __forceinline__ uint64_t shfl_down64(uint64_t v) {
-    const uint32_t lo = (uint32_t)__shfl_down((int)(uint32_t)v, 1, WAVE);
-    const uint32_t hi = (uint32_t)__shfl_down((int)(uint32_t)(v >> 32), 1, WAVE);
-    return (uint64_t)lo | ((uint64_t)hi << 32);
+__device__ __forceinline__ uint32_t from_upper(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x130, 0xf, 0xf, false);
+}
+__device__ __forceinline__ uint64_t from_lower64(uint64_t v) {
+    return (uint64_t)from_lower((uint32_t)v) | ((uint64_t)from_lower((uint32_t)(v >> 32)) << 32);
+}
+__device__ __forceinline__ uint64_t from_upper64(uint64_t v) {
+    return (uint64_t)from_upper((uint32_t)v) | ((uint64_t)from_upper((uint32_t)(v >> 32)) << 32);
+}
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int i) {
+    return (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, i) |
+           ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), i) << 32);
 }
 __device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
     const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src, WAVE);
@@ -482,12 +491,12 @@ __device__ __forceinline__ void perm_partition_body(
                 const uint32_t w0 = o - (uint32_t)lane;
                 const int last = w0 < left ? (int)(left - 1 - w0 < (uint32_t)(WAVE - 1) ? left - 1 - w0 : WAVE - 1)
                                            : -1;
-                uint64_t kp = shfl_up64(k[j]), kn = shfl_down64(k[j]);
-                uint32_t tp = (uint32_t)__shfl_up((int)t[j], 1, WAVE);
-                uint32_t tn = (uint32_t)__shfl_down((int)t[j], 1, WAVE);
-                const uint64_t ekp = shfl64(ek, j), ekn = shfl64(ek, 8 + j);
-                const uint32_t etp = (uint32_t)__shfl((int)et, j, WAVE);
-                const uint32_t etn = (uint32_t)__shfl((int)et, 8 + j, WAVE);
+                uint64_t kp = from_lower64(k[j]), kn = from_upper64(k[j]);
+                uint32_t tp = from_lower(t[j]);
+                uint32_t tn = from_upper(t[j]);
+                const uint64_t ekp = readlane64(ek, j), ekn = readlane64(ek, 8 + j);
+                const uint32_t etp = (uint32_t)__builtin_amdgcn_readlane((int)et, j);
+                const uint32_t etn = (uint32_t)__builtin_amdgcn_readlane((int)et, 8 + j);
                 bool mp = false, mn = false;
                 uint32_t pv = NONE, nx = NONE;
                 if (ok[j]) {
