@@ -48,11 +48,6 @@ __device__ __forceinline__ bool request_in_bounds(uint64_t st, uint32_t len, uin
     return st <= n_tokens && len <= n_tokens - st && out <= n_blocks && nb <= n_blocks - out;
 }
 
-__device__ __forceinline__ uint64_t readlane64(uint64_t v, int i) {
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, i);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), i);
-    return (uint64_t)lo | ((uint64_t)hi << 32);
-}
 
 constexpr int GATHER_BATCH = 16;                         // requests per store round
 

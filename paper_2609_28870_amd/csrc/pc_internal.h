@@ -144,6 +144,25 @@ __device__ __forceinline__ uint32_t wave_incl_or(uint32_t x) {
     return x;
 }
 
+// lane i receives lane i - 1's value (from_lower) or lane i + 1's
+// (from_upper) with one DPP move across the whole wave (wave_shr:1 /
+// wave_shl:1); the lane without a source keeps its own value
+__device__ __forceinline__ uint32_t from_lower(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x138, 0xf, 0xf, false);
+}
+__device__ __forceinline__ uint32_t from_upper(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x130, 0xf, 0xf, false);
+}
+__device__ __forceinline__ uint64_t from_lower64(uint64_t v) {
+    return (uint64_t)from_lower((uint32_t)v) | ((uint64_t)from_lower((uint32_t)(v >> 32)) << 32);
+}
+__device__ __forceinline__ uint64_t from_upper64(uint64_t v) {
+    return (uint64_t)from_upper((uint32_t)v) | ((uint64_t)from_upper((uint32_t)(v >> 32)) << 32);
+}
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int i) {
+    return (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, i) |
+           ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), i) << 32);
+}
 // exclusive prefix sum across the 64 lanes of a wave
 __device__ __forceinline__ uint32_t wave_excl_scan(uint32_t v) { return wave_incl_scan(v) - v; }
 

@@ -277,25 +277,6 @@ __device__ __forceinline__ bool scan_run(const uint64_t *__restrict__ sk, uint64
     return false;
 }
 
-// lane i receives lane i - 1's value (from_lower) or lane i + 1's
-// (from_upper) with one DPP move across the whole wave (wave_shr:1 /
-// wave_shl:1); the lane without a source keeps its own value
-__device__ __forceinline__ uint32_t from_lower(uint32_t x) {
-    return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x138, 0xf, 0xf, false);
-}
-__device__ __forceinline__ uint32_t from_upper(uint32_t x) {
-    return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x130, 0xf, 0xf, false);
-}
-__device__ __forceinline__ uint64_t from_lower64(uint64_t v) {
-    return (uint64_t)from_lower((uint32_t)v) | ((uint64_t)from_lower((uint32_t)(v >> 32)) << 32);
-}
-__device__ __forceinline__ uint64_t from_upper64(uint64_t v) {
-    return (uint64_t)from_upper((uint32_t)v) | ((uint64_t)from_upper((uint32_t)(v >> 32)) << 32);
-}
-__device__ __forceinline__ uint64_t readlane64(uint64_t v, int i) {
-    return (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, i) |
-           ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), i) << 32);
-}
 __device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
     const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src, WAVE);
     const uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(v >> 32), src, WAVE);

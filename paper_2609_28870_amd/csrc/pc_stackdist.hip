@@ -235,7 +235,7 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_count_kernel(
     for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
         // invalid lanes take digit RADIX (never counted) so they end runs
         const uint32_t d = ok[i] ? (t[i] >> s) & dmask : (uint32_t)DOM_RADIX;
-        const uint32_t dl = (uint32_t)__shfl_up((int)d, 1, WAVE);
+        const uint32_t dl = from_lower(d);   // lane 0 keeps its own and is a head anyway
         const bool head = lane == 0 || dl != d;
         const uint64_t heads = ballot(head);
         // next head above this lane (or 64): the run is [lane, next)
