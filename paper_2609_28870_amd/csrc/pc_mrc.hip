@@ -187,7 +187,7 @@ pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uin
 
     const int cus = pc::device_cus();
     uint64_t grid = (n + pc::MRC_THREADS * pc::MRC_PER - 1) / (pc::MRC_THREADS * pc::MRC_PER);
-    if (grid > (uint64_t)cus * 8) grid = (uint64_t)cus * 8;
+    if (grid > (uint64_t)cus * 16) grid = (uint64_t)cus * 16;   // 16 workgroups per CU hide the load latency
     if (grid == 0) grid = 1;
     const size_t shmem = (size_t)n_caps * 8 + (size_t)bins * 8 + (size_t)bins * 8;
     PC_LAUNCH(pc::K_MRC_HIST, pc::mrc_hist_kernel, dim3((unsigned)grid), dim3(pc::MRC_THREADS), shmem, s, dist,

@@ -250,7 +250,7 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_count_kernel(
 
 // Segmented exclusive scan over tiles, per digit (a bucket's first tile
 // restarts the sum), in three steps over groups of SEG_GROUP tiles.
-constexpr int SEG_GROUP = 1024;
+constexpr int SEG_GROUP = 256;
 constexpr int SEG_BATCH = 16;
 
 __device__ __forceinline__ uint64_t total_tiles(const uint32_t *tfirst_end, uint64_t fixed) {
