@@ -62,11 +62,19 @@ __device__ __forceinline__ uint64_t cnt_lt(uint64_t X, const uint32_t *__restric
 __global__ __launch_bounds__(256) void sd_cold_count_kernel(const uint32_t *__restrict__ prev,
                                                             uint64_t n, uint32_t *__restrict__ cnt) {
     __shared__ uint32_t tmp[4];
-    const uint64_t base = (uint64_t)blockIdx.x * LOCAL_SPAN;
+    constexpr int PER = LOCAL_SPAN / 256;   // 16 consecutive values per thread
+    const uint64_t base = (uint64_t)blockIdx.x * LOCAL_SPAN + (uint64_t)threadIdx.x * PER;
     uint32_t c = 0;
-    for (int j = 0; j < (int)(LOCAL_SPAN / 256); ++j) {
-        const uint64_t t = base + (uint64_t)j * 256 + threadIdx.x;
-        if (t < n && prev[t] == NONE) ++c;
+    if (base + PER <= n && (reinterpret_cast<uintptr_t>(prev) & 15) == 0) {
+        const uint4 *p = reinterpret_cast<const uint4 *>(prev + base);   // four 16-byte loads in flight
+        uint4 v[PER / 4];
+#pragma unroll
+        for (int q = 0; q < PER / 4; ++q) v[q] = p[q];
+#pragma unroll
+        for (int q = 0; q < PER / 4; ++q)
+            c += (v[q].x == NONE) + (v[q].y == NONE) + (v[q].z == NONE) + (v[q].w == NONE);
+    } else {
+        for (int j = 0; j < PER; ++j) c += (base + j < n && prev[base + j] == NONE) ? 1u : 0u;
     }
     uint32_t total;
     block_excl_scan(c, tmp, &total);
