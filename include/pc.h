@@ -44,6 +44,7 @@ typedef enum {
 
 #define PC_NONE 0xFFFFFFFFu
 #define PC_MAX_CAPS 1024u
+#define PC_HASH_DEEPEST_FIRST 1u   /* pc_hash_blocks flag */
 #define PC_MAX_PROFILE_EDGES 128u  /* time-histogram edges of the profiles */
 #define PC_MAX_FREQ 2048u          /* largest exact frequency / request-count bin */
 #define PC_FREQ_CLASSES 32u        /* frequency classes floor(log2 f) */
@@ -86,6 +87,11 @@ int pc_version(void);
  *              keys written whose byte p (bits 8p .. 8p+7) is d, p = 0..3.
  *              Zeroed by the call.  Handing it to pc_prev_next_use spares that
  *              call a full read of the keys.
+ *   flags      0, or PC_HASH_DEEPEST_FIRST: each request's blocks (keys and
+ *              depths) are written in descending depth order inside the
+ *              request's range, i.e. block b goes to blk_off[r+1] - 1 - b
+ *              (the recency order of request-level residency; the same as
+ *              pc_request_order applied afterwards).
  * A request whose tokens run past n_tokens, or whose blocks run past
  * n_blocks, is skipped and the workspace status (pc_workspace_status) is set
  * to 2; nothing is read or written out of bounds.
@@ -95,7 +101,7 @@ pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_
                          const uint32_t *tok_len, uint32_t n_seqs, uint32_t block_size,
                          const uint64_t *parent, uint64_t root, const uint64_t *blk_off,
                          uint64_t n_blocks, uint64_t *keys, uint32_t *depth, uint32_t *key_hist,
-                         void *ws, size_t ws_bytes, void *stream);
+                         uint32_t flags, void *ws, size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
  * Previous / next use of every access.

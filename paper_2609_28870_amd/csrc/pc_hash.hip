@@ -79,8 +79,9 @@ __global__ __launch_bounds__(FUSE_THREADS) void hash_fused_kernel(
     const int32_t *__restrict__ tokens, uint64_t n_tokens, const uint64_t *__restrict__ tok_start,
     const uint32_t *__restrict__ tok_len, uint32_t n_seqs, uint32_t B, const uint64_t *__restrict__ parent,
     uint64_t root, const uint64_t *__restrict__ blk_off, uint64_t n_blocks, uint64_t *__restrict__ keys,
-    uint32_t *__restrict__ depth, uint32_t *__restrict__ key_hist, uint32_t *__restrict__ counter,
+    uint32_t *__restrict__ depth, uint32_t *__restrict__ key_hist, uint32_t flags, uint32_t *__restrict__ counter,
     int32_t *__restrict__ err) {
+    const bool deepest_first = (flags & PC_HASH_DEEPEST_FIRST) != 0;
     __shared__ uint64_t s_tile[FUSE_WAVES][WAVE * FUSE_ROW];
     __shared__ uint32_t s_hist[4 * 256];   // byte histograms of the keys written
     for (int i = threadIdx.x; i < 4 * 256; i += FUSE_THREADS) s_hist[i] = 0;
@@ -187,7 +188,9 @@ __global__ __launch_bounds__(FUSE_THREADS) void hash_fused_kernel(
         __builtin_amdgcn_wave_barrier();
         // ---- keys and depths of row i back, coalesced per request
         {
-            const uint64_t pos = out + b;
+            // output position of this round's first block (or, deepest
+            // first, of its mirror image inside the request)
+            const uint64_t pos = deepest_first ? out + nb - 1 - b : out + b;
             uint64_t act = active;
             while (act) {
                 int ids[GATHER_BATCH];
@@ -211,8 +214,9 @@ __global__ __launch_bounds__(FUSE_THREADS) void hash_fused_kernel(
                         const uint64_t pi = readlane64(pos, i);
                         const uint32_t bi = (uint32_t)__builtin_amdgcn_readlane((int)b, i);
                         if ((uint32_t)lane < mi) {
-                            keys[pi + lane] = v[q];
-                            if (depth) depth[pi + lane] = bi + lane;
+                            const uint64_t at = deepest_first ? pi - lane : pi + lane;
+                            keys[at] = v[q];
+                            if (depth) depth[at] = bi + lane;
                             if (key_hist) {
                                 const uint32_t lo = (uint32_t)v[q];
 #pragma unroll
@@ -249,7 +253,7 @@ pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_
                          const uint32_t *tok_len,
                          uint32_t n_seqs, uint32_t block_size, const uint64_t *parent, uint64_t root,
                          const uint64_t *blk_off, uint64_t n_blocks, uint64_t *keys, uint32_t *depth,
-                         uint32_t *key_hist, void *ws, size_t ws_bytes, void *stream) {
+                         uint32_t *key_hist, uint32_t flags, void *ws, size_t ws_bytes, void *stream) {
     if (block_size < 2 || block_size > 1024 || (block_size & 1)) return PC_ERR_INVALID;
     if (n_seqs >= 0x80000000u) return PC_ERR_TOO_LARGE;
     if (n_blocks >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
@@ -280,7 +284,7 @@ pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_
     if (grid == 0) grid = 1;
     PC_LAUNCH(pc::K_HASH, pc::hash_fused_kernel, dim3(grid), dim3(pc::FUSE_THREADS), 0, s, tokens, n_tokens,
               tok_start, tok_len, n_seqs, block_size, parent, root, blk_off, n_blocks, keys, depth, key_hist,
-              counters, hdr);
+              flags, counters, hdr);
     return PC_OK;
 }
 

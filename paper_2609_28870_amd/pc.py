@@ -50,7 +50,7 @@ def lib():
     L.pc_hash_blocks_ws.argtypes = [_u32]
     L.pc_hash_blocks.restype = _st
     L.pc_hash_blocks.argtypes = [_vp, _u64, _vp, _vp, _u32, _u32, _vp, _u64, _vp, _u64, _vp, _vp,
-                                 _vp, _vp, _sz, _vp]
+                                 _vp, _u32, _vp, _sz, _vp]
     L.pc_prev_next_use_ws.restype = _sz
     L.pc_prev_next_use_ws.argtypes = [_u64]
     L.pc_prev_next_use.restype = _st
@@ -159,10 +159,13 @@ def hash_blocks(tokens: torch.Tensor, tok_start: torch.Tensor, tok_len: torch.Te
                 blk_off: torch.Tensor, n_blocks: int, block_size: int = 16,
                 parent: Optional[torch.Tensor] = None, root: int = 0, want_depth: bool = True,
                 keys: Optional[torch.Tensor] = None, depth: Optional[torch.Tensor] = None,
-                ws: Optional[torch.Tensor] = None, key_hist: Optional[torch.Tensor] = None):
+                ws: Optional[torch.Tensor] = None, key_hist: Optional[torch.Tensor] = None,
+                deepest_first: bool = False):
     """pc_hash_blocks: keys (int64 bits of uint64) and depth (int32 bits);
     with ``key_hist`` (int32[1024]) also the byte histograms of the keys'
-    low four bytes, which prev_next_use can take instead of counting them."""
+    low four bytes, which prev_next_use can take instead of counting them.
+    ``deepest_first`` writes each request's blocks in descending depth order
+    (the recency order of request-level residency)."""
     L = lib()
     dev = _dev()
     n_seqs = tok_len.numel()
@@ -174,8 +177,8 @@ def hash_blocks(tokens: torch.Tensor, tok_start: torch.Tensor, tok_len: torch.Te
         ws = workspace(L.pc_hash_blocks_ws(n_seqs))
     check(L.pc_hash_blocks(_ptr(tokens), tokens.numel(), _ptr(tok_start), _ptr(tok_len), n_seqs,
                            block_size, _ptr(parent), root & (2 ** 64 - 1), _ptr(blk_off), n_blocks,
-                           _ptr(keys), _ptr(depth) if want_depth else None, _ptr(key_hist), _ptr(ws),
-                           ws.numel(), _stream()))
+                           _ptr(keys), _ptr(depth) if want_depth else None, _ptr(key_hist),
+                           1 if deepest_first else 0, _ptr(ws), ws.numel(), _stream()))
     return keys, (depth if want_depth else None), ws
 
 
@@ -400,8 +403,9 @@ class Pipeline:
     the session-level distance instead; it needs ``session``, the session of
     every request, and takes no next-use histogram.
     ``residency="request"`` (every block of a request resident at once,
-    Sec. 3.1) first puts each request's accesses in recency order (deepest
-    block first), runs prev/next and the stack distance on that order, turns
+    Sec. 3.1) hashes each request's blocks straight into recency order
+    (deepest block first; ``keys_r`` and ``depth_r`` alias ``keys`` and
+    ``depth``), runs prev/next and the stack distance on that order, turns
     the result into the request-level distance and bins that, with depth in
     the same order; the next-use histogram is not taken in that mode.  Its
     bins are valid at capacities of at least the largest request."""
@@ -441,16 +445,15 @@ class Pipeline:
         else:
             self.ws_sd = workspace(L.pc_stack_distance_ws(n))
         if self.request:
-            self.keys_r = torch.empty(n, dtype=torch.int64, device=dev)
-            self.depth_r = torch.empty(n, dtype=torch.int32, device=dev)
+            self.keys_r, self.depth_r = self.keys, self.depth   # hashed in recency order
             self.dist_req = torch.empty(n, dtype=torch.int32, device=dev)
-            self.ws_ro = workspace(L.pc_request_order_ws())
             self.ws_req = workspace(L.pc_stack_distance_req_ws())
         self.ws_mrc = workspace(L.pc_mrc_weighted_ws(n, k))
 
     def run(self):
         hash_blocks(self.tokens, self.tok_start, self.tok_len, self.blk_off, self.n, self.B,
-                    keys=self.keys, depth=self.depth, ws=self.ws_hash, key_hist=self.key_hist)
+                    keys=self.keys, depth=self.depth, ws=self.ws_hash, key_hist=self.key_hist,
+                    deepest_first=self.request)
         if self.residency == "session":
             prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
             stack_distance_session(self.prev, self.blk_off, self.session, dist_sess=self.dist, ws=self.ws_sd)
@@ -463,9 +466,6 @@ class Pipeline:
             mrc_weighted(self.dist, self.caps, self.depth, self.next if self.with_nextuse else None,
                          self.alpha, self.beta, out=self.bins, ws=self.ws_mrc)
             return
-        request_order(self.keys, self.blk_off, self.depth, keys_out=self.keys_r, depth_out=self.depth_r,
-                      ws=self.ws_ro)
-        # the reordered keys are a permutation of the hashed ones: same histogram
         prev_next_use(self.keys_r, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
         stack_distance(self.prev, self.next, self.dist, ws=self.ws_sd)
         stack_distance_req(self.prev, self.dist, self.blk_off, dist_req=self.dist_req, ws=self.ws_req)
@@ -481,7 +481,6 @@ class Pipeline:
         stages = [("hash", self.ws_hash), ("prev_next", self.ws_pn), ("stack_distance", self.ws_sd),
                   ("mrc", self.ws_mrc)]
         if self.request:
-            stages.insert(1, ("request_order", self.ws_ro))
             stages.append(("stack_distance_req", self.ws_req))
         return {name: workspace_status(ws) for name, ws in stages}
 

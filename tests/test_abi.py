@@ -52,7 +52,7 @@ FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails va
 def test_hash_rejects_bad_arguments(L):
     ws = L.pc_hash_blocks_ws(4)
     args = lambda B=16, n_seqs=4, nb=100, wsz=ws, tokens=FAKE, w=FAKE: (
-        tokens, 1000, FAKE, FAKE, n_seqs, B, None, 0, FAKE, nb, FAKE, None, None, w, wsz, None)
+        tokens, 1000, FAKE, FAKE, n_seqs, B, None, 0, FAKE, nb, FAKE, None, None, 0, w, wsz, None)
     assert L.pc_hash_blocks(*args(B=15)) == -1
     assert L.pc_hash_blocks(*args(B=0)) == -1
     assert L.pc_hash_blocks(*args(B=2048)) == -1

@@ -53,8 +53,7 @@ def full():
 
 def test_device_status_clean(full):
     _, _, p = full
-    assert p.status() == {"hash": 0, "request_order": 0, "prev_next": 0, "stack_distance": 0,
-                          "stack_distance_req": 0, "mrc": 0}
+    assert p.status() == {"hash": 0, "prev_next": 0, "stack_distance": 0, "stack_distance_req": 0, "mrc": 0}
 
 
 def test_sampled_requests_reversed(full):

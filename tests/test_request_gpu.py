@@ -97,6 +97,27 @@ def test_hand_worked_examples():
         assert list(g["dist_req"][recency_perm(blk_off, keys.size)]) == want, name
 
 
+@pytest.mark.parametrize("B", [16, 6])
+def test_hash_deepest_first_is_the_request_order(B):
+    """pc_hash_blocks with PC_HASH_DEEPEST_FIRST writes what pc_request_order
+    makes of its depth-order output (aligned fast path and any-size path)."""
+    tr = pcgen.make_trace("agent", n_sessions=60)
+    keys, depth = oracle.hash_trace(tr, B)
+    bo = tr.blk_off(B)
+    up = pc.upload_trace(tr, B)
+    h1 = torch.empty(1024, dtype=torch.int32, device="cuda")
+    h2 = torch.empty(1024, dtype=torch.int32, device="cuda")
+    k1, d1, ws = pc.hash_blocks(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"], B,
+                                key_hist=h1, deepest_first=True)
+    assert pc.workspace_status(ws) == 0
+    _, _, ws = pc.hash_blocks(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"], B,
+                              key_hist=h2)
+    perm = recency_perm(bo, keys.size)
+    assert np.array_equal(pc.as_u64(k1), keys[perm])
+    assert np.array_equal(pc.as_u32(d1), depth[perm])
+    assert torch.equal(h1, h2)
+
+
 # --------------------------------------------------------------- structure
 
 def random_requests(count, seed, sessions=(1, 6), turns=(1, 30)):
@@ -244,8 +265,7 @@ def pipeline_request(tr, caps, a, b, B=16):
                     pc.to_dev_u64(caps), B, a, b, residency="request")
     p.run()
     torch.cuda.synchronize()
-    assert p.status() == {"hash": 0, "request_order": 0, "prev_next": 0, "stack_distance": 0,
-                          "stack_distance_req": 0, "mrc": 0}
+    assert p.status() == {"hash": 0, "prev_next": 0, "stack_distance": 0, "stack_distance_req": 0, "mrc": 0}
     return p
 
 
