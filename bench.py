@@ -36,7 +36,6 @@ ALGO_BYTES = {
     "sd_dominance_pass": lambda B: 8 + 8,         # (t, acc) in and out
     "sd_local_finish": lambda B: 8 + 4 + 4,       # (t, acc), prev in; dist out
     "mrc_hist": lambda B: 12,                     # dist, depth, next in
-    "request_order": lambda B: 12 + 12,           # key, depth in; reversed copies out
     "request_distance": lambda B: 4 + 4 + 4,      # prev, per-access dist in; dist_req out
     "session_distance": lambda B: 4 + 4,          # prev in; dist_sess out
     "reuse_profile_pack": lambda B: 4 + 8,        # next in; (next, request) out
@@ -53,7 +52,7 @@ HIP_KERNEL = {"sort_onesweep_pass": "pc::sort_pass_kernel", "link_partition": "p
               "perm_partition": "pc::perm_partition_kernel", "hash_blocks": "pc::hash_fused_kernel",
               "sd_local_finish": "pc::sd_local_kernel",
               "perm_local": "pc::perm_local_kernel", "mrc_hist": "pc::mrc_hist_kernel",
-              "request_order": "pc::req_order_kernel", "request_distance": "pc::req_dist_kernel",
+              "request_distance": "pc::req_dist_kernel",
               "session_distance": "pc::sess_dist_kernel", "reuse_profile_walk": "pc::prof_walk_kernel",
               "reuse_profile_pack": "pc::prof_pack_kernel"}
 PROFILES = {"access": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9.md"),
@@ -323,13 +322,13 @@ def main():
                 "sort_digit_scan": "prev_next", "sort_onesweep_pass": "prev_next",
                 "link_partition": "prev_next",
                 "perm_partition": "prev_next", "perm_local": "prev_next", "mrc_hist": "mrc",
-                "mrc_cost": "mrc", "request_order": "request_order", "request_distance": "request_distance",
+                "mrc_cost": "mrc", "request_distance": "request_distance",
                 "session_requests": "session_profile" if args.profile else "session_distance",
                 "session_distance": "session_distance",
                 "reuse_profile_pack": "reuse_profile", "reuse_profile_walk": "reuse_profile",
                 "session_profile": "session_profile"}
     stage_bytes = {"hash": 4 * B + 8 + 4, "prev_next": 16, "stack_distance": 8,
-                   "mrc": 8 if request or session_mode else 12, "request_order": 24, "request_distance": 12,
+                   "mrc": 8 if request or session_mode else 12, "request_distance": 12,
                    "session_distance": 8, "reuse_profile": 24}
 
     def stage_name(kid):
