@@ -225,14 +225,17 @@ __global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_kernel(
 // pass therefore reserves its output runs with one global atomic per
 // (workgroup, digit) instead of a look-back, stages each tile digit-sorted
 // in LDS and writes each run contiguously.
-constexpr int LINK_THREADS = 512;
-constexpr int LINK_ITEMS = 8;                          // link: 4096-element tiles
+constexpr int LINK_THREADS = 256;
+constexpr int LINK_ITEMS = 8;                          // link: 2048-element tiles
 constexpr int LINK_TILE = LINK_THREADS * LINK_ITEMS;
 constexpr int PART_THREADS = 512;
 constexpr int PART_ITEMS = 16;                         // plain partition: 8192-element tiles
 constexpr int PERM_TILE = PART_THREADS * PART_ITEMS;   // the larger tile
-constexpr int PERM_RADIX = 1024;
+constexpr int PERM_RADIX = 1024;   // digits of a later pass (a chunk spans two earlier buckets)
+constexpr int LINK_RADIX = 512;    // digits of the first pass: at most 512 buckets
 constexpr int PERM_LOCAL_BITS = 13;
+constexpr uint64_t PERM_CHUNK_MAX = 1ull << 20;   // elements per workgroup, later passes
+constexpr uint64_t LINK_CHUNK_MAX = 1ull << 17;   // elements per workgroup, link
 
 // After the four passes over the low 32 key bits, equal keys are contiguous
 // unless different keys share those bits ("mixed" runs, a few percent of the
@@ -349,28 +352,31 @@ __device__ __forceinline__ uint32_t resolve_mixed(const uint64_t *__restrict__ s
 // element its slot inside its digit, the tile is staged digit-sorted in LDS
 // (times, then (prev, next) pairs, through a single buffer), and each
 // digit's part is appended to the workgroup's run.  Longer tiles give longer
-// runs per digit, hence fewer partially written lines; the link keeps 4096
-// because it holds keys and neighbours per element.  A chunk spans at most 1024 consecutive buckets (see the
-// plan), so digit = bucket mod 1024 names them without collision.
-template <int TILE, int THREADS>
+// runs per digit, hence fewer partially written lines; the link keeps 2048
+// because it holds keys and neighbours per element and waits on more loads:
+// four small workgroups per CU overlap those waits better than two large.  A chunk of a later pass
+// spans at most 1024 consecutive buckets (see the plan), so digit = bucket
+// mod 1024 names them without collision; the first pass has at most 512.
+template <int TILE, int THREADS, int RADIX_N>
 struct PermLds {
     uint64_t stage[TILE];   // bucket names while counting; per tile: times (as u32), then (prev, next) pairs
-    uint32_t cnt[PERM_RADIX];
-    uint32_t lstart[PERM_RADIX];
-    uint32_t cur[PERM_RADIX];
+    uint32_t cnt[RADIX_N];
+    uint32_t lstart[RADIX_N];
+    uint32_t cur[RADIX_N];
     uint32_t tmp[THREADS / WAVE];
     int32_t budget;   // positions the link may still scan for long mixed runs
     uint32_t nmixed;  // mixed-run requests of the current tile (the list lives in `stage`)
 };
 
-template <bool FROM_SORT, int PERM_THREADS, int ITEMS>
+template <bool FROM_SORT, int PERM_THREADS, int ITEMS, int RADIX_N>
 __device__ __forceinline__ void perm_partition_body(
-    PermLds<PERM_THREADS * ITEMS, PERM_THREADS> &L, const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t,
+    PermLds<PERM_THREADS * ITEMS, PERM_THREADS, RADIX_N> &L, const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t,
     const uint64_t *__restrict__ in_pn, uint64_t n, int s, uint64_t per_wg, uint32_t *__restrict__ cursor,
     uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn, bool full, int32_t *__restrict__ overflow) {
     uint32_t *s_stage = reinterpret_cast<uint32_t *>(L.stage), *s_cnt = L.cnt, *s_lstart = L.lstart,
              *s_cur = L.cur, *s_bucket = reinterpret_cast<uint32_t *>(L.stage), *s_tmp = L.tmp;
-    constexpr int DPT = PERM_RADIX / PERM_THREADS;   // digits per thread
+    static_assert(RADIX_N % PERM_THREADS == 0, "whole digits per thread");
+    constexpr int DPT = RADIX_N / PERM_THREADS;   // digits per thread
     // positions fit 32 bits (n < 2^32 - 1); offsets from a tile's base are
     // compared against what is left, so nothing wraps near the end
     if ((uint64_t)blockIdx.x * per_wg >= n) return;
@@ -379,7 +385,7 @@ __device__ __forceinline__ void perm_partition_body(
     const uint32_t hi = (uint64_t)lo + per_wg < n ? (uint32_t)(lo + per_wg) : (uint32_t)n;
 
     // ---- count the chunk's digits and reserve one run per digit
-    for (int i = tid0; i < PERM_RADIX; i += PERM_THREADS) s_cnt[i] = 0;
+    for (int i = tid0; i < RADIX_N; i += PERM_THREADS) s_cnt[i] = 0;
     if (tid0 == 0) L.budget = (int32_t)(2 * (hi - lo) + 4096);
     __syncthreads();
     // eight loads in flight per thread before their LDS updates
@@ -396,7 +402,7 @@ __device__ __forceinline__ void perm_partition_body(
             // (a time outside [0, n) can only come from inconsistent input;
             // it reserves nothing and its element is not written)
             if ((uint32_t)(q * PERM_THREADS + tid0) < left && tt[q] < n) {
-                const uint32_t d = (tt[q] >> s) & (PERM_RADIX - 1);
+                const uint32_t d = (tt[q] >> s) & (RADIX_N - 1);
                 atomicAdd(&s_cnt[d], 1u);
                 s_bucket[d] = tt[q] >> s;   // every writer of digit d writes the same bucket
             }
@@ -420,7 +426,7 @@ __device__ __forceinline__ void perm_partition_body(
         int tid = threadIdx.x;
         __asm__ volatile("" : "+v"(tid));
         const int lane = tid & (WAVE - 1);
-        for (int i = tid; i < PERM_RADIX; i += PERM_THREADS) s_cnt[i] = 0;
+        for (int i = tid; i < RADIX_N; i += PERM_THREADS) s_cnt[i] = 0;
         if (tid == 0) L.nmixed = 0;
         __syncthreads();
         // per-tile base pointers keep the per-lane offsets 32-bit.  Every
@@ -545,7 +551,7 @@ __device__ __forceinline__ void perm_partition_body(
         }
 #pragma unroll
         for (int j = 0; j < ITEMS; ++j)
-            if (ok[j]) pos[j] = atomicAdd(&s_cnt[(t[j] >> s) & (PERM_RADIX - 1)], 1u);
+            if (ok[j]) pos[j] = atomicAdd(&s_cnt[(t[j] >> s) & (RADIX_N - 1)], 1u);
         __syncthreads();
         uint32_t c[DPT], mine = 0, total;
 #pragma unroll
@@ -563,7 +569,7 @@ __device__ __forceinline__ void perm_partition_body(
 #pragma unroll
         for (int j = 0; j < ITEMS; ++j) {
             if (!ok[j]) continue;
-            pos[j] += s_lstart[(t[j] >> s) & (PERM_RADIX - 1)];
+            pos[j] += s_lstart[(t[j] >> s) & (RADIX_N - 1)];
             s_stage[pos[j]] = t[j];
         }
         __syncthreads();
@@ -575,7 +581,7 @@ __device__ __forceinline__ void perm_partition_body(
             dst[r] = ~0u;
             if (slot < total) {
                 const uint32_t tt = s_stage[slot];
-                const uint32_t d = (tt >> s) & (PERM_RADIX - 1);
+                const uint32_t d = (tt >> s) & (RADIX_N - 1);
                 dst[r] = s_cur[d] + (slot - s_lstart[d]);
                 if (dst[r] < n) out_t[dst[r]] = tt;
             }
@@ -594,26 +600,26 @@ __device__ __forceinline__ void perm_partition_body(
     }
 }
 
-// The link variant holds more state per element (keys and neighbours), so it
-// runs two workgroups per CU; the plain partition runs three.  The first link
+// The link variant holds more state per element (keys and neighbours): four
+// 256-thread workgroups per CU; the plain partition runs two of 512.  The first link
 // (over keys sorted by their low 32 bits) raises *flag when a mixed run is too
 // long to scan; the second one runs only then (only_if = flag), over fully
 // sorted keys.
-__global__ __launch_bounds__(LINK_THREADS, 4) void link_partition_kernel(
+__global__ __launch_bounds__(LINK_THREADS, 8) void link_partition_kernel(
     const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t, uint64_t n, int s, uint64_t per_wg,
     uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn,
     const int32_t *__restrict__ only_if, int32_t *__restrict__ flag) {
     if (only_if && *only_if == 0) return;
-    __shared__ PermLds<LINK_TILE, LINK_THREADS> L;
-    perm_partition_body<true, LINK_THREADS, LINK_ITEMS>(L, sk, in_t, nullptr, n, s, per_wg, cursor, out_t, out_pn, only_if != nullptr,
+    __shared__ PermLds<LINK_TILE, LINK_THREADS, LINK_RADIX> L;
+    perm_partition_body<true, LINK_THREADS, LINK_ITEMS, LINK_RADIX>(L, sk, in_t, nullptr, n, s, per_wg, cursor, out_t, out_pn, only_if != nullptr,
                               flag);
 }
 
 __global__ __launch_bounds__(PART_THREADS, 4) void perm_partition_kernel(
     const uint32_t *__restrict__ in_t, const uint64_t *__restrict__ in_pn, uint64_t n, int s, uint64_t per_wg,
     uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn) {
-    __shared__ PermLds<PERM_TILE, PART_THREADS> L;
-    perm_partition_body<false, PART_THREADS, PART_ITEMS>(L, nullptr, in_t, in_pn, n, s, per_wg, cursor, out_t, out_pn, true, nullptr);
+    __shared__ PermLds<PERM_TILE, PART_THREADS, PERM_RADIX> L;
+    perm_partition_body<false, PART_THREADS, PART_ITEMS, PERM_RADIX>(L, nullptr, in_t, in_pn, n, s, per_wg, cursor, out_t, out_pn, true, nullptr);
 }
 
 // cursor[b] = b << s: each bucket's output run starts at its first t
@@ -766,16 +772,25 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
     // between the first sort buffers ((prev, next) pairs in k1, t in v1) and,
     // once the sorted keys have been consumed, the second ones (k2, v2).
     const pc::PermPlan pp = pc::plan_perm(n);
+    if (pp.buckets[0] > (uint64_t)pc::LINK_RADIX) return PC_ERR_TOO_LARGE;   // the plan never splits wider
     uint32_t *bt[2] = {w.v1, w.v2};
     uint64_t *bpn[2] = {w.k1, w.k2};
-    // chunks of at most 2^20 elements: small enough that a chunk of a later
-    // pass spans at most two buckets of the previous one, large enough that
-    // each bucket cursor sees few atomics
-    uint64_t per_wg = (n + (uint64_t)cus * 2 - 1) / ((uint64_t)cus * 2);
-    per_wg = (per_wg + pc::PERM_TILE - 1) / pc::PERM_TILE * pc::PERM_TILE;
-    if (per_wg > (1ull << 20)) per_wg = 1ull << 20;
-    if (per_wg < (uint64_t)pc::PERM_TILE) per_wg = pc::PERM_TILE;
+    // Chunks of a later pass hold at most 2^20 elements: small enough that
+    // one spans at most two buckets of the previous pass, large enough that
+    // each bucket cursor sees few atomics.  The link's chunks are smaller:
+    // the runs that its workgroups in flight append to then lie closer
+    // together, and the link, which waits on more loads per element than
+    // the plain partition, gains from that.
+    auto chunk = [&](uint64_t cap, uint64_t tile) {
+        uint64_t c = (n + (uint64_t)cus * 2 - 1) / ((uint64_t)cus * 2);
+        c = (c + tile - 1) / tile * tile;
+        if (c > cap) c = cap;
+        return c < tile ? tile : c;
+    };
+    const uint64_t per_wg = chunk(pc::PERM_CHUNK_MAX, pc::PERM_TILE);
     const unsigned ptiles = (unsigned)((n + per_wg - 1) / per_wg);
+    const uint64_t per_wg_link = chunk(pc::LINK_CHUNK_MAX, pc::LINK_TILE);
+    const unsigned ltiles = (unsigned)((n + per_wg_link - 1) / per_wg_link);
     const unsigned cg0 = (unsigned)((pp.buckets[0] + 255) / 256);
 
     const uint64_t *kin = keys;
@@ -785,8 +800,8 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
             // first link, over keys sorted by their low 32 bits
             PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg0), dim3(256), 0, s, w.cursor, pp.buckets[0],
                       pp.s[0]);
-            PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ptiles), dim3(pc::LINK_THREADS), 0, s, kin, vin,
-                      n, pp.s[0], per_wg, w.cursor, bt[0], bpn[0], (const int32_t *)nullptr, need_high);
+            PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ltiles), dim3(pc::LINK_THREADS), 0, s, kin, vin,
+                      n, pp.s[0], per_wg_link, w.cursor, bt[0], bpn[0], (const int32_t *)nullptr, need_high);
             PC_LAUNCH(pc::K_SORT_HIST, pc::sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n,
                       pc::SORT_PASSES / 2, w.hist, (const int32_t *)need_high);
             PC_LAUNCH(pc::K_SORT_SCAN, pc::sort_scan_kernel, dim3(1), dim3(pc::RADIX), 0, s,
@@ -803,8 +818,8 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
     }
     // second link, over fully sorted keys, only if the first one gave up
     PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg0), dim3(256), 0, s, w.cursor, pp.buckets[0], pp.s[0]);
-    PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ptiles), dim3(pc::LINK_THREADS), 0, s, kin, vin, n,
-              pp.s[0], per_wg, w.cursor, bt[0], bpn[0], (const int32_t *)need_high, (int32_t *)nullptr);
+    PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ltiles), dim3(pc::LINK_THREADS), 0, s, kin, vin, n,
+              pp.s[0], per_wg_link, w.cursor, bt[0], bpn[0], (const int32_t *)need_high, (int32_t *)nullptr);
     int cur = 0;
     for (int i = 1; i < pp.passes; ++i) {
         const unsigned cg = (unsigned)((pp.buckets[i] + 255) / 256);
