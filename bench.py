@@ -219,12 +219,18 @@ def main():
                          "1e6 with --residency request)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 4 GiB device copy (for rocprof counter calibration)")
+    ap.add_argument("--settle", type=float, default=20.0,
+                    help="seconds to wait before touching the device (memory that another process "
+                         "released just before is reclaimed in the background meanwhile)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the hot path here is single-GPU "
               "(multi-GPU sharding is a design note, not built); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
+    if args.settle > 0:
+        log("waiting %.0f s before touching the device" % args.settle)
+        time.sleep(args.settle)
     import torch
     import pcgen
     from paper_2609_28870_amd import pc

@@ -345,18 +345,22 @@ __device__ __forceinline__ uint32_t resolve_mixed(const uint64_t *__restrict__ s
     return res;
 }
 
-// One workgroup owns a contiguous chunk of the input.  It first counts the
-// chunk's digits, reserves one run per digit in the bucket's output range with
-// a single global atomic (so each bucket cursor sees one atomic per workgroup,
-// not per tile), then streams the chunk tile by tile: LDS counters give each
-// element its slot inside its digit, the tile is staged digit-sorted in LDS
-// (times, then (prev, next) pairs, through a single buffer), and each
-// digit's part is appended to the workgroup's run.  Longer tiles give longer
-// runs per digit, hence fewer partially written lines; the link keeps 2048
-// because it holds keys and neighbours per element and waits on more loads:
-// four small workgroups per CU overlap those waits better than two large.  A chunk of a later pass
-// spans at most 1024 consecutive buckets (see the plan), so digit = bucket
-// mod 1024 names them without collision; the first pass has at most 512.
+// One workgroup owns a contiguous chunk of the input and streams it tile by
+// tile: LDS counters give each element its slot inside its digit, the tile
+// is staged digit-sorted in LDS (times, then (prev, next) pairs, through a
+// single buffer), and each digit's part is appended to a run reserved in the
+// bucket's output range.  The link reserves once per chunk: it first counts
+// the chunk's digits and takes one run per digit with a single global atomic,
+// so each bucket cursor sees one atomic per workgroup and the runs a
+// workgroup appends to stay few and long.  Later passes skip that extra read
+// of t and reserve per tile (their tiles are four times larger, so the runs
+// stay long enough).  Longer tiles give longer runs per digit, hence fewer
+// partially written lines; the link keeps 2048 because it holds keys and
+// neighbours per element and waits on more loads: four small workgroups per
+// CU overlap those waits better than two large.  A tile or chunk of a later
+// pass spans at most 1024 consecutive buckets (see the plan), so digit =
+// bucket mod 1024 names them without collision; the first pass has at most
+// 512.
 template <int TILE, int THREADS, int RADIX_N>
 struct PermLds {
     uint64_t stage[TILE];   // bucket names while counting; per tile: times (as u32), then (prev, next) pairs
@@ -368,7 +372,7 @@ struct PermLds {
     uint32_t nmixed;  // mixed-run requests of the current tile (the list lives in `stage`)
 };
 
-template <bool FROM_SORT, int PERM_THREADS, int ITEMS, int RADIX_N>
+template <bool FROM_SORT, int PERM_THREADS, int ITEMS, int RADIX_N, bool PER_TILE>
 __device__ __forceinline__ void perm_partition_body(
     PermLds<PERM_THREADS * ITEMS, PERM_THREADS, RADIX_N> &L, const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t,
     const uint64_t *__restrict__ in_pn, uint64_t n, int s, uint64_t per_wg, uint32_t *__restrict__ cursor,
@@ -376,6 +380,9 @@ __device__ __forceinline__ void perm_partition_body(
     uint32_t *s_stage = reinterpret_cast<uint32_t *>(L.stage), *s_cnt = L.cnt, *s_lstart = L.lstart,
              *s_cur = L.cur, *s_bucket = reinterpret_cast<uint32_t *>(L.stage), *s_tmp = L.tmp;
     static_assert(RADIX_N % PERM_THREADS == 0, "whole digits per thread");
+    // per-tile bucket names live in the stage buffer, which the link's
+    // mixed-run list also uses
+    static_assert(!(PER_TILE && FROM_SORT), "the link reserves per chunk");
     constexpr int DPT = RADIX_N / PERM_THREADS;   // digits per thread
     // positions fit 32 bits (n < 2^32 - 1); offsets from a tile's base are
     // compared against what is left, so nothing wraps near the end
@@ -384,10 +391,11 @@ __device__ __forceinline__ void perm_partition_body(
     const uint32_t lo = (uint32_t)((uint64_t)blockIdx.x * per_wg);
     const uint32_t hi = (uint64_t)lo + per_wg < n ? (uint32_t)(lo + per_wg) : (uint32_t)n;
 
-    // ---- count the chunk's digits and reserve one run per digit
+    // ---- (per chunk) count the chunk's digits and reserve one run per digit
     for (int i = tid0; i < RADIX_N; i += PERM_THREADS) s_cnt[i] = 0;
     if (tid0 == 0) L.budget = (int32_t)(2 * (hi - lo) + 4096);
     __syncthreads();
+    if constexpr (!PER_TILE) {
     // eight loads in flight per thread before their LDS updates
     for (uint32_t b0 = lo; b0 < hi; b0 += 8 * PERM_THREADS) {
         const uint32_t left = hi - b0;
@@ -416,6 +424,7 @@ __device__ __forceinline__ void perm_partition_body(
         if (c) s_cur[d] = atomicAdd(&cursor[s_bucket[d]], c);
     }
     __syncthreads();
+    }
 
     // ---- stream the chunk tile by tile
     constexpr int TILE = PERM_THREADS * ITEMS;
@@ -550,8 +559,15 @@ __device__ __forceinline__ void perm_partition_body(
             }
         }
 #pragma unroll
-        for (int j = 0; j < ITEMS; ++j)
-            if (ok[j]) pos[j] = atomicAdd(&s_cnt[(t[j] >> s) & (RADIX_N - 1)], 1u);
+        for (int j = 0; j < ITEMS; ++j) {
+            // (per tile: a time outside [0, n), from inconsistent input,
+            // reserves nothing and is not written)
+            if (PER_TILE) ok[j] = ok[j] && t[j] < n;
+            if (ok[j]) {
+                pos[j] = atomicAdd(&s_cnt[(t[j] >> s) & (RADIX_N - 1)], 1u);
+                if (PER_TILE) s_bucket[(t[j] >> s) & (RADIX_N - 1)] = t[j] >> s;
+            }
+        }
         __syncthreads();
         uint32_t c[DPT], mine = 0, total;
 #pragma unroll
@@ -564,6 +580,7 @@ __device__ __forceinline__ void perm_partition_body(
         for (int q = 0; q < DPT; ++q) {
             s_lstart[tid * DPT + q] = run;
             run += c[q];
+            if (PER_TILE && c[q]) s_cur[tid * DPT + q] = atomicAdd(&cursor[s_bucket[tid * DPT + q]], c[q]);
         }
         __syncthreads();
 #pragma unroll
@@ -594,8 +611,9 @@ __device__ __forceinline__ void perm_partition_body(
 #pragma unroll
         for (int r = 0; r < ITEMS; ++r)
             if (dst[r] < n) out_pn[dst[r]] = L.stage[tid + r * PERM_THREADS];
+        if (!PER_TILE)
 #pragma unroll
-        for (int q = 0; q < DPT; ++q) s_cur[tid * DPT + q] += c[q];
+            for (int q = 0; q < DPT; ++q) s_cur[tid * DPT + q] += c[q];
         __syncthreads();
     }
 }
@@ -611,7 +629,7 @@ __global__ __launch_bounds__(LINK_THREADS, 8) void link_partition_kernel(
     const int32_t *__restrict__ only_if, int32_t *__restrict__ flag) {
     if (only_if && *only_if == 0) return;
     __shared__ PermLds<LINK_TILE, LINK_THREADS, LINK_RADIX> L;
-    perm_partition_body<true, LINK_THREADS, LINK_ITEMS, LINK_RADIX>(L, sk, in_t, nullptr, n, s, per_wg, cursor, out_t, out_pn, only_if != nullptr,
+    perm_partition_body<true, LINK_THREADS, LINK_ITEMS, LINK_RADIX, false>(L, sk, in_t, nullptr, n, s, per_wg, cursor, out_t, out_pn, only_if != nullptr,
                               flag);
 }
 
@@ -619,7 +637,7 @@ __global__ __launch_bounds__(PART_THREADS, 4) void perm_partition_kernel(
     const uint32_t *__restrict__ in_t, const uint64_t *__restrict__ in_pn, uint64_t n, int s, uint64_t per_wg,
     uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn) {
     __shared__ PermLds<PERM_TILE, PART_THREADS, PERM_RADIX> L;
-    perm_partition_body<false, PART_THREADS, PART_ITEMS, PERM_RADIX>(L, nullptr, in_t, in_pn, n, s, per_wg, cursor, out_t, out_pn, true, nullptr);
+    perm_partition_body<false, PART_THREADS, PART_ITEMS, PERM_RADIX, true>(L, nullptr, in_t, in_pn, n, s, per_wg, cursor, out_t, out_pn, true, nullptr);
 }
 
 // cursor[b] = b << s: each bucket's output run starts at its first t
