@@ -223,37 +223,55 @@ __device__ __forceinline__ void load_tile(const TileLoc &L, const uint32_t *__re
 // the segmented scan over tiles.  Only counts are needed here, so instead of
 // ranking lanes each run of equal digits in a 64-lane chunk (runs are long at
 // the top levels, where t grows with v) adds its length with one LDS atomic.
+// A workgroup takes COUNT_TPW consecutive tiles and issues every lookup and
+// load of all of them before counting: one tile's work is too short to
+// cover the chain of dependent loads (tile -> bucket -> range -> elements).
+constexpr int COUNT_TPW = 4;
 template <bool FIRST>
 __global__ __launch_bounds__(DOM_THREADS) void sd_count_kernel(
     const uint32_t *__restrict__ in_t, uint64_t n, const uint32_t *__restrict__ Zc, int s, int k,
     const uint32_t *__restrict__ tfirst, uint64_t nbuckets, const uint32_t *__restrict__ tile_bucket,
     uint16_t *__restrict__ cnt, uint8_t *__restrict__ seg) {
-    __shared__ uint32_t s_cnt[DOM_RADIX];
+    __shared__ uint32_t s_cnt[COUNT_TPW][DOM_RADIX];
     const int tid = threadIdx.x, lane = tid & (WAVE - 1), w = tid / WAVE;
-    const uint64_t tile = blockIdx.x;
-    const TileLoc L = locate_tile<FIRST>(tile, n, Zc, s + k, tfirst, nbuckets, tile_bucket);
-    if (!L.valid) return;
-    if (tid < DOM_RADIX) s_cnt[tid] = 0;
-    uint32_t t[DOM_CHUNKS_PER_WAVE], acc[DOM_CHUNKS_PER_WAVE];
-    bool ok[DOM_CHUNKS_PER_WAVE];
-    load_tile<FIRST>(L, in_t, nullptr, w, lane, t, acc, ok, false);
+    const uint64_t tile0 = (uint64_t)blockIdx.x * COUNT_TPW;
+    // an invalid tile (past the level's last) has an empty range: it loads
+    // nothing, and every later tile is invalid too
+    TileLoc L[COUNT_TPW];
+#pragma unroll
+    for (int q = 0; q < COUNT_TPW; ++q)
+        L[q] = locate_tile<FIRST>(tile0 + q, n, Zc, s + k, tfirst, nbuckets, tile_bucket);
+    if (!L[0].valid) return;
+    for (int i = tid; i < COUNT_TPW * DOM_RADIX; i += DOM_THREADS) (&s_cnt[0][0])[i] = 0;
+    uint32_t t[COUNT_TPW][DOM_CHUNKS_PER_WAVE], acc[DOM_CHUNKS_PER_WAVE];
+    bool ok[COUNT_TPW][DOM_CHUNKS_PER_WAVE];
+#pragma unroll
+    for (int q = 0; q < COUNT_TPW; ++q) load_tile<FIRST>(L[q], in_t, nullptr, w, lane, t[q], acc, ok[q], false);
     __syncthreads();
     const uint32_t dmask = (1u << k) - 1u;
 #pragma unroll
-    for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
-        // invalid lanes take digit RADIX (never counted) so they end runs
-        const uint32_t d = ok[i] ? (t[i] >> s) & dmask : (uint32_t)DOM_RADIX;
-        const uint32_t dl = from_lower(d);   // lane 0 keeps its own and is a head anyway
-        const bool head = lane == 0 || dl != d;
-        const uint64_t heads = ballot(head);
-        // next head above this lane (or 64): the run is [lane, next)
-        const uint64_t above = lane == WAVE - 1 ? 0ull : heads & (~0ull << (lane + 1));
-        const uint32_t next = above ? (uint32_t)__builtin_ctzll(above) : (uint32_t)WAVE;
-        if (head && d < (uint32_t)DOM_RADIX) atomicAdd(&s_cnt[d], next - (uint32_t)lane);
+    for (int q = 0; q < COUNT_TPW; ++q) {
+#pragma unroll
+        for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
+            // invalid lanes take digit RADIX (never counted) so they end runs
+            const uint32_t d = ok[q][i] ? (t[q][i] >> s) & dmask : (uint32_t)DOM_RADIX;
+            const uint32_t dl = from_lower(d);   // lane 0 keeps its own and is a head anyway
+            const bool head = lane == 0 || dl != d;
+            const uint64_t heads = ballot(head);
+            // next head above this lane (or 64): the run is [lane, next)
+            const uint64_t above = lane == WAVE - 1 ? 0ull : heads & (~0ull << (lane + 1));
+            const uint32_t next = above ? (uint32_t)__builtin_ctzll(above) : (uint32_t)WAVE;
+            if (head && d < (uint32_t)DOM_RADIX) atomicAdd(&s_cnt[q][d], next - (uint32_t)lane);
+        }
     }
     __syncthreads();
-    if (tid < DOM_RADIX) cnt[tile * DOM_RADIX + tid] = (uint16_t)s_cnt[tid];
-    if (tid == 0) seg[tile] = FIRST ? (tile == 0) : (tile == L.first_tile);
+#pragma unroll
+    for (int q = 0; q < COUNT_TPW; ++q) {
+        if (!L[q].valid) break;
+        const uint64_t tile = tile0 + q;
+        if (tid < DOM_RADIX) cnt[tile * DOM_RADIX + tid] = (uint16_t)s_cnt[q][tid];
+        if (tid == 0) seg[tile] = FIRST ? (tile == 0) : (tile == L[q].first_tile);
+    }
 }
 
 // Segmented exclusive scan over tiles, per digit (a bucket's first tile
@@ -835,10 +853,11 @@ static pc_status sd_levels(const uint32_t *first, uint64_t n, const SdPlan &p, S
         uint32_t *da = (i & 1) ? w.ba : w.aa;
         const int S = p.s[i] + p.k[i];
         const unsigned grid = (unsigned)p.grid[i];
+        const unsigned cgrid = (unsigned)((p.grid[i] + COUNT_TPW - 1) / COUNT_TPW);
         const unsigned groups = (unsigned)((p.grid[i] + SEG_GROUP - 1) / SEG_GROUP);
         const uint64_t fixed = (n + DOM_TILE - 1) / DOM_TILE;
         if (i == 0) {
-            PC_LAUNCH(K_SD_COUNT, sd_count_kernel<true>, dim3(grid), dim3(DOM_THREADS), 0, s, first, n, w.Zc,
+            PC_LAUNCH(K_SD_COUNT, sd_count_kernel<true>, dim3(cgrid), dim3(DOM_THREADS), 0, s, first, n, w.Zc,
                       p.s[i], p.k[i], (const uint32_t *)nullptr, (uint64_t)1, (const uint32_t *)nullptr, w.cnt,
                       w.seg);
         } else {
@@ -848,7 +867,7 @@ static pc_status sd_levels(const uint32_t *first, uint64_t n, const SdPlan &p, S
             PC_LAUNCH(K_SD_SCAN, sd_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, s, w.tcount, nb, w.tfirst);
             PC_LAUNCH(K_SD_TILES, sd_tile_bucket_kernel, dim3((unsigned)((p.grid[i] + 255) / 256)), dim3(256), 0,
                       s, w.tfirst, nb, p.grid[i], w.tile_bucket);
-            PC_LAUNCH(K_SD_COUNT, sd_count_kernel<false>, dim3(grid), dim3(DOM_THREADS), 0, s, src_t, n, w.Zc,
+            PC_LAUNCH(K_SD_COUNT, sd_count_kernel<false>, dim3(cgrid), dim3(DOM_THREADS), 0, s, src_t, n, w.Zc,
                       p.s[i], p.k[i], w.tfirst, nb, w.tile_bucket, w.cnt, w.seg);
         }
         const uint32_t *tend = i == 0 ? nullptr : w.tfirst + p.nbuckets[i];
