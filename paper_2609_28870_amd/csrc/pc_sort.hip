@@ -232,10 +232,10 @@ constexpr int PART_THREADS = 512;
 constexpr int PART_ITEMS = 16;                         // plain partition: 8192-element tiles
 constexpr int PERM_TILE = PART_THREADS * PART_ITEMS;   // the larger tile
 constexpr int PERM_RADIX = 1024;   // digits of a later pass (a chunk spans two earlier buckets)
-constexpr int LINK_RADIX = 512;    // digits of the first pass: at most 512 buckets
-constexpr int PERM_LOCAL_BITS = 13;
+constexpr int LINK_RADIX = 256;    // digits of the first pass: at most 256 buckets
+constexpr int PERM_LOCAL_BITS = 14;
 constexpr uint64_t PERM_CHUNK_MAX = 1ull << 20;   // elements per workgroup, later passes
-constexpr uint64_t LINK_CHUNK_MAX = 1ull << 17;   // elements per workgroup, link
+constexpr uint64_t LINK_CHUNK_MAX = 1ull << 16;   // elements per workgroup, link
 
 // After the four passes over the low 32 key bits, equal keys are contiguous
 // unless different keys share those bits ("mixed" runs, a few percent of the
@@ -360,7 +360,7 @@ __device__ __forceinline__ uint32_t resolve_mixed(const uint64_t *__restrict__ s
 // CU overlap those waits better than two large.  A tile or chunk of a later
 // pass spans at most 1024 consecutive buckets (see the plan), so digit =
 // bucket mod 1024 names them without collision; the first pass has at most
-// 512.
+// 256.
 template <int TILE, int THREADS, int RADIX_N>
 struct PermLds {
     uint64_t stage[TILE];   // bucket names while counting; per tile: times (as u32), then (prev, next) pairs
@@ -623,7 +623,7 @@ __device__ __forceinline__ void perm_partition_body(
 // (over keys sorted by their low 32 bits) raises *flag when a mixed run is too
 // long to scan; the second one runs only then (only_if = flag), over fully
 // sorted keys.
-__global__ __launch_bounds__(LINK_THREADS, 8) void link_partition_kernel(
+__global__ __launch_bounds__(LINK_THREADS, 4) void link_partition_kernel(
     const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t, uint64_t n, int s, uint64_t per_wg,
     uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn,
     const int32_t *__restrict__ only_if, int32_t *__restrict__ flag) {
@@ -646,9 +646,10 @@ __global__ void perm_cursor_kernel(uint32_t *__restrict__ cursor, uint64_t nb, i
     if (b < nb) cursor[b] = (uint32_t)(b << s);
 }
 
-// every 8192-range of t holds exactly its own triples: place the (prev,
-// next) pairs by t in LDS and write prev / next in time order
-constexpr int LOCAL_THREADS = 512;
+// every 16384-range of t holds exactly its own triples: place the (prev,
+// next) pairs by t in LDS (128 KB, one 1024-thread workgroup per CU) and
+// write prev / next in time order
+constexpr int LOCAL_THREADS = 1024;
 __global__ __launch_bounds__(LOCAL_THREADS) void perm_local_kernel(const uint32_t *__restrict__ in_t,
                                                                    const uint64_t *__restrict__ in_pn,
                                                                    uint64_t n, uint32_t *__restrict__ prev,
@@ -691,11 +692,11 @@ struct SortWs {
 };
 
 // Partition plan for the way back to time order.  The last step uses
-// 8192-ranges of t.  Every pass splits into at most 512 buckets, so a
-// workgroup chunk (at most 2^20 elements, smaller than any earlier bucket of
-// >= 2^22) spans at most two earlier buckets, i.e. at most 1024 consecutive
-// buckets of its own pass, and (bucket mod 1024) names them without collision
-// inside the chunk.
+// 16384-ranges of t.  The link splits into at most 256 buckets, later passes
+// into at most 512 per earlier bucket.  Every bucket is at least 16384 wide,
+// so a tile of a later pass (8192 elements) spans at most two earlier
+// buckets, i.e. at most 1024 consecutive buckets of its own pass, and
+// (bucket mod 1024) names them without collision inside the tile.
 struct PermPlan {
     int passes;
     int s[4];
@@ -710,8 +711,9 @@ static PermPlan plan_perm(uint64_t n) {
     int hi = nbits;   // bits above PERM_LOCAL_BITS still to split
     int cur = nbits;
     int shifts[4], k = 0;
-    // up to 9 bits per pass: longer runs per tile and bucket than 10
-    int width = 9;
+    // 8 bits in the link (its tiles are small), up to 9 in later passes:
+    // longer runs per tile and bucket than 10
+    int width = 8;
     while (cur > PERM_LOCAL_BITS && k < 4) {
         int next_s = cur - width > PERM_LOCAL_BITS ? cur - width : PERM_LOCAL_BITS;
         shifts[k++] = next_s;
@@ -793,12 +795,12 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
     if (pp.buckets[0] > (uint64_t)pc::LINK_RADIX) return PC_ERR_TOO_LARGE;   // the plan never splits wider
     uint32_t *bt[2] = {w.v1, w.v2};
     uint64_t *bpn[2] = {w.k1, w.k2};
-    // Chunks of a later pass hold at most 2^20 elements: small enough that
-    // one spans at most two buckets of the previous pass, large enough that
-    // each bucket cursor sees few atomics.  The link's chunks are smaller:
-    // the runs that its workgroups in flight append to then lie closer
-    // together, and the link, which waits on more loads per element than
-    // the plain partition, gains from that.
+    // Work per workgroup: later passes take chunks of up to 2^20 elements
+    // (they reserve per tile, so the chunk only spreads the work).  The
+    // link reserves per chunk and its chunks are smaller: the runs that its
+    // workgroups in flight append to then lie closer together, and the
+    // link, which waits on more loads per element than the plain
+    // partition, gains from that.
     auto chunk = [&](uint64_t cap, uint64_t tile) {
         uint64_t c = (n + (uint64_t)cus * 2 - 1) / ((uint64_t)cus * 2);
         c = (c + tile - 1) / tile * tile;
