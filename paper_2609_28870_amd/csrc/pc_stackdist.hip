@@ -563,8 +563,19 @@ __global__ __launch_bounds__(LOC_THREADS, 6) void sd_local_kernel(
     }
     const uint32_t tofs = (uint32_t)tid * PER;
     const uint64_t tbase = r0 + tofs;
+    // a full range with aligned bases moves prev and D as two 16-byte
+    // vectors per thread
+    const bool vec = nt == LOCAL_SPAN && ((reinterpret_cast<uintptr_t>(pb) | reinterpret_cast<uintptr_t>(dist + r0)) & 15) == 0;
+    static_assert(PER == 8, "two 16-byte vectors per thread");
+    if (vec) {
+        const uint4 a = reinterpret_cast<const uint4 *>(pb + tofs)[0];
+        const uint4 b = reinterpret_cast<const uint4 *>(pb + tofs)[1];
+        p[0] = a.x; p[1] = a.y; p[2] = a.z; p[3] = a.w;
+        p[4] = b.x; p[5] = b.y; p[6] = b.z; p[7] = b.w;
+    } else {
 #pragma unroll
-    for (int j = 0; j < PER; ++j) p[j] = pb[tofs + j < nt ? tofs + j : 0u];
+        for (int j = 0; j < PER; ++j) p[j] = pb[tofs + j < nt ? tofs + j : 0u];
+    }
     __syncthreads();   // chunk histograms zeroed
 
     // ---- level A: digit = bits 6..11 of t, chunks of 64 in v order
@@ -643,17 +654,23 @@ __global__ __launch_bounds__(LOC_THREADS, 6) void sd_local_kernel(
     for (int j = 0; j < PER; ++j) cold += (tbase + j < n && p[j] == NONE) ? 1u : 0u;
     uint32_t allcold;
     uint32_t z = Zc[blockIdx.x] + block_excl_scan(cold, s_tmp, &allcold);
+    uint32_t dv[PER];
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
-        const uint64_t tt = tbase + j;
-        if (tt < n) {
-            if (p[j] == NONE) {
-                dist[tt] = NONE;
-                ++z;
-            } else {
-                dist[tt] = z + slot[tt - r0] - (p[j] + 1u);
-            }
+        if (p[j] == NONE) {
+            dv[j] = NONE;
+            ++z;
+        } else {
+            dv[j] = z + slot[(tofs + j) & (LOCAL_SPAN - 1)] - (p[j] + 1u);
         }
+    }
+    if (vec) {
+        reinterpret_cast<uint4 *>(dist + tbase)[0] = make_uint4(dv[0], dv[1], dv[2], dv[3]);
+        reinterpret_cast<uint4 *>(dist + tbase)[1] = make_uint4(dv[4], dv[5], dv[6], dv[7]);
+    } else {
+#pragma unroll
+        for (int j = 0; j < PER; ++j)
+            if (tbase + j < n) dist[tbase + j] = dv[j];
     }
 }
 
