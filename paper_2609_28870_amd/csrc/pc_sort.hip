@@ -379,11 +379,14 @@ __device__ __forceinline__ void perm_partition_body(
     uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn, bool full, int32_t *__restrict__ overflow) {
     uint32_t *s_stage = reinterpret_cast<uint32_t *>(L.stage), *s_cnt = L.cnt, *s_lstart = L.lstart,
              *s_cur = L.cur, *s_bucket = reinterpret_cast<uint32_t *>(L.stage), *s_tmp = L.tmp;
-    static_assert(RADIX_N % PERM_THREADS == 0, "whole digits per thread");
+    static_assert(RADIX_N % PERM_THREADS == 0 || PERM_THREADS % RADIX_N == 0, "whole digits per thread");
     // per-tile bucket names live in the stage buffer, which the link's
     // mixed-run list also uses
     static_assert(!(PER_TILE && FROM_SORT), "the link reserves per chunk");
-    constexpr int DPT = RADIX_N / PERM_THREADS;   // digits per thread
+    // digits per thread; with fewer digits than threads, threads below
+    // RADIX_N own one digit each
+    constexpr int DPT = RADIX_N >= PERM_THREADS ? RADIX_N / PERM_THREADS : 1;
+    const bool owner = (int)threadIdx.x * DPT < RADIX_N;
     // positions fit 32 bits (n < 2^32 - 1); offsets from a tile's base are
     // compared against what is left, so nothing wraps near the end
     if ((uint64_t)blockIdx.x * per_wg >= n) return;
@@ -418,7 +421,7 @@ __device__ __forceinline__ void perm_partition_body(
     }
     __syncthreads();
 #pragma unroll
-    for (int q = 0; q < DPT; ++q) {
+    for (int q = 0; q < DPT && owner; ++q) {
         const int d = tid0 * DPT + q;
         const uint32_t c = s_cnt[d];
         if (c) s_cur[d] = atomicAdd(&cursor[s_bucket[d]], c);
@@ -572,12 +575,12 @@ __device__ __forceinline__ void perm_partition_body(
         uint32_t c[DPT], mine = 0, total;
 #pragma unroll
         for (int q = 0; q < DPT; ++q) {
-            c[q] = s_cnt[tid * DPT + q];
+            c[q] = owner ? s_cnt[tid * DPT + q] : 0u;
             mine += c[q];
         }
         uint32_t run = block_excl_scan(mine, s_tmp, &total);
 #pragma unroll
-        for (int q = 0; q < DPT; ++q) {
+        for (int q = 0; q < DPT && owner; ++q) {
             s_lstart[tid * DPT + q] = run;
             run += c[q];
             if (PER_TILE && c[q]) s_cur[tid * DPT + q] = atomicAdd(&cursor[s_bucket[tid * DPT + q]], c[q]);
@@ -613,7 +616,8 @@ __device__ __forceinline__ void perm_partition_body(
             if (dst[r] < n) out_pn[dst[r]] = L.stage[tid + r * PERM_THREADS];
         if (!PER_TILE)
 #pragma unroll
-            for (int q = 0; q < DPT; ++q) s_cur[tid * DPT + q] += c[q];
+            for (int q = 0; q < DPT; ++q)
+                if (owner) s_cur[tid * DPT + q] += c[q];
         __syncthreads();
     }
 }

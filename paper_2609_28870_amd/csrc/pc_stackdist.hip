@@ -404,10 +404,14 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     const uint32_t *__restrict__ Zc, int s, int k, const uint32_t *__restrict__ tfirst,
     uint64_t nbuckets, const uint32_t *__restrict__ tile_bucket, const uint32_t *__restrict__ pre,
     int32_t *__restrict__ err) {
-    __shared__ uint16_t s_h[DOM_CHUNKS][DOM_RADIX];     // chunk histograms -> column prefix
+    // chunk histograms -> column prefix; once every position is known, the
+    // staged tile (t, then acc) in the same space: 36 KB of LDS in all, so
+    // four workgroups share a CU
+    __shared__ uint16_t s_h[DOM_CHUNKS][DOM_RADIX];
     __shared__ uint16_t s_pl[DOM_CHUNKS][DOM_RADIX];    // 2-D prefix (earlier chunks, smaller digit)
-    __shared__ uint32_t s_st[DOM_TILE];                 // staged t
-    __shared__ uint32_t s_sa[DOM_TILE];                 // staged acc
+    static_assert(sizeof(s_h) >= 2 * DOM_TILE * sizeof(uint32_t), "the stage fits the histograms");
+    uint32_t *s_st = reinterpret_cast<uint32_t *>(&s_h[0][0]);   // staged t
+    uint32_t *s_sa = s_st + DOM_TILE;                           // staged acc
     // per-digit tile starts and smaller-digit counts; before that, the two
     // half sums of the column prefix
     __shared__ uint32_t s_part[2][DOM_RADIX];
@@ -496,14 +500,22 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     __syncthreads();
 
     // ---- stage the tile digit-partitioned, with the level's count added
+    uint32_t pj[DOM_CHUNKS_PER_WAVE];
 #pragma unroll
     for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
         if (ok[i]) {
             const int c = w * DOM_CHUNKS_PER_WAVE + i;
             const uint32_t d = (t[i] >> s) & dmask;
-            const uint32_t j = s_lstart[d] + s_h[c][d] + q_ic[i];
-            s_st[j] = t[i];
-            s_sa[j] = acc[i] + s_gl[d] + s_pl[c][d] + l_ic[i];
+            pj[i] = s_lstart[d] + s_h[c][d] + q_ic[i];
+            acc[i] += s_gl[d] + s_pl[c][d] + l_ic[i];
+        }
+    }
+    __syncthreads();   // the histograms are read: their space becomes the stage
+#pragma unroll
+    for (int i = 0; i < DOM_CHUNKS_PER_WAVE; ++i) {
+        if (ok[i]) {
+            s_st[pj[i]] = t[i];
+            s_sa[pj[i]] = acc[i];
         }
     }
     __syncthreads();
