@@ -222,9 +222,10 @@ __global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_kernel(
 // triples with t in [a, b) fill exactly positions [a, b) once they are
 // partitioned by the top bits of t; the order inside a range does not matter
 // because the last step places every triple at its own t.  Each partition
-// pass therefore reserves its output runs with one global atomic per
-// (workgroup, digit) instead of a look-back, stages each tile digit-sorted
-// in LDS and writes each run contiguously.
+// pass therefore reserves its output runs with global atomics on per-bucket
+// cursors (per workgroup chunk in the link, per tile later; see below)
+// instead of a look-back, stages each tile digit-sorted in LDS and writes
+// each run contiguously.
 constexpr int LINK_THREADS = 256;
 constexpr int LINK_ITEMS = 8;                          // link: 2048-element tiles
 constexpr int LINK_TILE = LINK_THREADS * LINK_ITEMS;
