@@ -230,7 +230,8 @@ def stream(kind, n, seed=0):
     return pcgen.random_keys(n, max(n // 10, 1), seed)
 
 
-@pytest.mark.parametrize("n", [0, 1, 2, 3, 63, 64, 65, 2047, 2048, 2049, 4095, 4096, 4097, 8193])
+@pytest.mark.parametrize("n", [0, 1, 2, 3, 63, 64, 65, 2047, 2048, 2049, 4095, 4096, 4097, 8193, 16383, 16384,
+                               16385])
 def test_small_and_ragged_sizes(n):
     check_keys_path(stream("mixed", n, n), caps=np.array([1, 2, 5, 100, 1000], np.uint64),
                     label="ragged%d" % n)
@@ -248,7 +249,9 @@ def test_degenerate_streams(kind):
     assert LAST_HIGH_KEY[0] == (kind == "lowsame"), kind
 
 
-@pytest.mark.parametrize("n", [(1 << 20) + 12345, (1 << 21) - 1])
+# 2^22 + 777 and 2^23 + 5 give the way back to time order a second
+# partition pass of one and two bits after the link's eight
+@pytest.mark.parametrize("n", [(1 << 20) + 12345, (1 << 21) - 1, (1 << 22) + 777, (1 << 23) + 5])
 def test_two_level_sizes(n):
     check_keys_path(stream("mixed", n, 9), label="twolevel%d" % n)
 
