@@ -158,10 +158,12 @@ pc_status pc_stack_distance(const uint32_t *prev, const uint32_t *next, uint64_t
  * the caller's to exclude.  Keys inside one request must be distinct (chained
  * prefix hashes are); otherwise the results are unspecified (memory-safe).
  *
- * Pipeline: pc_request_order puts each request's accesses in that recency
- * order (deepest block first); pc_prev_next_use and pc_stack_distance run
- * unchanged on the reordered keys; pc_stack_distance_req turns their outputs
- * into dist_req (same order).  All arrays of one pipeline share that order.
+ * Pipeline: pc_hash_blocks with PC_HASH_DEEPEST_FIRST writes each request's
+ * accesses in that recency order (deepest block first), or pc_request_order
+ * reorders keys written in depth order; pc_prev_next_use and
+ * pc_stack_distance run unchanged on the reordered keys;
+ * pc_stack_distance_req turns their outputs into dist_req (same order).  All
+ * arrays of one pipeline share that order.
  * ------------------------------------------------------------------------ */
 
 /* Each request's accesses in reverse: keys_out[blk_off[r+1]-1-j] =
@@ -306,8 +308,11 @@ pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uin
  * record a non-zero code there instead of faulting or hanging:
  *   1  a wait on another workgroup (decoupled look-back) gave up after a
  *      bounded spin (outputs undefined);
- *   2  pc_hash_blocks: a request's tokens or blocks fall outside the arrays
- *      (that request was skipped);
+ *   2  a bad layout: pc_hash_blocks, a request's tokens or blocks fall
+ *      outside the arrays (that request was skipped); the calls that take a
+ *      request table, a table that is not a non-decreasing prefix ending at
+ *      n; pc_stack_distance, prev / next that are not mutual links (outputs
+ *      undefined, nothing written out of bounds);
  *   3  pc_mrc_weighted and the profiles: edges not non-decreasing (bins
  *      undefined);
  *   4  pc_prev_next_use: a given key histogram does not sum to n.
