@@ -1,0 +1,84 @@
+"""Host logic of bench.py (CPU only): the one-GPU guard, the kernel tables,
+the committed counter summaries it reads and the characterisation summary
+arithmetic."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_exits_with_a_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2", "--settle", "0"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def test_every_timed_kernel_has_algorithmic_bytes():
+    assert set(bench.HIP_KERNEL) <= set(bench.ALGO_BYTES)
+    for name, f in bench.ALGO_BYTES.items():
+        assert f(16) > 0, name
+
+
+@pytest.mark.parametrize("mode", ["access", "request", "session", "profile"])
+def test_committed_profiles_parse(mode):
+    path = bench.PROFILES[mode]
+    text = open(path).read()
+    blob = json.loads(text[text.index("```json") + 7:text.rindex("```")])
+    assert len(blob["source_sha256"]) == 64
+    # the copy calibration: FETCH_SIZE counts half of what a copy reads
+    assert 1.9 < blob["fetch_scale"] < 2.1 and 0.9 < blob["write_scale"] < 1.1
+    ids = {e["id"] for e in blob["kernels"].values()}
+    assert "sort_onesweep_pass" in ids and "hash_blocks" in ids
+    for e in blob["kernels"].values():
+        assert e["avg_ms"] > 0 and e["launches_per_run"] > 0
+        assert e["read_bytes"] >= 0 and e["write_bytes"] >= 0
+    # each summary names the commands that made it, from committed files only
+    assert "rocprofv3 --kernel-trace --stats" in text and "--pmc FETCH_SIZE" in text
+    assert "_work" not in text
+
+
+def test_traffic_only_for_the_sources_it_was_taken_with(monkeypatch, tmp_path):
+    text = open(bench.PROFILES["access"]).read()
+    blob = json.loads(text[text.index("```json") + 7:text.rindex("```")])
+    for sha, want in ((bench.source_sha256(), True), ("0" * 64, False)):
+        blob["source_sha256"] = sha
+        p = tmp_path / ("p_%s.md" % want)
+        p.write_text("x\n```json\n" + json.dumps(blob) + "\n```\n")
+        monkeypatch.setattr(bench, "PROFILE", str(p))
+        got = bench.measured_traffic("sort_onesweep_pass")
+        assert (got is not None) == want
+        if want:
+            e = blob["kernels"]["pc::sort_pass_kernel"]
+            assert got["read_bytes"] == e["read_bytes"] and got["write_bytes"] == e["write_bytes"]
+
+
+def test_quantile_and_profile_summary():
+    e = [10, 20, 30]
+    assert bench._quantile([0, 0, 0, 0], e, 0.5) is None
+    assert bench._quantile([1, 1, 1, 1], e, 0.5) == 20       # two of four at or below the second bin
+    assert bench._quantile([0, 0, 0, 4], e, 0.5) == float("inf")
+    # 4 blocks used once, 2 used twice, 1 used three times; sessions of
+    # footprint 1 (x3) and 7 (x1)
+    freq = [0, 4, 2, 1]
+    rp = {"interval": [1, 0, 0, 0], "lifetime": [5, 1, 1, 0], "freq": freq}
+    fp = [0, 3, 0, 0, 0, 0, 0, 1]
+    sp = {"footprint": fp, "duration": [4, 0], "gap": [0, 0]}
+    bench.PROFILE_EDGES_US, saved = [10, 20, 30], bench.PROFILE_EDGES_US
+    try:
+        s = bench.profile_summary(rp, sp)
+    finally:
+        bench.PROFILE_EDGES_US = saved
+    assert s["one_access_blocks"] == round(4 / 7, 4)
+    assert s["p_reuse_after_1"] == round(3 / 7, 4)
+    assert s["p_reuse_after_2"] == round(1 / 3, 4)
+    assert s["sessions"] == 4
+    # the top 10% of 4 sessions is the largest one: 7 of 10 blocks
+    assert s["footprint_top10pct_share"] == 0.7
