@@ -12,9 +12,10 @@
 // link step resolves such short "mixed" runs by scanning them, and when a
 // run is too long to scan it flags the four passes over the high bits and a
 // second link (then the full 64-bit sort makes equal keys adjacent).
-//   * one pass computes the four 8-bit digit histograms of a group of
-//     passes (LDS-privatised, then global atomics), one workgroup scans them
-//     into digit bases;
+//   * the four 8-bit digit histograms of a group of passes come from the
+//     caller (the hash kernel counts them while it writes the keys) or from
+//     one counting pass (LDS-privatised, then global atomics); one workgroup
+//     scans them into digit bases;
 //   * each of the eight sort passes is a single "onesweep" kernel: a
 //     workgroup takes the next tile from an atomic counter (so every tile it
 //     waits on is already running), ranks its 8192 elements by digit with
