@@ -1,6 +1,7 @@
 """Parity at the benchmark's full size and launch configuration.
 
-The full-scale mixed trace (2e9 context tokens, ~2.1e9 block accesses) runs
+The full-scale mixed trace (2e9 context tokens, ~2.1e9 block accesses) and
+the full chat-shaped trace (20,000 sessions, ~2.2e8 block accesses) run
 through the same Pipeline bench.py times.  The oracle cannot redo the whole
 trace, so it checks:
 
@@ -33,11 +34,11 @@ def say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-@pytest.fixture(scope="module")
-def full():
+@pytest.fixture(scope="module", params=["full", "chat"])
+def full(request):
     assert torch.cuda.is_available()
-    tr = pcgen.make_trace("full")
-    say("full trace generated:", tr.n_requests, "requests", tr.n_blocks(), "accesses")
+    tr = pcgen.make_trace(request.param)
+    say(request.param, "trace generated:", tr.n_requests, "requests", tr.n_blocks(), "accesses")
     caps = tr.caps()
     B = 16
     up = pc.upload_trace(tr, B)
