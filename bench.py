@@ -40,7 +40,24 @@ ALGO_BYTES = {
     "session_distance": lambda B: 4 + 4,          # prev in; dist_sess out
     "reuse_profile_pack": lambda B: 4 + 8,        # next in; (next, request) out
     "reuse_profile_walk": lambda B: 4 + 8,        # prev (chain starts) and one (next, request) per step in
+    # chained prev/next: its own key, the two linked requests' keys at the
+    # same depths, prev + next out
+    "chain_stair": lambda B: 8 + 8 + 8 + 8,
 }
+# generic prev/next kernels: per element of the key streams they sort
+GENERIC_PN = ("sort_digit_hist", "sort_digit_scan", "sort_onesweep_pass", "link_partition", "perm_partition",
+              "perm_local")
+
+
+def chain_bytes(name, n, n_slots, m, n_req):
+    """Algorithmic bytes per launch of the chained prev/next's own kernels
+    (n accesses, n_slots anchor slots, m unresolved accesses, n_req requests)."""
+    return {# two launches: the layout check (offsets in), the anchors (key in; slot key + record out)
+            "chain_anchor": (n_req * 16 + n_slots * (8 + 8 + 16)) // 2,
+            "chain_scan": n_slots * (4 + 4 + 4) // 3,     # three launches over the slot counts
+            "chain_compact": 8 * n + m * (8 + 8 + 4 + 1),  # prev + next in; key in, (key, pos, flag) out
+            "chain_merge": m * (1 + 4 + 4 + 4 + 8),       # (flag, pos, prev, next) in; prev / next out
+            }.get(name)
 
 
 def log(*a):
@@ -54,7 +71,9 @@ HIP_KERNEL = {"sort_onesweep_pass": "pc::sort_pass_kernel", "link_partition": "p
               "perm_local": "pc::perm_local_kernel", "mrc_hist": "pc::mrc_hist_kernel",
               "request_distance": "pc::req_dist_kernel",
               "session_distance": "pc::sess_dist_kernel", "reuse_profile_walk": "pc::prof_walk_kernel",
-              "reuse_profile_pack": "pc::prof_pack_kernel"}
+              "reuse_profile_pack": "pc::prof_pack_kernel", "chain_stair": "pc::chain_stair_kernel",
+              "chain_compact": "pc::chain_compact_kernel", "chain_anchor": "pc::chain_anchor_kernel",
+              "chain_merge": "pc::chain_merge_kernel"}
 PROFILES = {"access": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9.md"),
             "request": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_request.md"),
             "session": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_session.md"),
@@ -219,6 +238,8 @@ def main():
                          "1e6 with --residency request)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 4 GiB device copy (for rocprof counter calibration)")
+    ap.add_argument("--prev-next", default="chained", choices=["chained", "generic"],
+                    help="prev/next from the chain structure of the keys (default) or the generic sort")
     ap.add_argument("--settle", type=float, default=20.0,
                     help="seconds to wait before touching the device (memory that another process "
                          "released just before is reclaimed in the background meanwhile)")
@@ -254,10 +275,11 @@ def main():
     if args.profile:
         prof_edges = pc.to_dev_u64(np.array(PROFILE_EDGES_US, np.uint64))
         pipe = pc.Profiler(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
-                           up["session"], up["ts_us"], prof_edges, B)
+                           up["session"], up["ts_us"], prof_edges, B, chained=args.prev_next == "chained")
     else:
         pipe = pc.Pipeline(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
-                           caps, B, alpha, beta, residency=args.residency, session=up["session"])
+                           caps, B, alpha, beta, residency=args.residency, session=up["session"],
+                           chained=args.prev_next == "chained")
     torch.cuda.synchronize()
     log("inputs resident in HBM; device memory in use %.1f GB" % (torch.cuda.memory_allocated() / 1e9))
 
@@ -294,11 +316,23 @@ def main():
 
     ms_step = wall * 1e3 / args.steps
     value = n_blocks / (ms_step / 1e3)
-    # the four high-key sort passes exit at once unless the first link
-    # asked for them; count only passes that moved data
-    high = pipe.high_key_passes_ran() if not args.profile else pc.high_key_passes_ran(pipe.ws_pn)
-    work_launches = {"sort_onesweep_pass": 8 if high else 4, "link_partition": 2 if high else 1,
-                     "sort_digit_hist": 2 if high else 1}
+    # the four high-key sort passes of each inner prev/next exit at once
+    # unless its first link asked for them; count only passes that moved data
+    chain = pc.chained_info(pipe.ws_pn) if pipe.chained else None
+    if chain:
+        log("chained prev/next:", chain)
+        if chain["generic"]:
+            raise SystemExit("the chained prev/next fell back to the generic path on this trace: %s" % chain)
+        calls = 2
+        highs = int(chain["high_anchor"]) + int(chain["high_unresolved"])
+        n_slots = n_blocks // 64 + trace.n_requests + 1
+        pn_elems = n_slots + chain["unresolved"]
+    else:
+        calls = 1
+        highs = int(pc.high_key_passes_ran(pipe.ws_pn))
+        n_slots = pn_elems = n_blocks
+    work_launches = {"sort_onesweep_pass": 4 * calls + 4 * highs, "link_partition": calls + highs,
+                     "sort_digit_hist": calls + highs}
     kernels = {}
     for name, (launches, ms) in prof.items():
         if launches == 0:
@@ -307,8 +341,15 @@ def main():
         wl = work_launches.get(name, launches // args.steps)
         entry = {"launches_per_step": launches // args.steps, "working_launches_per_step": wl,
                  "ms_per_step": round(per_step, 4)}
-        if name in ALGO_BYTES:
-            per_launch = (8 if (request or session_mode) and name == "mrc_hist" else ALGO_BYTES[name](B)) * n_blocks
+        cb_bytes = chain_bytes(name, n_blocks, n_slots, chain["unresolved"], trace.n_requests) if chain else None
+        if name in ALGO_BYTES or cb_bytes is not None:
+            if cb_bytes is not None:
+                per_launch = cb_bytes
+            elif name in GENERIC_PN:
+                # elements sorted per inner call, averaged over the calls
+                per_launch = ALGO_BYTES[name](B) * pn_elems // calls
+            else:
+                per_launch = (8 if (request or session_mode) and name == "mrc_hist" else ALGO_BYTES[name](B)) * n_blocks
             entry["algo_bytes_per_launch"] = per_launch
             entry["avg_working_launch_ms"] = round(per_step / wl, 4)
             entry["algo_GBps"] = round(per_launch * wl / per_step / 1e6, 1)
@@ -327,7 +368,9 @@ def main():
     stage_of = {"hash_blocks": "hash", "sort_digit_hist": "prev_next",
                 "sort_digit_scan": "prev_next", "sort_onesweep_pass": "prev_next",
                 "link_partition": "prev_next",
-                "perm_partition": "prev_next", "perm_local": "prev_next", "mrc_hist": "mrc",
+                "perm_partition": "prev_next", "perm_local": "prev_next", "chain_anchor": "prev_next",
+                "chain_stair": "prev_next", "chain_scan": "prev_next", "chain_compact": "prev_next",
+                "chain_merge": "prev_next", "mrc_hist": "mrc",
                 "mrc_cost": "mrc", "request_distance": "request_distance",
                 "session_requests": "session_profile" if args.profile else "session_distance",
                 "session_distance": "session_distance",
@@ -399,7 +442,8 @@ def main():
         "cpu_baseline": cb,
         "kernels": kernels,
         "stages": stages,
-        "high_key_sort_passes": high,
+        "high_key_sort_passes": highs,
+        "chained_prev_next": chain,
     }
     if args.profile:
         out["metric"] = "KV-block accesses/sec for hash+prev/next+workload characterisation; achieved HBM GB/s"

@@ -11,7 +11,9 @@
  * Common rules
  *   - Every array argument is DEVICE memory (hipMalloc / a torch tensor on the
  *     GPU) unless stated otherwise.  The caller owns all memory; the library
- *     never allocates, frees or synchronises.  Scratch space comes only from
+ *     never allocates or frees, and only pc_prev_next_chained and the
+ *     read-back calls (pc_workspace_status, pc_prof_read) synchronise.
+ *     Scratch space comes only from
  *     the caller's workspace `ws` of at least the size the matching `*_ws`
  *     query returns (256-byte aligned).
  *   - Work is enqueued on `stream` and the call returns; outputs are valid once
@@ -127,6 +129,43 @@ pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_
 size_t pc_prev_next_use_ws(uint64_t n);
 pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uint32_t *next,
                            const uint32_t *key_hist, void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Previous / next use of every access of a chained-key trace.
+ *
+ * Same prev and next as pc_prev_next_use, for keys laid out as
+ * pc_hash_blocks writes them: request r's blocks at blk_off[r] ..
+ * blk_off[r+1] - 1, ascending depth (flags 0) or descending depth
+ * (PC_HASH_DEEPEST_FIRST).  Chained keys fix the whole prefix (Sec. 2.2), so
+ * a request's reuse links come in long runs to very few earlier requests:
+ * the call links anchors every 64 depths with the generic prev/next, extends
+ * each anchor link over the 64 depths it covers by comparing keys, runs the
+ * generic prev/next over the accesses left without a link (first and last
+ * uses, mostly), and checks the merged result.  The outputs are exact for any
+ * keys: when the check fails, the block layout is invalid, or the unresolved
+ * accesses do not fit the workspace, the generic prev/next runs over all keys.
+ *
+ *   keys      uint64[n]; prev, next uint32[n] outputs.
+ *   blk_off   uint64[n_seqs+1], blk_off[0] = 0, non-decreasing, blk_off[n_seqs]
+ *             = n.  Any other layout sets the workspace status to 2 and takes
+ *             the generic path (outputs still exact).
+ *   flags     0 or PC_HASH_DEEPEST_FIRST.
+ *   key_hist  as for pc_prev_next_use; used only by the generic path over all
+ *             keys.
+ * Unlike the other entry points this call synchronises `stream` twice (it
+ * reads back the number of unresolved accesses and the check's verdict), so
+ * it cannot be captured into a graph.  Workspace words after the call:
+ * word 1 = 1 if the generic path ran over all keys, word 2 = the number of
+ * accesses that went through the generic prev/next of the unresolved ones,
+ * word 3 = why the generic path ran (1 layout, 2 too many unresolved,
+ * 3 check failed, 4 an inner call reported an error), word 6 = 1 if the
+ * prev/next over the anchors (or, when word 1 = 1, over all keys) also
+ * sorted by the high key bits, word 7 = the same for the unresolved ones.
+ * ------------------------------------------------------------------------ */
+size_t pc_prev_next_chained_ws(uint64_t n, uint32_t n_seqs);
+pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t *blk_off, uint32_t n_seqs,
+                               uint32_t flags, uint32_t *prev, uint32_t *next, const uint32_t *key_hist,
+                               void *ws, size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
  * Exact LRU stack distance of every access.

@@ -33,6 +33,11 @@ static const char *kernel_name(KernelId k) {
     case K_SESS_PROFILE: return "session_profile";
     case K_PROF_PACK: return "reuse_profile_pack";
     case K_PROF_WALK: return "reuse_profile_walk";
+    case K_CHAIN_ANCHOR: return "chain_anchor";
+    case K_CHAIN_STAIR: return "chain_stair";
+    case K_CHAIN_SCAN: return "chain_scan";
+    case K_CHAIN_COMPACT: return "chain_compact";
+    case K_CHAIN_MERGE: return "chain_merge";
     case K_COUNT: break;
     }
     return "";

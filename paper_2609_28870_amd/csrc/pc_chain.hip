@@ -1,0 +1,495 @@
+// Previous / next use of every access from the chain structure of the keys
+// (pc_prev_next_chained).  Same outputs as pc_prev_next_use.
+//
+// A block key is chained over the whole token prefix (Sec. 2.2: a cached
+// block is reusable only when everything before it matches), so an access
+// at depth d of request r and one at depth d of request c carry the same key
+// exactly when the two requests agree on their first d + 1 blocks (up to
+// hash collisions, which the checks below catch).  Hence the latest earlier
+// request sharing r's block at depth d is a step function of d that changes
+// only where r leaves one earlier request's prefix: a request's reuse links
+// come in long runs to very few earlier requests.
+//
+// GPU mapping, S = 64 = one wave of depths:
+//   1. anchors: the key at every depth a*S of every request goes to slot
+//      base(r) + a, base(r) = floor(blk_off[r] / S) + r (slots of different
+//      requests never overlap; the one or two slots between requests hold a
+//      filler key), and the generic prev/next runs over the slots
+//      (~n/64 + n_seqs keys);
+//   2. staircase: one wave per slot (r, a) takes the request c of the
+//      anchor's previous use; lanes d = a*S .. a*S+63 compare r's and c's
+//      keys and every lane before the first mismatch links to c at depth d.
+//      The anchor's next use gives the next links the same way.  Both sides
+//      evaluate the same symmetric predicate, so a prev link r -> c at depth
+//      d exists exactly when the next link c -> r at depth d does;
+//   3. every access left without a prev or a next link (first and last
+//      occurrences, and the lanes after a change of request inside a wave)
+//      is compacted in time order and the generic prev/next runs over them;
+//      the merge writes its links back, checking that a link it adds never
+//      ends at an access that already has a staircase link on that side.
+// Exactness: staircase links join equal keys at an earlier position and are
+// one-to-one (anchor links are); merged links join consecutive compacted
+// accesses with equal keys; the merge check makes prev one-to-one overall;
+// every access without a prev went through the compacted prev/next, so no
+// two of them share a key.  A one-to-one prev map whose links join equal keys
+// and that has one start per key orders each key's accesses into one chain,
+// i.e. it is the exact prev (and next its inverse).  If the check fails, the
+// block layout is invalid, or too many accesses stay unresolved, the generic
+// prev/next runs over all keys instead.  Both ways the outputs are exact.
+#include "pc_internal.h"
+
+namespace pc {
+
+constexpr uint32_t UNK = 0xFFFFFFFEu;    // "no staircase link" (never a position: n < 2^32 - 1)
+constexpr int CH_S = 64;                 // depths per anchor = lanes per wave
+constexpr int CH_THREADS = 256;
+constexpr int SCAN_THREADS = 1024;
+constexpr int SCAN_ITEMS = 4;
+constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;
+constexpr uint64_t FILLER_KEY = 0xA5A5A5A5A5A5A5A5ull;
+
+// header words of the chained workspace
+constexpr int HW_STATUS = 0;
+constexpr int HW_PATH = 1;       // 0 = chain path verified, 1 = generic over all keys
+constexpr int HW_UNRESOLVED = 2; // accesses that went through the compacted prev/next
+constexpr int HW_REASON = 3;     // why the generic path ran: 1 layout, 2 too many unresolved, 3 check, 4 nested error
+constexpr int HW_BAD = 4;        // device flag: invalid block layout
+constexpr int HW_FAIL = 5;       // device flag: a merge check failed
+constexpr int HW_HIGH_ANCHOR = 6;     // the prev/next over the anchors also sorted by the high key bits
+constexpr int HW_HIGH_UNRESOLVED = 7; // the prev/next over the unresolved accesses did
+
+__device__ __forceinline__ int wave_id_uniform() {
+    return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / WAVE));
+}
+
+// Per slot, written with the anchor keys: the anchor's position, the number
+// of depths the slot covers (0 for a filler slot) and the anchor depth
+// (NONE for a filler).  Depth a*S + lane sits at pos + lane, or pos - lane in
+// the deepest-first layout.
+struct Slot {
+    uint64_t pos;
+    uint32_t lanes, depth;
+};
+__device__ __forceinline__ Slot load_slot(const uint4 *__restrict__ rec, uint64_t j) {
+    const uint4 v = rec[j];
+    return Slot{(uint64_t)v.x | ((uint64_t)v.y << 32), v.z, v.w};
+}
+__device__ __forceinline__ uint64_t lane_pos(const Slot &q, int lane, int deepest) {
+    return deepest ? q.pos - (uint64_t)lane : q.pos + (uint64_t)lane;
+}
+
+// Every request: blk_off[r] <= blk_off[r+1], blk_off[0] = 0, blk_off[R] = n.
+__global__ void chain_layout_kernel(const uint64_t *__restrict__ off, uint32_t n_seqs, uint64_t n,
+                                    int32_t *__restrict__ hdr) {
+    const uint64_t r = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= n_seqs) return;
+    const uint64_t a = off[r], b = off[r + 1];
+    bool ok = a <= b && b <= n;
+    if (r == 0) ok = ok && a == 0;
+    if (r + 1 == n_seqs) ok = ok && b == n;
+    if (!ok) {
+        atomicOr(hdr + HW_BAD, 1);
+        atomicOr(hdr + HW_STATUS, DEV_ERR_BAD_LAYOUT);
+    }
+}
+
+// One wave per request: the request's anchors go to slots
+// base(r) .. base(r) + ceil(len / S) - 1, base(r) = floor(blk_off[r] / S) + r,
+// in time order (ascending depth, or descending in the deepest-first
+// layout); the slots up to the next request's first one get filler keys.
+__global__ __launch_bounds__(CH_THREADS) void chain_anchor_kernel(
+    const uint64_t *__restrict__ keys, const uint64_t *__restrict__ off, uint32_t n_seqs, uint64_t n_slots,
+    int deepest, uint64_t *__restrict__ akeys, uint4 *__restrict__ rec, const int32_t *__restrict__ hdr) {
+    if (hdr[HW_BAD]) return;
+    const int lane = threadIdx.x & (WAVE - 1);
+    const uint64_t waves = (uint64_t)gridDim.x * (CH_THREADS / WAVE);
+    for (uint64_t r = (uint64_t)blockIdx.x * (CH_THREADS / WAVE) + wave_id_uniform(); r < n_seqs; r += waves) {
+        const uint64_t o0 = off[r], o1 = off[r + 1];
+        const uint64_t len = o1 - o0, base = o0 / CH_S + r, n_anchor = (len + CH_S - 1) / CH_S;
+        const uint64_t next_base = (r + 1 < n_seqs) ? o1 / CH_S + r + 1 : n_slots;
+        for (uint64_t i = lane; base + i < next_base; i += WAVE) {
+            const uint64_t j = base + i;
+            if (i < n_anchor) {
+                const uint64_t d = (deepest ? n_anchor - 1 - i : i) * CH_S;
+                const uint64_t p = deepest ? o1 - 1 - d : o0 + d;
+                const uint64_t lanes = len - d < (uint64_t)CH_S ? len - d : (uint64_t)CH_S;
+                akeys[j] = keys[p];
+                rec[j] = make_uint4((uint32_t)p, (uint32_t)(p >> 32), (uint32_t)lanes, (uint32_t)d);
+            } else {
+                akeys[j] = FILLER_KEY;
+                rec[j] = make_uint4(0u, 0u, 0u, NONE);
+            }
+        }
+    }
+}
+
+// Slots per wave iteration: their loads are issued together so the three
+// dependent levels (slot record and anchor links, linked records, keys)
+// overlap across slots.
+constexpr int CH_BATCH = 4;
+
+// Links of one side for one slot: the lanes before the first depth at which
+// the slot's request and the linked anchor's request differ (both must cover
+// the depth) link to the linked request at that depth; UNK elsewhere.
+__device__ __forceinline__ uint32_t stair_claim(const Slot &q, const Slot &c, uint64_t kr, uint64_t kc, int lane,
+                                                int deepest) {
+    const bool eq = c.depth == q.depth && lane < (int)q.lanes && lane < (int)c.lanes && kc == kr;
+    const uint64_t m = ballot(eq);
+    const int lead = (~m == 0) ? WAVE : __builtin_ctzll(~m);
+    return lane < lead ? (uint32_t)lane_pos(c, lane, deepest) : UNK;
+}
+
+// One wave per slot: prev / next staircase links of the slot's depths and
+// the count of its accesses left unresolved.  A link to a filler slot or to
+// an anchor at another depth (equal keys there are a collision) claims
+// nothing.
+__global__ __launch_bounds__(CH_THREADS) void chain_stair_kernel(
+    const uint64_t *__restrict__ keys, uint64_t n_slots, const uint4 *__restrict__ rec,
+    const uint32_t *__restrict__ aprev, const uint32_t *__restrict__ anext, int deepest,
+    uint32_t *__restrict__ prev, uint32_t *__restrict__ next, uint32_t *__restrict__ cnt,
+    const int32_t *__restrict__ hdr) {
+    if (hdr[HW_BAD]) return;
+    const int lane = threadIdx.x & (WAVE - 1);
+    const uint64_t waves = (uint64_t)gridDim.x * (CH_THREADS / WAVE);
+    const Slot none{0, 0, NONE};
+    for (uint64_t j0 = ((uint64_t)blockIdx.x * (CH_THREADS / WAVE) + wave_id_uniform()) * CH_BATCH; j0 < n_slots;
+         j0 += waves * CH_BATCH) {
+        Slot q[CH_BATCH], cp[CH_BATCH], cx[CH_BATCH];
+        uint32_t lp[CH_BATCH], lx[CH_BATCH];
+#pragma unroll
+        for (int k = 0; k < CH_BATCH; ++k) {
+            const bool in = j0 + k < n_slots;
+            q[k] = in ? load_slot(rec, j0 + k) : none;
+            lp[k] = in ? aprev[j0 + k] : NONE;
+            lx[k] = in ? anext[j0 + k] : NONE;
+        }
+#pragma unroll
+        for (int k = 0; k < CH_BATCH; ++k) {
+            cp[k] = lp[k] != NONE ? load_slot(rec, lp[k]) : none;
+            cx[k] = lx[k] != NONE ? load_slot(rec, lx[k]) : none;
+        }
+        uint64_t kr[CH_BATCH], kp[CH_BATCH], kx[CH_BATCH];
+#pragma unroll
+        for (int k = 0; k < CH_BATCH; ++k) {
+            const bool v = lane < (int)q[k].lanes;
+            kr[k] = v ? keys[lane_pos(q[k], lane, deepest)] : 0;
+            kp[k] = v && cp[k].depth == q[k].depth && lane < (int)cp[k].lanes ? keys[lane_pos(cp[k], lane, deepest)]
+                                                                              : ~kr[k];
+            kx[k] = v && cx[k].depth == q[k].depth && lane < (int)cx[k].lanes ? keys[lane_pos(cx[k], lane, deepest)]
+                                                                              : ~kr[k];
+        }
+#pragma unroll
+        for (int k = 0; k < CH_BATCH; ++k) {
+            if (j0 + k >= n_slots) break;
+            const bool v = lane < (int)q[k].lanes;
+            const uint32_t p = stair_claim(q[k], cp[k], kr[k], kp[k], lane, deepest);
+            const uint32_t x = stair_claim(q[k], cx[k], kr[k], kx[k], lane, deepest);
+            if (v) {
+                const uint64_t pr = lane_pos(q[k], lane, deepest);
+                prev[pr] = p;
+                next[pr] = x;
+            }
+            const uint64_t m = ballot(v && (p == UNK || x == UNK));
+            if (lane == 0) cnt[j0 + k] = (uint32_t)__popcll(m);
+        }
+    }
+}
+
+// Exclusive scan of cnt[0 .. m) into out[0 .. m], out[m] = total: tile sums,
+// one workgroup over the tile sums, then each tile again with its base.
+__global__ __launch_bounds__(SCAN_THREADS) void chain_scan_tiles_kernel(const uint32_t *__restrict__ cnt,
+                                                                        uint64_t m, uint32_t *__restrict__ tsum,
+                                                                        const int32_t *__restrict__ hdr) {
+    if (hdr[HW_BAD]) return;
+    __shared__ uint32_t tmp[SCAN_THREADS / WAVE];
+    const uint64_t t0 = (uint64_t)blockIdx.x * SCAN_TILE;
+    uint32_t s = 0;
+#pragma unroll
+    for (int k = 0; k < SCAN_ITEMS; ++k) {
+        const uint64_t i = t0 + (uint64_t)k * SCAN_THREADS + threadIdx.x;
+        if (i < m) s += cnt[i];
+    }
+    uint32_t total = 0;
+    block_excl_scan(s, tmp, &total);
+    if (threadIdx.x == 0) tsum[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(SCAN_THREADS) void chain_scan_top_kernel(uint32_t *__restrict__ tsum, uint64_t tiles,
+                                                                      int32_t *__restrict__ hdr) {
+    if (hdr[HW_BAD]) return;
+    __shared__ uint32_t tmp[SCAN_THREADS / WAVE];
+    uint32_t carry = 0;
+    for (uint64_t t0 = 0; t0 < tiles; t0 += SCAN_THREADS) {
+        const uint64_t i = t0 + threadIdx.x;
+        const uint32_t v = i < tiles ? tsum[i] : 0;
+        uint32_t total = 0;
+        const uint32_t e = block_excl_scan(v, tmp, &total);
+        if (i < tiles) tsum[i] = carry + e;
+        carry += total;
+    }
+    if (threadIdx.x == 0) hdr[HW_UNRESOLVED] = (int32_t)carry;
+}
+
+__global__ __launch_bounds__(SCAN_THREADS) void chain_scan_apply_kernel(const uint32_t *__restrict__ cnt, uint64_t m,
+                                                                        const uint32_t *__restrict__ tsum,
+                                                                        uint32_t *__restrict__ out,
+                                                                        const int32_t *__restrict__ hdr) {
+    if (hdr[HW_BAD]) return;
+    __shared__ uint32_t tmp[SCAN_THREADS / WAVE];
+    // each thread scans SCAN_ITEMS consecutive entries
+    const uint64_t i0 = (uint64_t)blockIdx.x * SCAN_TILE + (uint64_t)threadIdx.x * SCAN_ITEMS;
+    uint32_t v[SCAN_ITEMS], s = 0;
+#pragma unroll
+    for (int k = 0; k < SCAN_ITEMS; ++k) {
+        v[k] = (i0 + k < m) ? cnt[i0 + k] : 0;
+        s += v[k];
+    }
+    uint32_t total = 0;
+    uint32_t run = tsum[blockIdx.x] + block_excl_scan(s, tmp, &total);
+#pragma unroll
+    for (int k = 0; k < SCAN_ITEMS; ++k) {
+        if (i0 + k < m) out[i0 + k] = run;
+        run += v[k];
+    }
+    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) out[m] = (uint32_t)hdr[HW_UNRESOLVED];
+}
+
+// One wave per slot: the slot's unresolved accesses, in time order, into
+// (key, position, which sides are open).
+__global__ __launch_bounds__(CH_THREADS) void chain_compact_kernel(
+    const uint64_t *__restrict__ keys, uint64_t n_slots, const uint4 *__restrict__ rec,
+    const uint32_t *__restrict__ coff, int deepest, const uint32_t *__restrict__ prev,
+    const uint32_t *__restrict__ next, uint64_t *__restrict__ ckeys, uint32_t *__restrict__ cpos,
+    uint8_t *__restrict__ cflag) {
+    const int lane = threadIdx.x & (WAVE - 1);
+    const uint64_t waves = (uint64_t)gridDim.x * (CH_THREADS / WAVE);
+    const uint64_t above = ~((2ull << lane) - 1);   // lanes above this one (none for lane 63)
+    for (uint64_t j0 = ((uint64_t)blockIdx.x * (CH_THREADS / WAVE) + wave_id_uniform()) * CH_BATCH; j0 < n_slots;
+         j0 += waves * CH_BATCH) {
+        Slot q[CH_BATCH];
+        uint32_t base[CH_BATCH], pv[CH_BATCH], nv[CH_BATCH];
+#pragma unroll
+        for (int k = 0; k < CH_BATCH; ++k) {
+            const bool in = j0 + k < n_slots;
+            q[k] = in ? load_slot(rec, j0 + k) : Slot{0, 0, NONE};
+            base[k] = in ? coff[j0 + k] : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < CH_BATCH; ++k) {
+            const bool v = lane < (int)q[k].lanes;
+            const uint64_t pr = lane_pos(q[k], lane, deepest);
+            pv[k] = v ? prev[pr] : 0;
+            nv[k] = v ? next[pr] : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < CH_BATCH; ++k) {
+            const bool open = lane < (int)q[k].lanes && (pv[k] == UNK || nv[k] == UNK);
+            const uint64_t m = ballot(open);
+            // time order: lanes ascending, or descending in the deepest-first layout
+            const uint32_t rank = deepest ? (uint32_t)__popcll(m & above) : mbcnt(m);
+            if (open) {
+                const uint64_t pr = lane_pos(q[k], lane, deepest);
+                const uint64_t o = (uint64_t)base[k] + rank;
+                ckeys[o] = keys[pr];
+                cpos[o] = (uint32_t)pr;
+                cflag[o] = (uint8_t)((pv[k] == UNK ? 1 : 0) | (nv[k] == UNK ? 2 : 0));
+            }
+        }
+    }
+}
+
+// Links of the compacted accesses back into prev / next; flags an added link
+// that would end at an access whose own side is already linked.
+__global__ __launch_bounds__(CH_THREADS) void chain_merge_kernel(const uint32_t *__restrict__ cpos,
+                                                                 const uint8_t *__restrict__ cflag,
+                                                                 const uint32_t *__restrict__ cprev,
+                                                                 const uint32_t *__restrict__ cnext, uint64_t m,
+                                                                 uint32_t *__restrict__ prev,
+                                                                 uint32_t *__restrict__ next,
+                                                                 int32_t *__restrict__ hdr) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    bool bad = false;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m; i += stride) {
+        const uint32_t f = cflag[i];
+        const uint32_t p = cpos[i];
+        if (f & 1) {
+            const uint32_t t = cprev[i];
+            if (t != NONE) {
+                bad |= !(cflag[t] & 2);
+                prev[p] = cpos[t];
+            } else {
+                prev[p] = NONE;
+            }
+        }
+        if (f & 2) {
+            const uint32_t u = cnext[i];
+            if (u != NONE) {
+                bad |= !(cflag[u] & 1);
+                next[p] = cpos[u];
+            } else {
+                next[p] = NONE;
+            }
+        }
+    }
+    if (bad) atomicOr(hdr + HW_FAIL, 1);
+}
+
+// an inner prev/next call's header: its status into ours (word 0), its
+// high-bit flag (word 1) into word `high_word` of ours
+__global__ void chain_status_kernel(const int32_t *__restrict__ nested, int32_t *__restrict__ hdr, int high_word) {
+    if (threadIdx.x != 0) return;
+    if (nested[0]) atomicOr(hdr + HW_STATUS, nested[0]);
+    hdr[high_word] = nested[1];
+}
+
+struct ChainWs {
+    int32_t *hdr;
+    void *generic;        // pc_prev_next_use workspace over all keys (also the unresolved stage's space)
+    size_t generic_bytes;
+    uint64_t *akeys;
+    uint4 *rec;
+    uint32_t *aprev, *anext, *cnt, *coff, *tsum;
+    void *aws;            // pc_prev_next_use workspace over the slots
+    size_t aws_bytes;
+    size_t bytes;
+};
+
+static uint64_t chain_slots(uint64_t n, uint32_t n_seqs) { return n / CH_S + n_seqs + 1; }
+
+static ChainWs carve_chain(void *ws, uint64_t n, uint32_t n_seqs) {
+    Carver c{(char *)ws, 0};
+    ChainWs w;
+    const uint64_t ns = chain_slots(n, n_seqs);
+    w.hdr = c.take<int32_t>(WS_HEADER / sizeof(int32_t));
+    w.generic_bytes = pc_prev_next_use_ws(n);
+    w.generic = c.take<char>(w.generic_bytes);
+    w.akeys = c.take<uint64_t>(ns);
+    w.rec = c.take<uint4>(ns);
+    w.aprev = c.take<uint32_t>(ns);
+    w.anext = c.take<uint32_t>(ns);
+    w.cnt = c.take<uint32_t>(ns);
+    w.coff = c.take<uint32_t>(ns + 1);
+    w.tsum = c.take<uint32_t>((ns + SCAN_TILE - 1) / SCAN_TILE + 1);
+    w.aws_bytes = pc_prev_next_use_ws(ns);
+    w.aws = c.take<char>(w.aws_bytes);
+    w.bytes = c.off;
+    return w;
+}
+
+// The unresolved stage's arrays inside the generic workspace (unused until a
+// fallback); false if they do not fit.
+struct OpenWs {
+    uint64_t *ckeys;
+    uint32_t *cpos, *cprev, *cnext;
+    uint8_t *cflag;
+    void *ws;
+    size_t ws_bytes;
+};
+static bool carve_open(const ChainWs &w, uint64_t m, OpenWs *o) {
+    Carver c{(char *)w.generic, 0};
+    o->ckeys = c.take<uint64_t>(m);
+    o->cpos = c.take<uint32_t>(m);
+    o->cprev = c.take<uint32_t>(m);
+    o->cnext = c.take<uint32_t>(m);
+    o->cflag = c.take<uint8_t>(m);
+    o->ws_bytes = pc_prev_next_use_ws(m);
+    o->ws = c.take<char>(o->ws_bytes);
+    return c.off <= w.generic_bytes;
+}
+
+static pc_status read_words(const int32_t *src, int32_t *dst, int count, hipStream_t s) {
+    if (hipMemcpyAsync(dst, src, sizeof(int32_t) * count, hipMemcpyDeviceToHost, s) != hipSuccess)
+        return PC_ERR_DEVICE;
+    if (hipStreamSynchronize(s) != hipSuccess) return PC_ERR_DEVICE;
+    return PC_OK;
+}
+
+static unsigned wave_grid(uint64_t items, int cus) {
+    uint64_t g = (items + CH_THREADS / WAVE - 1) / (CH_THREADS / WAVE);
+    const uint64_t cap = (uint64_t)cus * 32;
+    if (g > cap) g = cap;
+    return (unsigned)(g ? g : 1);
+}
+
+}  // namespace pc
+
+extern "C" {
+
+size_t pc_prev_next_chained_ws(uint64_t n, uint32_t n_seqs) { return pc::carve_chain(nullptr, n, n_seqs).bytes; }
+
+pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t *blk_off, uint32_t n_seqs,
+                               uint32_t flags, uint32_t *prev, uint32_t *next, const uint32_t *key_hist,
+                               void *ws, size_t ws_bytes, void *stream) {
+    using namespace pc;
+    if (n >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
+    if (n > 0 && (!keys || !prev || !next || !blk_off)) return PC_ERR_INVALID;
+    if (flags & ~PC_HASH_DEEPEST_FIRST) return PC_ERR_INVALID;
+    if (!ws) return PC_ERR_WORKSPACE;
+    if (ws_bytes < pc_prev_next_chained_ws(n, n_seqs)) return PC_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    const ChainWs w = carve_chain(ws, n, n_seqs);
+    pc_status st = fill_u32(reinterpret_cast<uint32_t *>(w.hdr), 0u, 8, s);
+    if (st != PC_OK || n == 0) return st;
+    const int deepest = (flags & PC_HASH_DEEPEST_FIRST) ? 1 : 0;
+    const int cus = device_cus();
+
+    auto generic = [&](int reason) -> pc_status {
+        pc_status g = pc_prev_next_use(keys, n, prev, next, key_hist, w.generic, w.generic_bytes, stream);
+        if (g != PC_OK) return g;
+        PC_LAUNCH(K_FILL32, chain_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)w.generic, w.hdr,
+                  HW_HIGH_ANCHOR);
+        if ((g = fill_u32(reinterpret_cast<uint32_t *>(w.hdr + HW_PATH), 1u, 1, s)) != PC_OK) return g;
+        return fill_u32(reinterpret_cast<uint32_t *>(w.hdr + HW_REASON), (uint32_t)reason, 1, s);
+    };
+    if (n_seqs == 0) return generic(1);
+
+    const uint64_t ns = chain_slots(n, n_seqs);
+    PC_LAUNCH(K_CHAIN_ANCHOR, chain_layout_kernel, dim3((unsigned)((n_seqs + 255) / 256)), dim3(256), 0, s,
+              blk_off, n_seqs, n, w.hdr);
+    PC_LAUNCH(K_CHAIN_ANCHOR, chain_anchor_kernel, dim3(wave_grid(n_seqs, cus)), dim3(CH_THREADS), 0, s, keys,
+              blk_off, n_seqs, ns, deepest, w.akeys, w.rec, (const int32_t *)w.hdr);
+    if ((st = pc_prev_next_use(w.akeys, ns, w.aprev, w.anext, nullptr, w.aws, w.aws_bytes, stream)) != PC_OK)
+        return st;
+    PC_LAUNCH(K_FILL32, chain_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)w.aws, w.hdr,
+              HW_HIGH_ANCHOR);
+    PC_LAUNCH(K_CHAIN_STAIR, chain_stair_kernel, dim3(wave_grid((ns + CH_BATCH - 1) / CH_BATCH, cus)),
+              dim3(CH_THREADS), 0, s, keys, ns, (const uint4 *)w.rec, w.aprev, w.anext, deepest, prev, next, w.cnt,
+              (const int32_t *)w.hdr);
+    const uint64_t tiles = (ns + SCAN_TILE - 1) / SCAN_TILE;
+    PC_LAUNCH(K_CHAIN_SCAN, chain_scan_tiles_kernel, dim3((unsigned)tiles), dim3(SCAN_THREADS), 0, s, w.cnt, ns,
+              w.tsum, (const int32_t *)w.hdr);
+    PC_LAUNCH(K_CHAIN_SCAN, chain_scan_top_kernel, dim3(1), dim3(SCAN_THREADS), 0, s, w.tsum, tiles, w.hdr);
+    PC_LAUNCH(K_CHAIN_SCAN, chain_scan_apply_kernel, dim3((unsigned)tiles), dim3(SCAN_THREADS), 0, s, w.cnt, ns,
+              w.tsum, w.coff, (const int32_t *)w.hdr);
+
+    // the unresolved count decides the rest (first read-back)
+    int32_t h[8], nested = 0;
+    if ((st = read_words(w.hdr, h, 8, s)) != PC_OK) return st;
+    if ((st = read_words((const int32_t *)w.aws, &nested, 1, s)) != PC_OK) return st;
+    if (h[HW_BAD]) return generic(1);
+    if (nested) return generic(4);
+    const uint64_t m = (uint32_t)h[HW_UNRESOLVED];
+    OpenWs o;
+    if (!carve_open(w, m, &o)) return generic(2);
+
+    PC_LAUNCH(K_CHAIN_COMPACT, chain_compact_kernel, dim3(wave_grid((ns + CH_BATCH - 1) / CH_BATCH, cus)),
+              dim3(CH_THREADS), 0, s, keys, ns, (const uint4 *)w.rec, w.coff, deepest, prev, next, o.ckeys, o.cpos,
+              o.cflag);
+    if ((st = pc_prev_next_use(o.ckeys, m, o.cprev, o.cnext, nullptr, o.ws, o.ws_bytes, stream)) != PC_OK)
+        return st;
+    PC_LAUNCH(K_FILL32, chain_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)o.ws, w.hdr,
+              HW_HIGH_UNRESOLVED);
+    uint64_t mg = (m + CH_THREADS - 1) / CH_THREADS;
+    if (mg > (uint64_t)cus * 16) mg = (uint64_t)cus * 16;
+    PC_LAUNCH(K_CHAIN_MERGE, chain_merge_kernel, dim3((unsigned)(mg ? mg : 1)), dim3(CH_THREADS), 0, s, o.cpos,
+              o.cflag, o.cprev, o.cnext, m, prev, next, w.hdr);
+
+    // second read-back: the merge check and the nested call's status
+    if ((st = read_words(w.hdr, h, 8, s)) != PC_OK) return st;
+    if ((st = read_words((const int32_t *)o.ws, &nested, 1, s)) != PC_OK) return st;
+    if (nested) return generic(4);
+    if (h[HW_FAIL]) return generic(3);
+    return PC_OK;
+}
+
+}  // extern "C"

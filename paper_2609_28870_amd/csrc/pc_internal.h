@@ -63,6 +63,11 @@ enum KernelId {
     K_SESS_PROFILE,
     K_PROF_PACK,
     K_PROF_WALK,
+    K_CHAIN_ANCHOR,
+    K_CHAIN_STAIR,
+    K_CHAIN_SCAN,
+    K_CHAIN_COMPACT,
+    K_CHAIN_MERGE,
     K_COUNT
 };
 

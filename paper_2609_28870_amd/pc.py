@@ -55,6 +55,10 @@ def lib():
     L.pc_prev_next_use_ws.argtypes = [_u64]
     L.pc_prev_next_use.restype = _st
     L.pc_prev_next_use.argtypes = [_vp, _u64, _vp, _vp, _vp, _vp, _sz, _vp]
+    L.pc_prev_next_chained_ws.restype = _sz
+    L.pc_prev_next_chained_ws.argtypes = [_u64, _u32]
+    L.pc_prev_next_chained.restype = _st
+    L.pc_prev_next_chained.argtypes = [_vp, _u64, _vp, _u32, _u32, _vp, _vp, _vp, _vp, _sz, _vp]
     L.pc_stack_distance_ws.restype = _sz
     L.pc_stack_distance_ws.argtypes = [_u64]
     L.pc_stack_distance.restype = _st
@@ -205,6 +209,37 @@ def high_key_passes_ran(ws: torch.Tensor) -> bool:
     Synchronises the current stream."""
     torch.cuda.current_stream().synchronize()
     return bool(int(ws[4:8].view(torch.int32).item()))
+
+
+def prev_next_chained(keys: torch.Tensor, blk_off: torch.Tensor, prev: Optional[torch.Tensor] = None,
+                      nxt: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                      key_hist: Optional[torch.Tensor] = None, deepest_first: bool = False):
+    """pc_prev_next_chained: the same prev / next as prev_next_use for keys
+    laid out per request as hash_blocks writes them (synchronises the stream
+    twice)."""
+    L = lib()
+    n = keys.numel()
+    n_seqs = blk_off.numel() - 1
+    dev = _dev()
+    if prev is None:
+        prev = torch.empty(n, dtype=torch.int32, device=dev)
+    if nxt is None:
+        nxt = torch.empty(n, dtype=torch.int32, device=dev)
+    if ws is None:
+        ws = workspace(L.pc_prev_next_chained_ws(n, n_seqs))
+    check(L.pc_prev_next_chained(_ptr(keys), n, _ptr(blk_off), n_seqs, 1 if deepest_first else 0,
+                                 _ptr(prev), _ptr(nxt), _ptr(key_hist), _ptr(ws), ws.numel(), _stream()))
+    return prev, nxt, ws
+
+
+def chained_info(ws: torch.Tensor) -> dict:
+    """What the last pc_prev_next_chained call on this workspace did: whether
+    the generic prev/next ran over all keys (and why), and how many accesses
+    went through the generic prev/next of the unresolved ones.  Synchronises."""
+    torch.cuda.current_stream().synchronize()
+    w = ws[:32].view(torch.int32).cpu().tolist()
+    return {"generic": bool(w[1]), "unresolved": w[2] & 0xFFFFFFFF, "reason": w[3],
+            "high_anchor": bool(w[6]), "high_unresolved": bool(w[7])}
 
 
 def stack_distance(prev: torch.Tensor, nxt: torch.Tensor, dist: Optional[torch.Tensor] = None,
@@ -412,7 +447,7 @@ class Pipeline:
 
     def __init__(self, tokens, tok_start, tok_len, blk_off, n_blocks: int, caps,
                  block_size: int = 16, alpha: int = 1, beta: int = 0, with_nextuse: bool = True,
-                 residency: str = "access", session: Optional[torch.Tensor] = None):
+                 residency: str = "access", session: Optional[torch.Tensor] = None, chained: bool = True):
         if residency not in ("access", "request", "session"):
             raise PcError("residency must be 'access', 'request' or 'session'")
         if residency == "session" and session is None:
@@ -439,7 +474,9 @@ class Pipeline:
         self.bins = {name: torch.empty(k + 1, dtype=torch.int64, device=dev)
                      for name in ("count", "depthsum", "cost_lo", "cost_hi", "nextuse")}
         self.ws_hash = workspace(L.pc_hash_blocks_ws(tok_len.numel()))
-        self.ws_pn = workspace(L.pc_prev_next_use_ws(n))
+        self.chained = chained
+        self.ws_pn = workspace(L.pc_prev_next_chained_ws(n, tok_len.numel()) if chained
+                               else L.pc_prev_next_use_ws(n))
         if residency == "session":
             self.ws_sd = workspace(L.pc_stack_distance_session_ws(n, tok_len.numel()))
         else:
@@ -455,27 +492,38 @@ class Pipeline:
                     keys=self.keys, depth=self.depth, ws=self.ws_hash, key_hist=self.key_hist,
                     deepest_first=self.request)
         if self.residency == "session":
-            prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
+            self._prev_next(self.keys)
             stack_distance_session(self.prev, self.blk_off, self.session, dist_sess=self.dist, ws=self.ws_sd)
             mrc_weighted(self.dist, self.caps, self.depth, None, self.alpha, self.beta, out=self.bins,
                          ws=self.ws_mrc)
             return
         if not self.request:
-            prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
+            self._prev_next(self.keys)
             stack_distance(self.prev, self.next, self.dist, ws=self.ws_sd)
             mrc_weighted(self.dist, self.caps, self.depth, self.next if self.with_nextuse else None,
                          self.alpha, self.beta, out=self.bins, ws=self.ws_mrc)
             return
-        prev_next_use(self.keys_r, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
+        self._prev_next(self.keys_r)
         stack_distance(self.prev, self.next, self.dist, ws=self.ws_sd)
         stack_distance_req(self.prev, self.dist, self.blk_off, dist_req=self.dist_req, ws=self.ws_req)
         mrc_weighted(self.dist_req, self.caps, self.depth_r, None, self.alpha, self.beta,
                      out=self.bins, ws=self.ws_mrc)
 
+    def _prev_next(self, keys):
+        if self.chained:
+            prev_next_chained(keys, self.blk_off, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist,
+                              deepest_first=self.request)
+        else:
+            prev_next_use(keys, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
+
     def high_key_passes_ran(self) -> bool:
-        """Whether the last prev/next call also sorted by the high 32 key
-        bits (decided on the device; see pc_prev_next_use).  Synchronises."""
+        """Whether the last generic prev/next call also sorted by the high 32
+        key bits (decided on the device; see pc_prev_next_use).  Synchronises."""
         return high_key_passes_ran(self.ws_pn)
+
+    def chained_info(self) -> dict:
+        """What the last chained prev/next did (see chained_info)."""
+        return chained_info(self.ws_pn)
 
     def status(self) -> dict:
         stages = [("hash", self.ws_hash), ("prev_next", self.ws_pn), ("stack_distance", self.ws_sd),
@@ -491,7 +539,8 @@ class Profiler:
     (footprints, requests, durations, gaps), buffers allocated once."""
 
     def __init__(self, tokens, tok_start, tok_len, blk_off, n_blocks: int, session, ts_us, edges,
-                 block_size: int = 16, freq_max: int = 2048, fp_max: int = 1 << 16, rq_max: int = 2048):
+                 block_size: int = 16, freq_max: int = 2048, fp_max: int = 1 << 16, rq_max: int = 2048,
+                 chained: bool = True):
         L = lib()
         dev = _dev()
         self.tokens, self.tok_start, self.tok_len, self.blk_off = tokens, tok_start, tok_len, blk_off
@@ -505,7 +554,9 @@ class Profiler:
         self.prev = torch.empty(n, dtype=torch.int32, device=dev)
         self.next = torch.empty(n, dtype=torch.int32, device=dev)
         self.ws_hash = workspace(L.pc_hash_blocks_ws(tok_len.numel()))
-        self.ws_pn = workspace(L.pc_prev_next_use_ws(n))
+        self.chained = chained
+        self.ws_pn = workspace(L.pc_prev_next_chained_ws(n, tok_len.numel()) if chained
+                               else L.pc_prev_next_use_ws(n))
         self.ws_rp = workspace(L.pc_reuse_profile_ws(n))
         self.ws_sp = workspace(L.pc_session_profile_ws(tok_len.numel()))
         k = edges.numel()
@@ -521,7 +572,10 @@ class Profiler:
     def run(self):
         hash_blocks(self.tokens, self.tok_start, self.tok_len, self.blk_off, self.n, self.B,
                     want_depth=False, keys=self.keys, ws=self.ws_hash, key_hist=self.key_hist)
-        prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
+        if self.chained:
+            prev_next_chained(self.keys, self.blk_off, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
+        else:
+            prev_next_use(self.keys, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
         reuse_profile(self.prev, self.next, self.blk_off, self.ts_us, self.edges, self.freq_max,
                       out=self.reuse, ws=self.ws_rp)
         session_profile(self.blk_off, self.session, self.ts_us, self.n, self.edges, self.fp_max, self.rq_max,

@@ -73,6 +73,19 @@ def test_prev_next_rejects_bad_arguments(L):
     assert L.pc_prev_next_use(FAKE, n, FAKE, FAKE, None, FAKE, ws - 1, None) == -3
 
 
+def test_prev_next_chained_rejects_bad_arguments(L):
+    n, seqs = 1000, 10
+    ws = L.pc_prev_next_chained_ws(n, seqs)
+    assert ws > L.pc_prev_next_use_ws(n)
+    assert L.pc_prev_next_chained(FAKE, 0xFFFFFFFF, FAKE, seqs, 0, FAKE, FAKE, None, FAKE, 1 << 40, None) == -2
+    assert L.pc_prev_next_chained(None, n, FAKE, seqs, 0, FAKE, FAKE, None, FAKE, ws, None) == -1
+    assert L.pc_prev_next_chained(FAKE, n, None, seqs, 0, FAKE, FAKE, None, FAKE, ws, None) == -1
+    assert L.pc_prev_next_chained(FAKE, n, FAKE, seqs, 0, FAKE, None, None, FAKE, ws, None) == -1
+    assert L.pc_prev_next_chained(FAKE, n, FAKE, seqs, 2, FAKE, FAKE, None, FAKE, ws, None) == -1
+    assert L.pc_prev_next_chained(FAKE, n, FAKE, seqs, 0, FAKE, FAKE, None, None, ws, None) == -3
+    assert L.pc_prev_next_chained(FAKE, n, FAKE, seqs, 0, FAKE, FAKE, None, FAKE, ws - 1, None) == -3
+
+
 def test_stack_distance_rejects_bad_arguments(L):
     n = 5000
     ws = L.pc_stack_distance_ws(n)
@@ -188,5 +201,5 @@ def test_profiling_table(L):
     names = [L.pc_prof_kernel_name(i).decode() for i in range(n)]
     assert "hash_blocks" in names and "sd_dominance_pass" in names and "mrc_hist" in names
     assert all(names) and len(set(names)) == n
-    assert names[-1] == "reuse_profile_walk"
+    assert names[-1] == "chain_merge" and "chain_stair" in names
     assert pc.prof_read() is not None

@@ -22,9 +22,12 @@ def test_more_than_one_gpu_exits_with_a_message():
 
 
 def test_every_timed_kernel_has_algorithmic_bytes():
-    assert set(bench.HIP_KERNEL) <= set(bench.ALGO_BYTES)
+    chain = {k for k in bench.HIP_KERNEL if bench.chain_bytes(k, 1 << 20, 1 << 14, 1 << 17, 1000) is not None}
+    assert set(bench.HIP_KERNEL) <= set(bench.ALGO_BYTES) | chain
     for name, f in bench.ALGO_BYTES.items():
         assert f(16) > 0, name
+    for name in chain:
+        assert bench.chain_bytes(name, 1 << 20, 1 << 14, 1 << 17, 1000) > 0, name
 
 
 @pytest.mark.parametrize("mode", ["access", "request", "session", "profile"])
