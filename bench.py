@@ -55,7 +55,8 @@ def chain_bytes(name, n, n_slots, m, n_req):
     return {# two launches: the layout check (offsets in), the anchors (key in; slot key + record out)
             "chain_anchor": (n_req * 16 + n_slots * (8 + 8 + 16)) // 2,
             "chain_scan": n_slots * (4 + 4 + 4) // 3,     # three launches over the slot counts
-            "chain_compact": 8 * n + m * (8 + 8 + 4 + 1),  # prev + next in; key in, (key, pos, flag) out
+            # slot record, masks, offset in; key in, (key, pos, flag) out
+            "chain_compact": n_slots * (16 + 16 + 4) + m * (8 + 8 + 4 + 1),
             "chain_merge": m * (1 + 4 + 4 + 4 + 8),       # (flag, pos, prev, next) in; prev / next out
             }.get(name)
 

@@ -126,7 +126,7 @@ __global__ __launch_bounds__(CH_THREADS) void chain_anchor_kernel(
 // Slots per wave iteration: their loads are issued together so the three
 // dependent levels (slot record and anchor links, linked records, keys)
 // overlap across slots.
-constexpr int CH_BATCH = 4;
+constexpr int CH_BATCH = 2;
 
 // Links of one side for one slot: the lanes before the first depth at which
 // the slot's request and the linked anchor's request differ (both must cover
@@ -139,14 +139,15 @@ __device__ __forceinline__ uint32_t stair_claim(const Slot &q, const Slot &c, ui
     return lane < lead ? (uint32_t)lane_pos(c, lane, deepest) : UNK;
 }
 
-// One wave per slot: prev / next staircase links of the slot's depths and
-// the count of its accesses left unresolved.  A link to a filler slot or to
+// One wave per slot: prev / next staircase links of the slot's depths, the
+// lanes left without a prev and without a next link (two masks), and their
+// count.  A link to a filler slot or to
 // an anchor at another depth (equal keys there are a collision) claims
 // nothing.
 __global__ __launch_bounds__(CH_THREADS) void chain_stair_kernel(
     const uint64_t *__restrict__ keys, uint64_t n_slots, const uint4 *__restrict__ rec,
     const uint32_t *__restrict__ aprev, const uint32_t *__restrict__ anext, int deepest,
-    uint32_t *__restrict__ prev, uint32_t *__restrict__ next, uint32_t *__restrict__ cnt,
+    uint32_t *__restrict__ prev, uint32_t *__restrict__ next, uint32_t *__restrict__ cnt, uint4 *__restrict__ open,
     const int32_t *__restrict__ hdr) {
     if (hdr[HW_BAD]) return;
     const int lane = threadIdx.x & (WAVE - 1);
@@ -189,8 +190,11 @@ __global__ __launch_bounds__(CH_THREADS) void chain_stair_kernel(
                 prev[pr] = p;
                 next[pr] = x;
             }
-            const uint64_t m = ballot(v && (p == UNK || x == UNK));
-            if (lane == 0) cnt[j0 + k] = (uint32_t)__popcll(m);
+            const uint64_t mp = ballot(v && p == UNK), mx = ballot(v && x == UNK);
+            if (lane == 0) {
+                cnt[j0 + k] = (uint32_t)__popcll(mp | mx);
+                open[j0 + k] = make_uint4((uint32_t)mp, (uint32_t)(mp >> 32), (uint32_t)mx, (uint32_t)(mx >> 32));
+            }
         }
     }
 }
@@ -255,44 +259,40 @@ __global__ __launch_bounds__(SCAN_THREADS) void chain_scan_apply_kernel(const ui
 }
 
 // One wave per slot: the slot's unresolved accesses, in time order, into
-// (key, position, which sides are open).
+// (key, position, which sides are open), from the stair kernel's lane masks.
 __global__ __launch_bounds__(CH_THREADS) void chain_compact_kernel(
     const uint64_t *__restrict__ keys, uint64_t n_slots, const uint4 *__restrict__ rec,
-    const uint32_t *__restrict__ coff, int deepest, const uint32_t *__restrict__ prev,
-    const uint32_t *__restrict__ next, uint64_t *__restrict__ ckeys, uint32_t *__restrict__ cpos,
-    uint8_t *__restrict__ cflag) {
+    const uint4 *__restrict__ open, const uint32_t *__restrict__ coff, int deepest,
+    uint64_t *__restrict__ ckeys, uint32_t *__restrict__ cpos, uint8_t *__restrict__ cflag) {
     const int lane = threadIdx.x & (WAVE - 1);
     const uint64_t waves = (uint64_t)gridDim.x * (CH_THREADS / WAVE);
+    const uint64_t bit = 1ull << lane;
     const uint64_t above = ~((2ull << lane) - 1);   // lanes above this one (none for lane 63)
     for (uint64_t j0 = ((uint64_t)blockIdx.x * (CH_THREADS / WAVE) + wave_id_uniform()) * CH_BATCH; j0 < n_slots;
          j0 += waves * CH_BATCH) {
         Slot q[CH_BATCH];
-        uint32_t base[CH_BATCH], pv[CH_BATCH], nv[CH_BATCH];
+        uint64_t mp[CH_BATCH], mx[CH_BATCH];
+        uint32_t base[CH_BATCH];
 #pragma unroll
         for (int k = 0; k < CH_BATCH; ++k) {
             const bool in = j0 + k < n_slots;
             q[k] = in ? load_slot(rec, j0 + k) : Slot{0, 0, NONE};
+            const uint4 o = in ? open[j0 + k] : make_uint4(0u, 0u, 0u, 0u);
+            mp[k] = (uint64_t)o.x | ((uint64_t)o.y << 32);
+            mx[k] = (uint64_t)o.z | ((uint64_t)o.w << 32);
             base[k] = in ? coff[j0 + k] : 0;
         }
 #pragma unroll
         for (int k = 0; k < CH_BATCH; ++k) {
-            const bool v = lane < (int)q[k].lanes;
-            const uint64_t pr = lane_pos(q[k], lane, deepest);
-            pv[k] = v ? prev[pr] : 0;
-            nv[k] = v ? next[pr] : 0;
-        }
-#pragma unroll
-        for (int k = 0; k < CH_BATCH; ++k) {
-            const bool open = lane < (int)q[k].lanes && (pv[k] == UNK || nv[k] == UNK);
-            const uint64_t m = ballot(open);
+            const uint64_t m = mp[k] | mx[k];
             // time order: lanes ascending, or descending in the deepest-first layout
             const uint32_t rank = deepest ? (uint32_t)__popcll(m & above) : mbcnt(m);
-            if (open) {
+            if (m & bit) {
                 const uint64_t pr = lane_pos(q[k], lane, deepest);
                 const uint64_t o = (uint64_t)base[k] + rank;
                 ckeys[o] = keys[pr];
                 cpos[o] = (uint32_t)pr;
-                cflag[o] = (uint8_t)((pv[k] == UNK ? 1 : 0) | (nv[k] == UNK ? 2 : 0));
+                cflag[o] = (uint8_t)((mp[k] & bit ? 1 : 0) | (mx[k] & bit ? 2 : 0));
             }
         }
     }
@@ -348,6 +348,7 @@ struct ChainWs {
     size_t generic_bytes;
     uint64_t *akeys;
     uint4 *rec;
+    uint4 *open;
     uint32_t *aprev, *anext, *cnt, *coff, *tsum;
     void *aws;            // pc_prev_next_use workspace over the slots
     size_t aws_bytes;
@@ -365,6 +366,7 @@ static ChainWs carve_chain(void *ws, uint64_t n, uint32_t n_seqs) {
     w.generic = c.take<char>(w.generic_bytes);
     w.akeys = c.take<uint64_t>(ns);
     w.rec = c.take<uint4>(ns);
+    w.open = c.take<uint4>(ns);
     w.aprev = c.take<uint32_t>(ns);
     w.anext = c.take<uint32_t>(ns);
     w.cnt = c.take<uint32_t>(ns);
@@ -406,7 +408,7 @@ static pc_status read_words(const int32_t *src, int32_t *dst, int count, hipStre
 
 static unsigned wave_grid(uint64_t items, int cus) {
     uint64_t g = (items + CH_THREADS / WAVE - 1) / (CH_THREADS / WAVE);
-    const uint64_t cap = (uint64_t)cus * 32;
+    const uint64_t cap = (uint64_t)cus * 128;
     if (g > cap) g = cap;
     return (unsigned)(g ? g : 1);
 }
@@ -454,7 +456,7 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
               HW_HIGH_ANCHOR);
     PC_LAUNCH(K_CHAIN_STAIR, chain_stair_kernel, dim3(wave_grid((ns + CH_BATCH - 1) / CH_BATCH, cus)),
               dim3(CH_THREADS), 0, s, keys, ns, (const uint4 *)w.rec, w.aprev, w.anext, deepest, prev, next, w.cnt,
-              (const int32_t *)w.hdr);
+              w.open, (const int32_t *)w.hdr);
     const uint64_t tiles = (ns + SCAN_TILE - 1) / SCAN_TILE;
     PC_LAUNCH(K_CHAIN_SCAN, chain_scan_tiles_kernel, dim3((unsigned)tiles), dim3(SCAN_THREADS), 0, s, w.cnt, ns,
               w.tsum, (const int32_t *)w.hdr);
@@ -473,8 +475,8 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
     if (!carve_open(w, m, &o)) return generic(2);
 
     PC_LAUNCH(K_CHAIN_COMPACT, chain_compact_kernel, dim3(wave_grid((ns + CH_BATCH - 1) / CH_BATCH, cus)),
-              dim3(CH_THREADS), 0, s, keys, ns, (const uint4 *)w.rec, w.coff, deepest, prev, next, o.ckeys, o.cpos,
-              o.cflag);
+              dim3(CH_THREADS), 0, s, keys, ns, (const uint4 *)w.rec, (const uint4 *)w.open, w.coff, deepest,
+              o.ckeys, o.cpos, o.cflag);
     if ((st = pc_prev_next_use(o.ckeys, m, o.cprev, o.cnext, nullptr, o.ws, o.ws_bytes, stream)) != PC_OK)
         return st;
     PC_LAUNCH(K_FILL32, chain_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)o.ws, w.hdr,
