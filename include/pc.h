@@ -11,8 +11,9 @@
  * Common rules
  *   - Every array argument is DEVICE memory (hipMalloc / a torch tensor on the
  *     GPU) unless stated otherwise.  The caller owns all memory; the library
- *     never allocates or frees, and only pc_prev_next_chained and the
- *     read-back calls (pc_workspace_status, pc_prof_read) synchronise.
+ *     never allocates or frees, and only pc_prev_next_chained,
+ *     pc_stack_distance_runs and the read-back calls (pc_workspace_status,
+ *     pc_prof_read) synchronise.
  *     Scratch space comes only from
  *     the caller's workspace `ws` of at least the size the matching `*_ws`
  *     query returns (256-byte aligned).
@@ -182,6 +183,29 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
 size_t pc_stack_distance_ws(uint64_t n);
 pc_status pc_stack_distance(const uint32_t *prev, const uint32_t *next, uint64_t n,
                             uint32_t *dist, void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Exact LRU stack distance of every access, from the runs of the prev stream.
+ *
+ * Same dist as pc_stack_distance (Sec. 5; Appendix B).  When t - 1 and t are
+ * both warm and prev(t) = prev(t - 1) + 1, the reuse window of t is that of
+ * t - 1 shifted by one position, with one block leaving and one entering, so
+ * dist(t) = dist(t - 1); a maximal chain of such accesses is a run.  Chained
+ * block keys give about one run per request, so the call counts over runs
+ * instead of accesses: per run, the earlier runs whose previous uses come
+ * first (the previous uses of a run are one contiguous range, disjoint from
+ * every other run's), then the run's distance along all its accesses.
+ *
+ *   prev, next uint32[n] as produced by pc_prev_next_use; dist uint32[n] out.
+ * With more than n/16 + 1024 runs (streams without that structure) the call
+ * runs pc_stack_distance instead (same result).  It synchronises `stream`
+ * once (it reads the number of runs back).  Workspace words after the call:
+ * word 1 = 1 if pc_stack_distance ran, word 2 = the number of runs, word 3 =
+ * the number of cold accesses.
+ * ------------------------------------------------------------------------ */
+size_t pc_stack_distance_runs_ws(uint64_t n);
+pc_status pc_stack_distance_runs(const uint32_t *prev, const uint32_t *next, uint64_t n,
+                                 uint32_t *dist, void *ws, size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
  * Request-level residency (Sec. 3.1 "Simulator": every block of a request

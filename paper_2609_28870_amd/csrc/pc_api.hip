@@ -38,6 +38,11 @@ static const char *kernel_name(KernelId k) {
     case K_CHAIN_SCAN: return "chain_scan";
     case K_CHAIN_COMPACT: return "chain_compact";
     case K_CHAIN_MERGE: return "chain_merge";
+    case K_RUNS_COUNT: return "runs_count";
+    case K_RUNS_SCAN: return "runs_scan";
+    case K_RUNS_COMPACT: return "runs_compact";
+    case K_RUNS_MERGE: return "runs_merge";
+    case K_RUNS_FILL: return "runs_fill";
     case K_COUNT: break;
     }
     return "";

@@ -68,6 +68,11 @@ enum KernelId {
     K_CHAIN_SCAN,
     K_CHAIN_COMPACT,
     K_CHAIN_MERGE,
+    K_RUNS_COUNT,
+    K_RUNS_SCAN,
+    K_RUNS_COMPACT,
+    K_RUNS_MERGE,
+    K_RUNS_FILL,
     K_COUNT
 };
 

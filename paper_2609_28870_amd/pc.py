@@ -59,6 +59,10 @@ def lib():
     L.pc_prev_next_chained_ws.argtypes = [_u64, _u32]
     L.pc_prev_next_chained.restype = _st
     L.pc_prev_next_chained.argtypes = [_vp, _u64, _vp, _u32, _u32, _vp, _vp, _vp, _vp, _sz, _vp]
+    L.pc_stack_distance_runs_ws.restype = _sz
+    L.pc_stack_distance_runs_ws.argtypes = [_u64]
+    L.pc_stack_distance_runs.restype = _st
+    L.pc_stack_distance_runs.argtypes = [_vp, _vp, _u64, _vp, _vp, _sz, _vp]
     L.pc_stack_distance_ws.restype = _sz
     L.pc_stack_distance_ws.argtypes = [_u64]
     L.pc_stack_distance.restype = _st
@@ -252,6 +256,28 @@ def stack_distance(prev: torch.Tensor, nxt: torch.Tensor, dist: Optional[torch.T
         ws = workspace(L.pc_stack_distance_ws(n))
     check(L.pc_stack_distance(_ptr(prev), _ptr(nxt), n, _ptr(dist), _ptr(ws), ws.numel(), _stream()))
     return dist, ws
+
+
+def stack_distance_runs(prev: torch.Tensor, nxt: torch.Tensor, dist: Optional[torch.Tensor] = None,
+                        ws: Optional[torch.Tensor] = None):
+    """pc_stack_distance_runs: the same distances as stack_distance, counted
+    over the runs of the prev stream (synchronises the stream once)."""
+    L = lib()
+    n = prev.numel()
+    if dist is None:
+        dist = torch.empty(n, dtype=torch.int32, device=_dev())
+    if ws is None:
+        ws = workspace(L.pc_stack_distance_runs_ws(n))
+    check(L.pc_stack_distance_runs(_ptr(prev), _ptr(nxt), n, _ptr(dist), _ptr(ws), ws.numel(), _stream()))
+    return dist, ws
+
+
+def runs_info(ws: torch.Tensor) -> dict:
+    """What the last pc_stack_distance_runs call on this workspace did.
+    Synchronises."""
+    torch.cuda.current_stream().synchronize()
+    w = ws[:16].view(torch.int32).cpu().tolist()
+    return {"generic": bool(w[1]), "runs": w[2] & 0xFFFFFFFF, "cold": w[3] & 0xFFFFFFFF}
 
 
 def request_order(keys: torch.Tensor, blk_off: torch.Tensor, depth: Optional[torch.Tensor] = None,
@@ -480,7 +506,7 @@ class Pipeline:
         if residency == "session":
             self.ws_sd = workspace(L.pc_stack_distance_session_ws(n, tok_len.numel()))
         else:
-            self.ws_sd = workspace(L.pc_stack_distance_ws(n))
+            self.ws_sd = workspace(L.pc_stack_distance_runs_ws(n) if chained else L.pc_stack_distance_ws(n))
         if self.request:
             self.keys_r, self.depth_r = self.keys, self.depth   # hashed in recency order
             self.dist_req = torch.empty(n, dtype=torch.int32, device=dev)
@@ -499,12 +525,12 @@ class Pipeline:
             return
         if not self.request:
             self._prev_next(self.keys)
-            stack_distance(self.prev, self.next, self.dist, ws=self.ws_sd)
+            self._stack_distance()
             mrc_weighted(self.dist, self.caps, self.depth, self.next if self.with_nextuse else None,
                          self.alpha, self.beta, out=self.bins, ws=self.ws_mrc)
             return
         self._prev_next(self.keys_r)
-        stack_distance(self.prev, self.next, self.dist, ws=self.ws_sd)
+        self._stack_distance()
         stack_distance_req(self.prev, self.dist, self.blk_off, dist_req=self.dist_req, ws=self.ws_req)
         mrc_weighted(self.dist_req, self.caps, self.depth_r, None, self.alpha, self.beta,
                      out=self.bins, ws=self.ws_mrc)
@@ -515,6 +541,12 @@ class Pipeline:
                               deepest_first=self.request)
         else:
             prev_next_use(keys, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
+
+    def _stack_distance(self):
+        if self.chained:
+            stack_distance_runs(self.prev, self.next, self.dist, ws=self.ws_sd)
+        else:
+            stack_distance(self.prev, self.next, self.dist, ws=self.ws_sd)
 
     def high_key_passes_ran(self) -> bool:
         """Whether the last generic prev/next call also sorted by the high 32

@@ -86,6 +86,18 @@ def test_prev_next_chained_rejects_bad_arguments(L):
     assert L.pc_prev_next_chained(FAKE, n, FAKE, seqs, 0, FAKE, FAKE, None, FAKE, ws - 1, None) == -3
 
 
+def test_stack_distance_runs_rejects_bad_arguments(L):
+    n = 1000
+    ws = L.pc_stack_distance_runs_ws(n)
+    assert ws >= L.pc_stack_distance_ws(n)
+    assert L.pc_stack_distance_runs(FAKE, FAKE, 0xFFFFFFFF, FAKE, FAKE, 1 << 40, None) == -2
+    assert L.pc_stack_distance_runs(None, FAKE, n, FAKE, FAKE, ws, None) == -1
+    assert L.pc_stack_distance_runs(FAKE, None, n, FAKE, FAKE, ws, None) == -1
+    assert L.pc_stack_distance_runs(FAKE, FAKE, n, None, FAKE, ws, None) == -1
+    assert L.pc_stack_distance_runs(FAKE, FAKE, n, FAKE, None, ws, None) == -3
+    assert L.pc_stack_distance_runs(FAKE, FAKE, n, FAKE, FAKE, ws - 1, None) == -3
+
+
 def test_stack_distance_rejects_bad_arguments(L):
     n = 5000
     ws = L.pc_stack_distance_ws(n)
@@ -201,5 +213,5 @@ def test_profiling_table(L):
     names = [L.pc_prof_kernel_name(i).decode() for i in range(n)]
     assert "hash_blocks" in names and "sd_dominance_pass" in names and "mrc_hist" in names
     assert all(names) and len(set(names)) == n
-    assert names[-1] == "chain_merge" and "chain_stair" in names
+    assert names[-1] == "runs_fill" and "chain_stair" in names and "runs_merge" in names
     assert pc.prof_read() is not None
