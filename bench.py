@@ -43,6 +43,11 @@ ALGO_BYTES = {
     # chained prev/next: its own key, the two linked requests' keys at the
     # same depths, prev + next out
     "chain_stair": lambda B: 8 + 8 + 8 + 8,
+    # stack distance over runs: prev read by the count, compaction and fill,
+    # dist written by the fill
+    "runs_count": lambda B: 4,
+    "runs_compact": lambda B: 4,
+    "runs_fill": lambda B: 4 + 4,
 }
 # generic prev/next kernels: per element of the key streams they sort
 GENERIC_PN = ("sort_digit_hist", "sort_digit_scan", "sort_onesweep_pass", "link_partition", "perm_partition",
@@ -74,7 +79,8 @@ HIP_KERNEL = {"sort_onesweep_pass": "pc::sort_pass_kernel", "link_partition": "p
               "session_distance": "pc::sess_dist_kernel", "reuse_profile_walk": "pc::prof_walk_kernel",
               "reuse_profile_pack": "pc::prof_pack_kernel", "chain_stair": "pc::chain_stair_kernel",
               "chain_compact": "pc::chain_compact_kernel", "chain_anchor": "pc::chain_anchor_kernel",
-              "chain_merge": "pc::chain_merge_kernel"}
+              "chain_merge": "pc::chain_merge_kernel", "runs_count": "pc::runs_count_kernel",
+              "runs_compact": "pc::runs_compact_kernel", "runs_fill": "pc::runs_fill_kernel"}
 PROFILES = {"access": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9.md"),
             "request": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_request.md"),
             "session": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_session.md"),
@@ -240,7 +246,8 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 4 GiB device copy (for rocprof counter calibration)")
     ap.add_argument("--prev-next", default="chained", choices=["chained", "generic"],
-                    help="prev/next from the chain structure of the keys (default) or the generic sort")
+                    help="prev/next from the chain structure of the keys and the stack distance over runs "
+                         "(default), or the generic sort and the dominance count over accesses")
     ap.add_argument("--settle", type=float, default=20.0,
                     help="seconds to wait before touching the device (memory that another process "
                          "released just before is reclaimed in the background meanwhile)")
@@ -382,7 +389,7 @@ def main():
                    "session_distance": 8, "reuse_profile": 24}
 
     def stage_name(kid):
-        return stage_of.get(kid, "stack_distance" if kid.startswith("sd_") else "other")
+        return stage_of.get(kid, "stack_distance" if kid.startswith(("sd_", "runs_")) else "other")
 
     stages = {}
     for name, e in kernels.items():
@@ -445,6 +452,8 @@ def main():
         "stages": stages,
         "high_key_sort_passes": highs,
         "chained_prev_next": chain,
+        "stack_distance_runs": (pc.runs_info(pipe.ws_sd) if pipe.chained and not args.profile
+                                and not session_mode else None),
     }
     if args.profile:
         out["metric"] = "KV-block accesses/sec for hash+prev/next+workload characterisation; achieved HBM GB/s"
