@@ -43,11 +43,11 @@ ALGO_BYTES = {
     # chained prev/next: its own key, the two linked requests' keys at the
     # same depths, prev + next out
     "chain_stair": lambda B: 8 + 8 + 8 + 8,
-    # stack distance over runs: prev read by the count, compaction and fill,
-    # dist written by the fill
+    # stack distance over runs: prev read by the count and the compaction,
+    # dist written by the fill from the run list
     "runs_count": lambda B: 4,
     "runs_compact": lambda B: 4,
-    "runs_fill": lambda B: 4 + 4,
+    "runs_fill": lambda B: 4,
 }
 # generic prev/next kernels: per element of the key streams they sort
 GENERIC_PN = ("sort_digit_hist", "sort_digit_scan", "sort_onesweep_pass", "link_partition", "perm_partition",

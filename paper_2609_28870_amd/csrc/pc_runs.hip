@@ -28,7 +28,7 @@
 // Passes: count heads and cold accesses per 4096-position tile; scan; read
 // the number of runs back (the call synchronises once); compact the runs
 // (head's prev, head position, end position, cold count before the head);
-// merge levels; fill D along every run.  With more runs than 1/16 of the
+// merge levels; write D from the run list (prev is not read again).  With more runs than 1/16 of the
 // accesses plus 1024 the call runs pc_stack_distance instead.
 #include "pc_internal.h"
 
@@ -250,44 +250,69 @@ __global__ __launch_bounds__(256) void runs_merge_kernel(const uint32_t *__restr
     idx2[q] = idx[i];
 }
 
-// D along every run: cold -> none, else z + acc - p - 1 of the run's head.
-__global__ __launch_bounds__(RUN_THREADS) void runs_fill_kernel(const uint32_t *__restrict__ prev, uint64_t n,
-                                                                const uint2 *__restrict__ off,
-                                                                const uint32_t *__restrict__ rp,
-                                                                const uint32_t *__restrict__ rz,
-                                                                const uint32_t *__restrict__ acc,
+// Distance of every run, in place of its cold count: z + acc - p - 1.
+__global__ __launch_bounds__(256) void runs_dist_kernel(const uint32_t *__restrict__ rp,
+                                                        const uint32_t *__restrict__ acc, uint64_t r,
+                                                        uint32_t *__restrict__ rz) {
+    const uint64_t s = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (s < r) rz[s] = rz[s] + acc[s] - rp[s] - 1;
+}
+
+// D of every position from the run list alone: a warm position lies in
+// exactly one run [h, e], every other position is cold.  The runs that can
+// touch a tile are the one in progress at its start and those starting in
+// it; a thread finds the run at its first position by binary search and
+// walks on.
+__global__ __launch_bounds__(RUN_THREADS) void runs_fill_kernel(uint64_t n, uint64_t r, const uint2 *__restrict__ off,
+                                                                uint64_t tiles, const uint32_t *__restrict__ rh,
+                                                                const uint32_t *__restrict__ re,
+                                                                const uint32_t *__restrict__ rd,
                                                                 uint32_t *__restrict__ dist) {
-    __shared__ uint32_t tmp[RUN_THREADS / WAVE];
-    RunView v;
-    load_view(prev, n, v);
-    uint32_t heads = 0;
-#pragma unroll
-    for (int k = 0; k < RUN_ITEMS; ++k) heads += v.t0 + k < n && is_head(v.p[k], k ? v.p[k - 1] : v.before);
-    uint32_t th = 0;
-    uint32_t hs = off[blockIdx.x].x + block_excl_scan(heads, tmp, &th);
-    uint32_t d[RUN_ITEMS];
-    uint32_t cur = NONE;   // distance of the run in progress
-    if (hs > 0) {
-        const uint32_t s = hs - 1;
-        cur = rz[s] + acc[s] - rp[s] - 1;
+    // thread i holds positions tile0 + 1024 g + 4 i .. + 3 for g = 0..3
+    // (increasing), so each 16-byte store covers 1 KB across the wave
+    const uint64_t tile0 = (uint64_t)blockIdx.x * RUN_TILE;
+    const uint64_t t0 = tile0 + (uint64_t)threadIdx.x * 4;
+    const uint64_t first = off[blockIdx.x].x;
+    const int64_t lo = first ? (int64_t)first - 1 : 0;
+    const int64_t hi = blockIdx.x + 1 < tiles ? (int64_t)off[blockIdx.x + 1].x : (int64_t)r;
+    // last run in [lo, hi) with head <= t0, or lo - 1
+    int64_t a = lo, b = hi;
+    while (a < b) {
+        const int64_t m = (a + b) >> 1;
+        if (rh[m] <= t0) a = m + 1;
+        else b = m;
     }
+    int64_t s = a - 1;
+    // the current run's end and distance and the next run's head, in
+    // registers: loads only where a run starts
+    bool in_run = s >= lo;
+    uint64_t end = in_run ? re[s] : 0;
+    uint32_t dv = in_run ? rd[s] : NONE;
+    uint64_t next_head = s + 1 < hi ? rh[s + 1] : ~0ull;
+    const bool vec = (reinterpret_cast<uintptr_t>(dist) & 15) == 0;
 #pragma unroll
-    for (int k = 0; k < RUN_ITEMS; ++k) {
-        const uint32_t p = v.p[k];
-        if (v.t0 + k < n && is_head(p, k ? v.p[k - 1] : v.before)) {
-            cur = rz[hs] + acc[hs] - rp[hs] - 1;
-            ++hs;
+    for (int g = 0; g < RUN_ITEMS / 4; ++g) {
+        const uint64_t tg = t0 + (uint64_t)g * (RUN_THREADS * 4);
+        uint32_t d[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const uint64_t t = tg + k;
+            while (t >= next_head) {
+                ++s;
+                in_run = true;
+                end = re[s];
+                dv = rd[s];
+                next_head = s + 1 < hi ? rh[s + 1] : ~0ull;
+            }
+            d[k] = (in_run && end >= t) ? dv : NONE;
         }
-        d[k] = p == NONE ? NONE : cur;
-    }
-    if (v.t0 + RUN_ITEMS <= n && (reinterpret_cast<uintptr_t>(dist) & 15) == 0) {
-        uint4 *q = reinterpret_cast<uint4 *>(dist + v.t0);
+        if (vec && tg + 4 <= n) {
+            *reinterpret_cast<uint4 *>(dist + tg) = make_uint4(d[0], d[1], d[2], d[3]);
+        } else {
 #pragma unroll
-        for (int k = 0; k < RUN_ITEMS / 4; ++k) q[k] = make_uint4(d[4 * k], d[4 * k + 1], d[4 * k + 2], d[4 * k + 3]);
-    } else {
-#pragma unroll
-        for (int k = 0; k < RUN_ITEMS; ++k)
-            if (v.t0 + k < n) dist[v.t0 + k] = d[k];
+            for (int k = 0; k < 4; ++k)
+                if (tg + k < n) dist[tg + k] = d[k];
+        }
     }
 }
 
@@ -381,8 +406,12 @@ pc_status pc_stack_distance_runs(const uint32_t *prev, const uint32_t *next, uin
             cur ^= 1;
         }
     }
-    PC_LAUNCH(K_RUNS_FILL, runs_fill_kernel, dim3((unsigned)tiles), dim3(RUN_THREADS), 0, s, prev, n,
-              (const uint2 *)w.off, (const uint32_t *)w.rp, (const uint32_t *)w.rz, (const uint32_t *)w.acc, dist);
+    if (r > 0)
+        PC_LAUNCH(K_RUNS_MERGE, runs_dist_kernel, dim3((unsigned)((r + 255) / 256)), dim3(256), 0, s,
+                  (const uint32_t *)w.rp, (const uint32_t *)w.acc, r, w.rz);
+    PC_LAUNCH(K_RUNS_FILL, runs_fill_kernel, dim3((unsigned)tiles), dim3(RUN_THREADS), 0, s, n, r,
+              (const uint2 *)w.off, tiles, (const uint32_t *)w.rh, (const uint32_t *)w.re, (const uint32_t *)w.rz,
+              dist);
     return PC_OK;
 }
 
