@@ -40,9 +40,9 @@ ALGO_BYTES = {
     "session_distance": lambda B: 4 + 4,          # prev in; dist_sess out
     "reuse_profile_pack": lambda B: 4 + 8,        # next in; (next, request) out
     "reuse_profile_walk": lambda B: 4 + 8,        # prev (chain starts) and one (next, request) per step in
-    # chained prev/next: its own key, the two linked requests' keys at the
-    # same depths, prev + next out
-    "chain_stair": lambda B: 8 + 8 + 8 + 8,
+    # chained prev/next: its own key and the linked request's key at the same
+    # depth in, the prev link and its mirrored next link out
+    "chain_stair": lambda B: 8 + 8 + 4 + 4,
     # stack distance over runs: prev read by the count and the compaction,
     # dist written by the fill from the run list
     "runs_count": lambda B: 4,

@@ -18,10 +18,10 @@
 //      (~n/64 + n_seqs keys);
 //   2. staircase: one wave per slot (r, a) takes the request c of the
 //      anchor's previous use; lanes d = a*S .. a*S+63 compare r's and c's
-//      keys and every lane before the first mismatch links to c at depth d.
-//      The anchor's next use gives the next links the same way.  Both sides
-//      evaluate the same symmetric predicate, so a prev link r -> c at depth
-//      d exists exactly when the next link c -> r at depth d does;
+//      keys and every lane before the first mismatch links to c at depth d,
+//      writing the prev link at r and the mirrored next link at c (anchor
+//      links are one-to-one, so each slot has at most one such claimant,
+//      which also records the lanes it linked in the slot's claimed mask);
 //   3. every access left without a prev or a next link (first and last
 //      occurrences, and the lanes after a change of request inside a wave)
 //      is compacted in time order and the generic prev/next runs over them;
@@ -128,8 +128,8 @@ __global__ __launch_bounds__(CH_THREADS) void chain_anchor_kernel(
 // overlap across slots.
 constexpr int CH_BATCH = 2;
 
-// Links of one side for one slot: the lanes before the first depth at which
-// the slot's request and the linked anchor's request differ (both must cover
+// The prev links of one slot: the lanes before the first depth at which the
+// slot's request and the linked anchor's request differ (both must cover
 // the depth) link to the linked request at that depth; UNK elsewhere.
 __device__ __forceinline__ uint32_t stair_claim(const Slot &q, const Slot &c, uint64_t kr, uint64_t kc, int lane,
                                                 int deepest) {
@@ -139,44 +139,37 @@ __device__ __forceinline__ uint32_t stair_claim(const Slot &q, const Slot &c, ui
     return lane < lead ? (uint32_t)lane_pos(c, lane, deepest) : UNK;
 }
 
-// One wave per slot: prev / next staircase links of the slot's depths, the
-// lanes left without a prev and without a next link (two masks), and their
-// count.  A link to a filler slot or to
-// an anchor at another depth (equal keys there are a collision) claims
-// nothing.
+// One wave per slot: the prev links of the slot's depths and their mirrored
+// next links, the lanes left without a prev link (open[j].xy), and the
+// lanes the linked slot got a next link for (claimed[link]).  A link to a
+// filler slot or to an anchor at another depth (equal keys there are a
+// collision) claims nothing.
 __global__ __launch_bounds__(CH_THREADS) void chain_stair_kernel(
     const uint64_t *__restrict__ keys, uint64_t n_slots, const uint4 *__restrict__ rec,
-    const uint32_t *__restrict__ aprev, const uint32_t *__restrict__ anext, int deepest,
-    uint32_t *__restrict__ prev, uint32_t *__restrict__ next, uint32_t *__restrict__ cnt, uint4 *__restrict__ open,
-    const int32_t *__restrict__ hdr) {
+    const uint32_t *__restrict__ aprev, int deepest, uint32_t *__restrict__ prev, uint32_t *__restrict__ next,
+    uint4 *__restrict__ open, uint2 *__restrict__ claimed, const int32_t *__restrict__ hdr) {
     if (hdr[HW_BAD]) return;
     const int lane = threadIdx.x & (WAVE - 1);
     const uint64_t waves = (uint64_t)gridDim.x * (CH_THREADS / WAVE);
     const Slot none{0, 0, NONE};
     for (uint64_t j0 = ((uint64_t)blockIdx.x * (CH_THREADS / WAVE) + wave_id_uniform()) * CH_BATCH; j0 < n_slots;
          j0 += waves * CH_BATCH) {
-        Slot q[CH_BATCH], cp[CH_BATCH], cx[CH_BATCH];
-        uint32_t lp[CH_BATCH], lx[CH_BATCH];
+        Slot q[CH_BATCH], cp[CH_BATCH];
+        uint32_t lp[CH_BATCH];
 #pragma unroll
         for (int k = 0; k < CH_BATCH; ++k) {
             const bool in = j0 + k < n_slots;
             q[k] = in ? load_slot(rec, j0 + k) : none;
             lp[k] = in ? aprev[j0 + k] : NONE;
-            lx[k] = in ? anext[j0 + k] : NONE;
         }
 #pragma unroll
-        for (int k = 0; k < CH_BATCH; ++k) {
-            cp[k] = lp[k] != NONE ? load_slot(rec, lp[k]) : none;
-            cx[k] = lx[k] != NONE ? load_slot(rec, lx[k]) : none;
-        }
-        uint64_t kr[CH_BATCH], kp[CH_BATCH], kx[CH_BATCH];
+        for (int k = 0; k < CH_BATCH; ++k) cp[k] = lp[k] != NONE ? load_slot(rec, lp[k]) : none;
+        uint64_t kr[CH_BATCH], kp[CH_BATCH];
 #pragma unroll
         for (int k = 0; k < CH_BATCH; ++k) {
             const bool v = lane < (int)q[k].lanes;
             kr[k] = v ? keys[lane_pos(q[k], lane, deepest)] : 0;
             kp[k] = v && cp[k].depth == q[k].depth && lane < (int)cp[k].lanes ? keys[lane_pos(cp[k], lane, deepest)]
-                                                                              : ~kr[k];
-            kx[k] = v && cx[k].depth == q[k].depth && lane < (int)cx[k].lanes ? keys[lane_pos(cx[k], lane, deepest)]
                                                                               : ~kr[k];
         }
 #pragma unroll
@@ -184,19 +177,34 @@ __global__ __launch_bounds__(CH_THREADS) void chain_stair_kernel(
             if (j0 + k >= n_slots) break;
             const bool v = lane < (int)q[k].lanes;
             const uint32_t p = stair_claim(q[k], cp[k], kr[k], kp[k], lane, deepest);
-            const uint32_t x = stair_claim(q[k], cx[k], kr[k], kx[k], lane, deepest);
-            if (v) {
-                const uint64_t pr = lane_pos(q[k], lane, deepest);
-                prev[pr] = p;
-                next[pr] = x;
-            }
-            const uint64_t mp = ballot(v && p == UNK), mx = ballot(v && x == UNK);
+            const uint64_t pr = lane_pos(q[k], lane, deepest);
+            if (v) prev[pr] = p;
+            if (p != UNK) next[p] = (uint32_t)pr;
+            const uint64_t mp = ballot(v && p == UNK), mc = ballot(p != UNK);
             if (lane == 0) {
-                cnt[j0 + k] = (uint32_t)__popcll(mp | mx);
-                open[j0 + k] = make_uint4((uint32_t)mp, (uint32_t)(mp >> 32), (uint32_t)mx, (uint32_t)(mx >> 32));
+                open[j0 + k] = make_uint4((uint32_t)mp, (uint32_t)(mp >> 32), 0u, 0u);
+                if (lp[k] != NONE) claimed[lp[k]] = make_uint2((uint32_t)mc, (uint32_t)(mc >> 32));
             }
         }
     }
+}
+
+// Per slot: the lanes without a next link (valid and not claimed), into
+// open[j].zw, and the count of lanes open on either side.
+__global__ __launch_bounds__(256) void chain_count_kernel(uint64_t n_slots, const uint4 *__restrict__ rec,
+                                                          const uint2 *__restrict__ claimed, uint4 *__restrict__ open,
+                                                          uint32_t *__restrict__ cnt, const int32_t *__restrict__ hdr) {
+    if (hdr[HW_BAD]) return;
+    const uint64_t j = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= n_slots) return;
+    const uint32_t lanes = rec[j].z;
+    const uint64_t valid = lanes >= (uint32_t)WAVE ? ~0ull : (1ull << lanes) - 1;
+    const uint2 c = claimed[j];
+    const uint64_t mx = valid & ~((uint64_t)c.x | ((uint64_t)c.y << 32));
+    const uint4 o = open[j];
+    const uint64_t mp = (uint64_t)o.x | ((uint64_t)o.y << 32);
+    open[j] = make_uint4(o.x, o.y, (uint32_t)mx, (uint32_t)(mx >> 32));
+    cnt[j] = (uint32_t)__popcll(mp | mx);
 }
 
 // Exclusive scan of cnt[0 .. m) into out[0 .. m], out[m] = total: tile sums,
@@ -349,6 +357,7 @@ struct ChainWs {
     uint64_t *akeys;
     uint4 *rec;
     uint4 *open;
+    uint2 *claimed;
     uint32_t *aprev, *anext, *cnt, *coff, *tsum;
     void *aws;            // pc_prev_next_use workspace over the slots
     size_t aws_bytes;
@@ -367,6 +376,7 @@ static ChainWs carve_chain(void *ws, uint64_t n, uint32_t n_seqs) {
     w.akeys = c.take<uint64_t>(ns);
     w.rec = c.take<uint4>(ns);
     w.open = c.take<uint4>(ns);
+    w.claimed = c.take<uint2>(ns);
     w.aprev = c.take<uint32_t>(ns);
     w.anext = c.take<uint32_t>(ns);
     w.cnt = c.take<uint32_t>(ns);
@@ -454,9 +464,12 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
         return st;
     PC_LAUNCH(K_FILL32, chain_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)w.aws, w.hdr,
               HW_HIGH_ANCHOR);
+    if ((st = fill_u32(reinterpret_cast<uint32_t *>(w.claimed), 0u, 2 * ns, s)) != PC_OK) return st;
     PC_LAUNCH(K_CHAIN_STAIR, chain_stair_kernel, dim3(wave_grid((ns + CH_BATCH - 1) / CH_BATCH, cus)),
-              dim3(CH_THREADS), 0, s, keys, ns, (const uint4 *)w.rec, w.aprev, w.anext, deepest, prev, next, w.cnt,
-              w.open, (const int32_t *)w.hdr);
+              dim3(CH_THREADS), 0, s, keys, ns, (const uint4 *)w.rec, w.aprev, deepest, prev, next, w.open,
+              w.claimed, (const int32_t *)w.hdr);
+    PC_LAUNCH(K_CHAIN_SCAN, chain_count_kernel, dim3((unsigned)((ns + 255) / 256)), dim3(256), 0, s, ns,
+              (const uint4 *)w.rec, (const uint2 *)w.claimed, w.open, w.cnt, (const int32_t *)w.hdr);
     const uint64_t tiles = (ns + SCAN_TILE - 1) / SCAN_TILE;
     PC_LAUNCH(K_CHAIN_SCAN, chain_scan_tiles_kernel, dim3((unsigned)tiles), dim3(SCAN_THREADS), 0, s, w.cnt, ns,
               w.tsum, (const int32_t *)w.hdr);

@@ -28,8 +28,9 @@
 // Passes: count heads and cold accesses per 4096-position tile; scan; read
 // the number of runs back (the call synchronises once); compact the runs
 // (head's prev, head position, end position, cold count before the head);
-// merge levels; write D from the run list (prev is not read again).  With more runs than 1/16 of the
-// accesses plus 1024 the call runs pc_stack_distance instead.
+// merge levels; write D from the run list (prev is not read again).  With
+// more runs than 1/16 of the accesses plus 1024 the call runs
+// pc_stack_distance instead.
 #include "pc_internal.h"
 
 namespace pc {
@@ -46,8 +47,9 @@ constexpr int RW_PATH = 1;    // 0 = runs, 1 = pc_stack_distance
 constexpr int RW_RUNS = 2;    // number of runs
 constexpr int RW_COLD = 3;    // number of cold accesses
 
-// This thread's 16 consecutive prev values and the one before them (the
-// previous thread's last, across the tile edge from global memory).
+// This thread's 16 consecutive prev values and the ones just before and
+// after them (from the neighbouring lanes, or from memory across waves and
+// tiles).
 struct RunView {
     uint32_t p[RUN_ITEMS];
     uint32_t before;   // prev(t0 - 1), NONE at t = 0
