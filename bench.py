@@ -43,10 +43,11 @@ ALGO_BYTES = {
     # chained prev/next: its own key and the linked request's key at the same
     # depth in, the prev link and its mirrored next link out
     "chain_stair": lambda B: 8 + 8 + 4 + 4,
-    # stack distance over runs: prev read by the count and the compaction,
-    # dist written by the fill from the run list
+    # stack distance over runs: prev read once by the count (which keeps
+    # three bits per position for the compaction), dist written by the fill
+    # from the run list
     "runs_count": lambda B: 4,
-    "runs_compact": lambda B: 4,
+    "runs_compact": lambda B: 0.5,
     "runs_fill": lambda B: 4,
 }
 # generic prev/next kernels: per element of the key streams they sort

@@ -453,7 +453,12 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
         if ((g = fill_u32(reinterpret_cast<uint32_t *>(w.hdr + HW_PATH), 1u, 1, s)) != PC_OK) return g;
         return fill_u32(reinterpret_cast<uint32_t *>(w.hdr + HW_REASON), (uint32_t)reason, 1, s);
     };
-    if (n_seqs == 0) return generic(1);
+    if (n_seqs == 0) {   // n > 0 accesses in no request: an invalid layout
+        if ((st = fill_u32(reinterpret_cast<uint32_t *>(w.hdr + HW_STATUS), (uint32_t)DEV_ERR_BAD_LAYOUT, 1, s)) !=
+            PC_OK)
+            return st;
+        return generic(1);
+    }
 
     const uint64_t ns = chain_slots(n, n_seqs);
     PC_LAUNCH(K_CHAIN_ANCHOR, chain_layout_kernel, dim3((unsigned)((n_seqs + 255) / 256)), dim3(256), 0, s,

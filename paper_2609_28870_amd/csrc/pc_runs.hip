@@ -25,10 +25,11 @@
 // right block adds the sibling's prefix sum of len at that rank, and the
 // merged prefix sums follow from the two blocks' own.
 //
-// Passes: count heads and cold accesses per 4096-position tile; scan; read
-// the number of runs back (the call synchronises once); compact the runs
-// (head's prev, head position, end position, cold count before the head);
-// merge levels; write D from the run list (prev is not read again).  With
+// Passes: count heads and cold accesses per 4096-position tile, keeping
+// three bits per position (head, cold, last of a run); scan; read the number
+// of runs back (the call synchronises once); compact the runs from those
+// bits (head's prev, head position, end position, cold count before the
+// head); merge levels; write D from the run list.  prev is streamed once.  With
 // more runs than 1/16 of the accesses plus 1024 the call runs
 // pc_stack_distance instead.
 #include "pc_internal.h"
@@ -88,21 +89,35 @@ __device__ __forceinline__ bool is_head(uint32_t p, uint32_t before) {
     return p != NONE && (before == NONE || p != before + 1);
 }
 
+// Per 4096-position tile: the number of run heads and of cold accesses, and
+// per thread (16 positions) three bit masks: heads and cold accesses
+// (low / high half of .x) and last accesses of runs (.y).
 __global__ __launch_bounds__(RUN_THREADS) void runs_count_kernel(const uint32_t *__restrict__ prev, uint64_t n,
-                                                                 uint2 *__restrict__ counts) {
+                                                                 uint2 *__restrict__ counts,
+                                                                 uint2 *__restrict__ marks) {
     __shared__ uint32_t tmp[RUN_THREADS / WAVE];
     RunView v;
     load_view(prev, n, v);
-    uint32_t heads = 0, cold = 0;
+    uint32_t hm = 0, cm = 0, em = 0;
 #pragma unroll
     for (int k = 0; k < RUN_ITEMS; ++k) {
-        const bool in = v.t0 + k < n;
-        heads += in && is_head(v.p[k], k ? v.p[k - 1] : v.before);
-        cold += in && v.p[k] == NONE;
+        const uint64_t t = v.t0 + k;
+        const uint32_t p = v.p[k];
+        if (t < n) {
+            if (p == NONE) {
+                cm |= 1u << k;
+            } else {
+                if (is_head(p, k ? v.p[k - 1] : v.before)) hm |= 1u << k;
+                // last access of its run: the next one is cold, a head, or past the end
+                const uint32_t q = k + 1 < RUN_ITEMS ? v.p[k + 1] : v.after;
+                if (t + 1 >= n || q == NONE || q != p + 1) em |= 1u << k;
+            }
+        }
     }
+    marks[(uint64_t)blockIdx.x * RUN_THREADS + threadIdx.x] = make_uint2(hm | (cm << 16), em);
     uint32_t th = 0, tc = 0;
-    block_excl_scan(heads, tmp, &th);
-    block_excl_scan(cold, tmp, &tc);
+    block_excl_scan((uint32_t)__popc(hm), tmp, &th);
+    block_excl_scan((uint32_t)__popc(cm), tmp, &tc);
     if (threadIdx.x == 0) counts[blockIdx.x] = make_uint2(th, tc);
 }
 
@@ -172,42 +187,36 @@ __global__ __launch_bounds__(RSCAN_THREADS) void runs_scan_apply_kernel(const ui
 }
 
 // Per run s (in time order): p[s] = prev(head), h[s] = head position,
-// e[s] = last position, z[s] = cold accesses before the head.
+// e[s] = last position, z[s] = cold accesses before the head; from the
+// count pass's bit masks, reading prev only at the heads.
 __global__ __launch_bounds__(RUN_THREADS) void runs_compact_kernel(const uint32_t *__restrict__ prev, uint64_t n,
                                                                    const uint2 *__restrict__ off,
+                                                                   const uint2 *__restrict__ marks,
                                                                    uint32_t *__restrict__ rp, uint32_t *__restrict__ rh,
                                                                    uint32_t *__restrict__ re,
                                                                    uint32_t *__restrict__ rz) {
     __shared__ uint32_t tmp[RUN_THREADS / WAVE];
-    RunView v;
-    load_view(prev, n, v);
-    uint32_t heads = 0, cold = 0;
-#pragma unroll
-    for (int k = 0; k < RUN_ITEMS; ++k) {
-        const bool in = v.t0 + k < n;
-        heads += in && is_head(v.p[k], k ? v.p[k - 1] : v.before);
-        cold += in && v.p[k] == NONE;
-    }
+    const uint64_t t0 = (uint64_t)blockIdx.x * RUN_TILE + (uint64_t)threadIdx.x * RUN_ITEMS;
+    const uint2 mk = marks[(uint64_t)blockIdx.x * RUN_THREADS + threadIdx.x];
+    const uint32_t hm = mk.x & 0xFFFFu, cm = mk.x >> 16, em = mk.y;
     uint32_t th = 0, tc = 0;
     const uint2 o = off[blockIdx.x];
-    uint32_t hs = o.x + block_excl_scan(heads, tmp, &th);   // runs started before this thread's first t
-    uint32_t cs = o.y + block_excl_scan(cold, tmp, &tc);
-#pragma unroll
-    for (int k = 0; k < RUN_ITEMS; ++k) {
-        const uint64_t t = v.t0 + k;
-        const uint32_t p = v.p[k];
-        if (t < n && p == NONE) ++cs;
-        if (t < n && p != NONE) {
-            if (is_head(p, k ? v.p[k - 1] : v.before)) {
-                rp[hs] = p;
-                rh[hs] = (uint32_t)t;
-                rz[hs] = cs;
-                ++hs;
-            }
-            // last access of its run: the next one is cold, a head, or past the end
-            const uint32_t q = k + 1 < RUN_ITEMS ? v.p[k + 1] : v.after;
-            if (t + 1 >= n || q == NONE || q != p + 1) re[hs - 1] = (uint32_t)t;
-        }
+    const uint32_t hs0 = o.x + block_excl_scan((uint32_t)__popc(hm), tmp, &th);   // runs started before t0
+    const uint32_t cs0 = o.y + block_excl_scan((uint32_t)__popc(cm), tmp, &tc);
+    // heads: one per set bit, numbered in position order
+    for (uint32_t m = hm; m; m &= m - 1) {
+        const int k = __builtin_ctz(m);
+        const uint32_t below = (1u << k) - 1;
+        const uint32_t s = hs0 + (uint32_t)__popc(hm & below);
+        rp[s] = prev[t0 + k];
+        rh[s] = (uint32_t)(t0 + k);
+        rz[s] = cs0 + (uint32_t)__popc(cm & below);
+    }
+    // run ends: the run is the last one started at or before the position
+    for (uint32_t m = em; m; m &= m - 1) {
+        const int k = __builtin_ctz(m);
+        const uint32_t upto = (k == 31) ? ~0u : (2u << k) - 1;
+        re[hs0 + (uint32_t)__popc(hm & upto) - 1] = (uint32_t)(t0 + k);
     }
 }
 
@@ -328,7 +337,7 @@ struct RunsWs {
     int32_t *hdr;
     void *sd;   // pc_stack_distance workspace (the fallback); the arrays below live inside it
     size_t sd_bytes;
-    uint2 *counts, *tsum, *off;
+    uint2 *counts, *tsum, *off, *marks;
     uint32_t *rp, *rh, *re, *rz, *acc, *key[2], *pre[2], *idx[2];
     size_t bytes;
 };
@@ -344,6 +353,7 @@ static RunsWs carve_runs(void *ws, uint64_t n) {
     w.counts = c.take<uint2>(tiles);
     w.tsum = c.take<uint2>((tiles + RSCAN_TILE - 1) / RSCAN_TILE + 1);
     w.off = c.take<uint2>(tiles);
+    w.marks = c.take<uint2>(tiles * RUN_THREADS);
     w.rp = c.take<uint32_t>(rm);
     w.rh = c.take<uint32_t>(rm);
     w.re = c.take<uint32_t>(rm);
@@ -379,7 +389,8 @@ pc_status pc_stack_distance_runs(const uint32_t *prev, const uint32_t *next, uin
     if (st != PC_OK || n == 0) return st;
     const uint64_t tiles = (n + RUN_TILE - 1) / RUN_TILE;
     const uint64_t stiles = (tiles + RSCAN_TILE - 1) / RSCAN_TILE;
-    PC_LAUNCH(K_RUNS_COUNT, runs_count_kernel, dim3((unsigned)tiles), dim3(RUN_THREADS), 0, s, prev, n, w.counts);
+    PC_LAUNCH(K_RUNS_COUNT, runs_count_kernel, dim3((unsigned)tiles), dim3(RUN_THREADS), 0, s, prev, n, w.counts,
+              w.marks);
     PC_LAUNCH(K_RUNS_SCAN, runs_scan_tiles_kernel, dim3((unsigned)stiles), dim3(RSCAN_THREADS), 0, s,
               (const uint2 *)w.counts, tiles, w.tsum);
     PC_LAUNCH(K_RUNS_SCAN, runs_scan_top_kernel, dim3(1), dim3(RSCAN_THREADS), 0, s, w.tsum, stiles, w.hdr);
@@ -395,7 +406,7 @@ pc_status pc_stack_distance_runs(const uint32_t *prev, const uint32_t *next, uin
         return fill_u32(reinterpret_cast<uint32_t *>(w.hdr + RW_PATH), 1u, 1, s);
     }
     PC_LAUNCH(K_RUNS_COMPACT, runs_compact_kernel, dim3((unsigned)tiles), dim3(RUN_THREADS), 0, s, prev, n,
-              (const uint2 *)w.off, w.rp, w.rh, w.re, w.rz);
+              (const uint2 *)w.off, (const uint2 *)w.marks, w.rp, w.rh, w.re, w.rz);
     if (r > 0) {
         const unsigned rg = (unsigned)((r + 255) / 256);
         PC_LAUNCH(K_RUNS_MERGE, runs_init_kernel, dim3(rg), dim3(256), 0, s, (const uint32_t *)w.rp,
