@@ -102,6 +102,23 @@ def test_hash_tiny_trace_bit_exact():
     assert np.array_equal(gk, ok) and np.array_equal(gd, od)
 
 
+@pytest.mark.parametrize("B", [32, 48, 64, 256])
+def test_hash_multiples_of_16_aligned_and_not(B):
+    # 16-byte aligned streams take 16-byte loads, streams shifted by one token
+    # the scalar path; both must give the oracle's keys
+    tr = pcgen.make_trace("tiny")
+    ok, od = oracle.hash_trace(tr, B)
+    gk, gd = gpu_hash(tr, B)
+    assert np.array_equal(gk, ok) and np.array_equal(gd, od)
+    tr2 = pcgen.subtrace(tr, 0, tr.n_requests)
+    tr2.tok_start = tr.tok_start + np.uint64(1)
+    tr2.tok_len = np.where(tr.tok_len > 0, tr.tok_len - 1, 0).astype(np.uint32)
+    tr2.tokens = np.concatenate([tr.tokens, np.zeros(1, np.int32)])
+    ok2, od2 = oracle.hash_trace(tr2, B)
+    gk2, gd2 = gpu_hash(tr2, B)
+    assert np.array_equal(gk2, ok2) and np.array_equal(gd2, od2)
+
+
 @pytest.mark.parametrize("B", [2, 6, 64, 256])
 def test_hash_other_block_sizes(B):
     tr = pcgen.make_trace("tiny")
