@@ -435,7 +435,7 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": "%s trace (%s), block size %d" % (
-                args.workload, "70%% chat / 30%% agent sessions up to 2e9 context tokens"
+                args.workload, "70% chat / 30% agent sessions up to 2e9 context tokens"
                 if args.workload == "full" else "%s sessions" % (args.sessions or "default"), B),
             "n_block_accesses": n_blocks,
             "n_requests": trace.n_requests,
