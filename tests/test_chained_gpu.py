@@ -170,3 +170,30 @@ def test_empty_and_single():
         if keys.size == 0:
             continue
         exact(keys, off)
+
+
+@pytest.mark.parametrize("residency", ["access", "request", "session"])
+def test_pipeline_chained_equals_generic(residency):
+    # the same trace through both prev/next and stack-distance paths: every
+    # output equal (each path is also checked against the oracle elsewhere)
+    tr = pcgen.make_trace("agent", n_sessions=80)
+    up = pc.upload_trace(tr, 16)
+    caps = pc.to_dev_u64(tr.caps(16))
+    outs = []
+    for chained in (True, False):
+        p = pc.Pipeline(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"], caps, 16,
+                        7, 3, residency=residency, session=up["session"], chained=chained)
+        p.run()
+        torch.cuda.synchronize()
+        assert all(v == 0 for v in p.status().values()), p.status()
+        o = {"prev": pc.as_u32(p.prev), "next": pc.as_u32(p.next), "dist": pc.as_u32(p.dist),
+             "bins": pc.bins_to_host(p.bins)}
+        if residency == "request":
+            o["dist_req"] = pc.as_u32(p.dist_req)
+        outs.append(o)
+    a, b = outs
+    for k in a:
+        if k == "bins":
+            assert a[k] == b[k]
+        else:
+            assert np.array_equal(a[k], b[k]), k
