@@ -197,3 +197,20 @@ def test_pipeline_chained_equals_generic(residency):
             assert a[k] == b[k]
         else:
             assert np.array_equal(a[k], b[k]), k
+
+
+def test_profiler_chained_equals_generic():
+    tr = pcgen.make_trace("chat", n_sessions=150)
+    up = pc.upload_trace(tr, 16)
+    edges = pc.to_dev_u64(np.array([10 ** k for k in range(1, 11)], np.uint64))
+    outs = []
+    for chained in (True, False):
+        p = pc.Profiler(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"], up["session"],
+                        up["ts_us"], edges, 16, chained=chained)
+        p.run()
+        torch.cuda.synchronize()
+        assert all(v == 0 for v in p.status().values()), p.status()
+        outs.append((pc.as_u32(p.prev), pc.as_u32(p.next), pc.hists_to_host(p.reuse), pc.hists_to_host(p.sessions)))
+    (pa, na, ra, sa), (pb, nb, rb, sb) = outs
+    assert np.array_equal(pa, pb) and np.array_equal(na, nb)
+    assert ra == rb and sa == sb
