@@ -82,11 +82,22 @@ HIP_KERNEL = {"sort_onesweep_pass": "pc::sort_pass_kernel", "link_partition": "p
               "chain_compact": "pc::chain_compact_kernel", "chain_anchor": "pc::chain_anchor_kernel",
               "chain_merge": "pc::chain_merge_kernel", "runs_count": "pc::runs_count_kernel",
               "runs_compact": "pc::runs_compact_kernel", "runs_fill": "pc::runs_fill_kernel"}
-PROFILES = {"access": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9.md"),
-            "request": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_request.md"),
-            "session": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_session.md"),
-            "profile": os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_profile.md")}
-PROFILE = PROFILES["access"]
+# committed counter summaries, by (mode, prev/next path); a run whose path has
+# none reports no counter traffic
+PROFILES = {("access", "chained"): os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9.md"),
+            ("request", "chained"): os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_request.md"),
+            ("session", "chained"): os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_session.md"),
+            ("profile", "chained"): os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_profile.md"),
+            ("access", "generic"): os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_generic.md")}
+PROFILE = PROFILES[("access", "chained")]
+
+
+def profile_for(mode, prev_next, workload="full", block_size=16):
+    """The committed summary for this run's kernels, or None: summaries are
+    taken on the full trace at block size 16 only."""
+    if workload != "full" or block_size != 16:
+        return None
+    return PROFILES.get((mode, prev_next))
 
 
 def source_sha256():
@@ -103,6 +114,8 @@ def source_sha256():
 
 
 def _profile_blob():
+    if PROFILE is None:
+        return None
     try:
         text = open(PROFILE).read()
         blob = json.loads(text[text.index("```json") + 7:text.rindex("```")])
@@ -189,20 +202,40 @@ def profile_summary(rp, sp):
             "intra_session_gap_us_p50_upper": _quantile(sp["gap"], e, 0.5)}
 
 
+def cpu_model():
+    """The host CPU's model name (Linux /proc/cpuinfo), or None."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def baseline_threads(n_caps):
+    """One capacity simulation per thread, as many threads as capacities but
+    no more than the host's cores and a one-GPU share of them (16)."""
+    return max(1, min(n_caps, os.cpu_count() or 1, 16))
+
+
 def cpu_baseline(trace, caps, alpha, beta, budget_accesses, request=False):
-    """The oracle (plain C, one thread) over the first requests of the same
-    trace: hash, prev/next, next-use histogram and one LRU simulation per
-    capacity edge -- the same outputs as one GPU step.  In request mode:
-    hash and the request-level bins (one pinned-request simulation per
-    feasible edge, the recency-list walk for the others)."""
+    """The oracle (plain C) over the first requests of the same trace: hash,
+    prev/next, next-use histogram and one LRU simulation per capacity edge --
+    the same outputs as one GPU step.  Requests are hashed by ranges on a
+    thread pool and the per-capacity simulations run one per thread.  In
+    request mode: hash and the request-level bins (one pinned-request
+    simulation per feasible edge, the recency-list walk for the others)."""
     import oracle
     import pcgen
+    threads = baseline_threads(len(caps))
     nb = (trace.tok_len // np.uint32(trace.block_size)).astype(np.int64)
     r = int(np.searchsorted(np.cumsum(nb), budget_accesses)) + 1
     r = min(r, trace.n_requests)
     sub = pcgen.subtrace(trace, 0, r)
     t0 = time.perf_counter()
-    keys, depth = oracle.hash_trace(sub)
+    keys, depth = oracle.hash_trace(sub, threads=threads)
     ids = oracle.key_ids(keys)
     if request == "profile":
         bo = sub.blk_off()
@@ -211,20 +244,66 @@ def cpu_baseline(trace, caps, alpha, beta, budget_accesses, request=False):
         oracle.session_profile(bo, sub.session, ts, PROFILE_EDGES_US, 1 << 16, 2048)
         what = "reuse and session profiles"
     elif request == "session":
-        oracle.mrc_bins_session(keys, sub.blk_off(), sub.session.astype(np.uint32), caps, depth, alpha, beta, ids)
+        oracle.mrc_bins_session(keys, sub.blk_off(), sub.session.astype(np.uint32), caps, depth, alpha, beta, ids,
+                                threads=threads)
         what = "prev/next + session-level bins (%d per-capacity session LRU simulations)" % len(caps)
     elif request:
-        oracle.mrc_bins_req(keys, sub.blk_off(), caps, depth, alpha, beta, ids)
+        oracle.mrc_bins_req(keys, sub.blk_off(), caps, depth, alpha, beta, ids, threads=threads)
         what = "request-level bins"
     else:
         _, nxt = oracle.prev_next(keys, ids)
         oracle.nextuse_hist(nxt, caps)
-        oracle.mrc_bins(keys, caps, depth, alpha, beta, ids)
+        oracle.mrc_bins(keys, caps, depth, alpha, beta, ids, threads=threads)
         what = "prev/next + %d per-capacity LRU simulations" % len(caps)
     dt = time.perf_counter() - t0
-    return {"value": keys.size / dt, "unit": "block-accesses/s", "cores": 1, "kind": "oracle",
-            "sample": "first %d requests (%d block accesses) of the same trace; hash + %s; %.1f s" % (
-                r, keys.size, what, dt)}
+    return {"value": keys.size / dt, "unit": "block-accesses/s", "cores": threads, "kind": "oracle",
+            "nproc": os.cpu_count(), "cpu_model": cpu_model(),
+            "sample": "first %d requests (%d block accesses) of the same trace; hash + %s; %.1f s on %d threads "
+                      "(hashing by request ranges, one capacity simulation per thread)" % (
+                          r, keys.size, what, dt, threads)}
+
+
+GOLDEN_FULL = os.path.join(ROOT, "tests", "golden", "fullsize_full.txt")
+
+
+def read_fullsize_golden(path):
+    """The oracle's full-size reference: n, per-capacity (cap, hits,
+    depth sum over hits) and the next-use histogram."""
+    g = {"caps": []}
+    with open(path) as f:
+        for line in f:
+            w = line.split("#", 1)[0].split()
+            if not w:
+                continue
+            if w[0] == "cap":
+                g["caps"].append((int(w[1]), int(w[2]), int(w[3]), int(w[4], 16)))
+            elif w[0] == "nextuse":
+                g["nextuse"] = [int(x) for x in w[1:]]
+            elif w[0] in ("n", "requests", "distinct", "depth_total"):
+                g[w[0]] = int(w[1])
+            elif w[0].startswith("fp_"):
+                g[w[0]] = int(w[1], 16)
+    return g
+
+
+def check_against_golden(bins, caps, n, path):
+    """Compare this run's bins with the oracle's full-size reference (hits and
+    depth sums at every capacity, next-use histogram); raises on a mismatch."""
+    g = read_fullsize_golden(path)
+    if g["n"] != n or [c for c, _, _, _ in g["caps"]] != [int(c) for c in caps]:
+        raise SystemExit("reference %s is for another trace or capacity list" % path)
+    h = d = 0
+    for k, (c, hits, dsum, _) in enumerate(g["caps"]):
+        h += bins["count"][k]
+        d += bins["depthsum"][k]
+        if h != hits or d != dsum:
+            raise SystemExit("bins differ from the oracle's reference at capacity %d: hits %d vs %d, "
+                             "depth sum %d vs %d" % (c, h, hits, d, dsum))
+    if sum(bins["count"]) != n or bins["depthsum"] and sum(bins["depthsum"]) != g["depth_total"]:
+        raise SystemExit("bin totals differ from the oracle's reference")
+    if bins["nextuse"] != g["nextuse"]:
+        raise SystemExit("next-use histogram differs from the oracle's reference")
+    return {"reference": os.path.relpath(path, ROOT), "capacities": len(g["caps"]), "bins_match": True}
 
 
 def main():
@@ -280,7 +359,7 @@ def main():
     request = args.residency == "request"
     session_mode = args.residency == "session"
     global PROFILE
-    PROFILE = PROFILES["profile" if args.profile else args.residency]
+    PROFILE = profile_for("profile" if args.profile else args.residency, args.prev_next, args.workload, B)
     if args.profile:
         prof_edges = pc.to_dev_u64(np.array(PROFILE_EDGES_US, np.uint64))
         pipe = pc.Profiler(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
@@ -412,6 +491,12 @@ def main():
         # the curves themselves (exact integers -> float64 ratios)
         bins = pc.bins_to_host(pipe.bins)
         hr, csr = pc.curves(bins["count"], bins["cost"])
+    # the last timed step's bins against the oracle's full-size reference
+    oracle_check = None
+    if (not args.profile and args.residency == "access" and args.workload == "full" and B == 16
+            and args.sessions is None and os.path.exists(GOLDEN_FULL)):
+        oracle_check = check_against_golden(bins, caps_np, n_blocks, GOLDEN_FULL)
+        log("bins match the oracle's full-size reference at all %d capacities" % oracle_check["capacities"])
     cb = None
     sample = args.cpu_sample if args.cpu_sample is not None else (1_000_000 if request else 100_000_000)
     if sample > 0:
@@ -449,6 +534,7 @@ def main():
         },
         "roofline": roof,
         "cpu_baseline": cb,
+        "oracle_check": oracle_check,
         "kernels": kernels,
         "stages": stages,
         "high_key_sort_passes": highs,

@@ -42,6 +42,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
@@ -80,7 +81,13 @@ def lib():
         L.orc_stack_distance_bit.argtypes = [_u32p, ctypes.c_uint64, _u32p]
         L.orc_lru_sim.restype = ctypes.c_int
         L.orc_lru_sim.argtypes = [_u32p, _u32p, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64,
-                                  _u64p, _u64p, _u8p]
+                                  _u64p, _u64p, _u8p, _u64p]
+        L.orc_fp_u32.restype = ctypes.c_uint64
+        L.orc_fp_u32.argtypes = [_u32p, ctypes.c_uint64, ctypes.c_uint64]
+        L.orc_dist_bins.restype = ctypes.c_int
+        L.orc_dist_bins.argtypes = [_u32p, ctypes.c_uint64, ctypes.c_uint64, _u64p, ctypes.c_uint32, _u64p, _u64p]
+        L.orc_fp_u64.restype = ctypes.c_uint64
+        L.orc_fp_u64.argtypes = [_u64p, ctypes.c_uint64, ctypes.c_uint64]
         L.orc_stack_distance_req_walk.restype = ctypes.c_int
         L.orc_stack_distance_req_walk.argtypes = [_u32p, _u64p, ctypes.c_uint64, ctypes.c_uint64, _u32p]
         L.orc_stack_distance_req_bit.restype = ctypes.c_int
@@ -117,32 +124,70 @@ def step(x: int, w: int) -> int:
     return int(lib().orc_step(x & (2 ** 64 - 1), w & (2 ** 64 - 1)))
 
 
-def hash_requests(tokens, tok_start, tok_len, block_size=16, parent=None, root=0):
+def block_digest(tokens):
+    """Digest of one block: S folded over its token-pair words from 0."""
+    t = _c(tokens, np.int32)
+    if t.size < 2 or t.size % 2:
+        raise ValueError("a block has an even number of tokens")
+    return int(lib().orc_block_digest(_p(t, _i32p), t.size))
+
+
+def hash_requests(tokens, tok_start, tok_len, block_size=16, parent=None, root=0, threads=1):
     """Keys and depths of every full block of every request, request-major.
 
     key(b) = S(key(b-1), digest(block b)), key(-1) = root or parent[r];
     digest = S folded over the block's token-pair words from 0;
-    S(x, w) = mix64((x xor w) + 0x9E3779B97F4A7C15)."""
+    S(x, w) = mix64((x xor w) + 0x9E3779B97F4A7C15).
+    With threads > 1, contiguous ranges of requests are hashed by separate
+    threads into their own slices of the output (requests are independent)."""
     if block_size < 2 or block_size % 2:
         raise ValueError("block size must be even and >= 2")
     tokens = _c(tokens, np.int32)
     tok_start = _c(tok_start, np.uint64)
     tok_len = _c(tok_len, np.uint32)
-    n = int((tok_len.astype(np.uint64) // np.uint64(block_size)).sum())
+    nb = tok_len.astype(np.uint64) // np.uint64(block_size)
+    off = np.zeros(tok_len.size + 1, np.uint64)
+    np.cumsum(nb, out=off[1:])
+    n = int(off[-1])
     keys = np.empty(n, np.uint64)
     depth = np.empty(n, np.uint32)
     par = _c(parent, np.uint64) if parent is not None else None
-    got = lib().orc_hash_requests(_p(tokens, _i32p), _p(tok_start, _u64p), _p(tok_len, _u32p),
-                                  tok_len.size, block_size,
-                                  _p(par, _u64p) if par is not None else None, root,
-                                  _p(keys, _u64p), _p(depth, _u32p))
-    assert got == n
+
+    def part(r0, r1):
+        o = int(off[r0])
+        got = lib().orc_hash_requests(
+            _p(tokens, _i32p), _p(tok_start[r0:r1], _u64p), _p(tok_len[r0:r1], _u32p), r1 - r0, block_size,
+            _p(par[r0:r1], _u64p) if par is not None else None, root, _p(keys[o:], _u64p),
+            _p(depth[o:], _u32p))
+        assert got == int(off[r1]) - o
+
+    R = tok_len.size
+    if threads <= 1 or R < 2 * threads:
+        if R:
+            part(0, R)
+    else:
+        # split by accesses, so every thread gets about the same work
+        cuts = np.searchsorted(off, np.linspace(0, n, threads + 1)[1:-1].astype(np.uint64))
+        bounds = [0] + sorted(set(int(c) for c in cuts)) + [R]
+        with ThreadPoolExecutor(threads) as ex:
+            list(ex.map(lambda ab: part(*ab), [(a, b) for a, b in zip(bounds[:-1], bounds[1:]) if b > a]))
     return keys, depth
 
 
-def hash_trace(trace, block_size=None):
+def fingerprint(a, t0=0):
+    """sum over t of mix64(mix64(t0 + t + 1) + a[t]) mod 2^64 for a uint32 or
+    uint64 array (a whole-array check for arrays too large to store)."""
+    a = np.asarray(a)
+    if a.dtype in (np.uint32, np.int32):
+        a = _c(a.view(np.uint32) if a.dtype == np.int32 else a, np.uint32)
+        return int(lib().orc_fp_u32(_p(a, _u32p), a.size, t0))
+    a = _c(a.view(np.uint64) if a.dtype == np.int64 else a, np.uint64)
+    return int(lib().orc_fp_u64(_p(a, _u64p), a.size, t0))
+
+
+def hash_trace(trace, block_size=None, threads=1):
     return hash_requests(trace.tokens, trace.tok_start, trace.tok_len,
-                         block_size or trace.block_size)
+                         block_size or trace.block_size, threads=threads)
 
 
 def key_ids(keys):
@@ -182,22 +227,29 @@ def stack_distance_bit(prev):
     return d
 
 
-def lru(keys, caps, depth=None, ids=None, flags=False):
-    """Per capacity: (hits, sum of depth over hits[, per-access hit flags])."""
+def lru(keys, caps, depth=None, ids=None, flags=False, threads=1, fingerprints=False):
+    """Per capacity: (hits, sum of depth over hits[, fingerprint][, per-access
+    hit flags]); the fingerprint is the sum of mix64(t + 1) over the hits t.
+    With threads > 1 the capacities are simulated concurrently, one
+    simulation per thread (each is the same single-threaded list walk)."""
     if ids is None:
         ids = key_ids(keys)
     id_, n_ids = ids
     dep = _c(depth, np.uint32) if depth is not None else None
-    out = []
-    for c in caps:
+
+    def one(c):
         h = ctypes.c_uint64(0)
         dh = ctypes.c_uint64(0)
+        fp = ctypes.c_uint64(0)
         fl = np.empty(id_.size, np.uint8) if flags else None
         assert lib().orc_lru_sim(_p(id_, _u32p), _p(dep, _u32p) if dep is not None else None,
                                  id_.size, n_ids, int(c), ctypes.byref(h), ctypes.byref(dh),
-                                 _p(fl, _u8p) if fl is not None else None) == 0
-        out.append((h.value, dh.value, fl) if flags else (h.value, dh.value))
-    return out
+                                 _p(fl, _u8p) if fl is not None else None,
+                                 ctypes.byref(fp) if fingerprints else None) == 0
+        r = (h.value, dh.value) + ((fp.value,) if fingerprints else ())
+        return r + (fl,) if flags else r
+
+    return _per_capacity(one, caps, threads)
 
 
 def belady(keys, caps, ids=None, nxt=None, flags=False):
@@ -217,7 +269,7 @@ def belady(keys, caps, ids=None, nxt=None, flags=False):
     return out
 
 
-def mrc_bins(keys, caps, depth=None, alpha=1, beta=0, ids=None):
+def mrc_bins(keys, caps, depth=None, alpha=1, beta=0, ids=None, threads=1):
     """Bins over the capacity edges, from one LRU simulation per capacity.
 
     Bin k (k < K) holds the accesses that hit at caps[k] but not at the
@@ -228,7 +280,7 @@ def mrc_bins(keys, caps, depth=None, alpha=1, beta=0, ids=None):
     n = keys.size
     if depth is None:
         depth = np.zeros(n, np.uint32)
-    res = lru(keys, caps, depth, ids)
+    res = lru(keys, caps, depth, ids, threads=threads)
     count, dsum = [], []
     ph, pd = 0, 0
     for h, dh in res:
@@ -258,11 +310,12 @@ def curves(count, cost):
     return hr, csr
 
 
-def nextuse_hist(nxt, caps):
+def nextuse_hist(nxt, caps, t0=0):
     """Histogram of next(t) - t over the capacity edges (never reused -> last
-    bin); bin k = number of edges <= gap."""
+    bin); bin k = number of edges <= gap.  ``nxt`` may be the slice of a
+    longer array that starts at position t0."""
     nxt = np.asarray(nxt, np.uint32)
-    t = np.arange(nxt.size, dtype=np.uint64)
+    t = np.arange(t0, t0 + nxt.size, dtype=np.uint64)
     caps = np.asarray(caps, np.uint64)
     hist = [0] * (caps.size + 1)
     none = nxt == NONE
@@ -273,6 +326,21 @@ def nextuse_hist(nxt, caps):
         hist[i] = int(bc[i])
     hist[caps.size] += int(none.sum())
     return hist
+
+
+def dist_bins(dist, caps, t0=0, count=None, fp=None):
+    """Capacity bins of a distance array (the pc_mrc_weighted convention)
+    and, per bin, the sum of mix64(t + 1) over its accesses t.  Prefix sums
+    give the hits and the hit-set fingerprint at every capacity.  Adds into
+    ``count`` / ``fp`` (uint64[K+1]) when given, so a long array can be
+    binned in pieces; returns them."""
+    d = _c(dist, np.uint32)
+    cp = _c(caps, np.uint64)
+    k = cp.size
+    count = np.zeros(k + 1, np.uint64) if count is None else count
+    fp = np.zeros(k + 1, np.uint64) if fp is None else fp
+    assert lib().orc_dist_bins(_p(d, _u32p), d.size, t0, _p(cp, _u64p), k, _p(count, _u64p), _p(fp, _u64p)) == 0
+    return count, fp
 
 
 # ------------------------------------------------------------ request level
@@ -309,7 +377,7 @@ def stack_distance_req_bit(keys, blk_off, ids=None):
     return d
 
 
-def lru_req(keys, blk_off, caps, depth=None, ids=None, flags=False):
+def lru_req(keys, blk_off, caps, depth=None, ids=None, flags=False, threads=1):
     """Per capacity: (hits, depth sum over hits[, flags]) of a request-level
     LRU cache, or None where the capacity is below the largest request."""
     if ids is None:
@@ -317,8 +385,8 @@ def lru_req(keys, blk_off, caps, depth=None, ids=None, flags=False):
     id_, n_ids = ids
     bo, ns = _req(blk_off)
     dep = _c(depth, np.uint32) if depth is not None else None
-    out = []
-    for c in caps:
+
+    def one(c):
         h = ctypes.c_uint64(0)
         dh = ctypes.c_uint64(0)
         fl = np.empty(id_.size, np.uint8) if flags else None
@@ -326,11 +394,21 @@ def lru_req(keys, blk_off, caps, depth=None, ids=None, flags=False):
                                    ns, n_ids, int(c), ctypes.byref(h), ctypes.byref(dh),
                                    _p(fl, _u8p) if fl is not None else None)
         if rc == -3:
-            out.append(None)
-            continue
+            return None
         assert rc == 0
-        out.append((h.value, dh.value, fl) if flags else (h.value, dh.value))
-    return out
+        return (h.value, dh.value, fl) if flags else (h.value, dh.value)
+
+    return _per_capacity(one, caps, threads)
+
+
+def _per_capacity(one, caps, threads):
+    """[one(c) for c in caps], on a thread pool when threads > 1 (each call
+    is one single-threaded simulation; ctypes releases the GIL)."""
+    caps = list(caps)
+    if threads <= 1 or len(caps) <= 1:
+        return [one(c) for c in caps]
+    with ThreadPoolExecutor(min(threads, len(caps))) as ex:
+        return list(ex.map(one, caps))
 
 
 def max_request_blocks(blk_off):
@@ -338,7 +416,7 @@ def max_request_blocks(blk_off):
     return int((bo[1:] - bo[:-1]).max()) if bo.size > 1 else 0
 
 
-def mrc_bins_req(keys, blk_off, caps, depth=None, alpha=1, beta=0, ids=None):
+def mrc_bins_req(keys, blk_off, caps, depth=None, alpha=1, beta=0, ids=None, threads=1):
     """Bins over the capacity edges from one request-level simulation per
     capacity.  Only feasible edges (>= the largest request) are simulated;
     the bins of infeasible edges hold the accesses whose request-level
@@ -351,7 +429,7 @@ def mrc_bins_req(keys, blk_off, caps, depth=None, alpha=1, beta=0, ids=None):
     caps = [int(c) for c in caps]
     mx = max_request_blocks(blk_off)
     feas = [c >= mx and c > 0 for c in caps]
-    sim = lru_req(keys, blk_off, [c for c, f in zip(caps, feas) if f], depth, ids)
+    sim = lru_req(keys, blk_off, [c for c, f in zip(caps, feas) if f], depth, ids, threads=threads)
     it = iter(sim)
     res = []
     d = None
@@ -397,7 +475,7 @@ def stack_distance_session_walk(keys, blk_off, sess, ids=None):
     return d
 
 
-def lru_session(keys, blk_off, sess, caps, depth=None, ids=None, flags=False):
+def lru_session(keys, blk_off, sess, caps, depth=None, ids=None, flags=False, threads=1):
     """Per capacity: (hits, depth sum over hits[, flags]) of a session-level
     LRU cache simulated literally."""
     if ids is None:
@@ -406,26 +484,27 @@ def lru_session(keys, blk_off, sess, caps, depth=None, ids=None, flags=False):
     bo, ns = _req(blk_off)
     sv, n_sess = _sess(sess, ns)
     dep = _c(depth, np.uint32) if depth is not None else None
-    out = []
-    for c in caps:
+
+    def one(c):
         h = ctypes.c_uint64(0)
         dh = ctypes.c_uint64(0)
         fl = np.empty(id_.size, np.uint8) if flags else None
         assert lib().orc_session_sim(_p(id_, _u32p), _p(dep, _u32p) if dep is not None else None, _p(bo, _u64p),
                                      _p(sv, _u32p), ns, n_ids, n_sess, int(c), ctypes.byref(h), ctypes.byref(dh),
                                      _p(fl, _u8p) if fl is not None else None) == 0
-        out.append((h.value, dh.value, fl) if flags else (h.value, dh.value))
-    return out
+        return (h.value, dh.value, fl) if flags else (h.value, dh.value)
+
+    return _per_capacity(one, caps, threads)
 
 
-def mrc_bins_session(keys, blk_off, sess, caps, depth=None, alpha=1, beta=0, ids=None):
+def mrc_bins_session(keys, blk_off, sess, caps, depth=None, alpha=1, beta=0, ids=None, threads=1):
     """Bins over the capacity edges from one session-level simulation per
     capacity (same layout as ``mrc_bins``)."""
     keys = _c(keys, np.uint64)
     n = keys.size
     if depth is None:
         depth = np.zeros(n, np.uint32)
-    res = lru_session(keys, blk_off, sess, caps, depth, ids)
+    res = lru_session(keys, blk_off, sess, caps, depth, ids, threads=threads)
     count, dsum = [], []
     ph, pd = 0, 0
     for h, dh in res:

@@ -38,7 +38,9 @@
 /* token-pair words, then chained from the parent block.               */
 /* ------------------------------------------------------------------ */
 
-uint64_t orc_mix64(uint64_t z)
+/* The step and the finalizer are kept file-local (and inlined) for the
+ * hashing and fingerprint loops below; orc_mix64 / orc_step export them. */
+static inline uint64_t mix64(uint64_t z)
 {
     z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
     z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
@@ -46,23 +48,29 @@ uint64_t orc_mix64(uint64_t z)
 }
 
 /* one step: S(x, w) = mix64((x xor w) + golden gamma) */
-uint64_t orc_step(uint64_t x, uint64_t w)
+static inline uint64_t step(uint64_t x, uint64_t w)
 {
-    return orc_mix64((x ^ w) + 0x9E3779B97F4A7C15ull);
+    return mix64((x ^ w) + 0x9E3779B97F4A7C15ull);
 }
+
+uint64_t orc_mix64(uint64_t z) { return mix64(z); }
+
+uint64_t orc_step(uint64_t x, uint64_t w) { return step(x, w); }
 
 /* digest of one block of B tokens (B even): fold S over the B/2 words
  * w_k = tok[2k] | tok[2k+1] << 32, starting from 0 */
-uint64_t orc_block_digest(const int32_t *tok, uint32_t B)
+static inline uint64_t block_digest(const int32_t *tok, uint32_t B)
 {
     uint64_t d = 0;
     for (uint32_t k = 0; k < B / 2; k++) {
         uint64_t lo = (uint64_t)(uint32_t)tok[2 * k];
         uint64_t hi = (uint64_t)(uint32_t)tok[2 * k + 1];
-        d = orc_step(d, lo | (hi << 32));
+        d = step(d, lo | (hi << 32));
     }
     return d;
 }
+
+uint64_t orc_block_digest(const int32_t *tok, uint32_t B) { return block_digest(tok, B); }
 
 /* Hash every full block of every request, request by request.
  * Request r covers tokens[tok_start[r] .. tok_start[r]+tok_len[r]).
@@ -81,7 +89,7 @@ uint64_t orc_hash_requests(const int32_t *tokens, const uint64_t *tok_start,
         uint32_t nb = tok_len[r] / B;
         const int32_t *t = tokens + tok_start[r];
         for (uint32_t b = 0; b < nb; b++) {
-            key = orc_step(key, orc_block_digest(t + (uint64_t)b * B, B));
+            key = step(key, block_digest(t + (uint64_t)b * B, B));
             keys[out] = key;
             if (depth) depth[out] = b;
             out++;
@@ -101,24 +109,75 @@ static uint64_t slot_of(uint64_t key, uint64_t mask)
 }
 
 /* id[t] = index of key[t] among distinct keys in order of first access.
- * Returns the number of distinct keys, or (uint64_t)-1 on allocation failure. */
+ * The table starts small and doubles whenever it is half full, so its size
+ * follows the number of distinct keys, not the number of accesses.  The
+ * slot of a key a few accesses ahead is prefetched (a hint only).
+ * Returns the number of distinct keys, or (uint64_t)-1 on allocation failure
+ * or when there are 2^32 - 1 or more distinct keys. */
 uint64_t orc_key_ids(const uint64_t *keys, uint64_t n, uint32_t *id)
 {
-    uint64_t cap = 16;
-    while (cap < 2 * n + 2) cap <<= 1;
+    uint64_t cap = 1u << 16;
     uint64_t *tk = (uint64_t *)malloc(cap * sizeof(uint64_t));
     uint32_t *tv = (uint32_t *)malloc(cap * sizeof(uint32_t));
     if (!tk || !tv) { free(tk); free(tv); return (uint64_t)-1; }
     for (uint64_t i = 0; i < cap; i++) tv[i] = ORC_NONE;
     uint64_t mask = cap - 1, distinct = 0;
+    const uint64_t ahead = 16;
     for (uint64_t t = 0; t < n; t++) {
+        if (t + ahead < n) {
+            uint64_t ps = slot_of(keys[t + ahead], mask);
+            __builtin_prefetch(&tk[ps]);
+            __builtin_prefetch(&tv[ps]);
+        }
         uint64_t s = slot_of(keys[t], mask);
         while (tv[s] != ORC_NONE && tk[s] != keys[t]) s = (s + 1) & mask;
-        if (tv[s] == ORC_NONE) { tk[s] = keys[t]; tv[s] = (uint32_t)distinct++; }
+        if (tv[s] == ORC_NONE) {
+            if (distinct >= ORC_NONE) { free(tk); free(tv); return (uint64_t)-1; }
+            tk[s] = keys[t];
+            tv[s] = (uint32_t)distinct++;
+            if (2 * distinct >= cap) {
+                /* double the table and re-insert every key */
+                uint64_t ncap = cap * 2, nmask = ncap - 1;
+                uint64_t *nk = (uint64_t *)malloc(ncap * sizeof(uint64_t));
+                uint32_t *nv = (uint32_t *)malloc(ncap * sizeof(uint32_t));
+                if (!nk || !nv) { free(nk); free(nv); free(tk); free(tv); return (uint64_t)-1; }
+                for (uint64_t i = 0; i < ncap; i++) nv[i] = ORC_NONE;
+                for (uint64_t i = 0; i < cap; i++) {
+                    if (tv[i] == ORC_NONE) continue;
+                    uint64_t q = slot_of(tk[i], nmask);
+                    while (nv[q] != ORC_NONE) q = (q + 1) & nmask;
+                    nk[q] = tk[i];
+                    nv[q] = tv[i];
+                }
+                free(tk); free(tv);
+                tk = nk; tv = nv; cap = ncap; mask = nmask;
+                id[t] = (uint32_t)(distinct - 1);
+                continue;
+            }
+        }
         id[t] = tv[s];
     }
     free(tk); free(tv);
     return distinct;
+}
+
+/* Fingerprints of arrays too large to keep: sum over positions t of
+ * mix64(mix64(t0 + t + 1) + a[t]) mod 2^64.  Every term depends on both the
+ * position and the value, so changing, dropping or moving one element
+ * changes the sum (up to a 64-bit collision).  t0 lets a long array be
+ * fingerprinted in pieces: the sums of the pieces add up. */
+uint64_t orc_fp_u32(const uint32_t *a, uint64_t n, uint64_t t0)
+{
+    uint64_t s = 0;
+    for (uint64_t t = 0; t < n; t++) s += mix64(mix64(t0 + t + 1) + (uint64_t)a[t]);
+    return s;
+}
+
+uint64_t orc_fp_u64(const uint64_t *a, uint64_t n, uint64_t t0)
+{
+    uint64_t s = 0;
+    for (uint64_t t = 0; t < n; t++) s += mix64(mix64(t0 + t + 1) + a[t]);
+    return s;
 }
 
 /* prev[t] = last earlier position with the same key, next[t] = first later
@@ -212,16 +271,19 @@ int orc_stack_distance_bit(const uint32_t *prev, uint64_t n, uint32_t *dist)
  * resident when accessed is a hit; otherwise it is inserted at the front and,
  * if the cache then holds more than cap blocks, the least recently used one
  * is evicted.  cap = 0 never hits.
- * Outputs: hit count, sum of depth over hits, optional per-access hit flags. */
+ * Outputs: hit count, sum of depth over hits, optional per-access hit flags,
+ * optional fingerprint of the hit set: sum of mix64(t + 1) over the hits t
+ * (mod 2^64), which names which accesses hit, not only how many. */
 int orc_lru_sim(const uint32_t *id, const uint32_t *depth, uint64_t n, uint64_t n_ids,
-                uint64_t cap, uint64_t *hits_out, uint64_t *depth_hits_out, uint8_t *hit_flag)
+                uint64_t cap, uint64_t *hits_out, uint64_t *depth_hits_out, uint8_t *hit_flag,
+                uint64_t *fp_out)
 {
     uint32_t *nx = (uint32_t *)malloc((n_ids + 1) * sizeof(uint32_t));
     uint32_t *pv = (uint32_t *)malloc((n_ids + 1) * sizeof(uint32_t));
     uint8_t *in = (uint8_t *)calloc(n_ids + 1, 1);
     if (!nx || !pv || !in) { free(nx); free(pv); free(in); return -1; }
     uint32_t head = ORC_NONE, tail = ORC_NONE;
-    uint64_t size = 0, hits = 0, dh = 0;
+    uint64_t size = 0, hits = 0, dh = 0, fp = 0;
     for (uint64_t t = 0; t < n; t++) {
         uint32_t u = id[t];
         int hit = 0;
@@ -233,6 +295,7 @@ int orc_lru_sim(const uint32_t *id, const uint32_t *depth, uint64_t n, uint64_t 
             hit = 1;
             hits++;
             if (depth) dh += depth[t];
+            if (fp_out) fp += mix64(t + 1);
             if (u != head) { /* move to front */
                 nx[pv[u]] = nx[u];
                 if (nx[u] != ORC_NONE) pv[nx[u]] = pv[u]; else tail = pv[u];
@@ -255,6 +318,7 @@ int orc_lru_sim(const uint32_t *id, const uint32_t *depth, uint64_t n, uint64_t 
     }
     *hits_out = hits;
     if (depth_hits_out) *depth_hits_out = dh;
+    if (fp_out) *fp_out = fp;
     free(nx); free(pv); free(in);
     return 0;
 }
@@ -598,5 +662,34 @@ int orc_stack_distance_session_walk(const uint32_t *id, const uint64_t *blk_off,
         head = s;
     }
     free(last); free(nx); free(pv); free(fp); free(seen);
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* Capacity bins of a distance array, with the hit-set fingerprint of   */
+/* each bin: bin k < K holds the accesses with caps[k-1] <= D < caps[k]  */
+/* (caps[-1] = 0), bin K the cold ones and D >= caps[K-1].  An access    */
+/* hits at caps[k] exactly when its bin is <= k, so prefix sums of the   */
+/* bins give hits and the hit-set fingerprint (sum of mix64(t0 + t + 1)) */
+/* at every capacity.  count and fp have K + 1 entries and are added to. */
+/* ------------------------------------------------------------------ */
+int orc_dist_bins(const uint32_t *dist, uint64_t n, uint64_t t0, const uint64_t *caps, uint32_t K,
+                  uint64_t *count, uint64_t *fp)
+{
+    for (uint64_t t = 0; t < n; t++) {
+        uint32_t d = dist[t];
+        uint32_t b = K;
+        if (d != ORC_NONE) {
+            /* number of edges <= d */
+            uint32_t lo = 0, hi = K;
+            while (lo < hi) {
+                uint32_t mid = (lo + hi) / 2;
+                if (caps[mid] <= (uint64_t)d) lo = mid + 1; else hi = mid;
+            }
+            b = lo;
+        }
+        count[b] += 1;
+        fp[b] += mix64(t0 + t + 1);
+    }
     return 0;
 }

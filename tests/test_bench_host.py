@@ -32,7 +32,7 @@ def test_every_timed_kernel_has_algorithmic_bytes():
 
 @pytest.mark.parametrize("mode", ["access", "request", "session", "profile"])
 def test_committed_profiles_parse(mode):
-    path = bench.PROFILES[mode]
+    path = bench.PROFILES[(mode, "chained")]
     text = open(path).read()
     blob = json.loads(text[text.index("```json") + 7:text.rindex("```")])
     assert len(blob["source_sha256"]) == 64
@@ -49,7 +49,7 @@ def test_committed_profiles_parse(mode):
 
 
 def test_traffic_only_for_the_sources_it_was_taken_with(monkeypatch, tmp_path):
-    text = open(bench.PROFILES["access"]).read()
+    text = open(bench.PROFILES[("access", "chained")]).read()
     blob = json.loads(text[text.index("```json") + 7:text.rindex("```")])
     for sha, want in ((bench.source_sha256(), True), ("0" * 64, False)):
         blob["source_sha256"] = sha
@@ -85,3 +85,51 @@ def test_quantile_and_profile_summary():
     assert s["sessions"] == 4
     # the top 10% of 4 sessions is the largest one: 7 of 10 blocks
     assert s["footprint_top10pct_share"] == 0.7
+
+
+def test_profile_is_chosen_by_mode_and_path(monkeypatch):
+    assert bench.profile_for("access", "chained") == bench.PROFILES[("access", "chained")]
+    assert bench.profile_for("access", "chained", "chat") is None
+    assert bench.profile_for("access", "chained", "full", 64) is None
+    # a path without a committed summary reports no counter traffic
+    monkeypatch.setattr(bench, "PROFILE", bench.profile_for("request", "generic"))
+    assert bench.PROFILE is None
+    assert bench.measured_traffic("hash_blocks") is None and bench.measured_stage_bytes(lambda k: k) is None
+
+
+def test_cpu_baseline_reports_threads_nproc_and_model():
+    import numpy as np
+    import pcgen
+    tr = pcgen.make_trace("tiny")
+    cb = bench.cpu_baseline(tr, tr.caps(), 1, 0, 20_000)
+    assert cb["cores"] == bench.baseline_threads(tr.caps().size) >= 1
+    assert cb["nproc"] == os.cpu_count()
+    assert cb["kind"] == "oracle" and cb["value"] > 0 and "threads" in cb["sample"]
+    assert "cpu_model" in cb
+
+
+def test_golden_check_accepts_the_oracle_and_rejects_a_change(tmp_path):
+    # a reference written the way tests/golden/make_fullsize.py writes it,
+    # for the tiny trace, checked against the oracle's own bins
+    import numpy as np
+    import oracle
+    import pcgen
+    tr = pcgen.make_trace("tiny")
+    caps = tr.caps()
+    keys, depth = oracle.hash_trace(tr)
+    prev, nxt = oracle.prev_next(keys)
+    sims = oracle.lru(keys, [int(c) for c in caps], depth, fingerprints=True)
+    nu = oracle.nextuse_hist(nxt, caps)
+    p = tmp_path / "ref.txt"
+    with open(p, "w") as f:
+        f.write("n %d\ndepth_total %d\nnextuse %s\n" % (keys.size, int(depth.sum()), " ".join(map(str, nu))))
+        for c, (h, dh, fp) in zip(caps, sims):
+            f.write("cap %d %d %d 0x%016x\n" % (int(c), h, dh, fp))
+    count, dsum, cost = oracle.mrc_bins(keys, caps, depth)
+    bins = {"count": count, "depthsum": dsum, "nextuse": nu}
+    assert bench.check_against_golden(bins, caps, keys.size, str(p))["bins_match"]
+    bad = dict(bins, count=list(count))
+    bad["count"][3] += 1
+    bad["count"][4] -= 1
+    with pytest.raises(SystemExit):
+        bench.check_against_golden(bad, caps, keys.size, str(p))

@@ -1,20 +1,25 @@
 """Parity at the benchmark's full size and launch configuration.
 
-The full-scale mixed trace (2e9 context tokens, ~2.1e9 block accesses) and
-the full chat-shaped trace (20,000 sessions, ~2.2e8 block accesses) run
-through the same Pipeline bench.py times.  The oracle cannot redo the whole
-trace, so it checks:
+Three traces run through the same Pipeline bench.py times: the chat-shaped
+trace (20,000 sessions, ~2.2e8 block accesses), the full-scale mixed trace
+(2e9 context tokens, ~2.1e9 block accesses) and the same mix up to 2.2e9
+context tokens (~2.3e9 accesses, so positions pass 2^31).  They are checked
+against the oracle's full-size references (``tests/golden/fullsize_*.txt``,
+written by ``tests/golden/make_fullsize.py`` from ``oracle/`` alone):
 
-* keys of sampled requests (hashed one by one by the oracle);
-* exact windows: distances and prev links only depend on the past, so for a
-  window [a, b) of the trace the oracle's own run over that window gives the
-  exact prev/next/dist of every access whose previous use lies inside it
-  (and the first window, a = 0, gives every access in it);
-* properties that hold at any size, checked with plain torch ops on the GPU
-  (independent of libpc): prev/next are inverse links between equal keys,
-  cold accesses equal first occurrences, and the bins equal a torch
-  bucketize of the distances.
+* every array (keys, depth, prev, next, dist) through a position-keyed
+  fingerprint of all its elements;
+* every capacity's LRU hit count, depth sum over the hits and hit-set
+  fingerprint (which accesses hit), from the GPU's bins and distances;
+* the next-use histogram and the number of distinct blocks.
+
+Besides, the oracle recomputes sampled requests' keys and three exact
+windows of the trace (distances and links only depend on the past), the
+distances of the runs path equal the generic dominance count's element by
+element, and properties that hold at any size are checked with plain torch
+ops on the GPU (prev/next are inverse links between equal keys).
 """
+import os
 import sys
 
 import numpy as np
@@ -23,21 +28,45 @@ import torch
 
 import oracle
 import pcgen
+from fingerprints import array_fp, hit_fps
 from paper_2609_28870_amd import pc
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(1500)]
 NONE = pc.NONE
 P_LIN = 3_000_000_000
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+# workload name -> (pcgen config, context-token target override)
+WORKLOADS = {"chat": ("chat", None), "full": ("full", None), "full_2g2": ("full", 2_200_000_000)}
 
 
 def say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-@pytest.fixture(scope="module", params=["full", "chat"])
+def read_reference(name):
+    g = {"caps": []}
+    with open(os.path.join(GOLDEN, "fullsize_%s.txt" % name)) as f:
+        for line in f:
+            w = line.split("#", 1)[0].split()
+            if not w:
+                continue
+            if w[0] == "cap":
+                g["caps"].append((int(w[1]), int(w[2]), int(w[3]), int(w[4], 16)))
+            elif w[0] == "nextuse":
+                g["nextuse"] = [int(x) for x in w[1:]]
+            elif w[0].startswith("fp_"):
+                g[w[0]] = int(w[1], 16)
+            elif w[0] != "workload":
+                g[w[0]] = int(w[1])
+    return g
+
+
+@pytest.fixture(scope="module", params=["chat", "full", "full_2g2"])
 def full(request):
     assert torch.cuda.is_available()
-    tr = pcgen.make_trace(request.param)
+    cfg, target = WORKLOADS[request.param]
+    say(request.param, "generating the trace")
+    tr = pcgen.make_trace(cfg, target_tokens=target)
     say(request.param, "trace generated:", tr.n_requests, "requests", tr.n_blocks(), "accesses")
     caps = tr.caps()
     B = 16
@@ -46,9 +75,71 @@ def full(request):
                     pc.to_dev_u64(caps), B, 2 * B * P_LIN, 2 * B * B)
     p.run()
     torch.cuda.synchronize()
-    say("pipeline done, status", p.status())
+    say(request.param, "pipeline done, status", p.status())
+    p.reference = read_reference(request.param)
+    p.name = request.param
     yield tr, caps, p
-    del p
+    del p, up
+    torch.cuda.empty_cache()
+
+
+def test_reference_is_for_this_trace(full):
+    tr, caps, p = full
+    g = p.reference
+    assert g["n"] == p.n and g["requests"] == tr.n_requests
+    assert [c for c, _, _, _ in g["caps"]] == [int(c) for c in caps]
+    if p.name == "full_2g2":
+        assert p.n > 2 ** 31
+
+
+def test_all_arrays_match_the_oracle(full):
+    _, _, p = full
+    g = p.reference
+    for name, t in (("keys", p.keys), ("depth", p.depth), ("prev", p.prev), ("next", p.next), ("dist", p.dist)):
+        got = array_fp(t)
+        say(p.name, name, "fingerprint", hex(got))
+        assert got == g["fp_" + name], name
+
+
+def test_every_capacity_matches_the_oracle(full):
+    _, caps, p = full
+    g = p.reference
+    bins = pc.bins_to_host(p.bins)
+    h = d = 0
+    for k, (c, hits, dsum, _) in enumerate(g["caps"]):
+        h += bins["count"][k]
+        d += bins["depthsum"][k]
+        assert (h, d) == (hits, dsum), c
+    assert sum(bins["count"]) == p.n and sum(bins["depthsum"]) == g["depth_total"]
+    assert bins["nextuse"] == g["nextuse"]
+    # which accesses hit, at every capacity, from the GPU's distances
+    got = hit_fps(p.dist, torch.tensor(caps.astype(np.int64), device="cuda"))
+    assert got == [(hits, fp) for _, hits, _, fp in g["caps"]]
+
+
+def test_cold_accesses_are_the_distinct_blocks(full):
+    _, _, p = full
+    n = p.n
+    chunk = 1 << 27
+    cold = 0
+    for lo in range(0, n, chunk):
+        cold += int((p.prev[lo:lo + chunk] == -1).sum())
+    assert cold == p.reference["distinct"]
+
+
+def test_runs_distances_equal_the_generic_dominance_count(full):
+    _, _, p = full
+    info = pc.runs_info(p.ws_sd)
+    say(p.name, "stack distance over runs:", info)
+    assert not info["generic"]
+    ref, ws = pc.stack_distance(p.prev, p.next)
+    torch.cuda.synchronize()
+    assert pc.workspace_status(ws) == 0
+    del ws
+    chunk = 1 << 28
+    for lo in range(0, p.n, chunk):
+        assert torch.equal(ref[lo:lo + chunk], p.dist[lo:lo + chunk]), lo
+    del ref
     torch.cuda.empty_cache()
 
 
@@ -81,12 +172,14 @@ def window_requests(tr, a, b):
     return r0, r1, int(off[r0])
 
 
-@pytest.mark.parametrize("where", ["start", "middle", "end"])
+@pytest.mark.parametrize("where", ["start", "middle", "high", "end"])
 def test_exact_windows(full, where):
     tr, _, p = full
     n = p.n
     m = 3_000_000
-    a = {"start": 0, "middle": n // 2, "end": n - m}[where]
+    if where == "high" and n < 2 ** 31 + 2 * m:
+        pytest.skip("positions stay below 2^31 on this trace")
+    a = {"start": 0, "middle": n // 2, "high": 2 ** 31 + m, "end": n - m}[where]
     r0, r1, base = window_requests(tr, a, a + m)
     keys, _ = oracle.hash_requests(tr.tokens, tr.tok_start[r0:r1], tr.tok_len[r0:r1], 16)
     keys = keys[a - base:a - base + m]

@@ -85,6 +85,56 @@ def test_parent_chaining_equals_one_pass():
     assert np.all(rooted != full)
 
 
+def _split_words(words):
+    """int32 tokens whose packed words (tok[2k] | tok[2k+1] << 32) are `words`."""
+    toks = []
+    for w in words:
+        toks += [w & 0xFFFFFFFF, w >> 32]
+    return np.array(toks, np.uint32).view(np.int32)
+
+
+def _published():
+    return {int(k): int(v, 16) for k, v in read_golden("splitmix64_seed0.txt")}
+
+
+def test_four_token_block_folds_words_in_order_and_chains():
+    # Published splitmix64 outputs only: out_k = mix64(k G).  With w0 = 0 the
+    # first fold step is S(0, 0) = out1; with w1 = out1 ^ G the second is
+    # mix64(2G) = out2, which is the digest; with root = out2 ^ 2G the key is
+    # mix64(3G) = out3.  A reversed fold, a hi/lo swap inside a word, or a
+    # digest that is not chained from the root would all miss out3.
+    out = _published()
+    toks = _split_words([0, out[1] ^ G])
+    assert oracle.block_digest(toks) == out[2]
+    keys, depth = oracle.hash_requests(*_req([toks]), 4, root=out[2] ^ ((2 * G) & M64))
+    assert int(keys[0]) == out[3] and list(depth) == [0]
+    # the same block under a parent instead of the root
+    keys, _ = oracle.hash_requests(*_req([toks]), 4, parent=[out[2] ^ ((2 * G) & M64)])
+    assert int(keys[0]) == out[3]
+
+
+def test_sixteen_token_block_from_published_outputs():
+    # Eight words chosen so that the fold visits out1, out2, out3, out1,
+    # out3, out2, out2, out1: word k = d_{k-1} ^ (j - 1) G sends the digest
+    # to mix64(j G) = out_j.  Then root = out1 ^ 2G gives the key out3.
+    out = _published()
+    path = [1, 2, 3, 1, 3, 2, 2, 1]
+    words, d = [], 0
+    for j in path:
+        words.append(d ^ (((j - 1) * G) & M64))
+        d = out[j]
+    toks = _split_words(words)
+    assert oracle.block_digest(toks) == out[1]
+    keys, _ = oracle.hash_requests(*_req([toks]), 16, root=out[1] ^ ((2 * G) & M64))
+    assert int(keys[0]) == out[3]
+    # a two-block request: the second block's key chains from the first key
+    keys2, depth2 = oracle.hash_requests(*_req([np.concatenate([toks, toks])]), 16,
+                                         root=out[1] ^ ((2 * G) & M64))
+    assert int(keys2[0]) == out[3] and list(depth2) == [0, 1]
+    # reversed word order must not give the same digest
+    assert oracle.block_digest(_split_words(words[::-1])) != out[1]
+
+
 def test_digest_is_fold_over_words_from_zero():
     # a block of B=2 tokens is one word: digest = S(0, w); key = S(root, digest)
     w = 7 | (9 << 32)
