@@ -185,6 +185,29 @@ pc_status pc_stack_distance(const uint32_t *prev, const uint32_t *next, uint64_t
                             uint32_t *dist, void *ws, size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
+ * Exact LRU stack distance without allocation, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same dist as pc_stack_distance, with
+ * the workspace taken from a fixed 128 MiB device array inside the library
+ * (one per GPU, held until the process ends) instead of the caller: the
+ * call allocates nothing and synchronises nothing.  The caller passes the
+ * inputs and the output as for pc_stack_distance.
+ *   n above pc_stack_distance_noalloc_max_n() (about 8.0e6 accesses: the n
+ *   whose workspace still fits the array) returns PC_ERR_TOO_LARGE before
+ *   anything is enqueued.
+ * Every call on one GPU shares that GPU's array: calls that overlap on one
+ * device (two streams, two threads) race and must be ordered by the caller.
+ * The array keeps the last call's contents; each call clears what it reads.
+ * The device-side status word lives in that array and is not reported:
+ * prev / next that are not mutual links give unspecified distances (never a
+ * write out of bounds).  Keep pc_prof_enable off for calls that must not
+ * allocate (the timing events are created on demand).
+ * ------------------------------------------------------------------------ */
+uint64_t pc_stack_distance_noalloc_max_n(void);
+pc_status pc_stack_distance_noalloc(const uint32_t *prev, const uint32_t *next, uint64_t n, uint32_t *dist,
+                                    void *stream);
+
+/* ------------------------------------------------------------------------
  * Exact LRU stack distance of every access, from the runs of the prev stream.
  *
  * Same dist as pc_stack_distance (Sec. 5; Appendix B).  When t - 1 and t are

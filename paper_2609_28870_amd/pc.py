@@ -63,6 +63,10 @@ def lib():
     L.pc_stack_distance_runs_ws.argtypes = [_u64]
     L.pc_stack_distance_runs.restype = _st
     L.pc_stack_distance_runs.argtypes = [_vp, _vp, _u64, _vp, _vp, _sz, _vp]
+    L.pc_stack_distance_noalloc_max_n.restype = _u64
+    L.pc_stack_distance_noalloc_max_n.argtypes = []
+    L.pc_stack_distance_noalloc.restype = _st
+    L.pc_stack_distance_noalloc.argtypes = [_vp, _vp, _u64, _vp, _vp]
     L.pc_stack_distance_ws.restype = _sz
     L.pc_stack_distance_ws.argtypes = [_u64]
     L.pc_stack_distance.restype = _st
@@ -256,6 +260,18 @@ def stack_distance(prev: torch.Tensor, nxt: torch.Tensor, dist: Optional[torch.T
         ws = workspace(L.pc_stack_distance_ws(n))
     check(L.pc_stack_distance(_ptr(prev), _ptr(nxt), n, _ptr(dist), _ptr(ws), ws.numel(), _stream()))
     return dist, ws
+
+
+def stack_distance_noalloc(prev: torch.Tensor, nxt: torch.Tensor, dist: torch.Tensor):
+    """pc_stack_distance_noalloc: the same distances as stack_distance into a
+    caller-provided ``dist``, with the library's own fixed device scratch
+    (nothing is allocated; calls on one GPU must not overlap)."""
+    check(lib().pc_stack_distance_noalloc(_ptr(prev), _ptr(nxt), prev.numel(), _ptr(dist), _stream()))
+    return dist
+
+
+def stack_distance_noalloc_max_n() -> int:
+    return int(lib().pc_stack_distance_noalloc_max_n())
 
 
 def stack_distance_runs(prev: torch.Tensor, nxt: torch.Tensor, dist: Optional[torch.Tensor] = None,
