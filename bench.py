@@ -28,7 +28,9 @@ P_LIN = 3_000_000_000          # FLOPs per token, linear part (agent cost model)
 # algorithmic bytes per element for each kernel (inputs it must read and
 # outputs it must write, once each)
 ALGO_BYTES = {
-    "hash_blocks": lambda B: 4 * B + 8 + 4,       # tokens in, key and depth out
+    # tokens in, key out (the per-access hashing bytes of the measurement
+    # plan; the 4-byte depth the kernel also writes is not counted)
+    "hash_blocks": lambda B: 4 * B + 8,
     "sort_onesweep_pass": lambda B: 12 + 12,      # (key, t) in and out
     "link_partition": lambda B: 12 + 12,          # sorted (key, t) in, (t, prev, next) out
     "perm_partition": lambda B: 12 + 12,          # (t, prev, next) in and out
@@ -321,7 +323,7 @@ def main():
                     help="time the workload characterisation instead (hash, prev/next, reuse and session "
                          "profiles)")
     ap.add_argument("--cpu-sample", type=int, default=None,
-                    help="block accesses in the oracle's timed sample (0 = skip; default 1e8, "
+                    help="block accesses in the oracle's timed sample (0 = skip; default 4e8, "
                          "1e6 with --residency request)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 4 GiB device copy (for rocprof counter calibration)")
@@ -464,7 +466,7 @@ def main():
                 "session_distance": "session_distance",
                 "reuse_profile_pack": "reuse_profile", "reuse_profile_walk": "reuse_profile",
                 "session_profile": "session_profile"}
-    stage_bytes = {"hash": 4 * B + 8 + 4, "prev_next": 16, "stack_distance": 8,
+    stage_bytes = {"hash": 4 * B + 8, "prev_next": 16, "stack_distance": 8,
                    "mrc": 8 if request or session_mode else 12, "request_distance": 12,
                    "session_distance": 8, "reuse_profile": 24}
 
@@ -498,7 +500,7 @@ def main():
         oracle_check = check_against_golden(bins, caps_np, n_blocks, GOLDEN_FULL)
         log("bins match the oracle's full-size reference at all %d capacities" % oracle_check["capacities"])
     cb = None
-    sample = args.cpu_sample if args.cpu_sample is not None else (1_000_000 if request else 100_000_000)
+    sample = args.cpu_sample if args.cpu_sample is not None else (1_000_000 if request else 400_000_000)
     if sample > 0:
         log("timing the CPU oracle on a %d-access sample" % sample)
         kind = "profile" if args.profile else "session" if session_mode else request
