@@ -390,6 +390,36 @@ pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uin
                           void *stream);
 
 /* ------------------------------------------------------------------------
+ * Belady's MIN at many capacities at once: the offline ceiling every online
+ * policy is compared with (Sec. 3.2 "Belady's optimum"; Appendix B, the
+ * LRU-Belady gap under concurrency).  Demand paging: every accessed block
+ * is brought in, and when the cache already holds c blocks the resident
+ * block whose next use is farthest away leaves first (a block never used
+ * again is the farthest).  Hit counts are unique (victim ties occur only
+ * among blocks that are never used again).  Capacities are in blocks and
+ * need not be ordered; c = 0 never hits.
+ *
+ *   next      uint32[n] from pc_prev_next_use (PC_NONE: never used again);
+ *             an entry that is not PC_NONE and not in (t, n) sets the
+ *             workspace status to 2 and counts as PC_NONE
+ *   depth     uint32[n] or NULL (depth sums are then 0)
+ *   caps      uint64[n_caps] device memory, 1 <= n_caps <= PC_MAX_CAPS
+ *   hits      uint64[n_caps] out: hits at caps[k]
+ *   depthsum  uint64[n_caps] out: sum of depth over those hits (with the
+ *             linear cost of pc_mrc_weighted: saved = alpha*hits + beta*depthsum)
+ *   hit_flags uint8[n_caps * n] out or NULL: hit_flags[k*n + t] = 1 when
+ *             access t hits at caps[k]
+ * One wave simulates one capacity through the whole trace: the call takes
+ * time linear in n (about 1 s per 2.8e7 accesses), not one memory pass.
+ * Workspace: about n_caps * n / 8 bytes of bitmaps.  Status 5 reports an
+ * internal consistency check (not expected for a valid next[]).
+ * ------------------------------------------------------------------------ */
+size_t pc_belady_ws(uint64_t n, uint32_t n_caps);
+pc_status pc_belady(const uint32_t *next, const uint32_t *depth, uint64_t n, const uint64_t *caps,
+                    uint32_t n_caps, uint64_t *hits, uint64_t *depthsum, uint8_t *hit_flags, void *ws,
+                    size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
  * Device-side status.  Every call clears word 0 of its workspace; kernels
  * record a non-zero code there instead of faulting or hanging:
  *   1  a wait on another workgroup (decoupled look-back) gave up after a
@@ -401,7 +431,8 @@ pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uin
  *      undefined, nothing written out of bounds);
  *   3  pc_mrc_weighted and the profiles: edges not non-decreasing (bins
  *      undefined);
- *   4  pc_prev_next_use: a given key histogram does not sum to n.
+ *   4  pc_prev_next_use: a given key histogram does not sum to n;
+ *   5  pc_belady: an internal consistency check failed (results undefined).
  * This call copies the code of workspace `ws` to *code_out after
  * synchronising `stream` (the only synchronising call in the library).
  * ------------------------------------------------------------------------ */

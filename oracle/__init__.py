@@ -252,21 +252,26 @@ def lru(keys, caps, depth=None, ids=None, flags=False, threads=1, fingerprints=F
     return _per_capacity(one, caps, threads)
 
 
-def belady(keys, caps, ids=None, nxt=None, flags=False):
+def belady(keys, caps, ids=None, nxt=None, flags=False, threads=1):
+    """Hits of demand-paging MIN at each capacity (Sec. 3.2: the offline
+    ceiling): every access brings its block in, and a full cache evicts the
+    resident block whose next use is farthest (never used again counts as
+    farthest).  With ``flags`` also the per-access hit flags."""
     if ids is None:
         ids = key_ids(keys)
     id_, n_ids = ids
     if nxt is None:
         _, nxt = prev_next(keys, ids)
     nxt = _c(nxt, np.uint32)
-    out = []
-    for c in caps:
+
+    def one(c):
         h = ctypes.c_uint64(0)
         fl = np.empty(id_.size, np.uint8) if flags else None
         assert lib().orc_belady_sim(_p(id_, _u32p), _p(nxt, _u32p), id_.size, n_ids, int(c),
                                     ctypes.byref(h), _p(fl, _u8p) if fl is not None else None) == 0
-        out.append((h.value, fl) if flags else h.value)
-    return out
+        return (h.value, fl) if flags else h.value
+
+    return _per_capacity(one, caps, threads)
 
 
 def mrc_bins(keys, caps, depth=None, alpha=1, beta=0, ids=None, threads=1):

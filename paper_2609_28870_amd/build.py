@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRC_DIR = os.path.join(HERE, "csrc")
 SOURCES = ["pc_api.hip", "pc_hash.hip", "pc_sort.hip", "pc_chain.hip", "pc_stackdist.hip", "pc_runs.hip", "pc_session.hip", "pc_profile.hip", "pc_mrc.hip",
-           "pc_noalloc.hip"]
+           "pc_noalloc.hip", "pc_belady.hip"]
 OUT = os.path.join(HERE, "_lib", "libpc.so")
 ARCH = os.environ.get("PC_OFFLOAD_ARCH", "gfx950")
 

@@ -43,6 +43,7 @@ static const char *kernel_name(KernelId k) {
     case K_RUNS_COMPACT: return "runs_compact";
     case K_RUNS_MERGE: return "runs_merge";
     case K_RUNS_FILL: return "runs_fill";
+    case K_BELADY: return "belady";
     case K_COUNT: break;
     }
     return "";

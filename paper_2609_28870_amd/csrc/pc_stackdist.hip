@@ -687,18 +687,6 @@ __global__ __launch_bounds__(LOC_THREADS, 6) void sd_local_kernel(
 }
 
 // ---- request-level residency --------------------------------------------
-// Inclusive prefix max across the 64 lanes of a wave (the DPP pattern of
-// wave_incl_scan; lanes shifted in from outside a row contribute 0).
-__device__ __forceinline__ uint32_t wave_incl_max(uint32_t x) {
-    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false));   // row_shr:1
-    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false));   // row_shr:2
-    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false));   // row_shr:4
-    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false));   // row_shr:8
-    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false));   // row_bcast:15
-    x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false));   // row_bcast:31
-    return x;
-}
-
 // Request-level distance from the per-access distance of the request-ordered
 // stream.  With v = prev + 1 (0 for a cold access) and t in request [s, e):
 //     dist_req(t) = dist(t) - #{ j in [s, t) : v(j) < v(t) }.

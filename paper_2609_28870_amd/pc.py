@@ -98,6 +98,10 @@ def lib():
     L.pc_mrc_weighted.restype = _st
     L.pc_mrc_weighted.argtypes = [_vp, _vp, _vp, _u64, _vp, _u32, _u64, _u64, _vp, _vp, _vp, _vp,
                                   _vp, _vp, _sz, _vp]
+    L.pc_belady_ws.restype = _sz
+    L.pc_belady_ws.argtypes = [_u64, _u32]
+    L.pc_belady.restype = _st
+    L.pc_belady.argtypes = [_vp, _vp, _u64, _vp, _u32, _vp, _vp, _vp, _vp, _sz, _vp]
     L.pc_workspace_status.restype = _st
     L.pc_workspace_status.argtypes = [_vp, _sz, _vp, ctypes.POINTER(ctypes.c_int32)]
     L.pc_prof_enable.restype = None
@@ -423,6 +427,27 @@ def mrc_weighted(dist: torch.Tensor, caps: torch.Tensor, depth: Optional[torch.T
                             _ptr(out["depthsum"]), _ptr(out["cost_lo"]), _ptr(out["cost_hi"]),
                             _ptr(out["nextuse"]), _ptr(ws), ws.numel(),
                             _stream()))
+    return out, ws
+
+
+def belady(nxt: torch.Tensor, caps: torch.Tensor, depth: Optional[torch.Tensor] = None, flags: bool = False,
+           out: Optional[dict] = None, ws: Optional[torch.Tensor] = None):
+    """pc_belady: hits and depth sums of Belady's MIN at every capacity
+    (int64 tensors of uint64); with ``flags`` also the per-access hit flags
+    (uint8 [n_caps, n])."""
+    L = lib()
+    n = nxt.numel()
+    k = caps.numel()
+    dev = _dev()
+    if out is None:
+        out = {"hits": torch.empty(k, dtype=torch.int64, device=dev),
+               "depthsum": torch.empty(k, dtype=torch.int64, device=dev)}
+    if flags and "flags" not in out:
+        out["flags"] = torch.empty((k, n), dtype=torch.uint8, device=dev)
+    if ws is None:
+        ws = workspace(L.pc_belady_ws(n, k))
+    check(L.pc_belady(_ptr(nxt), _ptr(depth), n, _ptr(caps), k, _ptr(out["hits"]), _ptr(out["depthsum"]),
+                      _ptr(out.get("flags")) if flags else None, _ptr(ws), ws.numel(), _stream()))
     return out, ws
 
 

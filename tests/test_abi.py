@@ -202,6 +202,33 @@ def test_mrc_rejects_bad_arguments(L):
     assert call(ok(w=None)) == -3
 
 
+def test_belady_rejects_bad_arguments(L):
+    ws = L.pc_belady_ws(1000, 4)
+    assert ws > L.pc_belady_ws(10, 4) > 0
+    ok = lambda **kw: dict(dict(nxt=FAKE, depth=None, n=1000, caps=FAKE, k=4, hits=FAKE, ds=FAKE, fl=None,
+                                w=FAKE, wsz=ws), **kw)
+    call = lambda d: L.pc_belady(d["nxt"], d["depth"], d["n"], d["caps"], d["k"], d["hits"], d["ds"], d["fl"],
+                                 d["w"], d["wsz"], None)
+    assert call(ok(k=0)) == -1
+    assert call(ok(k=1025)) == -1
+    assert call(ok(caps=None)) == -1
+    assert call(ok(hits=None)) == -1
+    assert call(ok(nxt=None)) == -1
+    assert call(ok(n=0xFFFFFFFF)) == -2
+    assert call(ok(w=None)) == -3
+    assert call(ok(wsz=ws - 1)) == -3
+
+
+def test_stack_distance_noalloc_rejects_bad_arguments(L):
+    m = L.pc_stack_distance_noalloc_max_n()
+    assert 1_000_000 < m < 2 ** 32
+    assert L.pc_stack_distance_ws(m) <= 128 << 20 < L.pc_stack_distance_ws(m + 1)
+    assert L.pc_stack_distance_noalloc(FAKE, FAKE, m + 1, FAKE, None) == -2
+    assert L.pc_stack_distance_noalloc(FAKE, FAKE, 0xFFFFFFFF, FAKE, None) == -2
+    assert L.pc_stack_distance_noalloc(None, FAKE, 10, FAKE, None) == -1
+    assert L.pc_stack_distance_noalloc(FAKE, FAKE, 10, None, None) == -1
+
+
 def test_workspace_status_rejects_null(L):
     code = ctypes.c_int32(0)
     assert L.pc_workspace_status(None, 256, None, ctypes.byref(code)) == -1
@@ -213,5 +240,5 @@ def test_profiling_table(L):
     names = [L.pc_prof_kernel_name(i).decode() for i in range(n)]
     assert "hash_blocks" in names and "sd_dominance_pass" in names and "mrc_hist" in names
     assert all(names) and len(set(names)) == n
-    assert names[-1] == "runs_fill" and "chain_stair" in names and "runs_merge" in names
+    assert names[-1] == "belady" and "chain_stair" in names and "runs_merge" in names and "runs_fill" in names
     assert pc.prof_read() is not None
