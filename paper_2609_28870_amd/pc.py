@@ -510,11 +510,14 @@ class Pipeline:
     ``depth``), runs prev/next and the stack distance on that order, turns
     the result into the request-level distance and bins that, with depth in
     the same order; the next-use histogram is not taken in that mode.  Its
-    bins are valid at capacities of at least the largest request."""
+    bins are valid at capacities of at least the largest request.
+    ``with_belady`` (per-access mode) also runs Belady's MIN at every
+    capacity on the step's next-use index (``belady_out``)."""
 
     def __init__(self, tokens, tok_start, tok_len, blk_off, n_blocks: int, caps,
                  block_size: int = 16, alpha: int = 1, beta: int = 0, with_nextuse: bool = True,
-                 residency: str = "access", session: Optional[torch.Tensor] = None, chained: bool = True):
+                 residency: str = "access", session: Optional[torch.Tensor] = None, chained: bool = True,
+                 with_belady: bool = False):
         if residency not in ("access", "request", "session"):
             raise PcError("residency must be 'access', 'request' or 'session'")
         if residency == "session" and session is None:
@@ -553,6 +556,11 @@ class Pipeline:
             self.dist_req = torch.empty(n, dtype=torch.int32, device=dev)
             self.ws_req = workspace(L.pc_stack_distance_req_ws())
         self.ws_mrc = workspace(L.pc_mrc_weighted_ws(n, k))
+        self.with_belady = with_belady and residency == "access"
+        if self.with_belady:
+            self.belady_out = {"hits": torch.empty(k, dtype=torch.int64, device=dev),
+                               "depthsum": torch.empty(k, dtype=torch.int64, device=dev)}
+            self.ws_bel = workspace(L.pc_belady_ws(n, k))
 
     def run(self):
         hash_blocks(self.tokens, self.tok_start, self.tok_len, self.blk_off, self.n, self.B,
@@ -569,6 +577,8 @@ class Pipeline:
             self._stack_distance()
             mrc_weighted(self.dist, self.caps, self.depth, self.next if self.with_nextuse else None,
                          self.alpha, self.beta, out=self.bins, ws=self.ws_mrc)
+            if self.with_belady:
+                belady(self.next, self.caps, self.depth, out=self.belady_out, ws=self.ws_bel)
             return
         self._prev_next(self.keys_r)
         self._stack_distance()
@@ -603,6 +613,8 @@ class Pipeline:
                   ("mrc", self.ws_mrc)]
         if self.request:
             stages.append(("stack_distance_req", self.ws_req))
+        if self.with_belady:
+            stages.append(("belady", self.ws_bel))
         return {name: workspace_status(ws) for name, ws in stages}
 
 
