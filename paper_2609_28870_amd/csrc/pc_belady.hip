@@ -14,41 +14,39 @@
 // hit count is unique.
 //
 // GPU mapping: one workgroup of one wave per capacity, all capacities at
-// once; each wave runs its capacity's simulation through the trace.
-//
-//   c <= 1024: the resident set lives in registers, ceil(c / 64) slots per
-//   lane.  Per access: one compare per slot and a ballot find the value t;
-//   on a miss a free slot is taken, or the wave's largest value (a DPP
-//   max-reduction) is replaced.
-//
-//   c > 1024: the values below a threshold theta are bits of a bitmap over
-//   positions (with a one-bit-per-word summary); the values at or above it,
-//   the ones evictions take, sit in a sorted buffer in LDS (largest first).
-//   Accesses go 64 at a time, one per lane.  Before a batch the buffer is
-//   kept clear of the batch's 64 positions (its values below t0 + 128 go to
-//   the bitmap), so the batch's hits are the bitmap word of those positions
-//   (read and cleared in one exchange) plus the accesses whose block was
-//   accessed earlier in the same batch (a wave OR of one-hot next-use
-//   offsets).  The misses and the resident count give the batch's number of
-//   evictions.  If there are evictions and fewer than 64 dead blocks and
-//   buffer values, the buffer is refilled with the bitmap's largest values
-//   above the batch (whole words, top down, through the summary); with more
-//   than 1024 blocks resident this always yields enough, so no eviction of
-//   the batch can reach a bitmap value or a position of the batch.  The
-//   evictions then follow the batch's access order: each takes a dead block,
-//   or the larger of the buffer's largest value and the largest value
-//   inserted earlier in the batch (a masked DPP max over the lanes).  Values
-//   inserted by the batch go to the buffer (above theta, merged in sorted
-//   order) or to the bitmap; a buffer above 1024 values spills its lowest
-//   into the bitmap.  Bitmap words are touched only by their capacity's wave,
-//   through relaxed device-scope atomics (they live in L2).
+// once; each wave runs its capacity's simulation through the trace, 64
+// accesses (one per lane) at a time.  The values below a threshold theta
+// are bits of a bitmap over positions (with a one-bit-per-word summary);
+// the values at or above it, the ones evictions take, sit in a sorted
+// buffer in LDS (largest first).  Before a batch the buffer's values that
+// fall inside the batch's 64 positions leave it for a window register, so
+// the values present in the window are that register and one bitmap word,
+// read and cleared in one exchange.  Blocks accessed earlier in the same batch come
+// back inside it: their next uses are one-hot bits of the window.
+//   * When the batch needs no eviction, or only as many as there are dead
+//     blocks, nothing in the window can leave: the hits are the window word
+//     or'ed with those bits (a wave OR), and the batch's inserts go to the
+//     dead count, the bitmap or the buffer in bulk.
+//   * Otherwise the wave walks the batch in access order with the window in
+//     a register: a hit clears its bit, an eviction takes a dead block, else
+//     the larger of the buffer's largest value (the top 64 held one per
+//     lane) and the largest value inserted earlier in the batch above theta
+//     (kept as a running maximum), else -- both exhausted -- the buffer is
+//     refilled with the bitmap's largest values above the window (whole
+//     words, top down, through the summary), else the window's largest
+//     value; each insert sets a window bit, joins the batch's values above
+//     theta, or goes to the bitmap.
+// Values inserted above theta are merged into the buffer in sorted order
+// after the batch; a buffer above 256 values spills its lowest into the
+// bitmap.  Bitmap words are touched only by their capacity's wave, through
+// relaxed device-scope atomics (they live in L2); a workgroup fence orders
+// one batch's updates before the next batch's reads.
 #include "pc_internal.h"
 
 namespace pc {
 
-constexpr uint32_t BEL_SMALL = 1024;          // capacities up to this keep the resident set in registers
-constexpr uint32_t BEL_TARGET = 512;          // buffer size a refill aims for and a spill leaves
-constexpr uint32_t BEL_SPILL_AT = 1024;       // buffer size above which the lowest values are spilled
+constexpr uint32_t BEL_TARGET = 128;          // buffer size a refill aims for and a spill leaves
+constexpr uint32_t BEL_SPILL_AT = 256;        // buffer size above which the lowest values are spilled
 constexpr uint32_t BEL_BUF = BEL_SPILL_AT + 2 * WAVE;   // LDS buffer entries (largest fill: spill size + one batch)
 constexpr uint64_t BEL_INF = 1ull << 40;      // theta before the first refill: everything in the bitmap
 constexpr int32_t DEV_ERR_BELADY = 5;
@@ -103,79 +101,30 @@ __device__ __forceinline__ uint32_t load_next(const uint32_t *__restrict__ next,
     return x;
 }
 
-// ---- c <= 1024: SLOTS register slots per lane (0 = empty; no value is 0)
-template <int SLOTS>
-__device__ void belady_small(const uint32_t *__restrict__ next, const uint32_t *__restrict__ depth, uint64_t n,
-                             uint32_t c, uint8_t *__restrict__ flags, uint64_t *hits_out, uint64_t *dsum_out,
-                             int32_t *err) {
-    const int lane = threadIdx.x;
-    uint32_t R[SLOTS];
+// number of lanes whose value v (0 = none) exceeds x: the 64 values are
+// staged in LDS and every lane reads all of them (same addresses for all
+// lanes: broadcast reads, four values per read)
+__device__ __forceinline__ uint32_t count_above(uint32_t v, uint32_t x, uint32_t *s_tmp) {
+    __syncthreads();
+    s_tmp[threadIdx.x] = v;
+    __syncthreads();
+    const uint4 *q = reinterpret_cast<const uint4 *>(s_tmp);
+    uint32_t r = 0;
 #pragma unroll
-    for (int i = 0; i < SLOTS; ++i) R[i] = 0;
-    uint32_t size = 0;
-    uint64_t hits = 0, dsum = 0;
-    for (uint64_t t0 = 0; t0 < n; t0 += WAVE) {
-        const uint64_t t = t0 + lane;
-        const uint32_t xv = load_next(next, t, n, err);
-        const uint32_t dv = (t < n && depth) ? depth[t] : 0u;
-        const int nb = n - t0 < (uint64_t)WAVE ? (int)(n - t0) : WAVE;
-        uint64_t hm = 0;
-        for (int j = 0; j < nb; ++j) {
-            const uint32_t tj = (uint32_t)(t0 + j);
-            const uint32_t x = (uint32_t)__builtin_amdgcn_readlane((int)xv, j);
-            int hs = -1;
-#pragma unroll
-            for (int i = 0; i < SLOTS; ++i)
-                if (tj != 0 && R[i] == tj) hs = i;
-            if (ballot(hs >= 0)) {
-                hm |= 1ull << j;
-#pragma unroll
-                for (int i = 0; i < SLOTS; ++i)
-                    if (hs == i) R[i] = x;
-            } else if (size < c) {
-                int e = -1;
-#pragma unroll
-                for (int i = SLOTS - 1; i >= 0; --i)
-                    if (R[i] == 0) e = i;
-                const uint64_t em = ballot(e >= 0);   // non-empty: fewer than c <= 64 * SLOTS resident
-                if (lane == __builtin_ctzll(em)) {
-#pragma unroll
-                    for (int i = 0; i < SLOTS; ++i)
-                        if (e == i) R[i] = x;
-                }
-                ++size;
-            } else {
-                uint32_t m = 0;
-#pragma unroll
-                for (int i = 0; i < SLOTS; ++i) m = max(m, R[i]);
-                const uint32_t M = wave_max(m);
-                if (lane == __builtin_ctzll(ballot(m == M))) {
-                    bool done = false;
-#pragma unroll
-                    for (int i = 0; i < SLOTS; ++i)
-                        if (!done && R[i] == M) {
-                            R[i] = x;
-                            done = true;
-                        }
-                }
-            }
-        }
-        const bool h = (hm >> lane) & 1;
-        hits += (uint64_t)__popcll(hm);
-        dsum += wave_sum64(h ? dv : 0u);
-        if (flags && t < n) flags[t] = h ? 1 : 0;
+    for (int i = 0; i < WAVE / 4; ++i) {
+        const uint4 a = q[i];
+        r += (a.x > x) + (a.y > x) + (a.z > x) + (a.w > x);
     }
-    if (lane == 0) {
-        *hits_out = hits;
-        *dsum_out = dsum;
-    }
+    return r;
 }
 
-// ---- c > 1024: bitmap below theta, sorted LDS buffer at and above it
+// ---- the simulation of one capacity
 struct BelState {
     uint32_t *buf, *alt;   // buf[head .. head + bufn) descending; alt is the spare array
     uint32_t head, bufn;
     uint64_t theta;
+    uint64_t bm_hi;        // every bitmap value is below this
+    bool dirty;            // the bitmap changed since the last fence
 };
 
 // buffer back to index 0 (through the spare array)
@@ -194,8 +143,10 @@ __device__ __forceinline__ void compact(BelState &S) {
 // empty words; theta drops to the lowest value taken
 __device__ void refill(BelState &S, uint64_t *l0, uint64_t *l1, uint64_t lo, uint64_t n) {
     const int lane = threadIdx.x;
+    if (S.dirty) wave_fence();   // the bitmap's latest inserts first
     compact(S);
     uint64_t hi = S.theta < n + WAVE ? S.theta : n + WAVE;   // exclusive
+    if (S.bm_hi < hi) hi = S.bm_hi;
     const uint64_t wlo = lo >> 6;
     const uint64_t lo_mask = ~((1ull << (lo & 63)) - 1);
     while (S.bufn < BEL_TARGET && hi > lo) {
@@ -223,7 +174,10 @@ __device__ void refill(BelState &S, uint64_t *l0, uint64_t *l1, uint64_t lo, uin
                     }
                 }
             }
-            if (w2 == ~0ull || w2 < wlo) break;
+            if (w2 == ~0ull || w2 < wlo) {   // nothing left in [lo, hi)
+                hi = lo;
+                break;
+            }
             w = w2;
             bits = bm_load(&l0[w]);
             if (w == wlo) bits &= lo_mask;
@@ -246,102 +200,219 @@ __device__ void refill(BelState &S, uint64_t *l0, uint64_t *l1, uint64_t lo, uin
         }
         hi = w << 6 > lo ? w << 6 : lo;
     }
+    // every bitmap value at or above hi has been taken
+    if (hi < S.bm_hi) S.bm_hi = hi > lo ? hi : lo;
     wave_fence();
+    S.dirty = false;
     __syncthreads();
 }
 
-__device__ void belady_large(const uint32_t *__restrict__ next, const uint32_t *__restrict__ depth, uint64_t n,
-                             uint64_t c, uint64_t *__restrict__ l0, uint64_t *__restrict__ l1,
-                             uint8_t *__restrict__ flags, uint64_t *hits_out, uint64_t *dsum_out, int32_t *err,
-                             uint32_t *s_a, uint32_t *s_b, uint32_t *s_new) {
+// the buffer's top 64 values, one per lane (0 past its end)
+__device__ __forceinline__ uint32_t buffer_top(const BelState &S) {
+    return (uint32_t)threadIdx.x < S.bufn ? S.buf[S.head + threadIdx.x] : 0u;
+}
+
+__device__ __forceinline__ uint32_t clamp32(uint64_t v) { return v > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)v; }
+
+__device__ void belady_one(const uint32_t *__restrict__ next, const uint32_t *__restrict__ depth, uint64_t n,
+                           uint64_t c64, uint64_t *__restrict__ l0, uint64_t *__restrict__ l1,
+                           uint8_t *__restrict__ flags, uint64_t *hits_out, uint64_t *dsum_out, int32_t *err,
+                           uint32_t *s_a, uint32_t *s_b, uint32_t *s_new, uint32_t *s_tmp) {
     const int lane = threadIdx.x;
-    BelState S{s_a, s_b, 0, 0, BEL_INF};
-    uint64_t dead = 0, size = 0, hits = 0, dsum = 0;
+    BelState S{s_a, s_b, 0, 0, BEL_INF, 0, false};
+    // resident blocks never exceed n, so the capacity is clamped to 32 bits
+    const uint32_t c = clamp32(c64 < n ? c64 : n);
+    uint32_t dead = 0, size = 0;
+    uint64_t hits = 0, dsum = 0;
+    // this batch's next uses and depths, loaded one batch ahead
+    uint32_t xq = load_next(next, (uint64_t)lane, n, err);
+    uint32_t dq = ((uint64_t)lane < n && depth) ? depth[lane] : 0u;
     for (uint64_t t0 = 0; t0 < n; t0 += WAVE) {
         const uint64_t t = t0 + lane;
         const bool valid = t < n;
-        const uint32_t xv = load_next(next, t, n, err);
-        const uint32_t dv = (valid && depth) ? depth[t] : 0u;
+        const uint32_t xv = xq, dv = dq;
         const int nb = n - t0 < (uint64_t)WAVE ? (int)(n - t0) : WAVE;
         const uint64_t vmask = nb == WAVE ? ~0ull : (1ull << nb) - 1;
-        const uint64_t win_end = t0 + WAVE;
+        const uint64_t we = t0 + WAVE;
+        const uint32_t we32 = clamp32(we), t32 = (uint32_t)t0;
 
-        // keep the buffer out of this batch's positions
-        if (S.theta < t0 + 2 * WAVE) {
-            // values below t0 + 128 are the buffer's tail (descending)
+        // keep the buffer out of this batch's positions: its values inside the
+        // window (its tail, the buffer being descending) join the window word
+        uint64_t wlow = 0;
+        if (S.theta < we) {
             uint32_t lo = 0, hi = S.bufn;
             while (lo < hi) {
                 const uint32_t mid = (lo + hi) >> 1;
-                if ((uint64_t)S.buf[S.head + mid] >= t0 + 2 * WAVE) lo = mid + 1; else hi = mid;
+                if ((uint64_t)S.buf[S.head + mid] >= we) lo = mid + 1; else hi = mid;
             }
-            for (uint32_t i = lo + lane; i < S.bufn; i += WAVE) bm_insert(l0, l1, S.buf[S.head + i]);
+            uint64_t bw = 0;
+            for (uint32_t i = lo + lane; i < S.bufn; i += WAVE) bw |= 1ull << (S.buf[S.head + i] - t32);
+            wlow = wave_or64(bw);
             S.bufn = lo;
-            S.theta = t0 + 2 * WAVE;
-            wave_fence();
+            S.theta = we;
         }
 
-        // hits: the batch's bitmap word (taken and cleared), and blocks accessed
-        // earlier in the batch (their next use falls inside it)
+        // values present in the window: that register and the window's bitmap
+        // word, taken and cleared
         const uint64_t w = t0 >> 6;
-        uint64_t wbits = 0;
-        if (lane == 0) {
-            wbits = bm_xchg(&l0[w], 0ull);
-            if (wbits) bm_and(&l1[w >> 6], ~(1ull << (w & 63)));
-        }
-        wbits = readlane64(wbits, 0);
-        const bool inwin = xv != NONE && (uint64_t)xv < win_end;
-        const uint64_t link = wave_or64(inwin ? 1ull << ((uint64_t)xv - t0) : 0ull);
-        const uint64_t hm = (wbits | link) & vmask;
-        const uint64_t misses = (uint64_t)__popcll(vmask & ~hm);
-        const uint64_t E = size + misses > c ? size + misses - c : 0;
-        if (E > 0 && dead + S.bufn < (uint64_t)WAVE) {
-            refill(S, l0, l1, win_end, n);
-            if (dead + S.bufn < (uint64_t)WAVE) {   // cannot happen with more than 1024 blocks resident
-                if (lane == 0) atomicOr(err, DEV_ERR_BELADY);
-                return;
+        uint64_t wbits = wlow;
+        if (S.bm_hi > t0) {   // else the bitmap holds nothing at or above the window
+            uint64_t wb = 0;
+            if (lane == 0) {
+                wb = bm_xchg(&l0[w], 0ull);
+                if (wb) bm_and(&l1[w >> 6], ~(1ull << (w & 63)));
             }
+            wbits |= readlane64(wb, 0);
         }
-        const uint64_t deadm = ballot(valid && xv == NONE);
-        const uint64_t pend = ballot(valid && xv != NONE && (uint64_t)xv >= win_end && (uint64_t)xv >= S.theta);
-        const bool to_bitmap = valid && xv != NONE && (uint64_t)xv >= win_end && (uint64_t)xv < S.theta;
+        const bool inwin = xv != NONE && xv < we32;
+        const uint64_t link = wave_or64(inwin ? 1ull << (xv - t32) : 0ull);
+        uint64_t hm = (wbits | link) & vmask;
+        const uint32_t misses = (uint32_t)__popcll(vmask & ~hm);
+        const uint32_t E = size + misses > c ? size + misses - c : 0u;
+        if (E > dead && dead + S.bufn < (uint32_t)WAVE) refill(S, l0, l1, we, n);
 
-        // evictions in access order
-        uint64_t alive = pend;
+        bool to_buffer, to_bitmap;
         uint32_t popped = 0;
-        if (E == 0) {
-            dead += (uint64_t)__popcll(deadm);
-            size += misses;
-        } else if (dead >= E) {   // every eviction takes a dead block
-            dead += (uint64_t)__popcll(deadm) - E;
-            size = c;
+        if (E <= dead) {
+            // nothing in the window can leave: bulk
+            dead += (uint32_t)__popcll(ballot(valid && xv == NONE)) - E;
+            size = size + misses - E;
+            to_buffer = valid && xv != NONE && xv >= we32 && (uint64_t)xv >= S.theta;
+            to_bitmap = valid && xv != NONE && xv >= we32 && (uint64_t)xv < S.theta;
         } else {
-            alive = 0;
-            for (int j = 0; j < nb; ++j) {
+            // access by access.  The batch's inserts above the window are ranked
+            // by value; so are they jointly with the buffer's top 64 values
+            const bool pend = valid && xv != NONE && xv >= we32;
+            const uint64_t pmask = ballot(pend);
+            // pending values above this one (values are distinct)
+            const uint32_t rank = count_above(pend ? xv : 0u, xv, s_tmp);
+            __syncthreads();
+            if (pend) s_new[rank] = xv;
+            __syncthreads();
+            const uint32_t np = (uint32_t)__popcll(pmask);
+            const uint32_t sorted = (uint32_t)lane < np ? s_new[lane] : 0u;
+            uint32_t top = buffer_top(S);
+            const uint32_t nbt = S.bufn < (uint32_t)WAVE ? S.bufn : (uint32_t)WAVE;
+            const uint32_t th32 = clamp32(S.theta);
+            // joint rank: a pending value's rank plus the top buffer values above
+            // it; a top buffer value's index plus the pending values above it
+            uint32_t jr = 0, jb = 0;
+            if (pend) {
+                uint32_t lo = 0, hi = nbt;
+                while (lo < hi) {
+                    const uint32_t mid = (lo + hi) >> 1;
+                    if (S.buf[S.head + mid] > xv) lo = mid + 1; else hi = mid;
+                }
+                jr = rank + lo;
+            }
+            const bool isb = (uint32_t)lane < nbt;
+            if (isb) {
+                uint32_t lo = 0, hi = np;
+                while (lo < hi) {
+                    const uint32_t mid = (lo + hi) >> 1;
+                    if (s_new[mid] > top) lo = mid + 1; else hi = mid;
+                }
+                jb = (uint32_t)lane + lo;
+            }
+            const uint64_t b_lo = wave_or64(isb && jb < 64 ? 1ull << jb : 0ull);
+            const uint64_t b_hi = wave_or64(isb && jb >= 64 ? 1ull << (jb - 64) : 0ull);
+            // candidates at or above theta rank first; below them the bitmap
+            // may hold larger values, which only the general walk below handles
+            const uint32_t nhigh = nbt + (uint32_t)__popcll(ballot(pend && (uint64_t)xv >= S.theta));
+            (void)th32;
+            // evictions: the misses after the cache has filled up
+            uint64_t ev = vmask & ~hm;
+            for (uint32_t k = size; k < c && ev; ++k) ev &= ev - 1;
+            const uint64_t dm = ballot(valid && xv == NONE);
+            uint64_t al = b_lo, ah = b_hi, gl = 0, gh = 0;
+            uint32_t d = dead;
+            bool ok = true;
+            for (int j = 0; j < nb && ok; ++j) {
                 const uint64_t bit = 1ull << j;
-                if (!(hm & bit)) {
-                    if (size == c) {
-                        if (dead) {
-                            --dead;
-                        } else {
-                            const uint32_t pb = popped < S.bufn ? S.buf[S.head + popped] : 0u;
-                            const bool cand = (alive >> lane) & 1 & ((bit - 1) >> lane);
-                            const uint32_t pm = wave_max(cand ? xv : 0u);
-                            if (pm > pb) {
-                                alive &= ~ballot(cand && xv == pm);
-                            } else if (popped < S.bufn) {
-                                ++popped;
-                            } else {   // no candidate left: cannot happen (see refill)
-                                if (lane == 0) atomicOr(err, DEV_ERR_BELADY);
-                                return;
-                            }
-                        }
+                if (ev & bit) {
+                    if (d) {
+                        --d;
                     } else {
-                        ++size;
+                        const uint64_t cl = al & ~gl, ch = ah & ~gh;
+                        if (cl && (uint32_t)__builtin_ctzll(cl) < nhigh) {
+                            gl |= cl & (~cl + 1);
+                        } else if (!cl && ch && 64u + (uint32_t)__builtin_ctzll(ch) < nhigh) {
+                            gh |= ch & (~ch + 1);
+                        } else {
+                            ok = false;
+                        }
                     }
                 }
-                if (deadm & bit) ++dead;
-                if (pend & bit) alive |= bit;
+                if (dm & bit) {
+                    ++d;
+                } else if (pmask & bit) {
+                    const uint32_t r = (uint32_t)__builtin_amdgcn_readlane((int)jr, j);
+                    if (r < 64) al |= 1ull << r; else ah |= 1ull << (r - 64);
+                }
             }
+            uint64_t gone = 0;   // by pending rank
+            if (ok) {
+                dead = d;
+                size = c;   // evictions happened, so the cache is full
+                popped = (uint32_t)__popcll(gl & b_lo) + (uint32_t)__popcll(gh & b_hi);
+                const bool g = jr < 64 ? (gl >> jr) & 1 : (gh >> (jr - 64)) & 1;
+                gone = ballot(pend && g);   // lane mask
+            } else {
+            // the general walk: the window in a register, a refill when the
+            // buffer and the batch's inserts above theta run out, the window's
+            // largest value when nothing above the window is left
+            uint64_t avail = 0, rgone = 0;   // by pending rank: inserted so far / evicted again
+            uint64_t wreg = wbits;
+            hm = 0;
+            for (int j = 0; j < nb; ++j) {
+                const uint64_t bit = 1ull << j;
+                const uint32_t x = (uint32_t)__builtin_amdgcn_readlane((int)xv, j);
+                if (wreg & bit) {
+                    wreg &= ~bit;
+                    hm |= bit;
+                } else if (size < c) {
+                    ++size;
+                } else if (dead) {
+                    --dead;
+                } else {
+                    const uint64_t cand = avail & ~rgone;   // lowest rank = largest value
+                    const uint32_t pm = cand ? (uint32_t)__builtin_amdgcn_readlane((int)sorted, __builtin_ctzll(cand)) : 0u;
+                    uint32_t pb = popped < S.bufn ? (uint32_t)__builtin_amdgcn_readlane((int)top, popped) : 0u;
+                    if (pb == 0 && pm < clamp32(S.theta)) {
+                        // buffer exhausted and the bitmap may hold larger values
+                        S.head += popped;
+                        S.bufn -= popped;
+                        popped = 0;
+                        refill(S, l0, l1, we, n);
+                        top = buffer_top(S);
+                        pb = S.bufn ? (uint32_t)__builtin_amdgcn_readlane((int)top, 0) : 0u;
+                    }
+                    if (pm > pb) {
+                        rgone |= cand & (~cand + 1);
+                    } else if (pb) {
+                        ++popped;
+                    } else if (wreg & ~((bit << 1) - 1)) {
+                        // nothing resident above the window: its largest value
+                        wreg &= ~(1ull << (63 - __builtin_clzll(wreg)));
+                    } else {   // nothing to evict: cannot happen with c resident blocks
+                        if (lane == 0) atomicOr(err, DEV_ERR_BELADY);
+                        return;
+                    }
+                }
+                // lane j's block stays resident with its next use
+                if (x == NONE) {
+                    ++dead;
+                } else if (x < we32) {
+                    wreg |= 1ull << (x - t32);
+                } else {
+                    avail |= 1ull << (uint32_t)__builtin_amdgcn_readlane((int)rank, j);
+                }
+            }
+            gone = ballot(pend && ((rgone >> rank) & 1));
+            }
+            const bool alive = pend && !((gone >> lane) & 1);
+            to_buffer = alive && (uint64_t)xv >= S.theta;
+            to_bitmap = alive && (uint64_t)xv < S.theta;
         }
 
         // the batch's results
@@ -349,27 +420,29 @@ __device__ void belady_large(const uint32_t *__restrict__ next, const uint32_t *
         hits += (uint64_t)__popcll(hm);
         dsum += wave_sum64(h ? dv : 0u);
         if (flags && valid) flags[t] = h ? 1 : 0;
-        if (to_bitmap) bm_insert(l0, l1, xv);
+        if (ballot(to_bitmap)) {
+            if (to_bitmap) bm_insert(l0, l1, xv);
+            const uint64_t m = (uint64_t)wave_max(to_bitmap ? xv : 0u) + 1;
+            if (m > S.bm_hi) S.bm_hi = m;
+            S.dirty = true;
+        }
 
-        // buffer: drop the popped values, merge the surviving inserts
+        // buffer: drop the popped values, merge the batch's values above theta
         S.head += popped;
         S.bufn -= popped;
+        const uint64_t alive = ballot(to_buffer);
         const uint32_t nn = (uint32_t)__popcll(alive);
         if (nn) {
-            const bool mine = (alive >> lane) & 1;
             // rank among the new values (all distinct), largest first
-            uint32_t r = 0;
-            for (uint64_t m = alive; m; m &= m - 1) {
-                const uint32_t v = (uint32_t)__builtin_amdgcn_readlane((int)xv, __builtin_ctzll(m));
-                r += v > xv ? 1u : 0u;
-            }
+            const uint32_t r = count_above(to_buffer ? xv : 0u, xv, s_tmp);
             // buffer values above it (descending array: a lower bound)
             uint32_t lo = 0, hi = S.bufn;
             while (lo < hi) {
                 const uint32_t mid = (lo + hi) >> 1;
                 if (S.buf[S.head + mid] > xv) lo = mid + 1; else hi = mid;
             }
-            if (mine) {
+            __syncthreads();   // s_new may still be read above
+            if (to_buffer) {
                 s_new[r] = xv;
                 S.alt[r + lo] = xv;
             }
@@ -392,12 +465,22 @@ __device__ void belady_large(const uint32_t *__restrict__ next, const uint32_t *
         }
         // spill the lowest values when the buffer grows large
         if (S.bufn > BEL_SPILL_AT) {
+            const uint64_t top_spilled = (uint64_t)S.buf[S.head + BEL_TARGET] + 1;
             for (uint32_t i = BEL_TARGET + lane; i < S.bufn; i += WAVE) bm_insert(l0, l1, S.buf[S.head + i]);
+            if (top_spilled > S.bm_hi) S.bm_hi = top_spilled;
             S.bufn = BEL_TARGET;
             S.theta = S.buf[S.head + BEL_TARGET - 1];
+            S.dirty = true;
         }
-        wave_fence();
+        if (S.dirty) {   // this batch's bitmap updates before the next batch's reads
+            wave_fence();
+            S.dirty = false;
+        }
         __syncthreads();
+        // the next batch's loads, in flight during its window exchange
+        const uint64_t tn = t + WAVE;
+        xq = load_next(next, tn, n, err);
+        dq = (tn < n && depth) ? depth[tn] : 0u;
     }
     if (lane == 0) {
         *hits_out = hits;
@@ -412,6 +495,7 @@ __global__ __launch_bounds__(WAVE) void belady_kernel(const uint32_t *__restrict
                                                       uint64_t *__restrict__ hits, uint64_t *__restrict__ dsum,
                                                       uint8_t *__restrict__ flags, int32_t *__restrict__ err) {
     __shared__ uint32_t s_a[BEL_BUF], s_b[BEL_BUF], s_new[WAVE];
+    __shared__ __align__(16) uint32_t s_tmp[WAVE];
     const uint32_t k = blockIdx.x;
     const uint64_t c = caps[k];
     uint8_t *fl = flags ? flags + (uint64_t)k * n : nullptr;
@@ -424,17 +508,8 @@ __global__ __launch_bounds__(WAVE) void belady_kernel(const uint32_t *__restrict
         }
         return;
     }
-    if (c <= BEL_SMALL) {
-        const uint32_t c32 = (uint32_t)c;
-        if (c32 <= 64) belady_small<1>(next, depth, n, c32, fl, hits + k, dsum + k, err);
-        else if (c32 <= 128) belady_small<2>(next, depth, n, c32, fl, hits + k, dsum + k, err);
-        else if (c32 <= 256) belady_small<4>(next, depth, n, c32, fl, hits + k, dsum + k, err);
-        else if (c32 <= 512) belady_small<8>(next, depth, n, c32, fl, hits + k, dsum + k, err);
-        else belady_small<16>(next, depth, n, c32, fl, hits + k, dsum + k, err);
-        return;
-    }
-    belady_large(next, depth, n, c, l0s + (uint64_t)k * w0, l1s + (uint64_t)k * w1, fl, hits + k, dsum + k, err,
-                 s_a, s_b, s_new);
+    belady_one(next, depth, n, c, l0s + (uint64_t)k * w0, l1s + (uint64_t)k * w1, fl, hits + k, dsum + k, err, s_a,
+               s_b, s_new, s_tmp);
 }
 
 // bitmap words per capacity: one bit per position plus a word of slack, and

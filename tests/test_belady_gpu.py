@@ -1,11 +1,12 @@
 """Belady's MIN on the GPU (pc_belady) against the oracle's demand-paging
 MIN simulation (a max-heap on next use, pinned by exhaustive search and the
 textbook example): hit counts, depth sums and per-access hit flags at every
-capacity, in both of the kernel's regimes (resident set in registers up to
-1024 blocks, bitmap and sorted buffer above), on random streams, chained
-traces, the full agent-shaped trace and the edge cases; and the relations
-the paper relies on (LRU never beats MIN; both hit every reuse once the
-cache holds every block)."""
+capacity, from one block (every batch walked access by access, evictions
+reaching into the batch's own window) to capacities that hold everything
+(bulk batches only), on random streams, looping scans, chained traces, the
+full agent-shaped trace and the edge cases; and the relations the paper
+relies on (LRU never beats MIN; both hit every reuse once the cache holds
+every block)."""
 import numpy as np
 import pytest
 import torch
@@ -17,8 +18,8 @@ from paper_2609_28870_amd import pc
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
 NONE = pc.NONE
-# both regimes and their edges: register slots 1/2/4/8/16 per lane, bitmap above 1024
-CAPS = [0, 1, 2, 3, 7, 63, 64, 65, 100, 128, 129, 200, 256, 257, 500, 512, 513, 1000, 1024, 1025, 1100, 1500,
+# tiny to huge: window evictions, buffer refills and spills, bulk-only batches
+CAPS = [0, 1, 2, 3, 7, 63, 64, 65, 100, 128, 129, 191, 200, 256, 257, 500, 512, 513, 1000, 1024, 1025, 1100, 1500,
         2048, 3000, 5000, 10000, 40000, 10 ** 7]
 
 
