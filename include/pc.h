@@ -11,9 +11,11 @@
  * Common rules
  *   - Every array argument is DEVICE memory (hipMalloc / a torch tensor on the
  *     GPU) unless stated otherwise.  The caller owns all memory; the library
- *     never allocates or frees, and only pc_prev_next_chained,
- *     pc_stack_distance_runs and the read-back calls (pc_workspace_status,
- *     pc_prof_read) synchronise.
+ *     never allocates or frees, and only the read-back calls
+ *     (pc_workspace_status, pc_prof_read) synchronise: where a call picks
+ *     between two paths from its data, it does so on the device and gates
+ *     the launches of both, so any sequence of calls can be captured into a
+ *     graph.
  *     Scratch space comes only from
  *     the caller's workspace `ws` of at least the size the matching `*_ws`
  *     query returns (256-byte aligned).
@@ -153,9 +155,11 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
  *   flags     0 or PC_HASH_DEEPEST_FIRST.
  *   key_hist  as for pc_prev_next_use; used only by the generic path over all
  *             keys.
- * Unlike the other entry points this call synchronises `stream` twice (it
- * reads back the number of unresolved accesses and the check's verdict), so
- * it cannot be captured into a graph.  Workspace words after the call:
+ * Every choice between the two paths is made on the device: the unresolved
+ * stage is sized for the most unresolved accesses the workspace holds and
+ * works on the count the GPU wrote, and the generic path's launches are
+ * gated on the verdict, so the call does not synchronise.  Workspace words
+ * after the call:
  * word 1 = 1 if the generic path ran over all keys, word 2 = the number of
  * accesses that went through the generic prev/next of the unresolved ones,
  * word 3 = why the generic path ran (1 layout, 2 too many unresolved,
@@ -220,11 +224,13 @@ pc_status pc_stack_distance_noalloc(const uint32_t *prev, const uint32_t *next, 
  * every other run's), then the run's distance along all its accesses.
  *
  *   prev, next uint32[n] as produced by pc_prev_next_use; dist uint32[n] out.
- * With more than n/16 + 1024 runs (streams without that structure) the call
- * runs pc_stack_distance instead (same result).  It synchronises `stream`
- * once (it reads the number of runs back).  Workspace words after the call:
- * word 1 = 1 if pc_stack_distance ran, word 2 = the number of runs, word 3 =
- * the number of cold accesses.
+ * With more than n/16 + 1024 runs (streams without that structure) the
+ * dominance count of pc_stack_distance runs instead (same result).  The
+ * choice is made on the device: the call does not synchronise, and every
+ * launch of the path not taken returns at once, so a graph capture of the
+ * call replays correctly for any input.  Workspace words after the call:
+ * word 1 = 1 if pc_stack_distance's count ran, word 2 = the number of runs,
+ * word 3 = the number of cold accesses.
  * ------------------------------------------------------------------------ */
 size_t pc_stack_distance_runs_ws(uint64_t n);
 pc_status pc_stack_distance_runs(const uint32_t *prev, const uint32_t *next, uint64_t n,
@@ -434,7 +440,8 @@ pc_status pc_belady(const uint32_t *next, const uint32_t *depth, uint64_t n, con
  *   4  pc_prev_next_use: a given key histogram does not sum to n;
  *   5  pc_belady: an internal consistency check failed (results undefined).
  * This call copies the code of workspace `ws` to *code_out after
- * synchronising `stream` (the only synchronising call in the library).
+ * synchronising `stream` (with pc_prof_read, the only synchronising calls
+ * in the library).
  * ------------------------------------------------------------------------ */
 pc_status pc_workspace_status(const void *ws, size_t ws_bytes, void *stream, int32_t *code_out);
 

@@ -96,17 +96,42 @@ int device_cus() {
     return cus;
 }
 
+unsigned capped(uint64_t items, int per_cu) {
+    const uint64_t cap = (uint64_t)device_cus() * per_cu;
+    const uint64_t g = items < cap ? items : cap;
+    return (unsigned)(g ? g : 1);
+}
+
 __global__ void fill_u32_kernel(uint32_t *__restrict__ p, uint32_t value, size_t count) {
     size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     size_t stride = (size_t)gridDim.x * blockDim.x;
     for (; i < count; i += stride) p[i] = value;
 }
 
-pc_status fill_u32(uint32_t *p, uint32_t value, size_t count, hipStream_t s) {
-    if (count == 0) return PC_OK;
+__global__ void fill_u32_gated_kernel(uint32_t *__restrict__ p, uint32_t value, size_t count,
+                                      const int32_t *__restrict__ gate) {
+    if (*gate == 0) return;
+    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (; i < count; i += stride) p[i] = value;
+}
+
+static unsigned fill_blocks(size_t count) {
     size_t blocks = (count + 255) / 256;
     if (blocks > 65536) blocks = 65536;
-    PC_LAUNCH(K_FILL32, fill_u32_kernel, dim3((unsigned)blocks), dim3(256), 0, s, p, value, count);
+    return (unsigned)blocks;
+}
+
+pc_status fill_u32(uint32_t *p, uint32_t value, size_t count, hipStream_t s) {
+    if (count == 0) return PC_OK;
+    PC_LAUNCH(K_FILL32, fill_u32_kernel, dim3(fill_blocks(count)), dim3(256), 0, s, p, value, count);
+    return PC_OK;
+}
+
+pc_status fill_u32_gated(uint32_t *p, uint32_t value, size_t count, hipStream_t s, const int32_t *gate) {
+    if (!gate) return fill_u32(p, value, count, s);
+    if (count == 0) return PC_OK;
+    PC_LAUNCH(K_FILL32, fill_u32_gated_kernel, dim3(fill_blocks(count)), dim3(256), 0, s, p, value, count, gate);
     return PC_OK;
 }
 

@@ -57,6 +57,8 @@ constexpr int HW_BAD = 4;        // device flag: invalid block layout
 constexpr int HW_FAIL = 5;       // device flag: a merge check failed
 constexpr int HW_HIGH_ANCHOR = 6;     // the prev/next over the anchors also sorted by the high key bits
 constexpr int HW_HIGH_UNRESOLVED = 7; // the prev/next over the unresolved accesses did
+constexpr int HW_CHAIN = 8;      // gate: 1 while the chain path goes on
+constexpr int HW_WORDS = 16;     // header words cleared by each call
 
 __device__ __forceinline__ int wave_id_uniform() {
     return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / WAVE));
@@ -271,7 +273,9 @@ __global__ __launch_bounds__(SCAN_THREADS) void chain_scan_apply_kernel(const ui
 __global__ __launch_bounds__(CH_THREADS) void chain_compact_kernel(
     const uint64_t *__restrict__ keys, uint64_t n_slots, const uint4 *__restrict__ rec,
     const uint4 *__restrict__ open, const uint32_t *__restrict__ coff, int deepest,
-    uint64_t *__restrict__ ckeys, uint32_t *__restrict__ cpos, uint8_t *__restrict__ cflag) {
+    uint64_t *__restrict__ ckeys, uint32_t *__restrict__ cpos, uint8_t *__restrict__ cflag,
+    const int32_t *__restrict__ hdr) {
+    if (!hdr[HW_CHAIN]) return;   // (so the offsets stay below the unresolved capacity)
     const int lane = threadIdx.x & (WAVE - 1);
     const uint64_t waves = (uint64_t)gridDim.x * (CH_THREADS / WAVE);
     const uint64_t bit = 1ull << lane;
@@ -307,14 +311,17 @@ __global__ __launch_bounds__(CH_THREADS) void chain_compact_kernel(
 }
 
 // Links of the compacted accesses back into prev / next; flags an added link
-// that would end at an access whose own side is already linked.
+// that would end at an access whose own side is already linked.  The number
+// of compacted accesses is the one the scan wrote.
 __global__ __launch_bounds__(CH_THREADS) void chain_merge_kernel(const uint32_t *__restrict__ cpos,
                                                                  const uint8_t *__restrict__ cflag,
                                                                  const uint32_t *__restrict__ cprev,
-                                                                 const uint32_t *__restrict__ cnext, uint64_t m,
+                                                                 const uint32_t *__restrict__ cnext,
                                                                  uint32_t *__restrict__ prev,
                                                                  uint32_t *__restrict__ next,
                                                                  int32_t *__restrict__ hdr) {
+    if (!hdr[HW_CHAIN]) return;
+    const uint64_t m = (uint32_t)hdr[HW_UNRESOLVED];
     const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
     bool bad = false;
     for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m; i += stride) {
@@ -343,11 +350,44 @@ __global__ __launch_bounds__(CH_THREADS) void chain_merge_kernel(const uint32_t 
 }
 
 // an inner prev/next call's header: its status into ours (word 0), its
-// high-bit flag (word 1) into word `high_word` of ours
-__global__ void chain_status_kernel(const int32_t *__restrict__ nested, int32_t *__restrict__ hdr, int high_word) {
-    if (threadIdx.x != 0) return;
+// high-bit flag (word 1) into word `high_word` of ours; only when the inner
+// call ran (gate word of ours non-zero)
+__global__ void chain_status_kernel(const int32_t *__restrict__ nested, int32_t *__restrict__ hdr, int high_word,
+                                    int gate_word) {
+    if (threadIdx.x != 0 || !hdr[gate_word]) return;
     if (nested[0]) atomicOr(hdr + HW_STATUS, nested[0]);
     hdr[high_word] = nested[1];
+}
+
+// After the layout check: the chain path starts if the layout is valid.
+__global__ void chain_open_kernel(int32_t *__restrict__ hdr) {
+    if (threadIdx.x == 0) hdr[HW_CHAIN] = hdr[HW_BAD] ? 0 : 1;
+}
+
+// After the unresolved count: the chain path goes on if the layout is valid,
+// the anchors' prev/next reported no error and the unresolved accesses fit
+// the workspace; otherwise the reason is recorded.
+__global__ void chain_decide_kernel(int32_t *__restrict__ hdr, const int32_t *__restrict__ anchor_hdr,
+                                    uint32_t m_cap) {
+    if (threadIdx.x != 0) return;
+    int32_t reason = 0;
+    if (hdr[HW_BAD]) reason = 1;
+    else if (anchor_hdr[0]) reason = 4;
+    else if ((uint32_t)hdr[HW_UNRESOLVED] > m_cap) reason = 2;
+    hdr[HW_REASON] = reason;
+    hdr[HW_CHAIN] = reason == 0 ? 1 : 0;
+}
+
+// After the merge: the generic prev/next over all keys runs (HW_PATH = 1)
+// if the chain path stopped, the inner prev/next reported an error or the
+// merge check failed.
+__global__ void chain_verdict_kernel(int32_t *__restrict__ hdr, const int32_t *__restrict__ inner_hdr) {
+    if (threadIdx.x != 0) return;
+    int32_t reason = hdr[HW_REASON];
+    if (reason == 0 && inner_hdr[0]) reason = 4;
+    if (reason == 0 && hdr[HW_FAIL]) reason = 3;
+    hdr[HW_REASON] = reason;
+    hdr[HW_PATH] = reason != 0 ? 1 : 0;
 }
 
 struct ChainWs {
@@ -397,8 +437,8 @@ struct OpenWs {
     void *ws;
     size_t ws_bytes;
 };
-static bool carve_open(const ChainWs &w, uint64_t m, OpenWs *o) {
-    Carver c{(char *)w.generic, 0};
+static size_t carve_open(void *base, uint64_t m, OpenWs *o) {
+    Carver c{(char *)base, 0};
     o->ckeys = c.take<uint64_t>(m);
     o->cpos = c.take<uint32_t>(m);
     o->cprev = c.take<uint32_t>(m);
@@ -406,14 +446,19 @@ static bool carve_open(const ChainWs &w, uint64_t m, OpenWs *o) {
     o->cflag = c.take<uint8_t>(m);
     o->ws_bytes = pc_prev_next_use_ws(m);
     o->ws = c.take<char>(o->ws_bytes);
-    return c.off <= w.generic_bytes;
+    return c.off;
 }
 
-static pc_status read_words(const int32_t *src, int32_t *dst, int count, hipStream_t s) {
-    if (hipMemcpyAsync(dst, src, sizeof(int32_t) * count, hipMemcpyDeviceToHost, s) != hipSuccess)
-        return PC_ERR_DEVICE;
-    if (hipStreamSynchronize(s) != hipSuccess) return PC_ERR_DEVICE;
-    return PC_OK;
+// the most unresolved accesses the generic workspace holds (at most n)
+static uint64_t open_capacity(const ChainWs &w, uint64_t n) {
+    OpenWs o;
+    uint64_t lo = 0, hi = n;
+    while (lo < hi) {
+        const uint64_t mid = lo + (hi - lo + 1) / 2;
+        if (carve_open(nullptr, mid, &o) <= w.generic_bytes) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
 }
 
 static unsigned wave_grid(uint64_t items, int cus) {
@@ -440,36 +485,41 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
     if (ws_bytes < pc_prev_next_chained_ws(n, n_seqs)) return PC_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
     const ChainWs w = carve_chain(ws, n, n_seqs);
-    pc_status st = fill_u32(reinterpret_cast<uint32_t *>(w.hdr), 0u, 8, s);
+    pc_status st = fill_u32(reinterpret_cast<uint32_t *>(w.hdr), 0u, HW_WORDS, s);
     if (st != PC_OK || n == 0) return st;
     const int deepest = (flags & PC_HASH_DEEPEST_FIRST) ? 1 : 0;
     const int cus = device_cus();
 
-    auto generic = [&](int reason) -> pc_status {
-        pc_status g = pc_prev_next_use(keys, n, prev, next, key_hist, w.generic, w.generic_bytes, stream);
+    // the generic prev/next over all keys, gated on `gate` (nullptr: always)
+    auto generic = [&](const int32_t *gate) -> pc_status {
+        pc_status g = prev_next_core(keys, n, nullptr, prev, next, key_hist, w.generic, s, gate);
         if (g != PC_OK) return g;
         PC_LAUNCH(K_FILL32, chain_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)w.generic, w.hdr,
-                  HW_HIGH_ANCHOR);
-        if ((g = fill_u32(reinterpret_cast<uint32_t *>(w.hdr + HW_PATH), 1u, 1, s)) != PC_OK) return g;
-        return fill_u32(reinterpret_cast<uint32_t *>(w.hdr + HW_REASON), (uint32_t)reason, 1, s);
+                  HW_HIGH_ANCHOR, HW_PATH);
+        return PC_OK;
     };
     if (n_seqs == 0) {   // n > 0 accesses in no request: an invalid layout
         if ((st = fill_u32(reinterpret_cast<uint32_t *>(w.hdr + HW_STATUS), (uint32_t)DEV_ERR_BAD_LAYOUT, 1, s)) !=
-            PC_OK)
+                PC_OK ||
+            (st = fill_u32(reinterpret_cast<uint32_t *>(w.hdr + HW_PATH), 1u, 1, s)) != PC_OK ||
+            (st = fill_u32(reinterpret_cast<uint32_t *>(w.hdr + HW_REASON), 1u, 1, s)) != PC_OK)
             return st;
-        return generic(1);
+        return generic(nullptr);
     }
 
+    // Every decision below is taken on the device: later launches are gated
+    // on header words, so the call never waits for the GPU.
     const uint64_t ns = chain_slots(n, n_seqs);
+    const int32_t *chain = w.hdr + HW_CHAIN;
     PC_LAUNCH(K_CHAIN_ANCHOR, chain_layout_kernel, dim3((unsigned)((n_seqs + 255) / 256)), dim3(256), 0, s,
               blk_off, n_seqs, n, w.hdr);
+    PC_LAUNCH(K_CHAIN_ANCHOR, chain_open_kernel, dim3(1), dim3(64), 0, s, w.hdr);
     PC_LAUNCH(K_CHAIN_ANCHOR, chain_anchor_kernel, dim3(wave_grid(n_seqs, cus)), dim3(CH_THREADS), 0, s, keys,
               blk_off, n_seqs, ns, deepest, w.akeys, w.rec, (const int32_t *)w.hdr);
-    if ((st = pc_prev_next_use(w.akeys, ns, w.aprev, w.anext, nullptr, w.aws, w.aws_bytes, stream)) != PC_OK)
-        return st;
-    PC_LAUNCH(K_FILL32, chain_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)w.aws, w.hdr,
-              HW_HIGH_ANCHOR);
-    if ((st = fill_u32(reinterpret_cast<uint32_t *>(w.claimed), 0u, 2 * ns, s)) != PC_OK) return st;
+    if ((st = prev_next_core(w.akeys, ns, nullptr, w.aprev, w.anext, nullptr, w.aws, s, chain)) != PC_OK) return st;
+    PC_LAUNCH(K_FILL32, chain_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)w.aws, w.hdr, HW_HIGH_ANCHOR,
+              HW_CHAIN);
+    if ((st = fill_u32_gated(reinterpret_cast<uint32_t *>(w.claimed), 0u, 2 * ns, s, chain)) != PC_OK) return st;
     PC_LAUNCH(K_CHAIN_STAIR, chain_stair_kernel, dim3(wave_grid((ns + CH_BATCH - 1) / CH_BATCH, cus)),
               dim3(CH_THREADS), 0, s, keys, ns, (const uint4 *)w.rec, w.aprev, deepest, prev, next, w.open,
               w.claimed, (const int32_t *)w.hdr);
@@ -482,34 +532,29 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
     PC_LAUNCH(K_CHAIN_SCAN, chain_scan_apply_kernel, dim3((unsigned)tiles), dim3(SCAN_THREADS), 0, s, w.cnt, ns,
               w.tsum, w.coff, (const int32_t *)w.hdr);
 
-    // the unresolved count decides the rest (first read-back)
-    int32_t h[8], nested = 0;
-    if ((st = read_words(w.hdr, h, 8, s)) != PC_OK) return st;
-    if ((st = read_words((const int32_t *)w.aws, &nested, 1, s)) != PC_OK) return st;
-    if (h[HW_BAD]) return generic(1);
-    if (nested) return generic(4);
-    const uint64_t m = (uint32_t)h[HW_UNRESOLVED];
+    // the unresolved accesses: compacted, their own prev/next (over the
+    // count the scan wrote, sized for the most that fit), merged back
+    const uint64_t m_cap = open_capacity(w, n);
     OpenWs o;
-    if (!carve_open(w, m, &o)) return generic(2);
-
+    carve_open(w.generic, m_cap, &o);
+    PC_LAUNCH(K_CHAIN_SCAN, chain_decide_kernel, dim3(1), dim3(64), 0, s, w.hdr, (const int32_t *)w.aws,
+              (uint32_t)m_cap);
     PC_LAUNCH(K_CHAIN_COMPACT, chain_compact_kernel, dim3(wave_grid((ns + CH_BATCH - 1) / CH_BATCH, cus)),
               dim3(CH_THREADS), 0, s, keys, ns, (const uint4 *)w.rec, (const uint4 *)w.open, w.coff, deepest,
-              o.ckeys, o.cpos, o.cflag);
-    if ((st = pc_prev_next_use(o.ckeys, m, o.cprev, o.cnext, nullptr, o.ws, o.ws_bytes, stream)) != PC_OK)
-        return st;
+              o.ckeys, o.cpos, o.cflag, (const int32_t *)w.hdr);
+    const uint32_t *m_dev = reinterpret_cast<const uint32_t *>(w.hdr + HW_UNRESOLVED);
+    if ((st = prev_next_core(o.ckeys, m_cap, m_dev, o.cprev, o.cnext, nullptr, o.ws, s, chain)) != PC_OK) return st;
     PC_LAUNCH(K_FILL32, chain_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)o.ws, w.hdr,
-              HW_HIGH_UNRESOLVED);
-    uint64_t mg = (m + CH_THREADS - 1) / CH_THREADS;
+              HW_HIGH_UNRESOLVED, HW_CHAIN);
+    uint64_t mg = (m_cap + CH_THREADS - 1) / CH_THREADS;
     if (mg > (uint64_t)cus * 16) mg = (uint64_t)cus * 16;
     PC_LAUNCH(K_CHAIN_MERGE, chain_merge_kernel, dim3((unsigned)(mg ? mg : 1)), dim3(CH_THREADS), 0, s, o.cpos,
-              o.cflag, o.cprev, o.cnext, m, prev, next, w.hdr);
+              o.cflag, o.cprev, o.cnext, prev, next, w.hdr);
 
-    // second read-back: the merge check and the nested call's status
-    if ((st = read_words(w.hdr, h, 8, s)) != PC_OK) return st;
-    if ((st = read_words((const int32_t *)o.ws, &nested, 1, s)) != PC_OK) return st;
-    if (nested) return generic(4);
-    if (h[HW_FAIL]) return generic(3);
-    return PC_OK;
+    // the check's verdict; the generic path over all keys runs only if it
+    // (or an earlier step) says so
+    PC_LAUNCH(K_CHAIN_MERGE, chain_verdict_kernel, dim3(1), dim3(64), 0, s, w.hdr, (const int32_t *)o.ws);
+    return generic(w.hdr + HW_PATH);
 }
 
 }  // extern "C"

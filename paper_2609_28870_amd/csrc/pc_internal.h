@@ -93,11 +93,38 @@ void prof_end(int kid, hipStream_t s);
 // compute units of the current device (256 on MI355X)
 int device_cus();
 
+// Grid of a loop over `items` tiles: at most `per_cu` workgroups per compute
+// unit (each takes every gridDim-th tile), so a launch that its gate turns
+// off costs a few thousand empty workgroups, not one per tile.
+unsigned capped(uint64_t items, int per_cu);
+
 // fill a uint32 array with a value on a stream (used instead of memset so the
 // same code stays valid under graph capture)
 pc_status fill_u32(uint32_t *p, uint32_t value, size_t count, hipStream_t s);
 
+// Gates: a launch given a device word runs only when the word is non-zero
+// (nullptr: always), so a path chosen on the device needs no read-back.
+pc_status fill_u32_gated(uint32_t *p, uint32_t value, size_t count, hipStream_t s, const int32_t *gate);
+
+// pc_stack_distance with every launch gated; workspace as
+// pc_stack_distance_ws(n)
+pc_status stack_distance_gated(const uint32_t *prev, const uint32_t *next, uint64_t n, uint32_t *dist, void *ws,
+                               hipStream_t s, const int32_t *gate);
+
+// pc_prev_next_use over min(n, *n_dev) keys (n_dev: a count the GPU wrote;
+// nullptr: n), grids and workspace sized for n (pc_prev_next_use_ws(n)),
+// every launch gated
+pc_status prev_next_core(const uint64_t *keys, uint64_t n, const uint32_t *n_dev, uint32_t *prev, uint32_t *next,
+                         const uint32_t *key_hist, void *ws, hipStream_t s, const int32_t *gate);
+
 // ------------------------------------------------------------ device helpers
+__device__ __forceinline__ bool gated_off(const int32_t *gate) { return gate && *gate == 0; }
+__device__ __forceinline__ uint64_t dev_count(uint64_t n, const uint32_t *n_dev) {
+    if (!n_dev) return n;
+    const uint64_t m = *n_dev;
+    return m < n ? m : n;
+}
+
 __device__ __forceinline__ uint64_t lanemask_lt() {
     const int lane = threadIdx.x & (WAVE - 1);
     return lane ? (~0ull >> (64 - lane)) : 0ull;

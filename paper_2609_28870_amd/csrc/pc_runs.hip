@@ -47,6 +47,10 @@ constexpr int RW_STATUS = 0;
 constexpr int RW_PATH = 1;    // 0 = runs, 1 = pc_stack_distance
 constexpr int RW_RUNS = 2;    // number of runs
 constexpr int RW_COLD = 3;    // number of cold accesses
+constexpr int RW_RUNS_OK = 4; // 1 = the runs path runs (the gate of its kernels)
+
+// the number of runs (written by the scan)
+__device__ __forceinline__ uint64_t runs_of(const int32_t *hdr) { return (uint32_t)hdr[RW_RUNS]; }
 
 // This thread's 16 consecutive prev values and the ones just before and
 // after them (from the neighbouring lanes, or from memory across waves and
@@ -194,79 +198,92 @@ __global__ __launch_bounds__(RUN_THREADS) void runs_compact_kernel(const uint32_
                                                                    const uint2 *__restrict__ marks,
                                                                    uint32_t *__restrict__ rp, uint32_t *__restrict__ rh,
                                                                    uint32_t *__restrict__ re,
-                                                                   uint32_t *__restrict__ rz) {
+                                                                   uint32_t *__restrict__ rz, uint64_t tiles,
+                                                                   const int32_t *__restrict__ hdr) {
+    if (!hdr[RW_RUNS_OK]) return;
     __shared__ uint32_t tmp[RUN_THREADS / WAVE];
-    const uint64_t t0 = (uint64_t)blockIdx.x * RUN_TILE + (uint64_t)threadIdx.x * RUN_ITEMS;
-    const uint2 mk = marks[(uint64_t)blockIdx.x * RUN_THREADS + threadIdx.x];
-    const uint32_t hm = mk.x & 0xFFFFu, cm = mk.x >> 16, em = mk.y;
-    uint32_t th = 0, tc = 0;
-    const uint2 o = off[blockIdx.x];
-    const uint32_t hs0 = o.x + block_excl_scan((uint32_t)__popc(hm), tmp, &th);   // runs started before t0
-    const uint32_t cs0 = o.y + block_excl_scan((uint32_t)__popc(cm), tmp, &tc);
-    // heads: one per set bit, numbered in position order
-    for (uint32_t m = hm; m; m &= m - 1) {
-        const int k = __builtin_ctz(m);
-        const uint32_t below = (1u << k) - 1;
-        const uint32_t s = hs0 + (uint32_t)__popc(hm & below);
-        rp[s] = prev[t0 + k];
-        rh[s] = (uint32_t)(t0 + k);
-        rz[s] = cs0 + (uint32_t)__popc(cm & below);
-    }
-    // run ends: the run is the last one started at or before the position
-    for (uint32_t m = em; m; m &= m - 1) {
-        const int k = __builtin_ctz(m);
-        const uint32_t upto = (k == 31) ? ~0u : (2u << k) - 1;
-        re[hs0 + (uint32_t)__popc(hm & upto) - 1] = (uint32_t)(t0 + k);
+    for (uint64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+        const uint64_t t0 = tile * RUN_TILE + (uint64_t)threadIdx.x * RUN_ITEMS;
+        const uint2 mk = marks[tile * RUN_THREADS + threadIdx.x];
+        const uint32_t hm = mk.x & 0xFFFFu, cm = mk.x >> 16, em = mk.y;
+        uint32_t th = 0, tc = 0;
+        const uint2 o = off[tile];
+        const uint32_t hs0 = o.x + block_excl_scan((uint32_t)__popc(hm), tmp, &th);   // runs started before t0
+        const uint32_t cs0 = o.y + block_excl_scan((uint32_t)__popc(cm), tmp, &tc);
+        // heads: one per set bit, numbered in position order
+        for (uint32_t m = hm; m; m &= m - 1) {
+            const int k = __builtin_ctz(m);
+            const uint32_t below = (1u << k) - 1;
+            const uint32_t s = hs0 + (uint32_t)__popc(hm & below);
+            rp[s] = prev[t0 + k];
+            rh[s] = (uint32_t)(t0 + k);
+            rz[s] = cs0 + (uint32_t)__popc(cm & below);
+        }
+        // run ends: the run is the last one started at or before the position
+        for (uint32_t m = em; m; m &= m - 1) {
+            const int k = __builtin_ctz(m);
+            const uint32_t upto = (k == 31) ? ~0u : (2u << k) - 1;
+            re[hs0 + (uint32_t)__popc(hm & upto) - 1] = (uint32_t)(t0 + k);
+        }
     }
 }
 
 // Level 0: keys p, weights len = e - h + 1 as one-element prefix sums.
 __global__ __launch_bounds__(256) void runs_init_kernel(const uint32_t *__restrict__ rp, const uint32_t *__restrict__ rh,
-                                                        const uint32_t *__restrict__ re, uint64_t r,
+                                                        const uint32_t *__restrict__ re,
                                                         uint32_t *__restrict__ key, uint32_t *__restrict__ pre,
-                                                        uint32_t *__restrict__ idx, uint32_t *__restrict__ acc) {
-    const uint64_t s = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (s >= r) return;
-    key[s] = rp[s];
-    pre[s] = re[s] - rh[s] + 1;
-    idx[s] = (uint32_t)s;
-    acc[s] = 0;
+                                                        uint32_t *__restrict__ idx, uint32_t *__restrict__ acc,
+                                                        const int32_t *__restrict__ hdr) {
+    if (!hdr[RW_RUNS_OK]) return;
+    const uint64_t r = runs_of(hdr);
+    for (uint64_t s = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; s < r; s += (uint64_t)gridDim.x * blockDim.x) {
+        key[s] = rp[s];
+        pre[s] = re[s] - rh[s] + 1;
+        idx[s] = (uint32_t)s;
+        acc[s] = 0;
+    }
 }
 
 // One merge level: blocks of 2^lvl elements sorted by key with inclusive
 // prefix sums of the weights become blocks of 2^(lvl+1).
 __global__ __launch_bounds__(256) void runs_merge_kernel(const uint32_t *__restrict__ key, const uint32_t *__restrict__ pre,
-                                                         const uint32_t *__restrict__ idx, uint64_t r, int lvl,
+                                                         const uint32_t *__restrict__ idx, int lvl,
                                                          uint32_t *__restrict__ key2, uint32_t *__restrict__ pre2,
-                                                         uint32_t *__restrict__ idx2, uint32_t *__restrict__ acc) {
-    const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= r) return;
-    const uint64_t blk = i >> lvl;
-    const uint64_t sb = (blk ^ 1) << lvl;
-    uint64_t se = sb + (1ull << lvl);
-    if (se > r) se = r;
-    const uint32_t k = key[i];
-    uint64_t lo = sb, hi = sb < r ? se : sb;   // first sibling key >= k (keys are distinct)
-    while (lo < hi) {
-        const uint64_t mid = (lo + hi) >> 1;
-        if (key[mid] < k) lo = mid + 1;
-        else hi = mid;
+                                                         uint32_t *__restrict__ idx2, uint32_t *__restrict__ acc,
+                                                         const int32_t *__restrict__ hdr) {
+    if (!hdr[RW_RUNS_OK]) return;
+    const uint64_t r = runs_of(hdr);
+    if ((1ull << lvl) >= r) return;   // the merge took fewer levels
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < r; i += (uint64_t)gridDim.x * blockDim.x) {
+        const uint64_t blk = i >> lvl;
+        const uint64_t sb = (blk ^ 1) << lvl;
+        uint64_t se = sb + (1ull << lvl);
+        if (se > r) se = r;
+        const uint32_t k = key[i];
+        uint64_t lo = sb, hi = sb < r ? se : sb;   // first sibling key >= k (keys are distinct)
+        while (lo < hi) {
+            const uint64_t mid = (lo + hi) >> 1;
+            if (key[mid] < k) lo = mid + 1;
+            else hi = mid;
+        }
+        const uint64_t rank = lo - sb;
+        const uint32_t below = rank ? pre[lo - 1] : 0u;   // sibling weights with smaller keys
+        if (blk & 1) acc[idx[i]] += below;                 // the sibling holds the earlier runs
+        const uint64_t q = ((blk >> 1) << (lvl + 1)) + (i - (blk << lvl)) + rank;
+        key2[q] = k;
+        pre2[q] = pre[i] + below;
+        idx2[q] = idx[i];
     }
-    const uint64_t rank = lo - sb;
-    const uint32_t below = rank ? pre[lo - 1] : 0u;   // sibling weights with smaller keys
-    if (blk & 1) acc[idx[i]] += below;                 // the sibling holds the earlier runs
-    const uint64_t q = ((blk >> 1) << (lvl + 1)) + (i - (blk << lvl)) + rank;
-    key2[q] = k;
-    pre2[q] = pre[i] + below;
-    idx2[q] = idx[i];
 }
 
 // Distance of every run, in place of its cold count: z + acc - p - 1.
 __global__ __launch_bounds__(256) void runs_dist_kernel(const uint32_t *__restrict__ rp,
-                                                        const uint32_t *__restrict__ acc, uint64_t r,
-                                                        uint32_t *__restrict__ rz) {
-    const uint64_t s = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (s < r) rz[s] = rz[s] + acc[s] - rp[s] - 1;
+                                                        const uint32_t *__restrict__ acc,
+                                                        uint32_t *__restrict__ rz, const int32_t *__restrict__ hdr) {
+    if (!hdr[RW_RUNS_OK]) return;
+    const uint64_t r = runs_of(hdr);
+    for (uint64_t s = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; s < r; s += (uint64_t)gridDim.x * blockDim.x)
+        rz[s] = rz[s] + acc[s] - rp[s] - 1;
 }
 
 // D of every position from the run list alone: a warm position lies in
@@ -274,61 +291,75 @@ __global__ __launch_bounds__(256) void runs_dist_kernel(const uint32_t *__restri
 // touch a tile are the one in progress at its start and those starting in
 // it; a thread finds the run at its first position by binary search and
 // walks on.
-__global__ __launch_bounds__(RUN_THREADS) void runs_fill_kernel(uint64_t n, uint64_t r, const uint2 *__restrict__ off,
+__global__ __launch_bounds__(RUN_THREADS) void runs_fill_kernel(uint64_t n, const uint2 *__restrict__ off,
                                                                 uint64_t tiles, const uint32_t *__restrict__ rh,
                                                                 const uint32_t *__restrict__ re,
                                                                 const uint32_t *__restrict__ rd,
-                                                                uint32_t *__restrict__ dist) {
-    // thread i holds positions tile0 + 1024 g + 4 i .. + 3 for g = 0..3
-    // (increasing), so each 16-byte store covers 1 KB across the wave
-    const uint64_t tile0 = (uint64_t)blockIdx.x * RUN_TILE;
-    const uint64_t t0 = tile0 + (uint64_t)threadIdx.x * 4;
-    const uint64_t first = off[blockIdx.x].x;
-    const int64_t lo = first ? (int64_t)first - 1 : 0;
-    const int64_t hi = blockIdx.x + 1 < tiles ? (int64_t)off[blockIdx.x + 1].x : (int64_t)r;
-    // last run in [lo, hi) with head <= t0, or lo - 1
-    int64_t a = lo, b = hi;
-    while (a < b) {
-        const int64_t m = (a + b) >> 1;
-        if (rh[m] <= t0) a = m + 1;
-        else b = m;
-    }
-    int64_t s = a - 1;
-    // the current run's end and distance and the next run's head, in
-    // registers: loads only where a run starts
-    bool in_run = s >= lo;
-    uint64_t end = in_run ? re[s] : 0;
-    uint32_t dv = in_run ? rd[s] : NONE;
-    uint64_t next_head = s + 1 < hi ? rh[s + 1] : ~0ull;
-    const bool vec = (reinterpret_cast<uintptr_t>(dist) & 15) == 0;
-#pragma unroll
-    for (int g = 0; g < RUN_ITEMS / 4; ++g) {
-        const uint64_t tg = t0 + (uint64_t)g * (RUN_THREADS * 4);
-        uint32_t d[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const uint64_t t = tg + k;
-            while (t >= next_head) {
-                ++s;
-                in_run = true;
-                end = re[s];
-                dv = rd[s];
-                next_head = s + 1 < hi ? rh[s + 1] : ~0ull;
-            }
-            d[k] = (in_run && end >= t) ? dv : NONE;
+                                                                uint32_t *__restrict__ dist,
+                                                                const int32_t *__restrict__ hdr) {
+    if (!hdr[RW_RUNS_OK]) return;
+    const uint64_t r = runs_of(hdr);
+    for (uint64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+        // thread i holds positions tile0 + 1024 g + 4 i .. + 3 for g = 0..3
+        // (increasing), so each 16-byte store covers 1 KB across the wave
+        const uint64_t tile0 = tile * RUN_TILE;
+        const uint64_t t0 = tile0 + (uint64_t)threadIdx.x * 4;
+        const uint64_t first = off[tile].x;
+        const int64_t lo = first ? (int64_t)first - 1 : 0;
+        const int64_t hi = tile + 1 < tiles ? (int64_t)off[tile + 1].x : (int64_t)r;
+        // last run in [lo, hi) with head <= t0, or lo - 1
+        int64_t a = lo, b = hi;
+        while (a < b) {
+            const int64_t m = (a + b) >> 1;
+            if (rh[m] <= t0) a = m + 1;
+            else b = m;
         }
-        if (vec && tg + 4 <= n) {
-            *reinterpret_cast<uint4 *>(dist + tg) = make_uint4(d[0], d[1], d[2], d[3]);
-        } else {
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-                if (tg + k < n) dist[tg + k] = d[k];
+        int64_t s = a - 1;
+        // the current run's end and distance and the next run's head, in
+        // registers: loads only where a run starts
+        bool in_run = s >= lo;
+        uint64_t end = in_run ? re[s] : 0;
+        uint32_t dv = in_run ? rd[s] : NONE;
+        uint64_t next_head = s + 1 < hi ? rh[s + 1] : ~0ull;
+        const bool vec = (reinterpret_cast<uintptr_t>(dist) & 15) == 0;
+    #pragma unroll
+        for (int g = 0; g < RUN_ITEMS / 4; ++g) {
+            const uint64_t tg = t0 + (uint64_t)g * (RUN_THREADS * 4);
+            uint32_t d[4];
+    #pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint64_t t = tg + k;
+                while (t >= next_head) {
+                    ++s;
+                    in_run = true;
+                    end = re[s];
+                    dv = rd[s];
+                    next_head = s + 1 < hi ? rh[s + 1] : ~0ull;
+                }
+                d[k] = (in_run && end >= t) ? dv : NONE;
+            }
+            if (vec && tg + 4 <= n) {
+                *reinterpret_cast<uint4 *>(dist + tg) = make_uint4(d[0], d[1], d[2], d[3]);
+            } else {
+    #pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    if (tg + k < n) dist[tg + k] = d[k];
+            }
         }
     }
 }
 
 __global__ void runs_status_kernel(const int32_t *__restrict__ nested, int32_t *__restrict__ hdr) {
-    if (threadIdx.x == 0 && nested[0]) atomicOr(hdr + RW_STATUS, nested[0]);
+    if (threadIdx.x == 0 && hdr[RW_PATH] && nested[0]) atomicOr(hdr + RW_STATUS, nested[0]);
+}
+
+// the path, decided from the number of runs: over runs, or the dominance
+// count over accesses when there are more runs than the workspace holds
+__global__ void runs_decide_kernel(int32_t *__restrict__ hdr, uint64_t rmax) {
+    if (threadIdx.x != 0) return;
+    const bool over = runs_of(hdr) > rmax;
+    hdr[RW_PATH] = over ? 1 : 0;
+    hdr[RW_RUNS_OK] = over ? 0 : 1;
 }
 
 static uint64_t runs_max(uint64_t n) { return n / 16 + 1024; }
@@ -385,7 +416,7 @@ pc_status pc_stack_distance_runs(const uint32_t *prev, const uint32_t *next, uin
     if (ws_bytes < pc_stack_distance_runs_ws(n)) return PC_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
     const RunsWs w = carve_runs(ws, n);
-    pc_status st = fill_u32(reinterpret_cast<uint32_t *>(w.hdr), 0u, 4, s);
+    pc_status st = fill_u32(reinterpret_cast<uint32_t *>(w.hdr), 0u, 8, s);
     if (st != PC_OK || n == 0) return st;
     const uint64_t tiles = (n + RUN_TILE - 1) / RUN_TILE;
     const uint64_t stiles = (tiles + RSCAN_TILE - 1) / RSCAN_TILE;
@@ -396,35 +427,33 @@ pc_status pc_stack_distance_runs(const uint32_t *prev, const uint32_t *next, uin
     PC_LAUNCH(K_RUNS_SCAN, runs_scan_top_kernel, dim3(1), dim3(RSCAN_THREADS), 0, s, w.tsum, stiles, w.hdr);
     PC_LAUNCH(K_RUNS_SCAN, runs_scan_apply_kernel, dim3((unsigned)stiles), dim3(RSCAN_THREADS), 0, s,
               (const uint2 *)w.counts, tiles, (const uint2 *)w.tsum, w.off);
-    int32_t h[4];
-    if (hipMemcpyAsync(h, w.hdr, sizeof(h), hipMemcpyDeviceToHost, s) != hipSuccess) return PC_ERR_DEVICE;
-    if (hipStreamSynchronize(s) != hipSuccess) return PC_ERR_DEVICE;
-    const uint64_t r = (uint32_t)h[RW_RUNS];
-    if (r > runs_max(n)) {
-        if ((st = pc_stack_distance(prev, next, n, dist, w.sd, w.sd_bytes, stream)) != PC_OK) return st;
-        PC_LAUNCH(K_FILL32, runs_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)w.sd, w.hdr);
-        return fill_u32(reinterpret_cast<uint32_t *>(w.hdr + RW_PATH), 1u, 1, s);
+    // the path is decided on the device, so nothing here waits for the GPU:
+    // every later launch is gated on the decision, and the launches of the
+    // path not taken return at once (grids capped per compute unit)
+    const uint64_t rm = runs_max(n);
+    PC_LAUNCH(K_RUNS_SCAN, runs_decide_kernel, dim3(1), dim3(64), 0, s, w.hdr, rm);
+    if ((st = stack_distance_gated(prev, next, n, dist, w.sd, s, w.hdr + RW_PATH)) != PC_OK) return st;
+    PC_LAUNCH(K_FILL32, runs_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)w.sd, w.hdr);
+    const int32_t *ok = w.hdr;
+    PC_LAUNCH(K_RUNS_COMPACT, runs_compact_kernel, dim3(capped(tiles, 16)), dim3(RUN_THREADS), 0, s, prev, n,
+              (const uint2 *)w.off, (const uint2 *)w.marks, w.rp, w.rh, w.re, w.rz, tiles, ok);
+    const unsigned rg = capped((rm + 255) / 256, 16);
+    PC_LAUNCH(K_RUNS_MERGE, runs_init_kernel, dim3(rg), dim3(256), 0, s, (const uint32_t *)w.rp,
+              (const uint32_t *)w.rh, (const uint32_t *)w.re, w.key[0], w.pre[0], w.idx[0], w.acc, ok);
+    // one launch per level the largest run count needs; the levels past the
+    // actual count return at once
+    int cur = 0;
+    for (int lvl = 0; (1ull << lvl) < rm; ++lvl) {
+        PC_LAUNCH(K_RUNS_MERGE, runs_merge_kernel, dim3(rg), dim3(256), 0, s, (const uint32_t *)w.key[cur],
+                  (const uint32_t *)w.pre[cur], (const uint32_t *)w.idx[cur], lvl, w.key[cur ^ 1], w.pre[cur ^ 1],
+                  w.idx[cur ^ 1], w.acc, ok);
+        cur ^= 1;
     }
-    PC_LAUNCH(K_RUNS_COMPACT, runs_compact_kernel, dim3((unsigned)tiles), dim3(RUN_THREADS), 0, s, prev, n,
-              (const uint2 *)w.off, (const uint2 *)w.marks, w.rp, w.rh, w.re, w.rz);
-    if (r > 0) {
-        const unsigned rg = (unsigned)((r + 255) / 256);
-        PC_LAUNCH(K_RUNS_MERGE, runs_init_kernel, dim3(rg), dim3(256), 0, s, (const uint32_t *)w.rp,
-                  (const uint32_t *)w.rh, (const uint32_t *)w.re, r, w.key[0], w.pre[0], w.idx[0], w.acc);
-        int cur = 0;
-        for (int lvl = 0; (1ull << lvl) < r; ++lvl) {
-            PC_LAUNCH(K_RUNS_MERGE, runs_merge_kernel, dim3(rg), dim3(256), 0, s, (const uint32_t *)w.key[cur],
-                      (const uint32_t *)w.pre[cur], (const uint32_t *)w.idx[cur], r, lvl, w.key[cur ^ 1],
-                      w.pre[cur ^ 1], w.idx[cur ^ 1], w.acc);
-            cur ^= 1;
-        }
-    }
-    if (r > 0)
-        PC_LAUNCH(K_RUNS_MERGE, runs_dist_kernel, dim3((unsigned)((r + 255) / 256)), dim3(256), 0, s,
-                  (const uint32_t *)w.rp, (const uint32_t *)w.acc, r, w.rz);
-    PC_LAUNCH(K_RUNS_FILL, runs_fill_kernel, dim3((unsigned)tiles), dim3(RUN_THREADS), 0, s, n, r,
+    PC_LAUNCH(K_RUNS_MERGE, runs_dist_kernel, dim3(rg), dim3(256), 0, s, (const uint32_t *)w.rp,
+              (const uint32_t *)w.acc, w.rz, ok);
+    PC_LAUNCH(K_RUNS_FILL, runs_fill_kernel, dim3(capped(tiles, 16)), dim3(RUN_THREADS), 0, s, n,
               (const uint2 *)w.off, tiles, (const uint32_t *)w.rh, (const uint32_t *)w.re, (const uint32_t *)w.rz,
-              dist);
+              dist, ok);
     return PC_OK;
 }
 

@@ -27,6 +27,12 @@
 //     next) triples and move them back to time order (see below).
 // Waits in the look-back are bounded: after the spin limit the kernel
 // records an error in the workspace header instead of hanging.
+//
+// Inside the library the same kernels also serve a count the GPU wrote
+// (n_dev: the chained prev/next sorts the accesses it left unresolved, a
+// number it only knows on the device): grids are sized for the host bound n,
+// workgroups past the device count return at once, and every launch can be
+// gated on a device word, so no call ever waits for the GPU.
 #include "pc_internal.h"
 
 namespace pc {
@@ -46,8 +52,11 @@ constexpr uint32_t SPIN_LIMIT = 1u << 22;
 constexpr int HIST_DIGITS = SORT_PASSES / 2;
 __global__ __launch_bounds__(256) void sort_hist_kernel(const uint64_t *__restrict__ keys, uint64_t n, int p0,
                                                         uint32_t *__restrict__ hist,
-                                                        const int32_t *__restrict__ only_if) {
-    if (only_if && *only_if == 0) return;
+                                                        const int32_t *__restrict__ only_if,
+                                                        const uint32_t *__restrict__ n_dev,
+                                                        const int32_t *__restrict__ gate) {
+    if ((only_if && *only_if == 0) || gated_off(gate)) return;
+    n = dev_count(n, n_dev);
     __shared__ uint32_t h[HIST_DIGITS][RADIX];
     for (int i = threadIdx.x; i < HIST_DIGITS * RADIX; i += blockDim.x) (&h[0][0])[i] = 0;
     __syncthreads();
@@ -70,8 +79,11 @@ __global__ __launch_bounds__(256) void sort_hist_kernel(const uint64_t *__restri
 __global__ __launch_bounds__(RADIX) void sort_scan_kernel(const uint32_t *__restrict__ hist, int p0,
                                                           uint32_t *__restrict__ start, uint64_t n,
                                                           int32_t *__restrict__ err,
-                                                          const int32_t *__restrict__ only_if) {
-    if (only_if && *only_if == 0) return;
+                                                          const int32_t *__restrict__ only_if,
+                                                          const uint32_t *__restrict__ n_dev,
+                                                          const int32_t *__restrict__ gate) {
+    if ((only_if && *only_if == 0) || gated_off(gate)) return;
+    n = dev_count(n, n_dev);
     __shared__ uint32_t tmp[RADIX / WAVE];
     for (int p = 0; p < HIST_DIGITS; ++p) {
         uint32_t total;
@@ -85,9 +97,11 @@ __global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_kernel(
     const uint64_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
     uint64_t *__restrict__ keys_out, uint32_t *__restrict__ vals_out, uint64_t n, int shift,
     const uint32_t *__restrict__ start, uint64_t *__restrict__ status, uint32_t *__restrict__ counter,
-    uint32_t epoch, int32_t *__restrict__ err, const int32_t *__restrict__ only_if) {
+    uint32_t epoch, int32_t *__restrict__ err, const int32_t *__restrict__ only_if,
+    const uint32_t *__restrict__ n_dev, const int32_t *__restrict__ gate) {
     // passes over the high key bits run only when the link step needs them
-    if (only_if && *only_if == 0) return;
+    if ((only_if && *only_if == 0) || gated_off(gate)) return;
+    n = dev_count(n, n_dev);
     // Large tiles make each digit's run in the output long (about 32
     // elements of 8192), so the scattered writes are mostly whole lines; the
     // tile is staged twice through one buffer (keys, then values) and the
@@ -103,6 +117,10 @@ __global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_kernel(
     const int tid = threadIdx.x;
     const int lane = tid & (WAVE - 1);
     const int w = tid / WAVE;
+    // Workgroups past the tile count take no tile (the counter then hands
+    // out exactly the tiles there are) and leave at once: a grid sized for a
+    // bound well above a device count costs little.
+    if ((uint64_t)blockIdx.x * SORT_TILE >= n) return;
     if (tid == 0) s_tile = atomicAdd(counter, 1u);
     for (int i = tid; i < SORT_WAVES * RADIX / 2; i += SORT_THREADS) reinterpret_cast<uint32_t *>(&s_wcnt[0][0])[i] = 0;
     __syncthreads();
@@ -238,6 +256,29 @@ constexpr int LINK_RADIX = 256;    // digits of the first pass: at most 256 buck
 constexpr int PERM_LOCAL_BITS = 14;
 constexpr uint64_t PERM_CHUNK_MAX = 1ull << 20;   // elements per workgroup, later passes
 constexpr uint64_t LINK_CHUNK_MAX = 1ull << 16;   // elements per workgroup, link
+
+// Work per workgroup: later passes take chunks of up to 2^20 elements (they
+// reserve per tile, so the chunk only spreads the work).  The link reserves
+// per chunk and its chunks are smaller: the runs that its workgroups in
+// flight append to then lie closer together, and the link, which waits on
+// more loads per element than the plain partition, gains from that.  About
+// two chunks per CU; the same on the host (grids) and the device (a count
+// the GPU wrote).
+__host__ __device__ inline uint64_t chunk_elems(uint64_t n, int cus, uint64_t cap, uint64_t tile) {
+    uint64_t c = (n + (uint64_t)cus * 2 - 1) / ((uint64_t)cus * 2);
+    c = (c + tile - 1) / tile * tile;
+    if (c > cap) c = cap;
+    return c < tile ? tile : c;
+}
+// the most chunks any count up to n splits into (the grid of a pass)
+static uint64_t max_chunks(uint64_t n, int cus, uint64_t cap, uint64_t tile) {
+    const uint64_t by_cap = (n + cap - 1) / cap;
+    const uint64_t by_cus = (uint64_t)cus * 2 + 1;
+    const uint64_t at_n = (n + chunk_elems(n, cus, cap, tile) - 1) / chunk_elems(n, cus, cap, tile);
+    uint64_t g = by_cap > by_cus ? by_cap : by_cus;
+    if (at_n > g) g = at_n;
+    return g ? g : 1;
+}
 
 // After the four passes over the low 32 key bits, equal keys are contiguous
 // unless different keys share those bits ("mixed" runs, a few percent of the
@@ -630,24 +671,32 @@ __device__ __forceinline__ void perm_partition_body(
 // long to scan; the second one runs only then (only_if = flag), over fully
 // sorted keys.
 __global__ __launch_bounds__(LINK_THREADS, 4) void link_partition_kernel(
-    const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t, uint64_t n, int s, uint64_t per_wg,
+    const uint64_t *__restrict__ sk, const uint32_t *__restrict__ in_t, uint64_t n, int s, int cus,
     uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn,
-    const int32_t *__restrict__ only_if, int32_t *__restrict__ flag) {
-    if (only_if && *only_if == 0) return;
+    const int32_t *__restrict__ only_if, int32_t *__restrict__ flag, const uint32_t *__restrict__ n_dev,
+    const int32_t *__restrict__ gate) {
+    if ((only_if && *only_if == 0) || gated_off(gate)) return;
+    n = dev_count(n, n_dev);
+    const uint64_t per_wg = chunk_elems(n, cus, LINK_CHUNK_MAX, LINK_TILE);
     __shared__ PermLds<LINK_TILE, LINK_THREADS, LINK_RADIX> L;
     perm_partition_body<true, LINK_THREADS, LINK_ITEMS, LINK_RADIX, false>(L, sk, in_t, nullptr, n, s, per_wg, cursor, out_t, out_pn, only_if != nullptr,
                               flag);
 }
 
 __global__ __launch_bounds__(PART_THREADS, 4) void perm_partition_kernel(
-    const uint32_t *__restrict__ in_t, const uint64_t *__restrict__ in_pn, uint64_t n, int s, uint64_t per_wg,
-    uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn) {
+    const uint32_t *__restrict__ in_t, const uint64_t *__restrict__ in_pn, uint64_t n, int s, int cus,
+    uint32_t *__restrict__ cursor, uint32_t *__restrict__ out_t, uint64_t *__restrict__ out_pn,
+    const uint32_t *__restrict__ n_dev, const int32_t *__restrict__ gate) {
+    if (gated_off(gate)) return;
+    n = dev_count(n, n_dev);
+    const uint64_t per_wg = chunk_elems(n, cus, PERM_CHUNK_MAX, PERM_TILE);
     __shared__ PermLds<PERM_TILE, PART_THREADS, PERM_RADIX> L;
     perm_partition_body<false, PART_THREADS, PART_ITEMS, PERM_RADIX, true>(L, nullptr, in_t, in_pn, n, s, per_wg, cursor, out_t, out_pn, true, nullptr);
 }
 
 // cursor[b] = b << s: each bucket's output run starts at its first t
-__global__ void perm_cursor_kernel(uint32_t *__restrict__ cursor, uint64_t nb, int s) {
+__global__ void perm_cursor_kernel(uint32_t *__restrict__ cursor, uint64_t nb, int s, const int32_t *__restrict__ gate) {
+    if (gated_off(gate)) return;
     const uint64_t b = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (b < nb) cursor[b] = (uint32_t)(b << s);
 }
@@ -659,11 +708,16 @@ constexpr int LOCAL_THREADS = 1024;
 __global__ __launch_bounds__(LOCAL_THREADS) void perm_local_kernel(const uint32_t *__restrict__ in_t,
                                                                    const uint64_t *__restrict__ in_pn,
                                                                    uint64_t n, uint32_t *__restrict__ prev,
-                                                                   uint32_t *__restrict__ next) {
+                                                                   uint32_t *__restrict__ next,
+                                                                   const uint32_t *__restrict__ n_dev,
+                                                                   const int32_t *__restrict__ gate) {
     constexpr uint32_t SPAN = 1u << PERM_LOCAL_BITS;
     constexpr int PER = SPAN / LOCAL_THREADS;
     __shared__ uint64_t s_pn[SPAN];
+    if (gated_off(gate)) return;
+    n = dev_count(n, n_dev);
     const uint64_t r0 = (uint64_t)blockIdx.x * SPAN;
+    if (r0 >= n) return;
     const uint32_t cnt = n - r0 < SPAN ? (uint32_t)(n - r0) : SPAN;
     const uint32_t *tb = in_t + r0;
     const uint64_t *pb = in_pn + r0;
@@ -756,6 +810,88 @@ static SortWs carve_sort(void *ws, uint64_t n) {
     return w;
 }
 
+
+pc_status prev_next_core(const uint64_t *keys, uint64_t n, const uint32_t *n_dev, uint32_t *prev, uint32_t *next,
+                         const uint32_t *key_hist, void *ws, hipStream_t s, const int32_t *gate) {
+    SortWs w = carve_sort(ws, n);
+    pc_status st = fill_u32_gated(reinterpret_cast<uint32_t *>(w.hdr), 0u, 1, s, gate);
+    if (st != PC_OK || n == 0) return st;
+
+    const uint64_t tiles = (n + SORT_TILE - 1) / SORT_TILE;
+    if ((st = fill_u32_gated(w.hist, 0u, SORT_PASSES * RADIX, s, gate)) != PC_OK) return st;
+    if ((st = fill_u32_gated(w.counters, 0u, SORT_PASSES, s, gate)) != PC_OK) return st;
+    if ((st = fill_u32_gated(reinterpret_cast<uint32_t *>(w.status), 0u, tiles * RADIX * 2, s, gate)) != PC_OK)
+        return st;
+
+    const int cus = device_cus();
+    uint64_t hg = (n + 4095) / 4096;
+    if (hg > (uint64_t)cus * 4) hg = (uint64_t)cus * 4;
+    // flag (header word 1): the first link met a mixed run too long to scan,
+    // so the high-byte passes and a second link run
+    int32_t *need_high = w.hdr + 1;
+    if ((st = fill_u32_gated(reinterpret_cast<uint32_t *>(need_high), 0u, 1, s, gate)) != PC_OK) return st;
+    // the low bytes' histograms: handed in by the hash, or counted here
+    if (!key_hist)
+        PC_LAUNCH(K_SORT_HIST, sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n, 0, w.hist,
+                  (const int32_t *)nullptr, n_dev, gate);
+    PC_LAUNCH(K_SORT_SCAN, sort_scan_kernel, dim3(1), dim3(RADIX), 0, s, key_hist ? key_hist : w.hist, 0, w.start, n,
+              w.hdr, (const int32_t *)nullptr, n_dev, gate);
+
+    // Links + partition back to time order.  The sort leaves (key, t) in
+    // (k2, v2) after four passes and again after eight; the triples ping-pong
+    // between the first sort buffers ((prev, next) pairs in k1, t in v1) and,
+    // once the sorted keys have been consumed, the second ones (k2, v2).
+    // The plan is made for the bound n: with fewer elements its later
+    // buckets stay empty.
+    const PermPlan pp = plan_perm(n);
+    if (pp.buckets[0] > (uint64_t)LINK_RADIX) return PC_ERR_TOO_LARGE;   // the plan never splits wider
+    uint32_t *bt[2] = {w.v1, w.v2};
+    uint64_t *bpn[2] = {w.k1, w.k2};
+    const unsigned ptiles = (unsigned)max_chunks(n, cus, PERM_CHUNK_MAX, PERM_TILE);
+    const unsigned ltiles = (unsigned)max_chunks(n, cus, LINK_CHUNK_MAX, LINK_TILE);
+    const unsigned cg0 = (unsigned)((pp.buckets[0] + 255) / 256);
+
+    const uint64_t *kin = keys;
+    const uint32_t *vin = nullptr;
+    for (int p = 0; p < SORT_PASSES; ++p) {
+        if (p == SORT_PASSES / 2) {
+            // first link, over keys sorted by their low 32 bits
+            PC_LAUNCH(K_FILL32, perm_cursor_kernel, dim3(cg0), dim3(256), 0, s, w.cursor, pp.buckets[0], pp.s[0],
+                      gate);
+            PC_LAUNCH(K_LINK, link_partition_kernel, dim3(ltiles), dim3(LINK_THREADS), 0, s, kin, vin, n, pp.s[0],
+                      cus, w.cursor, bt[0], bpn[0], (const int32_t *)nullptr, need_high, n_dev, gate);
+            PC_LAUNCH(K_SORT_HIST, sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n, SORT_PASSES / 2,
+                      w.hist, (const int32_t *)need_high, n_dev, gate);
+            PC_LAUNCH(K_SORT_SCAN, sort_scan_kernel, dim3(1), dim3(RADIX), 0, s, w.hist + SORT_PASSES / 2 * RADIX,
+                      SORT_PASSES / 2, w.start, n, w.hdr, (const int32_t *)need_high, n_dev, gate);
+        }
+        uint64_t *kout = (p & 1) ? w.k2 : w.k1;
+        uint32_t *vout = (p & 1) ? w.v2 : w.v1;
+        PC_LAUNCH(K_SORT_PASS, sort_pass_kernel, dim3((unsigned)tiles), dim3(SORT_THREADS), 0, s, kin, vin, kout,
+                  vout, n, 8 * p, w.start + p * RADIX, w.status, w.counters + p, (uint32_t)(p + 1), w.hdr,
+                  p >= SORT_PASSES / 2 ? (const int32_t *)need_high : nullptr, n_dev, gate);
+        kin = kout;
+        vin = vout;
+    }
+    // second link, over fully sorted keys, only if the first one gave up
+    PC_LAUNCH(K_FILL32, perm_cursor_kernel, dim3(cg0), dim3(256), 0, s, w.cursor, pp.buckets[0], pp.s[0], gate);
+    PC_LAUNCH(K_LINK, link_partition_kernel, dim3(ltiles), dim3(LINK_THREADS), 0, s, kin, vin, n, pp.s[0], cus,
+              w.cursor, bt[0], bpn[0], (const int32_t *)need_high, (int32_t *)nullptr, n_dev, gate);
+    int cur = 0;
+    for (int i = 1; i < pp.passes; ++i) {
+        const unsigned cg = (unsigned)((pp.buckets[i] + 255) / 256);
+        PC_LAUNCH(K_FILL32, perm_cursor_kernel, dim3(cg), dim3(256), 0, s, w.cursor, pp.buckets[i], pp.s[i], gate);
+        const int nxt = cur ^ 1;
+        PC_LAUNCH(K_PERM, perm_partition_kernel, dim3(ptiles), dim3(PART_THREADS), 0, s, bt[cur], bpn[cur], n,
+                  pp.s[i], cus, w.cursor, bt[nxt], bpn[nxt], n_dev, gate);
+        cur = nxt;
+    }
+    const uint64_t span = 1ull << PERM_LOCAL_BITS;
+    PC_LAUNCH(K_PERM_LOCAL, perm_local_kernel, dim3((unsigned)((n + span - 1) / span)), dim3(LOCAL_THREADS), 0, s,
+              bt[cur], bpn[cur], n, prev, next, n_dev, gate);
+    return PC_OK;
+}
+
 }  // namespace pc
 
 extern "C" {
@@ -768,98 +904,7 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
     if (n > 0 && (!keys || !prev || !next)) return PC_ERR_INVALID;
     if (!ws) return PC_ERR_WORKSPACE;
     if (ws_bytes < pc_prev_next_use_ws(n)) return PC_ERR_WORKSPACE;
-    hipStream_t s = (hipStream_t)stream;
-    pc::SortWs w = pc::carve_sort(ws, n);
-    pc_status st = pc::fill_u32(reinterpret_cast<uint32_t *>(w.hdr), 0u, 1, s);
-    if (st != PC_OK || n == 0) return st;
-
-    const uint64_t tiles = (n + pc::SORT_TILE - 1) / pc::SORT_TILE;
-    if ((st = pc::fill_u32(w.hist, 0u, pc::SORT_PASSES * pc::RADIX, s)) != PC_OK) return st;
-    if ((st = pc::fill_u32(w.counters, 0u, pc::SORT_PASSES, s)) != PC_OK) return st;
-    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(w.status), 0u, tiles * pc::RADIX * 2, s)) != PC_OK)
-        return st;
-
-    const int cus = pc::device_cus();
-    uint64_t hg = (n + 4095) / 4096;
-    if (hg > (uint64_t)cus * 4) hg = (uint64_t)cus * 4;
-    // flag (header word 1): the first link met a mixed run too long to scan,
-    // so the high-byte passes and a second link run
-    int32_t *need_high = w.hdr + 1;
-    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(need_high), 0u, 1, s)) != PC_OK) return st;
-    // the low bytes' histograms: handed in by the hash, or counted here
-    if (!key_hist)
-        PC_LAUNCH(pc::K_SORT_HIST, pc::sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n, 0, w.hist,
-                  (const int32_t *)nullptr);
-    PC_LAUNCH(pc::K_SORT_SCAN, pc::sort_scan_kernel, dim3(1), dim3(pc::RADIX), 0, s, key_hist ? key_hist : w.hist,
-              0, w.start, n, w.hdr, (const int32_t *)nullptr);
-
-    // Links + partition back to time order.  The sort leaves (key, t) in
-    // (k2, v2) after four passes and again after eight; the triples ping-pong
-    // between the first sort buffers ((prev, next) pairs in k1, t in v1) and,
-    // once the sorted keys have been consumed, the second ones (k2, v2).
-    const pc::PermPlan pp = pc::plan_perm(n);
-    if (pp.buckets[0] > (uint64_t)pc::LINK_RADIX) return PC_ERR_TOO_LARGE;   // the plan never splits wider
-    uint32_t *bt[2] = {w.v1, w.v2};
-    uint64_t *bpn[2] = {w.k1, w.k2};
-    // Work per workgroup: later passes take chunks of up to 2^20 elements
-    // (they reserve per tile, so the chunk only spreads the work).  The
-    // link reserves per chunk and its chunks are smaller: the runs that its
-    // workgroups in flight append to then lie closer together, and the
-    // link, which waits on more loads per element than the plain
-    // partition, gains from that.
-    auto chunk = [&](uint64_t cap, uint64_t tile) {
-        uint64_t c = (n + (uint64_t)cus * 2 - 1) / ((uint64_t)cus * 2);
-        c = (c + tile - 1) / tile * tile;
-        if (c > cap) c = cap;
-        return c < tile ? tile : c;
-    };
-    const uint64_t per_wg = chunk(pc::PERM_CHUNK_MAX, pc::PERM_TILE);
-    const unsigned ptiles = (unsigned)((n + per_wg - 1) / per_wg);
-    const uint64_t per_wg_link = chunk(pc::LINK_CHUNK_MAX, pc::LINK_TILE);
-    const unsigned ltiles = (unsigned)((n + per_wg_link - 1) / per_wg_link);
-    const unsigned cg0 = (unsigned)((pp.buckets[0] + 255) / 256);
-
-    const uint64_t *kin = keys;
-    const uint32_t *vin = nullptr;
-    for (int p = 0; p < pc::SORT_PASSES; ++p) {
-        if (p == pc::SORT_PASSES / 2) {
-            // first link, over keys sorted by their low 32 bits
-            PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg0), dim3(256), 0, s, w.cursor, pp.buckets[0],
-                      pp.s[0]);
-            PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ltiles), dim3(pc::LINK_THREADS), 0, s, kin, vin,
-                      n, pp.s[0], per_wg_link, w.cursor, bt[0], bpn[0], (const int32_t *)nullptr, need_high);
-            PC_LAUNCH(pc::K_SORT_HIST, pc::sort_hist_kernel, dim3((unsigned)hg), dim3(256), 0, s, keys, n,
-                      pc::SORT_PASSES / 2, w.hist, (const int32_t *)need_high);
-            PC_LAUNCH(pc::K_SORT_SCAN, pc::sort_scan_kernel, dim3(1), dim3(pc::RADIX), 0, s,
-                      w.hist + pc::SORT_PASSES / 2 * pc::RADIX, pc::SORT_PASSES / 2, w.start, n, w.hdr,
-                      (const int32_t *)need_high);
-        }
-        uint64_t *kout = (p & 1) ? w.k2 : w.k1;
-        uint32_t *vout = (p & 1) ? w.v2 : w.v1;
-        PC_LAUNCH(pc::K_SORT_PASS, pc::sort_pass_kernel, dim3((unsigned)tiles), dim3(pc::SORT_THREADS), 0, s,
-                  kin, vin, kout, vout, n, 8 * p, w.start + p * pc::RADIX, w.status, w.counters + p,
-                  (uint32_t)(p + 1), w.hdr, p >= pc::SORT_PASSES / 2 ? (const int32_t *)need_high : nullptr);
-        kin = kout;
-        vin = vout;
-    }
-    // second link, over fully sorted keys, only if the first one gave up
-    PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg0), dim3(256), 0, s, w.cursor, pp.buckets[0], pp.s[0]);
-    PC_LAUNCH(pc::K_LINK, pc::link_partition_kernel, dim3(ltiles), dim3(pc::LINK_THREADS), 0, s, kin, vin, n,
-              pp.s[0], per_wg_link, w.cursor, bt[0], bpn[0], (const int32_t *)need_high, (int32_t *)nullptr);
-    int cur = 0;
-    for (int i = 1; i < pp.passes; ++i) {
-        const unsigned cg = (unsigned)((pp.buckets[i] + 255) / 256);
-        PC_LAUNCH(pc::K_FILL32, pc::perm_cursor_kernel, dim3(cg), dim3(256), 0, s, w.cursor, pp.buckets[i],
-                  pp.s[i]);
-        const int nxt = cur ^ 1;
-        PC_LAUNCH(pc::K_PERM, pc::perm_partition_kernel, dim3(ptiles), dim3(pc::PART_THREADS), 0, s, bt[cur],
-                  bpn[cur], n, pp.s[i], per_wg, w.cursor, bt[nxt], bpn[nxt]);
-        cur = nxt;
-    }
-    const uint64_t span = 1ull << pc::PERM_LOCAL_BITS;
-    PC_LAUNCH(pc::K_PERM_LOCAL, pc::perm_local_kernel, dim3((unsigned)((n + span - 1) / span)),
-              dim3(pc::LOCAL_THREADS), 0, s, bt[cur], bpn[cur], n, prev, next);
-    return PC_OK;
+    return pc::prev_next_core(keys, n, nullptr, prev, next, key_hist, ws, (hipStream_t)stream, nullptr);
 }
 
 }  // extern "C"

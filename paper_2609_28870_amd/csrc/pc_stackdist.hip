@@ -60,10 +60,14 @@ __device__ __forceinline__ uint64_t cnt_lt(uint64_t X, const uint32_t *__restric
 }
 
 __global__ __launch_bounds__(256) void sd_cold_count_kernel(const uint32_t *__restrict__ prev,
-                                                            uint64_t n, uint32_t *__restrict__ cnt) {
+                                                            uint64_t n, uint32_t *__restrict__ cnt,
+                                                            const int32_t *gate) {
+    if (gated_off(gate)) return;
     __shared__ uint32_t tmp[4];
     constexpr int PER = LOCAL_SPAN / 256;   // 16 consecutive values per thread
-    const uint64_t base = (uint64_t)blockIdx.x * LOCAL_SPAN + (uint64_t)threadIdx.x * PER;
+    const uint64_t nchunks = (n + LOCAL_SPAN - 1) / LOCAL_SPAN;
+    for (uint64_t chunk = blockIdx.x; chunk < nchunks; chunk += gridDim.x) {
+    const uint64_t base = chunk * LOCAL_SPAN + (uint64_t)threadIdx.x * PER;
     uint32_t c = 0;
     if (base + PER <= n && (reinterpret_cast<uintptr_t>(prev) & 15) == 0) {
         const uint4 *p = reinterpret_cast<const uint4 *>(prev + base);   // four 16-byte loads in flight
@@ -78,13 +82,16 @@ __global__ __launch_bounds__(256) void sd_cold_count_kernel(const uint32_t *__re
     }
     uint32_t total;
     block_excl_scan(c, tmp, &total);
-    if (threadIdx.x == 0) cnt[blockIdx.x] = total;
+    if (threadIdx.x == 0) cnt[chunk] = total;
+    }
 }
 
 // exclusive scan of m values (one workgroup); out[m] = total
 __global__ __launch_bounds__(SCAN_THREADS) void sd_scan_kernel(const uint32_t *__restrict__ in,
                                                                uint64_t m,
-                                                               uint32_t *__restrict__ out) {
+                                                               uint32_t *__restrict__ out,
+                                                               const int32_t *gate) {
+    if (gated_off(gate)) return;
     __shared__ uint32_t tmp[SCAN_THREADS / WAVE];
     const uint64_t seg = (m + SCAN_THREADS - 1) / SCAN_THREADS;
     const uint64_t lo = threadIdx.x * seg;
@@ -106,7 +113,9 @@ __global__ __launch_bounds__(SCAN_THREADS) void sd_scan_kernel(const uint32_t *_
 // scans itself on top of its offset.  out[m] = total.
 constexpr int SCAN_BLOCK = SCAN_THREADS * 4;
 __global__ __launch_bounds__(SCAN_THREADS) void sd_scan_reduce_kernel(const uint32_t *__restrict__ in, uint64_t m,
-                                                                      uint32_t *__restrict__ part) {
+                                                                      uint32_t *__restrict__ part,
+                                                                      const int32_t *gate) {
+    if (gated_off(gate)) return;
     __shared__ uint32_t tmp[SCAN_THREADS / WAVE];
     const uint64_t i0 = (uint64_t)blockIdx.x * SCAN_BLOCK + (uint64_t)threadIdx.x * 4;
     uint32_t x = 0;
@@ -119,7 +128,9 @@ __global__ __launch_bounds__(SCAN_THREADS) void sd_scan_reduce_kernel(const uint
 
 __global__ __launch_bounds__(SCAN_THREADS) void sd_scan_apply_kernel(const uint32_t *__restrict__ in, uint64_t m,
                                                                      const uint32_t *__restrict__ part_ex,
-                                                                     uint64_t nblocks, uint32_t *__restrict__ out) {
+                                                                     uint64_t nblocks, uint32_t *__restrict__ out,
+                                                                     const int32_t *gate) {
+    if (gated_off(gate)) return;
     __shared__ uint32_t tmp[SCAN_THREADS / WAVE];
     const uint64_t i0 = (uint64_t)blockIdx.x * SCAN_BLOCK + (uint64_t)threadIdx.x * 4;
     uint32_t v[4], x = 0;
@@ -140,7 +151,8 @@ __global__ __launch_bounds__(SCAN_THREADS) void sd_scan_apply_kernel(const uint3
 
 // tiles per bucket of a dominance pass (bucket = t >> S)
 __global__ void sd_tile_count_kernel(const uint32_t *__restrict__ Zc, uint64_t n, int S,
-                                     uint64_t nbuckets, uint32_t *__restrict__ tcount) {
+                                     uint64_t nbuckets, uint32_t *__restrict__ tcount, const int32_t *gate) {
+    if (gated_off(gate)) return;
     const uint64_t b = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= nbuckets) return;
     uint64_t lo = b << S, hi = (b + 1) << S;
@@ -162,7 +174,8 @@ struct TileLoc {
 // tile -> bucket of a level (largest b with tfirst[b] <= tile), computed
 // once per level so the level's kernels need one load instead of a search
 __global__ void sd_tile_bucket_kernel(const uint32_t *__restrict__ tfirst, uint64_t nbuckets, uint64_t max_tiles,
-                                      uint32_t *__restrict__ tile_bucket) {
+                                      uint32_t *__restrict__ tile_bucket, const int32_t *gate) {
+    if (gated_off(gate)) return;
     const uint64_t tile = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (tile >= max_tiles || tile >= tfirst[nbuckets]) return;
     uint64_t lo = 0, hi = nbuckets;
@@ -231,17 +244,20 @@ template <bool FIRST>
 __global__ __launch_bounds__(DOM_THREADS) void sd_count_kernel(
     const uint32_t *__restrict__ in_t, uint64_t n, const uint32_t *__restrict__ Zc, int s, int k,
     const uint32_t *__restrict__ tfirst, uint64_t nbuckets, const uint32_t *__restrict__ tile_bucket,
-    uint16_t *__restrict__ cnt, uint8_t *__restrict__ seg) {
+    uint16_t *__restrict__ cnt, uint8_t *__restrict__ seg, uint64_t groups, const int32_t *gate) {
+    if (gated_off(gate)) return;
     __shared__ uint32_t s_cnt[COUNT_TPW][DOM_RADIX];
     const int tid = threadIdx.x, lane = tid & (WAVE - 1), w = tid / WAVE;
-    const uint64_t tile0 = (uint64_t)blockIdx.x * COUNT_TPW;
+    for (uint64_t grp = blockIdx.x; grp < groups; grp += gridDim.x) {
+    __syncthreads();   // the previous group's counts are written out
+    const uint64_t tile0 = grp * COUNT_TPW;
     // an invalid tile (past the level's last) has an empty range: it loads
     // nothing, and every later tile is invalid too
     TileLoc L[COUNT_TPW];
 #pragma unroll
     for (int q = 0; q < COUNT_TPW; ++q)
         L[q] = locate_tile<FIRST>(tile0 + q, n, Zc, s + k, tfirst, nbuckets, tile_bucket);
-    if (!L[0].valid) return;
+    if (!L[0].valid) break;   // every later group is past the level's last tile too
     for (int i = tid; i < COUNT_TPW * DOM_RADIX; i += DOM_THREADS) (&s_cnt[0][0])[i] = 0;
     uint32_t t[COUNT_TPW][DOM_CHUNKS_PER_WAVE], acc[DOM_CHUNKS_PER_WAVE];
     bool ok[COUNT_TPW][DOM_CHUNKS_PER_WAVE];
@@ -272,6 +288,7 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_count_kernel(
         if (tid < DOM_RADIX) cnt[tile * DOM_RADIX + tid] = (uint16_t)s_cnt[q][tid];
         if (tid == 0) seg[tile] = FIRST ? (tile == 0) : (tile == L[q].first_tile);
     }
+    }
 }
 
 // Segmented exclusive scan over tiles, per digit (a bucket's first tile
@@ -288,7 +305,8 @@ __global__ __launch_bounds__(DOM_RADIX) void sd_seg_reduce_kernel(const uint16_t
                                                                   const uint8_t *__restrict__ seg,
                                                                   const uint32_t *tfirst_end, uint64_t fixed,
                                                                   uint32_t *__restrict__ gsum,
-                                                                  uint8_t *__restrict__ ghas) {
+                                                                  uint8_t *__restrict__ ghas, const int32_t *gate) {
+    if (gated_off(gate)) return;
     const uint64_t rows = total_tiles(tfirst_end, fixed);
     const uint64_t r0 = (uint64_t)blockIdx.x * SEG_GROUP;
     if (r0 >= rows) return;
@@ -324,7 +342,8 @@ constexpr int CARRY_THREADS = 1024;
 __global__ __launch_bounds__(CARRY_THREADS) void sd_seg_carry_kernel(const uint32_t *__restrict__ gsum,
                                                                      const uint8_t *__restrict__ ghas,
                                                                      const uint32_t *tfirst_end, uint64_t fixed,
-                                                                     uint32_t *__restrict__ gin) {
+                                                                     uint32_t *__restrict__ gin, const int32_t *gate) {
+    if (gated_off(gate)) return;
     __shared__ uint32_t s_val[CARRY_THREADS / WAVE];
     __shared__ uint32_t s_has[CARRY_THREADS / WAVE];
     const uint64_t rows = total_tiles(tfirst_end, fixed);
@@ -365,7 +384,8 @@ __global__ __launch_bounds__(DOM_RADIX) void sd_seg_scan_kernel(const uint16_t *
                                                                 const uint8_t *__restrict__ seg,
                                                                 const uint32_t *tfirst_end, uint64_t fixed,
                                                                 const uint32_t *__restrict__ gin,
-                                                                uint32_t *__restrict__ pre) {
+                                                                uint32_t *__restrict__ pre, const int32_t *gate) {
+    if (gated_off(gate)) return;
     const uint64_t rows = total_tiles(tfirst_end, fixed);
     const uint64_t r0 = (uint64_t)blockIdx.x * SEG_GROUP;
     if (r0 >= rows) return;
@@ -403,7 +423,8 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     uint32_t *__restrict__ out_t, uint32_t *__restrict__ out_acc, uint64_t n,
     const uint32_t *__restrict__ Zc, int s, int k, const uint32_t *__restrict__ tfirst,
     uint64_t nbuckets, const uint32_t *__restrict__ tile_bucket, const uint32_t *__restrict__ pre,
-    int32_t *__restrict__ err) {
+    int32_t *__restrict__ err, uint64_t ntiles, const int32_t *gate) {
+    if (gated_off(gate)) return;
     // chunk histograms -> column prefix; once every position is known, the
     // staged tile (t, then acc) in the same space: 36 KB of LDS in all, so
     // four workgroups share a CU
@@ -423,9 +444,10 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
     const int lane = tid & (WAVE - 1);
     const int w = tid / WAVE;
     const uint32_t dmask = (1u << k) - 1u;
-    const uint64_t tile = blockIdx.x;
+    for (uint64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    __syncthreads();   // the previous tile has left the LDS
     const TileLoc L = locate_tile<FIRST>(tile, n, Zc, s + k, tfirst, nbuckets, tile_bucket);
-    if (!L.valid) return;
+    if (!L.valid) break;   // every later tile is past the level's last too
     // same digit, earlier tiles of the bucket (threads below RADIX own a digit)
     const uint32_t G = tid < DOM_RADIX ? pre[tile * DOM_RADIX + tid] : 0u;
     {
@@ -532,6 +554,7 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
             atomicOr(err, DEV_ERR_BAD_LAYOUT);
         }
     }
+    }
 }
 
 // Last 12 bits, one workgroup per 4096-range of t, then D in t order.  The
@@ -541,7 +564,8 @@ __global__ __launch_bounds__(DOM_THREADS) void sd_dominance_kernel(
 __global__ __launch_bounds__(LOC_THREADS, 6) void sd_local_kernel(
     const uint32_t *__restrict__ in_t, const uint32_t *__restrict__ in_acc,
     const uint32_t *__restrict__ prev, uint64_t n, const uint32_t *__restrict__ Zc,
-    uint32_t *__restrict__ dist) {
+    uint32_t *__restrict__ dist, const int32_t *gate) {
+    if (gated_off(gate)) return;
     __shared__ uint32_t slot[LOCAL_SPAN];           // by t: acc + counts; first the column-prefix sums
     __shared__ uint16_t s_h[LOC_CHUNKS][64];        // chunk histograms -> column prefix
     __shared__ uint16_t s_pl[LOC_CHUNKS][64];       // 2-D prefix (earlier chunks, smaller digit)
@@ -553,7 +577,10 @@ __global__ __launch_bounds__(LOC_THREADS, 6) void sd_local_kernel(
     const int tid = threadIdx.x;
     const int lane = tid & (WAVE - 1);
     const int w = tid / WAVE;
-    const uint64_t r0 = (uint64_t)blockIdx.x * LOCAL_SPAN;
+    const uint64_t nchunks = (n + LOCAL_SPAN - 1) / LOCAL_SPAN;
+    for (uint64_t chunk = blockIdx.x; chunk < nchunks; chunk += gridDim.x) {
+    __syncthreads();   // the previous range has left the LDS
+    const uint64_t r0 = chunk * LOCAL_SPAN;
     const uint64_t r1 = r0 + LOCAL_SPAN < n ? r0 + LOCAL_SPAN : n;
     const uint64_t e0 = cnt_lt(r0, Zc), e1 = cnt_lt(r1, Zc);
     for (int i = tid; i < LOC_CHUNKS * 64 / 2; i += LOC_THREADS) reinterpret_cast<uint32_t *>(&s_h[0][0])[i] = 0;
@@ -665,7 +692,7 @@ __global__ __launch_bounds__(LOC_THREADS, 6) void sd_local_kernel(
 #pragma unroll
     for (int j = 0; j < PER; ++j) cold += (tbase + j < n && p[j] == NONE) ? 1u : 0u;
     uint32_t allcold;
-    uint32_t z = Zc[blockIdx.x] + block_excl_scan(cold, s_tmp, &allcold);
+    uint32_t z = Zc[chunk] + block_excl_scan(cold, s_tmp, &allcold);
     uint32_t dv[PER];
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
@@ -683,6 +710,7 @@ __global__ __launch_bounds__(LOC_THREADS, 6) void sd_local_kernel(
 #pragma unroll
         for (int j = 0; j < PER; ++j)
             if (tbase + j < n) dist[tbase + j] = dv[j];
+    }
     }
 }
 
@@ -847,15 +875,15 @@ static SdWs carve_sd(void *ws, uint64_t n, const SdPlan &p) {
 }
 
 // Z at every multiple of 4096 from the cold (prev = none) flags
-static pc_status sd_cold_prefix(const uint32_t *prev, uint64_t n, SdWs &w, hipStream_t s) {
+static pc_status sd_cold_prefix(const uint32_t *prev, uint64_t n, SdWs &w, hipStream_t s, const int32_t *gate) {
     const uint64_t nchunks = (n + LOCAL_SPAN - 1) / LOCAL_SPAN;
-    PC_LAUNCH(K_SD_COLD, sd_cold_count_kernel, dim3((unsigned)nchunks), dim3(256), 0, s, prev, n, w.cold);
+    PC_LAUNCH(K_SD_COLD, sd_cold_count_kernel, dim3(capped(nchunks, 16)), dim3(256), 0, s, prev, n, w.cold, gate);
     const uint64_t nblocks = (nchunks + SCAN_BLOCK - 1) / SCAN_BLOCK;
     PC_LAUNCH(K_SD_SCAN, sd_scan_reduce_kernel, dim3((unsigned)nblocks), dim3(SCAN_THREADS), 0, s, w.cold, nchunks,
-              w.part);
-    PC_LAUNCH(K_SD_SCAN, sd_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, s, w.part, nblocks, w.part_ex);
+              w.part, gate);
+    PC_LAUNCH(K_SD_SCAN, sd_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, s, w.part, nblocks, w.part_ex, gate);
     PC_LAUNCH(K_SD_SCAN, sd_scan_apply_kernel, dim3((unsigned)nblocks), dim3(SCAN_THREADS), 0, s, w.cold, nchunks,
-              w.part_ex, nblocks, w.Zc);
+              w.part_ex, nblocks, w.Zc, gate);
     return PC_OK;
 }
 
@@ -863,50 +891,68 @@ static pc_status sd_cold_prefix(const uint32_t *prev, uint64_t n, SdWs &w, hipSt
 // each element, PC_NONE for a slot without one), in the order whose
 // dominance count is wanted.  Leaves (t, acc) partitioned by t's 4096-range.
 static pc_status sd_levels(const uint32_t *first, uint64_t n, const SdPlan &p, SdWs &w, hipStream_t s,
-                           uint32_t **out_t, uint32_t **out_a) {
+                           uint32_t **out_t, uint32_t **out_a, const int32_t *gate) {
     uint32_t *src_t = nullptr, *src_a = nullptr;
     for (int i = 0; i < p.passes; ++i) {
         uint32_t *dt = (i & 1) ? w.bt : w.at;
         uint32_t *da = (i & 1) ? w.ba : w.aa;
         const int S = p.s[i] + p.k[i];
-        const unsigned grid = (unsigned)p.grid[i];
-        const unsigned cgrid = (unsigned)((p.grid[i] + COUNT_TPW - 1) / COUNT_TPW);
+        const uint64_t ntiles = p.grid[i];
+        const uint64_t cgroups = (p.grid[i] + COUNT_TPW - 1) / COUNT_TPW;
         const unsigned groups = (unsigned)((p.grid[i] + SEG_GROUP - 1) / SEG_GROUP);
         const uint64_t fixed = (n + DOM_TILE - 1) / DOM_TILE;
         if (i == 0) {
-            PC_LAUNCH(K_SD_COUNT, sd_count_kernel<true>, dim3(cgrid), dim3(DOM_THREADS), 0, s, first, n, w.Zc,
-                      p.s[i], p.k[i], (const uint32_t *)nullptr, (uint64_t)1, (const uint32_t *)nullptr, w.cnt,
-                      w.seg);
+            PC_LAUNCH(K_SD_COUNT, sd_count_kernel<true>, dim3(capped(cgroups, 8)), dim3(DOM_THREADS), 0, s, first, n,
+                      w.Zc, p.s[i], p.k[i], (const uint32_t *)nullptr, (uint64_t)1, (const uint32_t *)nullptr, w.cnt,
+                      w.seg, cgroups, gate);
         } else {
             const uint64_t nb = p.nbuckets[i];
             PC_LAUNCH(K_SD_TILES, sd_tile_count_kernel, dim3((unsigned)((nb + 255) / 256)), dim3(256), 0, s, w.Zc,
-                      n, S, nb, w.tcount);
-            PC_LAUNCH(K_SD_SCAN, sd_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, s, w.tcount, nb, w.tfirst);
+                      n, S, nb, w.tcount, gate);
+            PC_LAUNCH(K_SD_SCAN, sd_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, s, w.tcount, nb, w.tfirst, gate);
             PC_LAUNCH(K_SD_TILES, sd_tile_bucket_kernel, dim3((unsigned)((p.grid[i] + 255) / 256)), dim3(256), 0,
-                      s, w.tfirst, nb, p.grid[i], w.tile_bucket);
-            PC_LAUNCH(K_SD_COUNT, sd_count_kernel<false>, dim3(cgrid), dim3(DOM_THREADS), 0, s, src_t, n, w.Zc,
-                      p.s[i], p.k[i], w.tfirst, nb, w.tile_bucket, w.cnt, w.seg);
+                      s, w.tfirst, nb, p.grid[i], w.tile_bucket, gate);
+            PC_LAUNCH(K_SD_COUNT, sd_count_kernel<false>, dim3(capped(cgroups, 8)), dim3(DOM_THREADS), 0, s, src_t,
+                      n, w.Zc, p.s[i], p.k[i], w.tfirst, nb, w.tile_bucket, w.cnt, w.seg, cgroups, gate);
         }
         const uint32_t *tend = i == 0 ? nullptr : w.tfirst + p.nbuckets[i];
         PC_LAUNCH(K_SD_SEG, sd_seg_reduce_kernel, dim3(groups), dim3(DOM_RADIX), 0, s, w.cnt, w.seg, tend, fixed,
-                  w.gsum, w.ghas);
+                  w.gsum, w.ghas, gate);
         PC_LAUNCH(K_SD_SEG, sd_seg_carry_kernel, dim3(DOM_RADIX), dim3(CARRY_THREADS), 0, s, w.gsum, w.ghas, tend,
-                  fixed, w.gin);
+                  fixed, w.gin, gate);
         PC_LAUNCH(K_SD_SEG, sd_seg_scan_kernel, dim3(groups), dim3(DOM_RADIX), 0, s, w.cnt, w.seg, tend, fixed,
-                  w.gin, w.pre);
+                  w.gin, w.pre, gate);
         if (i == 0) {
-            PC_LAUNCH(K_SD_PASS, sd_dominance_kernel<true>, dim3(grid), dim3(DOM_THREADS), 0, s, first,
+            PC_LAUNCH(K_SD_PASS, sd_dominance_kernel<true>, dim3(capped(ntiles, 8)), dim3(DOM_THREADS), 0, s, first,
                       (const uint32_t *)nullptr, dt, da, n, w.Zc, p.s[i], p.k[i], (const uint32_t *)nullptr,
-                      (uint64_t)1, (const uint32_t *)nullptr, w.pre, w.hdr);
+                      (uint64_t)1, (const uint32_t *)nullptr, w.pre, w.hdr, ntiles, gate);
         } else {
-            PC_LAUNCH(K_SD_PASS, sd_dominance_kernel<false>, dim3(grid), dim3(DOM_THREADS), 0, s, src_t, src_a, dt,
-                      da, n, w.Zc, p.s[i], p.k[i], w.tfirst, p.nbuckets[i], w.tile_bucket, w.pre, w.hdr);
+            PC_LAUNCH(K_SD_PASS, sd_dominance_kernel<false>, dim3(capped(ntiles, 8)), dim3(DOM_THREADS), 0, s, src_t,
+                      src_a, dt, da, n, w.Zc, p.s[i], p.k[i], w.tfirst, p.nbuckets[i], w.tile_bucket, w.pre, w.hdr,
+                      ntiles, gate);
         }
         src_t = dt;
         src_a = da;
     }
     *out_t = src_t;
     *out_a = src_a;
+    return PC_OK;
+}
+
+// The whole dominance count; with a gate, every launch is skipped on the
+// device unless the gate word is non-zero.
+pc_status stack_distance_gated(const uint32_t *prev, const uint32_t *next, uint64_t n, uint32_t *dist, void *ws,
+                               hipStream_t s, const int32_t *gate) {
+    const SdPlan p = plan_sd(n);
+    SdWs w = carve_sd(ws, n, p);
+    pc_status st = fill_u32_gated(reinterpret_cast<uint32_t *>(w.hdr), 0u, 1, s, gate);
+    if (st != PC_OK || n == 0) return st;
+    if ((st = sd_cold_prefix(prev, n, w, s, gate)) != PC_OK) return st;
+    uint32_t *lt, *la;
+    if ((st = sd_levels(next, n, p, w, s, &lt, &la, gate)) != PC_OK) return st;
+    const uint64_t nchunks = (n + LOCAL_SPAN - 1) / LOCAL_SPAN;
+    PC_LAUNCH(K_SD_LOCAL, sd_local_kernel, dim3(capped(nchunks, 8)), dim3(LOC_THREADS), 0, s, lt, la, prev, n, w.Zc,
+              dist, gate);
     return PC_OK;
 }
 
@@ -925,18 +971,7 @@ pc_status pc_stack_distance(const uint32_t *prev, const uint32_t *next, uint64_t
     if (n > 0 && (!prev || !next || !dist)) return PC_ERR_INVALID;
     if (!ws) return PC_ERR_WORKSPACE;
     if (ws_bytes < pc_stack_distance_ws(n)) return PC_ERR_WORKSPACE;
-    hipStream_t s = (hipStream_t)stream;
-    const pc::SdPlan p = pc::plan_sd(n);
-    pc::SdWs w = pc::carve_sd(ws, n, p);
-    pc_status st = pc::fill_u32(reinterpret_cast<uint32_t *>(w.hdr), 0u, 1, s);
-    if (st != PC_OK || n == 0) return st;
-    if ((st = pc::sd_cold_prefix(prev, n, w, s)) != PC_OK) return st;
-    uint32_t *lt, *la;
-    if ((st = pc::sd_levels(next, n, p, w, s, &lt, &la)) != PC_OK) return st;
-    const uint64_t nchunks = (n + pc::LOCAL_SPAN - 1) / pc::LOCAL_SPAN;
-    PC_LAUNCH(pc::K_SD_LOCAL, pc::sd_local_kernel, dim3((unsigned)nchunks), dim3(pc::LOC_THREADS), 0, s, lt, la,
-              prev, n, w.Zc, dist);
-    return PC_OK;
+    return pc::stack_distance_gated(prev, next, n, dist, ws, (hipStream_t)stream, nullptr);
 }
 
 size_t pc_request_order_ws(void) { return pc::WS_HEADER; }

@@ -227,8 +227,8 @@ def prev_next_chained(keys: torch.Tensor, blk_off: torch.Tensor, prev: Optional[
                       nxt: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
                       key_hist: Optional[torch.Tensor] = None, deepest_first: bool = False):
     """pc_prev_next_chained: the same prev / next as prev_next_use for keys
-    laid out per request as hash_blocks writes them (synchronises the stream
-    twice)."""
+    laid out per request as hash_blocks writes them; the path is chosen on
+    the device (no synchronisation)."""
     L = lib()
     n = keys.numel()
     n_seqs = blk_off.numel() - 1
@@ -281,7 +281,8 @@ def stack_distance_noalloc_max_n() -> int:
 def stack_distance_runs(prev: torch.Tensor, nxt: torch.Tensor, dist: Optional[torch.Tensor] = None,
                         ws: Optional[torch.Tensor] = None):
     """pc_stack_distance_runs: the same distances as stack_distance, counted
-    over the runs of the prev stream (synchronises the stream once)."""
+    over the runs of the prev stream, or by the dominance count when there
+    are too many runs (chosen on the device; no synchronisation)."""
     L = lib()
     n = prev.numel()
     if dist is None:
