@@ -268,8 +268,12 @@ __global__ __launch_bounds__(SCAN_THREADS) void chain_scan_apply_kernel(const ui
     if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) out[m] = (uint32_t)hdr[HW_UNRESOLVED];
 }
 
-// One wave per slot: the slot's unresolved accesses, in time order, into
-// (key, position, which sides are open), from the stair kernel's lane masks.
+// The unresolved accesses, in time order, into (key, position, which sides
+// are open), from the stair kernel's lane masks.  Most slots have no open
+// lane (a request that continues an earlier one links all its depths but
+// the last few), so a wave first reads 64 slots' masks, offsets and records,
+// one per lane, and then takes only the slots with open lanes, two at a
+// time, one lane per depth.
 __global__ __launch_bounds__(CH_THREADS) void chain_compact_kernel(
     const uint64_t *__restrict__ keys, uint64_t n_slots, const uint4 *__restrict__ rec,
     const uint4 *__restrict__ open, const uint32_t *__restrict__ coff, int deepest,
@@ -280,31 +284,49 @@ __global__ __launch_bounds__(CH_THREADS) void chain_compact_kernel(
     const uint64_t waves = (uint64_t)gridDim.x * (CH_THREADS / WAVE);
     const uint64_t bit = 1ull << lane;
     const uint64_t above = ~((2ull << lane) - 1);   // lanes above this one (none for lane 63)
-    for (uint64_t j0 = ((uint64_t)blockIdx.x * (CH_THREADS / WAVE) + wave_id_uniform()) * CH_BATCH; j0 < n_slots;
-         j0 += waves * CH_BATCH) {
-        Slot q[CH_BATCH];
-        uint64_t mp[CH_BATCH], mx[CH_BATCH];
-        uint32_t base[CH_BATCH];
-#pragma unroll
-        for (int k = 0; k < CH_BATCH; ++k) {
-            const bool in = j0 + k < n_slots;
-            q[k] = in ? load_slot(rec, j0 + k) : Slot{0, 0, NONE};
-            const uint4 o = in ? open[j0 + k] : make_uint4(0u, 0u, 0u, 0u);
-            mp[k] = (uint64_t)o.x | ((uint64_t)o.y << 32);
-            mx[k] = (uint64_t)o.z | ((uint64_t)o.w << 32);
-            base[k] = in ? coff[j0 + k] : 0;
+    for (uint64_t j0 = ((uint64_t)blockIdx.x * (CH_THREADS / WAVE) + wave_id_uniform()) * WAVE; j0 < n_slots;
+         j0 += waves * WAVE) {
+        const uint64_t j = j0 + lane;
+        uint64_t mp = 0, mx = 0, pos = 0;
+        uint32_t base = 0;
+        if (j < n_slots) {
+            const uint4 o = open[j];
+            mp = (uint64_t)o.x | ((uint64_t)o.y << 32);
+            mx = (uint64_t)o.z | ((uint64_t)o.w << 32);
+            if (mp | mx) {
+                pos = load_slot(rec, j).pos;
+                base = coff[j];
+            }
         }
+        uint64_t todo = ballot((mp | mx) != 0);
+        while (todo) {
+            int src[2];
+            src[0] = __builtin_ctzll(todo);
+            todo &= todo - 1;
+            src[1] = todo ? __builtin_ctzll(todo) : -1;
+            if (todo) todo &= todo - 1;
+            uint64_t m[2], p[2], kk[2];
+            uint32_t b[2], f[2];
 #pragma unroll
-        for (int k = 0; k < CH_BATCH; ++k) {
-            const uint64_t m = mp[k] | mx[k];
-            // time order: lanes ascending, or descending in the deepest-first layout
-            const uint32_t rank = deepest ? (uint32_t)__popcll(m & above) : mbcnt(m);
-            if (m & bit) {
-                const uint64_t pr = lane_pos(q[k], lane, deepest);
-                const uint64_t o = (uint64_t)base[k] + rank;
-                ckeys[o] = keys[pr];
-                cpos[o] = (uint32_t)pr;
-                cflag[o] = (uint8_t)((mp[k] & bit ? 1 : 0) | (mx[k] & bit ? 2 : 0));
+            for (int k = 0; k < 2; ++k) {
+                const int L = src[k] < 0 ? src[0] : src[k];
+                const uint64_t a = shfl64(mp, L), x = shfl64(mx, L);
+                m[k] = src[k] < 0 ? 0ull : (a | x);
+                f[k] = (a & bit ? 1u : 0u) | (x & bit ? 2u : 0u);
+                p[k] = deepest ? shfl64(pos, L) - (uint64_t)lane : shfl64(pos, L) + (uint64_t)lane;
+                b[k] = (uint32_t)__shfl((int)base, L, WAVE);
+                kk[k] = (m[k] & bit) ? keys[p[k]] : 0ull;
+            }
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                if (m[k] & bit) {
+                    // time order: lanes ascending, or descending in the deepest-first layout
+                    const uint32_t rank = deepest ? (uint32_t)__popcll(m[k] & above) : mbcnt(m[k]);
+                    const uint64_t o = (uint64_t)b[k] + rank;
+                    ckeys[o] = kk[k];
+                    cpos[o] = (uint32_t)p[k];
+                    cflag[o] = (uint8_t)f[k];
+                }
             }
         }
     }
@@ -539,7 +561,7 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
     carve_open(w.generic, m_cap, &o);
     PC_LAUNCH(K_CHAIN_SCAN, chain_decide_kernel, dim3(1), dim3(64), 0, s, w.hdr, (const int32_t *)w.aws,
               (uint32_t)m_cap);
-    PC_LAUNCH(K_CHAIN_COMPACT, chain_compact_kernel, dim3(wave_grid((ns + CH_BATCH - 1) / CH_BATCH, cus)),
+    PC_LAUNCH(K_CHAIN_COMPACT, chain_compact_kernel, dim3(wave_grid((ns + WAVE - 1) / WAVE, cus)),
               dim3(CH_THREADS), 0, s, keys, ns, (const uint4 *)w.rec, (const uint4 *)w.open, w.coff, deepest,
               o.ckeys, o.cpos, o.cflag, (const int32_t *)w.hdr);
     const uint32_t *m_dev = reinterpret_cast<const uint32_t *>(w.hdr + HW_UNRESOLVED);

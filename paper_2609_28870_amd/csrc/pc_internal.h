@@ -119,6 +119,11 @@ pc_status prev_next_core(const uint64_t *keys, uint64_t n, const uint32_t *n_dev
 
 // ------------------------------------------------------------ device helpers
 __device__ __forceinline__ bool gated_off(const int32_t *gate) { return gate && *gate == 0; }
+__device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
+    const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src, WAVE);
+    const uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(v >> 32), src, WAVE);
+    return (uint64_t)lo | ((uint64_t)hi << 32);
+}
 __device__ __forceinline__ uint64_t dev_count(uint64_t n, const uint32_t *n_dev) {
     if (!n_dev) return n;
     const uint64_t m = *n_dev;

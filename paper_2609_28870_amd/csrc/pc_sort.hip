@@ -323,12 +323,6 @@ __device__ __forceinline__ bool scan_run(const uint64_t *__restrict__ sk, uint64
     return false;
 }
 
-__device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
-    const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src, WAVE);
-    const uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(v >> 32), src, WAVE);
-    return (uint64_t)lo | ((uint64_t)hi << 32);
-}
-
 // Previous (dir = -1) or next (dir = +1) element with the same full key as
 // sorted position i, whose adjacent element shares the low key bits but not
 // the key.  Lanes resolve such requests independently: each scans a few
