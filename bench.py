@@ -23,6 +23,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+AGENT_3E8_SESSIONS = 55000     # agent sessions for a trace of at least 3e8 block accesses (3.19e8)
 P_LIN = 3_000_000_000          # FLOPs per token, linear part (agent cost model)
 
 # algorithmic bytes per element for each kernel (inputs it must read and
@@ -84,22 +85,27 @@ HIP_KERNEL = {"sort_onesweep_pass": "pc::sort_pass_kernel", "link_partition": "p
               "chain_compact": "pc::chain_compact_kernel", "chain_anchor": "pc::chain_anchor_kernel",
               "chain_merge": "pc::chain_merge_kernel", "runs_count": "pc::runs_count_kernel",
               "runs_compact": "pc::runs_compact_kernel", "runs_fill": "pc::runs_fill_kernel"}
-# committed counter summaries, by (mode, prev/next path); a run whose path has
-# none reports no counter traffic
-PROFILES = {("access", "chained"): os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9.md"),
-            ("request", "chained"): os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_request.md"),
-            ("session", "chained"): os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_session.md"),
-            ("profile", "chained"): os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_profile.md"),
-            ("access", "generic"): os.path.join(ROOT, "profiles", "all_kernels_full_mixed_2e9_generic.md")}
-PROFILE = PROFILES[("access", "chained")]
+# committed counter summaries, by (mode, prev/next path, workload, block
+# size, session count); a run with none reports no counter traffic
+PROFILES = {
+    ("access", "chained", "full", 16, None): "all_kernels_full_mixed_2e9.md",
+    ("request", "chained", "full", 16, None): "all_kernels_full_mixed_2e9_request.md",
+    ("session", "chained", "full", 16, None): "all_kernels_full_mixed_2e9_session.md",
+    ("profile", "chained", "full", 16, None): "all_kernels_full_mixed_2e9_profile.md",
+    ("access", "generic", "full", 16, None): "all_kernels_full_mixed_2e9_generic.md",
+    ("access", "chained", "chat", 16, None): "all_kernels_chat_2e8.md",
+    ("access", "chained", "agent", 16, AGENT_3E8_SESSIONS): "all_kernels_agent_3e8.md",
+    ("access", "chained", "agent", 16, None): "all_kernels_agent_B16.md",
+    ("access", "chained", "agent", 64, None): "all_kernels_agent_B64.md",
+    ("access", "chained", "agent", 256, None): "all_kernels_agent_B256.md",
+}
+PROFILE = os.path.join(ROOT, "profiles", PROFILES[("access", "chained", "full", 16, None)])
 
 
-def profile_for(mode, prev_next, workload="full", block_size=16):
-    """The committed summary for this run's kernels, or None: summaries are
-    taken on the full trace at block size 16 only."""
-    if workload != "full" or block_size != 16:
-        return None
-    return PROFILES.get((mode, prev_next))
+def profile_for(mode, prev_next, workload="full", block_size=16, sessions=None):
+    """Path of the committed summary for this run's kernels, or None."""
+    name = PROFILES.get((mode, prev_next, workload, block_size, sessions))
+    return os.path.join(ROOT, "profiles", name) if name else None
 
 
 def source_sha256():
@@ -270,6 +276,9 @@ def cpu_baseline(trace, caps, alpha, beta, budget_accesses, request=False):
 
 
 GOLDEN_FULL = os.path.join(ROOT, "tests", "golden", "fullsize_full.txt")
+# the oracle's full-size references, by (workload, block size, session count)
+GOLDEN = {("full", 16, None): GOLDEN_FULL,
+          ("chat", 16, None): os.path.join(ROOT, "tests", "golden", "fullsize_chat.txt")}
 
 
 def read_fullsize_golden(path):
@@ -337,9 +346,9 @@ def main():
     ap.add_argument("--prev-next", default="chained", choices=["chained", "generic"],
                     help="prev/next from the chain structure of the keys and the stack distance over runs "
                          "(default), or the generic sort and the dominance count over accesses")
-    ap.add_argument("--settle", type=float, default=20.0,
-                    help="seconds to wait before touching the device (memory that another process "
-                         "released just before is reclaimed in the background meanwhile)")
+    ap.add_argument("--settle", type=float, default=0.0,
+                    help="seconds to wait before touching the device (0 by default: a process started "
+                         "right after another one that held most of HBM runs at the same speed)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the hot path here is single-GPU "
@@ -368,7 +377,8 @@ def main():
     request = args.residency == "request"
     session_mode = args.residency == "session"
     global PROFILE
-    PROFILE = profile_for("profile" if args.profile else args.residency, args.prev_next, args.workload, B)
+    PROFILE = profile_for("profile" if args.profile else args.residency, args.prev_next, args.workload, B,
+                          args.sessions)
     if args.profile:
         prof_edges = pc.to_dev_u64(np.array(PROFILE_EDGES_US, np.uint64))
         pipe = pc.Profiler(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
@@ -504,9 +514,9 @@ def main():
         hr, csr = pc.curves(bins["count"], bins["cost"])
     # the last timed step's bins against the oracle's full-size reference
     oracle_check = None
-    if (not args.profile and args.residency == "access" and args.workload == "full" and B == 16
-            and args.sessions is None and os.path.exists(GOLDEN_FULL)):
-        oracle_check = check_against_golden(bins, caps_np, n_blocks, GOLDEN_FULL)
+    golden = GOLDEN.get((args.workload, B, args.sessions))
+    if not args.profile and args.residency == "access" and golden and os.path.exists(golden):
+        oracle_check = check_against_golden(bins, caps_np, n_blocks, golden)
         log("bins match the oracle's full-size reference at all %d capacities" % oracle_check["capacities"])
     cb = None
     sample = args.cpu_sample if args.cpu_sample is not None else (

@@ -98,6 +98,7 @@ constexpr int FUSE_SPAN = 32;               // blocks per request per round
 constexpr int FUSE_ROWS = WAVE / FUSE_SPAN; // requests per sweep
 constexpr int FUSE_ROW = FUSE_SPAN + 1;     // padded LDS row
 constexpr int FUSE_SWEEPS = 4;              // sweeps whose loads are in flight together
+constexpr int HASH_WAVES_PER_CU = 32;       // waves per CU the request count is spread over
 
 __device__ __forceinline__ uint64_t digest16_words(const uint4 (&q)[4]) {
     uint64_t h = 0;
@@ -114,7 +115,7 @@ __global__ __launch_bounds__(FUSE_THREADS) void hash_fused_kernel(
     const uint32_t *__restrict__ tok_len, uint32_t n_seqs, uint32_t B, const uint64_t *__restrict__ parent,
     uint64_t root, const uint64_t *__restrict__ blk_off, uint64_t n_blocks, uint64_t *__restrict__ keys,
     uint32_t *__restrict__ depth, uint32_t *__restrict__ key_hist, uint32_t flags, uint32_t *__restrict__ counter,
-    int32_t *__restrict__ err) {
+    int32_t *__restrict__ err, int lanes) {
     const bool deepest_first = (flags & PC_HASH_DEEPEST_FIRST) != 0;
     __shared__ uint64_t s_tile[FUSE_WAVES][WAVE * FUSE_ROW];
     __shared__ uint32_t s_hist[4 * 256];   // byte histograms of the keys written
@@ -125,7 +126,9 @@ __global__ __launch_bounds__(FUSE_THREADS) void hash_fused_kernel(
     const int grp = lane / FUSE_SPAN;
     const uint32_t jj = (uint32_t)(lane & (FUSE_SPAN - 1));
     uint64_t *tile = s_tile[w];
-    bool done = false, busy = false;
+    // only the first `lanes` lanes take requests (all 64 still hash every
+    // round's blocks)
+    bool done = lane >= lanes, busy = false;
     uint32_t b = 0, nb = 0, fast = 0;
     uint64_t key = 0, out = 0, st = 0;
     while (true) {
@@ -137,8 +140,12 @@ __global__ __launch_bounds__(FUSE_THREADS) void hash_fused_kernel(
             if (lane == leader) base = atomicAdd(counter, (uint32_t)__popcll(needmask));
             base = __shfl(base, leader, WAVE);
             if (need) {
-                const uint32_t r = base + mbcnt(needmask);
-                if (r >= n_seqs) {
+                // requests are taken last to first: contexts grow turn by
+                // turn, so the longest chains start early instead of
+                // finishing the kernel alone
+                const uint32_t taken = base + mbcnt(needmask);
+                const uint32_t r = n_seqs - 1 - taken;
+                if (taken >= n_seqs) {
                     done = true;
                 } else {
                     const uint32_t len = tok_len[r];
@@ -316,14 +323,24 @@ pc_status pc_hash_blocks(const int32_t *tokens, uint64_t n_tokens, const uint64_
     if (st != PC_OK) return st;
 
     const int cus = pc::device_cus();
-    // persistent grid: a few workgroups per CU, requests handed out by a counter
-    uint64_t want = ((uint64_t)n_seqs + pc::FUSE_THREADS - 1) / pc::FUSE_THREADS;
+    // Persistent grid: a few workgroups per CU, requests handed out by a
+    // counter.  A wave's lanes advance their requests in lockstep rounds and
+    // share the round's digest work, so a wave that holds many long requests
+    // (the late turns of one large session arrive together) works for as
+    // long as all of them take.  With few requests per resident wave, fewer
+    // lanes per wave take requests (at least 8): the long ones spread over
+    // more waves and the slowest wave finishes sooner.
+    const uint64_t resident_waves = (uint64_t)cus * pc::HASH_WAVES_PER_CU;
+    uint64_t lanes = ((uint64_t)n_seqs + resident_waves - 1) / resident_waves;
+    lanes = lanes < 8 ? 8 : lanes > (uint64_t)pc::WAVE ? (uint64_t)pc::WAVE : lanes;
+    const uint64_t per_wg = lanes * pc::FUSE_WAVES;
+    uint64_t want = ((uint64_t)n_seqs + per_wg - 1) / per_wg;
     uint64_t cap = (uint64_t)cus * 8;
     unsigned grid = (unsigned)(want < cap ? want : cap);
     if (grid == 0) grid = 1;
     PC_LAUNCH(pc::K_HASH, pc::hash_fused_kernel, dim3(grid), dim3(pc::FUSE_THREADS), 0, s, tokens, n_tokens,
               tok_start, tok_len, n_seqs, block_size, parent, root, blk_off, n_blocks, keys, depth, key_hist,
-              flags, counters, hdr);
+              flags, counters, hdr, (int)lanes);
     return PC_OK;
 }
 

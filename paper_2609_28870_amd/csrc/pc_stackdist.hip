@@ -874,10 +874,17 @@ static SdWs carve_sd(void *ws, uint64_t n, const SdPlan &p) {
     return w;
 }
 
+// Workgroups per CU of the loops over tiles: enough that each takes only a
+// few tiles (one tile per workgroup balances best: a static share of many
+// tiles ran the dominance passes 25% slower), few enough that a launch gated
+// off costs little.
+constexpr int SD_GRID_PER_CU = 64;
+
 // Z at every multiple of 4096 from the cold (prev = none) flags
 static pc_status sd_cold_prefix(const uint32_t *prev, uint64_t n, SdWs &w, hipStream_t s, const int32_t *gate) {
     const uint64_t nchunks = (n + LOCAL_SPAN - 1) / LOCAL_SPAN;
-    PC_LAUNCH(K_SD_COLD, sd_cold_count_kernel, dim3(capped(nchunks, 16)), dim3(256), 0, s, prev, n, w.cold, gate);
+    PC_LAUNCH(K_SD_COLD, sd_cold_count_kernel, dim3(capped(nchunks, SD_GRID_PER_CU)), dim3(256), 0, s, prev, n,
+              w.cold, gate);
     const uint64_t nblocks = (nchunks + SCAN_BLOCK - 1) / SCAN_BLOCK;
     PC_LAUNCH(K_SD_SCAN, sd_scan_reduce_kernel, dim3((unsigned)nblocks), dim3(SCAN_THREADS), 0, s, w.cold, nchunks,
               w.part, gate);
@@ -900,11 +907,12 @@ static pc_status sd_levels(const uint32_t *first, uint64_t n, const SdPlan &p, S
         const uint64_t ntiles = p.grid[i];
         const uint64_t cgroups = (p.grid[i] + COUNT_TPW - 1) / COUNT_TPW;
         const unsigned groups = (unsigned)((p.grid[i] + SEG_GROUP - 1) / SEG_GROUP);
+        const unsigned grid = capped(ntiles, SD_GRID_PER_CU), cgrid = capped(cgroups, SD_GRID_PER_CU);
         const uint64_t fixed = (n + DOM_TILE - 1) / DOM_TILE;
         if (i == 0) {
-            PC_LAUNCH(K_SD_COUNT, sd_count_kernel<true>, dim3(capped(cgroups, 8)), dim3(DOM_THREADS), 0, s, first, n,
-                      w.Zc, p.s[i], p.k[i], (const uint32_t *)nullptr, (uint64_t)1, (const uint32_t *)nullptr, w.cnt,
-                      w.seg, cgroups, gate);
+            PC_LAUNCH(K_SD_COUNT, sd_count_kernel<true>, dim3(cgrid), dim3(DOM_THREADS), 0, s, first, n, w.Zc,
+                      p.s[i], p.k[i], (const uint32_t *)nullptr, (uint64_t)1, (const uint32_t *)nullptr, w.cnt, w.seg,
+                      cgroups, gate);
         } else {
             const uint64_t nb = p.nbuckets[i];
             PC_LAUNCH(K_SD_TILES, sd_tile_count_kernel, dim3((unsigned)((nb + 255) / 256)), dim3(256), 0, s, w.Zc,
@@ -912,8 +920,8 @@ static pc_status sd_levels(const uint32_t *first, uint64_t n, const SdPlan &p, S
             PC_LAUNCH(K_SD_SCAN, sd_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, s, w.tcount, nb, w.tfirst, gate);
             PC_LAUNCH(K_SD_TILES, sd_tile_bucket_kernel, dim3((unsigned)((p.grid[i] + 255) / 256)), dim3(256), 0,
                       s, w.tfirst, nb, p.grid[i], w.tile_bucket, gate);
-            PC_LAUNCH(K_SD_COUNT, sd_count_kernel<false>, dim3(capped(cgroups, 8)), dim3(DOM_THREADS), 0, s, src_t,
-                      n, w.Zc, p.s[i], p.k[i], w.tfirst, nb, w.tile_bucket, w.cnt, w.seg, cgroups, gate);
+            PC_LAUNCH(K_SD_COUNT, sd_count_kernel<false>, dim3(cgrid), dim3(DOM_THREADS), 0, s, src_t, n, w.Zc,
+                      p.s[i], p.k[i], w.tfirst, nb, w.tile_bucket, w.cnt, w.seg, cgroups, gate);
         }
         const uint32_t *tend = i == 0 ? nullptr : w.tfirst + p.nbuckets[i];
         PC_LAUNCH(K_SD_SEG, sd_seg_reduce_kernel, dim3(groups), dim3(DOM_RADIX), 0, s, w.cnt, w.seg, tend, fixed,
@@ -923,13 +931,12 @@ static pc_status sd_levels(const uint32_t *first, uint64_t n, const SdPlan &p, S
         PC_LAUNCH(K_SD_SEG, sd_seg_scan_kernel, dim3(groups), dim3(DOM_RADIX), 0, s, w.cnt, w.seg, tend, fixed,
                   w.gin, w.pre, gate);
         if (i == 0) {
-            PC_LAUNCH(K_SD_PASS, sd_dominance_kernel<true>, dim3(capped(ntiles, 8)), dim3(DOM_THREADS), 0, s, first,
+            PC_LAUNCH(K_SD_PASS, sd_dominance_kernel<true>, dim3(grid), dim3(DOM_THREADS), 0, s, first,
                       (const uint32_t *)nullptr, dt, da, n, w.Zc, p.s[i], p.k[i], (const uint32_t *)nullptr,
                       (uint64_t)1, (const uint32_t *)nullptr, w.pre, w.hdr, ntiles, gate);
         } else {
-            PC_LAUNCH(K_SD_PASS, sd_dominance_kernel<false>, dim3(capped(ntiles, 8)), dim3(DOM_THREADS), 0, s, src_t,
-                      src_a, dt, da, n, w.Zc, p.s[i], p.k[i], w.tfirst, p.nbuckets[i], w.tile_bucket, w.pre, w.hdr,
-                      ntiles, gate);
+            PC_LAUNCH(K_SD_PASS, sd_dominance_kernel<false>, dim3(grid), dim3(DOM_THREADS), 0, s, src_t, src_a, dt,
+                      da, n, w.Zc, p.s[i], p.k[i], w.tfirst, p.nbuckets[i], w.tile_bucket, w.pre, w.hdr, ntiles, gate);
         }
         src_t = dt;
         src_a = da;
@@ -951,8 +958,8 @@ pc_status stack_distance_gated(const uint32_t *prev, const uint32_t *next, uint6
     uint32_t *lt, *la;
     if ((st = sd_levels(next, n, p, w, s, &lt, &la, gate)) != PC_OK) return st;
     const uint64_t nchunks = (n + LOCAL_SPAN - 1) / LOCAL_SPAN;
-    PC_LAUNCH(K_SD_LOCAL, sd_local_kernel, dim3(capped(nchunks, 8)), dim3(LOC_THREADS), 0, s, lt, la, prev, n, w.Zc,
-              dist, gate);
+    PC_LAUNCH(K_SD_LOCAL, sd_local_kernel, dim3(capped(nchunks, SD_GRID_PER_CU)), dim3(LOC_THREADS), 0, s, lt, la,
+              prev, n, w.Zc, dist, gate);
     return PC_OK;
 }
 

@@ -30,26 +30,33 @@ def test_every_timed_kernel_has_algorithmic_bytes():
         assert bench.chain_bytes(name, 1 << 20, 1 << 14, 1 << 17, 1000) > 0, name
 
 
-@pytest.mark.parametrize("mode", ["access", "request", "session", "profile"])
-def test_committed_profiles_parse(mode):
-    path = bench.PROFILES[(mode, "chained")]
+@pytest.mark.parametrize("key", sorted(bench.PROFILES, key=str))
+def test_committed_profiles_parse(key):
+    path = bench.profile_for(*key)
     text = open(path).read()
     blob = json.loads(text[text.index("```json") + 7:text.rindex("```")])
     assert len(blob["source_sha256"]) == 64
     # the copy calibration: FETCH_SIZE counts half of what a copy reads
     assert 1.9 < blob["fetch_scale"] < 2.1 and 0.9 < blob["write_scale"] < 1.1
     ids = {e["id"] for e in blob["kernels"].values()}
-    assert "sort_onesweep_pass" in ids and "hash_blocks" in ids
+    assert "hash_blocks" in ids and ("chain_stair" in ids or "sort_onesweep_pass" in ids)
     for e in blob["kernels"].values():
         assert e["avg_ms"] > 0 and e["launches_per_run"] > 0
         assert e["read_bytes"] >= 0 and e["write_bytes"] >= 0
     # each summary names the commands that made it, from committed files only
     assert "rocprofv3 --kernel-trace --stats" in text and "--pmc FETCH_SIZE" in text
     assert "_work" not in text
+    # the bench arguments of the configuration, in every command
+    for arg in {"generic": ["--prev-next generic"], "chained": []}[key[1]] + \
+            {"request": ["--residency request"], "session": ["--residency session"], "profile": ["--profile"],
+             "access": []}[key[0]] + (["--workload %s" % key[2]] if key[2] != "full" else []) + \
+            (["--block-size %d" % key[3]] if key[3] != 16 else []) + \
+            (["--sessions %d" % key[4]] if key[4] else []):
+        assert text.count(arg) == 3, (key, arg)
 
 
 def test_traffic_only_for_the_sources_it_was_taken_with(monkeypatch, tmp_path):
-    text = open(bench.PROFILES[("access", "chained")]).read()
+    text = open(bench.profile_for("access", "chained")).read()
     blob = json.loads(text[text.index("```json") + 7:text.rindex("```")])
     for sha, want in ((bench.source_sha256(), True), ("0" * 64, False)):
         blob["source_sha256"] = sha
@@ -87,10 +94,14 @@ def test_quantile_and_profile_summary():
     assert s["footprint_top10pct_share"] == 0.7
 
 
-def test_profile_is_chosen_by_mode_and_path(monkeypatch):
-    assert bench.profile_for("access", "chained") == bench.PROFILES[("access", "chained")]
-    assert bench.profile_for("access", "chained", "chat") is None
+def test_profile_is_chosen_by_mode_path_and_workload(monkeypatch):
+    assert bench.profile_for("access", "chained") == bench.PROFILE
+    assert bench.profile_for("access", "chained", "chat").endswith("all_kernels_chat_2e8.md")
+    assert bench.profile_for("access", "chained", "agent", 64).endswith("all_kernels_agent_B64.md")
+    assert bench.profile_for("access", "chained", "agent", 16, bench.AGENT_3E8_SESSIONS).endswith(
+        "all_kernels_agent_3e8.md")
     assert bench.profile_for("access", "chained", "full", 64) is None
+    assert bench.profile_for("access", "chained", "agent", 16, 1234) is None
     # a path without a committed summary reports no counter traffic
     monkeypatch.setattr(bench, "PROFILE", bench.profile_for("request", "generic"))
     assert bench.PROFILE is None
