@@ -340,7 +340,11 @@ def main():
                          "1e6 with --residency request)")
     ap.add_argument("--belady", action="store_true",
                     help="also run Belady's MIN at every capacity in each step (pc_belady on the step's "
-                         "next-use index) and report the LRU-Belady gap at the paper's cache sizes")
+                         "next-use index) and report the LRU-Belady gap at the paper's cache sizes; MIN is "
+                         "sequential per capacity (about 6 s per step on the agent trace), so traces above "
+                         "--belady-max accesses are refused")
+    ap.add_argument("--belady-max", type=float, default=1e8,
+                    help="largest trace (block accesses) --belady runs on")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 4 GiB device copy (for rocprof counter calibration)")
     ap.add_argument("--prev-next", default="chained", choices=["chained", "generic"],
@@ -367,6 +371,10 @@ def main():
     trace = pcgen.make_trace(args.workload, n_sessions=args.sessions, block_size=B)
     caps_np = trace.caps(B)
     n_blocks = trace.n_blocks(B)
+    if args.belady and n_blocks > args.belady_max:
+        raise SystemExit("--belady on %d block accesses: Belady's MIN runs one sequential simulation per "
+                         "capacity (minutes per step at this size); use --workload agent, or raise "
+                         "--belady-max" % n_blocks)
     log("trace %s: %d requests, %d block accesses, %d processed tokens, generated in %.1f s" % (
         args.workload, trace.n_requests, n_blocks, trace.processed_tokens(), time.perf_counter() - t0))
 
@@ -412,6 +420,9 @@ def main():
     t1 = time.perf_counter()
     for i in range(args.steps):
         pipe.run()
+        if args.belady:   # seconds per step: say where the run is
+            torch.cuda.synchronize()
+            log("step %d done" % (i + 1))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t1
     pc.prof_enable(False)
@@ -500,7 +511,8 @@ def main():
     stages = {k: {"ms_per_step": round(v, 3),
                   "algo_GBps": round(stage_bytes[k] * n_blocks / v / 1e6, 1) if k in stage_bytes else None,
                   # counter-measured bytes (committed summary) over this run's time
-                  "measured_GBps": round(measured[k] / v / 1e6, 1) if measured and k in measured else None}
+                  "measured_GBps": (round(measured[k] / v / 1e6, 1) if measured and k in measured
+                                    and k in stage_bytes else None)}
               for k, v in stages.items()}
 
     # request-level bins hold only at capacities that fit the largest request
