@@ -82,6 +82,10 @@ __device__ __forceinline__ uint64_t wave_or64(uint64_t x) {
     return (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)lo, WAVE - 1) |
            ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)hi, WAVE - 1) << 32);
 }
+// inclusive prefix OR of one uint64 per lane
+__device__ __forceinline__ uint64_t wave_incl_or64(uint64_t x) {
+    return (uint64_t)wave_incl_or((uint32_t)x) | ((uint64_t)wave_incl_or((uint32_t)(x >> 32)) << 32);
+}
 // sum of one uint32 per lane, exact (as two 16-bit halves)
 __device__ __forceinline__ uint64_t wave_sum64(uint32_t x) {
     const uint32_t lo = wave_incl_scan(x & 0xFFFFu), hi = wave_incl_scan(x >> 16);
@@ -217,7 +221,7 @@ __device__ __forceinline__ uint32_t clamp32(uint64_t v) { return v > 0xFFFFFFFFu
 __device__ void belady_one(const uint32_t *__restrict__ next, const uint32_t *__restrict__ depth, uint64_t n,
                            uint64_t c64, uint64_t *__restrict__ l0, uint64_t *__restrict__ l1,
                            uint8_t *__restrict__ flags, uint64_t *hits_out, uint64_t *dsum_out, int32_t *err,
-                           uint32_t *s_a, uint32_t *s_b, uint32_t *s_new, uint32_t *s_tmp) {
+                           uint32_t *s_a, uint32_t *s_b, uint32_t *s_new, uint32_t *s_tmp, uint64_t *s_sb) {
     const int lane = threadIdx.x;
     BelState S{s_a, s_b, 0, 0, BEL_INF, 0, false};
     // resident blocks never exceed n, so the capacity is clamped to 32 bits
@@ -324,32 +328,71 @@ __device__ void belady_one(const uint32_t *__restrict__ next, const uint32_t *__
             uint64_t ev = vmask & ~hm;
             for (uint32_t k = size; k < c && ev; ++k) ev &= ev - 1;
             const uint64_t dm = ballot(valid && xv == NONE);
-            uint64_t al = b_lo, ah = b_hi, gl = 0, gh = 0;
-            uint32_t d = dead;
-            bool ok = true;
-            for (int j = 0; j < nb && ok; ++j) {
-                const uint64_t bit = 1ull << j;
-                if (ev & bit) {
-                    if (d) {
-                        --d;
-                    } else {
-                        const uint64_t cl = al & ~gl, ch = ah & ~gh;
-                        if (cl && (uint32_t)__builtin_ctzll(cl) < nhigh) {
-                            gl |= cl & (~cl + 1);
-                        } else if (!cl && ch && 64u + (uint32_t)__builtin_ctzll(ch) < nhigh) {
-                            gh |= ch & (~ch + 1);
-                        } else {
-                            ok = false;
-                        }
-                    }
-                }
-                if (dm & bit) {
-                    ++d;
-                } else if (pmask & bit) {
-                    const uint32_t r = (uint32_t)__builtin_amdgcn_readlane((int)jr, j);
-                    if (r < 64) al |= 1ull << r; else ah |= 1ull << (r - 64);
-                }
+            // (1) Evictions that find no dead block.  With D(j) evictions up to
+            // and including access j and S(j) dead blocks available before it
+            // (a dead insert counts from the next access on), the number left
+            // unserved is the running maximum of D(j) - S(j): the real
+            // evictions are the accesses where that maximum grows.
+            const uint64_t le = lane == WAVE - 1 ? ~0ull : (2ull << lane) - 1;   // lanes up to this one
+            const int64_t gap = (int64_t)__popcll(ev & le) - (int64_t)dead - (int64_t)__popcll(dm & (le >> 1));
+            const uint32_t un = wave_incl_max(gap > 0 ? (uint32_t)gap : 0u);
+            const uint32_t un_prev = (uint32_t)__shfl((int)un, (lane + WAVE - 1) & (WAVE - 1), WAVE);
+            const uint64_t real = ballot(un > (lane ? un_prev : 0u));
+            const uint32_t E = (uint32_t)__popcll(real);
+            // (2) Which candidates the real evictions take.  Each takes the
+            // largest one present (the lowest joint rank); the buffer's are
+            // present from the start, a pending one after its own access.  For
+            // a joint rank k let R(k) be the number of evictions that take a
+            // candidate ranked below k.  With A(k) buffer candidates below k,
+            // and r_i the count after the i-th eviction, r_i = min(r_{i-1} + 1,
+            // A(k) + P_i(k)) where P_i(k) counts the pending candidates below k
+            // inserted before it, hence R(k) = min(E, A(k) + E + m(k)) with
+            // m(k) the lowest prefix sum (from 0) of the sequence "-1 per
+            // eviction, then +1 per such insert", access by access.  The
+            // candidate of rank k is taken iff R(k + 1) > R(k).
+            s_sb[lane] = 0;
+            s_sb[lane + WAVE] = 0;
+            __syncthreads();
+            if (pend) s_sb[jr] = 1ull << lane;   // jr < 128: rank < 64, plus at most 64 buffer values
+            __syncthreads();
+            const uint64_t i0 = wave_incl_or64(s_sb[lane]), i1 = wave_incl_or64(s_sb[lane + WAVE]);
+            const uint64_t tot0 = readlane64(i0, WAVE - 1), tot1 = readlane64(i1, WAVE - 1);
+            // (the shuffles run on every lane: a lane that is off reads as 0)
+            const int prev_lane = (lane + WAVE - 1) & (WAVE - 1);
+            const uint64_t sh0 = shfl64(i0, prev_lane), sh1 = shfl64(i1, prev_lane);
+            const uint64_t below0 = lane ? sh0 : 0ull;            // access bits of pending ranks < lane
+            const uint64_t below1 = tot0 | (lane ? sh1 : 0ull);   // ranks < lane + 64
+            const uint64_t below2 = tot0 | tot1;                  // ranks < 128
+            const uint64_t lt = (1ull << lane) - 1;
+            const int a0 = __popcll(b_lo & lt), a1 = __popcll(b_lo) + __popcll(b_hi & lt);
+            const int a2 = __popcll(b_lo) + __popcll(b_hi);
+            int r0 = 0, r1 = 0, r2 = 0, m0 = 0, m1 = 0, m2 = 0;
+#pragma unroll
+            for (int j = 0; j < WAVE; ++j) {
+                const int pj = (int)((real >> j) & 1);
+                r0 -= pj;
+                r1 -= pj;
+                r2 -= pj;
+                m0 = r0 < m0 ? r0 : m0;
+                m1 = r1 < m1 ? r1 : m1;
+                m2 = r2 < m2 ? r2 : m2;
+                r0 += (int)((below0 >> j) & 1);
+                r1 += (int)((below1 >> j) & 1);
+                r2 += (int)((below2 >> j) & 1);
             }
+            const int Ei = (int)E;
+            const int R0 = a0 + Ei + m0 < Ei ? a0 + Ei + m0 : Ei;   // R(lane)
+            const int R1 = a1 + Ei + m1 < Ei ? a1 + Ei + m1 : Ei;   // R(lane + 64)
+            const int R2 = a2 + Ei + m2 < Ei ? a2 + Ei + m2 : Ei;   // R(128)
+            const int Rn = nhigh < (uint32_t)WAVE ? __builtin_amdgcn_readlane(R0, (int)nhigh)
+                           : nhigh < 2u * WAVE ? __builtin_amdgcn_readlane(R1, (int)nhigh - WAVE) : R2;
+            const int nxt_lane = (lane + 1) & (WAVE - 1);
+            const int R0n = __shfl(R0, nxt_lane, WAVE), R1n = __shfl(R1, nxt_lane, WAVE);
+            const int R0up = lane < WAVE - 1 ? R0n : __builtin_amdgcn_readlane(R1, 0);   // R(lane + 1)
+            const int R1up = lane < WAVE - 1 ? R1n : R2;                                  // R(lane + 65)
+            const uint64_t gl = ballot(R0up > R0), gh = ballot(R1up > R1);
+            const bool ok = Rn == Ei;
+            const uint32_t d = dead + (uint32_t)__popcll(dm) - ((uint32_t)__popcll(ev) - E);
             uint64_t gone = 0;   // by pending rank
             if (ok) {
                 dead = d;
@@ -496,6 +539,7 @@ __global__ __launch_bounds__(WAVE) void belady_kernel(const uint32_t *__restrict
                                                       uint8_t *__restrict__ flags, int32_t *__restrict__ err) {
     __shared__ uint32_t s_a[BEL_BUF], s_b[BEL_BUF], s_new[WAVE];
     __shared__ __align__(16) uint32_t s_tmp[WAVE];
+    __shared__ uint64_t s_sb[2 * WAVE];
     const uint32_t k = blockIdx.x;
     const uint64_t c = caps[k];
     uint8_t *fl = flags ? flags + (uint64_t)k * n : nullptr;
@@ -509,7 +553,7 @@ __global__ __launch_bounds__(WAVE) void belady_kernel(const uint32_t *__restrict
         return;
     }
     belady_one(next, depth, n, c, l0s + (uint64_t)k * w0, l1s + (uint64_t)k * w1, fl, hits + k, dsum + k, err, s_a,
-               s_b, s_new, s_tmp);
+               s_b, s_new, s_tmp, s_sb);
 }
 
 // bitmap words per capacity: one bit per position plus a word of slack, and

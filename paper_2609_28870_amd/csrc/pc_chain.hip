@@ -313,7 +313,8 @@ __global__ __launch_bounds__(CH_THREADS) void chain_compact_kernel(
                 const uint64_t a = shfl64(mp, L), x = shfl64(mx, L);
                 m[k] = src[k] < 0 ? 0ull : (a | x);
                 f[k] = (a & bit ? 1u : 0u) | (x & bit ? 2u : 0u);
-                p[k] = deepest ? shfl64(pos, L) - (uint64_t)lane : shfl64(pos, L) + (uint64_t)lane;
+                const uint64_t ps = shfl64(pos, L);
+                p[k] = deepest ? ps - (uint64_t)lane : ps + (uint64_t)lane;
                 b[k] = (uint32_t)__shfl((int)base, L, WAVE);
                 kk[k] = (m[k] & bit) ? keys[p[k]] : 0ull;
             }
