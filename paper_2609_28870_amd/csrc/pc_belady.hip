@@ -366,23 +366,40 @@ __device__ void belady_one(const uint32_t *__restrict__ next, const uint32_t *__
             const uint64_t lt = (1ull << lane) - 1;
             const int a0 = __popcll(b_lo & lt), a1 = __popcll(b_lo) + __popcll(b_hi & lt);
             const int a2 = __popcll(b_lo) + __popcll(b_hi);
-            int r0 = 0, r1 = 0, r2 = 0, m0 = 0, m1 = 0, m2 = 0;
+            // ranks 64 and up exist only when there are more than 64 candidates
+            const bool wide = nbt + np > (uint32_t)WAVE;
+            int r0 = 0, r2 = 0, m0 = 0, m2 = 0;
+            int r1 = 0, m1 = 0;
+            if (wide) {
 #pragma unroll
-            for (int j = 0; j < WAVE; ++j) {
-                const int pj = (int)((real >> j) & 1);
-                r0 -= pj;
-                r1 -= pj;
-                r2 -= pj;
-                m0 = r0 < m0 ? r0 : m0;
-                m1 = r1 < m1 ? r1 : m1;
-                m2 = r2 < m2 ? r2 : m2;
-                r0 += (int)((below0 >> j) & 1);
-                r1 += (int)((below1 >> j) & 1);
-                r2 += (int)((below2 >> j) & 1);
+                for (int j = 0; j < WAVE; ++j) {
+                    const int pj = (int)((real >> j) & 1);
+                    r0 -= pj;
+                    r1 -= pj;
+                    r2 -= pj;
+                    m0 = r0 < m0 ? r0 : m0;
+                    m1 = r1 < m1 ? r1 : m1;
+                    m2 = r2 < m2 ? r2 : m2;
+                    r0 += (int)((below0 >> j) & 1);
+                    r1 += (int)((below1 >> j) & 1);
+                    r2 += (int)((below2 >> j) & 1);
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < WAVE; ++j) {
+                    const int pj = (int)((real >> j) & 1);
+                    r0 -= pj;
+                    r2 -= pj;
+                    m0 = r0 < m0 ? r0 : m0;
+                    m2 = r2 < m2 ? r2 : m2;
+                    r0 += (int)((below0 >> j) & 1);
+                    r2 += (int)((below2 >> j) & 1);
+                }
+                m1 = m2;   // every rank from 64 on counts all candidates
             }
             const int Ei = (int)E;
             const int R0 = a0 + Ei + m0 < Ei ? a0 + Ei + m0 : Ei;   // R(lane)
-            const int R1 = a1 + Ei + m1 < Ei ? a1 + Ei + m1 : Ei;   // R(lane + 64)
+            const int R1 = a1 + Ei + m1 < Ei ? a1 + Ei + m1 : Ei;   // R(lane + 64) (= R(128) when not wide)
             const int R2 = a2 + Ei + m2 < Ei ? a2 + Ei + m2 : Ei;   // R(128)
             const int Rn = nhigh < (uint32_t)WAVE ? __builtin_amdgcn_readlane(R0, (int)nhigh)
                            : nhigh < 2u * WAVE ? __builtin_amdgcn_readlane(R1, (int)nhigh - WAVE) : R2;
