@@ -415,8 +415,10 @@ pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uin
  *             linear cost of pc_mrc_weighted: saved = alpha*hits + beta*depthsum)
  *   hit_flags uint8[n_caps * n] out or NULL: hit_flags[k*n + t] = 1 when
  *             access t hits at caps[k]
- * One wave simulates one capacity through the whole trace: the call takes
- * time linear in n (about 1 s per 2.8e7 accesses), not one memory pass.
+ * One wave simulates one capacity through the whole trace, all capacities
+ * at once: the call takes time linear in n, not one memory pass (on MI355X
+ * about 1 s per 2.8e7 accesses for a capacity that rarely evicts, up to
+ * 2.5 s for one that evicts on most accesses).
  * Workspace: about n_caps * n / 8 bytes of bitmaps.  Status 5 reports an
  * internal consistency check (not expected for a valid next[]).
  * ------------------------------------------------------------------------ */

@@ -515,7 +515,7 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
 
     // the generic prev/next over all keys, gated on `gate` (nullptr: always)
     auto generic = [&](const int32_t *gate) -> pc_status {
-        pc_status g = prev_next_core(keys, n, nullptr, prev, next, key_hist, w.generic, s, gate);
+        pc_status g = prev_next_core(keys, n, nullptr, prev, next, key_hist, w.generic, s, gate, gate != nullptr);
         if (g != PC_OK) return g;
         PC_LAUNCH(K_FILL32, chain_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)w.generic, w.hdr,
                   HW_HIGH_ANCHOR, HW_PATH);
@@ -539,7 +539,8 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
     PC_LAUNCH(K_CHAIN_ANCHOR, chain_open_kernel, dim3(1), dim3(64), 0, s, w.hdr);
     PC_LAUNCH(K_CHAIN_ANCHOR, chain_anchor_kernel, dim3(wave_grid(n_seqs, cus)), dim3(CH_THREADS), 0, s, keys,
               blk_off, n_seqs, ns, deepest, w.akeys, w.rec, (const int32_t *)w.hdr);
-    if ((st = prev_next_core(w.akeys, ns, nullptr, w.aprev, w.anext, nullptr, w.aws, s, chain)) != PC_OK) return st;
+    if ((st = prev_next_core(w.akeys, ns, nullptr, w.aprev, w.anext, nullptr, w.aws, s, chain, false)) != PC_OK)
+        return st;
     PC_LAUNCH(K_FILL32, chain_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)w.aws, w.hdr, HW_HIGH_ANCHOR,
               HW_CHAIN);
     if ((st = fill_u32_gated(reinterpret_cast<uint32_t *>(w.claimed), 0u, 2 * ns, s, chain)) != PC_OK) return st;
@@ -566,7 +567,8 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
               dim3(CH_THREADS), 0, s, keys, ns, (const uint4 *)w.rec, (const uint4 *)w.open, w.coff, deepest,
               o.ckeys, o.cpos, o.cflag, (const int32_t *)w.hdr);
     const uint32_t *m_dev = reinterpret_cast<const uint32_t *>(w.hdr + HW_UNRESOLVED);
-    if ((st = prev_next_core(o.ckeys, m_cap, m_dev, o.cprev, o.cnext, nullptr, o.ws, s, chain)) != PC_OK) return st;
+    if ((st = prev_next_core(o.ckeys, m_cap, m_dev, o.cprev, o.cnext, nullptr, o.ws, s, chain, false)) != PC_OK)
+        return st;
     PC_LAUNCH(K_FILL32, chain_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)o.ws, w.hdr,
               HW_HIGH_UNRESOLVED, HW_CHAIN);
     uint64_t mg = (m_cap + CH_THREADS - 1) / CH_THREADS;

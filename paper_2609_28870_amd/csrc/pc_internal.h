@@ -113,9 +113,10 @@ pc_status stack_distance_gated(const uint32_t *prev, const uint32_t *next, uint6
 
 // pc_prev_next_use over min(n, *n_dev) keys (n_dev: a count the GPU wrote;
 // nullptr: n), grids and workspace sized for n (pc_prev_next_use_ws(n)),
-// every launch gated
+// every launch gated; `rare`: a call whose gate is seldom on takes small
+// persistent grids (cheap when off, slower when on)
 pc_status prev_next_core(const uint64_t *keys, uint64_t n, const uint32_t *n_dev, uint32_t *prev, uint32_t *next,
-                         const uint32_t *key_hist, void *ws, hipStream_t s, const int32_t *gate);
+                         const uint32_t *key_hist, void *ws, hipStream_t s, const int32_t *gate, bool rare);
 
 // ------------------------------------------------------------ device helpers
 __device__ __forceinline__ bool gated_off(const int32_t *gate) { return gate && *gate == 0; }

@@ -93,39 +93,37 @@ __global__ __launch_bounds__(RADIX) void sort_scan_kernel(const uint32_t *__rest
     }
 }
 
-__global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_kernel(
-    const uint64_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
-    uint64_t *__restrict__ keys_out, uint32_t *__restrict__ vals_out, uint64_t n, int shift,
-    const uint32_t *__restrict__ start, uint64_t *__restrict__ status, uint32_t *__restrict__ counter,
-    uint32_t epoch, int32_t *__restrict__ err, const int32_t *__restrict__ only_if,
-    const uint32_t *__restrict__ n_dev, const int32_t *__restrict__ gate) {
-    // passes over the high key bits run only when the link step needs them
-    if ((only_if && *only_if == 0) || gated_off(gate)) return;
-    n = dev_count(n, n_dev);
-    // Large tiles make each digit's run in the output long (about 32
-    // elements of 8192), so the scattered writes are mostly whole lines; the
-    // tile is staged twice through one buffer (keys, then values) and the
-    // per-wave digit counters are 16-bit (a tile holds at most 8192
-    // elements), which keeps two workgroups on a CU
-    __shared__ uint64_t s_stage[SORT_TILE];
-    __shared__ uint16_t s_wcnt[SORT_WAVES][RADIX];
-    __shared__ uint32_t s_lstart[RADIX];
-    __shared__ uint32_t s_gbase[RADIX];
-    __shared__ uint32_t s_tmp[SORT_WAVES];
-    __shared__ uint32_t s_tile;
+// Large tiles make each digit's run in the output long (about 32 elements
+// of 8192), so the scattered writes are mostly whole lines; the tile is
+// staged twice through one buffer (keys, then values) and the per-wave digit
+// counters are 16-bit (a tile holds at most 8192 elements), which keeps two
+// workgroups on a CU
+struct SortLds {
+    uint64_t stage[SORT_TILE];
+    uint16_t wcnt[SORT_WAVES][RADIX];
+    uint32_t lstart[RADIX];
+    uint32_t gbase[RADIX];
+    uint32_t tmp[SORT_WAVES];
+    uint32_t tile;
+};
 
+// One tile of a pass: the workgroup takes the next tile from the counter
+// (tiles are handed out in order, so every tile a look-back waits on belongs
+// to a workgroup already running it); false when none is left.
+__device__ __forceinline__ bool sort_tile(SortLds &L, const uint64_t *__restrict__ keys_in,
+                                          const uint32_t *__restrict__ vals_in, uint64_t *__restrict__ keys_out,
+                                          uint32_t *__restrict__ vals_out, uint64_t n, int shift,
+                                          const uint32_t *__restrict__ start, uint64_t *__restrict__ status,
+                                          uint32_t *__restrict__ counter, uint32_t epoch, int32_t *__restrict__ err) {
     const int tid = threadIdx.x;
     const int lane = tid & (WAVE - 1);
     const int w = tid / WAVE;
-    // Workgroups past the tile count take no tile (the counter then hands
-    // out exactly the tiles there are) and leave at once: a grid sized for a
-    // bound well above a device count costs little.
-    if ((uint64_t)blockIdx.x * SORT_TILE >= n) return;
-    if (tid == 0) s_tile = atomicAdd(counter, 1u);
-    for (int i = tid; i < SORT_WAVES * RADIX / 2; i += SORT_THREADS) reinterpret_cast<uint32_t *>(&s_wcnt[0][0])[i] = 0;
+    if (tid == 0) L.tile = atomicAdd(counter, 1u);
+    for (int i = tid; i < SORT_WAVES * RADIX / 2; i += SORT_THREADS) reinterpret_cast<uint32_t *>(&L.wcnt[0][0])[i] = 0;
     __syncthreads();
-    const uint32_t tile = s_tile;
+    const uint32_t tile = L.tile;
     const uint64_t base = (uint64_t)tile * SORT_TILE;
+    if (base >= n) return false;
 
     uint64_t k[SORT_ITEMS];
     uint32_t v[SORT_ITEMS];
@@ -146,29 +144,29 @@ __global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_kernel(
         const uint64_t m = match_digit<8>(d, ballot(ok[j]));
         const uint32_t before = mbcnt(m);
         uint32_t cur = 0;
-        if (ok[j]) cur = s_wcnt[w][d];
+        if (ok[j]) cur = L.wcnt[w][d];
         pos[j] = cur + before;
-        if (ok[j] && before == 0) s_wcnt[w][d] = (uint16_t)(cur + (uint32_t)__popcll(m));
+        if (ok[j] && before == 0) L.wcnt[w][d] = (uint16_t)(cur + (uint32_t)__popcll(m));
     }
     __syncthreads();
     uint32_t cnt = 0;
     if (tid < RADIX) {
         for (int x = 0; x < SORT_WAVES; ++x) {
-            const uint32_t c = s_wcnt[x][tid];
-            s_wcnt[x][tid] = (uint16_t)cnt;
+            const uint32_t c = L.wcnt[x][tid];
+            L.wcnt[x][tid] = (uint16_t)cnt;
             cnt += c;
         }
     }
     uint32_t total;
-    const uint32_t lst = block_excl_scan(tid < RADIX ? cnt : 0u, s_tmp, &total);
-    if (tid < RADIX) s_lstart[tid] = lst;
+    const uint32_t lst = block_excl_scan(tid < RADIX ? cnt : 0u, L.tmp, &total);
+    if (tid < RADIX) L.lstart[tid] = lst;
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < SORT_ITEMS; ++j) {
         if (ok[j]) {
             const uint32_t d = (uint32_t)(k[j] >> shift) & 0xFF;
-            pos[j] += s_lstart[d] + s_wcnt[w][d];
-            s_stage[pos[j]] = k[j];
+            pos[j] += L.lstart[d] + L.wcnt[w][d];
+            L.stage[pos[j]] = k[j];
         }
     }
     // decoupled look-back over the per-digit counts of earlier tiles
@@ -198,7 +196,7 @@ __global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_kernel(
             }
             st_status64(mine, ep | FLAG_INC | (uint32_t)(excl + cnt));
         }
-        s_gbase[tid] = start[tid] + excl - lst;
+        L.gbase[tid] = start[tid] + excl - lst;
         // the last tile holds every digit's total: it must fill the digit's
         // range exactly (a caller's histogram that does not match the keys)
         if ((uint64_t)(tile + 1) * SORT_TILE >= n) {
@@ -217,13 +215,13 @@ __global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_kernel(
         const uint32_t i = (uint32_t)(tid + r * SORT_THREADS);
         dst[r] = NONE;
         if (i < n_tile) {
-            const uint64_t kk = s_stage[i];
-            dst[r] = s_gbase[(uint32_t)(kk >> shift) & 0xFF] + i;
+            const uint64_t kk = L.stage[i];
+            dst[r] = L.gbase[(uint32_t)(kk >> shift) & 0xFF] + i;
             if (dst[r] < n) keys_out[dst[r]] = kk;
         }
     }
     __syncthreads();
-    uint32_t *s_val = reinterpret_cast<uint32_t *>(s_stage);
+    uint32_t *s_val = reinterpret_cast<uint32_t *>(L.stage);
 #pragma unroll
     for (int j = 0; j < SORT_ITEMS; ++j)
         if (ok[j]) s_val[pos[j]] = v[j];
@@ -233,6 +231,43 @@ __global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_kernel(
         const uint32_t i = (uint32_t)(tid + r * SORT_THREADS);
         if (i < n_tile && dst[r] < n) vals_out[dst[r]] = s_val[i];
     }
+    return true;
+}
+
+__global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_kernel(
+    const uint64_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
+    uint64_t *__restrict__ keys_out, uint32_t *__restrict__ vals_out, uint64_t n, int shift,
+    const uint32_t *__restrict__ start, uint64_t *__restrict__ status, uint32_t *__restrict__ counter,
+    uint32_t epoch, int32_t *__restrict__ err, const int32_t *__restrict__ only_if,
+    const uint32_t *__restrict__ n_dev, const int32_t *__restrict__ gate) {
+    // passes over the high key bits run only when the link step needs them
+    if ((only_if && *only_if == 0) || gated_off(gate)) return;
+    n = dev_count(n, n_dev);
+    // Workgroups past the tile count take no tile (the counter then hands
+    // out exactly the tiles there are) and leave at once: a grid sized for a
+    // bound well above a device count costs little.
+    if ((uint64_t)blockIdx.x * SORT_TILE >= n) return;
+    __shared__ SortLds L;
+    sort_tile(L, keys_in, vals_in, keys_out, vals_out, n, shift, start, status, counter, epoch, err);
+}
+
+// The same pass from a small persistent grid (each workgroup takes tiles
+// until none are left), for launches that seldom do work: gated off, such a
+// launch costs a few hundred workgroups instead of one per tile.  When it
+// does run it is slower (11.0 against 7.5 ms for four passes over 2.1e9
+// keys), since one tile per workgroup overlaps one tile's tail with the next
+// one's loads.
+__global__ __launch_bounds__(SORT_THREADS, 4) void sort_pass_persistent_kernel(
+    const uint64_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
+    uint64_t *__restrict__ keys_out, uint32_t *__restrict__ vals_out, uint64_t n, int shift,
+    const uint32_t *__restrict__ start, uint64_t *__restrict__ status, uint32_t *__restrict__ counter,
+    uint32_t epoch, int32_t *__restrict__ err, const int32_t *__restrict__ only_if,
+    const uint32_t *__restrict__ n_dev, const int32_t *__restrict__ gate) {
+    if ((only_if && *only_if == 0) || gated_off(gate)) return;
+    n = dev_count(n, n_dev);
+    __shared__ SortLds L;
+    while (sort_tile(L, keys_in, vals_in, keys_out, vals_out, n, shift, start, status, counter, epoch, err))
+        __syncthreads();   // the tile has left the LDS before the next one comes in
 }
 
 // ---- links, and the way back to time order -------------------------------
@@ -710,28 +745,30 @@ __global__ __launch_bounds__(LOCAL_THREADS) void perm_local_kernel(const uint32_
     __shared__ uint64_t s_pn[SPAN];
     if (gated_off(gate)) return;
     n = dev_count(n, n_dev);
-    const uint64_t r0 = (uint64_t)blockIdx.x * SPAN;
-    if (r0 >= n) return;
-    const uint32_t cnt = n - r0 < SPAN ? (uint32_t)(n - r0) : SPAN;
-    const uint32_t *tb = in_t + r0;
-    const uint64_t *pb = in_pn + r0;
-    uint32_t tt[PER];
-    uint64_t v[PER];
+    // one range per workgroup, or several from a capped grid
+    for (uint64_t r0 = (uint64_t)blockIdx.x * SPAN; r0 < n; r0 += (uint64_t)gridDim.x * SPAN) {
+        const uint32_t cnt = n - r0 < SPAN ? (uint32_t)(n - r0) : SPAN;
+        const uint32_t *tb = in_t + r0;
+        const uint64_t *pb = in_pn + r0;
+        uint32_t tt[PER];
+        uint64_t v[PER];
 #pragma unroll
-    for (int q = 0; q < PER; ++q) {
-        const uint32_t j = threadIdx.x + q * LOCAL_THREADS;
-        const uint32_t jc = j < cnt ? j : 0u;
-        tt[q] = tb[jc];
-        v[q] = pb[jc];
-    }
+        for (int q = 0; q < PER; ++q) {
+            const uint32_t j = threadIdx.x + q * LOCAL_THREADS;
+            const uint32_t jc = j < cnt ? j : 0u;
+            tt[q] = tb[jc];
+            v[q] = pb[jc];
+        }
 #pragma unroll
-    for (int q = 0; q < PER; ++q)
-        if (threadIdx.x + q * LOCAL_THREADS < cnt) s_pn[(uint32_t)(tt[q] - r0) & (SPAN - 1)] = v[q];
-    __syncthreads();
-    for (uint32_t j = threadIdx.x; j < cnt; j += LOCAL_THREADS) {
-        const uint64_t x = s_pn[j];
-        prev[r0 + j] = (uint32_t)x;
-        next[r0 + j] = (uint32_t)(x >> 32);
+        for (int q = 0; q < PER; ++q)
+            if (threadIdx.x + q * LOCAL_THREADS < cnt) s_pn[(uint32_t)(tt[q] - r0) & (SPAN - 1)] = v[q];
+        __syncthreads();
+        for (uint32_t j = threadIdx.x; j < cnt; j += LOCAL_THREADS) {
+            const uint64_t x = s_pn[j];
+            prev[r0 + j] = (uint32_t)x;
+            next[r0 + j] = (uint32_t)(x >> 32);
+        }
+        __syncthreads();   // the range has left the LDS before the next one comes in
     }
 }
 
@@ -806,7 +843,7 @@ static SortWs carve_sort(void *ws, uint64_t n) {
 
 
 pc_status prev_next_core(const uint64_t *keys, uint64_t n, const uint32_t *n_dev, uint32_t *prev, uint32_t *next,
-                         const uint32_t *key_hist, void *ws, hipStream_t s, const int32_t *gate) {
+                         const uint32_t *key_hist, void *ws, hipStream_t s, const int32_t *gate, bool rare) {
     SortWs w = carve_sort(ws, n);
     pc_status st = fill_u32_gated(reinterpret_cast<uint32_t *>(w.hdr), 0u, 1, s, gate);
     if (st != PC_OK || n == 0) return st;
@@ -861,9 +898,17 @@ pc_status prev_next_core(const uint64_t *keys, uint64_t n, const uint32_t *n_dev
         }
         uint64_t *kout = (p & 1) ? w.k2 : w.k1;
         uint32_t *vout = (p & 1) ? w.v2 : w.v1;
-        PC_LAUNCH(K_SORT_PASS, sort_pass_kernel, dim3((unsigned)tiles), dim3(SORT_THREADS), 0, s, kin, vin, kout,
-                  vout, n, 8 * p, w.start + p * RADIX, w.status, w.counters + p, (uint32_t)(p + 1), w.hdr,
-                  p >= SORT_PASSES / 2 ? (const int32_t *)need_high : nullptr, n_dev, gate);
+        // the passes over the high bits, and every pass of a call that
+        // seldom runs, take the persistent grid
+        const int32_t *high = p >= SORT_PASSES / 2 ? (const int32_t *)need_high : nullptr;
+        if (high || rare)
+            PC_LAUNCH(K_SORT_PASS, sort_pass_persistent_kernel, dim3(capped(tiles, 2)), dim3(SORT_THREADS), 0, s,
+                      kin, vin, kout, vout, n, 8 * p, w.start + p * RADIX, w.status, w.counters + p,
+                      (uint32_t)(p + 1), w.hdr, high, n_dev, gate);
+        else
+            PC_LAUNCH(K_SORT_PASS, sort_pass_kernel, dim3((unsigned)tiles), dim3(SORT_THREADS), 0, s, kin, vin,
+                      kout, vout, n, 8 * p, w.start + p * RADIX, w.status, w.counters + p, (uint32_t)(p + 1),
+                      w.hdr, high, n_dev, gate);
         kin = kout;
         vin = vout;
     }
@@ -881,8 +926,9 @@ pc_status prev_next_core(const uint64_t *keys, uint64_t n, const uint32_t *n_dev
         cur = nxt;
     }
     const uint64_t span = 1ull << PERM_LOCAL_BITS;
-    PC_LAUNCH(K_PERM_LOCAL, perm_local_kernel, dim3((unsigned)((n + span - 1) / span)), dim3(LOCAL_THREADS), 0, s,
-              bt[cur], bpn[cur], n, prev, next, n_dev, gate);
+    const uint64_t ranges = (n + span - 1) / span;
+    PC_LAUNCH(K_PERM_LOCAL, perm_local_kernel, dim3(rare ? capped(ranges, 1) : (unsigned)ranges), dim3(LOCAL_THREADS),
+              0, s, bt[cur], bpn[cur], n, prev, next, n_dev, gate);
     return PC_OK;
 }
 
@@ -898,7 +944,7 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
     if (n > 0 && (!keys || !prev || !next)) return PC_ERR_INVALID;
     if (!ws) return PC_ERR_WORKSPACE;
     if (ws_bytes < pc_prev_next_use_ws(n)) return PC_ERR_WORKSPACE;
-    return pc::prev_next_core(keys, n, nullptr, prev, next, key_hist, ws, (hipStream_t)stream, nullptr);
+    return pc::prev_next_core(keys, n, nullptr, prev, next, key_hist, ws, (hipStream_t)stream, nullptr, false);
 }
 
 }  // extern "C"
