@@ -78,7 +78,7 @@ def log(*a):
 HIP_KERNEL = {"sort_onesweep_pass": "pc::sort_pass_kernel", "link_partition": "pc::link_partition_kernel",
               "perm_partition": "pc::perm_partition_kernel", "hash_blocks": "pc::hash_fused_kernel",
               "sd_local_finish": "pc::sd_local_kernel",
-              "perm_local": "pc::perm_local_kernel", "mrc_hist": "pc::mrc_hist_kernel",
+              "perm_local": "pc::perm_local_kernel", "mrc_hist": "pc::mrc_hist_kernel<false>",
               "request_distance": "pc::req_dist_kernel",
               "session_distance": "pc::sess_dist_kernel", "reuse_profile_walk": "pc::prof_walk_kernel",
               "reuse_profile_pack": "pc::prof_pack_kernel", "chain_stair": "pc::chain_stair_kernel",

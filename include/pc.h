@@ -48,7 +48,7 @@ typedef enum {
 } pc_status;
 
 #define PC_NONE 0xFFFFFFFFu
-#define PC_MAX_CAPS 1024u
+#define PC_MAX_CAPS 4096u
 #define PC_HASH_DEEPEST_FIRST 1u   /* pc_hash_blocks flag */
 #define PC_MAX_PROFILE_EDGES 128u  /* time-histogram edges of the profiles */
 #define PC_MAX_FREQ 2048u          /* largest exact frequency / request-count bin */
@@ -386,7 +386,8 @@ pc_status pc_session_profile(const uint64_t *blk_off, const uint32_t *session, c
  *   count, depthsum, cost_lo, cost_hi: uint64[n_caps+1] outputs (required)
  *   nextuse_hist: uint64[n_caps+1] output, required when next != NULL; when
  *          given it is always zeroed (and stays zero when next is NULL)
- * Outputs are zeroed on `stream` first, then accumulated.
+ * Outputs are zeroed on `stream` first, then accumulated.  One pass over the
+ * inputs counts up to 1024 edges; more edges take one more pass per 1024.
  * ------------------------------------------------------------------------ */
 size_t pc_mrc_weighted_ws(uint64_t n, uint32_t n_caps);
 pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uint32_t *next,

@@ -7,14 +7,18 @@
 // cost(t) = alpha + beta * depth[t].  Because LRU hits at capacity c exactly
 // when D < c, binning D on the capacity edges gives every capacity at once.
 //
-// GPU mapping: each thread takes 16 consecutive accesses (64-byte vector
-// loads of dist / depth / next), finds each one's bin by an upper-bound
-// search of the edges held in LDS (trying the previous access's bin first)
-// and accumulates runs of equal bins in registers, so one LDS atomic covers a
-// run; each workgroup then adds its non-zero LDS bins to the outputs with
-// global 64-bit atomics.  Integer
-// atomics make the result independent of scheduling order.  A last tiny
-// kernel forms alpha*count + beta*depthsum exactly as 128-bit integers.
+// GPU mapping: each thread takes 8 consecutive accesses (32-byte vector
+// loads of dist / depth / next) and keeps the value range of the bin it is
+// filling in registers, so an access that stays in that bin (neighbouring
+// accesses of one request usually do) costs two compares; any other value
+// finds its bin by an upper-bound search of the edges held in LDS.  Runs of
+// equal bins are accumulated in registers, so one LDS atomic covers a run;
+// each workgroup then adds its non-zero LDS bins to the outputs with global
+// 64-bit atomics.  Up to 1024 edges sit in LDS at once; more are taken 1024
+// at a time, one launch each, a launch counting only the accesses that fall
+// between its edges.  Integer atomics make the result independent of
+// scheduling order.  A last tiny kernel forms alpha*count + beta*depthsum
+// exactly as 128-bit integers.
 #include "pc_internal.h"
 
 namespace pc {
@@ -22,7 +26,7 @@ namespace pc {
 constexpr int MRC_THREADS = 256;
 
 // number of edges <= x (edges non-decreasing)
-__device__ __forceinline__ uint32_t upper_bound(const uint64_t *e, uint32_t m, uint64_t x) {
+__device__ __forceinline__ uint32_t upper_bound(const uint32_t *e, uint32_t m, uint32_t x) {
     uint32_t lo = 0, hi = m;
     while (lo < hi) {
         const uint32_t mid = (lo + hi) >> 1;
@@ -31,30 +35,61 @@ __device__ __forceinline__ uint32_t upper_bound(const uint64_t *e, uint32_t m, u
     return lo;
 }
 
-constexpr int MRC_PER = 16;   // consecutive accesses per thread
+constexpr int MRC_PER = 8;             // consecutive accesses per thread
+constexpr uint32_t MRC_EDGES = 1024;   // edges held in LDS by one launch
 
-// bin of x: number of edges <= x, trying the previous bin first (neighbouring
-// accesses of one request usually share it)
-__device__ __forceinline__ uint32_t bin_of(const uint64_t *e, uint32_t K, uint64_t x, uint32_t hint) {
-    if (hint <= K && (hint == 0 || e[hint - 1] <= x) && (hint == K || x < e[hint])) return hint;
-    return upper_bound(e, K, x);
+// Distances and gaps are 32-bit and NONE (no previous or next use) is the
+// largest 32-bit value; edges are held clamped to it, min(edge, NONE).  A
+// value x <= NONE - 1 is at or above an edge exactly when it is at or above
+// the clamped edge, and NONE is at or above every clamped edge, so it lands
+// in the last bin with no special case.
+//
+// The bin a value falls in and the range [lo, hi] of values that share it.
+// With several launches (CHUNKED) a value outside this launch's edges gets
+// the local bin K + 1, which is never written out: below `below` (the edge
+// before this launch's first), or at or above its last edge while later
+// edges remain.
+struct BinRange {
+    uint32_t lo, hi, bin;
+};
+
+__device__ __forceinline__ uint32_t clamp_edge(uint64_t e) { return e < NONE ? (uint32_t)e : NONE; }
+
+template <bool CHUNKED>
+__device__ __forceinline__ BinRange find_bin(const uint32_t *e, uint32_t K, uint32_t x, uint32_t below,
+                                             bool last) {
+    const uint32_t b = upper_bound(e, K, x);
+    BinRange r{b ? e[b - 1] : 0u, b < K ? e[b] - 1 : NONE, b};
+    if (CHUNKED) {
+        if (b == 0 && x < below) r = BinRange{0u, below - 1, K + 1};
+        else if (b == 0) r.lo = below;
+        else if (b == K && !last) r.bin = K + 1;
+    }
+    return r;
 }
 
+// One launch covers bins k0 .. k0 + Kc of the n_caps + 1 (the last of them
+// only when k0 + Kc == n_caps) with its Kc edges caps[k0 .. k0 + Kc) in LDS.
+template <bool CHUNKED>
 __global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
     const uint32_t *__restrict__ dist, const uint32_t *__restrict__ depth,
-    const uint32_t *__restrict__ next, uint64_t n, const uint64_t *__restrict__ caps, uint32_t K,
-    uint64_t *__restrict__ count, uint64_t *__restrict__ depthsum, uint64_t *__restrict__ nexthist,
-    int32_t *__restrict__ err) {
+    const uint32_t *__restrict__ next, uint64_t n, const uint64_t *__restrict__ caps, uint32_t n_caps,
+    uint32_t k0, uint32_t Kc, uint64_t *__restrict__ count, uint64_t *__restrict__ depthsum,
+    uint64_t *__restrict__ nexthist, int32_t *__restrict__ err) {
     extern __shared__ uint64_t smem[];
-    uint64_t *s_caps = smem;                  // K
-    uint64_t *s_ds = s_caps + K;              // K+1
-    uint32_t *s_cnt = reinterpret_cast<uint32_t *>(s_ds + K + 1);   // K+1
-    uint32_t *s_nh = s_cnt + K + 1;           // K+1
+    const uint32_t K = Kc;
+    uint64_t *s_ds = smem;                    // K+2
+    uint32_t *s_cnt = reinterpret_cast<uint32_t *>(s_ds + K + 2);   // K+2
+    uint32_t *s_nh = s_cnt + K + 2;           // K+2
+    uint32_t *s_caps = s_nh + K + 2;          // K, clamped to NONE
+    const bool last = !CHUNKED || k0 + K == n_caps;
+    const uint32_t below = CHUNKED && k0 ? clamp_edge(caps[k0 - 1]) : 0u;
     for (uint32_t i = threadIdx.x; i < K; i += blockDim.x) {
-        s_caps[i] = caps[i];
-        if (blockIdx.x == 0 && i + 1 < K && caps[i] > caps[i + 1]) atomicOr(err, DEV_ERR_BAD_CAPS);
+        s_caps[i] = clamp_edge(caps[k0 + i]);
+        if (blockIdx.x == 0 && k0 + i + 1 < n_caps && caps[k0 + i] > caps[k0 + i + 1])
+            atomicOr(err, DEV_ERR_BAD_CAPS);
     }
-    for (uint32_t i = threadIdx.x; i <= K; i += blockDim.x) {
+    for (uint32_t i = threadIdx.x; i < K + 2; i += blockDim.x) {
         s_ds[i] = 0;
         s_cnt[i] = 0;
         s_nh[i] = 0;
@@ -97,17 +132,18 @@ __global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
             for (int j = 0; j < MRC_PER; ++j) pv[j] = 0;
         }
         const int m = full ? MRC_PER : (int)(n - t0);
-        uint32_t cur = K + 1, cnt = 0, ncur = K + 1, ncnt = 0;
+        // current bins (range empty at the start: lo > hi)
+        BinRange cur{1u, 0u, K + 2}, ncur{1u, 0u, K + 2};
+        uint32_t cnt = 0, ncnt = 0;
         uint64_t ds = 0;
         for (int j = 0; j < m; ++j) {
             const uint32_t d = dv[j];
-            const uint32_t bin = d == NONE ? K : bin_of(s_caps, K, d, cur);
-            if (bin != cur) {
+            if (d < cur.lo || d > cur.hi) {
                 if (cnt) {
-                    atomicAdd(&s_cnt[cur], cnt);
-                    if (ds) atomicAdd(reinterpret_cast<unsigned long long *>(&s_ds[cur]), (unsigned long long)ds);
+                    atomicAdd(&s_cnt[cur.bin], cnt);
+                    if (ds) atomicAdd(reinterpret_cast<unsigned long long *>(&s_ds[cur.bin]), (unsigned long long)ds);
                 }
-                cur = bin;
+                cur = find_bin<CHUNKED>(s_caps, K, d, below, last);
                 cnt = 0;
                 ds = 0;
             }
@@ -115,27 +151,28 @@ __global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
             ds += pv[j];
             if (next) {
                 const uint32_t q = nv[j];
-                const uint32_t nb = q == NONE ? K : bin_of(s_caps, K, (uint64_t)q - (t0 + j), ncur);
-                if (nb != ncur) {
-                    if (ncnt) atomicAdd(&s_nh[ncur], ncnt);
-                    ncur = nb;
+                const uint32_t g = q == NONE ? NONE : q - (uint32_t)(t0 + j);
+                if (g < ncur.lo || g > ncur.hi) {
+                    if (ncnt) atomicAdd(&s_nh[ncur.bin], ncnt);
+                    ncur = find_bin<CHUNKED>(s_caps, K, g, below, last);
                     ncnt = 0;
                 }
                 ++ncnt;
             }
         }
         if (cnt) {
-            atomicAdd(&s_cnt[cur], cnt);
-            if (ds) atomicAdd(reinterpret_cast<unsigned long long *>(&s_ds[cur]), (unsigned long long)ds);
+            atomicAdd(&s_cnt[cur.bin], cnt);
+            if (ds) atomicAdd(reinterpret_cast<unsigned long long *>(&s_ds[cur.bin]), (unsigned long long)ds);
         }
-        if (ncnt) atomicAdd(&s_nh[ncur], ncnt);
+        if (ncnt) atomicAdd(&s_nh[ncur.bin], ncnt);
     }
     __syncthreads();
     for (uint32_t i = threadIdx.x; i <= K; i += blockDim.x) {
-        if (s_cnt[i]) atomicAdd(reinterpret_cast<unsigned long long *>(&count[i]), (unsigned long long)s_cnt[i]);
-        if (s_ds[i]) atomicAdd(reinterpret_cast<unsigned long long *>(&depthsum[i]), (unsigned long long)s_ds[i]);
+        if (s_cnt[i]) atomicAdd(reinterpret_cast<unsigned long long *>(&count[k0 + i]), (unsigned long long)s_cnt[i]);
+        if (s_ds[i])
+            atomicAdd(reinterpret_cast<unsigned long long *>(&depthsum[k0 + i]), (unsigned long long)s_ds[i]);
         if (next && s_nh[i])
-            atomicAdd(reinterpret_cast<unsigned long long *>(&nexthist[i]), (unsigned long long)s_nh[i]);
+            atomicAdd(reinterpret_cast<unsigned long long *>(&nexthist[k0 + i]), (unsigned long long)s_nh[i]);
     }
 }
 
@@ -187,11 +224,21 @@ pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uin
 
     const int cus = pc::device_cus();
     uint64_t grid = (n + pc::MRC_THREADS * pc::MRC_PER - 1) / (pc::MRC_THREADS * pc::MRC_PER);
-    if (grid > (uint64_t)cus * 16) grid = (uint64_t)cus * 16;   // 16 workgroups per CU hide the load latency
+    // up to 64 workgroups per CU: eight resident (32 registers of loads per
+    // lane keep eight waves per SIMD) and the rest queued behind them, which
+    // hid the load latency best; more make the final flush contend
+    if (grid > (uint64_t)cus * 64) grid = (uint64_t)cus * 64;
     if (grid == 0) grid = 1;
-    const size_t shmem = (size_t)n_caps * 8 + (size_t)bins * 8 + (size_t)bins * 8;
-    PC_LAUNCH(pc::K_MRC_HIST, pc::mrc_hist_kernel, dim3((unsigned)grid), dim3(pc::MRC_THREADS), shmem, s, dist,
-              depth, next, n, caps, n_caps, count, depthsum, nextuse_hist, hdr);
+    for (uint32_t k0 = 0; k0 < n_caps; k0 += pc::MRC_EDGES) {
+        const uint32_t Kc = n_caps - k0 < pc::MRC_EDGES ? n_caps - k0 : pc::MRC_EDGES;
+        const size_t shmem = (size_t)(Kc + 2) * 16 + (size_t)Kc * 4;
+        if (n_caps <= pc::MRC_EDGES)
+            PC_LAUNCH(pc::K_MRC_HIST, pc::mrc_hist_kernel<false>, dim3((unsigned)grid), dim3(pc::MRC_THREADS),
+                      shmem, s, dist, depth, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, hdr);
+        else
+            PC_LAUNCH(pc::K_MRC_HIST, pc::mrc_hist_kernel<true>, dim3((unsigned)grid), dim3(pc::MRC_THREADS),
+                      shmem, s, dist, depth, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, hdr);
+    }
     PC_LAUNCH(pc::K_MRC_COST, pc::mrc_cost_kernel, dim3((bins + 255) / 256), dim3(256), 0, s, count, depthsum,
               bins, alpha, beta, cost_lo, cost_hi);
     return PC_OK;

@@ -195,7 +195,7 @@ def test_mrc_rejects_bad_arguments(L):
                                        d["a"], d["b"], d["cnt"], d["ds"], d["lo"], d["hi"], d["nh"],
                                        d["w"], d["wsz"], None)
     assert call(ok(k=0)) == -1
-    assert call(ok(k=1025)) == -1
+    assert call(ok(k=4097)) == -1
     assert call(ok(caps=None)) == -1
     assert call(ok(nxt=FAKE)) == -1          # next without nextuse_hist
     assert call(ok(n=0xFFFFFFFF)) == -2
@@ -210,7 +210,7 @@ def test_belady_rejects_bad_arguments(L):
     call = lambda d: L.pc_belady(d["nxt"], d["depth"], d["n"], d["caps"], d["k"], d["hits"], d["ds"], d["fl"],
                                  d["w"], d["wsz"], None)
     assert call(ok(k=0)) == -1
-    assert call(ok(k=1025)) == -1
+    assert call(ok(k=4097)) == -1
     assert call(ok(caps=None)) == -1
     assert call(ok(hits=None)) == -1
     assert call(ok(nxt=None)) == -1

@@ -283,6 +283,45 @@ def test_determinism():
     assert gpu_bins(d1, caps) == gpu_bins(d2, caps)
 
 
+@pytest.mark.parametrize("k", [1024, 1025, 2500, 4096])
+def test_many_capacities(k):
+    # more edges than one launch holds in LDS (1024): each launch takes only
+    # the accesses between its own edges; duplicate edges, a zero edge and
+    # edges on both sides of every distance, aligned and unaligned views
+    n = 70001
+    keys = stream("mixed", n, 11)
+    ids = oracle.key_ids(keys)
+    op, on = oracle.prev_next(keys, ids)
+    od = oracle.stack_distance_bit(op)
+    rng = np.random.default_rng(k)
+    top = int(od[od != NONE].max()) + 2
+    caps = np.sort(np.concatenate([[0], rng.integers(0, top + top // 4, k - 1)])).astype(np.uint64)
+    dep = rng.integers(0, 5000, n).astype(np.uint32)
+    say("case many_capacities k", k, "n", n, "distinct edges", np.unique(caps).size)
+    cnt, dsum, cost = oracle.mrc_bins(keys, caps, dep, 1, 1, ids, threads=16)
+    nh = oracle.nextuse_hist(on, caps)
+    g = gpu_bins(od, caps, dep, on, 1, 1)
+    assert g["count"] == cnt and g["depthsum"] == dsum and g["cost"] == cost
+    assert g["nextuse"] == nh
+    # views one element past an aligned start: scalar loads throughout
+    shift = lambda a: pc.to_dev_u32(np.concatenate([[7], a]).astype(np.uint32))[1:]
+    out, ws = pc.mrc_weighted(shift(od), pc.to_dev_u64(caps), shift(dep), shift(on), 1, 1)
+    assert pc.workspace_status(ws) == 0
+    g = pc.bins_to_host(out)
+    assert g["count"] == cnt and g["depthsum"] == dsum and g["cost"] == cost
+    assert g["nextuse"] == nh
+
+
+def test_decreasing_edges_set_the_status():
+    # edges out of order inside one launch's edges and across two launches
+    od = oracle.stack_distance_bit(oracle.prev_next(stream("mixed", 5000, 2))[0])
+    for k, i in ((10, 4), (2000, 1023)):
+        caps = np.arange(1, k + 1, dtype=np.uint64)
+        caps[i] = caps[i + 1] + 1
+        out, ws = pc.mrc_weighted(pc.to_dev_u32(od), pc.to_dev_u64(caps))
+        assert pc.workspace_status(ws) == 3, (k, i)
+
+
 # ------------------------------------------------------- workload-shaped
 
 def test_agent_trace_reduced_all_stages():
