@@ -78,7 +78,7 @@ def log(*a):
 HIP_KERNEL = {"sort_onesweep_pass": "pc::sort_pass_kernel", "link_partition": "pc::link_partition_kernel",
               "perm_partition": "pc::perm_partition_kernel", "hash_blocks": "pc::hash_fused_kernel",
               "sd_local_finish": "pc::sd_local_kernel",
-              "perm_local": "pc::perm_local_kernel", "mrc_hist": "pc::mrc_hist_kernel<false>",
+              "perm_local": "pc::perm_local_kernel", "mrc_hist": "pc::mrc_hist_kernel",
               "request_distance": "pc::req_dist_kernel",
               "session_distance": "pc::sess_dist_kernel", "reuse_profile_walk": "pc::prof_walk_kernel",
               "reuse_profile_pack": "pc::prof_pack_kernel", "chain_stair": "pc::chain_stair_kernel",
@@ -151,7 +151,9 @@ def measured_traffic(kernel_id):
     FETCH_SIZE / WRITE_SIZE summary (calibrated on a plain copy), or None when
     the library has changed since those counters were taken."""
     blob = _profile_blob()
-    entry = blob["kernels"].get(HIP_KERNEL.get(kernel_id, "")) if blob else None
+    want = HIP_KERNEL.get(kernel_id)
+    # a kernel template appears under its instance's name, e.g. "k<2>"
+    entry = next((e for name, e in blob["kernels"].items() if name.split("<")[0] == want), None) if blob else None
     if entry is None:
         return None
     return {"read_bytes": entry["read_bytes"], "write_bytes": entry["write_bytes"],

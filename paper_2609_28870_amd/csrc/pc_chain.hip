@@ -125,10 +125,14 @@ __global__ __launch_bounds__(CH_THREADS) void chain_anchor_kernel(
     }
 }
 
-// Slots per wave iteration: their loads are issued together so the three
-// dependent levels (slot record and anchor links, linked records, keys)
-// overlap across slots.
-constexpr int CH_BATCH = 2;
+// Slots per wave iteration (BATCH): their loads are issued together so the
+// three dependent levels (slot record and anchor links, linked records,
+// keys) overlap across slots.  The linked keys are spread over the whole
+// trace, and their latency grows with its size: two slots per iteration
+// were fastest up to about 3e8 accesses (2.2e8: 0.99 against 1.09 ms with
+// sixteen), eight from about 9e8 (4.3 against 5.0 ms with two) and sixteen
+// at 2.1e9 (9.8 against 12.5 ms with two, 10.0 with eight).
+static int stair_batch(uint64_t n) { return n >= (1ull << 30) ? 16 : n >= (1ull << 29) ? 8 : 2; }
 
 // The prev links of one slot: the lanes before the first depth at which the
 // slot's request and the linked anchor's request differ (both must cover
@@ -146,6 +150,7 @@ __device__ __forceinline__ uint32_t stair_claim(const Slot &q, const Slot &c, ui
 // lanes the linked slot got a next link for (claimed[link]).  A link to a
 // filler slot or to an anchor at another depth (equal keys there are a
 // collision) claims nothing.
+template <int CH_BATCH>
 __global__ __launch_bounds__(CH_THREADS) void chain_stair_kernel(
     const uint64_t *__restrict__ keys, uint64_t n_slots, const uint4 *__restrict__ rec,
     const uint32_t *__restrict__ aprev, int deepest, uint32_t *__restrict__ prev, uint32_t *__restrict__ next,
@@ -544,9 +549,17 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
     PC_LAUNCH(K_FILL32, chain_status_kernel, dim3(1), dim3(64), 0, s, (const int32_t *)w.aws, w.hdr, HW_HIGH_ANCHOR,
               HW_CHAIN);
     if ((st = fill_u32_gated(reinterpret_cast<uint32_t *>(w.claimed), 0u, 2 * ns, s, chain)) != PC_OK) return st;
-    PC_LAUNCH(K_CHAIN_STAIR, chain_stair_kernel, dim3(wave_grid((ns + CH_BATCH - 1) / CH_BATCH, cus)),
-              dim3(CH_THREADS), 0, s, keys, ns, (const uint4 *)w.rec, w.aprev, deepest, prev, next, w.open,
-              w.claimed, (const int32_t *)w.hdr);
+    const int batch = stair_batch(n);
+    const dim3 stair_grid(wave_grid((ns + batch - 1) / batch, cus));
+    if (batch == 16)
+        PC_LAUNCH(K_CHAIN_STAIR, chain_stair_kernel<16>, stair_grid, dim3(CH_THREADS), 0, s, keys, ns,
+                  (const uint4 *)w.rec, w.aprev, deepest, prev, next, w.open, w.claimed, (const int32_t *)w.hdr);
+    else if (batch == 8)
+        PC_LAUNCH(K_CHAIN_STAIR, chain_stair_kernel<8>, stair_grid, dim3(CH_THREADS), 0, s, keys, ns,
+                  (const uint4 *)w.rec, w.aprev, deepest, prev, next, w.open, w.claimed, (const int32_t *)w.hdr);
+    else
+        PC_LAUNCH(K_CHAIN_STAIR, chain_stair_kernel<2>, stair_grid, dim3(CH_THREADS), 0, s, keys, ns,
+                  (const uint4 *)w.rec, w.aprev, deepest, prev, next, w.open, w.claimed, (const int32_t *)w.hdr);
     PC_LAUNCH(K_CHAIN_SCAN, chain_count_kernel, dim3((unsigned)((ns + 255) / 256)), dim3(256), 0, s, ns,
               (const uint4 *)w.rec, (const uint2 *)w.claimed, w.open, w.cnt, (const int32_t *)w.hdr);
     const uint64_t tiles = (ns + SCAN_TILE - 1) / SCAN_TILE;

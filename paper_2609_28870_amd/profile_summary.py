@@ -43,8 +43,7 @@ IDS = {"pc::hash_fused_kernel": "hash_blocks",
        "pc::sd_seg_reduce_kernel": "sd_seg_scan", "pc::sd_seg_carry_kernel": "sd_seg_scan",
        "pc::sd_seg_scan_kernel": "sd_seg_scan",
        "pc::sd_dominance_kernel<true>": "sd_dominance_pass", "pc::sd_dominance_kernel<false>": "sd_dominance_pass",
-       "pc::sd_local_kernel": "sd_local_finish", "pc::mrc_hist_kernel<false>": "mrc_hist",
-       "pc::mrc_hist_kernel<true>": "mrc_hist", "pc::mrc_cost_kernel": "mrc_cost",
+       "pc::sd_local_kernel": "sd_local_finish", "pc::mrc_hist_kernel": "mrc_hist", "pc::mrc_cost_kernel": "mrc_cost",
        "pc::req_order_kernel": "request_order", "pc::req_dist_kernel": "request_distance",
        "pc::sess_dist_kernel": "session_distance", "pc::sess_profile_kernel": "session_profile",
        "pc::prof_pack_kernel": "reuse_profile_pack", "pc::prof_walk_kernel": "reuse_profile_walk",
@@ -135,7 +134,7 @@ def summarize(trace, fetch, write, runs, title, cmds):
         rate = (rd + wr) / (avg / 1e3) / 1e9 if rd is not None and avg > 0 else None
         rows.append((name, len(ds) / runs, len(wd) / runs, sum(ds) / runs, avg, rd, wr, rate))
         if rd is not None:
-            machine[name] = {"id": IDS.get(name, name), "avg_ms": round(avg, 4),
+            machine[name] = {"id": IDS.get(name, IDS.get(name.split("<")[0], name)), "avg_ms": round(avg, 4),
                              "launches_per_run": round(len(wd) / runs, 2),
                              "read_bytes": int(rd), "write_bytes": int(wr)}
     L = ["# %s" % title, "",

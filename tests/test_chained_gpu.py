@@ -214,3 +214,30 @@ def test_profiler_chained_equals_generic():
     (pa, na, ra, sa), (pb, nb, rb, sb) = outs
     assert np.array_equal(pa, pb) and np.array_equal(na, nb)
     assert ra == rb and sa == sb
+
+
+@pytest.mark.timeout(900)
+def test_mid_size_trace_equals_generic():
+    # 5.8e8 accesses: between 2^29 and 2^30 the staircase takes eight slots
+    # per wave iteration (two below, as on the chat-shaped trace, sixteen
+    # above, as on the full-scale one); chained and generic prev / next on
+    # the GPU, element by element (both are checked against the oracle on
+    # smaller traces)
+    tr = pcgen.make_trace("chat", n_sessions=50000)
+    up = pc.upload_trace(tr, 16)
+    n = up["n_blocks"]
+    say("mid-size chat trace:", n, "accesses")
+    assert (1 << 29) <= n < (1 << 30), n
+    keys, _, _ = pc.hash_blocks(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], n, 16,
+                                want_depth=False)
+    del up["tokens"]
+    prev, nxt, ws = pc.prev_next_chained(keys, up["blk_off"])
+    torch.cuda.synchronize()
+    info = pc.chained_info(ws)
+    say("chained:", info)
+    assert pc.workspace_status(ws) == 0 and not info["generic"], info
+    del ws
+    gp, gn, gws = pc.prev_next_use(keys)
+    torch.cuda.synchronize()
+    assert pc.workspace_status(gws) == 0
+    assert torch.equal(prev, gp) and torch.equal(nxt, gn)
