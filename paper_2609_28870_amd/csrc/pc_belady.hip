@@ -16,31 +16,35 @@
 // GPU mapping: one workgroup of one wave per capacity, all capacities at
 // once; each wave runs its capacity's simulation through the trace, 64
 // accesses (one per lane) at a time.  The values below a threshold theta
-// are bits of a bitmap over positions (with a one-bit-per-word summary);
-// the values at or above it, the ones evictions take, sit in a sorted
-// buffer in LDS (largest first).  Before a batch the buffer's values that
-// fall inside the batch's 64 positions leave it for a window register, so
-// the values present in the window are that register and one bitmap word,
-// read and cleared in one exchange.  Blocks accessed earlier in the same batch come
-// back inside it: their next uses are one-hot bits of the window.
+// are bits of a bitmap over positions; the values at or above it, the ones
+// evictions take, sit in a sorted buffer in LDS (largest first).  The
+// bitmap's words for the 4096 positions just past the batch live in an LDS
+// ring, the rest in global memory (with a one-bit-per-word summary).
+// Before a batch the buffer's values that fall inside its 64 positions
+// leave it for a window register, so the values present in the window are
+// that register and one ring word.  Blocks accessed earlier in the same
+// batch come back inside it: their next uses are one-hot bits of the window.
 //   * When the batch needs no eviction, or only as many as there are dead
 //     blocks, nothing in the window can leave: the hits are the window word
 //     or'ed with those bits (a wave OR), and the batch's inserts go to the
 //     dead count, the bitmap or the buffer in bulk.
-//   * Otherwise the wave walks the batch in access order with the window in
-//     a register: a hit clears its bit, an eviction takes a dead block, else
-//     the larger of the buffer's largest value (the top 64 held one per
-//     lane) and the largest value inserted earlier in the batch above theta
-//     (kept as a running maximum), else -- both exhausted -- the buffer is
-//     refilled with the bitmap's largest values above the window (whole
-//     words, top down, through the summary), else the window's largest
-//     value; each insert sets a window bit, joins the batch's values above
-//     theta, or goes to the bitmap.
+//   * Otherwise the evictions (after the dead blocks) take the largest
+//     values present, which are among the buffer's top 64 and the batch's
+//     own inserts above theta; the wave decides them all at once from a
+//     joint ranking of those 128 candidates (a prefix maximum and, per rank,
+//     a lowest prefix sum over the batch).  When those candidates run out it
+//     walks the batch in access order instead, refilling the buffer from the
+//     bitmap's largest values above the window (whole words, top down) and
+//     taking the window's largest value when nothing above it is left.
 // Values inserted above theta are merged into the buffer in sorted order
 // after the batch; a buffer above 256 values spills its lowest into the
-// bitmap.  Bitmap words are touched only by their capacity's wave, through
-// relaxed device-scope atomics (they live in L2); a workgroup fence orders
-// one batch's updates before the next batch's reads.
+// bitmap.  Global bitmap words are touched only by their capacity's wave,
+// through relaxed device-scope atomics (they live in L2).  A word entering
+// the ring may still hold bits inserted before: every 16 batches, after a
+// fence, the words that entered are exchanged for zero and their bits are
+// merged into the ring at the next such sync, long before the window gets
+// there, so a batch waits on no global memory (the next uses themselves are
+// loaded four batches ahead).  A refill syncs at once.
 #include "pc_internal.h"
 
 namespace pc {
@@ -50,6 +54,10 @@ constexpr uint32_t BEL_SPILL_AT = 256;        // buffer size above which the low
 constexpr uint32_t BEL_BUF = BEL_SPILL_AT + 2 * WAVE;   // LDS buffer entries (largest fill: spill size + one batch)
 constexpr uint64_t BEL_INF = 1ull << 40;      // theta before the first refill: everything in the bitmap
 constexpr int32_t DEV_ERR_BELADY = 5;
+constexpr uint64_t BEL_RING = 64;             // bitmap words just past the window held in LDS
+constexpr uint64_t BEL_SYNC = 16;             // batches between two exchanges with the global bitmap
+static_assert(2 * BEL_SYNC <= BEL_RING, "a word entering the ring is merged before the window reaches it");
+constexpr int BEL_AHEAD = 4;                  // batches of next[] and depth[] loaded ahead
 
 __device__ __forceinline__ uint64_t bm_load(const uint64_t *p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -93,11 +101,13 @@ __device__ __forceinline__ uint64_t wave_sum64(uint32_t x) {
            ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)hi, WAVE - 1) << 16);
 }
 
-// next[t] of lane's access, NONE for an invalid entry (flagged)
-__device__ __forceinline__ uint32_t load_next(const uint32_t *__restrict__ next, uint64_t t, uint64_t n,
-                                              int32_t *err) {
-    if (t >= n) return NONE;
-    const uint32_t x = next[t];
+// next[t] of lane's access (NONE past the end), checked only when used so
+// that the load stays in flight until then
+__device__ __forceinline__ uint32_t load_next(const uint32_t *__restrict__ next, uint64_t t, uint64_t n) {
+    return t < n ? next[t] : NONE;
+}
+// the loaded next[t], NONE for an invalid entry (flagged)
+__device__ __forceinline__ uint32_t checked_next(uint32_t x, uint64_t t, uint64_t n, int32_t *err) {
     if (x != NONE && ((uint64_t)x <= t || (uint64_t)x >= n)) {
         atomicOr(err, DEV_ERR_BAD_LAYOUT);
         return NONE;
@@ -128,8 +138,64 @@ struct BelState {
     uint32_t head, bufn;
     uint64_t theta;
     uint64_t bm_hi;        // every bitmap value is below this
-    bool dirty;            // the bitmap changed since the last fence
+    uint64_t *ring;        // LDS: bitmap words [wb, wb + BEL_RING) of window word wb, slot w % BEL_RING
+    uint64_t ex_lo;        // ring words from here on may still have bits in the global bitmap
+    uint64_t fl_lo;        // ring words [fl_lo, fl_lo + fl_n) were exchanged and are not merged yet:
+    uint32_t fl_n;         //   lane i holds word fl_lo + i's bits in fl_val
+    uint64_t fl_val;
+    uint64_t w0;           // global bitmap words
 };
+
+// value x (not in the window) into the bitmap: an LDS ring word when the
+// ring holds its word (ring end rend, exclusive, in words), else the global
+// bitmap word and its summary bit
+__device__ __forceinline__ void bel_insert(const BelState &S, uint64_t *l0, uint64_t *l1, uint32_t x,
+                                           uint64_t rend) {
+    if ((uint64_t)(x >> 6) < rend)
+        atomicOr(reinterpret_cast<unsigned long long *>(&S.ring[(x >> 6) % BEL_RING]), 1ull << (x & 63));
+    else
+        bm_insert(l0, l1, x);
+}
+
+// Brings the ring up to date with the global bitmap for ring end rend: the
+// words exchanged at the last sync are merged (their exchanges have returned
+// after the fence), and the words that entered the ring since then are taken
+// out of the global bitmap (their global inserts are complete after the
+// fence).  Those exchanges return during the next batches and are merged at
+// the next sync, BEL_SYNC batches before the window can reach them; with
+// `full` they are waited for and merged at once.
+__device__ __forceinline__ void ring_sync(BelState &S, uint64_t *l0, uint64_t *l1, uint64_t rend, bool full) {
+    const int lane = threadIdx.x;
+    if (!full && S.fl_n == 0 && S.bm_hi <= (S.ex_lo << 6)) {
+        // nothing in flight, and the words to exchange hold no value
+        if (rend > S.ex_lo) S.ex_lo = rend;
+        return;
+    }
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's global inserts and exchanges have completed
+    wave_fence();
+    if ((uint32_t)lane < S.fl_n && S.fl_val)
+        atomicOr(reinterpret_cast<unsigned long long *>(&S.ring[(S.fl_lo + lane) % BEL_RING]), S.fl_val);
+    const uint64_t m = rend > S.ex_lo ? rend - S.ex_lo : 0;   // at most BEL_SYNC + 1 words
+    const uint64_t w = S.ex_lo + lane;
+    uint64_t v = 0;
+    if ((uint64_t)lane < m && w < S.w0) {
+        v = bm_xchg(&l0[w], 0ull);
+        bm_and(&l1[w >> 6], ~(1ull << (w & 63)));
+    }
+    S.fl_lo = S.ex_lo;
+    S.fl_n = (uint32_t)m;
+    S.fl_val = v;
+    if (rend > S.ex_lo) S.ex_lo = rend;
+    if (full) {
+        __builtin_amdgcn_s_waitcnt(0);
+        wave_fence();
+        if ((uint32_t)lane < S.fl_n && S.fl_val)
+            atomicOr(reinterpret_cast<unsigned long long *>(&S.ring[(S.fl_lo + lane) % BEL_RING]), S.fl_val);
+        S.fl_n = 0;
+        S.fl_val = 0;
+    }
+    __syncthreads();
+}
 
 // buffer back to index 0 (through the spare array)
 __device__ __forceinline__ void compact(BelState &S) {
@@ -143,14 +209,18 @@ __device__ __forceinline__ void compact(BelState &S) {
 }
 
 // the largest bitmap values in [lo, theta) to the buffer's tail until it
-// holds BEL_TARGET values: whole words, top down, the summary skipping
-// empty words; theta drops to the lowest value taken
-__device__ void refill(BelState &S, uint64_t *l0, uint64_t *l1, uint64_t lo, uint64_t n) {
+// holds BEL_TARGET values: whole words, top down (the global bitmap's words
+// past the ring first, the summary skipping empty words, then the ring's);
+// theta drops to the lowest value taken.  lo is the window's end and rend
+// the ring's end (words).
+__device__ void refill(BelState &S, uint64_t *l0, uint64_t *l1, uint64_t lo_all, uint64_t n, uint64_t rend) {
     const int lane = threadIdx.x;
-    if (S.dirty) wave_fence();   // the bitmap's latest inserts first
+    ring_sync(S, l0, l1, rend, true);   // every ring value in LDS, every insert visible
     compact(S);
     uint64_t hi = S.theta < n + WAVE ? S.theta : n + WAVE;   // exclusive
     if (S.bm_hi < hi) hi = S.bm_hi;
+    // global words: values from the ring's end on
+    const uint64_t lo = lo_all > (rend << 6) ? lo_all : (rend << 6);
     const uint64_t wlo = lo >> 6;
     const uint64_t lo_mask = ~((1ull << (lo & 63)) - 1);
     while (S.bufn < BEL_TARGET && hi > lo) {
@@ -204,10 +274,30 @@ __device__ void refill(BelState &S, uint64_t *l0, uint64_t *l1, uint64_t lo, uin
         }
         hi = w << 6 > lo ? w << 6 : lo;
     }
+    // ring words, top down, when the global ones did not suffice
+    if (hi > lo_all && hi <= lo) {
+        const uint64_t rlo_mask = ~((1ull << (lo_all & 63)) - 1);
+        while (S.bufn < BEL_TARGET && hi > lo_all) {
+            const uint64_t w = (hi - 1) >> 6;
+            const uint64_t room = hi - (w << 6);
+            uint64_t bits = S.ring[w % BEL_RING] & (room >= 64 ? ~0ull : (1ull << room) - 1);
+            if (w == (lo_all >> 6)) bits &= rlo_mask;
+            if (bits) {
+                if ((bits >> lane) & 1) {
+                    const uint64_t above = lane == WAVE - 1 ? 0ull : bits & (~0ull << (lane + 1));
+                    S.buf[S.bufn + (uint32_t)__popcll(above)] = (uint32_t)((w << 6) + lane);
+                }
+                S.bufn += (uint32_t)__popcll(bits);
+                S.theta = (w << 6) + (uint64_t)__builtin_ctzll(bits);
+                __syncthreads();
+                if (lane == 0) S.ring[w % BEL_RING] &= ~bits;
+                __syncthreads();
+            }
+            hi = w << 6 > lo_all ? w << 6 : lo_all;
+        }
+    }
     // every bitmap value at or above hi has been taken
-    if (hi < S.bm_hi) S.bm_hi = hi > lo ? hi : lo;
-    wave_fence();
-    S.dirty = false;
+    if (hi < S.bm_hi) S.bm_hi = hi > lo_all ? hi : lo_all;
     __syncthreads();
 }
 
@@ -219,19 +309,29 @@ __device__ __forceinline__ uint32_t buffer_top(const BelState &S) {
 __device__ __forceinline__ uint32_t clamp32(uint64_t v) { return v > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)v; }
 
 __device__ void belady_one(const uint32_t *__restrict__ next, const uint32_t *__restrict__ depth, uint64_t n,
-                           uint64_t c64, uint64_t *__restrict__ l0, uint64_t *__restrict__ l1,
+                           uint64_t c64, uint64_t *__restrict__ l0, uint64_t *__restrict__ l1, uint64_t w0,
                            uint8_t *__restrict__ flags, uint64_t *hits_out, uint64_t *dsum_out, int32_t *err,
-                           uint32_t *s_a, uint32_t *s_b, uint32_t *s_new, uint32_t *s_tmp, uint64_t *s_sb) {
+                           uint32_t *s_a, uint32_t *s_b, uint32_t *s_new, uint32_t *s_tmp, uint64_t *s_sb,
+                           uint64_t *s_ring) {
     const int lane = threadIdx.x;
-    BelState S{s_a, s_b, 0, 0, BEL_INF, 0, false};
+    // the global bitmap starts empty, so the ring's first words are complete
+    BelState S{s_a, s_b, 0, 0, BEL_INF, 0, s_ring, BEL_RING, 0, 0, 0, w0};
+    for (uint64_t i = lane; i < BEL_RING; i += WAVE) s_ring[i] = 0;
+    __syncthreads();
     // resident blocks never exceed n, so the capacity is clamped to 32 bits
     const uint32_t c = clamp32(c64 < n ? c64 : n);
     uint32_t dead = 0, size = 0;
     uint64_t hits = 0, dsum = 0;
-    // this batch's next uses and depths, loaded one batch ahead
-    uint32_t xq = load_next(next, (uint64_t)lane, n, err);
-    uint32_t dq = ((uint64_t)lane < n && depth) ? depth[lane] : 0u;
+    // next uses and depths loaded BEL_AHEAD batches ahead (xq, dq: this batch)
+    uint32_t xa[BEL_AHEAD], da[BEL_AHEAD];
+#pragma unroll
+    for (int b = 0; b < BEL_AHEAD; ++b) {
+        const uint64_t tb = (uint64_t)b * WAVE + lane;
+        xa[b] = load_next(next, tb, n);
+        da[b] = (tb < n && depth) ? depth[tb] : 0u;
+    }
     for (uint64_t t0 = 0; t0 < n; t0 += WAVE) {
+        const uint32_t xq = checked_next(xa[0], t0 + lane, n, err), dq = da[0];
         const uint64_t t = t0 + lane;
         const bool valid = t < n;
         const uint32_t xv = xq, dv = dq;
@@ -241,39 +341,38 @@ __device__ void belady_one(const uint32_t *__restrict__ next, const uint32_t *__
         const uint32_t we32 = clamp32(we), t32 = (uint32_t)t0;
 
         // keep the buffer out of this batch's positions: its values inside the
-        // window (its tail, the buffer being descending) join the window word
+        // window join the window word.  They are its smallest ones (the buffer
+        // is descending and holds no value below the window), distinct
+        // positions of the window, so at most its last 64 entries, one per lane.
         uint64_t wlow = 0;
         if (S.theta < we) {
-            uint32_t lo = 0, hi = S.bufn;
-            while (lo < hi) {
-                const uint32_t mid = (lo + hi) >> 1;
-                if ((uint64_t)S.buf[S.head + mid] >= we) lo = mid + 1; else hi = mid;
-            }
-            uint64_t bw = 0;
-            for (uint32_t i = lo + lane; i < S.bufn; i += WAVE) bw |= 1ull << (S.buf[S.head + i] - t32);
-            wlow = wave_or64(bw);
-            S.bufn = lo;
+            const uint32_t bn = S.bufn;
+            const bool has = (uint32_t)lane < bn;
+            const uint32_t v = has ? S.buf[S.head + bn - 1 - lane] : NONE;
+            const bool in = has && (uint64_t)v < we;
+            wlow = wave_or64(in ? 1ull << (v - t32) : 0ull);
+            S.bufn = bn - (uint32_t)__popcll(ballot(in));
             S.theta = we;
         }
 
-        // values present in the window: that register and the window's bitmap
-        // word, taken and cleared
+        // values present in the window: that register and the window's ring
+        // word (complete: merged at a sync at least BEL_SYNC batches ago),
+        // taken and cleared; the ring now ends BEL_RING words past the window
         const uint64_t w = t0 >> 6;
+        const uint64_t rend = w + BEL_RING;
         uint64_t wbits = wlow;
-        if (S.bm_hi > t0) {   // else the bitmap holds nothing at or above the window
-            uint64_t wb = 0;
-            if (lane == 0) {
-                wb = bm_xchg(&l0[w], 0ull);
-                if (wb) bm_and(&l1[w >> 6], ~(1ull << (w & 63)));
-            }
-            wbits |= readlane64(wb, 0);
+        if (S.bm_hi > t0) {   // else the bitmap holds nothing at or past the window
+            wbits |= S.ring[w % BEL_RING];
+            __syncthreads();
+            if (lane == 0) S.ring[w % BEL_RING] = 0;
+            __syncthreads();
         }
         const bool inwin = xv != NONE && xv < we32;
         const uint64_t link = wave_or64(inwin ? 1ull << (xv - t32) : 0ull);
         uint64_t hm = (wbits | link) & vmask;
         const uint32_t misses = (uint32_t)__popcll(vmask & ~hm);
         const uint32_t E = size + misses > c ? size + misses - c : 0u;
-        if (E > dead && dead + S.bufn < (uint32_t)WAVE) refill(S, l0, l1, we, n);
+        if (E > dead && dead + S.bufn < (uint32_t)WAVE) refill(S, l0, l1, we, n, rend);
 
         bool to_buffer, to_bitmap;
         uint32_t popped = 0;
@@ -443,7 +542,7 @@ __device__ void belady_one(const uint32_t *__restrict__ next, const uint32_t *__
                         S.head += popped;
                         S.bufn -= popped;
                         popped = 0;
-                        refill(S, l0, l1, we, n);
+                        refill(S, l0, l1, we, n, rend);
                         top = buffer_top(S);
                         pb = S.bufn ? (uint32_t)__builtin_amdgcn_readlane((int)top, 0) : 0u;
                     }
@@ -481,10 +580,9 @@ __device__ void belady_one(const uint32_t *__restrict__ next, const uint32_t *__
         dsum += wave_sum64(h ? dv : 0u);
         if (flags && valid) flags[t] = h ? 1 : 0;
         if (ballot(to_bitmap)) {
-            if (to_bitmap) bm_insert(l0, l1, xv);
+            if (to_bitmap) bel_insert(S, l0, l1, xv, rend);
             const uint64_t m = (uint64_t)wave_max(to_bitmap ? xv : 0u) + 1;
             if (m > S.bm_hi) S.bm_hi = m;
-            S.dirty = true;
         }
 
         // buffer: drop the popped values, merge the batch's values above theta
@@ -526,21 +624,25 @@ __device__ void belady_one(const uint32_t *__restrict__ next, const uint32_t *__
         // spill the lowest values when the buffer grows large
         if (S.bufn > BEL_SPILL_AT) {
             const uint64_t top_spilled = (uint64_t)S.buf[S.head + BEL_TARGET] + 1;
-            for (uint32_t i = BEL_TARGET + lane; i < S.bufn; i += WAVE) bm_insert(l0, l1, S.buf[S.head + i]);
+            for (uint32_t i = BEL_TARGET + lane; i < S.bufn; i += WAVE)
+                bel_insert(S, l0, l1, S.buf[S.head + i], rend);
             if (top_spilled > S.bm_hi) S.bm_hi = top_spilled;
             S.bufn = BEL_TARGET;
             S.theta = S.buf[S.head + BEL_TARGET - 1];
-            S.dirty = true;
-        }
-        if (S.dirty) {   // this batch's bitmap updates before the next batch's reads
-            wave_fence();
-            S.dirty = false;
         }
         __syncthreads();
-        // the next batch's loads, in flight during its window exchange
-        const uint64_t tn = t + WAVE;
-        xq = load_next(next, tn, n, err);
-        dq = (tn < n && depth) ? depth[tn] : 0u;
+        // every BEL_SYNC batches: the ring against the global bitmap, for the
+        // next batch's ring end
+        if ((w + 1) % BEL_SYNC == 0) ring_sync(S, l0, l1, rend + 1, false);
+        // the loads BEL_AHEAD batches ahead
+#pragma unroll
+        for (int b = 0; b + 1 < BEL_AHEAD; ++b) {
+            xa[b] = xa[b + 1];
+            da[b] = da[b + 1];
+        }
+        const uint64_t tn = t + (uint64_t)BEL_AHEAD * WAVE;
+        xa[BEL_AHEAD - 1] = load_next(next, tn, n);
+        da[BEL_AHEAD - 1] = (tn < n && depth) ? depth[tn] : 0u;
     }
     if (lane == 0) {
         *hits_out = hits;
@@ -557,6 +659,7 @@ __global__ __launch_bounds__(WAVE) void belady_kernel(const uint32_t *__restrict
     __shared__ uint32_t s_a[BEL_BUF], s_b[BEL_BUF], s_new[WAVE];
     __shared__ __align__(16) uint32_t s_tmp[WAVE];
     __shared__ uint64_t s_sb[2 * WAVE];
+    __shared__ uint64_t s_ring[BEL_RING];
     const uint32_t k = blockIdx.x;
     const uint64_t c = caps[k];
     uint8_t *fl = flags ? flags + (uint64_t)k * n : nullptr;
@@ -569,8 +672,8 @@ __global__ __launch_bounds__(WAVE) void belady_kernel(const uint32_t *__restrict
         }
         return;
     }
-    belady_one(next, depth, n, c, l0s + (uint64_t)k * w0, l1s + (uint64_t)k * w1, fl, hits + k, dsum + k, err, s_a,
-               s_b, s_new, s_tmp, s_sb);
+    belady_one(next, depth, n, c, l0s + (uint64_t)k * w0, l1s + (uint64_t)k * w1, w0, fl, hits + k, dsum + k, err,
+               s_a, s_b, s_new, s_tmp, s_sb, s_ring);
 }
 
 // bitmap words per capacity: one bit per position plus a word of slack, and
