@@ -418,8 +418,8 @@ pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uin
  *             access t hits at caps[k]
  * One wave simulates one capacity through the whole trace, all capacities
  * at once: the call takes time linear in n, not one memory pass (on MI355X
- * about 1 s per 2.8e7 accesses for a capacity that rarely evicts, up to
- * 2.5 s for one that evicts on most accesses).
+ * about 0.8 s per 2.8e7 accesses for a capacity that rarely evicts, up to
+ * 2.3 s for one that evicts on most accesses).
  * Workspace: about n_caps * n / 8 bytes of bitmaps.  Status 5 reports an
  * internal consistency check (not expected for a valid next[]).
  * ------------------------------------------------------------------------ */
