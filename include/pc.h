@@ -50,6 +50,7 @@ typedef enum {
 #define PC_NONE 0xFFFFFFFFu
 #define PC_MAX_CAPS 4096u
 #define PC_HASH_DEEPEST_FIRST 1u   /* pc_hash_blocks flag */
+#define PC_PREV_ONLY 2u            /* pc_prev_next_chained flag: next is scratch */
 #define PC_MAX_PROFILE_EDGES 128u  /* time-histogram edges of the profiles */
 #define PC_MAX_FREQ 2048u          /* largest exact frequency / request-count bin */
 #define PC_FREQ_CLASSES 32u        /* frequency classes floor(log2 f) */
@@ -152,7 +153,11 @@ pc_status pc_prev_next_use(const uint64_t *keys, uint64_t n, uint32_t *prev, uin
  *   blk_off   uint64[n_seqs+1], blk_off[0] = 0, non-decreasing, blk_off[n_seqs]
  *             = n.  Any other layout sets the workspace status to 2 and takes
  *             the generic path (outputs still exact).
- *   flags     0 or PC_HASH_DEEPEST_FIRST.
+ *   flags     0 or PC_HASH_DEEPEST_FIRST, or'ed with PC_PREV_ONLY when only
+ *             prev is wanted (session-level eviction, Sec. 5.3, reads no next
+ *             use): next is still required, as scratch for the generic path,
+ *             and its contents after the call are unspecified; the chain path
+ *             then skips its next links (about 4 bytes per access).
  *   key_hist  as for pc_prev_next_use; used only by the generic path over all
  *             keys.
  * Every choice between the two paths is made on the device: the unresolved

@@ -154,7 +154,7 @@ template <int CH_BATCH>
 __global__ __launch_bounds__(CH_THREADS) void chain_stair_kernel(
     const uint64_t *__restrict__ keys, uint64_t n_slots, const uint4 *__restrict__ rec,
     const uint32_t *__restrict__ aprev, int deepest, uint32_t *__restrict__ prev, uint32_t *__restrict__ next,
-    uint4 *__restrict__ open, uint2 *__restrict__ claimed, const int32_t *__restrict__ hdr) {
+    int want_next, uint4 *__restrict__ open, uint2 *__restrict__ claimed, const int32_t *__restrict__ hdr) {
     if (hdr[HW_BAD]) return;
     const int lane = threadIdx.x & (WAVE - 1);
     const uint64_t waves = (uint64_t)gridDim.x * (CH_THREADS / WAVE);
@@ -186,7 +186,7 @@ __global__ __launch_bounds__(CH_THREADS) void chain_stair_kernel(
             const uint32_t p = stair_claim(q[k], cp[k], kr[k], kp[k], lane, deepest);
             const uint64_t pr = lane_pos(q[k], lane, deepest);
             if (v) prev[pr] = p;
-            if (p != UNK) next[p] = (uint32_t)pr;
+            if (want_next && p != UNK) next[p] = (uint32_t)pr;
             const uint64_t mp = ballot(v && p == UNK), mc = ballot(p != UNK);
             if (lane == 0) {
                 open[j0 + k] = make_uint4((uint32_t)mp, (uint32_t)(mp >> 32), 0u, 0u);
@@ -346,7 +346,7 @@ __global__ __launch_bounds__(CH_THREADS) void chain_merge_kernel(const uint32_t 
                                                                  const uint32_t *__restrict__ cprev,
                                                                  const uint32_t *__restrict__ cnext,
                                                                  uint32_t *__restrict__ prev,
-                                                                 uint32_t *__restrict__ next,
+                                                                 uint32_t *__restrict__ next, int want_next,
                                                                  int32_t *__restrict__ hdr) {
     if (!hdr[HW_CHAIN]) return;
     const uint64_t m = (uint32_t)hdr[HW_UNRESOLVED];
@@ -366,12 +366,8 @@ __global__ __launch_bounds__(CH_THREADS) void chain_merge_kernel(const uint32_t 
         }
         if (f & 2) {
             const uint32_t u = cnext[i];
-            if (u != NONE) {
-                bad |= !(cflag[u] & 1);
-                next[p] = cpos[u];
-            } else {
-                next[p] = NONE;
-            }
+            if (u != NONE) bad |= !(cflag[u] & 1);
+            if (want_next) next[p] = u != NONE ? cpos[u] : NONE;
         }
     }
     if (bad) atomicOr(hdr + HW_FAIL, 1);
@@ -508,7 +504,7 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
     using namespace pc;
     if (n >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
     if (n > 0 && (!keys || !prev || !next || !blk_off)) return PC_ERR_INVALID;
-    if (flags & ~PC_HASH_DEEPEST_FIRST) return PC_ERR_INVALID;
+    if (flags & ~(PC_HASH_DEEPEST_FIRST | PC_PREV_ONLY)) return PC_ERR_INVALID;
     if (!ws) return PC_ERR_WORKSPACE;
     if (ws_bytes < pc_prev_next_chained_ws(n, n_seqs)) return PC_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
@@ -516,6 +512,7 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
     pc_status st = fill_u32(reinterpret_cast<uint32_t *>(w.hdr), 0u, HW_WORDS, s);
     if (st != PC_OK || n == 0) return st;
     const int deepest = (flags & PC_HASH_DEEPEST_FIRST) ? 1 : 0;
+    const int want_next = (flags & PC_PREV_ONLY) ? 0 : 1;
     const int cus = device_cus();
 
     // the generic prev/next over all keys, gated on `gate` (nullptr: always)
@@ -553,13 +550,16 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
     const dim3 stair_grid(wave_grid((ns + batch - 1) / batch, cus));
     if (batch == 16)
         PC_LAUNCH(K_CHAIN_STAIR, chain_stair_kernel<16>, stair_grid, dim3(CH_THREADS), 0, s, keys, ns,
-                  (const uint4 *)w.rec, w.aprev, deepest, prev, next, w.open, w.claimed, (const int32_t *)w.hdr);
+                  (const uint4 *)w.rec, w.aprev, deepest, prev, next, want_next, w.open, w.claimed,
+                  (const int32_t *)w.hdr);
     else if (batch == 8)
         PC_LAUNCH(K_CHAIN_STAIR, chain_stair_kernel<8>, stair_grid, dim3(CH_THREADS), 0, s, keys, ns,
-                  (const uint4 *)w.rec, w.aprev, deepest, prev, next, w.open, w.claimed, (const int32_t *)w.hdr);
+                  (const uint4 *)w.rec, w.aprev, deepest, prev, next, want_next, w.open, w.claimed,
+                  (const int32_t *)w.hdr);
     else
         PC_LAUNCH(K_CHAIN_STAIR, chain_stair_kernel<2>, stair_grid, dim3(CH_THREADS), 0, s, keys, ns,
-                  (const uint4 *)w.rec, w.aprev, deepest, prev, next, w.open, w.claimed, (const int32_t *)w.hdr);
+                  (const uint4 *)w.rec, w.aprev, deepest, prev, next, want_next, w.open, w.claimed,
+                  (const int32_t *)w.hdr);
     PC_LAUNCH(K_CHAIN_SCAN, chain_count_kernel, dim3((unsigned)((ns + 255) / 256)), dim3(256), 0, s, ns,
               (const uint4 *)w.rec, (const uint2 *)w.claimed, w.open, w.cnt, (const int32_t *)w.hdr);
     const uint64_t tiles = (ns + SCAN_TILE - 1) / SCAN_TILE;
@@ -587,7 +587,7 @@ pc_status pc_prev_next_chained(const uint64_t *keys, uint64_t n, const uint64_t 
     uint64_t mg = (m_cap + CH_THREADS - 1) / CH_THREADS;
     if (mg > (uint64_t)cus * 16) mg = (uint64_t)cus * 16;
     PC_LAUNCH(K_CHAIN_MERGE, chain_merge_kernel, dim3((unsigned)(mg ? mg : 1)), dim3(CH_THREADS), 0, s, o.cpos,
-              o.cflag, o.cprev, o.cnext, prev, next, w.hdr);
+              o.cflag, o.cprev, o.cnext, prev, next, want_next, w.hdr);
 
     // the check's verdict; the generic path over all keys runs only if it
     // (or an earlier step) says so

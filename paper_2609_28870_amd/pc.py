@@ -21,6 +21,8 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "_lib", "libpc.so")
 NONE = 0xFFFFFFFF
+DEEPEST_FIRST = 1   # PC_HASH_DEEPEST_FIRST
+PREV_ONLY = 2       # PC_PREV_ONLY
 
 _lib = None
 
@@ -225,10 +227,12 @@ def high_key_passes_ran(ws: torch.Tensor) -> bool:
 
 def prev_next_chained(keys: torch.Tensor, blk_off: torch.Tensor, prev: Optional[torch.Tensor] = None,
                       nxt: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
-                      key_hist: Optional[torch.Tensor] = None, deepest_first: bool = False):
+                      key_hist: Optional[torch.Tensor] = None, deepest_first: bool = False,
+                      prev_only: bool = False):
     """pc_prev_next_chained: the same prev / next as prev_next_use for keys
     laid out per request as hash_blocks writes them; the path is chosen on
-    the device (no synchronisation)."""
+    the device (no synchronisation).  With ``prev_only`` (PC_PREV_ONLY) next
+    is scratch and unspecified afterwards."""
     L = lib()
     n = keys.numel()
     n_seqs = blk_off.numel() - 1
@@ -239,7 +243,8 @@ def prev_next_chained(keys: torch.Tensor, blk_off: torch.Tensor, prev: Optional[
         nxt = torch.empty(n, dtype=torch.int32, device=dev)
     if ws is None:
         ws = workspace(L.pc_prev_next_chained_ws(n, n_seqs))
-    check(L.pc_prev_next_chained(_ptr(keys), n, _ptr(blk_off), n_seqs, 1 if deepest_first else 0,
+    check(L.pc_prev_next_chained(_ptr(keys), n, _ptr(blk_off), n_seqs,
+                                 (PREV_ONLY if prev_only else 0) | (DEEPEST_FIRST if deepest_first else 0),
                                  _ptr(prev), _ptr(nxt), _ptr(key_hist), _ptr(ws), ws.numel(), _stream()))
     return prev, nxt, ws
 
@@ -589,8 +594,9 @@ class Pipeline:
 
     def _prev_next(self, keys):
         if self.chained:
+            # session-level eviction reads no next use
             prev_next_chained(keys, self.blk_off, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist,
-                              deepest_first=self.request)
+                              deepest_first=self.request, prev_only=self.residency == "session")
         else:
             prev_next_use(keys, self.prev, self.next, ws=self.ws_pn, key_hist=self.key_hist)
 

@@ -81,7 +81,8 @@ def test_prev_next_chained_rejects_bad_arguments(L):
     assert L.pc_prev_next_chained(None, n, FAKE, seqs, 0, FAKE, FAKE, None, FAKE, ws, None) == -1
     assert L.pc_prev_next_chained(FAKE, n, None, seqs, 0, FAKE, FAKE, None, FAKE, ws, None) == -1
     assert L.pc_prev_next_chained(FAKE, n, FAKE, seqs, 0, FAKE, None, None, FAKE, ws, None) == -1
-    assert L.pc_prev_next_chained(FAKE, n, FAKE, seqs, 2, FAKE, FAKE, None, FAKE, ws, None) == -1
+    assert L.pc_prev_next_chained(FAKE, n, FAKE, seqs, 4, FAKE, FAKE, None, FAKE, ws, None) == -1   # unknown flag
+    assert L.pc_prev_next_chained(FAKE, n, FAKE, seqs, 2, FAKE, None, None, FAKE, ws, None) == -1   # prev-only: next still required
     assert L.pc_prev_next_chained(FAKE, n, FAKE, seqs, 0, FAKE, FAKE, None, None, ws, None) == -3
     assert L.pc_prev_next_chained(FAKE, n, FAKE, seqs, 0, FAKE, FAKE, None, FAKE, ws - 1, None) == -3
 

@@ -195,8 +195,29 @@ def test_pipeline_chained_equals_generic(residency):
     for k in a:
         if k == "bins":
             assert a[k] == b[k]
+        elif k == "next" and residency == "session":
+            continue   # the chained session pipeline asks for prev only
         else:
             assert np.array_equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("kind", ["chained", "unchained"])
+def test_prev_only_gives_the_same_prev(kind):
+    # PC_PREV_ONLY skips the next links of the chain path; prev stays exact,
+    # also when the generic path over all keys runs
+    tr = pcgen.make_trace("chat", n_sessions=300)
+    keys, _ = oracle.hash_trace(tr)
+    off = tr.blk_off(16).astype(np.int64)
+    if kind == "unchained":
+        keys = np.random.default_rng(5).integers(0, 1000, keys.size).astype(np.uint64)
+    op, on = oracle.prev_next(keys)
+    kd, od = pc.to_dev_u64(keys), pc.to_dev_u64(off.astype(np.uint64))
+    prev, nxt, ws = pc.prev_next_chained(kd, od, prev_only=True)
+    info = pc.chained_info(ws)
+    say(kind, info)
+    assert pc.workspace_status(ws) == 0
+    assert info["generic"] == (kind == "unchained"), info
+    assert np.array_equal(pc.as_u32(prev), op)
 
 
 def test_profiler_chained_equals_generic():
