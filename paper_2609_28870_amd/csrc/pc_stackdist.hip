@@ -1019,7 +1019,7 @@ pc_status pc_stack_distance_req(const uint32_t *prev, const uint32_t *dist, cons
     if (st != PC_OK || n == 0) return st;
     const int cus = pc::device_cus();
     uint64_t grid = ((uint64_t)n_seqs + 3) / 4;
-    if (grid > (uint64_t)cus * 16) grid = (uint64_t)cus * 16;
+    if (grid > (uint64_t)cus * 64) grid = (uint64_t)cus * 64;   // 64 per CU: 7.44 -> 7.15 ms on the full trace
     PC_LAUNCH(pc::K_REQ_DIST, pc::req_dist_kernel, dim3((unsigned)grid), dim3(256), 0, s, prev, dist, blk_off, n_seqs,
               n, dist_req, hdr);
     return PC_OK;
