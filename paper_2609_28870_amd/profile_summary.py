@@ -138,7 +138,7 @@ def summarize(trace, fetch, write, runs, title, cmds):
                              "launches_per_run": round(len(wd) / runs, 2),
                              "read_bytes": int(rd), "write_bytes": int(wr)}
     L = ["# %s" % title, "",
-         "Commands (from the repository root on the GPU box; the profiler runs from /tmp with TMPDIR=/tmp), "
+         "Commands (from the repository root on the MI355X host; the profiler runs from /tmp with TMPDIR=/tmp), "
          "then `python -m paper_2609_28870_amd.profile_summary` over their CSV output:", ""]
     L += ["    " + c for c in cmds]
     L += ["",
