@@ -38,7 +38,9 @@ ALGO_BYTES = {
     "perm_local": lambda B: 12 + 8,               # (t, prev, next) in, prev + next out
     "sd_dominance_pass": lambda B: 8 + 8,         # (t, acc) in and out
     "sd_local_finish": lambda B: 8 + 4 + 4,       # (t, acc), prev in; dist out
-    "mrc_hist": lambda B: 12,                     # dist, depth, next in
+    # dist, depth, next in (the per-access pipeline takes depth from the
+    # request layout, so there only dist and next count; see mrc_bytes)
+    "mrc_hist": lambda B: 12,
     "request_distance": lambda B: 4 + 4 + 4,      # prev, per-access dist in; dist_req out
     "session_distance": lambda B: 4 + 4,          # prev in; dist_sess out
     "reuse_profile_pack": lambda B: 4 + 8,        # next in; (next, request) out
@@ -453,6 +455,10 @@ def main():
         n_slots = pn_elems = n_blocks
     work_launches = {"sort_onesweep_pass": 4 * calls + 4 * highs, "link_partition": calls + highs,
                      "sort_digit_hist": calls + highs}
+    # bins: dist in, depth in unless it comes from the request layout, next in
+    # when the next-use histogram is taken
+    layout_depth = getattr(pipe, "layout_depth", False)
+    mrc_bytes = 4 + (0 if layout_depth else 4) + (4 if getattr(pipe, "with_nextuse", False) else 0)
     kernels = {}
     for name, (launches, ms) in prof.items():
         if launches == 0:
@@ -469,7 +475,7 @@ def main():
                 # elements sorted per inner call, averaged over the calls
                 per_launch = ALGO_BYTES[name](B) * pn_elems // calls
             else:
-                per_launch = (8 if (request or session_mode) and name == "mrc_hist" else ALGO_BYTES[name](B)) * n_blocks
+                per_launch = (mrc_bytes if name == "mrc_hist" else ALGO_BYTES[name](B)) * n_blocks
             entry["algo_bytes_per_launch"] = per_launch
             entry["avg_working_launch_ms"] = round(per_step / wl, 4)
             entry["algo_GBps"] = round(per_launch * wl / per_step / 1e6, 1)
@@ -492,14 +498,14 @@ def main():
                 "link_partition": "prev_next",
                 "perm_partition": "prev_next", "perm_local": "prev_next", "chain_anchor": "prev_next",
                 "chain_stair": "prev_next", "chain_scan": "prev_next", "chain_compact": "prev_next",
-                "chain_merge": "prev_next", "mrc_hist": "mrc",
+                "chain_merge": "prev_next", "mrc_hist": "mrc", "mrc_map": "mrc",
                 "mrc_cost": "mrc", "request_distance": "request_distance",
                 "session_requests": "session_profile" if args.profile else "session_distance",
                 "session_distance": "session_distance",
                 "reuse_profile_pack": "reuse_profile", "reuse_profile_walk": "reuse_profile",
                 "session_profile": "session_profile", "belady": "belady"}
     stage_bytes = {"hash": 4 * B + 8, "prev_next": 16, "stack_distance": 8,
-                   "mrc": 8 if request or session_mode else 12, "request_distance": 12,
+                   "mrc": mrc_bytes, "request_distance": 12,
                    "session_distance": 8, "reuse_profile": 24}
 
     def stage_name(kid):

@@ -44,6 +44,7 @@ static const char *kernel_name(KernelId k) {
     case K_RUNS_MERGE: return "runs_merge";
     case K_RUNS_FILL: return "runs_fill";
     case K_BELADY: return "belady";
+    case K_MRC_MAP: return "mrc_map";
     case K_COUNT: break;
     }
     return "";

@@ -74,6 +74,7 @@ enum KernelId {
     K_RUNS_MERGE,
     K_RUNS_FILL,
     K_BELADY,
+    K_MRC_MAP,
     K_COUNT
 };
 

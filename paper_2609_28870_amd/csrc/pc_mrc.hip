@@ -19,6 +19,15 @@
 // between its edges.  Integer atomics make the result independent of
 // scheduling order.  A last tiny kernel forms alpha*count + beta*depthsum
 // exactly as 128-bit integers.
+//
+// pc_mrc_weighted_layout takes the depths from the request layout instead
+// of an array: depth(t) = t - (start of t's request).  A map kernel writes a
+// bitmap of every request start and, per 64 positions, the start of the
+// request holding the first; a thread of the bins kernel finds its first
+// access's request start from those (the last start bit at or below it in
+// its 64-position word, else the word's entry) and follows the start bits
+// across its 8 accesses: 12 bytes of map per 64 accesses instead of 256
+// bytes of depth.
 #include "pc_internal.h"
 
 namespace pc {
@@ -70,9 +79,10 @@ __device__ __forceinline__ BinRange find_bin(const uint32_t *e, uint32_t K, uint
 
 // One launch covers bins k0 .. k0 + Kc of the n_caps + 1 (the last of them
 // only when k0 + Kc == n_caps) with its Kc edges caps[k0 .. k0 + Kc) in LDS.
-template <bool CHUNKED>
+template <bool CHUNKED, bool LAYOUT>
 __global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
     const uint32_t *__restrict__ dist, const uint32_t *__restrict__ depth,
+    const uint32_t *__restrict__ gstart, const uint8_t *__restrict__ startbits,
     const uint32_t *__restrict__ next, uint64_t n, const uint64_t *__restrict__ caps, uint32_t n_caps,
     uint32_t k0, uint32_t Kc, uint64_t *__restrict__ count, uint64_t *__restrict__ depthsum,
     uint64_t *__restrict__ nexthist, int32_t *__restrict__ err) {
@@ -127,7 +137,22 @@ __global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
                 nv[j] = (in && next) ? next[t0 + j] : 0u;
             }
         }
-        if (!depth) {
+        if (LAYOUT) {
+            // the depth within the request: the last request start at or below
+            // t0 (in the 64-position word, else the word's entry), then the
+            // starts among the thread's accesses
+            const uint64_t wd = t0 >> 6;
+            const uint64_t bits = reinterpret_cast<const uint64_t *>(startbits)[wd];
+            const uint32_t sh = (uint32_t)(t0 & 63);
+            const uint64_t upto = sh == 63 ? bits : bits & ((2ull << sh) - 1);   // starts at or below t0
+            uint32_t st = upto ? (uint32_t)((wd << 6) + 63 - __builtin_clzll(upto)) : gstart[wd];
+            const uint32_t sb = (uint32_t)(bits >> sh);
+#pragma unroll
+            for (int j = 0; j < MRC_PER; ++j) {
+                if (j && ((sb >> j) & 1u)) st = (uint32_t)(t0 + j);
+                pv[j] = (uint32_t)(t0 + j) - st;
+            }
+        } else if (!depth) {
 #pragma unroll
             for (int j = 0; j < MRC_PER; ++j) pv[j] = 0;
         }
@@ -176,6 +201,28 @@ __global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
     }
 }
 
+// The layout map, one thread per request: bit t of startbits set when a
+// request starts at t (the bitmap is zeroed first), and gstart[w] = the
+// start of the request holding position 64w.  Checks the layout as
+// pc_prev_next_chained does.
+__global__ __launch_bounds__(256) void mrc_map_kernel(const uint64_t *__restrict__ off, uint32_t n_seqs, uint64_t n,
+                                                      uint32_t *__restrict__ gstart, uint32_t *__restrict__ startbits,
+                                                      int32_t *__restrict__ err) {
+    const uint64_t r = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= n_seqs) return;
+    const uint64_t a = off[r], b = off[r + 1];
+    bool ok = a <= b && b <= n;
+    if (r == 0) ok = ok && a == 0;
+    if (r + 1 == n_seqs) ok = ok && b == n;
+    if (!ok) {
+        atomicOr(err, DEV_ERR_BAD_LAYOUT);
+        return;
+    }
+    if (a == b) return;
+    atomicOr(&startbits[a >> 5], 1u << (a & 31));
+    for (uint64_t w = (a + 63) / 64; w * 64 < b; ++w) gstart[w] = (uint32_t)a;
+}
+
 // cost = alpha*count + beta*depthsum as a 128-bit integer (hi:lo), mod 2^128
 __global__ void mrc_cost_kernel(const uint64_t *__restrict__ count, const uint64_t *__restrict__ depthsum,
                                 uint32_t bins, uint64_t alpha, uint64_t beta, uint64_t *__restrict__ lo,
@@ -188,6 +235,90 @@ __global__ void mrc_cost_kernel(const uint64_t *__restrict__ count, const uint64
     const uint64_t s = a_lo + b_lo;
     lo[i] = s;
     hi[i] = a_hi + b_hi + (s < a_lo ? 1ull : 0ull);
+}
+
+
+// workspace of pc_mrc_weighted_layout: the header, gstart (one word per 64
+// positions) and the start bitmap (one bit per position, whole 64-bit words)
+struct MrcLayoutWs {
+    int32_t *hdr;
+    uint32_t *gstart, *startbits;
+    size_t bytes;
+};
+static MrcLayoutWs mrc_layout_carve(void *ws, uint64_t n) {
+    MrcLayoutWs w{};
+    char *base = static_cast<char *>(ws);
+    size_t off = 0;
+    w.hdr = reinterpret_cast<int32_t *>(base);
+    off += WS_HEADER;
+    const uint64_t words = (n + 63) / 64;
+    w.gstart = reinterpret_cast<uint32_t *>(base + off);
+    off = align_up(off + words * sizeof(uint32_t));
+    w.startbits = reinterpret_cast<uint32_t *>(base + off);
+    off = align_up(off + words * sizeof(uint64_t));
+    w.bytes = off;
+    return w;
+}
+
+// both entry points: depths from `depth` (or none), or from the layout
+// blk_off (then ws is a layout workspace)
+static pc_status mrc_run(const uint32_t *dist, const uint32_t *depth, const uint64_t *blk_off, uint32_t n_seqs,
+                         const uint32_t *next, uint64_t n, const uint64_t *caps, uint32_t n_caps, uint64_t alpha,
+                         uint64_t beta, uint64_t *count, uint64_t *depthsum, uint64_t *cost_lo, uint64_t *cost_hi,
+                         uint64_t *nextuse_hist, void *ws, size_t ws_bytes, hipStream_t s) {
+    (void)ws_bytes;
+    if (n >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
+    if (n_caps == 0 || n_caps > PC_MAX_CAPS) return PC_ERR_INVALID;
+    if (!caps || !count || !depthsum || !cost_lo || !cost_hi) return PC_ERR_INVALID;
+    if (n > 0 && !dist) return PC_ERR_INVALID;
+    if (next && !nextuse_hist) return PC_ERR_INVALID;
+    if (!ws) return PC_ERR_WORKSPACE;
+    int32_t *hdr = reinterpret_cast<int32_t *>(ws);
+    const uint32_t bins = n_caps + 1;
+    pc_status st;
+    if ((st = fill_u32(reinterpret_cast<uint32_t *>(hdr), 0u, 1, s)) != PC_OK) return st;
+    if ((st = fill_u32(reinterpret_cast<uint32_t *>(count), 0u, 2 * (size_t)bins, s)) != PC_OK) return st;
+    if ((st = fill_u32(reinterpret_cast<uint32_t *>(depthsum), 0u, 2 * (size_t)bins, s)) != PC_OK) return st;
+    if (nextuse_hist && (st = fill_u32(reinterpret_cast<uint32_t *>(nextuse_hist), 0u, 2 * (size_t)bins, s)) != PC_OK)
+        return st;
+
+    const int cus = device_cus();
+    const bool layout = blk_off != nullptr;
+    const MrcLayoutWs lw = mrc_layout_carve(ws, n);
+    if (layout && n > 0) {
+        if (n_seqs == 0) return fill_u32(reinterpret_cast<uint32_t *>(hdr), (uint32_t)DEV_ERR_BAD_LAYOUT, 1, s);
+        if ((st = fill_u32(lw.startbits, 0u, 2 * ((n + 63) / 64), s)) != PC_OK) return st;
+        PC_LAUNCH(K_MRC_MAP, mrc_map_kernel, dim3((unsigned)(((uint64_t)n_seqs + 255) / 256)), dim3(256), 0, s,
+                  blk_off, n_seqs, n, lw.gstart, lw.startbits, hdr);
+    }
+    const uint32_t *gs = layout ? lw.gstart : nullptr;
+    const uint8_t *sb = layout ? reinterpret_cast<const uint8_t *>(lw.startbits) : nullptr;
+    uint64_t grid = (n + MRC_THREADS * MRC_PER - 1) / (MRC_THREADS * MRC_PER);
+    // up to 64 workgroups per CU: eight resident (32 registers of loads per
+    // lane keep eight waves per SIMD) and the rest queued behind them, which
+    // hid the load latency best; more make the final flush contend
+    if (grid > (uint64_t)cus * 64) grid = (uint64_t)cus * 64;
+    if (grid == 0) grid = 1;
+    for (uint32_t k0 = 0; k0 < n_caps; k0 += MRC_EDGES) {
+        const uint32_t Kc = n_caps - k0 < MRC_EDGES ? n_caps - k0 : MRC_EDGES;
+        const size_t shmem = (size_t)(Kc + 2) * 16 + (size_t)Kc * 4;
+        const bool chunked = n_caps > MRC_EDGES;
+        if (!chunked && !layout)
+            PC_LAUNCH(K_MRC_HIST, (mrc_hist_kernel<false, false>), dim3((unsigned)grid), dim3(MRC_THREADS), shmem,
+                      s, dist, depth, gs, sb, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, hdr);
+        else if (!chunked)
+            PC_LAUNCH(K_MRC_HIST, (mrc_hist_kernel<false, true>), dim3((unsigned)grid), dim3(MRC_THREADS), shmem,
+                      s, dist, depth, gs, sb, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, hdr);
+        else if (!layout)
+            PC_LAUNCH(K_MRC_HIST, (mrc_hist_kernel<true, false>), dim3((unsigned)grid), dim3(MRC_THREADS), shmem,
+                      s, dist, depth, gs, sb, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, hdr);
+        else
+            PC_LAUNCH(K_MRC_HIST, (mrc_hist_kernel<true, true>), dim3((unsigned)grid), dim3(MRC_THREADS), shmem,
+                      s, dist, depth, gs, sb, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, hdr);
+    }
+    PC_LAUNCH(K_MRC_COST, mrc_cost_kernel, dim3((bins + 255) / 256), dim3(256), 0, s, count, depthsum, bins, alpha,
+              beta, cost_lo, cost_hi);
+    return PC_OK;
 }
 
 }  // namespace pc
@@ -205,43 +336,25 @@ pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uin
                           uint64_t *count, uint64_t *depthsum, uint64_t *cost_lo, uint64_t *cost_hi,
                           uint64_t *nextuse_hist, void *ws, size_t ws_bytes, void *stream) {
     if (n >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
-    if (n_caps == 0 || n_caps > PC_MAX_CAPS) return PC_ERR_INVALID;
-    if (!caps || !count || !depthsum || !cost_lo || !cost_hi) return PC_ERR_INVALID;
-    if (n > 0 && !dist) return PC_ERR_INVALID;
-    if (next && !nextuse_hist) return PC_ERR_INVALID;
-    if (!ws) return PC_ERR_WORKSPACE;
-    if (ws_bytes < pc_mrc_weighted_ws(n, n_caps)) return PC_ERR_WORKSPACE;
-    hipStream_t s = (hipStream_t)stream;
-    int32_t *hdr = reinterpret_cast<int32_t *>(ws);
-    const uint32_t bins = n_caps + 1;
-    pc_status st;
-    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(hdr), 0u, 1, s)) != PC_OK) return st;
-    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(count), 0u, 2 * (size_t)bins, s)) != PC_OK) return st;
-    if ((st = pc::fill_u32(reinterpret_cast<uint32_t *>(depthsum), 0u, 2 * (size_t)bins, s)) != PC_OK) return st;
-    if (nextuse_hist &&
-        (st = pc::fill_u32(reinterpret_cast<uint32_t *>(nextuse_hist), 0u, 2 * (size_t)bins, s)) != PC_OK)
-        return st;
+    if (ws && ws_bytes < pc_mrc_weighted_ws(n, n_caps)) return PC_ERR_WORKSPACE;
+    return pc::mrc_run(dist, depth, nullptr, 0, next, n, caps, n_caps, alpha, beta, count, depthsum, cost_lo, cost_hi,
+                       nextuse_hist, ws, ws_bytes, (hipStream_t)stream);
+}
 
-    const int cus = pc::device_cus();
-    uint64_t grid = (n + pc::MRC_THREADS * pc::MRC_PER - 1) / (pc::MRC_THREADS * pc::MRC_PER);
-    // up to 64 workgroups per CU: eight resident (32 registers of loads per
-    // lane keep eight waves per SIMD) and the rest queued behind them, which
-    // hid the load latency best; more make the final flush contend
-    if (grid > (uint64_t)cus * 64) grid = (uint64_t)cus * 64;
-    if (grid == 0) grid = 1;
-    for (uint32_t k0 = 0; k0 < n_caps; k0 += pc::MRC_EDGES) {
-        const uint32_t Kc = n_caps - k0 < pc::MRC_EDGES ? n_caps - k0 : pc::MRC_EDGES;
-        const size_t shmem = (size_t)(Kc + 2) * 16 + (size_t)Kc * 4;
-        if (n_caps <= pc::MRC_EDGES)
-            PC_LAUNCH(pc::K_MRC_HIST, pc::mrc_hist_kernel<false>, dim3((unsigned)grid), dim3(pc::MRC_THREADS),
-                      shmem, s, dist, depth, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, hdr);
-        else
-            PC_LAUNCH(pc::K_MRC_HIST, pc::mrc_hist_kernel<true>, dim3((unsigned)grid), dim3(pc::MRC_THREADS),
-                      shmem, s, dist, depth, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, hdr);
-    }
-    PC_LAUNCH(pc::K_MRC_COST, pc::mrc_cost_kernel, dim3((bins + 255) / 256), dim3(256), 0, s, count, depthsum,
-              bins, alpha, beta, cost_lo, cost_hi);
-    return PC_OK;
+size_t pc_mrc_weighted_layout_ws(uint64_t n, uint32_t n_caps) {
+    (void)n_caps;
+    return pc::mrc_layout_carve(nullptr, n).bytes;
+}
+
+pc_status pc_mrc_weighted_layout(const uint32_t *dist, const uint64_t *blk_off, uint32_t n_seqs,
+                                 const uint32_t *next, uint64_t n, const uint64_t *caps, uint32_t n_caps,
+                                 uint64_t alpha, uint64_t beta, uint64_t *count, uint64_t *depthsum, uint64_t *cost_lo,
+                                 uint64_t *cost_hi, uint64_t *nextuse_hist, void *ws, size_t ws_bytes, void *stream) {
+    if (n >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
+    if (n > 0 && !blk_off) return PC_ERR_INVALID;
+    if (ws && ws_bytes < pc_mrc_weighted_layout_ws(n, n_caps)) return PC_ERR_WORKSPACE;
+    return pc::mrc_run(dist, nullptr, blk_off, n_seqs, next, n, caps, n_caps, alpha, beta, count, depthsum, cost_lo,
+                       cost_hi, nextuse_hist, ws, ws_bytes, (hipStream_t)stream);
 }
 
 }  // extern "C"

@@ -100,6 +100,11 @@ def lib():
     L.pc_mrc_weighted.restype = _st
     L.pc_mrc_weighted.argtypes = [_vp, _vp, _vp, _u64, _vp, _u32, _u64, _u64, _vp, _vp, _vp, _vp,
                                   _vp, _vp, _sz, _vp]
+    L.pc_mrc_weighted_layout_ws.restype = _sz
+    L.pc_mrc_weighted_layout_ws.argtypes = [_u64, _u32]
+    L.pc_mrc_weighted_layout.restype = _st
+    L.pc_mrc_weighted_layout.argtypes = [_vp, _vp, _u32, _vp, _u64, _vp, _u32, _u64, _u64, _vp, _vp, _vp, _vp,
+                                         _vp, _vp, _sz, _vp]
     L.pc_belady_ws.restype = _sz
     L.pc_belady_ws.argtypes = [_u64, _u32]
     L.pc_belady.restype = _st
@@ -436,6 +441,27 @@ def mrc_weighted(dist: torch.Tensor, caps: torch.Tensor, depth: Optional[torch.T
     return out, ws
 
 
+def mrc_weighted_layout(dist: torch.Tensor, caps: torch.Tensor, blk_off: torch.Tensor,
+                        nxt: Optional[torch.Tensor] = None, alpha: int = 1, beta: int = 0,
+                        out: Optional[dict] = None, ws: Optional[torch.Tensor] = None):
+    """pc_mrc_weighted_layout: as mrc_weighted with depth[t] = t - blk_off[r]
+    for the request r holding t (the ascending layout of hash_blocks)."""
+    L = lib()
+    n = dist.numel()
+    k = caps.numel()
+    dev = _dev()
+    if out is None:
+        out = {name: torch.empty(k + 1, dtype=torch.int64, device=dev)
+               for name in ("count", "depthsum", "cost_lo", "cost_hi", "nextuse")}
+    if ws is None:
+        ws = workspace(L.pc_mrc_weighted_layout_ws(n, k))
+    check(L.pc_mrc_weighted_layout(_ptr(dist), _ptr(blk_off), blk_off.numel() - 1, _ptr(nxt), n, _ptr(caps), k,
+                                   alpha & (2 ** 64 - 1), beta & (2 ** 64 - 1), _ptr(out["count"]),
+                                   _ptr(out["depthsum"]), _ptr(out["cost_lo"]), _ptr(out["cost_hi"]),
+                                   _ptr(out["nextuse"]), _ptr(ws), ws.numel(), _stream()))
+    return out, ws
+
+
 def belady(nxt: torch.Tensor, caps: torch.Tensor, depth: Optional[torch.Tensor] = None, flags: bool = False,
            out: Optional[dict] = None, ws: Optional[torch.Tensor] = None):
     """pc_belady: hits and depth sums of Belady's MIN at every capacity
@@ -518,12 +544,17 @@ class Pipeline:
     the same order; the next-use histogram is not taken in that mode.  Its
     bins are valid at capacities of at least the largest request.
     ``with_belady`` (per-access mode) also runs Belady's MIN at every
-    capacity on the step's next-use index (``belady_out``)."""
+    capacity on the step's next-use index (``belady_out``).
+
+    In the per-access and session modes the bins take each block's depth
+    from the request layout (``mrc_weighted_layout``) and the hash writes no
+    depth (``depth`` is None); ``depth_array=True``, and Belady's MIN, keep
+    the depth array."""
 
     def __init__(self, tokens, tok_start, tok_len, blk_off, n_blocks: int, caps,
                  block_size: int = 16, alpha: int = 1, beta: int = 0, with_nextuse: bool = True,
                  residency: str = "access", session: Optional[torch.Tensor] = None, chained: bool = True,
-                 with_belady: bool = False):
+                 with_belady: bool = False, depth_array: bool = False):
         if residency not in ("access", "request", "session"):
             raise PcError("residency must be 'access', 'request' or 'session'")
         if residency == "session" and session is None:
@@ -539,10 +570,12 @@ class Pipeline:
         self.request = residency == "request"
         self.session = session
         self.with_nextuse = with_nextuse and residency == "access"
+        self.with_belady = with_belady and residency == "access"
+        self.layout_depth = not (depth_array or self.request or self.with_belady)
         n = self.n
         self.keys = torch.empty(n, dtype=torch.int64, device=dev)
         self.key_hist = torch.empty(4 * 256, dtype=torch.int32, device=dev)
-        self.depth = torch.empty(n, dtype=torch.int32, device=dev)
+        self.depth = None if self.layout_depth else torch.empty(n, dtype=torch.int32, device=dev)
         self.prev = torch.empty(n, dtype=torch.int32, device=dev)
         self.next = torch.empty(n, dtype=torch.int32, device=dev)
         self.dist = torch.empty(n, dtype=torch.int32, device=dev)
@@ -561,8 +594,8 @@ class Pipeline:
             self.keys_r, self.depth_r = self.keys, self.depth   # hashed in recency order
             self.dist_req = torch.empty(n, dtype=torch.int32, device=dev)
             self.ws_req = workspace(L.pc_stack_distance_req_ws())
-        self.ws_mrc = workspace(L.pc_mrc_weighted_ws(n, k))
-        self.with_belady = with_belady and residency == "access"
+        self.ws_mrc = workspace(L.pc_mrc_weighted_layout_ws(n, k) if self.layout_depth
+                                else L.pc_mrc_weighted_ws(n, k))
         if self.with_belady:
             self.belady_out = {"hits": torch.empty(k, dtype=torch.int64, device=dev),
                                "depthsum": torch.empty(k, dtype=torch.int64, device=dev)}
@@ -570,19 +603,17 @@ class Pipeline:
 
     def run(self):
         hash_blocks(self.tokens, self.tok_start, self.tok_len, self.blk_off, self.n, self.B,
-                    keys=self.keys, depth=self.depth, ws=self.ws_hash, key_hist=self.key_hist,
-                    deepest_first=self.request)
+                    want_depth=not self.layout_depth, keys=self.keys, depth=self.depth, ws=self.ws_hash,
+                    key_hist=self.key_hist, deepest_first=self.request)
         if self.residency == "session":
             self._prev_next(self.keys)
             stack_distance_session(self.prev, self.blk_off, self.session, dist_sess=self.dist, ws=self.ws_sd)
-            mrc_weighted(self.dist, self.caps, self.depth, None, self.alpha, self.beta, out=self.bins,
-                         ws=self.ws_mrc)
+            self._bins(None)
             return
         if not self.request:
             self._prev_next(self.keys)
             self._stack_distance()
-            mrc_weighted(self.dist, self.caps, self.depth, self.next if self.with_nextuse else None,
-                         self.alpha, self.beta, out=self.bins, ws=self.ws_mrc)
+            self._bins(self.next if self.with_nextuse else None)
             if self.with_belady:
                 belady(self.next, self.caps, self.depth, out=self.belady_out, ws=self.ws_bel)
             return
@@ -591,6 +622,13 @@ class Pipeline:
         stack_distance_req(self.prev, self.dist, self.blk_off, dist_req=self.dist_req, ws=self.ws_req)
         mrc_weighted(self.dist_req, self.caps, self.depth_r, None, self.alpha, self.beta,
                      out=self.bins, ws=self.ws_mrc)
+
+    def _bins(self, nxt):
+        if self.layout_depth:
+            mrc_weighted_layout(self.dist, self.caps, self.blk_off, nxt, self.alpha, self.beta, out=self.bins,
+                                ws=self.ws_mrc)
+        else:
+            mrc_weighted(self.dist, self.caps, self.depth, nxt, self.alpha, self.beta, out=self.bins, ws=self.ws_mrc)
 
     def _prev_next(self, keys):
         if self.chained:

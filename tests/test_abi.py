@@ -203,6 +203,23 @@ def test_mrc_rejects_bad_arguments(L):
     assert call(ok(w=None)) == -3
 
 
+def test_mrc_layout_rejects_bad_arguments(L):
+    ws = L.pc_mrc_weighted_layout_ws(10, 4)
+    assert ws > L.pc_mrc_weighted_layout_ws(0, 4)
+    ok = lambda **kw: dict(dict(dist=FAKE, off=FAKE, seqs=2, nxt=None, n=10, caps=FAKE, k=4, a=1, b=0,
+                                cnt=FAKE, ds=FAKE, lo=FAKE, hi=FAKE, nh=None, w=FAKE, wsz=ws), **kw)
+    call = lambda d: L.pc_mrc_weighted_layout(d["dist"], d["off"], d["seqs"], d["nxt"], d["n"], d["caps"], d["k"],
+                                              d["a"], d["b"], d["cnt"], d["ds"], d["lo"], d["hi"], d["nh"],
+                                              d["w"], d["wsz"], None)
+    assert call(ok(off=None)) == -1
+    assert call(ok(k=0)) == -1
+    assert call(ok(k=4097)) == -1
+    assert call(ok(nxt=FAKE)) == -1
+    assert call(ok(n=0xFFFFFFFF)) == -2
+    assert call(ok(w=None)) == -3
+    assert call(ok(wsz=ws - 1)) == -3
+
+
 def test_belady_rejects_bad_arguments(L):
     ws = L.pc_belady_ws(1000, 4)
     assert ws > L.pc_belady_ws(10, 4) > 0
@@ -241,5 +258,6 @@ def test_profiling_table(L):
     names = [L.pc_prof_kernel_name(i).decode() for i in range(n)]
     assert "hash_blocks" in names and "sd_dominance_pass" in names and "mrc_hist" in names
     assert all(names) and len(set(names)) == n
-    assert names[-1] == "belady" and "chain_stair" in names and "runs_merge" in names and "runs_fill" in names
+    assert names[-1] == "mrc_map" and "belady" in names and "chain_stair" in names and "runs_merge" in names
+    assert "runs_fill" in names
     assert pc.prof_read() is not None

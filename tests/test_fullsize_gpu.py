@@ -76,6 +76,11 @@ def full(request):
     p.run()
     torch.cuda.synchronize()
     say(request.param, "pipeline done, status", p.status())
+    # the pipeline takes depths from the request layout; the hash kernel's
+    # depth output, for the checks of the depth array
+    _, p.depth_out, _ = pc.hash_blocks(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
+                                       B, keys=p.keys, ws=p.ws_hash)
+    torch.cuda.synchronize()
     p.reference = read_reference(request.param)
     p.name = request.param
     yield tr, caps, p
@@ -95,7 +100,7 @@ def test_reference_is_for_this_trace(full):
 def test_all_arrays_match_the_oracle(full):
     _, _, p = full
     g = p.reference
-    for name, t in (("keys", p.keys), ("depth", p.depth), ("prev", p.prev), ("next", p.next), ("dist", p.dist)):
+    for name, t in (("keys", p.keys), ("depth", p.depth_out), ("prev", p.prev), ("next", p.next), ("dist", p.dist)):
         got = array_fp(t)
         say(p.name, name, "fingerprint", hex(got))
         assert got == g["fp_" + name], name
@@ -161,7 +166,7 @@ def test_sampled_request_keys(full):
         want, wd = oracle.hash_requests(tr.tokens, tr.tok_start[r:r + 1], tr.tok_len[r:r + 1], 16)
         got = pc.as_u64(p.keys[lo:hi])
         assert np.array_equal(got, want), r
-        assert np.array_equal(pc.as_u32(p.depth[lo:hi]), wd), r
+        assert np.array_equal(pc.as_u32(p.depth_out[lo:hi]), wd), r
 
 
 def window_requests(tr, a, b):
@@ -246,7 +251,7 @@ def test_bins_match_torch_bucketize(full):
         b = torch.bucketize(d, edges, right=True)
         b[d == NONE] = k
         count += torch.bincount(b, minlength=k + 1)
-        dep = p.depth[lo:hi].to(torch.int64)
+        dep = p.depth_out[lo:hi].to(torch.int64)   # the hash kernel's, against the bins' layout depths
         dsum.scatter_add_(0, b, dep)
         nx = p.next[lo:hi].to(torch.int64) & 0xFFFFFFFF
         gap = nx - torch.arange(lo, hi, device="cuda", dtype=torch.int64)

@@ -97,6 +97,7 @@ def test_bins_match_torch_bucketize(full):
     edges = torch.tensor(caps.astype(np.int64), device="cuda")
     count = torch.zeros(k + 1, dtype=torch.int64, device="cuda")
     dsum = torch.zeros(k + 1, dtype=torch.int64, device="cuda")
+    off = torch.tensor(tr.blk_off().astype(np.int64), device="cuda")
     chunk = 1 << 27
     for lo in range(0, n, chunk):
         hi = min(n, lo + chunk)
@@ -104,7 +105,10 @@ def test_bins_match_torch_bucketize(full):
         bk = torch.bucketize(d, edges, right=True)
         bk[d == NONE] = k
         count += torch.bincount(bk, minlength=k + 1)
-        dsum.scatter_add_(0, bk, p.depth[lo:hi].to(torch.int64))
+        # depth = position in the request, from the offsets with torch
+        t = torch.arange(lo, hi, device="cuda", dtype=torch.int64)
+        dep = t - off[torch.searchsorted(off, t, right=True) - 1]
+        dsum.scatter_add_(0, bk, dep)
     g = pc.bins_to_host(p.bins)
     assert g["count"] == count.cpu().tolist()
     assert g["depthsum"] == dsum.cpu().tolist()
