@@ -404,12 +404,14 @@ pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uin
 /* ------------------------------------------------------------------------
  * The same bins with each access's depth taken from the request layout
  * instead of an array: depth[t] = t - blk_off[r] for the request r holding
- * position t, which is the block's depth in its request's prefix when the
- * keys are laid out as pc_hash_blocks writes them with flags 0 (Sec. 4.4,
- * the miss cost grows with the block's position in the prompt).  The hash
+ * position t (flags 0), or blk_off[r+1] - 1 - t (PC_HASH_DEEPEST_FIRST),
+ * which is the block's depth in its request's prefix when the keys are laid
+ * out as pc_hash_blocks writes them with the same flags (Sec. 4.4, the miss
+ * cost grows with the block's position in the prompt).  The hash
  * then need not write depth, and the bins read 12 bytes of layout map per
  * 64 accesses (built in the workspace) instead of 256 bytes of depth.
  *
+ *   flags     0 or PC_HASH_DEEPEST_FIRST.
  *   blk_off   uint64[n_seqs+1] device memory, blk_off[0] = 0, non-decreasing,
  *             blk_off[n_seqs] = n (empty requests allowed); any other layout
  *             sets the workspace status to 2 and leaves the bins undefined.
@@ -417,7 +419,7 @@ pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uin
  *   workspace (pc_mrc_weighted_layout_ws) holds 12 bytes per 64 accesses.
  * ------------------------------------------------------------------------ */
 size_t pc_mrc_weighted_layout_ws(uint64_t n, uint32_t n_caps);
-pc_status pc_mrc_weighted_layout(const uint32_t *dist, const uint64_t *blk_off, uint32_t n_seqs,
+pc_status pc_mrc_weighted_layout(const uint32_t *dist, const uint64_t *blk_off, uint32_t n_seqs, uint32_t flags,
                                  const uint32_t *next, uint64_t n, const uint64_t *caps, uint32_t n_caps,
                                  uint64_t alpha, uint64_t beta, uint64_t *count, uint64_t *depthsum,
                                  uint64_t *cost_lo, uint64_t *cost_hi, uint64_t *nextuse_hist, void *ws,

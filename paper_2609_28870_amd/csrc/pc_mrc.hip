@@ -27,7 +27,11 @@
 // access's request start from those (the last start bit at or below it in
 // its 64-position word, else the word's entry) and follows the start bits
 // across its 8 accesses: 12 bytes of map per 64 accesses instead of 256
-// bytes of depth.
+// bytes of depth.  In the deepest-first layout (request-level residency)
+// depth(t) = (last position of t's request) - t: the bitmap marks every
+// request's last position and the table holds, per 64 positions, the last
+// position of the request holding the word's last one; a thread looks up
+// from its last access and follows the marks down.
 #include "pc_internal.h"
 
 namespace pc {
@@ -85,7 +89,7 @@ __global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
     const uint32_t *__restrict__ gstart, const uint8_t *__restrict__ startbits,
     const uint32_t *__restrict__ next, uint64_t n, const uint64_t *__restrict__ caps, uint32_t n_caps,
     uint32_t k0, uint32_t Kc, uint64_t *__restrict__ count, uint64_t *__restrict__ depthsum,
-    uint64_t *__restrict__ nexthist, int32_t *__restrict__ err) {
+    uint64_t *__restrict__ nexthist, int desc, int32_t *__restrict__ err) {
     extern __shared__ uint64_t smem[];
     const uint32_t K = Kc;
     uint64_t *s_ds = smem;                    // K+2
@@ -138,19 +142,31 @@ __global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
             }
         }
         if (LAYOUT) {
-            // the depth within the request: the last request start at or below
-            // t0 (in the 64-position word, else the word's entry), then the
-            // starts among the thread's accesses
             const uint64_t wd = t0 >> 6;
             const uint64_t bits = reinterpret_cast<const uint64_t *>(startbits)[wd];
-            const uint32_t sh = (uint32_t)(t0 & 63);
-            const uint64_t upto = sh == 63 ? bits : bits & ((2ull << sh) - 1);   // starts at or below t0
-            uint32_t st = upto ? (uint32_t)((wd << 6) + 63 - __builtin_clzll(upto)) : gstart[wd];
+            const uint32_t sh = (uint32_t)(t0 & 63);   // a multiple of 8, at most 56
             const uint32_t sb = (uint32_t)(bits >> sh);
+            if (!desc) {
+                // the last request start at or below t0 (in the 64-position
+                // word, else the word's entry), then the starts among the
+                // thread's accesses
+                const uint64_t upto = bits & ((2ull << sh) - 1);
+                uint32_t st = upto ? (uint32_t)((wd << 6) + 63 - __builtin_clzll(upto)) : gstart[wd];
 #pragma unroll
-            for (int j = 0; j < MRC_PER; ++j) {
-                if (j && ((sb >> j) & 1u)) st = (uint32_t)(t0 + j);
-                pv[j] = (uint32_t)(t0 + j) - st;
+                for (int j = 0; j < MRC_PER; ++j) {
+                    if (j && ((sb >> j) & 1u)) st = (uint32_t)(t0 + j);
+                    pv[j] = (uint32_t)(t0 + j) - st;
+                }
+            } else {
+                // the first request end at or above t0 + 7 (in the word, else
+                // the word's entry), then the ends among the thread's accesses
+                const uint64_t from = bits >> (sh + MRC_PER - 1);
+                uint32_t en = from ? (uint32_t)((wd << 6) + sh + MRC_PER - 1 + __builtin_ctzll(from)) : gstart[wd];
+#pragma unroll
+                for (int j = MRC_PER - 1; j >= 0; --j) {
+                    if (j < MRC_PER - 1 && ((sb >> j) & 1u)) en = (uint32_t)(t0 + j);
+                    pv[j] = en - (uint32_t)(t0 + j);
+                }
             }
         } else if (!depth) {
 #pragma unroll
@@ -203,11 +219,13 @@ __global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
 
 // The layout map, one thread per request: bit t of startbits set when a
 // request starts at t (the bitmap is zeroed first), and gstart[w] = the
-// start of the request holding position 64w.  Checks the layout as
+// start of the request holding position 64w; in the deepest-first layout
+// (desc) bit t marks a request's last position and gstart[w] holds the last
+// position of the request holding the word's last one.  Checks the layout as
 // pc_prev_next_chained does.
 __global__ __launch_bounds__(256) void mrc_map_kernel(const uint64_t *__restrict__ off, uint32_t n_seqs, uint64_t n,
-                                                      uint32_t *__restrict__ gstart, uint32_t *__restrict__ startbits,
-                                                      int32_t *__restrict__ err) {
+                                                      int desc, uint32_t *__restrict__ gstart,
+                                                      uint32_t *__restrict__ startbits, int32_t *__restrict__ err) {
     const uint64_t r = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (r >= n_seqs) return;
     const uint64_t a = off[r], b = off[r + 1];
@@ -219,8 +237,19 @@ __global__ __launch_bounds__(256) void mrc_map_kernel(const uint64_t *__restrict
         return;
     }
     if (a == b) return;
-    atomicOr(&startbits[a >> 5], 1u << (a & 31));
-    for (uint64_t w = (a + 63) / 64; w * 64 < b; ++w) gstart[w] = (uint32_t)a;
+    if (!desc) {
+        atomicOr(&startbits[a >> 5], 1u << (a & 31));
+        for (uint64_t w = (a + 63) / 64; w * 64 < b; ++w) gstart[w] = (uint32_t)a;
+    } else {
+        const uint64_t e = b - 1, words = (n + 63) / 64;
+        atomicOr(&startbits[e >> 5], 1u << (e & 31));
+        // words whose last position (n - 1 for the last word) lies in [a, b)
+        for (uint64_t w = a / 64; w < words; ++w) {
+            const uint64_t last = 64 * w + 63 < n ? 64 * w + 63 : n - 1;
+            if (last >= b) break;
+            gstart[w] = (uint32_t)e;
+        }
+    }
 }
 
 // cost = alpha*count + beta*depthsum as a 128-bit integer (hi:lo), mod 2^128
@@ -263,7 +292,7 @@ static MrcLayoutWs mrc_layout_carve(void *ws, uint64_t n) {
 // both entry points: depths from `depth` (or none), or from the layout
 // blk_off (then ws is a layout workspace)
 static pc_status mrc_run(const uint32_t *dist, const uint32_t *depth, const uint64_t *blk_off, uint32_t n_seqs,
-                         const uint32_t *next, uint64_t n, const uint64_t *caps, uint32_t n_caps, uint64_t alpha,
+                         int desc, const uint32_t *next, uint64_t n, const uint64_t *caps, uint32_t n_caps, uint64_t alpha,
                          uint64_t beta, uint64_t *count, uint64_t *depthsum, uint64_t *cost_lo, uint64_t *cost_hi,
                          uint64_t *nextuse_hist, void *ws, size_t ws_bytes, hipStream_t s) {
     (void)ws_bytes;
@@ -289,7 +318,7 @@ static pc_status mrc_run(const uint32_t *dist, const uint32_t *depth, const uint
         if (n_seqs == 0) return fill_u32(reinterpret_cast<uint32_t *>(hdr), (uint32_t)DEV_ERR_BAD_LAYOUT, 1, s);
         if ((st = fill_u32(lw.startbits, 0u, 2 * ((n + 63) / 64), s)) != PC_OK) return st;
         PC_LAUNCH(K_MRC_MAP, mrc_map_kernel, dim3((unsigned)(((uint64_t)n_seqs + 255) / 256)), dim3(256), 0, s,
-                  blk_off, n_seqs, n, lw.gstart, lw.startbits, hdr);
+                  blk_off, n_seqs, n, desc, lw.gstart, lw.startbits, hdr);
     }
     const uint32_t *gs = layout ? lw.gstart : nullptr;
     const uint8_t *sb = layout ? reinterpret_cast<const uint8_t *>(lw.startbits) : nullptr;
@@ -305,16 +334,16 @@ static pc_status mrc_run(const uint32_t *dist, const uint32_t *depth, const uint
         const bool chunked = n_caps > MRC_EDGES;
         if (!chunked && !layout)
             PC_LAUNCH(K_MRC_HIST, (mrc_hist_kernel<false, false>), dim3((unsigned)grid), dim3(MRC_THREADS), shmem,
-                      s, dist, depth, gs, sb, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, hdr);
+                      s, dist, depth, gs, sb, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, desc, hdr);
         else if (!chunked)
             PC_LAUNCH(K_MRC_HIST, (mrc_hist_kernel<false, true>), dim3((unsigned)grid), dim3(MRC_THREADS), shmem,
-                      s, dist, depth, gs, sb, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, hdr);
+                      s, dist, depth, gs, sb, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, desc, hdr);
         else if (!layout)
             PC_LAUNCH(K_MRC_HIST, (mrc_hist_kernel<true, false>), dim3((unsigned)grid), dim3(MRC_THREADS), shmem,
-                      s, dist, depth, gs, sb, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, hdr);
+                      s, dist, depth, gs, sb, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, desc, hdr);
         else
             PC_LAUNCH(K_MRC_HIST, (mrc_hist_kernel<true, true>), dim3((unsigned)grid), dim3(MRC_THREADS), shmem,
-                      s, dist, depth, gs, sb, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, hdr);
+                      s, dist, depth, gs, sb, next, n, caps, n_caps, k0, Kc, count, depthsum, nextuse_hist, desc, hdr);
     }
     PC_LAUNCH(K_MRC_COST, mrc_cost_kernel, dim3((bins + 255) / 256), dim3(256), 0, s, count, depthsum, bins, alpha,
               beta, cost_lo, cost_hi);
@@ -337,7 +366,7 @@ pc_status pc_mrc_weighted(const uint32_t *dist, const uint32_t *depth, const uin
                           uint64_t *nextuse_hist, void *ws, size_t ws_bytes, void *stream) {
     if (n >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
     if (ws && ws_bytes < pc_mrc_weighted_ws(n, n_caps)) return PC_ERR_WORKSPACE;
-    return pc::mrc_run(dist, depth, nullptr, 0, next, n, caps, n_caps, alpha, beta, count, depthsum, cost_lo, cost_hi,
+    return pc::mrc_run(dist, depth, nullptr, 0, 0, next, n, caps, n_caps, alpha, beta, count, depthsum, cost_lo, cost_hi,
                        nextuse_hist, ws, ws_bytes, (hipStream_t)stream);
 }
 
@@ -346,14 +375,15 @@ size_t pc_mrc_weighted_layout_ws(uint64_t n, uint32_t n_caps) {
     return pc::mrc_layout_carve(nullptr, n).bytes;
 }
 
-pc_status pc_mrc_weighted_layout(const uint32_t *dist, const uint64_t *blk_off, uint32_t n_seqs,
+pc_status pc_mrc_weighted_layout(const uint32_t *dist, const uint64_t *blk_off, uint32_t n_seqs, uint32_t flags,
                                  const uint32_t *next, uint64_t n, const uint64_t *caps, uint32_t n_caps,
                                  uint64_t alpha, uint64_t beta, uint64_t *count, uint64_t *depthsum, uint64_t *cost_lo,
                                  uint64_t *cost_hi, uint64_t *nextuse_hist, void *ws, size_t ws_bytes, void *stream) {
     if (n >= (uint64_t)PC_NONE) return PC_ERR_TOO_LARGE;
     if (n > 0 && !blk_off) return PC_ERR_INVALID;
+    if (flags & ~PC_HASH_DEEPEST_FIRST) return PC_ERR_INVALID;
     if (ws && ws_bytes < pc_mrc_weighted_layout_ws(n, n_caps)) return PC_ERR_WORKSPACE;
-    return pc::mrc_run(dist, nullptr, blk_off, n_seqs, next, n, caps, n_caps, alpha, beta, count, depthsum, cost_lo,
+    return pc::mrc_run(dist, nullptr, blk_off, n_seqs, (flags & PC_HASH_DEEPEST_FIRST) ? 1 : 0, next, n, caps, n_caps, alpha, beta, count, depthsum, cost_lo,
                        cost_hi, nextuse_hist, ws, ws_bytes, (hipStream_t)stream);
 }
 

@@ -103,8 +103,8 @@ def lib():
     L.pc_mrc_weighted_layout_ws.restype = _sz
     L.pc_mrc_weighted_layout_ws.argtypes = [_u64, _u32]
     L.pc_mrc_weighted_layout.restype = _st
-    L.pc_mrc_weighted_layout.argtypes = [_vp, _vp, _u32, _vp, _u64, _vp, _u32, _u64, _u64, _vp, _vp, _vp, _vp,
-                                         _vp, _vp, _sz, _vp]
+    L.pc_mrc_weighted_layout.argtypes = [_vp, _vp, _u32, _u32, _vp, _u64, _vp, _u32, _u64, _u64, _vp, _vp, _vp,
+                                         _vp, _vp, _vp, _sz, _vp]
     L.pc_belady_ws.restype = _sz
     L.pc_belady_ws.argtypes = [_u64, _u32]
     L.pc_belady.restype = _st
@@ -443,9 +443,10 @@ def mrc_weighted(dist: torch.Tensor, caps: torch.Tensor, depth: Optional[torch.T
 
 def mrc_weighted_layout(dist: torch.Tensor, caps: torch.Tensor, blk_off: torch.Tensor,
                         nxt: Optional[torch.Tensor] = None, alpha: int = 1, beta: int = 0,
-                        out: Optional[dict] = None, ws: Optional[torch.Tensor] = None):
+                        out: Optional[dict] = None, ws: Optional[torch.Tensor] = None, deepest_first: bool = False):
     """pc_mrc_weighted_layout: as mrc_weighted with depth[t] = t - blk_off[r]
-    for the request r holding t (the ascending layout of hash_blocks)."""
+    for the request r holding t (the ascending layout of hash_blocks), or
+    blk_off[r + 1] - 1 - t with ``deepest_first``."""
     L = lib()
     n = dist.numel()
     k = caps.numel()
@@ -455,7 +456,8 @@ def mrc_weighted_layout(dist: torch.Tensor, caps: torch.Tensor, blk_off: torch.T
                for name in ("count", "depthsum", "cost_lo", "cost_hi", "nextuse")}
     if ws is None:
         ws = workspace(L.pc_mrc_weighted_layout_ws(n, k))
-    check(L.pc_mrc_weighted_layout(_ptr(dist), _ptr(blk_off), blk_off.numel() - 1, _ptr(nxt), n, _ptr(caps), k,
+    check(L.pc_mrc_weighted_layout(_ptr(dist), _ptr(blk_off), blk_off.numel() - 1,
+                                   DEEPEST_FIRST if deepest_first else 0, _ptr(nxt), n, _ptr(caps), k,
                                    alpha & (2 ** 64 - 1), beta & (2 ** 64 - 1), _ptr(out["count"]),
                                    _ptr(out["depthsum"]), _ptr(out["cost_lo"]), _ptr(out["cost_hi"]),
                                    _ptr(out["nextuse"]), _ptr(ws), ws.numel(), _stream()))
@@ -546,10 +548,10 @@ class Pipeline:
     ``with_belady`` (per-access mode) also runs Belady's MIN at every
     capacity on the step's next-use index (``belady_out``).
 
-    In the per-access and session modes the bins take each block's depth
-    from the request layout (``mrc_weighted_layout``) and the hash writes no
-    depth (``depth`` is None); ``depth_array=True``, and Belady's MIN, keep
-    the depth array."""
+    The bins take each block's depth from the request layout
+    (``mrc_weighted_layout``) and the hash writes no depth (``depth`` and
+    ``depth_r`` are None); ``depth_array=True``, and Belady's MIN, keep the
+    depth array."""
 
     def __init__(self, tokens, tok_start, tok_len, blk_off, n_blocks: int, caps,
                  block_size: int = 16, alpha: int = 1, beta: int = 0, with_nextuse: bool = True,
@@ -571,7 +573,7 @@ class Pipeline:
         self.session = session
         self.with_nextuse = with_nextuse and residency == "access"
         self.with_belady = with_belady and residency == "access"
-        self.layout_depth = not (depth_array or self.request or self.with_belady)
+        self.layout_depth = not (depth_array or self.with_belady)
         n = self.n
         self.keys = torch.empty(n, dtype=torch.int64, device=dev)
         self.key_hist = torch.empty(4 * 256, dtype=torch.int32, device=dev)
@@ -620,8 +622,12 @@ class Pipeline:
         self._prev_next(self.keys_r)
         self._stack_distance()
         stack_distance_req(self.prev, self.dist, self.blk_off, dist_req=self.dist_req, ws=self.ws_req)
-        mrc_weighted(self.dist_req, self.caps, self.depth_r, None, self.alpha, self.beta,
-                     out=self.bins, ws=self.ws_mrc)
+        if self.layout_depth:
+            mrc_weighted_layout(self.dist_req, self.caps, self.blk_off, None, self.alpha, self.beta, out=self.bins,
+                                ws=self.ws_mrc, deepest_first=True)
+        else:
+            mrc_weighted(self.dist_req, self.caps, self.depth_r, None, self.alpha, self.beta,
+                         out=self.bins, ws=self.ws_mrc)
 
     def _bins(self, nxt):
         if self.layout_depth:

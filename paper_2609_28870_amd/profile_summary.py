@@ -44,6 +44,7 @@ IDS = {"pc::hash_fused_kernel": "hash_blocks",
        "pc::sd_seg_scan_kernel": "sd_seg_scan",
        "pc::sd_dominance_kernel<true>": "sd_dominance_pass", "pc::sd_dominance_kernel<false>": "sd_dominance_pass",
        "pc::sd_local_kernel": "sd_local_finish", "pc::mrc_hist_kernel": "mrc_hist", "pc::mrc_cost_kernel": "mrc_cost",
+       "pc::mrc_map_kernel": "mrc_map",
        "pc::req_order_kernel": "request_order", "pc::req_dist_kernel": "request_distance",
        "pc::sess_dist_kernel": "session_distance", "pc::sess_profile_kernel": "session_profile",
        "pc::prof_pack_kernel": "reuse_profile_pack", "pc::prof_walk_kernel": "reuse_profile_walk",

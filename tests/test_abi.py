@@ -206,12 +206,14 @@ def test_mrc_rejects_bad_arguments(L):
 def test_mrc_layout_rejects_bad_arguments(L):
     ws = L.pc_mrc_weighted_layout_ws(10, 4)
     assert ws > L.pc_mrc_weighted_layout_ws(0, 4)
-    ok = lambda **kw: dict(dict(dist=FAKE, off=FAKE, seqs=2, nxt=None, n=10, caps=FAKE, k=4, a=1, b=0,
+    ok = lambda **kw: dict(dict(dist=FAKE, off=FAKE, seqs=2, fl=0, nxt=None, n=10, caps=FAKE, k=4, a=1, b=0,
                                 cnt=FAKE, ds=FAKE, lo=FAKE, hi=FAKE, nh=None, w=FAKE, wsz=ws), **kw)
-    call = lambda d: L.pc_mrc_weighted_layout(d["dist"], d["off"], d["seqs"], d["nxt"], d["n"], d["caps"], d["k"],
+    call = lambda d: L.pc_mrc_weighted_layout(d["dist"], d["off"], d["seqs"], d["fl"], d["nxt"], d["n"], d["caps"],
+                                              d["k"],
                                               d["a"], d["b"], d["cnt"], d["ds"], d["lo"], d["hi"], d["nh"],
                                               d["w"], d["wsz"], None)
     assert call(ok(off=None)) == -1
+    assert call(ok(fl=2)) == -1
     assert call(ok(k=0)) == -1
     assert call(ok(k=4097)) == -1
     assert call(ok(nxt=FAKE)) == -1

@@ -46,6 +46,11 @@ def full():
     p.run()
     torch.cuda.synchronize()
     say("request-level pipeline done, status", p.status())
+    # the pipeline takes depths from the request layout; the hash kernel's
+    # depth output (deepest first), for the checks of the depth array
+    _, p.depth_out, _ = pc.hash_blocks(up["tokens"], up["tok_start"], up["tok_len"], up["blk_off"], up["n_blocks"],
+                                       B, keys=p.keys_r, ws=p.ws_hash, deepest_first=True)
+    torch.cuda.synchronize()
     yield tr, caps, p
     del p
     torch.cuda.empty_cache()
@@ -67,7 +72,7 @@ def test_sampled_requests_reversed(full):
             continue
         want, wd = oracle.hash_requests(tr.tokens, tr.tok_start[r:r + 1], tr.tok_len[r:r + 1], B)
         assert np.array_equal(pc.as_u64(p.keys_r[lo:hi]), want[::-1]), r
-        assert np.array_equal(pc.as_u32(p.depth_r[lo:hi]), wd[::-1]), r
+        assert np.array_equal(pc.as_u32(p.depth_out[lo:hi]), wd[::-1]), r
 
 
 @pytest.mark.parametrize("where", ["start", "middle", "end"])
@@ -130,7 +135,7 @@ def test_bins_match_torch_bucketize(full):
         bk = torch.bucketize(d, edges, right=True)
         bk[d == NONE] = k
         count += torch.bincount(bk, minlength=k + 1)
-        dsum.scatter_add_(0, bk, p.depth_r[lo:hi].to(torch.int64))
+        dsum.scatter_add_(0, bk, p.depth_out[lo:hi].to(torch.int64))   # the hash kernel's, against the layout's
     g = pc.bins_to_host(p.bins)
     assert g["count"] == count.cpu().tolist()
     assert g["depthsum"] == dsum.cpu().tolist()

@@ -329,18 +329,25 @@ def layout_of(case, n, rng):
     return L
 
 
+@pytest.mark.parametrize("desc", [False, True])
 @pytest.mark.parametrize("case,n,k", [("ragged", 70001, 20), ("short", 70001, 20), ("empty_reqs", 20003, 20),
                                       ("single", 4099, 20), ("one_request", 9, 5), ("short", 1, 5),
-                                      ("short", 7, 5), ("short", 8, 5), ("ragged", 70001, 2500)])
-def test_bins_with_depth_from_the_layout(case, n, k):
-    # depth[t] = t - blk_off[r] for the request r holding t: the same bins
-    # as with that depth passed as an array, and as the oracle's; the
-    # request starts fall at every offset within the 8-access groups
+                                      ("short", 7, 5), ("short", 8, 5), ("short", 63, 5), ("short", 64, 5),
+                                      ("short", 65, 5), ("ragged", 70001, 2500)])
+def test_bins_with_depth_from_the_layout(case, n, k, desc):
+    # depth[t] = t - blk_off[r] for the request r holding t (or, deepest
+    # first, blk_off[r + 1] - 1 - t): the same bins as with that depth passed
+    # as an array, and as the oracle's; request starts and ends fall at every
+    # offset within the 8-access groups and the 64-position words
     rng = np.random.default_rng(n + k)
     L = layout_of(case, n, rng)
     off = np.concatenate([[0], np.cumsum(L)]).astype(np.uint64)
     assert int(off[-1]) == n
-    depth = (np.arange(n, dtype=np.int64) - np.repeat(off[:-1].astype(np.int64), L)).astype(np.uint32)
+    pos = np.arange(n, dtype=np.int64)
+    if desc:
+        depth = (np.repeat(off[1:].astype(np.int64), L) - 1 - pos).astype(np.uint32)
+    else:
+        depth = (pos - np.repeat(off[:-1].astype(np.int64), L)).astype(np.uint32)
     keys = stream("mixed", n, 13)
     ids = oracle.key_ids(keys)
     op, on = oracle.prev_next(keys, ids)
@@ -350,7 +357,7 @@ def test_bins_with_depth_from_the_layout(case, n, k):
     say("case layout", case, "n", n, "requests", len(L), "caps", k)
     a, b = 2 * 16 * 3_000_000_000, 2 * 16 * 16
     out, ws = pc.mrc_weighted_layout(pc.to_dev_u32(od), pc.to_dev_u64(caps), pc.to_dev_u64(off), pc.to_dev_u32(on),
-                                     a, b)
+                                     a, b, deepest_first=desc)
     assert pc.workspace_status(ws) == 0
     g = pc.bins_to_host(out)
     assert g == gpu_bins(od, caps, depth, on, a, b)
@@ -363,8 +370,10 @@ def test_bins_layout_rejects_an_invalid_layout():
     od = oracle.stack_distance_bit(oracle.prev_next(stream("mixed", 5000, 2))[0])
     caps = pc.to_dev_u64(np.array([1, 10, 100], np.uint64))
     for off in ([0, 100, 4000], [1, 2500, 5000], [0, 3000, 2000, 5000]):
-        out, ws = pc.mrc_weighted_layout(pc.to_dev_u32(od), caps, pc.to_dev_u64(np.array(off, np.uint64)))
-        assert pc.workspace_status(ws) == 2, off
+        for desc in (False, True):
+            out, ws = pc.mrc_weighted_layout(pc.to_dev_u32(od), caps, pc.to_dev_u64(np.array(off, np.uint64)),
+                                             deepest_first=desc)
+            assert pc.workspace_status(ws) == 2, off
 
 
 def test_decreasing_edges_set_the_status():
