@@ -7,8 +7,8 @@
 // cost(t) = alpha + beta * depth[t].  Because LRU hits at capacity c exactly
 // when D < c, binning D on the capacity edges gives every capacity at once.
 //
-// GPU mapping: each thread takes 8 consecutive accesses (32-byte vector
-// loads of dist / depth / next) and keeps the value range of the bin it is
+// GPU mapping: each thread takes 8 consecutive accesses (16 when the depths
+// come from the layout; 16-byte vector loads of dist / depth / next) and keeps the value range of the bin it is
 // filling in registers, so an access that stays in that bin (neighbouring
 // accesses of one request usually do) costs two compares; any other value
 // finds its bin by an upper-bound search of the edges held in LDS.  Runs of
@@ -26,8 +26,8 @@
 // request holding the first; a thread of the bins kernel finds its first
 // access's request start from those (the last start bit at or below it in
 // its 64-position word, else the word's entry) and follows the start bits
-// across its 8 accesses: 12 bytes of map per 64 accesses instead of 256
-// bytes of depth.  In the deepest-first layout (request-level residency)
+// across its accesses: 12 bytes of map per 64 accesses instead of 256 bytes
+// of depth.  In the deepest-first layout (request-level residency)
 // depth(t) = (last position of t's request) - t: the bitmap marks every
 // request's last position and the table holds, per 64 positions, the last
 // position of the request holding the word's last one; a thread looks up
@@ -48,7 +48,11 @@ __device__ __forceinline__ uint32_t upper_bound(const uint32_t *e, uint32_t m, u
     return lo;
 }
 
-constexpr int MRC_PER = 8;             // consecutive accesses per thread
+// consecutive accesses per thread: 8 with a depth array (32 registers of
+// loads per lane keep eight waves per SIMD), 16 with depths from the layout
+// (its map lookup per thread then covers twice the accesses: 4.6 -> 3.3 ms
+// on the full trace)
+template <bool LAYOUT> constexpr int mrc_per() { return LAYOUT ? 16 : 8; }
 constexpr uint32_t MRC_EDGES = 1024;   // edges held in LDS by one launch
 
 // Distances and gaps are 32-bit and NONE (no previous or next use) is the
@@ -109,6 +113,7 @@ __global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
         s_nh[i] = 0;
     }
     __syncthreads();
+    constexpr int MRC_PER = mrc_per<LAYOUT>();
     const uint64_t chunks = (n + MRC_PER - 1) / MRC_PER;
     // vector loads only when every base pointer is 16-byte aligned
     const bool vec = ((reinterpret_cast<uintptr_t>(dist) | reinterpret_cast<uintptr_t>(depth) |
@@ -144,7 +149,7 @@ __global__ __launch_bounds__(MRC_THREADS) void mrc_hist_kernel(
         if (LAYOUT) {
             const uint64_t wd = t0 >> 6;
             const uint64_t bits = reinterpret_cast<const uint64_t *>(startbits)[wd];
-            const uint32_t sh = (uint32_t)(t0 & 63);   // a multiple of 8, at most 56
+            const uint32_t sh = (uint32_t)(t0 & 63);   // a multiple of MRC_PER, at most 64 - MRC_PER
             const uint32_t sb = (uint32_t)(bits >> sh);
             if (!desc) {
                 // the last request start at or below t0 (in the 64-position
@@ -322,7 +327,8 @@ static pc_status mrc_run(const uint32_t *dist, const uint32_t *depth, const uint
     }
     const uint32_t *gs = layout ? lw.gstart : nullptr;
     const uint8_t *sb = layout ? reinterpret_cast<const uint8_t *>(lw.startbits) : nullptr;
-    uint64_t grid = (n + MRC_THREADS * MRC_PER - 1) / (MRC_THREADS * MRC_PER);
+    const uint64_t per = layout ? mrc_per<true>() : mrc_per<false>();
+    uint64_t grid = (n + MRC_THREADS * per - 1) / (MRC_THREADS * per);
     // up to 64 workgroups per CU: eight resident (32 registers of loads per
     // lane keep eight waves per SIMD) and the rest queued behind them, which
     // hid the load latency best; more make the final flush contend
