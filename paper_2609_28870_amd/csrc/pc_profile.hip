@@ -47,10 +47,12 @@ __global__ __launch_bounds__(256) void prof_pack_kernel(const uint32_t *__restri
 // (a long session's blocks, whose chains are all long, spread over many
 // waves); the chain starts found in a chunk go to a per-wave queue in LDS, and
 // every lane whose chain has ended takes the next start, so lanes stay busy
-// however unequal the chains are.  Each lane step reads packed[t] (the
-// chain's next position and its request), bins the gap since the previous
-// access and, at the chain's end, the block's lifetime and frequency.
-// Histograms accumulate in LDS and are added to the outputs at the end.
+// however unequal the chains are.  A lane holds packed[t] of its position t
+// (the chain's next position and t's request); each step loads t's request
+// timestamp and packed[] of the next position together (one memory latency
+// per step, not two), bins the gap since the previous access and, at the
+// chain's end, the block's lifetime and frequency.  Histograms accumulate in
+// LDS and are added to the outputs at the end.
 __global__ __launch_bounds__(PROF_THREADS) void prof_walk_kernel(
     const uint32_t *__restrict__ prev, const uint64_t *__restrict__ packed, const uint64_t *__restrict__ ts_us,
     uint32_t n_seqs, uint64_t n, const uint64_t *__restrict__ edges, uint32_t n_edges, uint32_t freq_max,
@@ -83,6 +85,7 @@ __global__ __launch_bounds__(PROF_THREADS) void prof_walk_kernel(
     uint32_t qh = 0, qt = 0;                                 // queue head / tail (wave-uniform)
     bool active = false;
     uint32_t t = 0, f = 0;
+    uint64_t a = 0;   // packed[t]
     uint64_t ts_first = 0, ts_last = 0;
     uint32_t *queue = s_queue[wv];
     for (;;) {
@@ -103,6 +106,7 @@ __global__ __launch_bounds__(PROF_THREADS) void prof_walk_kernel(
             const uint32_t r = mbcnt(idle);
             if (r < avail) {
                 t = queue[(qh + r) % PROF_QUEUE];
+                a = packed[t];
                 active = true;
                 f = 0;
             }
@@ -111,10 +115,12 @@ __global__ __launch_bounds__(PROF_THREADS) void prof_walk_kernel(
         __builtin_amdgcn_wave_barrier();
         if (ballot(active) == 0) break;   // no chain left: the queue is empty and every chunk scanned
         if (active) {
-            const uint64_t a = packed[t];
             const uint32_t nx = (uint32_t)a;
             const uint32_t r = (uint32_t)(a >> 32);
+            const bool ends = nx == NONE || nx <= t || (uint64_t)nx >= n;   // chains run forward
+            // both loads in flight at once
             const uint64_t ts = r < n_seqs ? ts_us[r] : 0;
+            const uint64_t an = ends ? 0ull : packed[nx];
             if (f == 0) {
                 ts_first = ts;
             } else {
@@ -122,7 +128,7 @@ __global__ __launch_bounds__(PROF_THREADS) void prof_walk_kernel(
             }
             ts_last = ts;
             ++f;
-            if (nx == NONE || nx <= t || (uint64_t)nx >= n) {   // chains run forward; anything else ends it
+            if (ends) {   // anything but a later position ends the chain
                 if (nx != NONE) atomicOr(err, DEV_ERR_BAD_LAYOUT);
                 const uint32_t cls = 31u - (uint32_t)__builtin_clz(f);
                 atomicAdd(&s_class[cls * kb + edge_bin(s_edges, n_edges, ts_last - ts_first)], 1u);
@@ -130,6 +136,7 @@ __global__ __launch_bounds__(PROF_THREADS) void prof_walk_kernel(
                 active = false;
             } else {
                 t = nx;
+                a = an;
             }
         }
     }
