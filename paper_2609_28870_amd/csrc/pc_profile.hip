@@ -202,7 +202,7 @@ pc_status pc_reuse_profile(const uint32_t *prev, const uint32_t *next, const uin
     if (n == 0) return PC_OK;
     const int cus = pc::device_cus();
     uint64_t pg = ((uint64_t)n_seqs + 3) / 4;
-    if (pg > (uint64_t)cus * 16) pg = (uint64_t)cus * 16;
+    if (pg > (uint64_t)cus * 64) pg = (uint64_t)cus * 64;   // 64 per CU: 5.9 -> 5.3 ms on the full trace
     PC_LAUNCH(pc::K_PROF_PACK, pc::prof_pack_kernel, dim3((unsigned)pg), dim3(256), 0, s, next, blk_off, n_seqs, n,
               w.packed, w.hdr);
     const uint64_t chunks = (n + pc::WAVE - 1) / pc::WAVE;
