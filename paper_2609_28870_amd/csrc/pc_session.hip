@@ -326,7 +326,7 @@ pc_status pc_stack_distance_session(const uint32_t *prev, const uint64_t *blk_of
     PC_LAUNCH(pc::K_SESS_REQ, pc::sess_footprint_kernel, dim3(fgrid), dim3(256), 0, s, w.l.prev_s, w.l.next_s,
               blk_off, n_seqs, n, w.w, w.hdr);
     uint64_t grid = ((uint64_t)n_seqs + 3) / 4;
-    if (grid > (uint64_t)cus * 16) grid = (uint64_t)cus * 16;
+    if (grid > (uint64_t)cus * 64) grid = (uint64_t)cus * 64;   // 64 per CU: 4.57 -> 4.38 ms on the full trace
     PC_LAUNCH(pc::K_SESS_DIST, pc::sess_dist_kernel, dim3((unsigned)grid), dim3(256), 0, s, prev, blk_off, n_seqs, n,
               w.req_page, w.l.next_s, w.w, dist_sess);
     return PC_OK;
